@@ -1,0 +1,185 @@
+"""CPU oracle for the batched routing scorer -- test infrastructure only.
+
+A ctypes front end for ``lodestar_oracle.c``.  Only the tests, the smoke check
+and the benchmark's CPU-baseline leg use it; the HIP library never does, and
+the two share no code.  Every function is a plain transcription of what the
+paper defines (see the C file for the passages each one follows).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+F64, F32, BF16 = 0, 1, 2
+MODES = {"f64": F64, "fp32": F32, "f32": F32, "bf16": BF16}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lodestar_oracle.c")
+_LIB = os.path.join(_HERE, "liblsoracle.so")
+_CFLAGS = ["-O2", "-mfma", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared", "-fPIC", "-std=c11"]
+
+
+def compile_c(src: str, out: str) -> str:
+    tmp = out + ".tmp"
+    subprocess.check_call(["gcc", *_CFLAGS, "-o", tmp, src, "-lm"])
+    os.replace(tmp, out)
+    return out
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (no GPU code involved)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        compile_c(_SRC, _LIB)
+    return _LIB
+
+
+_libs = {}
+
+
+def _open(path):
+    if path not in _libs:
+        lib = ctypes.CDLL(path)
+        P = ctypes.c_void_p
+        i32, i64, f32, dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+        lib.lso_bf16_round.argtypes = [f32]
+        lib.lso_bf16_round.restype = f32
+        lib.lso_overlap.argtypes = [i32, P, P, P, i32, P, P, P, ctypes.c_int]
+        lib.lso_features.argtypes = [ctypes.c_int, i32, P, i32, i32, i32, P]
+        lib.lso_param_count.argtypes = [i32, i32, P]
+        lib.lso_param_count.restype = i64
+        lib.lso_forward.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i64, P, P, ctypes.c_int]
+        lib.lso_argmin.argtypes = [i32, P, P]
+        lib.lso_argmin.restype = i32
+        lib.lso_score.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, P, P, i32, P, P, P,
+                                  P, P, P, P, P, ctypes.c_int]
+        lib.lso_update.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, f32, P, P]
+        for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update):
+            f.restype = ctypes.c_int
+        _libs[path] = lib
+    return _libs[path]
+
+
+_active = None
+
+
+def _load():
+    if _active is not None:
+        return _open(_active)
+    return _open(build())
+
+
+def use_library(path) -> None:
+    """Point this module at another build of the oracle source (None: the default)."""
+    global _active
+    _active = path
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _mode(m):
+    return MODES[m] if isinstance(m, str) else int(m)
+
+
+def bf16_round(x) -> np.ndarray:
+    lib = _load()
+    x = np.asarray(x, dtype=np.float32)
+    return np.array([lib.lso_bf16_round(float(v)) for v in x.ravel()], dtype=np.float32).reshape(x.shape)
+
+
+def overlap(req_off, req_hashes, inst_off, inst_hashes, sel=None, threads=0) -> np.ndarray:
+    lib = _load()
+    req_off = _c(req_off, np.int64); req_hashes = _c(req_hashes, np.uint64)
+    inst_off = _c(inst_off, np.int64); inst_hashes = _c(inst_hashes, np.uint64)
+    N = inst_off.shape[0] - 1
+    R = req_off.shape[0] - 1
+    sel_a = None if sel is None else _c(sel, np.int32)
+    n_sel = R if sel_a is None else sel_a.shape[0]
+    out = np.zeros((n_sel, N), dtype=np.int32)
+    rc = lib.lso_overlap(n_sel, _ptr(sel_a), _ptr(req_off), _ptr(req_hashes), N, _ptr(inst_off),
+                         _ptr(inst_hashes), _ptr(out), threads)
+    assert rc == 0, rc
+    return out
+
+
+def features(mode, inst_row, L, n, l) -> np.ndarray:
+    lib = _load()
+    inst_row = _c(inst_row, np.float32)
+    x = np.zeros(inst_row.shape[0] + 5, dtype=np.float64)
+    lib.lso_features(_mode(mode), inst_row.shape[0], _ptr(inst_row), int(L), int(n), int(l), _ptr(x))
+    return x
+
+
+def param_count(d, hidden) -> int:
+    lib = _load()
+    h = _c(hidden, np.int32)
+    return int(lib.lso_param_count(d, h.shape[0], _ptr(h)))
+
+
+def forward(mode, d, hidden, params, mu, inv_sigma, x, threads=0) -> np.ndarray:
+    lib = _load()
+    h = _c(hidden, np.int32)
+    params = _c(params, np.float32); mu = _c(mu, np.float32); inv_sigma = _c(inv_sigma, np.float32)
+    x = _c(x, np.float64).reshape(-1, d)
+    out = np.zeros(x.shape[0], dtype=np.float64)
+    rc = lib.lso_forward(_mode(mode), d, h.shape[0], _ptr(h), _ptr(params), _ptr(mu), _ptr(inv_sigma),
+                         x.shape[0], _ptr(x), _ptr(out), threads)
+    assert rc == 0, rc
+    return out
+
+
+def argmin(scores):
+    lib = _load()
+    s = _c(scores, np.float64)
+    m = np.zeros(1, dtype=np.float64)
+    i = lib.lso_argmin(s.shape[0], _ptr(s), _ptr(m))
+    return int(i), float(m[0])
+
+
+def score(mode, d, hidden, params, mu, inv_sigma, req_off, req_hashes, prompt_len, inst_feat,
+          inst_off, inst_hashes, sel=None, threads=0) -> dict:
+    """Overlap, features, model and argmin for the selected requests."""
+    lib = _load()
+    h = _c(hidden, np.int32)
+    params = _c(params, np.float32); mu = _c(mu, np.float32); inv_sigma = _c(inv_sigma, np.float32)
+    req_off = _c(req_off, np.int64); req_hashes = _c(req_hashes, np.uint64)
+    prompt_len = _c(prompt_len, np.int32); inst_feat = _c(inst_feat, np.float32)
+    inst_off = _c(inst_off, np.int64); inst_hashes = _c(inst_hashes, np.uint64)
+    N = inst_off.shape[0] - 1
+    R = req_off.shape[0] - 1
+    sel_a = None if sel is None else _c(sel, np.int32)
+    n_sel = R if sel_a is None else sel_a.shape[0]
+    ov = np.zeros((n_sel, N), dtype=np.int32)
+    sc = np.zeros((n_sel, N), dtype=np.float64)
+    ch = np.zeros(n_sel, dtype=np.int32)
+    mn = np.zeros(n_sel, dtype=np.float64)
+    ft = np.zeros((n_sel, d), dtype=np.float64)
+    rc = lib.lso_score(_mode(mode), d, h.shape[0], _ptr(h), _ptr(params), _ptr(mu), _ptr(inv_sigma),
+                       n_sel, _ptr(sel_a), _ptr(req_off), _ptr(req_hashes), _ptr(prompt_len), N,
+                       _ptr(inst_feat), _ptr(inst_off), _ptr(inst_hashes),
+                       _ptr(ov), _ptr(sc), _ptr(ch), _ptr(mn), _ptr(ft), threads)
+    assert rc == 0, rc
+    return {"overlap": ov, "scores": sc, "chosen": ch, "min_ttft": mn, "feat": ft}
+
+
+def update(mode, d, hidden, params, mu, inv_sigma, feats, ttft, lr) -> dict:
+    """One SGD step; returns the new params, the gradient and the pre-step loss."""
+    lib = _load()
+    h = _c(hidden, np.int32)
+    p = np.array(params, dtype=np.float32, copy=True)
+    mu = _c(mu, np.float32); inv_sigma = _c(inv_sigma, np.float32)
+    feats = _c(feats, np.float32).reshape(-1, d); ttft = _c(ttft, np.float32)
+    grad = np.zeros(p.shape[0], dtype=np.float64)
+    loss = np.zeros(1, dtype=np.float64)
+    rc = lib.lso_update(_mode(mode), d, h.shape[0], _ptr(h), _ptr(p), _ptr(mu), _ptr(inv_sigma),
+                        feats.shape[0], _ptr(feats), _ptr(ttft), float(lr), _ptr(grad), _ptr(loss))
+    assert rc == 0, rc
+    return {"params": p, "grad": grad, "loss": float(loss[0])}

@@ -1,0 +1,465 @@
+/*
+ * CPU oracle for the batched routing scorer -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, obviously correct implementations of what the routing hot path
+ * computes, written from the paper (Lodestar, arXiv 2606.00946).  Only the test
+ * suite, the smoke check and the benchmark's CPU-baseline leg may load this
+ * library; the product path never does.  It shares no code, header, table or
+ * helper with the HIP library.
+ *
+ * Precision modes:
+ *   LSO_F64  -- the definition, evaluated in double precision.
+ *   LSO_F32  -- the kernel's precision: fp32 values, every dot product an
+ *               fmaf chain that starts from the bias and runs over the inputs in
+ *               ascending order, no other contraction.
+ *   LSO_BF16 -- as LSO_F32, but every layer's weights and input activations are
+ *               first rounded to bfloat16 (round to nearest, ties to even).
+ * Routing decisions are compared in the kernel's precision; scores are also
+ * compared with the LSO_F64 definition within a tolerance.
+ *
+ * Build: gcc -O2 -mfma -ffp-contract=off -fopenmp -shared -fPIC
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { LSO_F64 = 0, LSO_F32 = 1, LSO_BF16 = 2 };
+#define LSO_BLOCK_TOKENS 16
+#define LSO_DERIVED 5
+#define LSO_MAX_LAYERS 8
+
+/* ------------------------------------------------------------------------- */
+/* bfloat16 rounding from the number format's definition: 8 significant bits,  */
+/* the same exponent range as binary32, round to nearest with ties to even.    */
+/* ------------------------------------------------------------------------- */
+float lso_bf16_round(float x)
+{
+    if (x == 0.0f || isinf(x)) return x;
+    if (isnan(x)) return x;
+    int e;
+    double m = frexp((double)x, &e);           /* x = m * 2^e, 0.5 <= |m| < 1 */
+    (void)m;
+    if (e < -125) e = -125;                    /* below binary32's smallest normal the quantum stays 2^-133 */
+    double scale = ldexp(1.0, 8 - e);          /* 8 significant bits */
+    double q = nearbyint((double)x * scale);   /* ties-to-even in the default rounding mode */
+    double r = q / scale;
+    if (fabs(r) >= ldexp(1.0, 128)) return (float)copysign(INFINITY, r);
+    return (float)r;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Prefix overlap (Section 2 Background: prefix reuse is strictly sequential,  */
+/* a cached block helps only if every earlier block is cached too; Section    */
+/* 4.2 Prefix KV cache tracker: tokenized prompt in, per-instance hit out).    */
+/* The overlap of request r on instance i is the number of leading blocks of   */
+/* r that are all in instance i's cached set.                                  */
+/* ------------------------------------------------------------------------- */
+static int cmp_u64(const void* a, const void* b)
+{
+    uint64_t x = *(const uint64_t*)a, y = *(const uint64_t*)b;
+    return (x > y) - (x < y);
+}
+
+typedef struct { uint64_t* keys; int64_t count; } lso_set;
+
+static void build_sets(int32_t N, const int64_t* inst_off, const uint64_t* hashes, lso_set* sets)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t i = 0; i < N; ++i) {
+        int64_t c = inst_off[i + 1] - inst_off[i];
+        uint64_t* k = (uint64_t*)malloc((size_t)(c > 0 ? c : 1) * sizeof(uint64_t));
+        memcpy(k, hashes + inst_off[i], (size_t)c * sizeof(uint64_t));
+        qsort(k, (size_t)c, sizeof(uint64_t), cmp_u64);
+        int64_t u = 0;                          /* order and duplicates are irrelevant to a set */
+        for (int64_t t = 0; t < c; ++t)
+            if (u == 0 || k[u - 1] != k[t]) k[u++] = k[t];
+        sets[i].keys = k;
+        sets[i].count = u;
+    }
+}
+
+static void free_sets(int32_t N, lso_set* sets)
+{
+    for (int32_t i = 0; i < N; ++i) free(sets[i].keys);
+}
+
+static int in_set(const lso_set* s, uint64_t key)
+{
+    return bsearch(&key, s->keys, (size_t)s->count, sizeof(uint64_t), cmp_u64) != NULL;
+}
+
+static int32_t overlap_one(const uint64_t* h, int64_t n, const lso_set* s)
+{
+    int32_t l = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (!in_set(s, h[j])) break;
+        ++l;
+    }
+    return l;
+}
+
+static void set_threads(int threads)
+{
+#ifdef _OPENMP
+    if (threads > 0) omp_set_num_threads(threads);
+#else
+    (void)threads;
+#endif
+}
+
+/* out[q*N + i] = overlap of request sel[q] (all requests when sel == NULL) on instance i */
+int lso_overlap(int32_t n_sel, const int32_t* sel, const int64_t* req_off, const uint64_t* req_hashes,
+                int32_t N, const int64_t* inst_off, const uint64_t* inst_hashes, int32_t* out, int threads)
+{
+    set_threads(threads);
+    lso_set* sets = (lso_set*)calloc((size_t)N, sizeof(lso_set));
+    if (!sets) return -2;
+    build_sets(N, inst_off, inst_hashes, sets);
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int32_t q = 0; q < n_sel; ++q) {
+        int32_t r = sel ? sel[q] : q;
+        for (int32_t i = 0; i < N; ++i)
+            out[(int64_t)q * N + i] = overlap_one(req_hashes + req_off[r], req_off[r + 1] - req_off[r], &sets[i]);
+    }
+    free_sets(N, sets);
+    free(sets);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Pair features (Section 4.1, Features; Alg. 4 inputs).  The raw row is the   */
+/* instance state followed by the request and pair columns:                    */
+/*   [ inst_feat[i] | L, n | l, kappa, u ]                                     */
+/* L = prompt tokens, n = hashed blocks, l = overlap in blocks,                */
+/* kappa = 16 l / L the expected hit ratio (Section 2: fraction of the input   */
+/* tokens whose KV blocks are already cached; 0 when L = 0), u = L - 16 l the  */
+/* tokens left to prefill.  kappa is divided in the mode's precision.          */
+/* ------------------------------------------------------------------------- */
+void lso_features(int mode, int32_t d_inst, const float* inst_row, int32_t L, int32_t n, int32_t l, double* x)
+{
+    for (int32_t c = 0; c < d_inst; ++c) x[c] = (double)inst_row[c];
+    x[d_inst + 0] = (double)L;
+    x[d_inst + 1] = (double)n;
+    x[d_inst + 2] = (double)l;
+    int64_t hit_tokens = (int64_t)LSO_BLOCK_TOKENS * l;
+    if (L == 0) x[d_inst + 3] = 0.0;
+    else if (mode == LSO_F64) x[d_inst + 3] = (double)hit_tokens / (double)L;
+    else x[d_inst + 3] = (double)((float)hit_tokens / (float)L);
+    x[d_inst + 4] = (double)((int64_t)L - hit_tokens);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Reward model (Section 4.1, Request-instance reward model / Model            */
+/* architecture): one MLP shared by every instance, ReLU hidden layers, scalar */
+/* output.  The output is the predicted TTFT in seconds; the reward is its     */
+/* negation.  Inputs are z-scored per feature first (Alg. 4, Normalize).       */
+/* Parameters are packed per layer as W [out x in] row-major, then b [out].    */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int n_layers;
+    int in[LSO_MAX_LAYERS], out[LSO_MAX_LAYERS];
+    const float* W[LSO_MAX_LAYERS];
+    const float* b[LSO_MAX_LAYERS];
+    int64_t W_off[LSO_MAX_LAYERS], b_off[LSO_MAX_LAYERS];
+    int max_width;
+} lso_net;
+
+static int net_init(lso_net* net, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params)
+{
+    if (n_hidden < 0 || n_hidden + 1 > LSO_MAX_LAYERS || d < 1) return -1;
+    int64_t off = 0;
+    int prev = d;
+    net->n_layers = n_hidden + 1;
+    net->max_width = d;
+    for (int l = 0; l < net->n_layers; ++l) {
+        int o = (l < n_hidden) ? hidden[l] : 1;
+        if (o < 1) return -1;
+        net->in[l] = prev;
+        net->out[l] = o;
+        net->W_off[l] = off;
+        net->W[l] = params ? params + off : NULL;
+        off += (int64_t)o * prev;
+        net->b_off[l] = off;
+        net->b[l] = params ? params + off : NULL;
+        off += o;
+        if (o > net->max_width) net->max_width = o;
+        prev = o;
+    }
+    return 0;
+}
+
+int64_t lso_param_count(int32_t d, int32_t n_hidden, const int32_t* hidden)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, NULL)) return -1;
+    int l = net.n_layers - 1;
+    return net.b_off[l] + net.out[l];
+}
+
+/* One pair, definition in double precision. */
+static double forward_f64(const lso_net* net, const float* mu, const float* inv_sigma, const double* x,
+                          double* buf_a, double* buf_b)
+{
+    int d = net->in[0];
+    for (int k = 0; k < d; ++k) buf_a[k] = (x[k] - (double)mu[k]) * (double)inv_sigma[k];
+    double* a = buf_a;
+    double* z = buf_b;
+    for (int l = 0; l < net->n_layers; ++l) {
+        int K = net->in[l], O = net->out[l];
+        for (int j = 0; j < O; ++j) {
+            double acc = (double)net->b[l][j];
+            for (int k = 0; k < K; ++k) acc += (double)net->W[l][(int64_t)j * K + k] * a[k];
+            z[j] = acc;
+        }
+        if (l + 1 == net->n_layers) return z[0];
+        for (int j = 0; j < O; ++j) z[j] = z[j] > 0.0 ? z[j] : 0.0;
+        double* t = a; a = z; z = t;
+    }
+    return 0.0;
+}
+
+/* One pair in the kernel's precision (fp32 fma chains, optional bf16 operands). */
+static float forward_lowp(int mode, const lso_net* net, const float* mu, const float* inv_sigma, const double* x,
+                          float* buf_a, float* buf_b)
+{
+    int bf = (mode == LSO_BF16);
+    int d = net->in[0];
+    for (int k = 0; k < d; ++k) {
+        float xf = (float)x[k];
+        float t = xf - mu[k];
+        t = t * inv_sigma[k];
+        buf_a[k] = bf ? lso_bf16_round(t) : t;
+    }
+    float* a = buf_a;
+    float* z = buf_b;
+    for (int l = 0; l < net->n_layers; ++l) {
+        int K = net->in[l], O = net->out[l];
+        for (int j = 0; j < O; ++j) {
+            float acc = net->b[l][j];
+            for (int k = 0; k < K; ++k) {
+                float w = net->W[l][(int64_t)j * K + k];
+                if (bf) w = lso_bf16_round(w);
+                acc = fmaf(w, a[k], acc);
+            }
+            z[j] = acc;
+        }
+        if (l + 1 == net->n_layers) return z[0];
+        for (int j = 0; j < O; ++j) {
+            float h = z[j] > 0.0f ? z[j] : 0.0f;
+            z[j] = bf ? lso_bf16_round(h) : h;
+        }
+        float* t = a; a = z; z = t;
+    }
+    return 0.0f;
+}
+
+/* scores[r] for raw feature rows x [rows x d] (double holding the raw values). */
+int lso_forward(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params,
+                const float* mu, const float* inv_sigma, int64_t rows, const double* x, double* scores, int threads)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    set_threads(threads);
+#pragma omp parallel
+    {
+        double* da = (double*)malloc(sizeof(double) * (size_t)net.max_width);
+        double* db = (double*)malloc(sizeof(double) * (size_t)net.max_width);
+        float* fa = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+        float* fb = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+#pragma omp for schedule(static)
+        for (int64_t r = 0; r < rows; ++r) {
+            const double* xr = x + r * d;
+            scores[r] = (mode == LSO_F64) ? forward_f64(&net, mu, inv_sigma, xr, da, db)
+                                          : (double)forward_lowp(mode, &net, mu, inv_sigma, xr, fa, fb);
+        }
+        free(da); free(db); free(fa); free(fb);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Greedy routing (Section 4.1: route to the highest predicted reward; Alg. 4  */
+/* argmax).  With the model predicting TTFT this is the smallest prediction.   */
+/* Ties go to the lowest instance id; -0 equals +0; NaN ranks after +inf, so   */
+/* NaN wins only when every score is NaN, and then instance 0 wins.            */
+/* ------------------------------------------------------------------------- */
+static int better(double a, int32_t ia, double b, int32_t ib)
+{
+    if (isnan(a)) return isnan(b) && ia < ib;
+    if (isnan(b)) return 1;
+    if (a < b) return 1;
+    if (a > b) return 0;
+    return ia < ib;
+}
+
+int32_t lso_argmin(int32_t N, const double* scores, double* min_out)
+{
+    int32_t best = 0;
+    for (int32_t i = 1; i < N; ++i)
+        if (better(scores[i], i, scores[best], best)) best = i;
+    if (min_out) *min_out = N > 0 ? scores[best] : NAN;
+    return best;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Whole scoring pass for selected requests: overlap, features, model, argmin. */
+/* Outputs are indexed by position q in sel (all requests when sel == NULL).   */
+/* feat_out (nullable) receives the raw feature row of the chosen pair.        */
+/* ------------------------------------------------------------------------- */
+int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params,
+              const float* mu, const float* inv_sigma,
+              int32_t n_sel, const int32_t* sel, const int64_t* req_off, const uint64_t* req_hashes,
+              const int32_t* prompt_len, int32_t N, const float* inst_feat,
+              const int64_t* inst_off, const uint64_t* inst_hashes,
+              int32_t* overlap_out, double* scores_out, int32_t* chosen_out, double* min_out,
+              double* feat_out, int threads)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    if (d <= LSO_DERIVED || N < 1) return -1;
+    int32_t d_inst = d - LSO_DERIVED;
+    set_threads(threads);
+    lso_set* sets = (lso_set*)calloc((size_t)N, sizeof(lso_set));
+    if (!sets) return -2;
+    build_sets(N, inst_off, inst_hashes, sets);
+#pragma omp parallel
+    {
+        double* x = (double*)malloc(sizeof(double) * (size_t)d * (size_t)N);
+        double* s = (double*)malloc(sizeof(double) * (size_t)N);
+        int32_t* ov = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+        double* da = (double*)malloc(sizeof(double) * (size_t)net.max_width);
+        double* db = (double*)malloc(sizeof(double) * (size_t)net.max_width);
+        float* fa = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+        float* fb = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+#pragma omp for schedule(dynamic, 1)
+        for (int32_t q = 0; q < n_sel; ++q) {
+            int32_t r = sel ? sel[q] : q;
+            int64_t n = req_off[r + 1] - req_off[r];
+            for (int32_t i = 0; i < N; ++i) {
+                ov[i] = overlap_one(req_hashes + req_off[r], n, &sets[i]);
+                double* xi = x + (int64_t)i * d;
+                lso_features(mode, d_inst, inst_feat + (int64_t)i * d_inst, prompt_len[r], (int32_t)n, ov[i], xi);
+                s[i] = (mode == LSO_F64) ? forward_f64(&net, mu, inv_sigma, xi, da, db)
+                                         : (double)forward_lowp(mode, &net, mu, inv_sigma, xi, fa, fb);
+            }
+            double m;
+            int32_t c = lso_argmin(N, s, &m);
+            if (overlap_out) memcpy(overlap_out + (int64_t)q * N, ov, sizeof(int32_t) * (size_t)N);
+            if (scores_out) memcpy(scores_out + (int64_t)q * N, s, sizeof(double) * (size_t)N);
+            if (chosen_out) chosen_out[q] = c;
+            if (min_out) min_out[q] = m;
+            if (feat_out) memcpy(feat_out + (int64_t)q * d, x + (int64_t)c * d, sizeof(double) * (size_t)d);
+        }
+        free(x); free(s); free(ov); free(da); free(db); free(fa); free(fb);
+    }
+    free_sets(N, sets);
+    free(sets);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Online update (Section 4.3.2: the predictor is retrained on recent          */
+/* (features, observed TTFT) records).  The paper does not state the loss or   */
+/* the optimiser; this is one plain SGD step on the mean squared error,        */
+/*   L = (1/B) sum_b (t_b - y_b)^2,   W <- W - lr * dL/dW,                      */
+/* with gradients by the chain rule through the ReLU layers and accumulated in */
+/* double precision over samples in ascending order.                           */
+/* Mode LSO_BF16 rounds to bfloat16 exactly the quantities the kernel holds in */
+/* bfloat16 (inputs, weights and activations of every layer, and every layer's */
+/* output gradient before it multiplies anything); sums stay in double.        */
+/* grad_out (nullable, double, same packing as params), loss_out (nullable).   */
+/* ------------------------------------------------------------------------- */
+int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
+               const float* mu, const float* inv_sigma, int32_t B, const float* feats, const float* ttft,
+               float lr, double* grad_out, double* loss_out)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    if (B < 1) return -1;
+    int bf = (mode == LSO_BF16);
+    int L = net.n_layers;
+    int64_t P = lso_param_count(d, n_hidden, hidden);
+    double* grad = (double*)calloc((size_t)P, sizeof(double));
+    int W = net.max_width;
+    /* act[l] = input of layer l (act[0] = normalised features), pre[l] = pre-activation of layer l */
+    double* act = (double*)malloc(sizeof(double) * (size_t)W * (size_t)(L + 1));
+    double* pre = (double*)malloc(sizeof(double) * (size_t)W * (size_t)L);
+    double* delta = (double*)malloc(sizeof(double) * (size_t)W);
+    double* dnext = (double*)malloc(sizeof(double) * (size_t)W);
+    /* weights as used by the arithmetic of this mode */
+    double* Wq = (double*)malloc(sizeof(double) * (size_t)P);
+    for (int64_t t = 0; t < P; ++t) Wq[t] = (double)params[t];
+    if (bf)
+        for (int l = 0; l < L; ++l)
+            for (int64_t t = 0; t < (int64_t)net.out[l] * net.in[l]; ++t)
+                Wq[net.W_off[l] + t] = (double)lso_bf16_round(params[net.W_off[l] + t]);
+    double loss = 0.0;
+
+    for (int32_t b = 0; b < B; ++b) {
+        const float* xb = feats + (int64_t)b * d;
+        double* a0 = act;
+        for (int k = 0; k < d; ++k) {
+            if (bf) {
+                float t = xb[k] - mu[k];
+                t = t * inv_sigma[k];
+                a0[k] = (double)lso_bf16_round(t);
+            } else {
+                a0[k] = ((double)xb[k] - (double)mu[k]) * (double)inv_sigma[k];
+            }
+        }
+        /* forward */
+        for (int l = 0; l < L; ++l) {
+            int K = net.in[l], O = net.out[l];
+            const double* a = act + (int64_t)l * W;
+            double* z = pre + (int64_t)l * W;
+            double* an = act + (int64_t)(l + 1) * W;
+            for (int j = 0; j < O; ++j) {
+                double acc = (double)params[net.b_off[l] + j];
+                for (int k = 0; k < K; ++k) acc += Wq[net.W_off[l] + (int64_t)j * K + k] * a[k];
+                if (bf) acc = (double)(float)acc;
+                z[j] = acc;
+                if (l + 1 < L) {
+                    double h = acc > 0.0 ? acc : 0.0;
+                    an[j] = bf ? (double)lso_bf16_round((float)h) : h;
+                }
+            }
+        }
+        double t_hat = pre[(int64_t)(L - 1) * W];
+        double err = t_hat - (double)ttft[b];
+        loss += err * err;
+        /* backward: delta holds dL/dz of the current layer */
+        double g = 2.0 * err / (double)B;
+        delta[0] = bf ? (double)lso_bf16_round((float)g) : g;
+        for (int l = L - 1; l >= 0; --l) {
+            int K = net.in[l], O = net.out[l];
+            const double* a = act + (int64_t)l * W;
+            for (int j = 0; j < O; ++j) {
+                double dj = delta[j];
+                double* gw = grad + net.W_off[l] + (int64_t)j * K;
+                for (int k = 0; k < K; ++k) gw[k] += dj * a[k];
+                grad[net.b_off[l] + j] += dj;
+            }
+            if (l == 0) break;
+            const double* zp = pre + (int64_t)(l - 1) * W;
+            for (int k = 0; k < K; ++k) {
+                double s = 0.0;
+                for (int j = 0; j < O; ++j) s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];
+                if (bf) s = (double)(float)s;
+                double dk = zp[k] > 0.0 ? s : 0.0;
+                dnext[k] = bf ? (double)lso_bf16_round((float)dk) : dk;
+            }
+            memcpy(delta, dnext, sizeof(double) * (size_t)K);
+        }
+    }
+    if (loss_out) *loss_out = loss / (double)B;
+    for (int64_t t = 0; t < P; ++t) {
+        if (grad_out) grad_out[t] = grad[t];
+        params[t] = (float)((double)params[t] - (double)lr * grad[t]);
+    }
+    free(grad); free(act); free(pre); free(delta); free(dnext); free(Wq);
+    return 0;
+}

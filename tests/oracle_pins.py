@@ -1,0 +1,409 @@
+"""Pins for the CPU oracle: checks against facts fixed outside the oracle.
+
+Each ``pin_*`` function raises AssertionError when the oracle disagrees with a
+hand-derived fixture, a closed form, an invariant of the definition, a library
+routine on a special case, or brute force on tiny inputs.  The same functions
+run against the real oracle (test_oracle_pins.py) and against deliberately
+broken copies of it (test_oracle_mutants.py), which must each fail at least one.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import os
+
+import numpy as np
+
+import oracle
+
+GOLD = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def golden(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def _csr(lists, dtype=np.uint64):
+    off = np.zeros(len(lists) + 1, dtype=np.int64)
+    off[1:] = np.cumsum([len(x) for x in lists])
+    flat = np.array([v for x in lists for v in x], dtype=dtype) if off[-1] else np.zeros(0, dtype)
+    return off, flat
+
+
+def _pack(layers):
+    """layers: list of (W [out, in], b [out]) -> flat fp32 in the oracle's packing."""
+    return np.concatenate([np.concatenate([np.asarray(W, np.float64).ravel(), np.asarray(b, np.float64)])
+                           for W, b in layers]).astype(np.float32)
+
+
+def _brute_overlap(req, cache):
+    """Largest k such that every one of the first k request blocks is cached."""
+    s = set(int(v) for v in cache)
+    best = 0
+    for k in range(len(req) + 1):
+        if all(int(h) in s for h in req[:k]):
+            best = k
+    return best
+
+
+# ---------------------------------------------------------------------------
+# bfloat16 rounding
+# ---------------------------------------------------------------------------
+def pin_bf16_definition():
+    f = np.float32
+    hand = [
+        (1.0, 1.0),
+        (1.00390625, 1.0),                      # 1 + 2^-8: tie -> even mantissa (1.0)
+        (1.01171875, 1.015625),                 # 1 + 3*2^-8: tie -> even (1 + 2^-6)
+        (float(np.nextafter(f(1.00390625), f(2))), 1.0078125),   # just above the tie rounds up
+        (float(np.nextafter(f(1.00390625), f(0))), 1.0),         # just below rounds down
+        (-2.0078125, -2.0),                     # -(2 + 2^-7): tie -> even
+        (2.0 ** -149, 0.0),                     # smallest subnormal vanishes
+        (2.0 ** -134, 0.0),                     # half the subnormal quantum 2^-133: tie -> 0
+        (3 * 2.0 ** -134, 2.0 ** -132),         # 1.5 quanta: tie -> even (2 quanta)
+        (float(np.finfo(np.float32).max), float("inf")),
+        (-0.0, -0.0),
+    ]
+    for x, want in hand:
+        got = float(oracle.bf16_round(np.float32(x)))
+        assert got == want and np.signbit(got) == np.signbit(want), (x, got, want)
+    assert np.isnan(oracle.bf16_round(np.float32("nan")))
+    # torch's float -> bfloat16 conversion is round-to-nearest-even as well
+    import torch
+    rng = np.random.default_rng(7)
+    vals = np.concatenate([
+        rng.standard_normal(3000).astype(np.float32),
+        (rng.standard_normal(500) * 1e-39).astype(np.float32),
+        (rng.integers(1, 1 << 16, 500).astype(np.uint32) << np.uint32(16) | np.uint32(0x8000)).view(np.float32),
+    ])
+    vals = vals[np.isfinite(vals)]
+    ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float32).numpy()
+    ours = oracle.bf16_round(vals)
+    assert np.array_equal(ours.view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# prefix overlap
+# ---------------------------------------------------------------------------
+def pin_overlap_worked_example():
+    g = golden("prefix_worked_example.json")
+    caches = [c["cache"] for c in g["cases"]]
+    inst_off, inst_h = _csr(caches)
+    req_off, req_h = _csr([g["request_hashes"]])
+    ov = oracle.overlap(req_off, req_h, inst_off, inst_h)[0]
+    assert list(ov) == [c["overlap"] for c in g["cases"]], ov
+    for c, o in zip(g["cases"], ov):
+        x = oracle.features("fp32", np.zeros(1, np.float32), g["prompt_len"], g["n_blocks"], o)
+        assert x[3] == o == c["hit_tokens"] // g["block_tokens"]
+        assert x[4] == float(np.float32(c["hit_tokens"]) / np.float32(g["prompt_len"]))
+        assert x[5] == g["prompt_len"] - c["hit_tokens"]
+
+
+def pin_overlap_bruteforce_exhaustive():
+    """Every request over a 5-letter alphabet up to 4 blocks against every cache subset."""
+    alphabet = [0, 1, 2, 3, (1 << 64) - 1]
+    reqs = [list(t) for k in range(5) for t in itertools.product(alphabet, repeat=k)]
+    caches = [[a for bit, a in enumerate(alphabet) if m >> bit & 1] for m in range(1 << len(alphabet))]
+    req_off, req_h = _csr(reqs)
+    inst_off, inst_h = _csr(caches)
+    ov = oracle.overlap(req_off, req_h, inst_off, inst_h)
+    for r, req in enumerate(reqs):
+        for i, cache in enumerate(caches):
+            assert ov[r, i] == _brute_overlap(req, cache), (req, cache, ov[r, i])
+
+
+def pin_overlap_invariants(seed=3, trials=60):
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        n = int(rng.integers(0, 12))
+        req = rng.integers(0, 20, n).astype(np.uint64)
+        cache = rng.choice(20, int(rng.integers(0, 20)), replace=False).astype(np.uint64)
+        extra = rng.integers(0, 20, 5).astype(np.uint64)
+        bigger = np.concatenate([cache, extra])
+        perm_dup = np.concatenate([cache[::-1], cache[: len(cache) // 2]])
+        full = np.concatenate([cache, req])
+        k = int(rng.integers(0, n + 1))
+        reqs = [req, req[:k]]
+        caches = [cache, bigger, perm_dup, full]
+        ov = oracle.overlap(*_csr([list(r) for r in reqs]), *_csr([list(c) for c in caches]))
+        l = ov[0, 0]
+        assert 0 <= l <= n
+        assert ov[0, 1] >= l                         # monotone in cache contents
+        assert ov[0, 2] == l                         # order and duplicates of the cache are irrelevant
+        assert ov[0, 3] == n                         # a cache holding every block gives a full run
+        assert ov[1, 0] == min(l, k)                 # truncating the request truncates the run
+        if n and int(req[0]) not in set(cache.tolist()):
+            assert l == 0
+        assert l == _brute_overlap(list(req), list(cache))
+
+
+# ---------------------------------------------------------------------------
+# features
+# ---------------------------------------------------------------------------
+def pin_features_closed_form():
+    row = np.array([3.0, -1.5, 0.25], np.float32)
+    x = oracle.features("fp32", row, 64, 4, 2)
+    assert list(x) == [3.0, -1.5, 0.25, 64.0, 4.0, 2.0, 0.5, 32.0]
+    x = oracle.features("f64", row, 87, 5, 2)
+    assert x[6] == 32.0 / 87.0 and x[7] == 55.0
+    x = oracle.features("fp32", row, 87, 5, 2)
+    assert x[6] == float(np.float32(32.0) / np.float32(87.0))
+    x = oracle.features("bf16", row, 0, 0, 0)
+    assert x[6] == 0.0 and x[7] == 0.0
+    x = oracle.features("f64", row, 8191, 511, 511)
+    assert x[6] == 8176.0 / 8191.0 and x[7] == 15.0
+
+
+# ---------------------------------------------------------------------------
+# forward pass and argmin
+# ---------------------------------------------------------------------------
+def _golden_net():
+    g = golden("mlp_two_pair_example.json")
+    params = _pack([(g["W1"], g["b1"]), (g["W2"], g["b2"]), (g["W3"], g["b3"])])
+    return g, params
+
+
+def pin_forward_golden():
+    g, params = _golden_net()
+    d = g["d"]
+    mu = np.zeros(d, np.float32); s = np.ones(d, np.float32)
+    for mode in ("f64", "fp32", "bf16"):
+        t = oracle.forward(mode, d, g["hidden"], params, mu, s, np.array(g["x"]))
+        assert list(t) == g["scores"], (mode, t)
+        assert oracle.argmin(t)[0] == g["chosen"]
+    # normalisation: x' = x * 2 + 1 with mu = 1 and inv_sigma = 0.5 gives the same inputs back
+    xs = np.array(g["x"]) * 2.0 + 1.0
+    t = oracle.forward("fp32", d, g["hidden"], params, np.ones(d, np.float32), np.full(d, 0.5, np.float32), xs)
+    assert list(t) == g["scores"]
+
+
+def pin_forward_bf16_rounding_points():
+    """One-unit nets (d = 1, hidden = [1]) in which exactly one quantity is not a
+    bfloat16 number, so each rounding point of the bf16 mode shows by itself.
+    Values are powers-of-two sums worked by hand; the fp32 mode keeps them."""
+    one = np.ones(1, np.float32); zero = np.zeros(1, np.float32)
+    cases = [
+        # (x, W1, b1, W2, b2, bf16 result, fp32 result)
+        (1 + 2**-8 + 2**-10, 1.0, 0.0, 1.0, 0.0, 1 + 2**-7, 1 + 2**-8 + 2**-10),   # input rounds up (0.625 quanta)
+        (1.0, 1 + 2**-10, 0.0, 1.0, 0.0, 1.0, 1 + 2**-10),                         # layer-1 weight rounds down
+        (3.0, 1 + 2**-7, 0.0, 1.0, 0.0, 3 + 2**-5, 3 + 3 * 2**-7),                  # activation 3.0234375: tie -> 3.03125
+        (1.0, 1.0, 0.0, 1 + 2**-10, 0.0, 1.0, 1 + 2**-10),                         # head weight rounds down
+        (1.0, 1.0, 2**-12, 1.0, 2**-12, 1 + 2**-12, 1 + 2**-11),                  # activation rounds, biases do not
+    ]
+    for x, w1, b1, w2, b2, want_bf, want_32 in cases:
+        params = np.array([w1, b1, w2, b2], np.float32)
+        t_bf = oracle.forward("bf16", 1, [1], params, zero, one, np.array([[x]]))[0]
+        t_32 = oracle.forward("fp32", 1, [1], params, zero, one, np.array([[x]]))[0]
+        assert t_bf == want_bf and t_32 == want_32, (x, w1, b1, w2, b2, t_bf, t_32)
+
+
+def pin_forward_linear_special_case(seed=5):
+    """Positive weights, biases and inputs keep every ReLU open: the net is the
+    affine map W3 (W2 (W1 x + b1) + b2) + b3."""
+    rng = np.random.default_rng(seed)
+    d, hidden = 7, [9, 6]
+    dims = [d, *hidden, 1]
+    layers = [(rng.uniform(0.1, 1.0, (dims[i + 1], dims[i])), rng.uniform(0.0, 0.5, dims[i + 1]))
+              for i in range(3)]
+    params = _pack(layers)
+    mu = rng.uniform(-1, 0, d).astype(np.float32)
+    s = rng.uniform(0.5, 2, d).astype(np.float32)
+    x = rng.uniform(0, 3, (11, d))
+    t = oracle.forward("f64", d, hidden, params, mu, s, x)
+    W = [np.asarray(L[0], np.float32).astype(np.float64) for L in layers]
+    b = [np.asarray(L[1], np.float32).astype(np.float64) for L in layers]
+    xt = (x - mu.astype(np.float64)) * s.astype(np.float64)
+    ref = (W[2] @ (W[1] @ (W[0] @ xt.T + b[0][:, None]) + b[1][:, None]) + b[2][:, None])[0]
+    assert np.allclose(t, ref, rtol=1e-12, atol=0), (t, ref)
+
+
+def pin_forward_relu_closed():
+    """A last hidden layer pushed far negative outputs zeros: t = b_out exactly."""
+    rng = np.random.default_rng(9)
+    d, hidden = 6, [8, 5]
+    layers = [(rng.standard_normal((8, 6)), rng.standard_normal(8)),
+              (rng.uniform(-1, 0, (5, 8)), np.full(5, -50.0)),
+              (rng.standard_normal((1, 5)), np.array([0.375]))]
+    params = _pack(layers)
+    x = rng.uniform(-1, 1, (9, d))
+    for mode in ("f64", "fp32", "bf16"):
+        t = oracle.forward(mode, d, hidden, params, np.zeros(d, np.float32), np.ones(d, np.float32), x)
+        assert np.all(t == 0.375), (mode, t)
+
+
+def pin_forward_lowp_bound(seed=11):
+    """The fp32 chain stays within the classic dot-product error bound of the
+    double-precision definition (gamma_K per layer, propagated with |W|)."""
+    rng = np.random.default_rng(seed)
+    d, hidden = 16, [32, 24]
+    dims = [d, *hidden, 1]
+    layers = [(rng.normal(0, np.sqrt(2 / dims[i]), (dims[i + 1], dims[i])), rng.uniform(-0.1, 0.1, dims[i + 1]))
+              for i in range(3)]
+    params = _pack(layers)
+    mu = np.zeros(d, np.float32); s = np.ones(d, np.float32)
+    x = rng.standard_normal((200, d)).astype(np.float32).astype(np.float64)
+    t64 = oracle.forward("f64", d, hidden, params, mu, s, x)
+    t32 = oracle.forward("fp32", d, hidden, params, mu, s, x)
+    # crude rigorous-enough bound: relative 1e-5 of the magnitude of |W| |a| sums
+    absnet = _pack([(np.abs(np.asarray(W, np.float32)), np.abs(np.asarray(b, np.float32))) for W, b in layers])
+    mag = oracle.forward("f64", d, hidden, absnet, mu, s, np.abs(x))
+    assert np.all(np.abs(t32 - t64) <= 1e-5 * mag + 1e-30), np.max(np.abs(t32 - t64) / mag)
+    assert not np.array_equal(t32, t64)              # the modes really do differ in rounding
+
+
+def pin_argmin_rules():
+    nan, inf = float("nan"), float("inf")
+    cases = [
+        ([3.0, 1.0, 2.0], 1),
+        ([1.0, 1.0, 0.5, 0.5], 2),                # exact tie -> lowest id
+        ([0.0, -0.0], 0), ([-0.0, 0.0], 0),       # signed zeros compare equal
+        ([nan, inf, 5.0], 2),
+        ([nan, inf], 1),                          # NaN ranks after +inf
+        ([nan, nan, nan], 0),                     # all NaN -> instance 0
+        ([-inf, -inf], 0),
+        ([7.0], 0),
+    ]
+    for s, want in cases:
+        got, m = oracle.argmin(np.array(s))
+        assert got == want, (s, got)
+        assert (np.isnan(m) and np.isnan(s[want])) or m == s[want]
+
+
+# ---------------------------------------------------------------------------
+# online update
+# ---------------------------------------------------------------------------
+def _check_grad(res, want, d, hidden):
+    shapes = [(2, 3), (2,), (2, 2), (2,), (1, 2), (1,)]
+    names = ["dW1", "db1", "dW2", "db2", "dW3", "db3"]
+    off = 0
+    for name, shp in zip(names, shapes):
+        n = int(np.prod(shp))
+        got = res["grad"][off:off + n]
+        assert np.array_equal(got, np.asarray(want[name], np.float64).ravel()), (name, got, want[name])
+        off += n
+
+
+def pin_update_golden():
+    g, params = _golden_net()
+    d = g["d"]
+    mu = np.zeros(d, np.float32); s = np.ones(d, np.float32)
+    sg = g["sgd"]
+    for mode in ("f64", "bf16"):
+        res = oracle.update(mode, d, g["hidden"], params, mu, s, np.array(g["x"]), np.array(sg["ttft"]), sg["lr"])
+        assert res["loss"] == sg["loss"], (mode, res["loss"])
+        _check_grad(res, sg, d, g["hidden"])
+        want = _pack([(sg["W1_new"], sg["b1_new"]), (sg["W2_new"], sg["b2_new"]), (sg["W3_new"], sg["b3_new"])])
+        assert np.array_equal(res["params"], want), (mode, res["params"], want)
+    one = g["sgd_first_sample_only"]
+    res = oracle.update("f64", d, g["hidden"], params, mu, s, np.array(g["x"][:1]), np.array(one["ttft"]), 0.25)
+    assert res["loss"] == one["loss"]
+    _check_grad(res, one, d, g["hidden"])
+
+
+def pin_update_bf16_rounding_points():
+    """One-unit net, one sample (d = 1, hidden = [1], x = 1, W1 = 1, b = 0,
+    head weight w = 1 + 2^-7).  t = w, g = 2 (t - y); the hidden-unit gradient
+    is w * g.  In bf16 mode g and w * g are rounded to bfloat16 before they
+    multiply anything; in f64 mode nothing is.  Values worked by hand."""
+    w = 1 + 2**-7
+    params = np.array([1.0, 0.0, w, 0.0], np.float32)
+    one = np.ones(1, np.float32); zero = np.zeros(1, np.float32)
+    x = np.ones((1, 1), np.float32)
+    cases = [
+        # y, mode, loss, [dW1, db1, dW2, db2]
+        (0.0, "bf16", 1.01568603515625, [2.03125, 2.03125, 2.015625, 2.015625]),        # w*g = 2.0313720703125 rounds
+        (0.0, "f64", 1.01568603515625, [2.0313720703125, 2.0313720703125, 2.015625, 2.015625]),
+        (2**-9, "bf16", 1.011753082275390625, [2.03125, 2.03125, 2.015625, 2.015625]),  # g = 2.01171875 rounds up
+        (2**-9, "f64", 1.011753082275390625, [2.027435302734375, 2.027435302734375, 2.01171875, 2.01171875]),
+    ]
+    for y, mode, loss, grad in cases:
+        res = oracle.update(mode, 1, [1], params, zero, one, x, np.array([y], np.float32), 0.0)
+        assert res["loss"] == loss and list(res["grad"]) == grad, (y, mode, res["loss"], res["grad"])
+
+
+def pin_update_invariants(seed=13):
+    rng = np.random.default_rng(seed)
+    d, hidden = 6, [7, 5]
+    dims = [d, *hidden, 1]
+    params = _pack([(rng.normal(0, 0.6, (dims[i + 1], dims[i])), rng.uniform(-0.2, 0.2, dims[i + 1])) for i in range(3)])
+    mu = rng.normal(0, 1, d).astype(np.float32); s = rng.uniform(0.5, 2, d).astype(np.float32)
+    x = rng.normal(0, 2, (8, d)).astype(np.float32); y = rng.uniform(0, 2, 8).astype(np.float32)
+    r0 = oracle.update("f64", d, hidden, params, mu, s, x, y, 0.0)
+    assert np.array_equal(r0["params"], params)                    # lr = 0 leaves the model unchanged
+    # the batch gradient is the mean of single-sample gradients
+    parts = [oracle.update("f64", d, hidden, params, mu, s, x[b:b + 1], y[b:b + 1], 0.1)["grad"] for b in range(8)]
+    assert np.allclose(r0["grad"], np.mean(parts, axis=0), rtol=1e-12, atol=1e-15)
+    # the step moves against the gradient
+    r1 = oracle.update("f64", d, hidden, params, mu, s, x, y, 1e-3)
+    dp = r1["params"].astype(np.float64) - params.astype(np.float64)
+    assert np.sum(dp * r0["grad"]) < 0
+    # loss agrees with the forward pass
+    t = oracle.forward("f64", d, hidden, params, mu, s, x.astype(np.float64))
+    assert np.isclose(r0["loss"], np.mean((t - y.astype(np.float64)) ** 2), rtol=1e-13)
+
+
+def pin_update_finite_difference(seed=17):
+    """Central differences of the forward-pass loss, in double precision."""
+    rng = np.random.default_rng(seed)
+    d, hidden = 5, [6, 4]
+    dims = [d, *hidden, 1]
+    params = _pack([(rng.normal(0, 0.8, (dims[i + 1], dims[i])), rng.uniform(-0.3, 0.3, dims[i + 1])) for i in range(3)])
+    mu = rng.normal(0, 0.5, d).astype(np.float32); s = rng.uniform(0.5, 1.5, d).astype(np.float32)
+    x = rng.normal(0, 2, (6, d)); y = rng.uniform(-1, 1, 6)
+    res = oracle.update("f64", d, hidden, params, mu, s, x.astype(np.float32), y.astype(np.float32), 0.0)
+
+    def loss(p):
+        t = oracle.forward("f64", d, hidden, p, mu, s, x.astype(np.float32).astype(np.float64))
+        return np.mean((t - y.astype(np.float32).astype(np.float64)) ** 2)
+
+    h = 2.0 ** -14
+    fd = np.zeros(params.shape[0])
+    for k in range(params.shape[0]):
+        pp = params.copy(); pm = params.copy()
+        pp[k] += np.float32(h); pm[k] -= np.float32(h)
+        fd[k] = (loss(pp) - loss(pm)) / (float(pp[k]) - float(pm[k]))
+    err = np.abs(fd - res["grad"]) / np.maximum(np.abs(res["grad"]), 1e-6)
+    assert np.mean(err < 1e-6) >= 0.95 and np.median(err) < 1e-8, (np.sort(err)[-5:], np.median(err))
+
+
+# ---------------------------------------------------------------------------
+# the whole scoring pass against an independent numpy pipeline on tiny inputs
+# ---------------------------------------------------------------------------
+def pin_score_pipeline_bruteforce(seed=19):
+    rng = np.random.default_rng(seed)
+    N, R, d_inst, hidden = 5, 9, 3, [6, 4]
+    d = d_inst + 5
+    caches = [list(rng.choice(12, int(rng.integers(0, 12)), replace=False)) for _ in range(N)]
+    reqs = [list(rng.integers(0, 12, int(rng.integers(0, 8)))) for _ in range(R)]
+    L = np.array([16 * len(r) + int(rng.integers(0, 16)) for r in reqs], np.int32)
+    feat = rng.uniform(0, 4, (N, d_inst)).astype(np.float32)
+    dims = [d, *hidden, 1]
+    layers = [(rng.normal(0, 0.7, (dims[i + 1], dims[i])), rng.uniform(-0.2, 0.2, dims[i + 1])) for i in range(3)]
+    params = _pack(layers)
+    mu = rng.normal(0, 1, d).astype(np.float32); s = rng.uniform(0.2, 1, d).astype(np.float32)
+    req_off, req_h = _csr(reqs); inst_off, inst_h = _csr(caches)
+    out = oracle.score("f64", d, hidden, params, mu, s, req_off, req_h, L, feat, inst_off, inst_h)
+    W = [np.asarray(Lr[0], np.float32).astype(np.float64) for Lr in layers]
+    b = [np.asarray(Lr[1], np.float32).astype(np.float64) for Lr in layers]
+    for r in range(R):
+        ov = np.array([_brute_overlap(reqs[r], c) for c in caches])
+        assert np.array_equal(out["overlap"][r], ov)
+        x = np.concatenate([feat.astype(np.float64),
+                            np.full((N, 1), float(L[r])), np.full((N, 1), float(len(reqs[r]))),
+                            ov[:, None].astype(np.float64),
+                            (16.0 * ov / L[r])[:, None] if L[r] else np.zeros((N, 1)),
+                            (L[r] - 16.0 * ov)[:, None]], axis=1)
+        a = (x - mu.astype(np.float64)) * s.astype(np.float64)
+        for l in range(3):
+            a = a @ W[l].T + b[l]
+            if l < 2:
+                a = np.maximum(a, 0.0)
+        t = a[:, 0]
+        assert np.allclose(out["scores"][r], t, rtol=1e-12, atol=1e-14), (out["scores"][r], t)
+        best = int(np.lexsort((np.arange(N), t))[0])
+        assert out["chosen"][r] == best and out["min_ttft"][r] == out["scores"][r][best]
+        assert np.array_equal(out["feat"][r], x[best])
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -1,0 +1,91 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and check that
+the pins catch every one of them.  This is what makes the pins worth trusting:
+a dropped term, a wrong sign, index or operand order anywhere in the oracle
+fails at least one of them."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "lodestar_oracle.c")
+
+# (name, original text, replacement): each must occur exactly once in the source
+MUTANTS = [
+    ("overlap_counts_all_cached", "if (!in_set(s, h[j])) break;", "if (!in_set(s, h[j])) continue;"),
+    ("overlap_off_by_one", "int32_t l = 0;\n    for (int64_t j = 0; j < n; ++j) {",
+     "int32_t l = 1;\n    for (int64_t j = 1; j < n; ++j) {"),
+    ("sets_not_deduplicated_wrongly", "if (u == 0 || k[u - 1] != k[t]) k[u++] = k[t];",
+     "if (u == 0 || k[u - 1] != k[t]) k[u++] = k[t]; else break;"),
+    ("hit_ratio_half_block", "int64_t hit_tokens = (int64_t)LSO_BLOCK_TOKENS * l;",
+     "int64_t hit_tokens = (int64_t)(LSO_BLOCK_TOKENS / 2) * l;"),
+    ("uncached_tokens_sign", "x[d_inst + 4] = (double)((int64_t)L - hit_tokens);",
+     "x[d_inst + 4] = (double)(hit_tokens - (int64_t)L);"),
+    ("columns_swapped", "x[d_inst + 0] = (double)L;\n    x[d_inst + 1] = (double)n;",
+     "x[d_inst + 0] = (double)n;\n    x[d_inst + 1] = (double)L;"),
+    ("f64_normalise_sign", "buf_a[k] = (x[k] - (double)mu[k]) * (double)inv_sigma[k];",
+     "buf_a[k] = (x[k] + (double)mu[k]) * (double)inv_sigma[k];"),
+    ("lowp_normalise_divides", "t = t * inv_sigma[k];\n        buf_a[k]", "t = t / inv_sigma[k];\n        buf_a[k]"),
+    ("f64_drops_bias", "double acc = (double)net->b[l][j];\n            for (int k = 0; k < K; ++k) acc +=",
+     "double acc = 0.0;\n            for (int k = 0; k < K; ++k) acc +="),
+    ("lowp_drops_bias", "float acc = net->b[l][j];", "float acc = 0.0f;"),
+    ("f64_transposed_weight", "acc += (double)net->W[l][(int64_t)j * K + k] * a[k];",
+     "acc += (double)net->W[l][(int64_t)k * O + j] * a[k];"),
+    ("lowp_skips_last_input", "for (int k = 0; k < K; ++k) {\n                float w",
+     "for (int k = 0; k + 1 < K; ++k) {\n                float w"),
+    ("f64_no_relu", "for (int j = 0; j < O; ++j) z[j] = z[j] > 0.0 ? z[j] : 0.0;", ""),
+    ("lowp_leaky_relu", "float h = z[j] > 0.0f ? z[j] : 0.0f;", "float h = z[j] > 0.0f ? z[j] : 0.01f * z[j];"),
+    ("bf16_skips_weights", "if (bf) w = lso_bf16_round(w);", ""),
+    ("bf16_ties_away", "double q = nearbyint((double)x * scale);", "double q = round((double)x * scale);"),
+    ("bf16_truncates", "double q = nearbyint((double)x * scale);", "double q = trunc((double)x * scale);"),
+    ("argmin_tie_highest", "    return ia < ib;\n}\n\nint32_t lso_argmin", "    return ia > ib;\n}\n\nint32_t lso_argmin"),
+    ("argmin_nan_first", "if (isnan(b)) return 1;", "if (isnan(b)) return 0;"),
+    ("argmin_is_argmax", "if (a < b) return 1;\n    if (a > b) return 0;", "if (a > b) return 1;\n    if (a < b) return 0;"),
+    ("update_wrong_sign", "params[t] = (float)((double)params[t] - (double)lr * grad[t]);",
+     "params[t] = (float)((double)params[t] + (double)lr * grad[t]);"),
+    ("update_no_factor_two", "double g = 2.0 * err / (double)B;", "double g = err / (double)B;"),
+    ("update_sum_not_mean", "double g = 2.0 * err / (double)B;", "double g = 2.0 * err;"),
+    ("update_mask_ignored", "double dk = zp[k] > 0.0 ? s : 0.0;", "double dk = s;"),
+    ("update_weight_grad_transposed", "for (int k = 0; k < K; ++k) gw[k] += dj * a[k];",
+     "for (int k = 0; k < K; ++k) gw[k] += dj * a[(k + 1) % K];"),
+    ("update_backprop_uses_row", "s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];",
+     "s += Wq[net.W_off[l] + (int64_t)k * O + j] * delta[j];"),
+    ("update_no_bias_grad", "grad[net.b_off[l] + j] += dj;", ""),
+    ("update_bf16_delta_unrounded", "dnext[k] = bf ? (double)lso_bf16_round((float)dk) : dk;", "dnext[k] = dk;"),
+    ("update_loss_not_mean", "if (loss_out) *loss_out = loss / (double)B;", "if (loss_out) *loss_out = loss;"),
+]
+
+_RUNNER = r"""
+import sys
+sys.path[:0] = [{root!r}, {tests!r}]
+import oracle
+oracle.use_library({lib!r})
+import oracle_pins
+failed = []
+for pin in oracle_pins.ALL_PINS:
+    try:
+        pin()
+    except Exception as e:
+        failed.append(pin.__name__)
+print("FAILED:" + ",".join(failed))
+"""
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(name, old, new, tmp_path):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} must occur once"
+    mutant_src = tmp_path / "mutant.c"
+    mutant_src.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    oracle.compile_c(str(mutant_src), lib)
+    code = _RUNNER.format(root=ROOT, tests=os.path.join(ROOT, "tests"), lib=lib)
+    proc = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    if proc.returncode != 0:
+        return                                  # the mutant crashed: caught
+    line = [l for l in proc.stdout.splitlines() if l.startswith("FAILED:")][-1]
+    assert line != "FAILED:", f"no pin caught mutant {name}"
