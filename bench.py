@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched routing scorer on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input,
+every input already resident in HBM:
+  1. ls_load_cache_state  -- rebuild every instance's prefix-cache hash table
+  2. ls_score_batch       -- prefix overlap, features, reward model, argmin
+  3. ls_update            -- one online SGD step of the reward model
+The printed value is (request, instance) pairs scored per second of step time;
+updates per second and per-kernel timings ride along.  Per-kernel durations
+come from HIP events recorded by the library on the stream of each call.
+
+    python bench.py [--steps K] [--warmup W] [--config large_batch] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "(request,instance) pairs scored/sec + online updates/sec; % HBM/MFMA roofline"
+
+# MI355X published peaks (dense)
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+# fp32 FMA on the vector ALUs without packed-fp32 instructions (disabled in this
+# build): 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
+PEAK_VALU_FP32_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def model_flops_per_pair(cfg):
+    d, (h1, h2) = cfg.d, cfg.hidden
+    return 2 * (d * h1 + h1 * h2 + h2)
+
+
+def update_flops(cfg, B):
+    d, (h1, h2) = cfg.d, cfg.hidden
+    fwd = 2 * (d * h1 + h1 * h2 + h2)
+    wgrad = 2 * (d * h1 + h1 * h2 + h2)
+    igrad = 2 * (h1 * h2)                 # gradient into the first hidden layer
+    return B * (fwd + wgrad + igrad)
+
+
+def cpu_baseline(w, target_s=12.0):
+    """The oracle, untuned, on a bounded sample of requests (all instances each)."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    cfg = w.cfg
+    mode = "bf16" if cfg.dtype == "bf16" else "fp32"
+    rng = np.random.default_rng(7)
+
+    def run(S):
+        sel = np.sort(rng.choice(cfg.R, min(S, cfg.R), replace=False)).astype(np.int32)
+        t = time.perf_counter()
+        oracle.score(mode, cfg.d, cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes, w.prompt_len,
+                     w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=threads)
+        return len(sel), time.perf_counter() - t
+
+    s0, t0 = run(16)
+    S = int(min(cfg.R, max(16, s0 * target_s / max(t0, 1e-3))))
+    s1, t1 = run(S)
+    return {
+        "value": s1 * cfg.N / t1, "unit": "pairs/s", "cores": threads, "kind": "oracle",
+        "sample": (f"{s1} of {cfg.R} requests x all {cfg.N} instances, {mode} oracle "
+                   f"(set build + overlap + features + MLP + argmin), {t1:.1f} s wall"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="large_batch")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the scorer shards by request with no collective, and this build "
+              "runs on a single MI355X; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_00946_amd import lodestar, synth
+
+    torch.cuda.set_device(0)
+    t = time.perf_counter()
+    w = synth.generate(args.config)
+    cfg = w.cfg
+    log(f"generated {cfg.name}: R={cfg.R} N={cfg.N} hashes={w.req_hashes.size} cached={w.inst_hashes.size} "
+        f"({time.perf_counter() - t:.1f} s)")
+
+    def dev(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int64) if a.dtype == np.uint64 else a).cuda()
+
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype, device=0)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    inst_h = dev(w.inst_hashes)
+    req_off, req_h, plen, feat = dev(w.req_off), dev(w.req_hashes), dev(w.prompt_len), dev(w.inst_feat)
+    upd_x, upd_y = dev(w.upd_feats), dev(w.upd_ttft)
+    R, N, B = cfg.R, cfg.N, cfg.update_batch
+    chosen = torch.empty(R, dtype=torch.int32, device="cuda")
+    min_ttft = torch.empty(R, dtype=torch.float32, device="cuda")
+    overlap = torch.empty(R * N, dtype=torch.int32, device="cuda")
+    loss = torch.empty(1, dtype=torch.float32, device="cuda")
+
+    def step():
+        ctx.ls_load_cache_state(w.inst_off, inst_h)
+        ctx.ls_score_batch(req_off, req_h, plen, feat, chosen, min_ttft, None, overlap, None)
+        ctx.ls_update(upd_x, upd_y, w.lr, loss, None)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+    ctx.ls_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = ctx.ls_profile_read()
+    ctx.ls_profile_enable(False)
+    log(f"timed {args.steps} steps: {(t1 - t0) * 1e3 / args.steps:.3f} ms/step")
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    pairs_per_s = R * N / (ms_step / 1e3)
+    phases = {k: round(v[1] / v[0], 4) for k, v in prof.items()}
+
+    # algorithmic work of each kernel kind per launch
+    n = np.diff(w.req_off)
+    ov = overlap.cpu().numpy().reshape(R, N).astype(np.int64)
+    probes = int(np.minimum(ov + 1, n[:, None]).sum())
+    k1_bytes = 64 * probes + 8 * int(n.sum()) + 4 * R * N
+    roof = {
+        "prefix_match": ("hbm", k1_bytes / 1e9, PEAK_HBM_GBS, "GB/s"),
+        "score_pairs": ("alu", model_flops_per_pair(cfg) * R * N / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
+        "update": ("alu", update_flops(cfg, B) / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
+    }
+    dom = max((k for k in prof if k in roof), key=lambda k: prof[k][1])
+    bound, work, peak, unit = roof[dom]
+    avg_s = prof[dom][1] / prof[dom][0] / 1e3
+    achieved = work / avg_s
+    result = {
+        "metric": METRIC,
+        "value": round(pairs_per_s, 1),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "requests": R, "instances": N, "update_batch": B,
+                   "cached_blocks": int(w.inst_hashes.size), "prompt_blocks": int(n.sum()),
+                   "predictor": f"{cfg.d}-{cfg.hidden[0]}-{cfg.hidden[1]}-1 {cfg.dtype}"},
+        "updates_per_s": round(1e3 / ms_step, 3),
+        "update_samples_per_s": round(B * 1e3 / ms_step, 1),
+        "kernel_ms": phases,
+        "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1),
+                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": None},
+        "useful_probes": probes,
+    }
+    ctx.close()
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

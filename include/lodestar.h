@@ -1,0 +1,177 @@
+/*
+ * lodestar.h -- C ABI of the MI355X (gfx950) batched routing scorer.
+ *
+ * The library implements the data-parallel hot path of Lodestar's learned
+ * router (arXiv 2606.00946): for every pending (request, instance) pair it
+ * measures the prefix-cache overlap of the request's block-hashed prompt with
+ * the instance's cached blocks, assembles the pair's feature row, runs the
+ * shared reward model and picks, per request, the instance with the smallest
+ * predicted TTFT (Section 4.1, Alg. 4).  It also applies one online SGD step to
+ * that model from logged (features, observed TTFT) rows (Section 4.3.2).
+ *
+ * Conventions shared by every entry point
+ *   - Every function returning int returns LS_OK (0) or a negative LS_ERR_*.
+ *     No C++ exception crosses the ABI.  ls_last_error() describes the last
+ *     failure on that context.
+ *   - Arguments are validated on the host before anything is enqueued; an
+ *     invalid call enqueues nothing and leaves the library state unchanged.
+ *   - Device pointers are caller-owned HIP device memory (for example torch
+ *     tensors on the current device); the caller keeps them alive and
+ *     unmodified until the work enqueued on `stream` has finished.
+ *   - `stream` is a hipStream_t (NULL: the legacy default stream).  Work is
+ *     asynchronous and ordered on that stream; library state (model, cache
+ *     state, workspace) is ordered by the stream of each call, so callers that
+ *     use several streams must order them themselves.
+ *   - A context is not thread-safe: use one per host thread, or serialise.
+ *   - The library owns its tables, model copies and workspace (hipMalloc);
+ *     workspace grows on demand, so a call that needs more than any earlier
+ *     call may allocate.
+ */
+#ifndef LODESTAR_H
+#define LODESTAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LS_OK 0
+#define LS_ERR_INVALID (-1)      /* bad argument, shape or null pointer */
+#define LS_ERR_NOMEM (-2)        /* device or host allocation failed */
+#define LS_ERR_DEVICE (-3)       /* a HIP runtime call or kernel launch failed */
+#define LS_ERR_STATE (-4)        /* no model or cache state yet, or an instance-count mismatch */
+#define LS_ERR_UNSUPPORTED (-5)  /* valid request this build does not implement */
+
+#define LS_FP32 0   /* fp32 weights and activations */
+#define LS_BF16 1   /* bf16 weights and layer inputs, fp32 accumulation, fp32 master weights */
+
+#define LS_MAX_HIDDEN 3
+#define LS_DERIVED_COLS 5
+
+typedef struct ls_ctx ls_ctx;
+
+/*
+ * Reward-model shape (Section 4.1, Model architecture and Features).
+ *   d          feature columns of a pair row, d > LS_DERIVED_COLS.  The row is
+ *              [ instance state (d - 5 columns) | L, n | l, kappa, u ]:
+ *              L = prompt tokens, n = hashed blocks, l = overlap in blocks,
+ *              kappa = block_tokens * l / L (0 when L = 0), u = L - block_tokens * l.
+ *   n_hidden   hidden layers (this build: 2).
+ *   hidden     widths, each 1..512.
+ *   block_tokens tokens per hashed KV block (16 in the evaluated engines).
+ *   dtype      LS_FP32 or LS_BF16.
+ */
+typedef struct ls_model_config {
+    int32_t d;
+    int32_t n_hidden;
+    int32_t hidden[LS_MAX_HIDDEN];
+    int32_t block_tokens;
+    int32_t dtype;
+} ls_model_config;
+
+/* Parameters of the packed model: for each layer d -> hidden[0] -> ... -> 1,
+ * W [out x in] row-major, then b [out].  Returns -1 for an invalid shape. */
+int64_t ls_param_count(const ls_model_config* cfg);
+
+/* Create a context on HIP device `device`.  *out is NULL on failure. */
+int ls_create(const ls_model_config* cfg, int device, ls_ctx** out);
+
+/* Wait for the context's outstanding work, free everything it owns.  NULL is a no-op. */
+void ls_destroy(ls_ctx* ctx);
+
+/* Message of the last failed call on ctx (never NULL; valid until the next call). */
+const char* ls_last_error(const ls_ctx* ctx);
+
+/*
+ * Install a model (Section 4.3.1, P2: the new model replaces the old one
+ * atomically with respect to scoring).  Host arrays, copied before return:
+ *   params     [ls_param_count] fp32, the packing above;
+ *   mu         [d] per-feature mean, inv_sigma [d] per-feature 1/sigma
+ *              (Alg. 4, per-feature z-score: x~ = (x - mu) * inv_sigma).
+ * Scoring and update calls enqueued on `stream` after this one see the new
+ * model.  LS_BF16 contexts keep fp32 masters and derive bf16 copies.
+ */
+int ls_set_model(ls_ctx* ctx, const float* params, int64_t n_params,
+                 const float* mu, const float* inv_sigma, void* stream);
+
+/* Copy the current fp32 master model to host arrays (any may be NULL).
+ * Synchronous: waits for the work enqueued on the context's streams. */
+int ls_get_model(ls_ctx* ctx, float* params, int64_t n_params, float* mu, float* inv_sigma);
+
+/*
+ * Replace the whole prefix-cache state (Section 4.2, Prefix KV cache tracker:
+ * the gateway's index of which prompt blocks each instance holds).
+ *   n_instances  N >= 1
+ *   inst_off     HOST   int64 [N+1], inst_off[0] = 0, non-decreasing: instance
+ *                i's hashes are hashes[inst_off[i] .. inst_off[i+1]).
+ *   hashes       DEVICE uint64 [inst_off[N]], any order, duplicates allowed,
+ *                every uint64 value allowed.  Read only during this call's
+ *                stream work.
+ * The library builds one hash table per instance on the device.  Instance ids
+ * are positions 0..N-1, shared with the rows of inst_feat in ls_score_batch.
+ */
+int ls_load_cache_state(ls_ctx* ctx, int32_t n_instances, const int64_t* inst_off,
+                        const uint64_t* hashes, void* stream);
+
+/*
+ * Score a batch of R requests against the N loaded instances (Section 4.1
+ * greedy routing; Alg. 4 normalise -> batched forward -> argmax of reward,
+ * here argmin of predicted TTFT, ties to the lowest instance id).
+ * DEVICE inputs:
+ *   req_off     int64 [R+1], req_off[0] = 0, non-decreasing; request r's block
+ *               hashes are req_hashes[req_off[r] .. req_off[r+1]), in prompt order.
+ *   req_hashes  uint64 [req_off[R]]
+ *   prompt_len  int32 [R] prompt tokens L (normally >= block_tokens * n_r)
+ *   inst_feat   fp32 [N x (d-5)] row-major instance-state columns
+ * DEVICE outputs (all but `chosen` may be NULL):
+ *   chosen      int32 [R]      argmin instance
+ *   min_ttft    fp32  [R]      its predicted TTFT (s); the reward is the negation
+ *   scores      fp32  [R x N]  every predicted TTFT, request-major
+ *   overlap     int32 [R x N]  leading cached blocks l (Section 2: prefix reuse
+ *                              is strictly sequential)
+ *   feat_out    fp32  [R x d]  raw feature row of the chosen pair (the training record)
+ * R = 0 is a no-op.  N must equal the loaded instance count (LS_ERR_STATE).
+ */
+int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
+                   const int64_t* req_off, const uint64_t* req_hashes, const int32_t* prompt_len,
+                   const float* inst_feat,
+                   int32_t* chosen, float* min_ttft, float* scores, int32_t* overlap, float* feat_out,
+                   void* stream);
+
+/*
+ * One SGD step on the installed model (Section 4.3.2, online learning; the
+ * loss and optimiser are this library's reading: mean squared error of the
+ * predicted TTFT, plain SGD).  L = (1/B) sum_b (t_b - y_b)^2, W <- W - lr dL/dW.
+ * DEVICE inputs:  feats fp32 [B x d] raw rows (same layout as feat_out),
+ *                 ttft  fp32 [B] observed TTFT in seconds.
+ * DEVICE outputs (nullable): loss_out fp32 [1] pre-step loss;
+ *                 grad_out fp32 [ls_param_count] dL/dW in the parameter packing.
+ * LS_BF16 contexts use bf16 GEMM operands (weights, layer inputs and each
+ * layer's output gradient), fp32 accumulation and fp32 master weights.
+ */
+int ls_update(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, float lr,
+              float* loss_out, float* grad_out, void* stream);
+
+/*
+ * Per-kernel timing (the library's own view of where the routing time goes;
+ * Section 5.4 measures the router's overhead end to end).  While enabled, each
+ * kernel launch group of the context is bracketed by HIP events on the stream
+ * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
+ * "score_pairs", "argmin", "update".
+ *   ls_profile_enable  enable != 0 starts recording (and clears old records).
+ *   ls_profile_read    synchronous; for up to max_kinds kinds writes the kind
+ *                      name (static string), the number of launches and the
+ *                      summed device time in milliseconds; *n_kinds gets the
+ *                      number of kinds with at least one launch.
+ */
+int ls_profile_enable(ls_ctx* ctx, int enable);
+int ls_profile_read(ls_ctx* ctx, int32_t max_kinds, const char** names, int64_t* launches, double* total_ms,
+                    int32_t* n_kinds);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LODESTAR_H */

@@ -23,7 +23,7 @@ _CFLAGS = ["-O2", "-mfma", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-
 
 
 def compile_c(src: str, out: str) -> str:
-    tmp = out + ".tmp"
+    tmp = f"{out}.{os.getpid()}.tmp"
     subprocess.check_call(["gcc", *_CFLAGS, "-o", tmp, src, "-lm"])
     os.replace(tmp, out)
     return out

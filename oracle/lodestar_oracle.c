@@ -222,7 +222,22 @@ static double forward_f64(const lso_net* net, const float* mu, const float* inv_
     return 0.0;
 }
 
-/* One pair in the kernel's precision (fp32 fma chains, optional bf16 operands). */
+/* Copy of the parameters with every weight (not bias) rounded to bf16. */
+static float* bf16_weights(const lso_net* net, const float* params)
+{
+    int l = net->n_layers - 1;
+    int64_t P = net->b_off[l] + net->out[l];
+    float* q = (float*)malloc(sizeof(float) * (size_t)P);
+    memcpy(q, params, sizeof(float) * (size_t)P);
+    for (l = 0; l < net->n_layers; ++l)
+        for (int64_t t = 0; t < (int64_t)net->out[l] * net->in[l]; ++t)
+            q[net->W_off[l] + t] = lso_bf16_round(params[net->W_off[l] + t]);
+    return q;
+}
+
+/* One pair in the kernel's precision (fp32 fma chains, optional bf16 operands).
+ * In LSO_BF16 mode `net` must already hold bf16-rounded weights (bf16_weights);
+ * the inputs and activations of every layer are rounded here. */
 static float forward_lowp(int mode, const lso_net* net, const float* mu, const float* inv_sigma, const double* x,
                           float* buf_a, float* buf_b)
 {
@@ -241,9 +256,7 @@ static float forward_lowp(int mode, const lso_net* net, const float* mu, const f
         for (int j = 0; j < O; ++j) {
             float acc = net->b[l][j];
             for (int k = 0; k < K; ++k) {
-                float w = net->W[l][(int64_t)j * K + k];
-                if (bf) w = lso_bf16_round(w);
-                acc = fmaf(w, a[k], acc);
+                acc = fmaf(net->W[l][(int64_t)j * K + k], a[k], acc);
             }
             z[j] = acc;
         }
@@ -263,6 +276,11 @@ int lso_forward(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, co
 {
     lso_net net;
     if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    float* q = NULL;
+    if (mode == LSO_BF16) {
+        q = bf16_weights(&net, params);
+        net_init(&net, d, n_hidden, hidden, q);
+    }
     set_threads(threads);
 #pragma omp parallel
     {
@@ -278,6 +296,7 @@ int lso_forward(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, co
         }
         free(da); free(db); free(fa); free(fb);
     }
+    free(q);
     return 0;
 }
 
@@ -322,6 +341,11 @@ int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
     if (net_init(&net, d, n_hidden, hidden, params)) return -1;
     if (d <= LSO_DERIVED || N < 1) return -1;
     int32_t d_inst = d - LSO_DERIVED;
+    float* q = NULL;
+    if (mode == LSO_BF16) {
+        q = bf16_weights(&net, params);
+        net_init(&net, d, n_hidden, hidden, q);
+    }
     set_threads(threads);
     lso_set* sets = (lso_set*)calloc((size_t)N, sizeof(lso_set));
     if (!sets) return -2;
@@ -358,6 +382,7 @@ int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
     }
     free_sets(N, sets);
     free(sets);
+    free(q);
     return 0;
 }
 
@@ -368,9 +393,14 @@ int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
 /*   L = (1/B) sum_b (t_b - y_b)^2,   W <- W - lr * dL/dW,                      */
 /* with gradients by the chain rule through the ReLU layers and accumulated in */
 /* double precision over samples in ascending order.                           */
-/* Mode LSO_BF16 rounds to bfloat16 exactly the quantities the kernel holds in */
-/* bfloat16 (inputs, weights and activations of every layer, and every layer's */
-/* output gradient before it multiplies anything); sums stay in double.        */
+/* LSO_F64 evaluates everything in double precision.  LSO_F32 and LSO_BF16    */
+/* run the forward pass in the kernel's precision -- the same fp32 fma chains  */
+/* as the scoring path -- so the ReLU masks, which floating point decides, are */
+/* taken in that precision; the backward sums stay in double.  LSO_BF16 also   */
+/* rounds to bfloat16 exactly the quantities the kernel holds in bfloat16      */
+/* (inputs, weights and activations of every layer, and every layer's output   */
+/* gradient before it multiplies anything); a gradient that is rounded is      */
+/* itself summed in the kernel's precision, an fp32 chain in ascending order.  */
 /* grad_out (nullable, double, same packing as params), loss_out (nullable).   */
 /* ------------------------------------------------------------------------- */
 int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
@@ -381,6 +411,7 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
     if (net_init(&net, d, n_hidden, hidden, params)) return -1;
     if (B < 1) return -1;
     int bf = (mode == LSO_BF16);
+    int lowp = (mode == LSO_F32 || mode == LSO_BF16);
     int L = net.n_layers;
     int64_t P = lso_param_count(d, n_hidden, hidden);
     double* grad = (double*)calloc((size_t)P, sizeof(double));
@@ -403,10 +434,10 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
         const float* xb = feats + (int64_t)b * d;
         double* a0 = act;
         for (int k = 0; k < d; ++k) {
-            if (bf) {
+            if (lowp) {
                 float t = xb[k] - mu[k];
                 t = t * inv_sigma[k];
-                a0[k] = (double)lso_bf16_round(t);
+                a0[k] = bf ? (double)lso_bf16_round(t) : (double)t;
             } else {
                 a0[k] = ((double)xb[k] - (double)mu[k]) * (double)inv_sigma[k];
             }
@@ -418,9 +449,15 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
             double* z = pre + (int64_t)l * W;
             double* an = act + (int64_t)(l + 1) * W;
             for (int j = 0; j < O; ++j) {
-                double acc = (double)params[net.b_off[l] + j];
-                for (int k = 0; k < K; ++k) acc += Wq[net.W_off[l] + (int64_t)j * K + k] * a[k];
-                if (bf) acc = (double)(float)acc;
+                double acc;
+                if (lowp) {
+                    float f = params[net.b_off[l] + j];
+                    for (int k = 0; k < K; ++k) f = fmaf((float)Wq[net.W_off[l] + (int64_t)j * K + k], (float)a[k], f);
+                    acc = (double)f;
+                } else {
+                    acc = (double)params[net.b_off[l] + j];
+                    for (int k = 0; k < K; ++k) acc += Wq[net.W_off[l] + (int64_t)j * K + k] * a[k];
+                }
                 z[j] = acc;
                 if (l + 1 < L) {
                     double h = acc > 0.0 ? acc : 0.0;
@@ -447,8 +484,15 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
             const double* zp = pre + (int64_t)(l - 1) * W;
             for (int k = 0; k < K; ++k) {
                 double s = 0.0;
-                for (int j = 0; j < O; ++j) s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];
-                if (bf) s = (double)(float)s;
+                if (bf) {
+                    /* rounded to bf16 below, so summed in the kernel's precision:
+                       an fp32 fma chain over the output units in ascending order */
+                    float f = 0.0f;
+                    for (int j = 0; j < O; ++j) f = fmaf((float)Wq[net.W_off[l] + (int64_t)j * K + k], (float)delta[j], f);
+                    s = (double)f;
+                } else {
+                    for (int j = 0; j < O; ++j) s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];
+                }
                 double dk = zp[k] > 0.0 ? s : 0.0;
                 dnext[k] = bf ? (double)lso_bf16_round((float)dk) : dk;
             }

@@ -1,0 +1,295 @@
+// K2/K3: pair features, shared reward model, per-request argmin.
+//
+// The reward model (Section 4.1, Request-instance reward model / Model
+// architecture) is one MLP shared by every instance; it scores the row
+// [instance state | request | pair] of each candidate and the request goes to
+// the best prediction (Alg. 4: normalise, one batched forward, argmax reward;
+// with the model predicting TTFT, argmin).
+//
+// Arithmetic order.  Every dot product is an fma chain that starts from the
+// bias and walks the inputs in ascending order, with no other contraction, so
+// a score is a deterministic function of its pair and identical pairs score
+// identically.  Because the instance columns come first in the row, the first
+// part of every layer-1 chain depends on the instance only: it is computed once
+// per (instance, unit) and resumed per pair with the five request/pair columns.
+// This leaves the chain, and so every rounding, unchanged.
+//
+// bf16 models (LS_BF16): weights and each layer's input activations are bf16
+// values, products are exact in fp32, sums and biases stay fp32.
+#include <climits>
+
+#include "ls_internal.h"
+
+namespace ls {
+
+// Round to the nearest bf16 value, ties to even (bits of a binary32).
+__device__ __forceinline__ float bf16_rne(float x) {
+    if (x != x) return x;
+    uint32_t u = __float_as_uint(x);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xFFFF0000u);
+}
+
+// Same, for values known not to be NaN (ReLU outputs).
+__device__ __forceinline__ float bf16_rne_num(float x) {
+    uint32_t u = __float_as_uint(x);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ float relu(float z) { return z > 0.0f ? z : 0.0f; }
+
+// ---------------------------------------------------------------------------
+// compute copy of the model
+// ---------------------------------------------------------------------------
+struct CopyArgs {
+    int d, h1, h2;
+    int64_t m_w1, m_b1, m_w2, m_b2, m_w3, m_b3;
+    int64_t c_w1, c_b1, c_w2t, c_b2, c_w3, c_b3, c_w1t, n_compute;
+    bool bf16;
+};
+
+__global__ void refresh_compute_kernel(CopyArgs a, const float* __restrict__ master, float* __restrict__ comp) {
+    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= a.n_compute) return;
+    float v;
+    bool weight = true;
+    if (t < a.c_b1) {                                   // W1 [h1 x d]
+        v = master[a.m_w1 + (t - a.c_w1)];
+    } else if (t < a.c_w2t) {                           // b1
+        v = master[a.m_b1 + (t - a.c_b1)];
+        weight = false;
+    } else if (t < a.c_b2) {                            // W2T[k][j] = W2[j][k]
+        int64_t e = t - a.c_w2t;
+        int64_t k = e / a.h2, j = e - k * a.h2;
+        v = master[a.m_w2 + j * a.h1 + k];
+    } else if (t < a.c_w3) {                            // b2
+        v = master[a.m_b2 + (t - a.c_b2)];
+        weight = false;
+    } else if (t < a.c_b3) {                            // W3 [h2]
+        v = master[a.m_w3 + (t - a.c_w3)];
+    } else if (t < a.c_w1t) {                           // b3
+        v = master[a.m_b3];
+        weight = false;
+    } else {                                            // W1T[c][k] = W1[k][c]
+        int64_t e = t - a.c_w1t;
+        int64_t c = e / a.h1, k = e - c * a.h1;
+        v = master[a.m_w1 + k * a.d + c];
+    }
+    comp[t] = (weight && a.bf16) ? bf16_rne(v) : v;
+}
+
+hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s) {
+    CopyArgs a{m.d, m.h1, m.h2, m.m_w1, m.m_b1, m.m_w2, m.m_b2, m.m_w3, m.m_b3,
+               m.c_w1, m.c_b1, m.c_w2t, m.c_b2, m.c_w3, m.c_b3, m.c_w1t, m.n_compute, m.bf16};
+    int64_t grid = (m.n_compute + 255) / 256;
+    hipLaunchKernelGGL(refresh_compute_kernel, dim3((uint32_t)grid), dim3(256), 0, s, a, master, compute);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// layer-1 instance partials: part_t[k][i] = chain over the instance columns
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ void instance_partial_kernel(const float* __restrict__ w1, const float* __restrict__ b1,
+                                        const float* __restrict__ mu, const float* __restrict__ isig,
+                                        const float* __restrict__ inst_feat, int d, int d_inst, int h1, int32_t N,
+                                        float* __restrict__ part_t) {
+    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)h1 * N) return;
+    int64_t k = t / N, i = t - k * N;
+    float acc = b1[k];
+    const float* __restrict__ row = inst_feat + i * d_inst;
+    const float* __restrict__ w = w1 + k * d;
+    for (int c = 0; c < d_inst; ++c) {
+        float x = __fmul_rn(__fsub_rn(row[c], mu[c]), isig[c]);
+        if (BF) x = bf16_rne(x);
+        acc = __builtin_fmaf(w[c], x, acc);
+    }
+    part_t[t] = acc;
+}
+
+hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,
+                                   const float* inv_sigma, const float* inst_feat, int32_t N, float* part_t,
+                                   hipStream_t s) {
+    int64_t n = (int64_t)m.h1 * N;
+    int64_t grid = (n + 255) / 256;
+    if (m.bf16)
+        hipLaunchKernelGGL(instance_partial_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, compute + m.c_w1,
+                           compute + m.c_b1, mu, inv_sigma, inst_feat, m.d, m.d_inst, m.h1, N, part_t);
+    else
+        hipLaunchKernelGGL(instance_partial_kernel<false>, dim3((uint32_t)grid), dim3(256), 0, s, compute + m.c_w1,
+                           compute + m.c_b1, mu, inv_sigma, inst_feat, m.d, m.d_inst, m.h1, N, part_t);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// pair scoring: one lane per pair, weights uniform across the wave
+// ---------------------------------------------------------------------------
+struct PairModel {
+    const float* __restrict__ w1;    // [h1 x d]
+    const float* __restrict__ w2t;   // [h1 x h2]
+    const float* __restrict__ b2;    // [h2]
+    const float* __restrict__ w3;    // [h2]
+    const float* __restrict__ b3;    // [1]
+    int d, d_inst, h1, h2;
+};
+
+// U consecutive layer-2 units starting at jb, then their head terms in order.
+template <bool BF, int U>
+__device__ __forceinline__ float unit_block(const PairModel& M, const float* __restrict__ part_i, int32_t N,
+                                            const float xt[5], int jb, float t) {
+    float acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc[u] = M.b2[jb + u];
+    for (int k = 0; k < M.h1; ++k) {
+        float z = part_i[(int64_t)k * N];
+        const float* __restrict__ w1 = M.w1 + (int64_t)k * M.d + M.d_inst;
+#pragma unroll
+        for (int c = 0; c < 5; ++c) z = __builtin_fmaf(w1[c], xt[c], z);
+        float a = relu(z);
+        if (BF) a = bf16_rne_num(a);
+        const float* __restrict__ w2 = M.w2t + (int64_t)k * M.h2 + jb;
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u] = __builtin_fmaf(w2[u], a, acc[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float hh = relu(acc[u]);
+        if (BF) hh = bf16_rne_num(hh);
+        t = __builtin_fmaf(M.w3[jb + u], hh, t);
+    }
+    return t;
+}
+
+template <bool BF>
+__global__ __launch_bounds__(256) void score_pairs_kernel(PairModel M, const float* __restrict__ mu,
+                                                          const float* __restrict__ isig,
+                                                          const float* __restrict__ part_t, int32_t R, int32_t N,
+                                                          const int64_t* __restrict__ req_off,
+                                                          const int32_t* __restrict__ prompt_len,
+                                                          const int32_t* __restrict__ overlap, int block_tokens,
+                                                          float* __restrict__ scores) {
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t total = (int64_t)R * N;
+    const bool valid = p < total;
+    const int64_t pp = valid ? p : 0;
+    const int64_t r = pp / N, i = pp - r * N;
+    const int32_t L = prompt_len[r];
+    const int64_t n = req_off[r + 1] - req_off[r];
+    const int32_t l = overlap[pp];
+    const int64_t hit = (int64_t)block_tokens * l;
+    float x[5];
+    x[0] = (float)L;
+    x[1] = (float)n;
+    x[2] = (float)l;
+    x[3] = (L == 0) ? 0.0f : (float)hit / (float)L;
+    x[4] = (float)((int64_t)L - hit);
+    float xt[5];
+#pragma unroll
+    for (int c = 0; c < 5; ++c) {
+        float v = __fmul_rn(__fsub_rn(x[c], mu[M.d_inst + c]), isig[M.d_inst + c]);
+        xt[c] = BF ? bf16_rne(v) : v;
+    }
+    const float* __restrict__ part_i = part_t + i;
+    float t = M.b3[0];
+    int jb = 0;
+    for (; jb + 32 <= M.h2; jb += 32) t = unit_block<BF, 32>(M, part_i, N, xt, jb, t);
+    if (jb + 16 <= M.h2) { t = unit_block<BF, 16>(M, part_i, N, xt, jb, t); jb += 16; }
+    if (jb + 8 <= M.h2) { t = unit_block<BF, 8>(M, part_i, N, xt, jb, t); jb += 8; }
+    if (jb + 4 <= M.h2) { t = unit_block<BF, 4>(M, part_i, N, xt, jb, t); jb += 4; }
+    if (jb + 2 <= M.h2) { t = unit_block<BF, 2>(M, part_i, N, xt, jb, t); jb += 2; }
+    if (jb + 1 <= M.h2) { t = unit_block<BF, 1>(M, part_i, N, xt, jb, t); jb += 1; }
+    if (valid) scores[p] = t;
+}
+
+hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
+                              const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
+                              const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s) {
+    int64_t total = (int64_t)R * N;
+    if (total <= 0) return hipSuccess;
+    PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
+                m.d, m.d_inst, m.h1, m.h2};
+    int64_t grid = (total + 255) / 256;
+    if (m.bf16)
+        hipLaunchKernelGGL(score_pairs_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t,
+                           R, N, req_off, prompt_len, overlap, m.block_tokens, scores);
+    else
+        hipLaunchKernelGGL(score_pairs_kernel<false>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t,
+                           R, N, req_off, prompt_len, overlap, m.block_tokens, scores);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// K3: per-request argmin, one wave per request
+// ---------------------------------------------------------------------------
+// Lexicographic order on (score, id): -0 equals +0, NaN after +inf, ties to the
+// lower id; id INT_MAX marks "no candidate yet".
+__device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
+    if (ia == INT_MAX) return false;
+    if (ib == INT_MAX) return true;
+    const bool an = a != a, bn = b != b;
+    if (an) return bn && ia < ib;
+    if (bn) return true;
+    if (a < b) return true;
+    if (a > b) return false;
+    return ia < ib;
+}
+
+__global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d, int d_inst, int block_tokens,
+                                                     const float* __restrict__ scores,
+                                                     const int64_t* __restrict__ req_off,
+                                                     const int32_t* __restrict__ prompt_len,
+                                                     const int32_t* __restrict__ overlap,
+                                                     const float* __restrict__ inst_feat,
+                                                     int32_t* __restrict__ chosen, float* __restrict__ min_ttft,
+                                                     float* __restrict__ feat_out) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    if (r >= R) return;
+    const float* __restrict__ s = scores + r * N;
+    float bs = 0.0f;
+    int bi = INT_MAX;
+    for (int i = lane; i < N; i += 64) {
+        float v = s[i];
+        if (better(v, i, bs, bi)) { bs = v; bi = i; }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        float os = __shfl_xor(bs, off);
+        int oi = __shfl_xor(bi, off);
+        if (better(os, oi, bs, bi)) { bs = os; bi = oi; }
+    }
+    if (lane == 0) {
+        chosen[r] = bi;
+        if (min_ttft) min_ttft[r] = bs;
+    }
+    if (feat_out) {
+        const int32_t L = prompt_len[r];
+        const int64_t n = req_off[r + 1] - req_off[r];
+        const int32_t l = overlap[r * N + bi];
+        const int64_t hit = (int64_t)block_tokens * l;
+        for (int c = lane; c < d; c += 64) {
+            float v;
+            if (c < d_inst) v = inst_feat[(int64_t)bi * d_inst + c];
+            else if (c == d_inst) v = (float)L;
+            else if (c == d_inst + 1) v = (float)n;
+            else if (c == d_inst + 2) v = (float)l;
+            else if (c == d_inst + 3) v = (L == 0) ? 0.0f : (float)hit / (float)L;
+            else v = (float)((int64_t)L - hit);
+            feat_out[r * d + c] = v;
+        }
+    }
+}
+
+hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const int64_t* req_off,
+                         const int32_t* prompt_len, const int32_t* overlap, const float* inst_feat,
+                         int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    int64_t grid = ((int64_t)R + 3) / 4;
+    hipLaunchKernelGGL(argmin_kernel, dim3((uint32_t)grid), dim3(256), 0, s, R, N, m.d, m.d_inst, m.block_tokens,
+                       scores, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft, feat_out);
+    return hipGetLastError();
+}
+
+}  // namespace ls

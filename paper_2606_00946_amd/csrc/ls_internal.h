@@ -1,0 +1,91 @@
+// Internal declarations shared by the HIP sources of liblodestar.
+// Nothing here is part of the C ABI (include/lodestar.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "lodestar.h"
+
+namespace ls {
+
+// ---------------------------------------------------------------------------
+// Prefix-cache hash tables.  One open-addressing table per instance; a bucket
+// is 8 uint64 keys (64 bytes, one HBM burst).  Empty slots hold kEmptyKey; the
+// key kEmptyKey itself is recorded in a per-instance flag instead.
+// ---------------------------------------------------------------------------
+constexpr int kBucketKeys = 8;
+constexpr uint64_t kEmptyKey = ~0ull;
+constexpr uint32_t kFlagHasEmptyKey = 1u;
+
+struct CacheTables {
+    uint64_t* keys = nullptr;        // [total_buckets * kBucketKeys]
+    int64_t* base = nullptr;         // [N] first bucket of instance i
+    uint32_t* nbuckets = nullptr;    // [N]
+    uint32_t* flags = nullptr;       // [N]
+    int32_t n = 0;
+};
+
+// Bucket of `key` in a table of nb buckets: Fibonacci hashing of the whole key,
+// high 32 bits mapped onto [0, nb) by a multiply-shift.
+__host__ __device__ inline uint32_t bucket_of(uint64_t key, uint32_t nb) {
+    uint64_t h = key * 0x9E3779B97F4A7C15ull;
+    return (uint32_t)(((h >> 32) * (uint64_t)nb) >> 32);
+}
+
+// ---------------------------------------------------------------------------
+// Model layout on the device.  Masters are fp32 in the ABI packing.  The
+// "compute copy" is what the kernels read: weights rounded to bf16 in LS_BF16
+// mode (kept as fp32 values), with layer 2 transposed so that a fixed input k
+// addresses consecutive output units.
+// ---------------------------------------------------------------------------
+struct ModelDims {
+    int d = 0, d_inst = 0, h1 = 0, h2 = 0;
+    bool bf16 = false;
+    int block_tokens = 16;
+    // master offsets (floats)
+    int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0, m_b3 = 0, n_params = 0;
+    // compute-copy offsets (floats)
+    int64_t c_w1 = 0;   // [h1 x d]  row-major (W1[k][c])
+    int64_t c_b1 = 0;   // [h1]
+    int64_t c_w2t = 0;  // [h1 x h2] W2T[k][j] = W2[j][k]
+    int64_t c_b2 = 0;   // [h2]
+    int64_t c_w3 = 0;   // [h2]
+    int64_t c_b3 = 0;   // [1]
+    int64_t c_w1t = 0;  // [d x h1]  W1T[c][k] = W1[k][c]  (update forward)
+    int64_t n_compute = 0;
+};
+
+ModelDims make_dims(const ls_model_config& cfg);
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (each returns hipGetLastError() of its launch).
+// ---------------------------------------------------------------------------
+hipError_t launch_fill_u64(uint64_t* p, uint64_t value, int64_t count, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t s);
+hipError_t launch_table_insert(const CacheTables& t, const int64_t* inst_off, const uint64_t* hashes,
+                               int64_t total, int32_t n_inst, hipStream_t s);
+
+hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const int64_t* req_off,
+                               const uint64_t* req_hashes, int32_t* overlap, hipStream_t s);
+
+hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s);
+hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,
+                                   const float* inv_sigma, const float* inst_feat, int32_t N, float* part_t,
+                                   hipStream_t s);
+hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
+                              const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
+                              const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s);
+hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const int64_t* req_off,
+                         const int32_t* prompt_len, const int32_t* overlap, const float* inst_feat,
+                         int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s);
+
+// Online update.  Workspace layout is chosen by update_workspace_floats().
+int64_t update_workspace_bytes(const ModelDims& m, int32_t B);
+hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,
+                         const float* inv_sigma, int32_t B, const float* feats, const float* ttft, float lr,
+                         float* loss_out, float* grad_out, void* workspace, hipStream_t s);
+
+}  // namespace ls

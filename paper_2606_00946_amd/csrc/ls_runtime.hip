@@ -1,0 +1,531 @@
+// Host side of liblodestar: the C ABI declared in include/lodestar.h.
+//
+// Every entry point validates its arguments on the host before enqueuing
+// anything, keeps the caller's device current only for its own duration, and
+// reports failures through a status code plus a per-context message.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ls_internal.h"
+
+struct ls_ctx {
+    ls_model_config cfg{};
+    ls::ModelDims dims;
+    int device = 0;
+    std::string err;
+    // model (fp32 masters in the ABI packing, the kernels' compute copy, z-score stats)
+    float* master = nullptr;
+    float* compute = nullptr;
+    float* mu = nullptr;
+    float* isig = nullptr;
+    bool have_model = false;
+    // cache state
+    ls::CacheTables tables;
+    int64_t table_cap_buckets = 0;
+    int32_t inst_cap = 0;
+    int64_t* inst_off_dev = nullptr;
+    bool have_cache = false;
+    // grow-only workspace
+    void* ws = nullptr;
+    size_t ws_cap = 0;
+    // pinned staging for host -> device copies, reusable once `stage_done` has fired
+    void* stage = nullptr;
+    size_t stage_cap = 0;
+    hipEvent_t stage_done = nullptr;
+    bool stage_pending = false;
+    // optional per-kernel timing
+    bool profiling = false;
+    struct Rec { int kind; hipEvent_t start, stop; };
+    std::vector<Rec> recs;
+    std::vector<hipEvent_t> spare;
+};
+
+namespace {
+
+int fail(ls_ctx* c, int code, const char* fmt, ...) {
+    if (c) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        c->err = buf;
+    }
+    return code;
+}
+
+#define LS_HIP(ctx, expr)                                                                          \
+    do {                                                                                           \
+        hipError_t e_ = (expr);                                                                    \
+        if (e_ != hipSuccess)                                                                      \
+            return fail((ctx), LS_ERR_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));       \
+    } while (0)
+
+// Makes ctx->device current for the scope and restores the caller's device.
+struct DeviceScope {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceScope(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceScope() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+bool valid_config(const ls_model_config* cfg, std::string* why) {
+    if (!cfg) { *why = "config is NULL"; return false; }
+    if (cfg->d <= LS_DERIVED_COLS || cfg->d > 4096) { *why = "d must be in (5, 4096]"; return false; }
+    if (cfg->n_hidden < 1 || cfg->n_hidden > LS_MAX_HIDDEN) { *why = "n_hidden must be 1..3"; return false; }
+    for (int l = 0; l < cfg->n_hidden; ++l)
+        if (cfg->hidden[l] < 1 || cfg->hidden[l] > 512) { *why = "hidden widths must be 1..512"; return false; }
+    if (cfg->block_tokens < 1) { *why = "block_tokens must be >= 1"; return false; }
+    if (cfg->dtype != LS_FP32 && cfg->dtype != LS_BF16) { *why = "dtype must be LS_FP32 or LS_BF16"; return false; }
+    return true;
+}
+
+// Wait for the last staged copy before the host buffer is rewritten; grow it if needed.
+int stage_reserve(ls_ctx* c, size_t bytes) {
+    if (c->stage_pending) {
+        LS_HIP(c, hipEventSynchronize(c->stage_done));
+        c->stage_pending = false;
+    }
+    if (bytes > c->stage_cap) {
+        if (c->stage) LS_HIP(c, hipHostFree(c->stage));
+        c->stage = nullptr;
+        c->stage_cap = 0;
+        size_t cap = (size_t)round_up((int64_t)bytes, 1 << 16);
+        if (hipHostMalloc(&c->stage, cap, hipHostMallocDefault) != hipSuccess) {
+            c->stage = nullptr;
+            return fail(c, LS_ERR_NOMEM, "pinned staging allocation of %zu bytes failed", cap);
+        }
+        c->stage_cap = cap;
+    }
+    return LS_OK;
+}
+
+int stage_copy(ls_ctx* c, void* dst, size_t bytes, hipStream_t s) {
+    LS_HIP(c, hipMemcpyAsync(dst, c->stage, bytes, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    return LS_OK;
+}
+
+// Grow-only device buffer; waits for outstanding device work before freeing.
+int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
+    if (bytes <= *cap) return LS_OK;
+    if (*p) {
+        LS_HIP(c, hipDeviceSynchronize());
+        LS_HIP(c, hipFree(*p));
+        *p = nullptr;
+        *cap = 0;
+    }
+    size_t want = (size_t)round_up((int64_t)bytes, 1 << 20);
+    if (hipMalloc(p, want) != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return fail(c, LS_ERR_NOMEM, "device allocation of %zu bytes failed", want);
+    }
+    *cap = want;
+    return LS_OK;
+}
+
+enum Kind { K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_COUNT };
+const char* const kKindNames[K_COUNT] = {"table_build", "prefix_match", "instance_partial", "score_pairs", "argmin",
+                                         "update"};
+
+hipEvent_t take_event(ls_ctx* c) {
+    if (!c->spare.empty()) {
+        hipEvent_t e = c->spare.back();
+        c->spare.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets one launch group with events when profiling is on.
+struct Timed {
+    ls_ctx* c;
+    int kind;
+    hipStream_t s;
+    hipEvent_t start = nullptr;
+    Timed(ls_ctx* c_, int kind_, hipStream_t s_) : c(c_), kind(kind_), s(s_) {
+        if (c->profiling && (start = take_event(c)) != nullptr) (void)hipEventRecord(start, s);
+    }
+    void done() {
+        if (!start) return;
+        hipEvent_t stop = take_event(c);
+        if (stop && hipEventRecord(stop, s) == hipSuccess) {
+            c->recs.push_back({kind, start, stop});
+        } else {
+            c->spare.push_back(start);
+            if (stop) c->spare.push_back(stop);
+        }
+        start = nullptr;
+    }
+};
+
+#define LS_TIMED(ctx, kind, s, expr)        \
+    do {                                     \
+        Timed t_((ctx), (kind), (s));        \
+        hipError_t e2_ = (expr);             \
+        t_.done();                           \
+        LS_HIP((ctx), e2_);                  \
+    } while (0)
+
+struct WsCarve {
+    char* base;
+    size_t off = 0;
+    template <class T>
+    T* take(int64_t count) {
+        T* p = reinterpret_cast<T*>(base + off);
+        off += (size_t)round_up(count * (int64_t)sizeof(T), 256);
+        return p;
+    }
+};
+
+}  // namespace
+
+namespace ls {
+
+ModelDims make_dims(const ls_model_config& cfg) {
+    ModelDims m;
+    m.d = cfg.d;
+    m.d_inst = cfg.d - LS_DERIVED_COLS;
+    m.h1 = cfg.hidden[0];
+    m.h2 = cfg.n_hidden >= 2 ? cfg.hidden[1] : 0;
+    m.bf16 = cfg.dtype == LS_BF16;
+    m.block_tokens = cfg.block_tokens;
+    int64_t o = 0;
+    m.m_w1 = o; o += (int64_t)m.h1 * m.d;
+    m.m_b1 = o; o += m.h1;
+    m.m_w2 = o; o += (int64_t)m.h2 * m.h1;
+    m.m_b2 = o; o += m.h2;
+    m.m_w3 = o; o += m.h2;
+    m.m_b3 = o; o += 1;
+    m.n_params = o;
+    o = 0;
+    m.c_w1 = o; o += (int64_t)m.h1 * m.d;
+    m.c_b1 = o; o += m.h1;
+    m.c_w2t = o; o += (int64_t)m.h1 * m.h2;
+    m.c_b2 = o; o += m.h2;
+    m.c_w3 = o; o += m.h2;
+    m.c_b3 = o; o += 1;
+    m.c_w1t = o; o += (int64_t)m.d * m.h1;
+    m.n_compute = o;
+    return m;
+}
+
+}  // namespace ls
+
+extern "C" {
+
+int64_t ls_param_count(const ls_model_config* cfg) {
+    std::string why;
+    if (!valid_config(cfg, &why)) return -1;
+    int64_t n = 0;
+    int prev = cfg->d;
+    for (int l = 0; l <= cfg->n_hidden; ++l) {
+        int out = l < cfg->n_hidden ? cfg->hidden[l] : 1;
+        n += (int64_t)out * prev + out;
+        prev = out;
+    }
+    return n;
+}
+
+const char* ls_last_error(const ls_ctx* ctx) {
+    if (!ctx) return "context is NULL";
+    return ctx->err.c_str();
+}
+
+int ls_create(const ls_model_config* cfg, int device, ls_ctx** out) {
+    if (!out) return LS_ERR_INVALID;
+    *out = nullptr;
+    std::string why;
+    if (!valid_config(cfg, &why)) return LS_ERR_INVALID;
+    if (cfg->n_hidden != 2) return LS_ERR_UNSUPPORTED;       // this build fuses exactly two hidden layers
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
+        (void)hipGetLastError();
+        return LS_ERR_DEVICE;
+    }
+    if (device < 0 || device >= ndev) return LS_ERR_INVALID;
+    ls_ctx* c = new (std::nothrow) ls_ctx();
+    if (!c) return LS_ERR_NOMEM;
+    c->cfg = *cfg;
+    c->device = device;
+    c->dims = ls::make_dims(*cfg);
+    DeviceScope dev(device);
+    bool ok = dev.ok;
+    ok = ok && hipMalloc((void**)&c->master, sizeof(float) * c->dims.n_params) == hipSuccess;
+    ok = ok && hipMalloc((void**)&c->compute, sizeof(float) * c->dims.n_compute) == hipSuccess;
+    ok = ok && hipMalloc((void**)&c->mu, sizeof(float) * cfg->d) == hipSuccess;
+    ok = ok && hipMalloc((void**)&c->isig, sizeof(float) * cfg->d) == hipSuccess;
+    ok = ok && hipEventCreateWithFlags(&c->stage_done, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+        (void)hipGetLastError();
+        ls_destroy(c);
+        return LS_ERR_NOMEM;
+    }
+    *out = c;
+    return LS_OK;
+}
+
+void ls_destroy(ls_ctx* c) {
+    if (!c) return;
+    {
+        DeviceScope dev(c->device);
+        (void)hipDeviceSynchronize();
+        for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->tables.keys,
+                        (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
+                        (void*)c->inst_off_dev, c->ws})
+            if (p) (void)hipFree(p);
+        if (c->stage) (void)hipHostFree(c->stage);
+        if (c->stage_done) (void)hipEventDestroy(c->stage_done);
+        for (auto& r : c->recs) {
+            (void)hipEventDestroy(r.start);
+            (void)hipEventDestroy(r.stop);
+        }
+        for (hipEvent_t e : c->spare) (void)hipEventDestroy(e);
+        (void)hipGetLastError();
+    }
+    delete c;
+}
+
+int ls_set_model(ls_ctx* c, const float* params, int64_t n_params, const float* mu, const float* inv_sigma,
+                 void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!params || !mu || !inv_sigma) return fail(c, LS_ERR_INVALID, "params, mu and inv_sigma must be non-NULL");
+    if (n_params != c->dims.n_params)
+        return fail(c, LS_ERR_INVALID, "n_params is %lld, the model needs %lld", (long long)n_params,
+                    (long long)c->dims.n_params);
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t pb = sizeof(float) * (size_t)n_params, db = sizeof(float) * (size_t)c->cfg.d;
+    int rc = stage_reserve(c, pb + 2 * db);
+    if (rc) return rc;
+    char* st = (char*)c->stage;
+    memcpy(st, params, pb);
+    memcpy(st + pb, mu, db);
+    memcpy(st + pb + db, inv_sigma, db);
+    LS_HIP(c, hipMemcpyAsync(c->master, st, pb, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->mu, st + pb, db, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->isig, st + pb + db, db, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    LS_HIP(c, ls::launch_refresh_compute_copy(c->dims, c->master, c->compute, s));
+    c->have_model = true;
+    return LS_OK;
+}
+
+int ls_get_model(ls_ctx* c, float* params, int64_t n_params, float* mu, float* inv_sigma) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    if (params && n_params != c->dims.n_params)
+        return fail(c, LS_ERR_INVALID, "n_params is %lld, the model has %lld", (long long)n_params,
+                    (long long)c->dims.n_params);
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    LS_HIP(c, hipDeviceSynchronize());
+    if (params) LS_HIP(c, hipMemcpy(params, c->master, sizeof(float) * (size_t)n_params, hipMemcpyDeviceToHost));
+    if (mu) LS_HIP(c, hipMemcpy(mu, c->mu, sizeof(float) * (size_t)c->cfg.d, hipMemcpyDeviceToHost));
+    if (inv_sigma) LS_HIP(c, hipMemcpy(inv_sigma, c->isig, sizeof(float) * (size_t)c->cfg.d, hipMemcpyDeviceToHost));
+    return LS_OK;
+}
+
+int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off, const uint64_t* hashes,
+                        void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (n_instances < 1) return fail(c, LS_ERR_INVALID, "n_instances must be >= 1");
+    if (!inst_off) return fail(c, LS_ERR_INVALID, "inst_off is NULL");
+    if (inst_off[0] != 0) return fail(c, LS_ERR_INVALID, "inst_off[0] must be 0");
+    for (int32_t i = 0; i < n_instances; ++i)
+        if (inst_off[i + 1] < inst_off[i]) return fail(c, LS_ERR_INVALID, "inst_off decreases at %d", i);
+    const int64_t total = inst_off[n_instances];
+    if (total > 0 && !hashes) return fail(c, LS_ERR_INVALID, "hashes is NULL");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+
+    // bucket layout: about four keys per 8-slot bucket (half load)
+    const int N = n_instances;
+    std::vector<int64_t> base(N);
+    std::vector<uint32_t> nb(N);
+    int64_t nbk = 0;
+    for (int i = 0; i < N; ++i) {
+        int64_t cnt = inst_off[i + 1] - inst_off[i];
+        int64_t b = (cnt + 3) / 4;
+        if (b < 1) b = 1;
+        if (b > 0x7fffffff) return fail(c, LS_ERR_UNSUPPORTED, "instance %d caches too many blocks", i);
+        base[i] = nbk;
+        nb[i] = (uint32_t)b;
+        nbk += b;
+    }
+    // device buffers
+    size_t cap = (size_t)c->table_cap_buckets * ls::kBucketKeys * sizeof(uint64_t);
+    int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t));
+    if (rc) return rc;
+    c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
+    if (N > c->inst_cap) {
+        LS_HIP(c, hipDeviceSynchronize());
+        for (void* p : {(void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags, (void*)c->inst_off_dev})
+            if (p) LS_HIP(c, hipFree(p));
+        c->tables.base = nullptr; c->tables.nbuckets = nullptr; c->tables.flags = nullptr; c->inst_off_dev = nullptr;
+        c->inst_cap = 0;
+        bool ok = hipMalloc((void**)&c->tables.base, sizeof(int64_t) * N) == hipSuccess &&
+                  hipMalloc((void**)&c->tables.nbuckets, sizeof(uint32_t) * N) == hipSuccess &&
+                  hipMalloc((void**)&c->tables.flags, sizeof(uint32_t) * N) == hipSuccess &&
+                  hipMalloc((void**)&c->inst_off_dev, sizeof(int64_t) * (N + 1)) == hipSuccess;
+        if (!ok) {
+            (void)hipGetLastError();
+            return fail(c, LS_ERR_NOMEM, "instance metadata allocation failed");
+        }
+        c->inst_cap = N;
+    }
+    // metadata through pinned staging
+    const size_t b_base = sizeof(int64_t) * N, b_nb = sizeof(uint32_t) * N, b_off = sizeof(int64_t) * (N + 1);
+    rc = stage_reserve(c, b_base + b_nb + b_off + 64);
+    if (rc) return rc;
+    char* st = (char*)c->stage;
+    memcpy(st, base.data(), b_base);
+    memcpy(st + b_base, nb.data(), b_nb);
+    memcpy(st + b_base + b_nb, inst_off, b_off);
+    LS_HIP(c, hipMemcpyAsync(c->tables.base, st, b_base, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->tables.nbuckets, st + b_base, b_nb, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->inst_off_dev, st + b_base + b_nb, b_off, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    c->tables.n = N;
+    // build
+    {
+        Timed t(c, K_TABLE, s);
+        hipError_t e = ls::launch_fill_u64(c->tables.keys, ls::kEmptyKey, nbk * ls::kBucketKeys, s);
+        if (e == hipSuccess) e = ls::launch_fill_u32(c->tables.flags, 0u, N, s);
+        if (e == hipSuccess) e = ls::launch_table_insert(c->tables, c->inst_off_dev, hashes, total, N, s);
+        t.done();
+        LS_HIP(c, e);
+    }
+    c->have_cache = true;
+    return LS_OK;
+}
+
+int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                   const int32_t* prompt_len, const float* inst_feat, int32_t* chosen, float* min_ttft,
+                   float* scores, int32_t* overlap, float* feat_out, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (R < 0) return fail(c, LS_ERR_INVALID, "R must be >= 0");
+    if (N < 1) return fail(c, LS_ERR_INVALID, "N must be >= 1");
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    if (!c->have_cache) return fail(c, LS_ERR_STATE, "no cache state has been loaded");
+    if (N != c->tables.n)
+        return fail(c, LS_ERR_STATE, "N is %d but the cache state has %d instances", N, c->tables.n);
+    if (R == 0) return LS_OK;
+    if (!req_off || !req_hashes || !prompt_len || !inst_feat || !chosen)
+        return fail(c, LS_ERR_INVALID, "req_off, req_hashes, prompt_len, inst_feat and chosen must be non-NULL");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const ls::ModelDims& m = c->dims;
+    const int64_t pairs = (int64_t)R * N;
+
+    size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
+    if (!overlap) need += (size_t)round_up(pairs * 4, 256);
+    if (!scores) need += (size_t)round_up(pairs * 4, 256);
+    int rc = grow(c, &c->ws, &c->ws_cap, need);
+    if (rc) return rc;
+    WsCarve w{(char*)c->ws};
+    float* part_t = w.take<float>((int64_t)m.h1 * N);
+    int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
+    float* sc = scores ? scores : w.take<float>(pairs);
+
+    LS_TIMED(c, K_PREFIX, s, ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, s));
+    LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
+    LS_TIMED(c, K_SCORE, s,
+             ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));
+    LS_TIMED(c, K_ARGMIN, s,
+             ls::launch_argmin(m, R, N, sc, req_off, prompt_len, ov, inst_feat, chosen, min_ttft, feat_out, s));
+    return LS_OK;
+}
+
+int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
+              float* grad_out, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (B < 1) return fail(c, LS_ERR_INVALID, "B must be >= 1");
+    if (!feats || !ttft) return fail(c, LS_ERR_INVALID, "feats and ttft must be non-NULL");
+    if (!std::isfinite(lr)) return fail(c, LS_ERR_INVALID, "lr must be finite");
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    int64_t need = ls::update_workspace_bytes(c->dims, B);
+    int rc = grow(c, &c->ws, &c->ws_cap, (size_t)need);
+    if (rc) return rc;
+    LS_TIMED(c, K_UPDATE, s,
+             ls::launch_update(c->dims, c->master, c->compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
+                               c->ws, s));
+    return LS_OK;
+}
+
+int ls_profile_enable(ls_ctx* c, int enable) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    DeviceScope dev(c->device);
+    if (!c->recs.empty()) {
+        LS_HIP(c, hipDeviceSynchronize());
+        for (auto& r : c->recs) {
+            c->spare.push_back(r.start);
+            c->spare.push_back(r.stop);
+        }
+        c->recs.clear();
+    }
+    c->profiling = enable != 0;
+    return LS_OK;
+}
+
+int ls_profile_read(ls_ctx* c, int32_t max_kinds, const char** names, int64_t* launches, double* total_ms,
+                    int32_t* n_kinds) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (max_kinds < 0 || (max_kinds > 0 && (!names || !launches || !total_ms)))
+        return fail(c, LS_ERR_INVALID, "output arrays must hold max_kinds entries");
+    DeviceScope dev(c->device);
+    int64_t cnt[K_COUNT] = {};
+    double ms[K_COUNT] = {};
+    for (auto& r : c->recs) {
+        LS_HIP(c, hipEventSynchronize(r.stop));
+        float t = 0.0f;
+        LS_HIP(c, hipEventElapsedTime(&t, r.start, r.stop));
+        cnt[r.kind] += 1;
+        ms[r.kind] += t;
+    }
+    int32_t k = 0;
+    for (int kind = 0; kind < K_COUNT; ++kind) {
+        if (!cnt[kind]) continue;
+        if (k < max_kinds) {
+            names[k] = kKindNames[kind];
+            launches[k] = cnt[kind];
+            total_ms[k] = ms[kind];
+        }
+        ++k;
+    }
+    if (n_kinds) *n_kinds = k;
+    return LS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,235 @@
+"""Thin ctypes binding of liblodestar.so (include/lodestar.h).
+
+Argument marshalling only: torch tensors are checked for dtype, device, shape
+and contiguity, then their data pointers and the current HIP stream are passed
+to the C functions of the same name.  Every step of the hot path runs in the
+library's HIP kernels.  There is no fallback: if the library is missing the
+import of a Context fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblodestar.so")
+
+LS_OK, LS_ERR_INVALID, LS_ERR_NOMEM, LS_ERR_DEVICE, LS_ERR_STATE, LS_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+LS_FP32, LS_BF16 = 0, 1
+DERIVED_COLS = 5
+_DTYPES = {"fp32": LS_FP32, "f32": LS_FP32, "bf16": LS_BF16}
+
+
+class LodestarError(RuntimeError):
+    def __init__(self, func, code, msg):
+        super().__init__(f"{func} returned {code}: {msg}")
+        self.code = code
+
+
+class ls_model_config(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("n_hidden", ctypes.c_int32), ("hidden", ctypes.c_int32 * 3),
+                ("block_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def library():
+    """Load liblodestar.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run `python -m paper_2606_00946_amd.build` first")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        cfgp = ctypes.POINTER(ls_model_config)
+        lib.ls_param_count.argtypes = [cfgp]
+        lib.ls_param_count.restype = i64
+        lib.ls_create.argtypes = [cfgp, ctypes.c_int, ctypes.POINTER(P)]
+        lib.ls_destroy.argtypes = [P]
+        lib.ls_destroy.restype = None
+        lib.ls_last_error.argtypes = [P]
+        lib.ls_last_error.restype = ctypes.c_char_p
+        lib.ls_set_model.argtypes = [P, P, i64, P, P, P]
+        lib.ls_get_model.argtypes = [P, P, i64, P, P]
+        lib.ls_load_cache_state.argtypes = [P, i32, P, P, P]
+        lib.ls_score_batch.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P, P, P]
+        lib.ls_update.argtypes = [P, i32, P, P, f32, P, P, P]
+        lib.ls_profile_enable.argtypes = [P, ctypes.c_int]
+        lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
+        for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
+                  lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read):
+            f.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def make_config(d, hidden, dtype="fp32", block_tokens=16) -> ls_model_config:
+    h = list(hidden) + [0] * (3 - len(hidden))
+    return ls_model_config(int(d), len(hidden), (ctypes.c_int32 * 3)(*h), int(block_tokens),
+                           _DTYPES[dtype] if isinstance(dtype, str) else int(dtype))
+
+
+def ls_param_count(d, hidden) -> int:
+    cfg = make_config(d, hidden)
+    return int(library().ls_param_count(ctypes.byref(cfg)))
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream))
+
+
+_EMPTY = {}
+
+
+def _empty_ptr(device):
+    """A valid one-element device buffer standing in for an empty tensor (whose
+    data pointer may be NULL); the library never reads it."""
+    import torch
+    if device not in _EMPTY:
+        _EMPTY[device] = torch.zeros(1, dtype=torch.int64, device=device)
+    return ctypes.c_void_p(_EMPTY[device].data_ptr())
+
+
+def _dev(t, name, dtypes, numel=None, allow_none=False):
+    """Device pointer of a contiguous CUDA tensor with one of `dtypes`."""
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    if t.numel() == 0:
+        return _empty_ptr(t.device)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _host(a, dtype, numel=None):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    if numel is not None and a.size != numel:
+        raise ValueError(f"expected {numel} elements, got {a.size}")
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Context:
+    """One ls_ctx: model, cache state and workspace on one device."""
+
+    def __init__(self, d, hidden, dtype="fp32", block_tokens=16, device=None):
+        import torch
+        self.lib = library()
+        self.cfg = make_config(d, hidden, dtype, block_tokens)
+        self.d = int(d)
+        self.hidden = tuple(hidden)
+        self.n_params = int(self.lib.ls_param_count(ctypes.byref(self.cfg)))
+        if self.n_params < 0:
+            raise ValueError("invalid model shape")
+        self.device = torch.cuda.current_device() if device is None else int(device)
+        h = ctypes.c_void_p()
+        rc = self.lib.ls_create(ctypes.byref(self.cfg), self.device, ctypes.byref(h))
+        if rc != LS_OK:
+            raise LodestarError("ls_create", rc, "could not create a context")
+        self.h = h
+        self.n_instances = None
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.ls_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, func, rc):
+        if rc != LS_OK:
+            raise LodestarError(func, rc, self.lib.ls_last_error(self.h).decode())
+        return rc
+
+    def last_error(self) -> str:
+        return self.lib.ls_last_error(self.h).decode()
+
+    # -- model -------------------------------------------------------------
+    def ls_set_model(self, params, mu, inv_sigma, stream=None):
+        p, pp = _host(params, np.float32, self.n_params)
+        m, mp = _host(mu, np.float32, self.d)
+        s, sp = _host(inv_sigma, np.float32, self.d)
+        return self._check("ls_set_model", self.lib.ls_set_model(self.h, pp, self.n_params, mp, sp, _stream(stream)))
+
+    def ls_get_model(self):
+        p = np.zeros(self.n_params, np.float32)
+        m = np.zeros(self.d, np.float32)
+        s = np.zeros(self.d, np.float32)
+        self._check("ls_get_model", self.lib.ls_get_model(self.h, p.ctypes.data_as(ctypes.c_void_p), self.n_params,
+                                                          m.ctypes.data_as(ctypes.c_void_p),
+                                                          s.ctypes.data_as(ctypes.c_void_p)))
+        return p, m, s
+
+    # -- cache state -------------------------------------------------------
+    def ls_load_cache_state(self, inst_off, hashes, stream=None):
+        import torch
+        off, offp = _host(inst_off, np.int64)
+        N = off.size - 1
+        hp = _dev(hashes, "hashes", (torch.int64, torch.uint64), int(off[-1]) if N >= 0 else None)
+        rc = self.lib.ls_load_cache_state(self.h, N, offp, hp, _stream(stream))
+        self._check("ls_load_cache_state", rc)
+        self.n_instances = N
+        return rc
+
+    # -- scoring -----------------------------------------------------------
+    def ls_score_batch(self, req_off, req_hashes, prompt_len, inst_feat, chosen, min_ttft=None, scores=None,
+                       overlap=None, feat_out=None, stream=None):
+        import torch
+        R = req_off.numel() - 1
+        N = inst_feat.shape[0] if inst_feat.dim() == 2 else (self.n_instances or 0)
+        d_inst = self.d - DERIVED_COLS
+        args = [
+            _dev(req_off, "req_off", (torch.int64,), R + 1),
+            _dev(req_hashes, "req_hashes", (torch.int64, torch.uint64)),
+            _dev(prompt_len, "prompt_len", (torch.int32,), R),
+            _dev(inst_feat, "inst_feat", (torch.float32,), N * d_inst),
+            _dev(chosen, "chosen", (torch.int32,), R),
+            _dev(min_ttft, "min_ttft", (torch.float32,), R, allow_none=True),
+            _dev(scores, "scores", (torch.float32,), R * N, allow_none=True),
+            _dev(overlap, "overlap", (torch.int32,), R * N, allow_none=True),
+            _dev(feat_out, "feat_out", (torch.float32,), R * self.d, allow_none=True),
+        ]
+        return self._check("ls_score_batch", self.lib.ls_score_batch(self.h, R, N, *args, _stream(stream)))
+
+    # -- online update -----------------------------------------------------
+    def ls_update(self, feats, ttft, lr, loss_out=None, grad_out=None, stream=None):
+        import torch
+        B = ttft.numel()
+        args = [
+            _dev(feats, "feats", (torch.float32,), B * self.d),
+            _dev(ttft, "ttft", (torch.float32,), B),
+        ]
+        lo = _dev(loss_out, "loss_out", (torch.float32,), 1, allow_none=True)
+        go = _dev(grad_out, "grad_out", (torch.float32,), self.n_params, allow_none=True)
+        return self._check("ls_update", self.lib.ls_update(self.h, B, *args, float(lr), lo, go, _stream(stream)))
+
+    # -- per-kernel timing ------------------------------------------------
+    def ls_profile_enable(self, enable=True):
+        return self._check("ls_profile_enable", self.lib.ls_profile_enable(self.h, 1 if enable else 0))
+
+    def ls_profile_read(self) -> dict:
+        """{kind: (launches, total_ms)} since profiling was enabled (synchronous)."""
+        k = 16
+        names = (ctypes.c_char_p * k)()
+        launches = (ctypes.c_int64 * k)()
+        ms = (ctypes.c_double * k)()
+        n = ctypes.c_int32()
+        self._check("ls_profile_read", self.lib.ls_profile_read(self.h, k, names, launches, ms, ctypes.byref(n)))
+        return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(min(k, n.value))}

@@ -289,7 +289,7 @@ def pin_update_golden():
     d = g["d"]
     mu = np.zeros(d, np.float32); s = np.ones(d, np.float32)
     sg = g["sgd"]
-    for mode in ("f64", "bf16"):
+    for mode in ("f64", "fp32", "bf16"):
         res = oracle.update(mode, d, g["hidden"], params, mu, s, np.array(g["x"]), np.array(sg["ttft"]), sg["lr"])
         assert res["loss"] == sg["loss"], (mode, res["loss"])
         _check_grad(res, sg, d, g["hidden"])
@@ -338,9 +338,11 @@ def pin_update_invariants(seed=13):
     r1 = oracle.update("f64", d, hidden, params, mu, s, x, y, 1e-3)
     dp = r1["params"].astype(np.float64) - params.astype(np.float64)
     assert np.sum(dp * r0["grad"]) < 0
-    # loss agrees with the forward pass
-    t = oracle.forward("f64", d, hidden, params, mu, s, x.astype(np.float64))
-    assert np.isclose(r0["loss"], np.mean((t - y.astype(np.float64)) ** 2), rtol=1e-13)
+    # loss agrees with the forward pass of the same precision
+    for mode in ("f64", "fp32", "bf16"):
+        t = oracle.forward(mode, d, hidden, params, mu, s, x.astype(np.float64))
+        r = oracle.update(mode, d, hidden, params, mu, s, x, y, 0.0)
+        assert np.isclose(r["loss"], np.mean((t - y.astype(np.float64)) ** 2), rtol=1e-13), mode
 
 
 def pin_update_finite_difference(seed=17):

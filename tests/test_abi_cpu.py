@@ -1,0 +1,74 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/lodestar.h declares, and rejects bad configurations
+before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_00946_amd import lodestar, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lodestar.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ls_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("ls_load_cache_state", "ls_score_batch", "ls_update", "ls_create", "ls_destroy",
+                     "ls_set_model", "ls_get_model", "ls_last_error", "ls_param_count"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = lodestar.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_param_count_matches_packing():
+    for cfg in synth.CONFIGS.values():
+        assert lodestar.ls_param_count(cfg.d, cfg.hidden) == synth.param_count(cfg.d, cfg.hidden)
+    assert lodestar.ls_param_count(8, [2, 2]) == 2 * 8 + 2 + 2 * 2 + 2 + 2 + 1
+    assert lodestar.ls_param_count(5, [4, 4]) == -1          # d must leave room for the 5 derived columns
+
+
+def test_create_rejects_bad_configs_on_the_host():
+    lib = lodestar.library()
+    h = ctypes.c_void_p(1)
+    bad = [lodestar.make_config(4, [8, 8]), lodestar.make_config(16, [0, 8]),
+           lodestar.make_config(16, [8, 8], dtype=7), lodestar.make_config(16, [600, 8])]
+    for cfg in bad:
+        assert lib.ls_create(ctypes.byref(cfg), 0, ctypes.byref(h)) == lodestar.LS_ERR_INVALID
+        assert h.value is None
+    three = lodestar.make_config(16, [128, 128, 128])
+    assert lib.ls_create(ctypes.byref(three), 0, ctypes.byref(h)) == lodestar.LS_ERR_UNSUPPORTED
+    assert lib.ls_create(None, 0, ctypes.byref(h)) == lodestar.LS_ERR_INVALID
+    assert lib.ls_last_error(None) == b"context is NULL"
+
+
+def test_entry_points_reject_null_context():
+    lib = lodestar.library()
+    assert lib.ls_set_model(None, None, 0, None, None, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_get_model(None, None, 0, None, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_load_cache_state(None, 1, None, None, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_score_batch(None, 1, 1, *([None] * 10)) == lodestar.LS_ERR_INVALID
+    assert lib.ls_update(None, 1, None, None, 0.1, None, None, None) == lodestar.LS_ERR_INVALID
+    lib.ls_destroy(None)
+
+
+def test_no_device_is_reported_as_device_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    lib = lodestar.library()
+    cfg = lodestar.make_config(16, [64, 64])
+    h = ctypes.c_void_p(1)
+    assert lib.ls_create(ctypes.byref(cfg), 0, ctypes.byref(h)) == lodestar.LS_ERR_DEVICE
+    assert h.value is None

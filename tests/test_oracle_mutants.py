@@ -34,11 +34,12 @@ MUTANTS = [
     ("lowp_drops_bias", "float acc = net->b[l][j];", "float acc = 0.0f;"),
     ("f64_transposed_weight", "acc += (double)net->W[l][(int64_t)j * K + k] * a[k];",
      "acc += (double)net->W[l][(int64_t)k * O + j] * a[k];"),
-    ("lowp_skips_last_input", "for (int k = 0; k < K; ++k) {\n                float w",
-     "for (int k = 0; k + 1 < K; ++k) {\n                float w"),
+    ("lowp_skips_last_input", "for (int k = 0; k < K; ++k) {\n                acc = fmaf(",
+     "for (int k = 0; k + 1 < K; ++k) {\n                acc = fmaf("),
     ("f64_no_relu", "for (int j = 0; j < O; ++j) z[j] = z[j] > 0.0 ? z[j] : 0.0;", ""),
     ("lowp_leaky_relu", "float h = z[j] > 0.0f ? z[j] : 0.0f;", "float h = z[j] > 0.0f ? z[j] : 0.01f * z[j];"),
-    ("bf16_skips_weights", "if (bf) w = lso_bf16_round(w);", ""),
+    ("bf16_skips_weights", "q[net->W_off[l] + t] = lso_bf16_round(params[net->W_off[l] + t]);",
+     "q[net->W_off[l] + t] = params[net->W_off[l] + t];"),
     ("bf16_ties_away", "double q = nearbyint((double)x * scale);", "double q = round((double)x * scale);"),
     ("bf16_truncates", "double q = nearbyint((double)x * scale);", "double q = trunc((double)x * scale);"),
     ("argmin_tie_highest", "    return ia < ib;\n}\n\nint32_t lso_argmin", "    return ia > ib;\n}\n\nint32_t lso_argmin"),
@@ -53,8 +54,14 @@ MUTANTS = [
      "for (int k = 0; k < K; ++k) gw[k] += dj * a[(k + 1) % K];"),
     ("update_backprop_uses_row", "s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];",
      "s += Wq[net.W_off[l] + (int64_t)k * O + j] * delta[j];"),
+    ("update_bf16_backprop_skips_unit", "for (int j = 0; j < O; ++j) f = fmaf(",
+     "for (int j = 1; j < O; ++j) f = fmaf("),
     ("update_no_bias_grad", "grad[net.b_off[l] + j] += dj;", ""),
     ("update_bf16_delta_unrounded", "dnext[k] = bf ? (double)lso_bf16_round((float)dk) : dk;", "dnext[k] = dk;"),
+    ("update_lowp_forward_unfused", "f = fmaf((float)Wq[net.W_off[l] + (int64_t)j * K + k], (float)a[k], f);",
+     "f = f + (float)Wq[net.W_off[l] + (int64_t)j * K + k] * (float)a[k];"),
+    ("update_lowp_inputs_in_double", "a0[k] = bf ? (double)lso_bf16_round(t) : (double)t;",
+     "a0[k] = bf ? (double)lso_bf16_round(t) : ((double)xb[k] - (double)mu[k]) * (double)inv_sigma[k];"),
     ("update_loss_not_mean", "if (loss_out) *loss_out = loss / (double)B;", "if (loss_out) *loss_out = loss;"),
 ]
 
