@@ -65,8 +65,12 @@ def cpu_baseline(w, target_s=12.0):
                      w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=threads)
         return len(sel), time.perf_counter() - t
 
+    # two points separate the per-call cost (building the instance sets) from the per-request cost
     s0, t0 = run(16)
-    S = int(min(cfg.R, max(16, s0 * target_s / max(t0, 1e-3))))
+    s1, t1 = run(64)
+    per_req = max((t1 - t0) / max(s1 - s0, 1), 1e-6)
+    fixed = max(t0 - s0 * per_req, 0.0)
+    S = int(min(cfg.R, max(64, (target_s - fixed) / per_req)))
     s1, t1 = run(S)
     return {
         "value": s1 * cfg.N / t1, "unit": "pairs/s", "cores": threads, "kind": "oracle",
