@@ -141,6 +141,17 @@ int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
                    void* stream);
 
 /*
+ * Scoring precision of an LS_BF16 context.  By default the bf16 model runs on
+ * the matrix cores; every candidate whose fast score lies within an error band
+ * of its request's best is then rescored with the canonical fp32 chain, and the
+ * decision (`chosen`) and `min_ttft` come from those canonical scores.  Scores
+ * outside the band are the fast ones.  enable != 0 scores every pair with the
+ * canonical chain instead (exact `scores`, slower).  fp32 contexts always use
+ * the canonical chain.  Takes effect for later ls_score_batch calls.
+ */
+int ls_set_exact_scores(ls_ctx* ctx, int enable);
+
+/*
  * One SGD step on the installed model (Section 4.3.2, online learning; the
  * loss and optimiser are this library's reading: mean squared error of the
  * predicted TTFT, plain SGD).  L = (1/B) sum_b (t_b - y_b)^2, W <- W - lr dL/dW.
@@ -159,7 +170,8 @@ int ls_update(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, flo
  * Section 5.4 measures the router's overhead end to end).  While enabled, each
  * kernel launch group of the context is bracketed by HIP events on the stream
  * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
- * "score_pairs", "argmin", "update".
+ * "score_pairs", "score_pairs_mfma", "band_select", "rescore", "argmin",
+ * "update".
  *   ls_profile_enable  enable != 0 starts recording (and clears old records).
  *   ls_profile_read    synchronous; for up to max_kinds kinds writes the kind
  *                      name (static string), the number of launches and the

@@ -16,28 +16,9 @@
 //
 // bf16 models (LS_BF16): weights and each layer's input activations are bf16
 // values, products are exact in fp32, sums and biases stay fp32.
-#include <climits>
-
-#include "ls_internal.h"
+#include "k_common.h"
 
 namespace ls {
-
-// Round to the nearest bf16 value, ties to even (bits of a binary32).
-__device__ __forceinline__ float bf16_rne(float x) {
-    if (x != x) return x;
-    uint32_t u = __float_as_uint(x);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return __uint_as_float(u & 0xFFFF0000u);
-}
-
-// Same, for values known not to be NaN (ReLU outputs).
-__device__ __forceinline__ float bf16_rne_num(float x) {
-    uint32_t u = __float_as_uint(x);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return __uint_as_float(u & 0xFFFF0000u);
-}
-
-__device__ __forceinline__ float relu(float z) { return z > 0.0f ? z : 0.0f; }
 
 // ---------------------------------------------------------------------------
 // compute copy of the model
@@ -126,42 +107,6 @@ hipError_t launch_instance_partial(const ModelDims& m, const float* compute, con
 // ---------------------------------------------------------------------------
 // pair scoring: one lane per pair, weights uniform across the wave
 // ---------------------------------------------------------------------------
-struct PairModel {
-    const float* __restrict__ w1;    // [h1 x d]
-    const float* __restrict__ w2t;   // [h1 x h2]
-    const float* __restrict__ b2;    // [h2]
-    const float* __restrict__ w3;    // [h2]
-    const float* __restrict__ b3;    // [1]
-    int d, d_inst, h1, h2;
-};
-
-// U consecutive layer-2 units starting at jb, then their head terms in order.
-template <bool BF, int U>
-__device__ __forceinline__ float unit_block(const PairModel& M, const float* __restrict__ part_i, int32_t N,
-                                            const float xt[5], int jb, float t) {
-    float acc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) acc[u] = M.b2[jb + u];
-    for (int k = 0; k < M.h1; ++k) {
-        float z = part_i[(int64_t)k * N];
-        const float* __restrict__ w1 = M.w1 + (int64_t)k * M.d + M.d_inst;
-#pragma unroll
-        for (int c = 0; c < 5; ++c) z = __builtin_fmaf(w1[c], xt[c], z);
-        float a = relu(z);
-        if (BF) a = bf16_rne_num(a);
-        const float* __restrict__ w2 = M.w2t + (int64_t)k * M.h2 + jb;
-#pragma unroll
-        for (int u = 0; u < U; ++u) acc[u] = __builtin_fmaf(w2[u], a, acc[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        float hh = relu(acc[u]);
-        if (BF) hh = bf16_rne_num(hh);
-        t = __builtin_fmaf(M.w3[jb + u], hh, t);
-    }
-    return t;
-}
-
 template <bool BF>
 __global__ __launch_bounds__(256) void score_pairs_kernel(PairModel M, const float* __restrict__ mu,
                                                           const float* __restrict__ isig,
@@ -175,31 +120,10 @@ __global__ __launch_bounds__(256) void score_pairs_kernel(PairModel M, const flo
     const bool valid = p < total;
     const int64_t pp = valid ? p : 0;
     const int64_t r = pp / N, i = pp - r * N;
-    const int32_t L = prompt_len[r];
-    const int64_t n = req_off[r + 1] - req_off[r];
-    const int32_t l = overlap[pp];
-    const int64_t hit = (int64_t)block_tokens * l;
-    float x[5];
-    x[0] = (float)L;
-    x[1] = (float)n;
-    x[2] = (float)l;
-    x[3] = (L == 0) ? 0.0f : (float)hit / (float)L;
-    x[4] = (float)((int64_t)L - hit);
-    float xt[5];
-#pragma unroll
-    for (int c = 0; c < 5; ++c) {
-        float v = __fmul_rn(__fsub_rn(x[c], mu[M.d_inst + c]), isig[M.d_inst + c]);
-        xt[c] = BF ? bf16_rne(v) : v;
-    }
-    const float* __restrict__ part_i = part_t + i;
-    float t = M.b3[0];
-    int jb = 0;
-    for (; jb + 32 <= M.h2; jb += 32) t = unit_block<BF, 32>(M, part_i, N, xt, jb, t);
-    if (jb + 16 <= M.h2) { t = unit_block<BF, 16>(M, part_i, N, xt, jb, t); jb += 16; }
-    if (jb + 8 <= M.h2) { t = unit_block<BF, 8>(M, part_i, N, xt, jb, t); jb += 8; }
-    if (jb + 4 <= M.h2) { t = unit_block<BF, 4>(M, part_i, N, xt, jb, t); jb += 4; }
-    if (jb + 2 <= M.h2) { t = unit_block<BF, 2>(M, part_i, N, xt, jb, t); jb += 2; }
-    if (jb + 1 <= M.h2) { t = unit_block<BF, 1>(M, part_i, N, xt, jb, t); jb += 1; }
+    float x[5], xt[5];
+    derived_columns(prompt_len[r], req_off[r + 1] - req_off[r], overlap[pp], block_tokens, x);
+    normalise_tail<BF>(x, mu, isig, M.d_inst, xt);
+    const float t = canonical_score<BF>(M, part_t + i, N, xt);
     if (valid) scores[p] = t;
 }
 
@@ -223,21 +147,9 @@ hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const fl
 // ---------------------------------------------------------------------------
 // K3: per-request argmin, one wave per request
 // ---------------------------------------------------------------------------
-// Lexicographic order on (score, id): -0 equals +0, NaN after +inf, ties to the
-// lower id; id INT_MAX marks "no candidate yet".
-__device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
-    if (ia == INT_MAX) return false;
-    if (ib == INT_MAX) return true;
-    const bool an = a != a, bn = b != b;
-    if (an) return bn && ia < ib;
-    if (bn) return true;
-    if (a < b) return true;
-    if (a > b) return false;
-    return ia < ib;
-}
-
 __global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d, int d_inst, int block_tokens,
                                                      const float* __restrict__ scores,
+                                                     const uint8_t* __restrict__ band,
                                                      const int64_t* __restrict__ req_off,
                                                      const int32_t* __restrict__ prompt_len,
                                                      const int32_t* __restrict__ overlap,
@@ -251,6 +163,7 @@ __global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d
     float bs = 0.0f;
     int bi = INT_MAX;
     for (int i = lane; i < N; i += 64) {
+        if (band && !band[r * N + i]) continue;          // only candidates that were rescored
         float v = s[i];
         if (better(v, i, bs, bi)) { bs = v; bi = i; }
     }
@@ -265,30 +178,22 @@ __global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d
         if (min_ttft) min_ttft[r] = bs;
     }
     if (feat_out) {
-        const int32_t L = prompt_len[r];
-        const int64_t n = req_off[r + 1] - req_off[r];
-        const int32_t l = overlap[r * N + bi];
-        const int64_t hit = (int64_t)block_tokens * l;
+        float x[5];
+        derived_columns(prompt_len[r], req_off[r + 1] - req_off[r], overlap[r * N + bi], block_tokens, x);
         for (int c = lane; c < d; c += 64) {
-            float v;
-            if (c < d_inst) v = inst_feat[(int64_t)bi * d_inst + c];
-            else if (c == d_inst) v = (float)L;
-            else if (c == d_inst + 1) v = (float)n;
-            else if (c == d_inst + 2) v = (float)l;
-            else if (c == d_inst + 3) v = (L == 0) ? 0.0f : (float)hit / (float)L;
-            else v = (float)((int64_t)L - hit);
+            const float v = c < d_inst ? inst_feat[(int64_t)bi * d_inst + c] : x[c - d_inst];
             feat_out[r * d + c] = v;
         }
     }
 }
 
-hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const int64_t* req_off,
-                         const int32_t* prompt_len, const int32_t* overlap, const float* inst_feat,
-                         int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s) {
+hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const uint8_t* band,
+                         const int64_t* req_off, const int32_t* prompt_len, const int32_t* overlap,
+                         const float* inst_feat, int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     int64_t grid = ((int64_t)R + 3) / 4;
     hipLaunchKernelGGL(argmin_kernel, dim3((uint32_t)grid), dim3(256), 0, s, R, N, m.d, m.d_inst, m.block_tokens,
-                       scores, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft, feat_out);
+                       scores, band, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft, feat_out);
     return hipGetLastError();
 }
 

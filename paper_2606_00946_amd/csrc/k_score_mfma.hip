@@ -1,0 +1,417 @@
+// K2 on the matrix cores: bf16 reward model for every pair, then an exact
+// decision by canonical rescoring of every candidate that could be the argmin.
+//
+// The reward model is one MLP shared by all instances (Section 4.1); in bf16
+// mode its weights and every layer input are bf16, sums fp32.  The bulk of the
+// work is the [pairs x h1] x [h1 x h2] hidden layer, a dense contraction, so it
+// runs as v_mfma_f32_32x32x16_bf16 with rows = units and columns = pairs:
+//   layer 1  A = W1 fragments, B = normalised bf16 pair rows, C = b1
+//   layer 2  A = W2 fragments (LDS), B = bf16(relu(layer-1 accumulators))
+//   head     A = [w3; |w3|; 0...], B = bf16(relu(layer-2 accumulators))
+// An accumulator of a 32x32 tile holds, in lane l and register r, unit
+// 8(r/4) + 4(l/32) + r%4 of pair l%32.  The next layer's B operand needs, in
+// lane l, eight consecutive k of pair l%32 -- so each layer's inputs are taken
+// in that register order (perm_unit below) and the weights are stored with the
+// same permutation of their input index: activations never leave registers.
+//
+// MFMA sums in an order of its own, so a bf16 activation near a rounding
+// boundary can round differently than in the canonical fma chain.  Every pair
+// therefore also gets an error scale E = kBandRel * (sum_j |w3_j| h2_j + |b3|)
+// (the |w3| row of the head tile).  Per request, every pair whose interval
+// [t - E, t + E] reaches the smallest t + E is rescored with the canonical
+// chain, and the argmin runs over those canonical scores only; the chosen
+// instance and its score are then the canonical ones whenever |t - t_canonical|
+// <= E holds for the pairs left out.  The tests check that bound on every
+// sampled pair with a margin.
+#include "k_common.h"
+
+namespace ls {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Input unit addressed by k-step s, lane half h, slot j of a B operand built
+// straight from the previous layer's accumulators (s = 2*m_tile + half).
+__host__ __device__ __forceinline__ int perm_unit(int s, int h, int j) {
+    return 32 * (s >> 1) + 16 * (s & 1) + 8 * (j >> 2) + 4 * h + (j & 3);
+}
+
+__device__ __forceinline__ uint16_t bf16_bits(float x) { return (uint16_t)(__float_as_uint(bf16_rne(x)) >> 16); }
+
+// ---------------------------------------------------------------------------
+// fragment tables, rebuilt from the fp32 masters whenever the model changes
+// ---------------------------------------------------------------------------
+__global__ void prepare_mfma_kernel(MfmaLayout L, const float* __restrict__ master, uint16_t* __restrict__ frag16,
+                                    float* __restrict__ frag32) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int d = L.d, h1 = L.h1;
+    const float* W1 = master + L.m_w1;
+    const float* W2 = master + L.m_w2;
+    const float* W3 = master + L.m_w3;
+    const int64_t nfrag = (L.w1_frags + L.w2_frags) * 512;
+    if (t < nfrag) {
+        const int j = (int)(t & 7);
+        const int lane = (int)((t >> 3) & 63);
+        const int64_t f = t >> 9;                       // fragment index
+        const int m = lane & 31, h = lane >> 5;
+        float v = 0.0f;
+        if (f < L.w1_frags) {                            // [s(4)][mt] : W1[32mt+m][16s+8h+j]
+            const int mt1 = h1 / 32;
+            const int s = (int)(f / mt1), mt = (int)(f % mt1);
+            const int c = 16 * s + 8 * h + j;
+            if (c < d) v = W1[(int64_t)(32 * mt + m) * d + c];
+        } else {                                         // [mt2][s(h1/16)] : W2[32mt2+m][perm(s,h,j)]
+            const int64_t g = f - L.w1_frags;
+            const int ks = h1 / 16;
+            const int mt2 = (int)(g / ks), s = (int)(g % ks);
+            v = W2[(int64_t)(32 * mt2 + m) * h1 + perm_unit(s, h, j)];
+        }
+        frag16[t] = bf16_bits(v);
+    } else if (t < L.n16) {                              // head weights [s(h2/16)][h][j] : w3[perm(s,h,j)]
+        const int64_t e = t - nfrag;
+        const int j = (int)(e & 7), h = (int)((e >> 3) & 1);
+        const int s = (int)(e >> 4);
+        frag16[t] = bf16_bits(W3[perm_unit(s, h, j)]);
+    } else if (t < L.n16 + L.n32) {                      // bias fragments [mt][h][r] for b1 then b2
+        const int64_t e = t - L.n16;
+        const int r = (int)(e & 15), h = (int)((e >> 4) & 1);
+        const int64_t mt = e >> 5;
+        const int unit_in_tile = 8 * (r >> 2) + 4 * h + (r & 3);
+        const int mt1 = h1 / 32;
+        float v;
+        if (mt < mt1) v = master[L.m_b1 + 32 * mt + unit_in_tile];
+        else v = master[L.m_b2 + 32 * (mt - mt1) + unit_in_tile];
+        frag32[e] = v;
+    }
+}
+
+hipError_t launch_prepare_mfma(const MfmaLayout& L, const float* master, uint16_t* frag16, float* frag32,
+                               hipStream_t s) {
+    const int64_t n = L.n16 + L.n32;
+    hipLaunchKernelGGL(prepare_mfma_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, L, master, frag16,
+                       frag32);
+    return hipGetLastError();
+}
+
+// Normalised bf16 instance columns, 64 per instance (zero past d_inst).
+__global__ void instance_rows_kernel(const float* __restrict__ inst_feat, const float* __restrict__ mu,
+                                     const float* __restrict__ isig, int d_inst, int32_t N,
+                                     uint16_t* __restrict__ xinst) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)N * 64) return;
+    const int64_t i = t >> 6;
+    const int c = (int)(t & 63);
+    float v = 0.0f;
+    if (c < d_inst) v = __fmul_rn(__fsub_rn(inst_feat[i * d_inst + c], mu[c]), isig[c]);
+    xinst[t] = bf16_bits(v);
+}
+
+hipError_t launch_instance_rows(const ModelDims& m, const float* mu, const float* inv_sigma, const float* inst_feat,
+                                int32_t N, uint16_t* xinst, hipStream_t s) {
+    const int64_t n = (int64_t)N * 64;
+    hipLaunchKernelGGL(instance_rows_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, inst_feat, mu,
+                       inv_sigma, m.d_inst, N, xinst);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// the MFMA scoring kernel: persistent, one 32-pair tile per wave at a time
+// ---------------------------------------------------------------------------
+struct MfmaArgs {
+    const bf16x8_t* __restrict__ w1frag;
+    const bf16x8_t* __restrict__ w2frag;
+    const uint4* __restrict__ w3pk;
+    const float* __restrict__ b1frag;
+    const float* __restrict__ b2frag;
+    const float* __restrict__ b3;
+    const uint16_t* __restrict__ xinst;
+    const float* __restrict__ mu;
+    const float* __restrict__ isig;
+    const int64_t* __restrict__ req_off;
+    const int32_t* __restrict__ prompt_len;
+    const int32_t* __restrict__ overlap;
+    float* __restrict__ scores;
+    float* __restrict__ errb;
+    int32_t R, N;
+    int d, d_inst, block_tokens;
+    float band_rel;
+};
+
+__device__ __forceinline__ f32x16_t load_bias(const float* __restrict__ p) {
+    const float4* q = reinterpret_cast<const float4*>(p);
+    float4 a = q[0], b = q[1], c = q[2], e = q[3];
+    f32x16_t v;
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    v[8] = c.x; v[9] = c.y; v[10] = c.z; v[11] = c.w;
+    v[12] = e.x; v[13] = e.y; v[14] = e.z; v[15] = e.w;
+    return v;
+}
+
+// bf16(relu(.)) of accumulator registers 8q .. 8q+7 as one B operand
+__device__ __forceinline__ bf16x8_t relu_pack(const f32x16_t& acc, int q) {
+    bf16x8_t out;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        f32x2_t v;
+        v[0] = relu(acc[8 * q + 2 * jj]);
+        v[1] = relu(acc[8 * q + 2 * jj + 1]);
+        bf16x2_t p = __builtin_convertvector(v, bf16x2_t);
+        out[2 * jj] = p[0];
+        out[2 * jj + 1] = p[1];
+    }
+    return out;
+}
+
+// One wave scores one tile of 32 pairs (one request, 32 consecutive instances)
+// at a time; the eight waves of a workgroup share the W1 and W2 fragments in
+// LDS (32 + 128 KB at h = 256).  Each layer runs in passes of MH row tiles so
+// that few accumulators are live at once.
+template <int MT1, int MT2, int D>
+__global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
+    static_assert(MT1 == MT2, "square hidden layers");
+    constexpr int KS2 = 2 * MT1;               // layer-2 k-steps: h1 / 16
+    constexpr int MH = MT1 < 4 ? MT1 : 4;       // row tiles per pass
+    constexpr int D_INST = D - 5;
+    constexpr int NW1 = 4 * MT1 * 64, NW2 = MT2 * KS2 * 64;
+    __shared__ bf16x8_t lds_w1[NW1];
+    __shared__ bf16x8_t lds_w2[NW2];
+    for (int f = threadIdx.x; f < NW1; f += blockDim.x) lds_w1[f] = A.w1frag[f];
+    for (int f = threadIdx.x; f < NW2; f += blockDim.x) lds_w2[f] = A.w2frag[f];
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int waves = blockDim.x >> 6;
+    const int h = lane >> 5, n = lane & 31;
+    const int tiles_per_req = (A.N + 31) >> 5;
+    const int64_t n_tiles = (int64_t)A.R * tiles_per_req;
+    const float b3 = A.b3[0];
+    // head A operand: row 0 = w3, row 1 = |w3|, other rows zero
+    const uint32_t hmask = n == 0 ? 0xffffffffu : n == 1 ? 0x7fff7fffu : 0u;
+
+    for (int64_t tile = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6); tile < n_tiles;
+         tile += (int64_t)gridDim.x * waves) {
+        const int64_t r = tile / tiles_per_req;
+        const int i = (int)(tile - r * tiles_per_req) * 32 + n;
+        const bool valid = i < A.N;
+        const int ii = valid ? i : 0;
+
+        // layer-1 B operands: the pair's normalised bf16 row
+        bf16x8_t xb[4];
+        {
+            float x[5], xt[5];
+            derived_columns(A.prompt_len[r], A.req_off[r + 1] - A.req_off[r], valid ? A.overlap[r * A.N + i] : 0,
+                            A.block_tokens, x);
+            normalise_tail<true>(x, A.mu, A.isig, D_INST, xt);
+            const bf16x8_t* row = reinterpret_cast<const bf16x8_t*>(A.xinst + (int64_t)ii * 64);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                bf16x8_t v = row[2 * s + h];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int c0 = 16 * s + j - D_INST;       // derived column held by half 0
+                    const int c1 = c0 + 8;                    // ... by half 1
+                    if (c0 >= 0 && c0 < 5 && h == 0) v[j] = (__bf16)xt[c0 < 5 ? c0 : 0];
+                    if (c1 >= 0 && c1 < 5 && h == 1) v[j] = (__bf16)xt[c1 < 5 ? c1 : 0];
+                }
+                xb[s] = valid ? v : bf16x8_t{};
+            }
+        }
+
+        // layer 1 in passes: acc = b1 + W1 x, then bf16(relu(.))
+        bf16x8_t hb[KS2];
+#pragma unroll
+        for (int g = 0; g < MT1; g += MH) {
+            f32x16_t acc[MH];
+#pragma unroll
+            for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b1frag + ((g + u) * 2 + h) * 16);
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int u = 0; u < MH; ++u)
+                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_w1[(s * MT1 + g + u) * 64 + lane], xb[s],
+                                                                     acc[u], 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < MH; ++u) {
+                hb[2 * (g + u)] = relu_pack(acc[u], 0);
+                hb[2 * (g + u) + 1] = relu_pack(acc[u], 1);
+            }
+        }
+
+        // layer 2 in passes, each pass fed straight into the head:
+        // head row 0 = t, row 1 = sum_j |w3_j| h2_j
+        f32x16_t hd = f32x16_t{};
+        hd[0] = h == 0 ? b3 : 0.0f;
+#pragma unroll
+        for (int g = 0; g < MT2; g += MH) {
+            f32x16_t acc[MH];
+#pragma unroll
+            for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b2frag + ((g + u) * 2 + h) * 16);
+#pragma unroll
+            for (int s = 0; s < KS2; ++s)
+#pragma unroll
+                for (int u = 0; u < MH; ++u)
+                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_w2[((g + u) * KS2 + s) * 64 + lane], hb[s],
+                                                                     acc[u], 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < MH; ++u)
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int sh = 2 * (g + u) + q;
+                    const uint4 w = A.w3pk[sh * 2 + h];
+                    const uint4 wm = make_uint4(w.x & hmask, w.y & hmask, w.z & hmask, w.w & hmask);
+                    bf16x8_t a;
+                    __builtin_memcpy(&a, &wm, sizeof a);
+                    hd = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, relu_pack(acc[u], q), hd, 0, 0, 0);
+                }
+        }
+        if (h == 0 && valid) {
+            const int64_t p = r * A.N + i;
+            A.scores[p] = hd[0];
+            A.errb[p] = A.band_rel * (hd[1] + fabsf(b3));
+        }
+    }
+}
+
+bool mfma_supported(const ModelDims& m) {
+    return m.bf16 && (m.d == 16 || m.d == 32 || m.d == 48 || m.d == 64) &&
+           (m.h1 == 64 || m.h1 == 128 || m.h1 == 256) && m.h1 == m.h2;
+}
+
+template <int MT>
+static void launch_mfma_d(const MfmaArgs& a, int d, int64_t grid, hipStream_t s) {
+    if (d == 64) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 64>), dim3((uint32_t)grid), dim3(512), 0, s, a);
+    else if (d == 48) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 48>), dim3((uint32_t)grid), dim3(512), 0, s, a);
+    else if (d == 32) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 32>), dim3((uint32_t)grid), dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 16>), dim3((uint32_t)grid), dim3(512), 0, s, a);
+}
+
+hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, const float* frag32,
+                                   const float* compute, const uint16_t* xinst, const float* mu,
+                                   const float* inv_sigma, int32_t R, int32_t N, const int64_t* req_off,
+                                   const int32_t* prompt_len, const int32_t* overlap, float* scores, float* errb,
+                                   int n_cu, hipStream_t s) {
+    const MfmaLayout Lay = make_mfma_layout(m);
+    MfmaArgs a;
+    a.w1frag = reinterpret_cast<const bf16x8_t*>(frag16);
+    a.w2frag = reinterpret_cast<const bf16x8_t*>(frag16 + Lay.w1_frags * 512);
+    a.w3pk = reinterpret_cast<const uint4*>(frag16 + (Lay.w1_frags + Lay.w2_frags) * 512);
+    a.b1frag = frag32;
+    a.b2frag = frag32 + (m.h1 / 32) * 32;
+    a.b3 = compute + m.c_b3;
+    a.xinst = xinst;
+    a.mu = mu;
+    a.isig = inv_sigma;
+    a.req_off = req_off;
+    a.prompt_len = prompt_len;
+    a.overlap = overlap;
+    a.scores = scores;
+    a.errb = errb;
+    a.R = R;
+    a.N = N;
+    a.d = m.d;
+    a.d_inst = m.d_inst;
+    a.block_tokens = m.block_tokens;
+    a.band_rel = kBandRel;
+    const int64_t tiles = (int64_t)R * ((N + 31) / 32);
+    int64_t grid = (tiles + 7) / 8;
+    if (grid > n_cu) grid = n_cu;
+    if (grid < 1) grid = 1;
+    if (m.h1 == 256) launch_mfma_d<8>(a, m.d, grid, s);
+    else if (m.h1 == 128) launch_mfma_d<4>(a, m.d, grid, s);
+    else launch_mfma_d<2>(a, m.d, grid, s);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// band selection and canonical rescoring
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool finite_f(float x) { return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u; }
+
+// One wave per request: U = min_i (t_i + E_i) over finite pairs; a pair is a
+// candidate if t_i - E_i <= U (or if t_i or E_i is not finite).
+__global__ __launch_bounds__(256) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
+                                                          const float* __restrict__ E, uint8_t* __restrict__ band,
+                                                          int64_t* __restrict__ list, uint32_t* __restrict__ count) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    if (r >= R) return;
+    const float* __restrict__ tr = t + r * N;
+    const float* __restrict__ er = E + r * N;
+    float U = INFINITY;
+    for (int i = lane; i < N; i += 64) {
+        const float ti = tr[i], ei = er[i];
+        if (finite_f(ti) && finite_f(ei)) U = fminf(U, ti + ei);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) U = fminf(U, __shfl_xor(U, off));
+    U = U + fabsf(U) * 0x1p-20f;                    // absorbs the rounding of the sums above
+    for (int i0 = 0; i0 < N; i0 += 64) {
+        const int i = i0 + lane;
+        bool in = false;
+        if (i < N) {
+            const float ti = tr[i], ei = er[i];
+            in = !(finite_f(ti) && finite_f(ei)) || (ti - ei <= U);
+            band[r * N + i] = in ? 1 : 0;
+        }
+        const uint64_t m = __ballot(in);
+        if (m == 0) continue;
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(count, (uint32_t)__popcll(m));
+        base = __shfl(base, 0);
+        if (in) list[base + __popcll(m & ((1ull << lane) - 1))] = r * N + i;
+    }
+}
+
+hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
+                              uint32_t* count, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + 3) / 4)), dim3(256), 0, s, R, N, t, E, band,
+                       list, count);
+    return hipGetLastError();
+}
+
+// Canonical score of every listed pair, written over its fast score.
+template <bool BF>
+__global__ __launch_bounds__(256) void rescore_kernel(PairModel M, const float* __restrict__ mu,
+                                                      const float* __restrict__ isig,
+                                                      const float* __restrict__ part_t, int32_t N,
+                                                      const int64_t* __restrict__ req_off,
+                                                      const int32_t* __restrict__ prompt_len,
+                                                      const int32_t* __restrict__ overlap, int block_tokens,
+                                                      const int64_t* __restrict__ list,
+                                                      const uint32_t* __restrict__ count, float* __restrict__ scores) {
+    const uint32_t cnt = *count;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < cnt; q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t p = list[q];
+        const int64_t r = p / N, i = p - r * N;
+        float x[5], xt[5];
+        derived_columns(prompt_len[r], req_off[r + 1] - req_off[r], overlap[p], block_tokens, x);
+        normalise_tail<BF>(x, mu, isig, M.d_inst, xt);
+        scores[p] = canonical_score<BF>(M, part_t + i, N, xt);
+    }
+}
+
+hipError_t launch_rescore(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
+                          const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
+                          const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
+                          const uint32_t* count, float* scores, int n_cu, hipStream_t s) {
+    PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
+                m.d, m.d_inst, m.h1, m.h2};
+    // enough lanes for about two candidates per request, capped at 8 waves per SIMD
+    int64_t want = ((int64_t)R * 2 + 255) / 256;
+    int64_t cap = (int64_t)n_cu * 8;
+    int64_t grid = want < cap ? want : cap;
+    if (grid < 1) grid = 1;
+    if (m.bf16)
+        hipLaunchKernelGGL(rescore_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t, N,
+                           req_off, prompt_len, overlap, m.block_tokens, list, count, scores);
+    else
+        hipLaunchKernelGGL(rescore_kernel<false>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t, N,
+                           req_off, prompt_len, overlap, m.block_tokens, list, count, scores);
+    return hipGetLastError();
+}
+
+}  // namespace ls

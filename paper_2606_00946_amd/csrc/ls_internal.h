@@ -60,6 +60,34 @@ struct ModelDims {
 
 ModelDims make_dims(const ls_model_config& cfg);
 
+// bf16 matrix-core path: fragment tables derived from the masters.
+// frag16 (bf16 bits): W1 [4][h1/32] fragments, W2 [h2/32][h1/16] fragments (a
+// fragment is 64 lanes x 8 bf16), then w3 as [h2/16][lane half][8].
+// frag32: b1 then b2 as [tile][lane half][16].
+struct MfmaLayout {
+    int d = 0, h1 = 0, h2 = 0;
+    int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0;
+    int64_t w1_frags = 0, w2_frags = 0, h_frags = 0, n16 = 0, n32 = 0;
+};
+
+inline MfmaLayout make_mfma_layout(const ModelDims& m) {
+    MfmaLayout L;
+    L.d = m.d; L.h1 = m.h1; L.h2 = m.h2;
+    L.m_w1 = m.m_w1; L.m_b1 = m.m_b1; L.m_w2 = m.m_w2; L.m_b2 = m.m_b2; L.m_w3 = m.m_w3;
+    L.w1_frags = (int64_t)(m.h1 / 32) * 4;
+    L.w2_frags = (int64_t)(m.h2 / 32) * (m.h1 / 16);
+    L.h_frags = m.h2 / 16;
+    L.n16 = (L.w1_frags + L.w2_frags) * 512 + L.h_frags * 16;
+    L.n32 = (int64_t)(m.h1 / 32 + m.h2 / 32) * 32;
+    return L;
+}
+
+// Half-width of the candidate band around each fast bf16 score, relative to
+// sum_j |w3_j| h2_j + |b3| (the magnitude the head sums).
+constexpr float kBandRel = 0x1p-7f;
+
+bool mfma_supported(const ModelDims& m);
+
 // ---------------------------------------------------------------------------
 // Kernel launchers (each returns hipGetLastError() of its launch).
 // ---------------------------------------------------------------------------
@@ -78,9 +106,25 @@ hipError_t launch_instance_partial(const ModelDims& m, const float* compute, con
 hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
                               const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
                               const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s);
-hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const int64_t* req_off,
-                         const int32_t* prompt_len, const int32_t* overlap, const float* inst_feat,
-                         int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s);
+hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const uint8_t* band,
+                         const int64_t* req_off, const int32_t* prompt_len, const int32_t* overlap,
+                         const float* inst_feat, int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s);
+
+hipError_t launch_prepare_mfma(const MfmaLayout& L, const float* master, uint16_t* frag16, float* frag32,
+                               hipStream_t s);
+hipError_t launch_instance_rows(const ModelDims& m, const float* mu, const float* inv_sigma, const float* inst_feat,
+                                int32_t N, uint16_t* xinst, hipStream_t s);
+hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, const float* frag32,
+                                   const float* compute, const uint16_t* xinst, const float* mu,
+                                   const float* inv_sigma, int32_t R, int32_t N, const int64_t* req_off,
+                                   const int32_t* prompt_len, const int32_t* overlap, float* scores, float* errb,
+                                   int n_cu, hipStream_t s);
+hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
+                              uint32_t* count, hipStream_t s);
+hipError_t launch_rescore(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
+                          const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
+                          const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
+                          const uint32_t* count, float* scores, int n_cu, hipStream_t s);
 
 // Online update.  Workspace layout is chosen by update_workspace_floats().
 int64_t update_workspace_bytes(const ModelDims& m, int32_t B);

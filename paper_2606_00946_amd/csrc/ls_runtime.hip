@@ -24,6 +24,11 @@ struct ls_ctx {
     float* mu = nullptr;
     float* isig = nullptr;
     bool have_model = false;
+    // bf16 matrix-core path (fragment tables derived from the masters)
+    uint16_t* frag16 = nullptr;
+    float* frag32 = nullptr;
+    bool exact_scores = false;
+    int n_cu = 1;
     // cache state
     ls::CacheTables tables;
     int64_t table_cap_buckets = 0;
@@ -138,9 +143,9 @@ int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
     return LS_OK;
 }
 
-enum Kind { K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_COUNT };
+enum Kind { K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_COUNT };
 const char* const kKindNames[K_COUNT] = {"table_build", "prefix_match", "instance_partial", "score_pairs", "argmin",
-                                         "update"};
+                                         "update", "score_pairs_mfma", "band_select", "rescore"};
 
 hipEvent_t take_event(ls_ctx* c) {
     if (!c->spare.empty()) {
@@ -272,6 +277,12 @@ int ls_create(const ls_model_config* cfg, int device, ls_ctx** out) {
     ok = ok && hipMalloc((void**)&c->mu, sizeof(float) * cfg->d) == hipSuccess;
     ok = ok && hipMalloc((void**)&c->isig, sizeof(float) * cfg->d) == hipSuccess;
     ok = ok && hipEventCreateWithFlags(&c->stage_done, hipEventDisableTiming) == hipSuccess;
+    ok = ok && hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess;
+    if (ok && ls::mfma_supported(c->dims)) {
+        const ls::MfmaLayout L = ls::make_mfma_layout(c->dims);
+        ok = hipMalloc((void**)&c->frag16, sizeof(uint16_t) * L.n16) == hipSuccess &&
+             hipMalloc((void**)&c->frag32, sizeof(float) * L.n32) == hipSuccess;
+    }
     if (!ok) {
         (void)hipGetLastError();
         ls_destroy(c);
@@ -286,7 +297,8 @@ void ls_destroy(ls_ctx* c) {
     {
         DeviceScope dev(c->device);
         (void)hipDeviceSynchronize();
-        for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->tables.keys,
+        for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->frag16,
+                        (void*)c->frag32, (void*)c->tables.keys,
                         (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
                         (void*)c->inst_off_dev, c->ws})
             if (p) (void)hipFree(p);
@@ -326,6 +338,8 @@ int ls_set_model(ls_ctx* c, const float* params, int64_t n_params, const float* 
     LS_HIP(c, hipEventRecord(c->stage_done, s));
     c->stage_pending = true;
     LS_HIP(c, ls::launch_refresh_compute_copy(c->dims, c->master, c->compute, s));
+    if (c->frag16)
+        LS_HIP(c, ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
     c->have_model = true;
     return LS_OK;
 }
@@ -443,9 +457,17 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     const ls::ModelDims& m = c->dims;
     const int64_t pairs = (int64_t)R * N;
 
+    const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
     if (!overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!scores) need += (size_t)round_up(pairs * 4, 256);
+    if (fast) {
+        need += (size_t)round_up((int64_t)N * 64 * 2, 256);      // bf16 instance rows
+        need += (size_t)round_up(pairs * 4, 256);                // error scales
+        need += (size_t)round_up(pairs, 256);                    // candidate flags
+        need += (size_t)round_up(pairs * 8, 256);                // candidate list
+        need += 256;                                             // candidate count
+    }
     int rc = grow(c, &c->ws, &c->ws_cap, need);
     if (rc) return rc;
     WsCarve w{(char*)c->ws};
@@ -455,10 +477,36 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
 
     LS_TIMED(c, K_PREFIX, s, ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, s));
     LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
-    LS_TIMED(c, K_SCORE, s,
-             ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));
+    const uint8_t* band = nullptr;
+    if (fast) {
+        uint16_t* xinst = w.take<uint16_t>((int64_t)N * 64);
+        float* eb = w.take<float>(pairs);
+        uint8_t* flags = w.take<uint8_t>(pairs);
+        int64_t* list = w.take<int64_t>(pairs);
+        uint32_t* count = w.take<uint32_t>(64);
+        LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_rows(m, c->mu, c->isig, inst_feat, N, xinst, s));
+        LS_TIMED(c, K_SCORE_MFMA, s,
+                 ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, xinst, c->mu, c->isig, R, N, req_off,
+                                             prompt_len, ov, sc, eb, c->n_cu, s));
+        LS_TIMED(c, K_BAND, s, ls::launch_fill_u32(count, 0u, 1, s));
+        LS_TIMED(c, K_BAND, s, ls::launch_band_select(R, N, sc, eb, flags, list, count, s));
+        LS_TIMED(c, K_RESCORE, s,
+                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list, count,
+                                    sc, c->n_cu, s));
+        band = flags;
+    } else {
+        LS_TIMED(c, K_SCORE, s,
+                 ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));
+    }
     LS_TIMED(c, K_ARGMIN, s,
-             ls::launch_argmin(m, R, N, sc, req_off, prompt_len, ov, inst_feat, chosen, min_ttft, feat_out, s));
+             ls::launch_argmin(m, R, N, sc, band, req_off, prompt_len, ov, inst_feat, chosen, min_ttft, feat_out, s));
+    return LS_OK;
+}
+
+int ls_set_exact_scores(ls_ctx* c, int enable) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    c->exact_scores = enable != 0;
     return LS_OK;
 }
 
@@ -479,6 +527,9 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     LS_TIMED(c, K_UPDATE, s,
              ls::launch_update(c->dims, c->master, c->compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
                                c->ws, s));
+    if (c->frag16)
+        LS_TIMED(c, K_UPDATE, s,
+                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
     return LS_OK;
 }
 

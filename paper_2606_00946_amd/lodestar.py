@@ -58,9 +58,10 @@ def library():
         lib.ls_score_batch.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_update.argtypes = [P, i32, P, P, f32, P, P, P]
         lib.ls_profile_enable.argtypes = [P, ctypes.c_int]
+        lib.ls_set_exact_scores.argtypes = [P, ctypes.c_int]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
-                  lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read):
+                  lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -219,6 +220,9 @@ class Context:
         lo = _dev(loss_out, "loss_out", (torch.float32,), 1, allow_none=True)
         go = _dev(grad_out, "grad_out", (torch.float32,), self.n_params, allow_none=True)
         return self._check("ls_update", self.lib.ls_update(self.h, B, *args, float(lr), lo, go, _stream(stream)))
+
+    def ls_set_exact_scores(self, enable=True):
+        return self._check("ls_set_exact_scores", self.lib.ls_set_exact_scores(self.h, 1 if enable else 0))
 
     # -- per-kernel timing ------------------------------------------------
     def ls_profile_enable(self, enable=True):

@@ -23,14 +23,50 @@ def to_dev(a):
     return torch.from_numpy(a).to("cuda")
 
 
+BAND_REL = 2.0 ** -7           # half-width of the candidate band, relative to sum_j |w3_j| h2_j + |b3|
+
+
+def uses_fast_path(d, hidden, dtype, exact=False):
+    """Whether a context scores on the bf16 matrix-core path (mirrors the library's rule)."""
+    return (dtype == "bf16" and not exact and d in (16, 32, 48, 64) and len(hidden) == 2
+            and hidden[0] == hidden[1] and hidden[0] in (64, 128, 256))
+
+
+def bf16_np(x):
+    """Round float32 values to bf16 (ties to even), vectorised; finite inputs."""
+    u = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
+def head_magnitude(w, rows):
+    """sum_j |w3_j| h2_j + |b3| for raw feature rows, bf16 model (the scale of the band)."""
+    d, (h1, h2) = w.cfg.d, w.cfg.hidden
+    p = w.params
+    o = 0
+    W1 = p[o:o + h1 * d].reshape(h1, d); o += h1 * d
+    b1 = p[o:o + h1]; o += h1
+    W2 = p[o:o + h2 * h1].reshape(h2, h1); o += h2 * h1
+    b2 = p[o:o + h2]; o += h2
+    W3 = p[o:o + h2]; o += h2
+    b3 = p[o]
+    xt = bf16_np(((rows.astype(np.float32) - w.mu) * w.inv_sigma).astype(np.float32)).astype(np.float64)
+    a1 = bf16_np(np.maximum(xt @ bf16_np(W1).astype(np.float64).T + b1, 0).astype(np.float32)).astype(np.float64)
+    a2 = bf16_np(np.maximum(a1 @ bf16_np(W2).astype(np.float64).T + b2, 0).astype(np.float32)).astype(np.float64)
+    return a2 @ np.abs(bf16_np(W3).astype(np.float64)) + abs(float(b3))
+
+
 class GpuRun:
     """A context loaded with one workload's model and cache state."""
 
-    def __init__(self, w, dtype=None, params=None):
+    def __init__(self, w, dtype=None, params=None, exact=False):
         import torch
         self.w = w
         cfg = w.cfg
         self.ctx = lodestar.Context(cfg.d, cfg.hidden, dtype or cfg.dtype)
+        self.exact = exact
+        if exact:
+            self.ctx.ls_set_exact_scores(True)
         self.ctx.ls_set_model(w.params if params is None else params, w.mu, w.inv_sigma)
         self.inst_hashes = to_dev(w.inst_hashes)
         self.ctx.ls_load_cache_state(w.inst_off, self.inst_hashes)
