@@ -96,8 +96,16 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
 hipError_t launch_table_insert(const CacheTables& t, const int64_t* inst_off, const uint64_t* hashes,
                                int64_t total, int32_t n_inst, hipStream_t s);
 
+// Group table for the prefix-sharing pass: a power of two >= 2R slots.
+inline int64_t group_table_size(int32_t R) {
+    int64_t g = 64;
+    while (g < 2 * (int64_t)R) g <<= 1;
+    return g;
+}
+int64_t prefix_workspace_bytes(int32_t R);
 hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const int64_t* req_off,
-                               const uint64_t* req_hashes, int32_t* overlap, hipStream_t s);
+                               const uint64_t* req_hashes, int32_t* overlap, void* workspace, int n_cu,
+                               hipStream_t s);
 
 hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s);
 hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,

@@ -459,6 +459,7 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
 
     const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
+    need += (size_t)round_up(ls::prefix_workspace_bytes(R), 256);
     if (!overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
@@ -472,10 +473,12 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     if (rc) return rc;
     WsCarve w{(char*)c->ws};
     float* part_t = w.take<float>((int64_t)m.h1 * N);
+    char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R));
     int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
     float* sc = scores ? scores : w.take<float>(pairs);
 
-    LS_TIMED(c, K_PREFIX, s, ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, s));
+    LS_TIMED(c, K_PREFIX, s,
+             ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu, s));
     LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     const uint8_t* band = nullptr;
     if (fast) {
