@@ -147,10 +147,13 @@ def main():
     ov = overlap.cpu().numpy().reshape(R, N).astype(np.int64)
     probes = int(np.minimum(ov + 1, n[:, None]).sum())
     k1_bytes = 64 * probes + 8 * int(n.sum()) + 4 * R * N
+    model_tflop = model_flops_per_pair(cfg) * R * N / 1e12
     roof = {
         "prefix_match": ("hbm", k1_bytes / 1e9, PEAK_HBM_GBS, "GB/s"),
-        "score_pairs": ("alu", model_flops_per_pair(cfg) * R * N / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
+        "score_pairs": ("alu", model_tflop, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
+        "score_pairs_mfma": ("mfma", model_tflop, PEAK_BF16_TFLOPS, "TFLOP/s"),
         "update": ("alu", update_flops(cfg, B) / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
+        "table_build": ("hbm", (8 + 64) * int(w.inst_hashes.size) / 1e9, PEAK_HBM_GBS, "GB/s"),
     }
     dom = max((k for k in prof if k in roof), key=lambda k: prof[k][1])
     bound, work, peak, unit = roof[dom]

@@ -43,6 +43,7 @@ __device__ __forceinline__ float unit_block(const PairModel& M, const float* __r
     float acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = M.b2[jb + u];
+#pragma unroll 4
     for (int k = 0; k < M.h1; ++k) {
         float z = part_i[(int64_t)k * N];
         const float* __restrict__ w1 = M.w1 + (int64_t)k * M.d + M.d_inst;

@@ -69,11 +69,13 @@ __global__ void prepare_mfma_kernel(MfmaLayout L, const float* __restrict__ mast
             v = W2[(int64_t)(32 * mt2 + m) * h1 + perm_unit(s, h, j)];
         }
         frag16[t] = bf16_bits(v);
-    } else if (t < L.n16) {                              // head weights [s(h2/16)][h][j] : w3[perm(s,h,j)]
+    } else if (t < L.n16) {                              // head fragments [s(h2/16)][lane][j]: rows w3, |w3|
         const int64_t e = t - nfrag;
-        const int j = (int)(e & 7), h = (int)((e >> 3) & 1);
-        const int s = (int)(e >> 4);
-        frag16[t] = bf16_bits(W3[perm_unit(s, h, j)]);
+        const int j = (int)(e & 7), lane = (int)((e >> 3) & 63);
+        const int s = (int)(e >> 9);
+        const int m = lane & 31, h = lane >> 5;
+        const float w = W3[perm_unit(s, h, j)];
+        frag16[t] = bf16_bits(m == 0 ? w : m == 1 ? fabsf(w) : 0.0f);
     } else if (t < L.n16 + L.n32) {                      // bias fragments [mt][h][r] for b1 then b2
         const int64_t e = t - L.n16;
         const int r = (int)(e & 15), h = (int)((e >> 4) & 1);
@@ -122,7 +124,7 @@ hipError_t launch_instance_rows(const ModelDims& m, const float* mu, const float
 struct MfmaArgs {
     const bf16x8_t* __restrict__ w1frag;
     const bf16x8_t* __restrict__ w2frag;
-    const uint4* __restrict__ w3pk;
+    const bf16x8_t* __restrict__ hfrag;
     const float* __restrict__ b1frag;
     const float* __restrict__ b2frag;
     const float* __restrict__ b3;
@@ -150,18 +152,27 @@ __device__ __forceinline__ f32x16_t load_bias(const float* __restrict__ p) {
     return v;
 }
 
-// bf16(relu(.)) of accumulator registers 8q .. 8q+7 as one B operand
+// bf16(relu(.)) of accumulator registers 8q .. 8q+7 as one B operand.  Rounding
+// first and clamping the bf16 bit patterns at 0 as signed 16-bit integers is the
+// same as relu-then-round for every non-NaN input (negative values and -0 map
+// to +0), and takes one packed integer max per two values.
+typedef short s16x2_t __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ bf16x8_t relu_pack(const f32x16_t& acc, int q) {
-    bf16x8_t out;
+    uint32_t w[4];
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
         f32x2_t v;
-        v[0] = relu(acc[8 * q + 2 * jj]);
-        v[1] = relu(acc[8 * q + 2 * jj + 1]);
-        bf16x2_t p = __builtin_convertvector(v, bf16x2_t);
-        out[2 * jj] = p[0];
-        out[2 * jj + 1] = p[1];
+        v[0] = acc[8 * q + 2 * jj];
+        v[1] = acc[8 * q + 2 * jj + 1];
+        const bf16x2_t p = __builtin_convertvector(v, bf16x2_t);
+        s16x2_t si;
+        __builtin_memcpy(&si, &p, sizeof si);
+        si = __builtin_elementwise_max(si, s16x2_t{0, 0});
+        __builtin_memcpy(&w[jj], &si, sizeof si);
     }
+    bf16x8_t out;
+    __builtin_memcpy(&out, w, sizeof out);
     return out;
 }
 
@@ -188,9 +199,8 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     const int tiles_per_req = (A.N + 31) >> 5;
     const int64_t n_tiles = (int64_t)A.R * tiles_per_req;
     const float b3 = A.b3[0];
-    // head A operand: row 0 = w3, row 1 = |w3|, other rows zero
-    const uint32_t hmask = n == 0 ? 0xffffffffu : n == 1 ? 0x7fff7fffu : 0u;
-
+    const bf16x8_t* __restrict__ hf = A.hfrag + lane;
+    const bf16x8_t* __restrict__ w1l = lds_w1 + lane;
     for (int64_t tile = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6); tile < n_tiles;
          tile += (int64_t)gridDim.x * waves) {
         const int64_t r = tile / tiles_per_req;
@@ -227,12 +237,23 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             f32x16_t acc[MH];
 #pragma unroll
             for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b1frag + ((g + u) * 2 + h) * 16);
+            bf16x8_t a_cur[MH], a_nxt[MH];
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
+            for (int u = 0; u < MH; ++u) a_cur[u] = w1l[(g + u) * 64];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                if (s + 1 < 4) {
+#pragma unroll
+                    for (int u = 0; u < MH; ++u) a_nxt[u] = w1l[((s + 1) * MT1 + g + u) * 64];
+                }
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int u = 0; u < MH; ++u)
-                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_w1[(s * MT1 + g + u) * 64 + lane], xb[s],
-                                                                     acc[u], 0, 0, 0);
+                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[u], xb[s], acc[u], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int u = 0; u < MH; ++u) a_cur[u] = a_nxt[u];
+            }
 #pragma unroll
             for (int u = 0; u < MH; ++u) {
                 hb[2 * (g + u)] = relu_pack(acc[u], 0);
@@ -240,33 +261,51 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             }
         }
 
-        // layer 2 in passes, each pass fed straight into the head:
-        // head row 0 = t, row 1 = sum_j |w3_j| h2_j
-        f32x16_t hd = f32x16_t{};
-        hd[0] = h == 0 ? b3 : 0.0f;
+        // layer 2 in passes, each pass fed straight into the head (two
+        // accumulators to halve the dependent chain): row 0 = t, row 1 =
+        // sum_j |w3_j| h2_j
+        f32x16_t hd0 = f32x16_t{}, hd1 = f32x16_t{};
+        hd0[0] = h == 0 ? b3 : 0.0f;
 #pragma unroll
         for (int g = 0; g < MT2; g += MH) {
             f32x16_t acc[MH];
 #pragma unroll
             for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b2frag + ((g + u) * 2 + h) * 16);
+            // one pass spans MH * KS2 fragments (64 KB at h = 256): a per-pass base
+            // keeps every read within the 16-bit immediate offset of ds_read.  The
+            // empty asm hides the base's value from the optimiser, which would
+            // otherwise hoist one address register per far fragment out of the loop.
+            uint32_t pass_base = (uint32_t)(g * KS2 * 64);
+            asm volatile("" : "+s"(pass_base));
+            const bf16x8_t* __restrict__ w2g = lds_w2 + pass_base + lane;
+            // software pipeline: the next k-step's fragments are read from LDS
+            // while this k-step's MFMAs run (the barriers pin that order)
+            bf16x8_t a_cur[MH], a_nxt[MH];
 #pragma unroll
-            for (int s = 0; s < KS2; ++s)
+            for (int u = 0; u < MH; ++u) a_cur[u] = w2g[u * KS2 * 64];
+#pragma unroll
+            for (int s = 0; s < KS2; ++s) {
+                if (s + 1 < KS2) {
+#pragma unroll
+                    for (int u = 0; u < MH; ++u) a_nxt[u] = w2g[(u * KS2 + s + 1) * 64];
+                }
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int u = 0; u < MH; ++u)
-                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_w2[((g + u) * KS2 + s) * 64 + lane], hb[s],
-                                                                     acc[u], 0, 0, 0);
+                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[u], hb[s], acc[u], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int u = 0; u < MH; ++u)
+                for (int u = 0; u < MH; ++u) a_cur[u] = a_nxt[u];
+            }
 #pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    const int sh = 2 * (g + u) + q;
-                    const uint4 w = A.w3pk[sh * 2 + h];
-                    const uint4 wm = make_uint4(w.x & hmask, w.y & hmask, w.z & hmask, w.w & hmask);
-                    bf16x8_t a;
-                    __builtin_memcpy(&a, &wm, sizeof a);
-                    hd = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, relu_pack(acc[u], q), hd, 0, 0, 0);
-                }
+            for (int u = 0; u < MH; ++u) {
+                hd0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hf[(2 * (g + u)) * 64], relu_pack(acc[u], 0), hd0, 0, 0,
+                                                              0);
+                hd1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hf[(2 * (g + u) + 1) * 64], relu_pack(acc[u], 1), hd1, 0,
+                                                              0, 0);
+            }
         }
+        const f32x16_t hd = hd0 + hd1;
         if (h == 0 && valid) {
             const int64_t p = r * A.N + i;
             A.scores[p] = hd[0];
@@ -297,7 +336,7 @@ hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, c
     MfmaArgs a;
     a.w1frag = reinterpret_cast<const bf16x8_t*>(frag16);
     a.w2frag = reinterpret_cast<const bf16x8_t*>(frag16 + Lay.w1_frags * 512);
-    a.w3pk = reinterpret_cast<const uint4*>(frag16 + (Lay.w1_frags + Lay.w2_frags) * 512);
+    a.hfrag = reinterpret_cast<const bf16x8_t*>(frag16 + (Lay.w1_frags + Lay.w2_frags) * 512);
     a.b1frag = frag32;
     a.b2frag = frag32 + (m.h1 / 32) * 32;
     a.b3 = compute + m.c_b3;
@@ -330,46 +369,74 @@ hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, c
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool finite_f(float x) { return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u; }
 
-// One wave per request: U = min_i (t_i + E_i) over finite pairs; a pair is a
-// candidate if t_i - E_i <= U (or if t_i or E_i is not finite).
-__global__ __launch_bounds__(256) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
-                                                          const float* __restrict__ E, uint8_t* __restrict__ band,
-                                                          int64_t* __restrict__ list, uint32_t* __restrict__ count) {
-    const int lane = threadIdx.x & 63;
-    const int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-    if (r >= R) return;
-    const float* __restrict__ tr = t + r * N;
-    const float* __restrict__ er = E + r * N;
+// One wave per request, 16 requests per workgroup: U = min_i (t_i + E_i) over
+// finite pairs; a pair is a candidate if t_i - E_i <= U (or if t_i or E_i is
+// not finite).  Candidates are appended to one list with a single atomic per
+// workgroup.
+constexpr int kBandWaves = 16;
+
+__device__ __forceinline__ bool band_member(float ti, float ei, float U) {
+    return !(finite_f(ti) && finite_f(ei)) || (ti - ei <= U);
+}
+
+__global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
+                                                           const float* __restrict__ E, uint8_t* __restrict__ band,
+                                                           int64_t* __restrict__ list, uint32_t* __restrict__ count) {
+    __shared__ uint32_t wcount[kBandWaves];
+    __shared__ uint32_t wbase[kBandWaves];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t r = (int64_t)blockIdx.x * kBandWaves + wv;
+    const bool live = r < R;
+    const float* __restrict__ tr = t + (live ? r : 0) * N;
+    const float* __restrict__ er = E + (live ? r : 0) * N;
     float U = INFINITY;
-    for (int i = lane; i < N; i += 64) {
-        const float ti = tr[i], ei = er[i];
-        if (finite_f(ti) && finite_f(ei)) U = fminf(U, ti + ei);
-    }
+    uint32_t cnt = 0;
+    if (live) {
+        for (int i = lane; i < N; i += 64) {
+            const float ti = tr[i], ei = er[i];
+            if (finite_f(ti) && finite_f(ei)) U = fminf(U, ti + ei);
+        }
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) U = fminf(U, __shfl_xor(U, off));
-    U = U + fabsf(U) * 0x1p-20f;                    // absorbs the rounding of the sums above
+        for (int off = 32; off >= 1; off >>= 1) U = fminf(U, __shfl_xor(U, off));
+        U = U + fabsf(U) * 0x1p-20f;                // absorbs the rounding of the sums above
+        for (int i0 = 0; i0 < N; i0 += 64) {
+            const int i = i0 + lane;
+            bool in = false;
+            if (i < N) {
+                in = band_member(tr[i], er[i], U);
+                band[r * N + i] = in ? 1 : 0;
+            }
+            cnt += (uint32_t)__popcll(__ballot(in));
+        }
+    }
+    if (lane == 0) wcount[wv] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t total = 0;
+        for (int k = 0; k < kBandWaves; ++k) total += wcount[k];
+        uint32_t base = total ? atomicAdd(count, total) : 0u;
+        for (int k = 0; k < kBandWaves; ++k) {
+            wbase[k] = base;
+            base += wcount[k];
+        }
+    }
+    __syncthreads();
+    if (!live) return;
+    uint32_t base = wbase[wv];
     for (int i0 = 0; i0 < N; i0 += 64) {
         const int i = i0 + lane;
-        bool in = false;
-        if (i < N) {
-            const float ti = tr[i], ei = er[i];
-            in = !(finite_f(ti) && finite_f(ei)) || (ti - ei <= U);
-            band[r * N + i] = in ? 1 : 0;
-        }
+        const bool in = i < N && band_member(tr[i], er[i], U);
         const uint64_t m = __ballot(in);
-        if (m == 0) continue;
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(count, (uint32_t)__popcll(m));
-        base = __shfl(base, 0);
         if (in) list[base + __popcll(m & ((1ull << lane) - 1))] = r * N + i;
+        base += (uint32_t)__popcll(m);
     }
 }
 
 hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
                               uint32_t* count, hipStream_t s) {
     if (R <= 0) return hipSuccess;
-    hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + 3) / 4)), dim3(256), 0, s, R, N, t, E, band,
-                       list, count);
+    hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)),
+                       dim3(64 * kBandWaves), 0, s, R, N, t, E, band, list, count);
     return hipGetLastError();
 }
 

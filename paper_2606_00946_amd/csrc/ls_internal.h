@@ -61,8 +61,8 @@ struct ModelDims {
 ModelDims make_dims(const ls_model_config& cfg);
 
 // bf16 matrix-core path: fragment tables derived from the masters.
-// frag16 (bf16 bits): W1 [4][h1/32] fragments, W2 [h2/32][h1/16] fragments (a
-// fragment is 64 lanes x 8 bf16), then w3 as [h2/16][lane half][8].
+// frag16 (bf16 bits): W1 [4][h1/32] fragments, W2 [h2/32][h1/16] fragments and
+// head fragments [h2/16] (rows w3 and |w3|); a fragment is 64 lanes x 8 bf16.
 // frag32: b1 then b2 as [tile][lane half][16].
 struct MfmaLayout {
     int d = 0, h1 = 0, h2 = 0;
@@ -77,7 +77,7 @@ inline MfmaLayout make_mfma_layout(const ModelDims& m) {
     L.w1_frags = (int64_t)(m.h1 / 32) * 4;
     L.w2_frags = (int64_t)(m.h2 / 32) * (m.h1 / 16);
     L.h_frags = m.h2 / 16;
-    L.n16 = (L.w1_frags + L.w2_frags) * 512 + L.h_frags * 16;
+    L.n16 = (L.w1_frags + L.w2_frags + L.h_frags) * 512;
     L.n32 = (int64_t)(m.h1 / 32 + m.h2 / 32) * 32;
     return L;
 }
