@@ -66,18 +66,23 @@ __global__ void table_insert_kernel(uint64_t* __restrict__ keys, const int64_t* 
     uint32_t b = bucket_of(key, nb);
     for (uint32_t probe = 0; probe < nb; ++probe) {
         uint64_t* bk = table + (int64_t)b * kBucketKeys;
+        // read the whole bucket (one 64-byte line), then try its slots in order.
+        // A slot changes at most once (empty -> key), so a stale read can only
+        // show a filled slot as empty; the CAS on it then returns the key that
+        // holds it.  Each slot is tried at most once per bucket, so the loop ends.
+        const ulonglong2* q = reinterpret_cast<const ulonglong2*>(bk);
+        const ulonglong2 v0 = q[0], v1 = q[1], v2 = q[2], v3 = q[3];
+        const uint64_t slot[kBucketKeys] = {v0.x, v0.y, v1.x, v1.y, v2.x, v2.y, v3.x, v3.y};
+#pragma unroll
         for (int s = 0; s < kBucketKeys; ++s) {
-            // A slot changes at most once (empty -> key), so a stale "empty"
-            // read is settled by the CAS and a non-empty read is final.
-            uint64_t cur = bk[s];
-            if (cur == key) return;
-            if (cur == kEmptyKey) {
-                unsigned long long old = atomicCAS((unsigned long long*)(bk + s),
-                                                   (unsigned long long)kEmptyKey, (unsigned long long)key);
+            if (slot[s] == key) return;
+            if (slot[s] == kEmptyKey) {
+                const unsigned long long old = atomicCAS((unsigned long long*)(bk + s), (unsigned long long)kEmptyKey,
+                                                         (unsigned long long)key);
                 if (old == kEmptyKey || old == key) return;
             }
         }
-        b = (b + 1 == nb) ? 0 : b + 1;
+        b = (b + 1 == nb) ? 0 : b + 1;                 // bucket full without the key
     }
 }
 
