@@ -11,8 +11,18 @@ updates per second and per-kernel timings ride along.  Per-kernel durations
 come from HIP events recorded by the library on the stream of each call.
 
     python bench.py [--steps K] [--warmup W] [--config large_batch] [--no-cpu-baseline]
+                    [--copy-probe-mib M]
+
+--copy-probe-mib runs M MiB device-to-device copies after the timed region; a
+hardware-counter pass over the same command reads FETCH_SIZE / WRITE_SIZE of
+that plain copy beside the scorer's kernels, which calibrates the counters.
+"roofline.traffic" is filled from a committed counter record
+(profiles/traffic_<kind>_<workload>.md) only while the sources of that kernel
+still hash to the digest the record was taken at; otherwise it is null.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +41,51 @@ PEAK_BF16_TFLOPS = 2500.0
 # fp32 FMA on the vector ALUs without packed-fp32 instructions (disabled in this
 # build): 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
 PEAK_VALU_FP32_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+
+
+# Kernels behind each timed kind (names as rocprofv3 prints them) and the
+# sources they are compiled from.
+KIND_KERNELS = {
+    "score_pairs_mfma": (["ls::score_pairs_mfma_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
+    "table_build": (["ls::table_insert_kernel"], ["k_cache.hip", "ls_internal.h"]),
+    "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::prefix_leaders_kernel",
+                      "ls::prefix_followers_kernel"], ["k_prefix.hip", "ls_internal.h"]),
+    "rescore": (["ls::rescore_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
+}
+
+
+def sources_digest(kind):
+    h = hashlib.sha256()
+    for f in KIND_KERNELS[kind][1]:
+        with open(os.path.join(ROOT, "paper_2606_00946_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_record(kind, workload):
+    """HBM bytes per launch from a committed counter record, if it is current."""
+    if kind not in KIND_KERNELS:
+        return None
+    digest = sources_digest(kind)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("record: "):
+                    continue
+                rec = json.loads(line[len("record: "):])
+                if rec.get("kind") == kind and rec.get("workload") == workload and rec.get("digest") == digest:
+                    return rec
+    return None
+
+
+def copy_probe(mib):
+    import torch
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy probe: 3 x {mib} MiB device-to-device")
 
 
 def log(msg):
@@ -86,6 +141,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="large_batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the scorer shards by request with no collective, and this build "
@@ -140,7 +196,7 @@ def main():
 
     ms_step = (t1 - t0) * 1e3 / args.steps
     pairs_per_s = R * N / (ms_step / 1e3)
-    phases = {k: round(v[1] / v[0], 4) for k, v in prof.items()}
+    phases = {k: round(v[1] / args.steps, 4) for k, v in prof.items()}
 
     # algorithmic work of each kernel kind per launch
     n = np.diff(w.req_off)
@@ -159,6 +215,8 @@ def main():
     bound, work, peak, unit = roof[dom]
     avg_s = prof[dom][1] / prof[dom][0] / 1e3
     achieved = work / avg_s
+    rec = traffic_record(dom, cfg.name)
+    traffic = None if rec is None else round(rec["bytes_per_launch"] / 1e9, 4)
     result = {
         "metric": METRIC,
         "value": round(pairs_per_s, 1),
@@ -177,12 +235,15 @@ def main():
                    "predictor": f"{cfg.d}-{cfg.hidden[0]}-{cfg.hidden[1]}-1 {cfg.dtype}"},
         "updates_per_s": round(1e3 / ms_step, 3),
         "update_samples_per_s": round(B * 1e3 / ms_step, 1),
-        "kernel_ms": phases,
+        "kernel_ms_per_step": phases,
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1),
-                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": None},
+                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "traffic_unit": "GB per launch", "digest": sources_digest(dom) if dom in KIND_KERNELS else None},
         "useful_probes": probes,
     }
     ctx.close()
+    if args.copy_probe_mib > 0:
+        copy_probe(args.copy_probe_mib)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(w)
