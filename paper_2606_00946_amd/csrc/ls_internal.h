@@ -93,8 +93,15 @@ bool mfma_supported(const ModelDims& m);
 // ---------------------------------------------------------------------------
 hipError_t launch_fill_u64(uint64_t* p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t s);
-hipError_t launch_table_insert(const CacheTables& t, const int64_t* inst_off, const uint64_t* hashes,
-                               int64_t total, int32_t n_inst, hipStream_t s);
+// Table build: one workgroup per segment of kSegBuckets buckets (seg_off[i] is
+// the first segment of instance i, n_seg the total), then a global pass over
+// the keys that overflowed their segment.  ovf_ws holds a counter (first 256
+// bytes) and table_overflow_capacity(total) int64 key indices.
+constexpr uint32_t kSegBuckets = 2048;
+int64_t table_overflow_capacity(int64_t total);
+hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
+                              const uint64_t* hashes, int64_t total, int32_t n_inst, void* ovf_ws, int n_cu,
+                              hipStream_t s);
 
 // Group table for the prefix-sharing pass: a power of two >= 2R slots.
 inline int64_t group_table_size(int32_t R) {

@@ -34,6 +34,9 @@ struct ls_ctx {
     int64_t table_cap_buckets = 0;
     int32_t inst_cap = 0;
     int64_t* inst_off_dev = nullptr;
+    int32_t* seg_off_dev = nullptr;    // [N + 1] first table segment of each instance
+    void* tws = nullptr;               // table-build overflow queue
+    size_t tws_cap = 0;
     bool have_cache = false;
     // grow-only workspace
     void* ws = nullptr;
@@ -300,7 +303,7 @@ void ls_destroy(ls_ctx* c) {
         for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->frag16,
                         (void*)c->frag32, (void*)c->tables.keys,
                         (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
-                        (void*)c->inst_off_dev, c->ws})
+                        (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws})
             if (p) (void)hipFree(p);
         if (c->stage) (void)hipHostFree(c->stage);
         if (c->stage_done) (void)hipEventDestroy(c->stage_done);
@@ -375,11 +378,13 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
 
-    // bucket layout: about four keys per 8-slot bucket (half load)
+    // bucket layout: about four keys per 8-slot bucket (half load), built in
+    // segments of kSegBuckets buckets
     const int N = n_instances;
     std::vector<int64_t> base(N);
     std::vector<uint32_t> nb(N);
-    int64_t nbk = 0;
+    std::vector<int32_t> seg_off(N + 1);
+    int64_t nbk = 0, nseg = 0;
     for (int i = 0; i < N; ++i) {
         int64_t cnt = inst_off[i + 1] - inst_off[i];
         int64_t b = (cnt + 3) / 4;
@@ -388,22 +393,31 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
         base[i] = nbk;
         nb[i] = (uint32_t)b;
         nbk += b;
+        seg_off[i] = (int32_t)nseg;
+        nseg += (b + ls::kSegBuckets - 1) / ls::kSegBuckets;
+        if (nseg > 0x7fffffff) return fail(c, LS_ERR_UNSUPPORTED, "cache state too large");
     }
+    seg_off[N] = (int32_t)nseg;
     // device buffers
     size_t cap = (size_t)c->table_cap_buckets * ls::kBucketKeys * sizeof(uint64_t);
     int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t));
     if (rc) return rc;
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
+    rc = grow(c, &c->tws, &c->tws_cap, 256 + sizeof(int64_t) * (size_t)ls::table_overflow_capacity(total));
+    if (rc) return rc;
     if (N > c->inst_cap) {
         LS_HIP(c, hipDeviceSynchronize());
-        for (void* p : {(void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags, (void*)c->inst_off_dev})
+        for (void* p : {(void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags, (void*)c->inst_off_dev,
+                        (void*)c->seg_off_dev})
             if (p) LS_HIP(c, hipFree(p));
         c->tables.base = nullptr; c->tables.nbuckets = nullptr; c->tables.flags = nullptr; c->inst_off_dev = nullptr;
+        c->seg_off_dev = nullptr;
         c->inst_cap = 0;
         bool ok = hipMalloc((void**)&c->tables.base, sizeof(int64_t) * N) == hipSuccess &&
                   hipMalloc((void**)&c->tables.nbuckets, sizeof(uint32_t) * N) == hipSuccess &&
                   hipMalloc((void**)&c->tables.flags, sizeof(uint32_t) * N) == hipSuccess &&
-                  hipMalloc((void**)&c->inst_off_dev, sizeof(int64_t) * (N + 1)) == hipSuccess;
+                  hipMalloc((void**)&c->inst_off_dev, sizeof(int64_t) * (N + 1)) == hipSuccess &&
+                  hipMalloc((void**)&c->seg_off_dev, sizeof(int32_t) * (N + 1)) == hipSuccess;
         if (!ok) {
             (void)hipGetLastError();
             return fail(c, LS_ERR_NOMEM, "instance metadata allocation failed");
@@ -412,24 +426,27 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     }
     // metadata through pinned staging
     const size_t b_base = sizeof(int64_t) * N, b_nb = sizeof(uint32_t) * N, b_off = sizeof(int64_t) * (N + 1);
-    rc = stage_reserve(c, b_base + b_nb + b_off + 64);
+    const size_t o_off = (size_t)round_up((int64_t)(b_base + b_nb), 8), o_seg = o_off + b_off;
+    const size_t b_seg = sizeof(int32_t) * (N + 1);
+    rc = stage_reserve(c, o_seg + b_seg + 64);
     if (rc) return rc;
     char* st = (char*)c->stage;
     memcpy(st, base.data(), b_base);
     memcpy(st + b_base, nb.data(), b_nb);
-    memcpy(st + b_base + b_nb, inst_off, b_off);
+    memcpy(st + o_off, inst_off, b_off);
+    memcpy(st + o_seg, seg_off.data(), b_seg);
     LS_HIP(c, hipMemcpyAsync(c->tables.base, st, b_base, hipMemcpyHostToDevice, s));
     LS_HIP(c, hipMemcpyAsync(c->tables.nbuckets, st + b_base, b_nb, hipMemcpyHostToDevice, s));
-    LS_HIP(c, hipMemcpyAsync(c->inst_off_dev, st + b_base + b_nb, b_off, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->inst_off_dev, st + o_off, b_off, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->seg_off_dev, st + o_seg, b_seg, hipMemcpyHostToDevice, s));
     LS_HIP(c, hipEventRecord(c->stage_done, s));
     c->stage_pending = true;
     c->tables.n = N;
     // build
     {
         Timed t(c, K_TABLE, s);
-        hipError_t e = ls::launch_fill_u64(c->tables.keys, ls::kEmptyKey, nbk * ls::kBucketKeys, s);
-        if (e == hipSuccess) e = ls::launch_fill_u32(c->tables.flags, 0u, N, s);
-        if (e == hipSuccess) e = ls::launch_table_insert(c->tables, c->inst_off_dev, hashes, total, N, s);
+        hipError_t e = ls::launch_table_build(c->tables, c->inst_off_dev, c->seg_off_dev, (int32_t)nseg, hashes, total,
+                                              N, c->tws, c->n_cu, s);
         t.done();
         LS_HIP(c, e);
     }

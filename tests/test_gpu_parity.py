@@ -263,6 +263,81 @@ def test_adversarial_overlaps_and_features(dtype):
     check_scoring(w, out, np.arange(R, dtype=np.int32))
 
 
+_PHI = 0x9E3779B97F4A7C15
+_PHI_INV = pow(_PHI, -1, 1 << 64)
+
+
+def _bucket(key, nb):
+    """Home bucket of a key in a table of nb buckets (the library's bucket rule)."""
+    return (((key * _PHI) % (1 << 64) >> 32) * nb) >> 32
+
+
+def _keys_homed_at(rng, b, nb, count):
+    """Distinct keys whose home bucket in a table of nb buckets is b."""
+    lo = -(-(b << 32) // nb)
+    hi = -(-((b + 1) << 32) // nb)
+    out = set()
+    while len(out) < count:
+        h = (int(rng.integers(lo, hi)) << 32) | int(rng.integers(0, 1 << 32))
+        k = (h * _PHI_INV) % (1 << 64)
+        assert _bucket(k, nb) == b
+        if k != (1 << 64) - 1:
+            out.add(k)
+    return sorted(out)
+
+
+@pytest.mark.parametrize("case", ["queued", "requeue_all"])
+def test_table_overflow_paths(case):
+    """Keys piled onto the last bucket of a table segment and of the whole table
+    overflow the segment being built; the build must still place every key where
+    a lookup finds it, through the overflow queue or, when more keys overflow
+    than the queue holds, through re-insertion of every key."""
+    note(f"table overflow {case}")
+    rng = np.random.default_rng(11)
+    seg = 2048
+    if case == "queued":
+        cnt = 12000                          # 3000 buckets: segments of 2048 and 952
+        nb = (cnt + 3) // 4
+        at_seg_end = _keys_homed_at(rng, seg - 1, nb, 60)
+        at_tab_end = _keys_homed_at(rng, nb - 1, nb, 60)
+        rest = [int(x) for x in rng.integers(0, 1 << 63, cnt - 120)]
+        big = rest[:5000] + at_seg_end + rest[5000:] + at_tab_end
+        piles = [at_seg_end, at_tab_end]
+    else:
+        cnt = 20000                          # every key homed at the last bucket of segment 0
+        nb = (cnt + 3) // 4
+        pile = _keys_homed_at(rng, seg - 1, nb, cnt)
+        big = list(pile)
+        piles = [pile[:300], pile[-300:]]
+    caches = [big, big[:7000], [int(x) for x in rng.integers(0, 1 << 63, 50)]]
+    absent = [_keys_homed_at(np.random.default_rng(99), seg - 1, nb, 2)[0],
+              _keys_homed_at(np.random.default_rng(98), nb - 1, nb, 2)[0]]
+    absent = [k for k in absent if k not in set(big)]
+    reqs = []
+    for p in piles:
+        reqs.append(p)                       # a run made of overflowed keys only
+        reqs.append(p[:25] + absent[:1] + p[25:40])
+        reqs.append(list(reversed(p[:50])))
+    reqs.append(big[:200])
+    reqs.append(big[4990:5100])
+    reqs.append(absent + big[:10])
+    inst_off, inst_h = oracle_pins._csr(caches)
+    req_off, req_h = oracle_pins._csr(reqs)
+    L = np.array([16 * len(r) + 3 for r in reqs], np.int32)
+    base = workload("tiny")
+    N, R, d = len(caches), len(reqs), base.cfg.d
+    w = synth.Workload(cfg=synth.dataclasses.replace(base.cfg, R=R, N=N), req_off=req_off, req_hashes=req_h,
+                       prompt_len=L, req_group=np.zeros(R, np.int32), inst_off=inst_off, inst_hashes=inst_h,
+                       inst_feat=np.random.default_rng(5).uniform(0, 4, (N, d - 5)).astype(np.float32),
+                       params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
+                       upd_ttft=base.upd_ttft, lr=base.lr)
+    out = GpuRun(w).score()
+    want = oracle.overlap(req_off, req_h, inst_off, inst_h)
+    np.testing.assert_array_equal(out["overlap"], want)
+    assert out["overlap"][0, 0] == len(piles[0])
+    check_scoring(w, out, np.arange(R, dtype=np.int32))
+
+
 def test_ties_go_to_lowest_instance():
     """Instances with identical state and cache score identically; the lowest id wins."""
     note("exact ties")
