@@ -37,6 +37,25 @@ struct UpdWs {
     int loss_blocks;
 };
 
+constexpr int kWgradChunk = 512;     // samples per split-K chunk (multiple of 16)
+constexpr int kWgradMaxChunks = 256;
+
+struct WgradPlan {
+    int S;
+    int64_t chunk;
+};
+
+static WgradPlan wgrad_plan(int32_t B) {
+    int64_t S = ((int64_t)B + kWgradChunk - 1) / kWgradChunk;
+    if (S < 1) S = 1;
+    if (S > kWgradMaxChunks) S = kWgradMaxChunks;
+    int64_t chunk = ((int64_t)B + S - 1) / S;
+    chunk = (chunk + 15) & ~int64_t(15);
+    S = ((int64_t)B + chunk - 1) / chunk;
+    if (S < 1) S = 1;
+    return {(int)S, chunk};
+}
+
 static int64_t align_floats(int64_t n) { return (n + 63) & ~int64_t(63); }
 
 static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
@@ -51,9 +70,14 @@ static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
     w.chunk = chunk;
     w.loss_blocks = (int)blocks_for(B, 256);
     int64_t maxmn = std::max<int64_t>({(int64_t)m.h2 * m.h1, (int64_t)m.h1 * m.d, (int64_t)m.h2});
+    // the matrix-core weight gradients keep one more column (the bias) per partial
+    const WgradPlan mp = wgrad_plan(B);
+    const int64_t maxmn1 = std::max<int64_t>({(int64_t)m.h2 * (m.h1 + 1), (int64_t)m.h1 * (m.d + 1),
+                                              (int64_t)m.h2 + 1});
+    const int64_t part_floats = std::max<int64_t>((int64_t)S * maxmn, (int64_t)mp.S * maxmn1);
     int64_t sizes[] = {(int64_t)m.d * B, (int64_t)m.h1 * B, (int64_t)m.h1 * B, (int64_t)m.h2 * B,
                        (int64_t)m.h2 * B, (int64_t)B, (int64_t)B, (int64_t)m.h2 * B, (int64_t)m.h1 * B,
-                       m.n_params, (int64_t)S * maxmn, (int64_t)w.loss_blocks};
+                       m.n_params, part_floats, (int64_t)w.loss_blocks};
     float** slots[] = {&w.xn, &w.z1, &w.a1, &w.z2, &w.a2, &w.t, &w.g, &w.d2, &w.d1, &w.grad, &w.part, &w.loss_part};
     int64_t off = 0;
     for (int k = 0; k < 12; ++k) {
@@ -79,6 +103,9 @@ __global__ void normalize_kernel(const float* __restrict__ feats, const float* _
     xn[t] = BF ? q_bf16(v) : v;
 }
 
+// U consecutive output units of one sample: each is the fma chain from its bias
+// over the inputs in ascending order.  Inputs are fetched eight at a time ahead
+// of their multiply-adds; the order of every chain is unchanged.
 template <bool BF, bool RELU, int U>
 __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const float* __restrict__ wt,
                                           const float* __restrict__ bias, float* __restrict__ z,
@@ -87,8 +114,20 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
     float acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = bias[jb + u];
-    for (int k = 0; k < K; ++k) {
-        float x = in[(int64_t)k * B + b];
+    int k = 0;
+    for (; k + 8 <= K; k += 8) {
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = in[(int64_t)(k + e) * B + b];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float* __restrict__ w = wt + (int64_t)(k + e) * O + jb;
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[u] = __builtin_fmaf(w[u], x[e], acc[u]);
+        }
+    }
+    for (; k < K; ++k) {
+        const float x = in[(int64_t)k * B + b];
         const float* __restrict__ w = wt + (int64_t)k * O + jb;
 #pragma unroll
         for (int u = 0; u < U; ++u) acc[u] = __builtin_fmaf(w[u], x, acc[u]);
@@ -104,7 +143,9 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
     }
 }
 
-// One layer for every sample: lane = sample, weights uniform across the wave.
+// One layer: lane = sample, blockIdx.y = a block of 32 output units (weights
+// are uniform across the wave), so a layer runs as (B / 256) x (O / 32)
+// workgroups.
 template <bool BF, bool RELU>
 __global__ __launch_bounds__(256) void layer_fwd_kernel(const float* __restrict__ in, const float* __restrict__ wt,
                                                         const float* __restrict__ bias, float* __restrict__ z,
@@ -112,13 +153,14 @@ __global__ __launch_bounds__(256) void layer_fwd_kernel(const float* __restrict_
     int64_t bt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     bool valid = bt < B;
     int64_t b = valid ? bt : 0;
-    int jb = 0;
-    for (; jb + 32 <= O; jb += 32) fwd_units<BF, RELU, 32>(in, wt, bias, z, a, B, K, O, jb, b, valid);
-    if (jb + 16 <= O) { fwd_units<BF, RELU, 16>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 16; }
-    if (jb + 8 <= O) { fwd_units<BF, RELU, 8>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 8; }
-    if (jb + 4 <= O) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 4; }
-    if (jb + 2 <= O) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 2; }
-    if (jb + 1 <= O) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 1; }
+    int jb = blockIdx.y * 32;
+    const int rem = O - jb;
+    if (rem >= 32) { fwd_units<BF, RELU, 32>(in, wt, bias, z, a, B, K, O, jb, b, valid); return; }
+    if (rem & 16) { fwd_units<BF, RELU, 16>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 16; }
+    if (rem & 8) { fwd_units<BF, RELU, 8>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 8; }
+    if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 4; }
+    if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 2; }
+    if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 1; }
 }
 
 // ---------------------------------------------------------------------------
@@ -222,6 +264,142 @@ __global__ __launch_bounds__(256) void gemm_nt_splitk_kernel(const float* __rest
             if (n < N) out[(int64_t)m * N + n] = acc[i][j];
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 mode: weight and bias gradients on the matrix cores.
+// C[m][n] = sum_b A[m][b] Bt[n][b] for n < N and C[m][N] = sum_b A[m][b], as
+// v_mfma_f32_32x32x16_bf16 with m-tiles as rows, samples as the reduction and
+// n-tiles as columns; the bias column comes from one more B operand of ones.
+// Every operand is a bf16 value already (layer inputs, output gradients), so
+// the products are exact and the sums fp32, as in the VALU path.  Lane l of a
+// fragment holds 8 consecutive samples of row l % 32 (samples 8 (l / 32) ..),
+// which is exactly 32 contiguous bytes of the feature-major arrays, so the
+// operands stream from memory without staging.  Split-K: workgroup s covers a
+// fixed chunk of samples; partials are summed in ascending s afterwards.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ bf16x8_t pack_bf16x8(const float (&v)[8]) {
+    // the values are bf16 numbers stored as fp32: the upper halves are exact
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = (__float_as_uint(v[2 * j]) >> 16) | (__float_as_uint(v[2 * j + 1]) & 0xFFFF0000u);
+    bf16x8_t out;
+    __builtin_memcpy(&out, w, sizeof out);
+    return out;
+}
+
+template <bool VEC>
+__device__ __forceinline__ bf16x8_t load_frag(const float* __restrict__ row, int64_t k, int64_t ke, bool valid) {
+    float v[8];
+    if (VEC && valid && k + 8 <= ke) {
+        const float4 p = *reinterpret_cast<const float4*>(row + k);
+        const float4 q = *reinterpret_cast<const float4*>(row + k + 4);
+        v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w; v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (valid && k + j < ke) ? row[k + j] : 0.0f;
+    }
+    return pack_bf16x8(v);
+}
+
+template <int NT, bool VEC>
+__global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
+                                                         float* __restrict__ part, int M, int N, int32_t B,
+                                                         int64_t chunk) {
+    const int lane = threadIdx.x & 63, mt = threadIdx.x >> 6;
+    const int row = lane & 31, half = lane >> 5;
+    const int s = blockIdx.x;
+    const int64_t kb = (int64_t)s * chunk;
+    const int64_t ke = min(kb + chunk, (int64_t)B);
+    const int m = mt * 32 + row;
+    const bool mvalid = m < M;
+    const float* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
+    const float* __restrict__ brow[NT];
+    bool nvalid[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int n = t * 32 + row;
+        nvalid[t] = n < N;
+        brow[t] = Bt + (int64_t)(nvalid[t] ? n : 0) * B;
+    }
+    bf16x8_t ones;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ones[j] = (__bf16)1.0f;
+    f32x16_t acc[NT + 1];
+#pragma unroll
+    for (int t = 0; t <= NT; ++t) acc[t] = f32x16_t{};
+    for (int64_t k0 = kb; k0 < ke; k0 += 16) {
+        const int64_t k = k0 + 8 * half;
+        const bf16x8_t a = load_frag<VEC>(arow, k, ke, mvalid);
+        bf16x8_t bb[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) bb[t] = load_frag<VEC>(brow[t], k, ke, nvalid[t]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb[t], acc[t], 0, 0, 0);
+        acc[NT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ones, acc[NT], 0, 0, 0);
+    }
+    // accumulator register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+    const int64_t ld = N + 1;
+    float* __restrict__ out = part + (int64_t)s * M * ld;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int mm = mt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (mm >= M) continue;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int nn = t * 32 + row;
+            if (nn < N) out[(int64_t)mm * ld + nn] = acc[t][r];
+        }
+        if (row == 0) out[(int64_t)mm * ld + N] = acc[NT][r];
+    }
+}
+
+// grad_w[m][n] (n < N) and grad_b[m] from the partials, summed over s ascending
+__global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M, int N, float* __restrict__ gw,
+                                    float* __restrict__ gb) {
+    const int64_t ld = N + 1, MN = (int64_t)M * ld;
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= MN) return;
+    float acc = 0.0f;
+    for (int s = 0; s < S; ++s) acc += part[(int64_t)s * MN + e];
+    const int64_t mm = e / ld, nn = e - mm * ld;
+    if (nn < N) gw[mm * N + nn] = acc;
+    else gb[mm] = acc;
+}
+
+template <int NT>
+static void launch_wgrad_nt(const float* A, const float* Bt, float* part, int M, int N, int32_t B, int S,
+                            int64_t chunk, hipStream_t s) {
+    const dim3 block(64 * ((M + 31) / 32));
+    if (B % 4 == 0)
+        hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), dim3(S), block, 0, s, A, Bt, part, M, N, B, chunk);
+    else
+        hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), dim3(S), block, 0, s, A, Bt, part, M, N, B, chunk);
+}
+
+// dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.
+static hipError_t weight_grad_mfma(const float* A, const float* Bt, int M, int N, int32_t B, float* part,
+                                   float* gw, float* gb, hipStream_t s) {
+    const WgradPlan p = wgrad_plan(B);
+    switch ((N + 31) / 32) {
+        case 1: launch_wgrad_nt<1>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 2: launch_wgrad_nt<2>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 3: launch_wgrad_nt<3>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 4: launch_wgrad_nt<4>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 5: launch_wgrad_nt<5>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 6: launch_wgrad_nt<6>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 7: launch_wgrad_nt<7>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        case 8: launch_wgrad_nt<8>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+        default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t MN = (int64_t)M * (N + 1);
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks_for(MN, 256)), dim3(256), 0, s, part, p.S, M, N, gw, gb);
+    return hipGetLastError();
 }
 
 // out[e] = sum over s ascending of part[s][e]
@@ -328,32 +506,48 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     // forward, saving pre-activations and activations
     hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, w.xn,
                        B, m.d);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(blocks_for(nB, 256)), dim3(256), 0, s, w.xn,
+    const uint32_t sb = blocks_for(nB, 256);
+    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
                        compute + m.c_w1t, compute + m.c_b1, w.z1, w.a1, B, m.d, m.h1);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(blocks_for(nB, 256)), dim3(256), 0, s, w.a1,
+    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
                        compute + m.c_w2t, compute + m.c_b2, w.z2, w.a2, B, m.h1, m.h2);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(blocks_for(nB, 256)), dim3(256), 0, s, w.a2,
+    hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, w.a2,
                        compute + m.c_w3, compute + m.c_b3, w.t, nullptr, B, m.h2, 1);
     // loss and output gradient
     hipLaunchKernelGGL(loss_grad_kernel<BF>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
     if (loss_out)
         hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, s, w.loss_part, w.loss_blocks, B, loss_out);
+    // bf16 operands: weight and bias gradients on the matrix cores
+    const bool mf = BF && m.h1 <= 256 && m.h2 <= 256 && m.d <= 256;
+    hipError_t e;
     // head layer
-    hipError_t e = weight_grad(w.g, w.a2, 1, m.h2, B, w, w.grad + m.m_w3, s);
+    if (mf) {
+        e = weight_grad_mfma(w.g, w.a2, 1, m.h2, B, w.part, w.grad + m.m_w3, w.grad + m.m_b3, s);
+    } else {
+        e = weight_grad(w.g, w.a2, 1, m.h2, B, w, w.grad + m.m_w3, s);
+        hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b3);
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b3);
     // second hidden layer
     hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB * m.h2, 256)), dim3(256), 0, s, w.g,
                        compute + m.c_w3, w.z2, w.d2, B, m.h2);
-    e = weight_grad(w.d2, w.a1, m.h2, m.h1, B, w, w.grad + m.m_w2, s);
+    if (mf) {
+        e = weight_grad_mfma(w.d2, w.a1, m.h2, m.h1, B, w.part, w.grad + m.m_w2, w.grad + m.m_b2, s);
+    } else {
+        e = weight_grad(w.d2, w.a1, m.h2, m.h1, B, w, w.grad + m.m_w2, s);
+        hipLaunchKernelGGL(rowsum_kernel, dim3(m.h2), dim3(256), 0, s, w.d2, B, w.grad + m.m_b2);
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(rowsum_kernel, dim3(m.h2), dim3(256), 0, s, w.d2, B, w.grad + m.m_b2);
     // first hidden layer
     hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (m.h1 + 63) / 64), dim3(256), 0, s,
                        compute + m.c_w2t, w.d2, w.z1, w.d1, m.h1, m.h2, B);
-    e = weight_grad(w.d1, w.xn, m.h1, m.d, B, w, w.grad + m.m_w1, s);
+    if (mf) {
+        e = weight_grad_mfma(w.d1, w.xn, m.h1, m.d, B, w.part, w.grad + m.m_w1, w.grad + m.m_b1, s);
+    } else {
+        e = weight_grad(w.d1, w.xn, m.h1, m.d, B, w, w.grad + m.m_w1, s);
+        hipLaunchKernelGGL(rowsum_kernel, dim3(m.h1), dim3(256), 0, s, w.d1, B, w.grad + m.m_b1);
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(rowsum_kernel, dim3(m.h1), dim3(256), 0, s, w.d1, B, w.grad + m.m_b1);
     // step and refresh the compute copy
     hipLaunchKernelGGL(sgd_kernel, dim3(blocks_for(m.n_params, 256)), dim3(256), 0, s, master, w.grad, lr,
                        m.n_params, grad_out);

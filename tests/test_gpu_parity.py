@@ -133,35 +133,52 @@ def test_bf16_exact_mode_matches_oracle_bitwise():
     run.ctx.close()
 
 
-@pytest.mark.parametrize("name", CONFIGS)
-def test_update_parity(name):
-    w = workload(name)
-    note(f"update parity {name} B={w.cfg.update_batch}")
+def _check_update(w, feats=None, ttft=None):
+    """One SGD step through the C ABI against the oracle's, per parameter tensor."""
+    feats = w.upd_feats if feats is None else feats
+    ttft = w.upd_ttft if ttft is None else ttft
     run = GpuRun(w)
-    got = run.update()
+    got = run.update(feats, ttft)
     # ReLU masks are decided in the kernel's precision on both sides (the oracle's
     # forward runs the same fp32 chains); the backward sums are double in the oracle
     mode = mode_of(w)
-    ref = oracle.update(mode, w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.upd_feats, w.upd_ttft, w.lr)
+    ref = oracle.update(mode, w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, feats, ttft, w.lr)
     assert abs(got["loss"] - ref["loss"]) <= 1e-5 * abs(ref["loss"]), (got["loss"], ref["loss"])
     if mode == "fp32":
         # against the double-precision definition only masks of pre-activations
         # within rounding of zero can differ
-        ref64 = oracle.update("f64", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.upd_feats, w.upd_ttft,
-                              w.lr)
+        ref64 = oracle.update("f64", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, feats, ttft, w.lr)
         assert np.linalg.norm(got["grad"] - ref64["grad"]) <= 1e-3 * np.linalg.norm(ref64["grad"])
+    report = []
     for lname, a, b in layer_slices(w.cfg.d, w.cfg.hidden):
         g, r = got["grad"][a:b], ref["grad"][a:b]
         nrm = np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)
         assert nrm <= 1e-4, f"{lname}: norm-wise relative gradient error {nrm}"
         ok, worst = rel_ok(g, r, 1e-4)
         assert ok, f"{lname}: elementwise gradient error {worst}"
+        report.append(f"{lname} {worst:.1e}")
         # the step: W' - W against the oracle's, allowing one ulp of W' for the final rounding
         dg = got["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
         dr = ref["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
         ulp = np.spacing(np.abs(ref["params"][a:b])).astype(np.float64)
         assert np.all(np.abs(dg - dr) <= 1e-4 * np.abs(dr) + ulp), lname
+    print(f"update B={feats.shape[0]} worst elementwise gradient error: " + ", ".join(report), flush=True)
     run.ctx.close()
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_update_parity(name):
+    w = workload(name)
+    note(f"update parity {name} B={w.cfg.update_batch}")
+    _check_update(w)
+
+
+@pytest.mark.parametrize("B", [77, 1030, 1032])
+def test_update_parity_bf16_ragged_batch(B):
+    """bf16 update at batch sizes that leave a ragged split-K chunk, aligned and not."""
+    w = workload("large_batch")
+    note(f"bf16 update ragged B={B}")
+    _check_update(w, w.upd_feats[:B], w.upd_ttft[:B])
 
 
 def _golden_model(dtype):
