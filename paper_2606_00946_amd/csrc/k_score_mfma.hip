@@ -461,12 +461,148 @@ __global__ __launch_bounds__(256) void rescore_kernel(PairModel M, const float* 
     }
 }
 
+// Same scores, one wave per listed pair (bf16 model, h1 = h2 = H): lanes own
+// output units, W2 sits in LDS as bf16 bits, the pair's layer-1 activations
+// and then its layer-2 outputs pass through a per-wave LDS row, and lane 0
+// runs the head chain.  Every chain keeps the canonical order (bias first,
+// inputs ascending), so each score is bitwise the one-lane-per-pair value.
+struct RescoreArgs {
+    const float* __restrict__ w1;     // [H x d] compute copy
+    const float* __restrict__ w2t;    // [H x H] W2T[k][j]
+    const float* __restrict__ b2;
+    const float* __restrict__ w3;
+    const float* __restrict__ b3;
+    const float* __restrict__ mu;
+    const float* __restrict__ isig;
+    const float* __restrict__ part_t;  // [H x N]
+    const int64_t* __restrict__ req_off;
+    const int32_t* __restrict__ prompt_len;
+    const int32_t* __restrict__ overlap;
+    const int64_t* __restrict__ list;
+    const uint32_t* __restrict__ count;
+    float* __restrict__ scores;
+    int32_t N;
+    int d, d_inst, block_tokens;
+};
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Each wave scores two pairs at once, so every weight it converts from bf16
+// serves two chains and the two head chains run side by side.
+constexpr int kRescoreWaves = 12;
+constexpr int kRescorePairs = 2;
+
+template <int H>
+__global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(RescoreArgs A) {
+    constexpr int U = H / 64;                  // units per lane
+    constexpr int P = kRescorePairs;
+    __shared__ uint16_t lds_w2[H * H];
+    __shared__ float lds_w3[H];
+    __shared__ __align__(16) float lds_row[kRescoreWaves][P][H];
+    for (int e = threadIdx.x; e < H * H; e += 64 * kRescoreWaves) lds_w2[e] = (uint16_t)(__float_as_uint(A.w2t[e]) >> 16);
+    for (int e = threadIdx.x; e < H; e += 64 * kRescoreWaves) lds_w3[e] = A.w3[e];
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    float w1c[U][5], b2v[U];
+#pragma unroll
+    for (int v = 0; v < U; ++v) {
+#pragma unroll
+        for (int c = 0; c < 5; ++c) w1c[v][c] = A.w1[(int64_t)(lane + 64 * v) * A.d + A.d_inst + c];
+        b2v[v] = A.b2[U * lane + v];
+    }
+    const float b3 = A.b3[0];
+    const int64_t cnt = *A.count;
+    for (int64_t q = ((int64_t)blockIdx.x * kRescoreWaves + wave) * P; q < cnt;
+         q += (int64_t)gridDim.x * kRescoreWaves * P) {
+        int64_t pp[P];
+#pragma unroll
+        for (int e = 0; e < P; ++e) pp[e] = A.list[q + e < cnt ? q + e : q];
+        // layer 1, resumed from the instance partial: unit lane + 64 v
+#pragma unroll
+        for (int e = 0; e < P; ++e) {
+            const int64_t r = pp[e] / A.N, i = pp[e] - r * A.N;
+            float x[5], xt[5];
+            derived_columns(A.prompt_len[r], A.req_off[r + 1] - A.req_off[r], A.overlap[pp[e]], A.block_tokens, x);
+            normalise_tail<true>(x, A.mu, A.isig, A.d_inst, xt);
+#pragma unroll
+            for (int v = 0; v < U; ++v) {
+                const int k = lane + 64 * v;
+                float z = A.part_t[(int64_t)k * A.N + i];
+#pragma unroll
+                for (int c = 0; c < 5; ++c) z = __builtin_fmaf(w1c[v][c], xt[c], z);
+                lds_row[wave][e][k] = bf16_rne_num(relu(z));
+            }
+        }
+        wave_sync();
+        // layer 2: units U lane .. U lane + U - 1
+        float acc[P][U];
+#pragma unroll
+        for (int e = 0; e < P; ++e)
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[e][u] = b2v[u];
+        for (int k = 0; k < H; k += 4) {
+            float av[P][4];
+#pragma unroll
+            for (int e = 0; e < P; ++e) {
+                const float4 a4 = *reinterpret_cast<const float4*>(&lds_row[wave][e][k]);
+                av[e][0] = a4.x; av[e][1] = a4.y; av[e][2] = a4.z; av[e][3] = a4.w;
+            }
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const uint16_t* wr = lds_w2 + (k + kk) * H + U * lane;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const float wv = __uint_as_float((uint32_t)wr[u] << 16);
+#pragma unroll
+                    for (int e = 0; e < P; ++e) acc[e][u] = __builtin_fmaf(wv, av[e][kk], acc[e][u]);
+                }
+            }
+        }
+        wave_sync();
+#pragma unroll
+        for (int e = 0; e < P; ++e)
+#pragma unroll
+            for (int u = 0; u < U; ++u) lds_row[wave][e][U * lane + u] = bf16_rne_num(relu(acc[e][u]));
+        wave_sync();
+        if (lane < P && q + lane < cnt) {
+            const float* hrow = lds_row[wave][lane];
+            float t = b3;
+            for (int j = 0; j < H; j += 4) {
+                const float4 h4 = *reinterpret_cast<const float4*>(hrow + j);
+                t = __builtin_fmaf(lds_w3[j], h4.x, t);
+                t = __builtin_fmaf(lds_w3[j + 1], h4.y, t);
+                t = __builtin_fmaf(lds_w3[j + 2], h4.z, t);
+                t = __builtin_fmaf(lds_w3[j + 3], h4.w, t);
+            }
+            A.scores[pp[lane]] = t;
+        }
+        wave_sync();
+    }
+}
+
 hipError_t launch_rescore(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
                           const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
                           const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
                           const uint32_t* count, float* scores, int n_cu, hipStream_t s) {
     PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
                 m.d, m.d_inst, m.h1, m.h2};
+    if (m.bf16 && m.h1 == m.h2 && (m.h1 == 64 || m.h1 == 128 || m.h1 == 256)) {
+        RescoreArgs A{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
+                      mu, inv_sigma, part_t, req_off, prompt_len, overlap, list, count, scores, N, m.d, m.d_inst,
+                      m.block_tokens};
+        const dim3 grid((uint32_t)n_cu), block(64 * kRescoreWaves);
+        switch (m.h1) {
+            case 64: hipLaunchKernelGGL(rescore_wave_kernel<64>, grid, block, 0, s, A); break;
+            case 128: hipLaunchKernelGGL(rescore_wave_kernel<128>, grid, block, 0, s, A); break;
+            default: hipLaunchKernelGGL(rescore_wave_kernel<256>, grid, block, 0, s, A); break;
+        }
+        return hipGetLastError();
+    }
+    // enough lanes for about two candidates per request, capped at 8 waves per SIMD
     // enough lanes for about two candidates per request, capped at 8 waves per SIMD
     int64_t want = ((int64_t)R * 2 + 255) / 256;
     int64_t cap = (int64_t)n_cu * 8;
