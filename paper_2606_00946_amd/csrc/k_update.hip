@@ -45,12 +45,15 @@ struct WgradPlan {
     int64_t chunk;
 };
 
-static WgradPlan wgrad_plan(int32_t B) {
-    int64_t S = ((int64_t)B + kWgradChunk - 1) / kWgradChunk;
+// Chunks of 512 samples (of 64 for a single m-tile, whose partials are tiny).
+static WgradPlan wgrad_plan(int32_t B, int M) {
+    const int64_t c0 = M <= 32 ? 64 : kWgradChunk;
+    const int64_t cap = M <= 32 ? 4 * kWgradMaxChunks : kWgradMaxChunks;
+    int64_t S = ((int64_t)B + c0 - 1) / c0;
     if (S < 1) S = 1;
-    if (S > kWgradMaxChunks) S = kWgradMaxChunks;
+    if (S > cap) S = cap;
     int64_t chunk = ((int64_t)B + S - 1) / S;
-    chunk = (chunk + 15) & ~int64_t(15);
+    chunk = (chunk + 63) & ~int64_t(63);
     S = ((int64_t)B + chunk - 1) / chunk;
     if (S < 1) S = 1;
     return {(int)S, chunk};
@@ -71,10 +74,10 @@ static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
     w.loss_blocks = (int)blocks_for(B, 256);
     int64_t maxmn = std::max<int64_t>({(int64_t)m.h2 * m.h1, (int64_t)m.h1 * m.d, (int64_t)m.h2});
     // the matrix-core weight gradients keep one more column (the bias) per partial
-    const WgradPlan mp = wgrad_plan(B);
-    const int64_t maxmn1 = std::max<int64_t>({(int64_t)m.h2 * (m.h1 + 1), (int64_t)m.h1 * (m.d + 1),
-                                              (int64_t)m.h2 + 1});
-    const int64_t part_floats = std::max<int64_t>((int64_t)S * maxmn, (int64_t)mp.S * maxmn1);
+    const int64_t mfma_floats = std::max<int64_t>({(int64_t)wgrad_plan(B, m.h2).S * m.h2 * (m.h1 + 1),
+                                                   (int64_t)wgrad_plan(B, m.h1).S * m.h1 * (m.d + 1),
+                                                   (int64_t)wgrad_plan(B, 1).S * (m.h2 + 1)});
+    const int64_t part_floats = std::max<int64_t>((int64_t)S * maxmn, mfma_floats);
     int64_t sizes[] = {(int64_t)m.d * B, (int64_t)m.h1 * B, (int64_t)m.h1 * B, (int64_t)m.h2 * B,
                        (int64_t)m.h2 * B, (int64_t)B, (int64_t)B, (int64_t)m.h2 * B, (int64_t)m.h1 * B,
                        m.n_params, part_floats, (int64_t)w.loss_blocks};
@@ -161,6 +164,120 @@ __global__ __launch_bounds__(256) void layer_fwd_kernel(const float* __restrict_
     if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 4; }
     if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 2; }
     if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 1; }
+}
+
+// The same chains with the weights of the workgroup's 32 output units staged
+// in LDS (wl[k][u], read as broadcasts) instead of fetched per wave.  One
+// kernel serves the three lane-per-sample products of the step:
+//   kFwdRelu   z = b + W a, a' = relu(z) (bf16 in bf16 mode); weight(k, o) = wt[k][o]
+//   kFwdHead   t = b3 + w3 . a2 (one output);                  weight(k, o) = wt[k][o]
+//   kBackprop  d1 = [z1 > 0] (W2^T d2) (bf16 in bf16 mode), the chain starting
+//              from zero;                                        weight(k, o) = wt[o][k]
+// where wt is the compute copy's W1T, W2T or w3.  Every chain keeps its order:
+// bias (or zero) first, then inputs k ascending.
+constexpr int kDenseMaxK = 256;
+enum DenseMode { kFwdRelu = 0, kFwdHead = 1, kBackprop = 2 };
+
+// Each lane carries kDenseSpl samples (64 apart), so one LDS weight read feeds
+// kDenseSpl chains.
+constexpr int kDenseSpl = 2;
+
+template <bool BF, int MODE, int U>
+__device__ __forceinline__ void dense_units(const float* __restrict__ in, const float* __restrict__ wl,
+                                            const float* __restrict__ bias, const float* __restrict__ zmask,
+                                            float* __restrict__ z, float* __restrict__ a, int32_t B, int K, int o0,
+                                            int uoff, const int64_t (&b)[kDenseSpl], const bool (&valid)[kDenseSpl]) {
+    constexpr int P = kDenseSpl;
+    float acc[P][U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float init = MODE == kBackprop ? 0.0f : bias[o0 + u];
+#pragma unroll
+        for (int j = 0; j < P; ++j) acc[j][u] = init;
+    }
+    int k = 0;
+    for (; k + 4 <= K; k += 4) {
+        float x[4][P];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int j = 0; j < P; ++j) x[e][j] = in[(int64_t)(k + e) * B + b[j]];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float* __restrict__ w = wl + (k + e) * 32 + uoff;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const float wv = w[u];
+#pragma unroll
+                for (int j = 0; j < P; ++j) acc[j][u] = __builtin_fmaf(wv, x[e][j], acc[j][u]);
+            }
+        }
+    }
+    for (; k < K; ++k) {
+        const float* __restrict__ w = wl + k * 32 + uoff;
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+            const float x = in[(int64_t)k * B + b[j]];
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[j][u] = __builtin_fmaf(w[u], x, acc[j][u]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+        if (!valid[j]) continue;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e = (int64_t)(o0 + u) * B + b[j];
+            if (MODE == kFwdRelu) {
+                z[e] = acc[j][u];
+                const float h = relu_u(acc[j][u]);
+                a[e] = BF ? q_bf16(h) : h;
+            } else if (MODE == kFwdHead) {
+                z[e] = acc[j][u];
+            } else {
+                const float v = zmask[e] > 0.0f ? acc[j][u] : 0.0f;
+                z[e] = BF ? q_bf16(v) : v;
+            }
+        }
+    }
+}
+
+template <bool BF, int MODE>
+__global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict__ in, const float* __restrict__ wt,
+                                                         const float* __restrict__ bias,
+                                                         const float* __restrict__ zmask, float* __restrict__ z,
+                                                         float* __restrict__ a, int32_t B, int K, int O) {
+    __shared__ __align__(16) float wl[kDenseMaxK * 32];
+    const int jb = blockIdx.y * 32;
+    const int nu = O - jb < 32 ? O - jb : 32;
+    for (int e = threadIdx.x; e < K * 32; e += blockDim.x) {
+        const int k = e >> 5, u = e & 31;
+        float v = 0.0f;
+        if (u < nu) v = MODE == kBackprop ? wt[(int64_t)(jb + u) * K + k] : wt[(int64_t)k * O + jb + u];
+        wl[e] = v;
+    }
+    __syncthreads();
+    // samples of this lane: block base + wave * 64 P + 64 j + lane
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t base = (int64_t)blockIdx.x * blockDim.x * kDenseSpl + (int64_t)wave * 64 * kDenseSpl + lane;
+    int64_t b[kDenseSpl];
+    bool valid[kDenseSpl];
+#pragma unroll
+    for (int j = 0; j < kDenseSpl; ++j) {
+        const int64_t bt = base + 64 * j;
+        valid[j] = bt < B;
+        b[j] = valid[j] ? bt : 0;
+    }
+    if (nu == 32) {
+        dense_units<BF, MODE, 32>(in, wl, bias, zmask, z, a, B, K, jb, 0, b, valid);
+        return;
+    }
+    int uo = 0;
+    if (nu & 16) { dense_units<BF, MODE, 16>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 16; }
+    if (nu & 8) { dense_units<BF, MODE, 8>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 8; }
+    if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 4; }
+    if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 2; }
+    if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 1; }
 }
 
 // ---------------------------------------------------------------------------
@@ -305,11 +422,105 @@ __device__ __forceinline__ bf16x8_t load_frag(const float* __restrict__ row, int
     return pack_bf16x8(v);
 }
 
+// One wave per m-tile (eight per workgroup); the B fragments, which every wave
+// of the workgroup needs, are converted once into LDS per stage of kWgradKs
+// k-steps (double-buffered) and read from there.
+constexpr int kWgradKs = 2;
+
 template <int NT, bool VEC>
 __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
                                                          float* __restrict__ part, int M, int N, int32_t B,
                                                          int64_t chunk) {
-    const int lane = threadIdx.x & 63, mt = threadIdx.x >> 6;
+    constexpr int KS = kWgradKs;
+    constexpr int NE = KS * NT * 64;                 // fragment lanes per stage
+    constexpr int EPT = (NE + 511) / 512;            // per thread
+    __shared__ bf16x8_t lds_b[2][NE];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, mt = tid >> 6;
+    const int row = lane & 31, half = lane >> 5;
+    const int s = blockIdx.x;
+    const int64_t kb = (int64_t)s * chunk;
+    const int64_t ke = min(kb + chunk, (int64_t)B);
+    const int m = mt * 32 + row;
+    const bool mvalid = m < M;
+    const float* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
+    // the fragment lanes this thread stages: (k-step, n-tile, lane) = f
+    const float* __restrict__ srow[EPT];
+    bool sval[EPT];
+    int soff[EPT];
+#pragma unroll
+    for (int x = 0; x < EPT; ++x) {
+        const int f = tid + 512 * x;
+        const int ks = f / (NT * 64), t = (f / 64) % NT, ln = f & 63;
+        const int n = t * 32 + (ln & 31);
+        sval[x] = f < NE && n < N;
+        srow[x] = Bt + (int64_t)(sval[x] ? n : 0) * B;
+        soff[x] = 16 * ks + 8 * (ln >> 5);
+    }
+    bf16x8_t ones;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ones[j] = (__bf16)1.0f;
+    f32x16_t acc[NT + 1];
+#pragma unroll
+    for (int t = 0; t <= NT; ++t) acc[t] = f32x16_t{};
+
+    bf16x8_t stage[EPT], a_next[KS];
+    auto fetch = [&](int64_t k0) {
+#pragma unroll
+        for (int x = 0; x < EPT; ++x) stage[x] = load_frag<VEC>(srow[x], k0 + soff[x], ke, sval[x]);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) a_next[ks] = load_frag<VEC>(arow, k0 + 16 * ks + 8 * half, ke, mvalid);
+    };
+    auto publish = [&](int buf) {
+#pragma unroll
+        for (int x = 0; x < EPT; ++x)
+            if (tid + 512 * x < NE) lds_b[buf][tid + 512 * x] = stage[x];
+    };
+    fetch(kb);
+    publish(0);
+    __syncthreads();
+    int buf = 0;
+    for (int64_t k0 = kb; k0 < ke; k0 += 16 * KS) {
+        bf16x8_t a_cur[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) a_cur[ks] = a_next[ks];
+        const bool more = k0 + 16 * KS < ke;
+        if (more) fetch(k0 + 16 * KS);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (k0 + 16 * ks >= ke) break;
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[ks], lds_b[buf][(ks * NT + t) * 64 + lane],
+                                                                 acc[t], 0, 0, 0);
+            acc[NT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[ks], ones, acc[NT], 0, 0, 0);
+        }
+        if (more) publish(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
+    }
+    const int64_t ld = N + 1;
+    float* __restrict__ out = part + (int64_t)s * M * ld;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int mm = mt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (mm >= M) continue;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int nn = t * 32 + row;
+            if (nn < N) out[(int64_t)mm * ld + nn] = acc[t][r];
+        }
+        if (row == 0) out[(int64_t)mm * ld + N] = acc[NT][r];
+    }
+}
+
+// A single m-tile (the head layer): one wave, no sharing, fragments straight
+// from memory.
+template <int NT, bool VEC>
+__global__ __launch_bounds__(64) void wgrad_direct_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
+                                                         float* __restrict__ part, int M, int N, int32_t B,
+                                                         int64_t chunk) {
+    const int lane = threadIdx.x & 63, mt = 0;
     const int row = lane & 31, half = lane >> 5;
     const int s = blockIdx.x;
     const int64_t kb = (int64_t)s * chunk;
@@ -364,7 +575,15 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= MN) return;
     float acc = 0.0f;
-    for (int s = 0; s < S; ++s) acc += part[(int64_t)s * MN + e];
+    int s = 0;
+    for (; s + 8 <= S; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = part[(int64_t)(s + j) * MN + e];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc += v[j];
+    }
+    for (; s < S; ++s) acc += part[(int64_t)s * MN + e];
     const int64_t mm = e / ld, nn = e - mm * ld;
     if (nn < N) gw[mm * N + nn] = acc;
     else gb[mm] = acc;
@@ -373,17 +592,20 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M
 template <int NT>
 static void launch_wgrad_nt(const float* A, const float* Bt, float* part, int M, int N, int32_t B, int S,
                             int64_t chunk, hipStream_t s) {
-    const dim3 block(64 * ((M + 31) / 32));
-    if (B % 4 == 0)
-        hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), dim3(S), block, 0, s, A, Bt, part, M, N, B, chunk);
-    else
-        hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), dim3(S), block, 0, s, A, Bt, part, M, N, B, chunk);
+    const bool vec = B % 4 == 0;
+    if (M <= 32) {
+        if (vec) hipLaunchKernelGGL((wgrad_direct_kernel<NT, true>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
+        else hipLaunchKernelGGL((wgrad_direct_kernel<NT, false>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
+    } else {
+        if (vec) hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), dim3(S), dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
+        else hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), dim3(S), dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
+    }
 }
 
 // dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.
 static hipError_t weight_grad_mfma(const float* A, const float* Bt, int M, int N, int32_t B, float* part,
                                    float* gw, float* gb, hipStream_t s) {
-    const WgradPlan p = wgrad_plan(B);
+    const WgradPlan p = wgrad_plan(B, M);
     switch ((N + 31) / 32) {
         case 1: launch_wgrad_nt<1>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
         case 2: launch_wgrad_nt<2>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
@@ -507,12 +729,23 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, w.xn,
                        B, m.d);
     const uint32_t sb = blocks_for(nB, 256);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
-                       compute + m.c_w1t, compute + m.c_b1, w.z1, w.a1, B, m.d, m.h1);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
-                       compute + m.c_w2t, compute + m.c_b2, w.z2, w.a2, B, m.h1, m.h2);
-    hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, w.a2,
-                       compute + m.c_w3, compute + m.c_b3, w.t, nullptr, B, m.h2, 1);
+    const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
+    const bool lds_w = m.d <= kDenseMaxK && m.h1 <= kDenseMaxK && m.h2 <= kDenseMaxK;
+    if (lds_w) {
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
+                           compute + m.c_w1t, compute + m.c_b1, nullptr, w.z1, w.a1, B, m.d, m.h1);
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
+                           compute + m.c_w2t, compute + m.c_b2, nullptr, w.z2, w.a2, B, m.h1, m.h2);
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, w.a2,
+                           compute + m.c_w3, compute + m.c_b3, nullptr, w.t, nullptr, B, m.h2, 1);
+    } else {
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
+                           compute + m.c_w1t, compute + m.c_b1, w.z1, w.a1, B, m.d, m.h1);
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
+                           compute + m.c_w2t, compute + m.c_b2, w.z2, w.a2, B, m.h1, m.h2);
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, w.a2,
+                           compute + m.c_w3, compute + m.c_b3, w.t, nullptr, B, m.h2, 1);
+    }
     // loss and output gradient
     hipLaunchKernelGGL(loss_grad_kernel<BF>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
     if (loss_out)
@@ -539,8 +772,12 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     }
     if (e != hipSuccess) return e;
     // first hidden layer
-    hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (m.h1 + 63) / 64), dim3(256), 0, s,
-                       compute + m.c_w2t, w.d2, w.z1, w.d1, m.h1, m.h2, B);
+    if (lds_w)
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, w.d2,
+                           compute + m.c_w2t, nullptr, w.z1, w.d1, nullptr, B, m.h2, m.h1);
+    else
+        hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (m.h1 + 63) / 64), dim3(256), 0, s,
+                           compute + m.c_w2t, w.d2, w.z1, w.d1, m.h1, m.h2, B);
     if (mf) {
         e = weight_grad_mfma(w.d1, w.xn, m.h1, m.d, B, w.part, w.grad + m.m_w1, w.grad + m.m_b1, s);
     } else {
