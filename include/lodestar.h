@@ -152,6 +152,19 @@ int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
 int ls_set_exact_scores(ls_ctx* ctx, int enable);
 
 /*
+ * How ls_score_batch finds the overlap of followers -- requests whose first
+ * block hash is shared with a longer request of the batch (Section 2: reuse is
+ * strictly sequential, so a follower's overlap equals the longer request's up
+ * to their common prefix).  Beyond that prefix, the follower's next block is
+ * either probed in every instance's table (mode 2), or first looked up in one
+ * pass over all cached keys, so that only followers whose next block is cached
+ * somewhere are probed (mode 1).  Mode 0 (the default) picks per call from the
+ * pair count and the total table size.  The overlaps are identical in every
+ * mode.  Returns LS_ERR_INVALID for other modes; takes effect for later calls.
+ */
+int ls_set_prefix_join(ls_ctx* ctx, int mode);
+
+/*
  * One SGD step on the installed model (Section 4.3.2, online learning; the
  * loss and optimiser are this library's reading: mean squared error of the
  * predicted TTFT, plain SGD).  L = (1/B) sum_b (t_b - y_b)^2, W <- W - lr dL/dW.

@@ -26,6 +26,7 @@ struct CacheTables {
     uint32_t* nbuckets = nullptr;    // [N]
     uint32_t* flags = nullptr;       // [N]
     int32_t n = 0;
+    int64_t total_buckets = 0;
 };
 
 // Bucket of `key` in a table of nb buckets: Fibonacci hashing of the whole key,
@@ -109,10 +110,13 @@ inline int64_t group_table_size(int32_t R) {
     while (g < 2 * (int64_t)R) g <<= 1;
     return g;
 }
-int64_t prefix_workspace_bytes(int32_t R);
+int64_t prefix_workspace_bytes(int32_t R, int32_t N);
+// Whether followers' continuations go through the semi-join (mode 0 decides
+// from the sizes, 1 always, 2 never).
+bool prefix_use_join(int32_t R, int32_t N, int64_t table_slots, int mode);
 hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const int64_t* req_off,
                                const uint64_t* req_hashes, int32_t* overlap, void* workspace, int n_cu,
-                               hipStream_t s);
+                               bool join, hipStream_t s);
 
 hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s);
 hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,

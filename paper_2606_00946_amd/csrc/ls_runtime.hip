@@ -28,6 +28,7 @@ struct ls_ctx {
     uint16_t* frag16 = nullptr;
     float* frag32 = nullptr;
     bool exact_scores = false;
+    int prefix_join = 0;     // 0 decide per call, 1 always, 2 never
     int n_cu = 1;
     // cache state
     ls::CacheTables tables;
@@ -442,6 +443,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     LS_HIP(c, hipEventRecord(c->stage_done, s));
     c->stage_pending = true;
     c->tables.n = N;
+    c->tables.total_buckets = nbk;
     // build
     {
         Timed t(c, K_TABLE, s);
@@ -476,7 +478,7 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
 
     const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
-    need += (size_t)round_up(ls::prefix_workspace_bytes(R), 256);
+    need += (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256);
     if (!overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
@@ -490,12 +492,15 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     if (rc) return rc;
     WsCarve w{(char*)c->ws};
     float* part_t = w.take<float>((int64_t)m.h1 * N);
-    char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R));
+    char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R, N));
     int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
     float* sc = scores ? scores : w.take<float>(pairs);
 
     LS_TIMED(c, K_PREFIX, s,
-             ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu, s));
+             ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu,
+                                     ls::prefix_use_join(R, N, c->tables.total_buckets * ls::kBucketKeys,
+                                                         c->prefix_join),
+                                     s));
     LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     const uint8_t* band = nullptr;
     if (fast) {
@@ -527,6 +532,14 @@ int ls_set_exact_scores(ls_ctx* c, int enable) {
     if (!c) return LS_ERR_INVALID;
     c->err.clear();
     c->exact_scores = enable != 0;
+    return LS_OK;
+}
+
+int ls_set_prefix_join(ls_ctx* c, int mode) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (mode < 0 || mode > 2) return fail(c, LS_ERR_INVALID, "prefix join mode must be 0, 1 or 2");
+    c->prefix_join = mode;
     return LS_OK;
 }
 

@@ -59,7 +59,7 @@ def head_magnitude(w, rows):
 class GpuRun:
     """A context loaded with one workload's model and cache state."""
 
-    def __init__(self, w, dtype=None, params=None, exact=False):
+    def __init__(self, w, dtype=None, params=None, exact=False, prefix_join=0):
         import torch
         self.w = w
         cfg = w.cfg
@@ -67,6 +67,8 @@ class GpuRun:
         self.exact = exact
         if exact:
             self.ctx.ls_set_exact_scores(True)
+        if prefix_join:
+            self.ctx.ls_set_prefix_join(prefix_join)
         self.ctx.ls_set_model(w.params if params is None else params, w.mu, w.inv_sigma)
         self.inst_hashes = to_dev(w.inst_hashes)
         self.ctx.ls_load_cache_state(w.inst_off, self.inst_hashes)

@@ -355,6 +355,75 @@ def test_table_overflow_paths(case):
     check_scoring(w, out, np.arange(R, dtype=np.int32))
 
 
+def _follower_workload(rng):
+    """A shared chain A with followers that leave it at different blocks and
+    continue with hashes cached on some instances, on none, or equal to the
+    all-ones key; plus unrelated keys so the tables span several buckets."""
+    E = (1 << 64) - 1
+    A = [int(x) for x in rng.integers(0, 1 << 63, 12)]
+    X, Y, Z, W2, V = (int(x) for x in rng.integers(0, 1 << 63, 5))
+    filler = lambda k: [int(x) for x in rng.integers(0, 1 << 63, k)]
+    caches = [
+        A[:10] + filler(300),                 # the whole leader chain
+        A[:5] + filler(300),                  # part of it
+        A[:10] + [X, Y] + filler(300),        # the chain and one follower's continuation
+        [],                                   # nothing
+        A[:3] + [E] + filler(300),            # the all-ones key after A[:3]
+        [X] + A[:6] + filler(300),            # X without the prefix before it
+        A[:2] + [W2, V] + filler(300),        # a continuation after two blocks
+    ]
+    reqs = [
+        (A[:10], 170),                        # leader of group A
+        (A[:6] + [X, Y, Z], 150),             # continuation cached on instance 2 only
+        (A[:4] + [Z], 90),                    # continuation cached nowhere
+        (A[:3] + [E, Z], 85),                 # continuation is the all-ones key
+        (A[:10], 160),                        # same prompt as the leader
+        (A[:7], 120),                         # ends inside the common prefix
+        (A[:2] + [W2, V, X], 99),             # continuation cached on instance 6
+        (A[:1] + [Z] * 3, 70),                # leaves after one block
+        ([X, Y], 40),                         # its own group
+        (A[:10] + [Y], 180),                  # longer than the leader: becomes the leader
+    ]
+    for _ in range(40):                       # more followers with private tails
+        k = int(rng.integers(0, 11))
+        reqs.append((A[:k] + filler(int(rng.integers(0, 4))), 16 * 16))
+    inst_off, inst_h = oracle_pins._csr(caches)
+    req_off, req_h = oracle_pins._csr([r for r, _ in reqs])
+    L = np.array([max(l, 16 * len(r)) for r, l in reqs], np.int32)
+    return inst_off, inst_h, req_off, req_h, L
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_followers_and_continuations(mode):
+    """Followers resolved from the leader, through the semi-join of their
+    continuation hashes (mode 1), or by probing (mode 2): identical overlaps."""
+    note(f"followers and continuations, join mode {mode}")
+    inst_off, inst_h, req_off, req_h, L = _follower_workload(np.random.default_rng(21))
+    base = workload("tiny")
+    N, R, d = len(inst_off) - 1, len(req_off) - 1, base.cfg.d
+    w = synth.Workload(cfg=synth.dataclasses.replace(base.cfg, R=R, N=N), req_off=req_off, req_hashes=req_h,
+                       prompt_len=L, req_group=np.zeros(R, np.int32), inst_off=inst_off, inst_hashes=inst_h,
+                       inst_feat=np.random.default_rng(6).uniform(0, 4, (N, d - 5)).astype(np.float32),
+                       params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
+                       upd_ttft=base.upd_ttft, lr=base.lr)
+    out = GpuRun(w, prefix_join=mode).score()
+    want = oracle.overlap(req_off, req_h, inst_off, inst_h)
+    np.testing.assert_array_equal(out["overlap"], want)
+    assert want[1, 2] == 8 and want[1, 0] == 6 and want[6, 6] == 4
+    check_scoring(w, out, np.arange(R, dtype=np.int32))
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+def test_join_modes_agree_on_a_full_workload(mode):
+    """The homogeneous workload with the semi-join forced on and off."""
+    w = workload("homogeneous")
+    note(f"homogeneous overlaps, join mode {mode}")
+    out = GpuRun(w, prefix_join=mode).score()
+    sel = sampled(w, k=48)
+    want = oracle.overlap(w.req_off, w.req_hashes, w.inst_off, w.inst_hashes, sel=sel)
+    np.testing.assert_array_equal(out["overlap"][sel], want)
+
+
 def test_ties_go_to_lowest_instance():
     """Instances with identical state and cache score identically; the lowest id wins."""
     note("exact ties")
