@@ -47,10 +47,14 @@ PEAK_VALU_FP32_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 # sources they are compiled from.
 KIND_KERNELS = {
     "score_pairs_mfma": (["ls::score_pairs_mfma_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
-    "table_build": (["ls::table_insert_kernel"], ["k_cache.hip", "ls_internal.h"]),
-    "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::prefix_leaders_kernel",
-                      "ls::prefix_followers_kernel"], ["k_prefix.hip", "ls_internal.h"]),
-    "rescore": (["ls::rescore_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
+    "table_build": (["ls::table_segment_kernel", "ls::table_overflow_kernel"], ["k_cache.hip", "ls_internal.h"]),
+    "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_filter_kernel",
+                      "ls::cont_scan_kernel", "ls::cont_probe_kernel", "ls::prefix_leaders_kernel",
+                      "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
+    "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "ls_internal.h"]),
+    "update": (["ls::dense_lane_kernel", "ls::wgrad_mfma_kernel", "ls::wgrad_direct_kernel", "ls::wgrad_reduce_kernel",
+                "ls::delta_head_kernel", "ls::normalize_kernel", "ls::loss_grad_kernel", "ls::loss_final_kernel",
+                "ls::sgd_kernel", "ls::refresh_compute_kernel"], ["k_update.hip", "k_score.hip", "ls_internal.h"]),
 }
 
 

@@ -1,0 +1,267 @@
+// Exact decisions on top of the matrix-core scores: per request, select every
+// pair whose fast score could still be the argmin within its error band, and
+// rescore those pairs with the canonical fp32 chain (bias first, inputs in
+// ascending order), so that the decision and its score are the canonical ones.
+//
+// The fast scorer writes, for each pair, its score t and an error scale
+// E = kBandRel * (sum_j |w3_j| h2_j + |b3|).  A pair is a candidate if
+// t - E <= min over the request of (t + E); the argmin then runs over the
+// candidates' canonical scores only.
+#include "k_common.h"
+
+namespace ls {
+
+// ---------------------------------------------------------------------------
+// band selection and canonical rescoring
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool finite_f(float x) { return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u; }
+
+// One wave per request, 16 requests per workgroup: U = min_i (t_i + E_i) over
+// finite pairs; a pair is a candidate if t_i - E_i <= U (or if t_i or E_i is
+// not finite).  Candidates are appended to one list with a single atomic per
+// workgroup.
+constexpr int kBandWaves = 16;
+
+__device__ __forceinline__ bool band_member(float ti, float ei, float U) {
+    return !(finite_f(ti) && finite_f(ei)) || (ti - ei <= U);
+}
+
+__global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
+                                                           const float* __restrict__ E, uint8_t* __restrict__ band,
+                                                           int64_t* __restrict__ list, uint32_t* __restrict__ count) {
+    __shared__ uint32_t wcount[kBandWaves];
+    __shared__ uint32_t wbase[kBandWaves];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t r = (int64_t)blockIdx.x * kBandWaves + wv;
+    const bool live = r < R;
+    const float* __restrict__ tr = t + (live ? r : 0) * N;
+    const float* __restrict__ er = E + (live ? r : 0) * N;
+    float U = INFINITY;
+    uint32_t cnt = 0;
+    if (live) {
+        for (int i = lane; i < N; i += 64) {
+            const float ti = tr[i], ei = er[i];
+            if (finite_f(ti) && finite_f(ei)) U = fminf(U, ti + ei);
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) U = fminf(U, __shfl_xor(U, off));
+        U = U + fabsf(U) * 0x1p-20f;                // absorbs the rounding of the sums above
+        for (int i0 = 0; i0 < N; i0 += 64) {
+            const int i = i0 + lane;
+            bool in = false;
+            if (i < N) {
+                in = band_member(tr[i], er[i], U);
+                band[r * N + i] = in ? 1 : 0;
+            }
+            cnt += (uint32_t)__popcll(__ballot(in));
+        }
+    }
+    if (lane == 0) wcount[wv] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t total = 0;
+        for (int k = 0; k < kBandWaves; ++k) total += wcount[k];
+        uint32_t base = total ? atomicAdd(count, total) : 0u;
+        for (int k = 0; k < kBandWaves; ++k) {
+            wbase[k] = base;
+            base += wcount[k];
+        }
+    }
+    __syncthreads();
+    if (!live) return;
+    uint32_t base = wbase[wv];
+    for (int i0 = 0; i0 < N; i0 += 64) {
+        const int i = i0 + lane;
+        const bool in = i < N && band_member(tr[i], er[i], U);
+        const uint64_t m = __ballot(in);
+        if (in) list[base + __popcll(m & ((1ull << lane) - 1))] = r * N + i;
+        base += (uint32_t)__popcll(m);
+    }
+}
+
+hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
+                              uint32_t* count, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)),
+                       dim3(64 * kBandWaves), 0, s, R, N, t, E, band, list, count);
+    return hipGetLastError();
+}
+
+// Canonical score of every listed pair, written over its fast score.
+template <bool BF>
+__global__ __launch_bounds__(256) void rescore_kernel(PairModel M, const float* __restrict__ mu,
+                                                      const float* __restrict__ isig,
+                                                      const float* __restrict__ part_t, int32_t N,
+                                                      const int64_t* __restrict__ req_off,
+                                                      const int32_t* __restrict__ prompt_len,
+                                                      const int32_t* __restrict__ overlap, int block_tokens,
+                                                      const int64_t* __restrict__ list,
+                                                      const uint32_t* __restrict__ count, float* __restrict__ scores) {
+    const uint32_t cnt = *count;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < cnt; q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t p = list[q];
+        const int64_t r = p / N, i = p - r * N;
+        float x[5], xt[5];
+        derived_columns(prompt_len[r], req_off[r + 1] - req_off[r], overlap[p], block_tokens, x);
+        normalise_tail<BF>(x, mu, isig, M.d_inst, xt);
+        scores[p] = canonical_score<BF>(M, part_t + i, N, xt);
+    }
+}
+
+// Same scores, one wave per listed pair (bf16 model, h1 = h2 = H): lanes own
+// output units, W2 sits in LDS as bf16 bits, the pair's layer-1 activations
+// and then its layer-2 outputs pass through a per-wave LDS row, and lane 0
+// runs the head chain.  Every chain keeps the canonical order (bias first,
+// inputs ascending), so each score is bitwise the one-lane-per-pair value.
+struct RescoreArgs {
+    const float* __restrict__ w1;     // [H x d] compute copy
+    const float* __restrict__ w2t;    // [H x H] W2T[k][j]
+    const float* __restrict__ b2;
+    const float* __restrict__ w3;
+    const float* __restrict__ b3;
+    const float* __restrict__ mu;
+    const float* __restrict__ isig;
+    const float* __restrict__ part_t;  // [H x N]
+    const int64_t* __restrict__ req_off;
+    const int32_t* __restrict__ prompt_len;
+    const int32_t* __restrict__ overlap;
+    const int64_t* __restrict__ list;
+    const uint32_t* __restrict__ count;
+    float* __restrict__ scores;
+    int32_t N;
+    int d, d_inst, block_tokens;
+};
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Each wave scores two pairs at once, so every weight it converts from bf16
+// serves two chains and the two head chains run side by side.
+constexpr int kRescoreWaves = 12;
+constexpr int kRescorePairs = 2;
+
+template <int H>
+__global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(RescoreArgs A) {
+    constexpr int U = H / 64;                  // units per lane
+    constexpr int P = kRescorePairs;
+    __shared__ uint16_t lds_w2[H * H];
+    __shared__ float lds_w3[H];
+    __shared__ __align__(16) float lds_row[kRescoreWaves][P][H];
+    for (int e = threadIdx.x; e < H * H; e += 64 * kRescoreWaves) lds_w2[e] = (uint16_t)(__float_as_uint(A.w2t[e]) >> 16);
+    for (int e = threadIdx.x; e < H; e += 64 * kRescoreWaves) lds_w3[e] = A.w3[e];
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    float w1c[U][5], b2v[U];
+#pragma unroll
+    for (int v = 0; v < U; ++v) {
+#pragma unroll
+        for (int c = 0; c < 5; ++c) w1c[v][c] = A.w1[(int64_t)(lane + 64 * v) * A.d + A.d_inst + c];
+        b2v[v] = A.b2[U * lane + v];
+    }
+    const float b3 = A.b3[0];
+    const int64_t cnt = *A.count;
+    for (int64_t q = ((int64_t)blockIdx.x * kRescoreWaves + wave) * P; q < cnt;
+         q += (int64_t)gridDim.x * kRescoreWaves * P) {
+        int64_t pp[P];
+#pragma unroll
+        for (int e = 0; e < P; ++e) pp[e] = A.list[q + e < cnt ? q + e : q];
+        // layer 1, resumed from the instance partial: unit lane + 64 v
+#pragma unroll
+        for (int e = 0; e < P; ++e) {
+            const int64_t r = pp[e] / A.N, i = pp[e] - r * A.N;
+            float x[5], xt[5];
+            derived_columns(A.prompt_len[r], A.req_off[r + 1] - A.req_off[r], A.overlap[pp[e]], A.block_tokens, x);
+            normalise_tail<true>(x, A.mu, A.isig, A.d_inst, xt);
+#pragma unroll
+            for (int v = 0; v < U; ++v) {
+                const int k = lane + 64 * v;
+                float z = A.part_t[(int64_t)k * A.N + i];
+#pragma unroll
+                for (int c = 0; c < 5; ++c) z = __builtin_fmaf(w1c[v][c], xt[c], z);
+                lds_row[wave][e][k] = bf16_rne_num(relu(z));
+            }
+        }
+        wave_sync();
+        // layer 2: units U lane .. U lane + U - 1
+        float acc[P][U];
+#pragma unroll
+        for (int e = 0; e < P; ++e)
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[e][u] = b2v[u];
+        for (int k = 0; k < H; k += 4) {
+            float av[P][4];
+#pragma unroll
+            for (int e = 0; e < P; ++e) {
+                const float4 a4 = *reinterpret_cast<const float4*>(&lds_row[wave][e][k]);
+                av[e][0] = a4.x; av[e][1] = a4.y; av[e][2] = a4.z; av[e][3] = a4.w;
+            }
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const uint16_t* wr = lds_w2 + (k + kk) * H + U * lane;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const float wv = __uint_as_float((uint32_t)wr[u] << 16);
+#pragma unroll
+                    for (int e = 0; e < P; ++e) acc[e][u] = __builtin_fmaf(wv, av[e][kk], acc[e][u]);
+                }
+            }
+        }
+        wave_sync();
+#pragma unroll
+        for (int e = 0; e < P; ++e)
+#pragma unroll
+            for (int u = 0; u < U; ++u) lds_row[wave][e][U * lane + u] = bf16_rne_num(relu(acc[e][u]));
+        wave_sync();
+        if (lane < P && q + lane < cnt) {
+            const float* hrow = lds_row[wave][lane];
+            float t = b3;
+            for (int j = 0; j < H; j += 4) {
+                const float4 h4 = *reinterpret_cast<const float4*>(hrow + j);
+                t = __builtin_fmaf(lds_w3[j], h4.x, t);
+                t = __builtin_fmaf(lds_w3[j + 1], h4.y, t);
+                t = __builtin_fmaf(lds_w3[j + 2], h4.z, t);
+                t = __builtin_fmaf(lds_w3[j + 3], h4.w, t);
+            }
+            A.scores[pp[lane]] = t;
+        }
+        wave_sync();
+    }
+}
+
+hipError_t launch_rescore(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
+                          const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
+                          const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
+                          const uint32_t* count, float* scores, int n_cu, hipStream_t s) {
+    PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
+                m.d, m.d_inst, m.h1, m.h2};
+    if (m.bf16 && m.h1 == m.h2 && (m.h1 == 64 || m.h1 == 128 || m.h1 == 256)) {
+        RescoreArgs A{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
+                      mu, inv_sigma, part_t, req_off, prompt_len, overlap, list, count, scores, N, m.d, m.d_inst,
+                      m.block_tokens};
+        const dim3 grid((uint32_t)n_cu), block(64 * kRescoreWaves);
+        switch (m.h1) {
+            case 64: hipLaunchKernelGGL(rescore_wave_kernel<64>, grid, block, 0, s, A); break;
+            case 128: hipLaunchKernelGGL(rescore_wave_kernel<128>, grid, block, 0, s, A); break;
+            default: hipLaunchKernelGGL(rescore_wave_kernel<256>, grid, block, 0, s, A); break;
+        }
+        return hipGetLastError();
+    }
+    // enough lanes for about two candidates per request, capped at 8 waves per SIMD
+    // enough lanes for about two candidates per request, capped at 8 waves per SIMD
+    int64_t want = ((int64_t)R * 2 + 255) / 256;
+    int64_t cap = (int64_t)n_cu * 8;
+    int64_t grid = want < cap ? want : cap;
+    if (grid < 1) grid = 1;
+    if (m.bf16)
+        hipLaunchKernelGGL(rescore_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t, N,
+                           req_off, prompt_len, overlap, m.block_tokens, list, count, scores);
+    else
+        hipLaunchKernelGGL(rescore_kernel<false>, dim3((uint32_t)grid), dim3(256), 0, s, M, mu, inv_sigma, part_t, N,
+                           req_off, prompt_len, overlap, m.block_tokens, list, count, scores);
+    return hipGetLastError();
+}
+
+}  // namespace ls
