@@ -56,11 +56,32 @@ def _open(path):
         lib.lso_score.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, P, P, i32, P, P, P,
                                   P, P, P, P, P, ctypes.c_int]
         lib.lso_update.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, f32, P, P]
-        for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update):
+        lib.lso_splitmix64_mix.argtypes = [ctypes.c_uint64]
+        lib.lso_splitmix64_mix.restype = ctypes.c_uint64
+        lib.lso_hrw_topk.argtypes = [i32, ctypes.c_uint64, i32, P]
+        lib.lso_hrw_topk.restype = i32
+        lib.lso_heuristic.argtypes = [i32, i32, P, P, dbl, dbl, dbl]
+        lib.lso_heuristic.restype = i32
+        lib.lso_route.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, P, P, i32, P, P, P,
+                                  ctypes.POINTER(Policy), P, P, P, P, ctypes.c_int]
+        for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update, lib.lso_route):
             f.restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
 
+
+class Policy(ctypes.Structure):
+    """Routing-policy parameters (mirrors lso_policy in the C file)."""
+    _fields_ = [("heuristic", ctypes.c_int32), ("count_col0", ctypes.c_int32), ("count_col1", ctypes.c_int32),
+                ("kv_col", ctypes.c_int32), ("k_filter", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("theta_imbal", ctypes.c_double), ("overload_k", ctypes.c_double), ("prefix_tau", ctypes.c_double),
+                ("n_samples", ctypes.c_int64), ("n_min", ctypes.c_int64),
+                ("epsilon", ctypes.c_double), ("tau_sat", ctypes.c_double), ("tau_ben", ctypes.c_double),
+                ("delta", ctypes.c_double), ("lo", ctypes.c_void_p), ("hi", ctypes.c_void_p)]
+
+
+ROUTE_OK, ROUTE_COLD_START, ROUTE_OOD = 0, 1, 2
+ROUTE_EXPLORED, ROUTE_KFILTER, ROUTE_TIEBREAK = 0x100, 0x200, 0x400
 
 _active = None
 
@@ -183,3 +204,55 @@ def update(mode, d, hidden, params, mu, inv_sigma, feats, ttft, lr) -> dict:
                         feats.shape[0], _ptr(feats), _ptr(ttft), float(lr), _ptr(grad), _ptr(loss))
     assert rc == 0, rc
     return {"params": p, "grad": grad, "loss": float(loss[0])}
+
+
+def splitmix64_mix(z: int) -> int:
+    return int(_load().lso_splitmix64_mix(ctypes.c_uint64(z & 0xFFFFFFFFFFFFFFFF)))
+
+
+def hrw_topk(N: int, key: int, K: int) -> np.ndarray:
+    out = np.zeros(max(K, 1), dtype=np.int32)
+    n = _load().lso_hrw_topk(N, ctypes.c_uint64(key & 0xFFFFFFFFFFFFFFFF), K, _ptr(out))
+    return out[:n]
+
+
+def heuristic(alg, m, c, theta=0.0, k=0.0, tau=0.0) -> int:
+    m = _c(m, np.float32); c = _c(c, np.float64)
+    return int(_load().lso_heuristic(int(alg), m.shape[0], _ptr(m), _ptr(c), float(theta), float(k), float(tau)))
+
+
+def policy(heuristic=1, count_cols=(-1, -1), theta_imbal=0.0, overload_k=0.0, prefix_tau=0.0, n_samples=0,
+           n_min=0, lo=None, hi=None, epsilon=0.0, kv_col=-1, tau_sat=0.0, tau_ben=0.0, k_filter=0, delta=-1.0):
+    """Policy parameters as the fp32 values the library receives (kept alive with the returned pair)."""
+    f = lambda v: float(np.float32(v))
+    lo_a = None if lo is None else _c(lo, np.float32)
+    hi_a = None if hi is None else _c(hi, np.float32)
+    p = Policy(int(heuristic), int(count_cols[0]), int(count_cols[1]), int(kv_col), int(k_filter), 0,
+               f(theta_imbal), f(overload_k), f(prefix_tau), int(n_samples), int(n_min),
+               f(epsilon), f(tau_sat), f(tau_ben), f(delta),
+               None if lo_a is None else lo_a.ctypes.data, None if hi_a is None else hi_a.ctypes.data)
+    return p, (lo_a, hi_a)
+
+
+def route(mode, d, hidden, params, mu, inv_sigma, req_off, req_hashes, prompt_len, inst_feat, inst_off,
+          inst_hashes, pol, rnd, sel=None, threads=0):
+    """Alg. 3 + Alg. 4 decisions for the selected requests: (chosen, status, heuristic choice)."""
+    lib = _load()
+    hidden_a = _c(hidden, np.int32)
+    params = _c(params, np.float32); mu = _c(mu, np.float32); inv_sigma = _c(inv_sigma, np.float32)
+    req_off = _c(req_off, np.int64); req_hashes = _c(req_hashes, np.uint64)
+    prompt_len = _c(prompt_len, np.int32); inst_feat = _c(inst_feat, np.float32)
+    inst_off = _c(inst_off, np.int64); inst_hashes = _c(inst_hashes, np.uint64)
+    rnd = _c(rnd, np.uint32)
+    R = req_off.shape[0] - 1
+    N = inst_off.shape[0] - 1
+    sel_a = None if sel is None else _c(sel, np.int32)
+    n_sel = R if sel_a is None else sel_a.shape[0]
+    chosen = np.zeros(n_sel, np.int32); status = np.zeros(n_sel, np.int32); heur = np.zeros(n_sel, np.int32)
+    p, _keep = pol
+    rc = lib.lso_route(_mode(mode), d, hidden_a.shape[0], _ptr(hidden_a), _ptr(params), _ptr(mu), _ptr(inv_sigma),
+                       n_sel, _ptr(sel_a), _ptr(req_off), _ptr(req_hashes), _ptr(prompt_len), N, _ptr(inst_feat),
+                       _ptr(inst_off), _ptr(inst_hashes), ctypes.byref(p), _ptr(rnd), _ptr(chosen), _ptr(status),
+                       _ptr(heur), threads)
+    assert rc == 0, rc
+    return chosen, status, heur

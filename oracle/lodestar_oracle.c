@@ -507,3 +507,220 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
     free(grad); free(act); free(pre); free(delta); free(dnext); free(Wq);
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Routing policy around the model: the gateway's routing with fallback       */
+/* (Alg. 3), the routing service's logic (Alg. 4: cold start, out-of-range    */
+/* guard, epsilon-greedy exploration, consistent-hashing K-filter, reward      */
+/* tie-break) and the heuristic it falls back to (Alg. 1, or Alg. 2).          */
+/* ------------------------------------------------------------------------- */
+
+/* splitmix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number     */
+/* generators", 2014): the state advances by 0x9e3779b97f4a7c15 and each       */
+/* output is the new state passed through this mixing function.                */
+uint64_t lso_splitmix64_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+/* Consistent hashing of a prefix group onto K instances (Section 4.1,        */
+/* Consistent hashing based filtering), as rendezvous hashing: instance i's   */
+/* weight for key k is output i+1 of splitmix64 seeded with k; the K heaviest */
+/* instances (ties to the lower id) are selected, heaviest first.             */
+int32_t lso_hrw_topk(int32_t N, uint64_t key, int32_t K, int32_t* out)
+{
+    int32_t n = K < N ? K : N;
+    for (int32_t t = 0; t < n; ++t) {
+        int32_t best = -1;
+        uint64_t bw = 0;
+        for (int32_t i = 0; i < N; ++i) {
+            int taken = 0;
+            for (int32_t u = 0; u < t; ++u) taken |= (out[u] == i);
+            if (taken) continue;
+            uint64_t w = lso_splitmix64_mix(key + 0x9e3779b97f4a7c15ull * (uint64_t)(i + 1));
+            if (best < 0 || w > bw) { best = i; bw = w; }
+        }
+        out[t] = best;
+    }
+    return n;
+}
+
+static int32_t argmin_count(int32_t N, const double* c)
+{
+    int32_t b = 0;
+    for (int32_t i = 1; i < N; ++i)
+        if (c[i] < c[b]) b = i;
+    return b;
+}
+
+/* Alg. 1 (prefix-cache-and-load) when alg == 1, Alg. 2 (prefix-aware with    */
+/* threshold tau) when alg == 2.  m[i] is the prefix match ratio of the       */
+/* request on instance i, c[i] its request count.  Mean and standard          */
+/* deviation are the population ones, summed in ascending instance order.     */
+/* Ties in every ordering go to the lower instance id.                        */
+int32_t lso_heuristic(int32_t alg, int32_t N, const float* m, const double* c, double theta, double k, double tau)
+{
+    if (alg == 2) {
+        int32_t b = 0;
+        for (int32_t i = 1; i < N; ++i)
+            if (m[i] > m[b]) b = i;
+        if ((double)m[b] > tau) return b;
+        return argmin_count(N, c);
+    }
+    double cmin = c[0], cmax = c[0];
+    for (int32_t i = 1; i < N; ++i) {
+        if (c[i] < cmin) cmin = c[i];
+        if (c[i] > cmax) cmax = c[i];
+    }
+    if (cmax - cmin > theta) return argmin_count(N, c);
+    double sum = 0.0;
+    for (int32_t i = 0; i < N; ++i) sum += c[i];
+    double mu = sum / (double)N;
+    double var = 0.0;
+    for (int32_t i = 0; i < N; ++i) var += (c[i] - mu) * (c[i] - mu);
+    double sigma = sqrt(var / (double)N);
+    double limit = mu + k * sigma;
+    /* the first instance in (m desc, c asc, id asc) order that is not overloaded */
+    int32_t b = -1;
+    for (int32_t i = 0; i < N; ++i) {
+        if (!(c[i] <= limit)) continue;
+        if (b < 0 || m[i] > m[b] || (m[i] == m[b] && c[i] < c[b])) b = i;
+    }
+    return b >= 0 ? b : argmin_count(N, c);
+}
+
+typedef struct {
+    int32_t heuristic;                  /* 1: Alg. 1, 2: Alg. 2 */
+    int32_t count_col0, count_col1;     /* instance columns summed into the request count (-1: unused) */
+    int32_t kv_col;                     /* instance column of KV-cache utilisation (-1: no K-filter) */
+    int32_t k_filter;                   /* K (0: no K-filter) */
+    int32_t pad;
+    double theta_imbal, overload_k, prefix_tau;
+    int64_t n_samples, n_min;
+    double epsilon, tau_sat, tau_ben, delta;
+    const float* lo;                    /* [d] feature bounds, NULL: no out-of-range guard */
+    const float* hi;
+} lso_policy;
+
+#define LSO_ROUTE_OK 0
+#define LSO_ROUTE_COLD_START 1
+#define LSO_ROUTE_OOD 2
+#define LSO_ROUTE_EXPLORED 0x100
+#define LSO_ROUTE_KFILTER 0x200
+#define LSO_ROUTE_TIEBREAK 0x400
+
+static int in_bounds(float v, float lo, float hi) { return lo <= v && v <= hi; }
+
+/* index of a 32-bit random word scaled onto [0, n) */
+static int32_t scale_u32(uint32_t u, int64_t n) { return (int32_t)(((uint64_t)u * (uint64_t)n) >> 32); }
+
+/* Routing decision for selected requests (outputs indexed by position in sel).
+ * rnd holds three uniform 32-bit words per request (exploration draw,
+ * exploration pick, tie-break pick), indexed by request id. */
+int lso_route(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params,
+              const float* mu, const float* inv_sigma,
+              int32_t n_sel, const int32_t* sel, const int64_t* req_off, const uint64_t* req_hashes,
+              const int32_t* prompt_len, int32_t N, const float* inst_feat,
+              const int64_t* inst_off, const uint64_t* inst_hashes, const lso_policy* pol, const uint32_t* rnd,
+              int32_t* chosen_out, int32_t* status_out, int32_t* heur_out, int threads)
+{
+    if (d <= LSO_DERIVED || N < 1) return -1;
+    int32_t d_inst = d - LSO_DERIVED;
+    int32_t Rsel = n_sel;
+    int32_t* ov = (int32_t*)malloc(sizeof(int32_t) * (size_t)Rsel * N);
+    double* sc = (double*)malloc(sizeof(double) * (size_t)Rsel * N);
+    int rc = lso_score(mode, d, n_hidden, hidden, params, mu, inv_sigma, n_sel, sel, req_off, req_hashes, prompt_len,
+                       N, inst_feat, inst_off, inst_hashes, ov, sc, NULL, NULL, NULL, threads);
+    if (rc) { free(ov); free(sc); return rc; }
+    /* per-instance quantities shared by every request */
+    double* cnt = (double*)malloc(sizeof(double) * (size_t)N);
+    int* inst_ok = (int*)malloc(sizeof(int) * (size_t)N);
+    double kv_sum = 0.0;
+    for (int32_t i = 0; i < N; ++i) {
+        const float* row = inst_feat + (int64_t)i * d_inst;
+        double ci = 0.0;
+        if (pol->count_col0 >= 0) ci += (double)row[pol->count_col0];
+        if (pol->count_col1 >= 0) ci += (double)row[pol->count_col1];
+        cnt[i] = ci;
+        int ok = 1;
+        if (pol->lo)
+            for (int32_t c = 0; c < d_inst; ++c) ok &= in_bounds(row[c], pol->lo[c], pol->hi[c]);
+        inst_ok[i] = ok;
+        if (pol->kv_col >= 0) kv_sum += (double)row[pol->kv_col];
+    }
+    int saturated = pol->kv_col >= 0 && kv_sum / (double)N > pol->tau_sat;
+    uint64_t explore_thr = (uint64_t)floor(pol->epsilon * 4294967296.0);
+    float* m = (float*)malloc(sizeof(float) * (size_t)N);
+    int32_t* C = (int32_t*)malloc(sizeof(int32_t) * (size_t)(pol->k_filter > 0 ? pol->k_filter : 1));
+    int32_t* S = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    for (int32_t q = 0; q < n_sel; ++q) {
+        int32_t r = sel ? sel[q] : q;
+        int64_t n = req_off[r + 1] - req_off[r];
+        int32_t L = prompt_len[r];
+        const double* s = sc + (int64_t)q * N;
+        double kl_max = 0.0;
+        for (int32_t i = 0; i < N; ++i) {
+            /* the hit ratio as the feature row holds it, in the mode's precision */
+            double row[LSO_DERIVED + 1];
+            lso_features(mode, 0, NULL, L, (int32_t)n, ov[(int64_t)q * N + i], row);
+            m[i] = (float)row[3];
+            double kl = (double)m[i] * (double)L;
+            if (i == 0 || kl > kl_max) kl_max = kl;
+        }
+        int32_t heur = lso_heuristic(pol->heuristic, N, m, cnt, pol->theta_imbal, pol->overload_k, pol->prefix_tau);
+        int32_t chosen, status;
+        int ood = 0;
+        if (pol->lo) {
+            ood |= !in_bounds((float)L, pol->lo[d_inst], pol->hi[d_inst]);
+            ood |= !in_bounds((float)n, pol->lo[d_inst + 1], pol->hi[d_inst + 1]);
+            for (int32_t i = 0; i < N; ++i) ood |= !inst_ok[i];
+        }
+        if (pol->n_samples < pol->n_min) {
+            chosen = heur; status = LSO_ROUTE_COLD_START;
+        } else if (ood) {
+            chosen = heur; status = LSO_ROUTE_OOD;
+        } else if ((uint64_t)rnd[(int64_t)r * 3] < explore_thr) {
+            chosen = scale_u32(rnd[(int64_t)r * 3 + 1], N); status = LSO_ROUTE_OK | LSO_ROUTE_EXPLORED;
+        } else {
+            status = LSO_ROUTE_OK;
+            chosen = lso_argmin(N, s, NULL);
+            int32_t nc = 0;
+            if (pol->k_filter > 0 && n >= 1 && saturated && kl_max > pol->tau_ben) {
+                nc = lso_hrw_topk(N, req_hashes[req_off[r]], pol->k_filter, C);
+                status |= LSO_ROUTE_KFILTER;
+                int inC = 0;
+                for (int32_t u = 0; u < nc; ++u) inC |= (C[u] == chosen);
+                if (!inC) {
+                    int32_t b = C[0];
+                    for (int32_t u = 1; u < nc; ++u)
+                        if (better(s[C[u]], C[u], s[b], b)) b = C[u];
+                    chosen = b;
+                }
+            }
+            double tb = s[chosen];
+            if (pol->delta >= 0.0 && !isnan(tb)) {
+                double lim = tb + pol->delta * fabs(tb);
+                int32_t ns = 0;
+                for (int32_t i = 0; i < N; ++i) {
+                    int scope = 1;
+                    if (nc > 0) {
+                        scope = 0;
+                        for (int32_t u = 0; u < nc; ++u) scope |= (C[u] == i);
+                    }
+                    if (scope && s[i] <= lim) S[ns++] = i;
+                }
+                if (ns > 1) {
+                    chosen = S[scale_u32(rnd[(int64_t)r * 3 + 2], ns)];
+                    status |= LSO_ROUTE_TIEBREAK;
+                }
+            }
+        }
+        if (chosen_out) chosen_out[q] = chosen;
+        if (status_out) status_out[q] = status;
+        if (heur_out) heur_out[q] = heur;
+    }
+    free(ov); free(sc); free(cnt); free(inst_ok); free(m); free(C); free(S);
+    return 0;
+}

@@ -408,4 +408,185 @@ def pin_score_pipeline_bruteforce(seed=19):
         assert np.array_equal(out["feat"][r], x[best])
 
 
+# ---------------------------------------------------------------------------
+# routing policy: splitmix64, rendezvous hashing, Alg. 1 / Alg. 2, Alg. 3 / Alg. 4
+# ---------------------------------------------------------------------------
+_GAMMA = 0x9E3779B97F4A7C15
+_M64 = (1 << 64) - 1
+
+
+def pin_splitmix64_published():
+    """splitmix64 seeded with 0: the first three outputs of the published generator."""
+    want = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+    assert [oracle.splitmix64_mix((_GAMMA * (k + 1)) & _M64) for k in range(3)] == want
+
+
+def pin_hrw_topk(seed=23, trials=40):
+    """Rendezvous top-K by brute-force sorting of the weights; adding an
+    instance moves at most one key slot, and only to the new instance."""
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        N = int(rng.integers(1, 40)); K = int(rng.integers(1, 6)); key = int(rng.integers(0, 1 << 63)) * 2 + 1
+        w = [oracle.splitmix64_mix((key + _GAMMA * (i + 1)) & _M64) for i in range(N + 1)]
+        brute = sorted(range(N), key=lambda i: (-w[i], i))[:K]
+        got = list(oracle.hrw_topk(N, key, K))
+        assert got == brute, (got, brute)
+        grown = set(oracle.hrw_topk(N + 1, key, K))
+        assert grown - set(got) <= {N} and len(grown ^ set(got)) <= 2
+
+
+def _brute_alg1(m, c, theta, k):
+    """Alg. 1 as printed: imbalance check, then sort by (match desc, count asc)
+    and take the first instance not above mean + k * std."""
+    N = len(c)
+    least = min(range(N), key=lambda i: (c[i], i))
+    if max(c) - min(c) > theta:
+        return least
+    mu = sum(c) / N
+    sigma = (sum((x - mu) ** 2 for x in c) / N) ** 0.5
+    for i in sorted(range(N), key=lambda i: (-float(m[i]), c[i], i)):
+        if c[i] <= mu + k * sigma:
+            return i
+    return least
+
+
+def _brute_alg2(m, c, tau):
+    N = len(c)
+    best = min(range(N), key=lambda i: (-float(m[i]), i))
+    if float(m[best]) > tau:
+        return best
+    return min(range(N), key=lambda i: (c[i], i))
+
+
+def pin_heuristics_hand():
+    f = np.float32
+    assert oracle.heuristic(1, f([0.9, 0.5, 0.1]), [10.0, 0.0, 5.0], theta=5.0, k=1.0) == 1      # imbalanced
+    # balanced: mean 2, std 0.816, k = 0 -> counts <= 2 qualify; best match among them is instance 2
+    assert oracle.heuristic(1, f([0.9, 0.5, 0.9]), [3.0, 2.0, 1.0], theta=10.0, k=0.0) == 2
+    # a count exactly at the limit qualifies (mean 2, k = 0)
+    assert oracle.heuristic(1, f([0.1, 0.9, 0.3]), [1.0, 2.0, 3.0], theta=10.0, k=0.0) == 1
+    # nobody qualifies (negative k): least loaded
+    assert oracle.heuristic(1, f([0.9, 0.5, 0.1]), [2.0, 1.0, 3.0], theta=10.0, k=-5.0) == 1
+    m = f([0.2, 0.6, 0.6])
+    assert oracle.heuristic(2, m, [5.0, 1.0, 0.0], tau=0.5) == 1                                  # above threshold
+    assert oracle.heuristic(2, m, [5.0, 1.0, 0.0], tau=float(f(0.6))) == 2                         # equal: not above
+    assert oracle.heuristic(2, m, [5.0, 1.0, 0.0], tau=0.7) == 2
+
+
+def pin_heuristics_bruteforce(seed=29, trials=300):
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        N = int(rng.integers(1, 9))
+        m = np.float32(rng.choice([0.0, 0.25, 0.5, 0.75, 1.0], N))
+        c = [float(v) for v in rng.integers(0, 6, N)]
+        theta = float(rng.choice([1.0, 3.0, 100.0])); k = float(rng.choice([-1.0, 0.0, 0.5, 1.0]))
+        tau = float(rng.choice([0.0, 0.25, 0.5, 0.9]))
+        assert oracle.heuristic(1, m, c, theta=theta, k=k) == _brute_alg1(m, c, theta, k)
+        assert oracle.heuristic(2, m, c, tau=tau) == _brute_alg2(m, c, tau)
+
+
+def _route_case(seed=31, R=12, N=8, dup=False):
+    """A small workload with the oracle's own (pinned) overlaps and scores."""
+    from paper_2606_00946_amd import synth
+    w = synth.generate("tiny", R=R, N=N)
+    feat = w.inst_feat.copy()
+    inst_lists = [w.inst_hashes[w.inst_off[i]:w.inst_off[i + 1]] for i in range(N)]
+    if dup:                                        # instances in identical pairs -> exact score ties
+        for i in range(N):
+            inst_lists[i] = inst_lists[i & ~1]
+            feat[i] = feat[i & ~1]
+    inst_off = np.zeros(N + 1, np.int64); inst_off[1:] = np.cumsum([len(x) for x in inst_lists])
+    inst_h = np.concatenate(inst_lists)
+    rnd = np.random.default_rng(seed).integers(0, 1 << 32, (R, 3), dtype=np.uint64).astype(np.uint32)
+    res = oracle.score("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                       w.prompt_len, feat, inst_off, inst_h)
+    sc, ch = res["scores"], res["chosen"]
+    ov = oracle.overlap(w.req_off, w.req_hashes, inst_off, inst_h)
+    return w, feat, inst_off, inst_h, rnd, sc, ch, ov
+
+
+def _run_route(case, **pol):
+    w, feat, inst_off, inst_h, rnd, _, _, _ = case
+    return oracle.route("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                        w.prompt_len, feat, inst_off, inst_h, oracle.policy(**pol), rnd)
+
+
+def _scaled(u, n):
+    return (int(u) * int(n)) >> 32
+
+
+def pin_route_branches():
+    case = _route_case()
+    w, feat, inst_off, inst_h, rnd, sc, ch, ov = case
+    R, N = w.cfg.R, w.cfg.N
+    d_inst = w.cfg.d - 5
+    counts = (0, 1)
+    cnt = [float(feat[i, 0]) + float(feat[i, 1]) for i in range(N)]
+    L = w.prompt_len
+    kappa = np.array([[np.float32(0.0) if L[r] == 0 else np.float32(np.float32(16 * ov[r, i]) / np.float32(L[r]))
+                       for i in range(N)] for r in range(R)], np.float32)
+    base = dict(heuristic=1, count_cols=counts, theta_imbal=4.0, overload_k=0.5, n_samples=100, n_min=10)
+    heur_want = [_brute_alg1(kappa[r], cnt, 4.0, 0.5) for r in range(R)]
+    # plain greedy: the argmin of the scores
+    c_, st, hr = _run_route(case, **base)
+    assert list(c_) == list(ch) and all(st == oracle.ROUTE_OK) and list(hr) == heur_want
+    # cold start: heuristic for everybody; n_samples == n_min is not a cold start
+    c_, st, _ = _run_route(case, **{**base, "n_samples": 9})
+    assert all(st == oracle.ROUTE_COLD_START) and list(c_) == heur_want
+    c_, st, _ = _run_route(case, **{**base, "n_samples": 10})
+    assert all(st == oracle.ROUTE_OK)
+    # out-of-range instance column: every request falls back; a bound equal to the value is in range
+    lo = np.full(w.cfg.d, -np.inf, np.float32); hi = np.full(w.cfg.d, np.inf, np.float32)
+    hi2 = hi.copy(); hi2[2] = np.nextafter(np.float32(feat[:, 2].max()), np.float32(-np.inf))
+    c_, st, _ = _run_route(case, **base, lo=lo, hi=hi2)
+    assert all(st == oracle.ROUTE_OOD) and list(c_) == heur_want
+    lo3 = lo.copy(); lo3[2] = np.float32(feat[:, 2].min())
+    _, st, _ = _run_route(case, **base, lo=lo3, hi=hi)
+    assert all(st == oracle.ROUTE_OK)
+    # out-of-range request column (prompt length): only the long prompts fall back
+    hi4 = hi.copy(); hi4[d_inst] = np.float32(np.median(L))
+    c_, st, _ = _run_route(case, **base, lo=lo, hi=hi4)
+    for r in range(R):
+        assert (st[r] == oracle.ROUTE_OOD) == (L[r] > hi4[d_inst])
+    # exploration: epsilon = 1 always, epsilon = 0 never; the draw is compared with floor(eps * 2^32)
+    c_, st, _ = _run_route(case, **base, epsilon=1.0)
+    assert all(st == oracle.ROUTE_EXPLORED) and list(c_) == [_scaled(rnd[r, 1], N) for r in range(R)]
+    rnd[0, 0] = 1 << 31; rnd[1, 0] = (1 << 31) - 1
+    _, st, _ = _run_route(case, **base, epsilon=0.5)
+    assert st[0] == oracle.ROUTE_OK and st[1] == oracle.ROUTE_EXPLORED
+    # tie-break: a huge margin makes every instance near-best
+    c_, st, _ = _run_route(case, **base, delta=1e30)
+    assert all(st == oracle.ROUTE_TIEBREAK) and list(c_) == [_scaled(rnd[r, 2], N) for r in range(R)]
+    # K-filter forced on (saturation and benefit thresholds below any value)
+    kf = dict(base, kv_col=4, tau_sat=-1.0, tau_ben=-1.0)
+    first = [int(w.req_hashes[w.req_off[r]]) for r in range(R)]
+    c_, st, _ = _run_route(case, **kf, k_filter=1)
+    assert all(st == oracle.ROUTE_KFILTER)
+    assert list(c_) == [int(oracle.hrw_topk(N, first[r], 1)[0]) for r in range(R)]
+    c_, st, _ = _run_route(case, **kf, k_filter=N)
+    assert list(c_) == list(ch)
+    # with K = 2 and a huge margin the tie-break stays inside the filtered pair
+    c_, st, _ = _run_route(case, **kf, k_filter=2, delta=1e30)
+    for r in range(R):
+        pair = sorted(oracle.hrw_topk(N, first[r], 2))
+        assert c_[r] == pair[_scaled(rnd[r, 2], 2)] and st[r] == oracle.ROUTE_KFILTER | oracle.ROUTE_TIEBREAK
+    # benefit threshold above every kappa * L: the filter stays off
+    c_, st, _ = _run_route(case, **dict(kf, tau_ben=1e30), k_filter=1)
+    assert list(c_) == list(ch) and all(st == oracle.ROUTE_OK)
+    # Alg. 2 as the fallback heuristic
+    _, _, hr = _run_route(case, **dict(base, heuristic=2, prefix_tau=0.25))
+    assert list(hr) == [_brute_alg2(kappa[r], cnt, float(np.float32(0.25))) for r in range(R)]
+
+
+def pin_route_exact_ties():
+    """Duplicated instances tie exactly; a zero margin picks uniformly among the tied ones."""
+    case = _route_case(dup=True)
+    w, feat, inst_off, inst_h, rnd, sc, ch, ov = case
+    c_, st, _ = _run_route(case, heuristic=1, count_cols=(0, 1), n_samples=1, n_min=0, delta=0.0)
+    for r in range(w.cfg.R):
+        tied = [i for i in range(w.cfg.N) if sc[r, i] == sc[r].min()]
+        assert len(tied) >= 2
+        assert c_[r] == tied[_scaled(rnd[r, 2], len(tied))] and st[r] == oracle.ROUTE_TIEBREAK
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -63,6 +63,25 @@ MUTANTS = [
     ("update_lowp_inputs_in_double", "a0[k] = bf ? (double)lso_bf16_round(t) : (double)t;",
      "a0[k] = bf ? (double)lso_bf16_round(t) : ((double)xb[k] - (double)mu[k]) * (double)inv_sigma[k];"),
     ("update_loss_not_mean", "if (loss_out) *loss_out = loss / (double)B;", "if (loss_out) *loss_out = loss;"),
+    ("mix_constant", "* 0xbf58476d1ce4e5b9ull", "* 0xbf58476d1ce4e5b8ull"),
+    ("hrw_index_offset", "0x9e3779b97f4a7c15ull * (uint64_t)(i + 1)", "0x9e3779b97f4a7c15ull * (uint64_t)i"),
+    ("hrw_lightest", "if (best < 0 || w > bw) { best = i; bw = w; }", "if (best < 0 || w < bw) { best = i; bw = w; }"),
+    ("alg1_strict_overload", "if (!(c[i] <= limit)) continue;", "if (!(c[i] < limit)) continue;"),
+    ("alg1_sample_std", "double sigma = sqrt(var / (double)N);",
+     "double sigma = sqrt(var / (double)(N > 1 ? N - 1 : 1));"),
+    ("alg1_count_desc", "(m[i] == m[b] && c[i] < c[b])", "(m[i] == m[b] && c[i] > c[b])"),
+    ("alg1_no_imbalance_check", "if (cmax - cmin > theta) return argmin_count(N, c);", ""),
+    ("alg2_ge_tau", "if ((double)m[b] > tau) return b;", "if ((double)m[b] >= tau) return b;"),
+    ("cold_start_le", "if (pol->n_samples < pol->n_min) {", "if (pol->n_samples <= pol->n_min) {"),
+    ("ood_open_bounds", "static int in_bounds(float v, float lo, float hi) { return lo <= v && v <= hi; }",
+     "static int in_bounds(float v, float lo, float hi) { return lo < v && v < hi; }"),
+    ("ood_ignores_instances", "for (int32_t i = 0; i < N; ++i) ood |= !inst_ok[i];", ""),
+    ("explore_le", "(uint64_t)rnd[(int64_t)r * 3] < explore_thr", "(uint64_t)rnd[(int64_t)r * 3] <= explore_thr"),
+    ("explore_wrong_word", "chosen = scale_u32(rnd[(int64_t)r * 3 + 1], N);",
+     "chosen = scale_u32(rnd[(int64_t)r * 3 + 2], N);"),
+    ("kfilter_ignores_benefit", "saturated && kl_max > pol->tau_ben", "saturated"),
+    ("tiebreak_ignores_scope", "if (scope && s[i] <= lim) S[ns++] = i;", "if (s[i] <= lim) S[ns++] = i;"),
+    ("tiebreak_strict", "if (scope && s[i] <= lim) S[ns++] = i;", "if (scope && s[i] < lim) S[ns++] = i;"),
 ]
 
 _RUNNER = r"""
