@@ -179,12 +179,103 @@ int ls_update(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, flo
               float* loss_out, float* grad_out, void* stream);
 
 /*
+ * Routing policy around the reward model.
+ *
+ * The gateway pre-computes a heuristic choice for every request and uses it
+ * whenever the routing service signals a fallback (Alg. 3); the service itself
+ * (Alg. 4) returns a fallback status on a cold start (fewer than n_min logged
+ * samples) or when a feature lies outside the bounds seen in training (the
+ * out-of-range guard of Section 4.3.1), explores uniformly with probability
+ * epsilon, and otherwise routes greedily on the model, with two refinements:
+ * when the cluster's KV cache is saturated and the request's best prefix
+ * benefit is large, the choice is restricted to K instances picked by
+ * consistent hashing of its prefix group (Section 4.1, Consistent hashing
+ * based filtering), and a near-best set within a relative margin delta is
+ * broken uniformly at random (the reward tiebreak).
+ *
+ * Heuristics: LS_HEUR_PREFIX_LOAD is the prefix-cache-and-load policy (Alg. 1):
+ * the least-loaded instance when request counts differ by more than
+ * theta_imbal, else the best prefix match (ties: fewer requests, lower id)
+ * among instances whose count is at most mean + overload_k * std (population
+ * statistics), else the least loaded.  LS_HEUR_PREFIX_THRESHOLD (Alg. 2)
+ * takes the best prefix match if it exceeds prefix_tau, else the least loaded.
+ * The prefix match ratio is the pair's kappa = 16 l / L; the request count
+ * c_i is the sum of the instance-feature columns count_cols (-1 skips one).
+ *
+ * Readings of points the paper leaves open:
+ *   - bounds cover the request columns (L, n) and the instance columns; the
+ *     pair columns (l, kappa, u) are not checked.  lo/hi are host arrays of
+ *     d floats (copied); NULL disables the guard.  lo <= v <= hi is in range.
+ *   - the prefix group is the request's first block hash; the K instances are
+ *     its rendezvous top-K: instance i weighs output i + 1 of splitmix64
+ *     (Steele, Lea and Flood, 2014) seeded with the hash, heaviest first.
+ *   - the benefit is max_i kappa_i * L in tokens; saturation is the mean of
+ *     instance column kv_col over all instances, compared with tau_sat.
+ *   - the near-best set is {i : t_i <= t* + delta |t*|} on predicted TTFT t
+ *     (the printed form on rewards is empty for negative rewards), taken within
+ *     the K instances when the filter applies; delta < 0 disables the
+ *     tie-break (lowest id wins ties then).
+ *   - random draws come from the caller: rnd holds three uniform uint32 words
+ *     per request (device, [R x 3]): exploration draw u0 (explore when
+ *     u0 < floor(epsilon * 2^32)), exploration pick u1 and tie-break pick u2,
+ *     a pick from n choices being (u * n) >> 32 over the choices in ascending
+ *     instance order.  rnd may be NULL only when epsilon == 0 and delta < 0.
+ * Decisions are exact: on the bf16 matrix-core path every pair that can be
+ * the greedy choice, a member of the near-best set or one of the K filtered
+ * instances is rescored with the canonical chain first.
+ */
+#define LS_HEUR_PREFIX_LOAD 1
+#define LS_HEUR_PREFIX_THRESHOLD 2
+
+#define LS_ROUTE_OK 0
+#define LS_ROUTE_COLD_START 1     /* fallback: not enough samples yet (chosen = heuristic) */
+#define LS_ROUTE_OOD 2            /* fallback: a feature outside the bounds (chosen = heuristic) */
+#define LS_ROUTE_EXPLORED 0x100   /* flag on LS_ROUTE_OK: uniform exploration */
+#define LS_ROUTE_KFILTER 0x200    /* flag on LS_ROUTE_OK: the choice was restricted to the K instances */
+#define LS_ROUTE_TIEBREAK 0x400   /* flag on LS_ROUTE_OK: drawn from a near-best set of two or more */
+
+#define LS_MAX_KFILTER 8
+
+typedef struct {
+    int32_t heuristic;        /* LS_HEUR_PREFIX_LOAD or LS_HEUR_PREFIX_THRESHOLD */
+    int32_t count_cols[2];    /* instance-feature columns summed into the request count */
+    float theta_imbal;        /* Alg. 1 imbalance threshold */
+    float overload_k;         /* Alg. 1 overload factor */
+    float prefix_tau;         /* Alg. 2 prefix-hit threshold */
+    int64_t n_samples;        /* logged samples so far */
+    int64_t n_min;            /* cold-start threshold */
+    const float* lo;          /* host [d] or NULL */
+    const float* hi;          /* host [d] or NULL */
+    float epsilon;            /* exploration rate in [0, 1] */
+    int32_t kv_col;           /* instance-feature column of KV-cache utilisation, -1: no K-filter */
+    float tau_sat;            /* saturation threshold on the mean of kv_col */
+    float tau_ben;            /* benefit threshold on max_i kappa_i * L (tokens) */
+    int32_t k_filter;         /* K in [0, LS_MAX_KFILTER]; 0: no K-filter */
+    float delta;              /* tie-break margin; < 0: no tie-break */
+} ls_policy;
+
+/*
+ * Scores a batch like ls_score_batch and then routes every request with the
+ * policy above.  Inputs as for ls_score_batch, plus rnd.  Outputs (device):
+ *   chosen   int32 [R]      the instance the request is forwarded to
+ *   status   int32 [R]      LS_ROUTE_* code and flags (nullable)
+ *   heur     int32 [R]      the heuristic's choice (nullable)
+ *   feat_out fp32  [R x d]  raw feature row of the chosen pair (nullable)
+ * LS_ERR_INVALID for a bad policy (unknown heuristic, column out of range,
+ * k_filter outside [0, LS_MAX_KFILTER], NaN parameters, missing rnd).
+ */
+int ls_route_batch(ls_ctx* ctx, const ls_policy* policy, int32_t R, int32_t N,
+                   const int64_t* req_off, const uint64_t* req_hashes, const int32_t* prompt_len,
+                   const float* inst_feat, const uint32_t* rnd,
+                   int32_t* chosen, int32_t* status, int32_t* heur, float* feat_out, void* stream);
+
+/*
  * Per-kernel timing (the library's own view of where the routing time goes;
  * Section 5.4 measures the router's overhead end to end).  While enabled, each
  * kernel launch group of the context is bracketed by HIP events on the stream
  * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
  * "score_pairs", "score_pairs_mfma", "band_select", "rescore", "argmin",
- * "update".
+ * "update", "route".
  *   ls_profile_enable  enable != 0 starts recording (and clears old records).
  *   ls_profile_read    synchronous; for up to max_kinds kinds writes the kind
  *                      name (static string), the number of launches and the

@@ -7,7 +7,7 @@
 // E = kBandRel * (sum_j |w3_j| h2_j + |b3|).  A pair is a candidate if
 // t - E <= min over the request of (t + E); the argmin then runs over the
 // candidates' canonical scores only.
-#include "k_common.h"
+#include "k_policy.h"
 
 namespace ls {
 
@@ -26,9 +26,22 @@ __device__ __forceinline__ bool band_member(float ti, float ei, float U) {
     return !(finite_f(ti) && finite_f(ei)) || (ti - ei <= U);
 }
 
+// Policy extensions (routing with the full Alg. 4): with a tie-break margin
+// delta >= 0 the bound grows to cover every pair that can be near-best, and
+// with the K-filter possible the K instances of the request's prefix group are
+// candidates too.
+struct BandPolicy {
+    double delta;                       // < 0: none
+    int32_t k_filter;                   // 0: none
+    const PolicyStats* stats;           // saturation flag (K-filter only)
+    const int64_t* req_off;
+    const uint64_t* req_hashes;
+};
+
 __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
-                                                           const float* __restrict__ E, uint8_t* __restrict__ band,
-                                                           int64_t* __restrict__ list, uint32_t* __restrict__ count) {
+                                                           const float* __restrict__ E, BandPolicy BP,
+                                                           uint8_t* __restrict__ band, int64_t* __restrict__ list,
+                                                           uint32_t* __restrict__ count) {
     __shared__ uint32_t wcount[kBandWaves];
     __shared__ uint32_t wbase[kBandWaves];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -36,21 +49,38 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
     const bool live = r < R;
     const float* __restrict__ tr = t + (live ? r : 0) * N;
     const float* __restrict__ er = E + (live ? r : 0) * N;
-    float U = INFINITY;
+    float U = INFINITY, L0 = INFINITY;
     uint32_t cnt = 0;
+    int32_t C[LS_MAX_KFILTER];
+    int nc = 0;
     if (live) {
         for (int i = lane; i < N; i += 64) {
             const float ti = tr[i], ei = er[i];
-            if (finite_f(ti) && finite_f(ei)) U = fminf(U, ti + ei);
+            if (finite_f(ti) && finite_f(ei)) {
+                U = fminf(U, ti + ei);
+                L0 = fminf(L0, ti - ei);
+            }
         }
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) U = fminf(U, __shfl_xor(U, off));
+        for (int off = 32; off >= 1; off >>= 1) {
+            U = fminf(U, __shfl_xor(U, off));
+            L0 = fminf(L0, __shfl_xor(L0, off));
+        }
+        if (BP.delta >= 0.0 && finite_f(U)) {
+            // the smallest canonical score lies in [L0, U]; c + delta |c| is largest at an end
+            const double a = (double)U + BP.delta * fabs((double)U);
+            const double b = (double)L0 + BP.delta * fabs((double)L0);
+            U = (float)(a > b ? a : b);
+        }
         U = U + fabsf(U) * 0x1p-20f;                // absorbs the rounding of the sums above
+        if (BP.k_filter > 0 && BP.stats->saturated && BP.req_off[r + 1] > BP.req_off[r])
+            nc = hrw_topk_wave(BP.req_hashes[BP.req_off[r]], N, BP.k_filter, C, lane);
         for (int i0 = 0; i0 < N; i0 += 64) {
             const int i = i0 + lane;
             bool in = false;
             if (i < N) {
                 in = band_member(tr[i], er[i], U);
+                for (int q = 0; q < nc; ++q) in |= (C[q] == i);
                 band[r * N + i] = in ? 1 : 0;
             }
             cnt += (uint32_t)__popcll(__ballot(in));
@@ -72,7 +102,7 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
     uint32_t base = wbase[wv];
     for (int i0 = 0; i0 < N; i0 += 64) {
         const int i = i0 + lane;
-        const bool in = i < N && band_member(tr[i], er[i], U);
+        const bool in = i < N && band[r * N + i];
         const uint64_t m = __ballot(in);
         if (in) list[base + __popcll(m & ((1ull << lane) - 1))] = r * N + i;
         base += (uint32_t)__popcll(m);
@@ -81,9 +111,17 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
 
 hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
                               uint32_t* count, hipStream_t s) {
+    return launch_band_select_policy(R, N, t, E, -1.0, 0, nullptr, nullptr, nullptr, band, list, count, s);
+}
+
+hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const float* E, double delta,
+                                     int32_t k_filter, const PolicyStats* stats, const int64_t* req_off,
+                                     const uint64_t* req_hashes, uint8_t* band, int64_t* list, uint32_t* count,
+                                     hipStream_t s) {
     if (R <= 0) return hipSuccess;
+    BandPolicy BP{delta, k_filter, stats, req_off, req_hashes};
     hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)),
-                       dim3(64 * kBandWaves), 0, s, R, N, t, E, band, list, count);
+                       dim3(64 * kBandWaves), 0, s, R, N, t, E, BP, band, list, count);
     return hipGetLastError();
 }
 

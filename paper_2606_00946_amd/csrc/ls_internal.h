@@ -140,6 +140,22 @@ hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, c
                                    int n_cu, hipStream_t s);
 hipError_t launch_band_select(int32_t R, int32_t N, const float* t, const float* E, uint8_t* band, int64_t* list,
                               uint32_t* count, hipStream_t s);
+struct PolicyStats;
+struct PolicyArgs;
+// Band selection for the routing policy: delta >= 0 widens the band to every
+// possible near-best pair, k_filter > 0 adds the K-filter's instances when the
+// batch is saturated (stats on the device).
+hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const float* E, double delta,
+                                     int32_t k_filter, const PolicyStats* stats, const int64_t* req_off,
+                                     const uint64_t* req_hashes, uint8_t* band, int64_t* list, uint32_t* count,
+                                     hipStream_t s);
+hipError_t launch_policy_stats(const PolicyArgs& P, const float* inst_feat, int32_t N, int d_inst, double* cnt,
+                               PolicyStats* st, hipStream_t s);
+hipError_t launch_route(const PolicyArgs& P, const PolicyStats* st, const double* cnt, const ModelDims& m, int32_t R,
+                        int32_t N, const int64_t* req_off, const uint64_t* req_hashes, const int32_t* prompt_len,
+                        const int32_t* overlap, const float* scores, const uint8_t* band, const float* inst_feat,
+                        const uint32_t* rnd, int32_t* chosen, int32_t* status, int32_t* heur, float* feat_out,
+                        hipStream_t s);
 hipError_t launch_rescore(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
                           const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
                           const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,

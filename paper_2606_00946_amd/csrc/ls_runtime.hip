@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "ls_internal.h"
+#include "k_policy.h"
 
 struct ls_ctx {
     ls_model_config cfg{};
@@ -147,9 +148,11 @@ int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
     return LS_OK;
 }
 
-enum Kind { K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_COUNT };
+enum Kind {
+    K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_ROUTE, K_COUNT
+};
 const char* const kKindNames[K_COUNT] = {"table_build", "prefix_match", "instance_partial", "score_pairs", "argmin",
-                                         "update", "score_pairs_mfma", "band_select", "rescore"};
+                                         "update", "score_pairs_mfma", "band_select", "rescore", "route"};
 
 hipEvent_t take_event(ls_ctx* c) {
     if (!c->spare.empty()) {
@@ -456,31 +459,34 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     return LS_OK;
 }
 
-int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
-                   const int32_t* prompt_len, const float* inst_feat, int32_t* chosen, float* min_ttft,
-                   float* scores, int32_t* overlap, float* feat_out, void* stream) {
-    if (!c) return LS_ERR_INVALID;
-    c->err.clear();
-    if (R < 0) return fail(c, LS_ERR_INVALID, "R must be >= 0");
-    if (N < 1) return fail(c, LS_ERR_INVALID, "N must be >= 1");
-    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
-    if (!c->have_cache) return fail(c, LS_ERR_STATE, "no cache state has been loaded");
+namespace {
+
+// Common checks of a scoring call; 1 with *rc set when the call must return.
+int check_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                const int32_t* prompt_len, const float* inst_feat, const int32_t* chosen, int* rc) {
+    *rc = LS_OK;
+    if (R < 0) return *rc = fail(c, LS_ERR_INVALID, "R must be >= 0"), 1;
+    if (N < 1) return *rc = fail(c, LS_ERR_INVALID, "N must be >= 1"), 1;
+    if (!c->have_model) return *rc = fail(c, LS_ERR_STATE, "no model has been set"), 1;
+    if (!c->have_cache) return *rc = fail(c, LS_ERR_STATE, "no cache state has been loaded"), 1;
     if (N != c->tables.n)
-        return fail(c, LS_ERR_STATE, "N is %d but the cache state has %d instances", N, c->tables.n);
-    if (R == 0) return LS_OK;
+        return *rc = fail(c, LS_ERR_STATE, "N is %d but the cache state has %d instances", N, c->tables.n), 1;
+    if (R == 0) return 1;
     if (!req_off || !req_hashes || !prompt_len || !inst_feat || !chosen)
-        return fail(c, LS_ERR_INVALID, "req_off, req_hashes, prompt_len, inst_feat and chosen must be non-NULL");
-    DeviceScope dev(c->device);
-    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
-    hipStream_t s = (hipStream_t)stream;
+        return *rc = fail(c, LS_ERR_INVALID,
+                          "req_off, req_hashes, prompt_len, inst_feat and chosen must be non-NULL"), 1;
+    return 0;
+}
+
+// Workspace of the scoring pipeline.
+size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool have_scores) {
     const ls::ModelDims& m = c->dims;
     const int64_t pairs = (int64_t)R * N;
-
     const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
     need += (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256);
-    if (!overlap) need += (size_t)round_up(pairs * 4, 256);
-    if (!scores) need += (size_t)round_up(pairs * 4, 256);
+    if (!have_overlap) need += (size_t)round_up(pairs * 4, 256);
+    if (!have_scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
         need += (size_t)round_up((int64_t)N * 64 * 2, 256);      // bf16 instance rows
         need += (size_t)round_up(pairs * 4, 256);                // error scales
@@ -488,9 +494,25 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
         need += (size_t)round_up(pairs * 8, 256);                // candidate list
         need += 256;                                             // candidate count
     }
-    int rc = grow(c, &c->ws, &c->ws_cap, need);
-    if (rc) return rc;
-    WsCarve w{(char*)c->ws};
+    return need;
+}
+
+struct Scored {
+    int32_t* ov = nullptr;
+    float* sc = nullptr;
+    const uint8_t* band = nullptr;   // candidates holding canonical scores (null: every pair)
+};
+
+// Overlaps and scores of every pair: canonical scores everywhere, or fast
+// scores with the candidate band rescored canonically.  delta / k_filter /
+// stats widen the band for the routing policy (delta < 0, k_filter 0: argmin
+// only).
+int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                 const int32_t* prompt_len, const float* inst_feat, int32_t* overlap, float* scores, double delta,
+                 int32_t k_filter, const ls::PolicyStats* stats, hipStream_t s, Scored* out) {
+    const ls::ModelDims& m = c->dims;
+    const int64_t pairs = (int64_t)R * N;
+    const bool fast = c->frag16 && !c->exact_scores;
     float* part_t = w.take<float>((int64_t)m.h1 * N);
     char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R, N));
     int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
@@ -514,7 +536,9 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
                  ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, xinst, c->mu, c->isig, R, N, req_off,
                                              prompt_len, ov, sc, eb, c->n_cu, s));
         LS_TIMED(c, K_BAND, s, ls::launch_fill_u32(count, 0u, 1, s));
-        LS_TIMED(c, K_BAND, s, ls::launch_band_select(R, N, sc, eb, flags, list, count, s));
+        LS_TIMED(c, K_BAND, s,
+                 ls::launch_band_select_policy(R, N, sc, eb, delta, k_filter, stats, req_off, req_hashes, flags, list,
+                                               count, s));
         LS_TIMED(c, K_RESCORE, s,
                  ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list, count,
                                     sc, c->n_cu, s));
@@ -523,8 +547,110 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
         LS_TIMED(c, K_SCORE, s,
                  ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));
     }
+    out->ov = ov;
+    out->sc = sc;
+    out->band = band;
+    return LS_OK;
+}
+
+}  // namespace
+
+int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                   const int32_t* prompt_len, const float* inst_feat, int32_t* chosen, float* min_ttft,
+                   float* scores, int32_t* overlap, float* feat_out, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    int rc;
+    if (check_batch(c, R, N, req_off, req_hashes, prompt_len, inst_feat, chosen, &rc)) return rc;
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    rc = grow(c, &c->ws, &c->ws_cap, pipeline_bytes(c, R, N, overlap != nullptr, scores != nullptr));
+    if (rc) return rc;
+    WsCarve w{(char*)c->ws};
+    Scored out;
+    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, -1.0, 0, nullptr, s,
+                      &out);
+    if (rc) return rc;
     LS_TIMED(c, K_ARGMIN, s,
-             ls::launch_argmin(m, R, N, sc, band, req_off, prompt_len, ov, inst_feat, chosen, min_ttft, feat_out, s));
+             ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov, inst_feat, chosen, min_ttft,
+                               feat_out, s));
+    return LS_OK;
+}
+
+int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const int64_t* req_off,
+                   const uint64_t* req_hashes, const int32_t* prompt_len, const float* inst_feat, const uint32_t* rnd,
+                   int32_t* chosen, int32_t* status, int32_t* heur, float* feat_out, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!pol) return fail(c, LS_ERR_INVALID, "policy is NULL");
+    const ls::ModelDims& m = c->dims;
+    const int d_inst = m.d_inst;
+    if (pol->heuristic != LS_HEUR_PREFIX_LOAD && pol->heuristic != LS_HEUR_PREFIX_THRESHOLD)
+        return fail(c, LS_ERR_INVALID, "unknown heuristic %d", pol->heuristic);
+    for (int k = 0; k < 2; ++k)
+        if (pol->count_cols[k] < -1 || pol->count_cols[k] >= d_inst)
+            return fail(c, LS_ERR_INVALID, "count column %d is outside [-1, %d)", pol->count_cols[k], d_inst);
+    if (pol->kv_col < -1 || pol->kv_col >= d_inst)
+        return fail(c, LS_ERR_INVALID, "kv column %d is outside [-1, %d)", pol->kv_col, d_inst);
+    if (pol->k_filter < 0 || pol->k_filter > LS_MAX_KFILTER)
+        return fail(c, LS_ERR_INVALID, "k_filter must be in [0, %d]", LS_MAX_KFILTER);
+    const float fp[] = {pol->theta_imbal, pol->overload_k, pol->prefix_tau, pol->epsilon, pol->tau_sat, pol->tau_ben,
+                        pol->delta};
+    for (float v : fp)
+        if (v != v) return fail(c, LS_ERR_INVALID, "policy parameters must not be NaN");
+    if (!(pol->epsilon >= 0.0f && pol->epsilon <= 1.0f)) return fail(c, LS_ERR_INVALID, "epsilon must be in [0, 1]");
+    if ((pol->lo == nullptr) != (pol->hi == nullptr))
+        return fail(c, LS_ERR_INVALID, "feature bounds lo and hi must both be given or both be NULL");
+    if (!rnd && (pol->epsilon > 0.0f || pol->delta >= 0.0f))
+        return fail(c, LS_ERR_INVALID, "rnd is required with exploration or a tie-break");
+    int rc;
+    if (check_batch(c, R, N, req_off, req_hashes, prompt_len, inst_feat, chosen, &rc)) return rc;
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    size_t need = pipeline_bytes(c, R, N, false, false);
+    need += (size_t)round_up((int64_t)N * 8, 256) + 256 + (size_t)round_up((int64_t)2 * m.d * 4, 256);
+    rc = grow(c, &c->ws, &c->ws_cap, need);
+    if (rc) return rc;
+    WsCarve w{(char*)c->ws};
+    double* cnt = w.take<double>(N);
+    ls::PolicyStats* st = w.take<ls::PolicyStats>(1);
+    float* bounds = w.take<float>(2 * (int64_t)m.d);
+    ls::PolicyArgs P{};
+    P.heuristic = pol->heuristic;
+    P.count_col0 = pol->count_cols[0];
+    P.count_col1 = pol->count_cols[1];
+    P.kv_col = pol->kv_col;
+    P.k_filter = pol->k_filter;
+    P.cold = pol->n_samples < pol->n_min ? 1 : 0;
+    P.theta_imbal = pol->theta_imbal;
+    P.overload_k = pol->overload_k;
+    P.prefix_tau = pol->prefix_tau;
+    P.tau_sat = pol->tau_sat;
+    P.tau_ben = pol->tau_ben;
+    P.delta = pol->delta;
+    P.explore_thr = (uint64_t)floor((double)pol->epsilon * 4294967296.0);
+    if (pol->lo) {
+        const size_t b = sizeof(float) * (size_t)m.d;
+        rc = stage_reserve(c, 2 * b + 64);
+        if (rc) return rc;
+        memcpy(c->stage, pol->lo, b);
+        memcpy((char*)c->stage + b, pol->hi, b);
+        LS_HIP(c, hipMemcpyAsync(bounds, c->stage, 2 * b, hipMemcpyHostToDevice, s));
+        LS_HIP(c, hipEventRecord(c->stage_done, s));
+        c->stage_pending = true;
+        P.lo = bounds;
+        P.hi = bounds + m.d;
+    }
+    LS_TIMED(c, K_ROUTE, s, ls::launch_policy_stats(P, inst_feat, N, d_inst, cnt, st, s));
+    Scored out;
+    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, nullptr, nullptr, pol->delta,
+                      pol->k_filter, st, s, &out);
+    if (rc) return rc;
+    LS_TIMED(c, K_ROUTE, s,
+             ls::launch_route(P, st, cnt, m, R, N, req_off, req_hashes, prompt_len, out.ov, out.sc, out.band, inst_feat,
+                              rnd, chosen, status, heur, feat_out, s));
     return LS_OK;
 }
 

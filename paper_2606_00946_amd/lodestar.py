@@ -33,6 +33,33 @@ class ls_model_config(ctypes.Structure):
                 ("block_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
+LS_HEUR_PREFIX_LOAD, LS_HEUR_PREFIX_THRESHOLD = 1, 2
+LS_ROUTE_OK, LS_ROUTE_COLD_START, LS_ROUTE_OOD = 0, 1, 2
+LS_ROUTE_EXPLORED, LS_ROUTE_KFILTER, LS_ROUTE_TIEBREAK = 0x100, 0x200, 0x400
+
+
+class ls_policy(ctypes.Structure):
+    _fields_ = [("heuristic", ctypes.c_int32), ("count_cols", ctypes.c_int32 * 2), ("theta_imbal", ctypes.c_float),
+                ("overload_k", ctypes.c_float), ("prefix_tau", ctypes.c_float), ("n_samples", ctypes.c_int64),
+                ("n_min", ctypes.c_int64), ("lo", ctypes.c_void_p), ("hi", ctypes.c_void_p),
+                ("epsilon", ctypes.c_float), ("kv_col", ctypes.c_int32), ("tau_sat", ctypes.c_float),
+                ("tau_ben", ctypes.c_float), ("k_filter", ctypes.c_int32), ("delta", ctypes.c_float)]
+
+
+def make_policy(heuristic=LS_HEUR_PREFIX_LOAD, count_cols=(-1, -1), theta_imbal=0.0, overload_k=0.0, prefix_tau=0.0,
+                n_samples=0, n_min=0, lo=None, hi=None, epsilon=0.0, kv_col=-1, tau_sat=0.0, tau_ben=0.0,
+                k_filter=0, delta=-1.0):
+    """An ls_policy; lo/hi are host float32 arrays of d bounds (kept alive on the returned object)."""
+    lo_a = None if lo is None else np.ascontiguousarray(lo, dtype=np.float32)
+    hi_a = None if hi is None else np.ascontiguousarray(hi, dtype=np.float32)
+    p = ls_policy(int(heuristic), (ctypes.c_int32 * 2)(*count_cols), theta_imbal, overload_k, prefix_tau,
+                  int(n_samples), int(n_min), None if lo_a is None else lo_a.ctypes.data,
+                  None if hi_a is None else hi_a.ctypes.data, epsilon, int(kv_col), tau_sat, tau_ben, int(k_filter),
+                  delta)
+    p._bounds = (lo_a, hi_a)
+    return p
+
+
 _lib = None
 
 
@@ -60,10 +87,11 @@ def library():
         lib.ls_profile_enable.argtypes = [P, ctypes.c_int]
         lib.ls_set_exact_scores.argtypes = [P, ctypes.c_int]
         lib.ls_set_prefix_join.argtypes = [P, ctypes.c_int]
+        lib.ls_route_batch.argtypes = [P, ctypes.POINTER(ls_policy), i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
-                  lib.ls_set_prefix_join):
+                  lib.ls_set_prefix_join, lib.ls_route_batch):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -210,6 +238,26 @@ class Context:
             _dev(feat_out, "feat_out", (torch.float32,), R * self.d, allow_none=True),
         ]
         return self._check("ls_score_batch", self.lib.ls_score_batch(self.h, R, N, *args, _stream(stream)))
+
+    def ls_route_batch(self, policy, req_off, req_hashes, prompt_len, inst_feat, rnd, chosen, status=None, heur=None,
+                       feat_out=None, stream=None):
+        import torch
+        R = req_off.numel() - 1
+        N = inst_feat.shape[0] if inst_feat.dim() == 2 else (self.n_instances or 0)
+        d_inst = self.d - DERIVED_COLS
+        args = [
+            _dev(req_off, "req_off", (torch.int64,), R + 1),
+            _dev(req_hashes, "req_hashes", (torch.int64, torch.uint64)),
+            _dev(prompt_len, "prompt_len", (torch.int32,), R),
+            _dev(inst_feat, "inst_feat", (torch.float32,), N * d_inst),
+            _dev(rnd, "rnd", (torch.int32, torch.uint32), 3 * R, allow_none=True),
+            _dev(chosen, "chosen", (torch.int32,), R),
+            _dev(status, "status", (torch.int32,), R, allow_none=True),
+            _dev(heur, "heur", (torch.int32,), R, allow_none=True),
+            _dev(feat_out, "feat_out", (torch.float32,), R * self.d, allow_none=True),
+        ]
+        return self._check("ls_route_batch",
+                           self.lib.ls_route_batch(self.h, ctypes.byref(policy), R, N, *args, _stream(stream)))
 
     # -- online update -----------------------------------------------------
     def ls_update(self, feats, ttft, lr, loss_out=None, grad_out=None, stream=None):
