@@ -138,6 +138,36 @@ def cpu_baseline(w, target_s=12.0):
     }
 
 
+ROUTE_POLICY = dict(heuristic=1, count_cols=(0, 1), theta_imbal=4.0, overload_k=0.5, n_samples=10000, n_min=1000,
+                    epsilon=0.05, kv_col=4, tau_sat=0.3, tau_ben=64.0, k_filter=2, delta=0.01)
+
+
+def time_route(ctx, w, dev_in, reps):
+    """The full routing policy (fallback heuristic, exploration, K-filter, tie-break) on the same batch, timed
+    on its own: it is a separate entry point and not part of the step above."""
+    import torch
+
+    from paper_2606_00946_amd import lodestar
+    R, N = w.cfg.R, w.cfg.N
+    pol = lodestar.make_policy(**ROUTE_POLICY)
+    rnd = torch.from_numpy(np.random.default_rng(3).integers(0, 1 << 32, (R, 3), dtype=np.uint64)
+                           .astype(np.uint32).view(np.int32)).cuda()
+    chosen = torch.empty(R, dtype=torch.int32, device="cuda")
+    status = torch.empty(R, dtype=torch.int32, device="cuda")
+    ctx.ls_route_batch(pol, *dev_in, rnd, chosen, status)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        ctx.ls_route_batch(pol, *dev_in, rnd, chosen, status)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    st = status.cpu().numpy()
+    return {"policy": "Alg. 4 with Alg. 1 fallback, epsilon 0.05, K-filter 2, delta 0.01",
+            "ms_per_batch": round(ms, 4), "pairs_per_s": round(R * N / (ms / 1e3), 1),
+            "explored": int(((st & 0x100) != 0).sum()), "kfilter": int(((st & 0x200) != 0).sum()),
+            "tiebreak": int(((st & 0x400) != 0).sum())}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -245,6 +275,7 @@ def main():
                      "traffic_unit": "GB per launch", "digest": sources_digest(dom) if dom in KIND_KERNELS else None},
         "useful_probes": probes,
     }
+    result["route"] = time_route(ctx, w, (req_off, req_h, plen, feat), args.steps)
     ctx.close()
     if args.copy_probe_mib > 0:
         copy_probe(args.copy_probe_mib)
