@@ -165,6 +165,18 @@ int ls_set_exact_scores(ls_ctx* ctx, int enable);
 int ls_set_prefix_join(ls_ctx* ctx, int mode);
 
 /*
+ * Declares that every instance's cached set is prefix-closed for every prompt
+ * of later ls_score_batch / ls_route_batch calls: if block j of a prompt is
+ * cached on an instance, its blocks 0..j-1 are too (the state an engine's
+ * tail-first LRU keeps, Section 2).  Whether a block is cached is then
+ * monotone along the prompt, and the library finds each run's end by a
+ * multi-way search (O(log n) probe rounds) instead of walking it.  The
+ * overlaps are exact under the invariant; without it they may be wrong (never
+ * out of [0, n]).  enable = 0 (the default) restores the general walk.
+ */
+int ls_set_prefix_closed(ls_ctx* ctx, int enable);
+
+/*
  * One SGD step on the installed model (Section 4.3.2, online learning; the
  * loss and optimiser are this library's reading: mean squared error of the
  * predicted TTFT, plain SGD).  L = (1/B) sum_b (t_b - y_b)^2, W <- W - lr dL/dW.

@@ -147,6 +147,49 @@ __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ 
     return l;
 }
 
+// Prefix-closed caches.  When every instance's cached set is prefix-closed for
+// every prompt (if block j of a prompt is cached, so are its blocks 0..j-1 --
+// the state an engine's tail-first LRU keeps), whether block j is cached is a
+// non-increasing function of j and the run is its first miss.  A wave then
+// searches instead of walking: each round probes 16 positions spread over the
+// open interval [lo, hi) (group g takes lo + (g + 1)(hi - lo) / 17, or lo + g
+// when the interval is short), which shrinks it about 17-fold; about four
+// rounds settle an 8k-block prompt.  Exact only under that invariant.
+__device__ __forceinline__ bool probe_block(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
+                                           uint64_t key, int q, int shift) {
+    if (key == kEmptyKey) return has_empty;
+    uint32_t b = bucket_of(key, nb);
+    for (uint32_t probe = 0; probe < nb; ++probe) {
+        const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(table + (int64_t)b * kBucketKeys + q * 2);
+        const bool found = (w.x == key) | (w.y == key);
+        const bool empty = (w.x == kEmptyKey) | (w.y == kEmptyKey);
+        if (((__ballot(found) >> shift) & 0xFull) != 0) return true;
+        if (((__ballot(empty) >> shift) & 0xFull) != 0) return false;
+        b = (b + 1 == nb) ? 0 : b + 1;
+    }
+    return false;
+}
+
+__device__ __forceinline__ int64_t search_run_wave(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
+                                                   const uint64_t* __restrict__ h, int64_t n, int lane) {
+    const int g = lane >> 2, q = lane & 3, shift = g * 4;
+    int64_t lo = 0, hi = n;                      // blocks [0, lo) cached; block hi is the first miss (or n)
+    while (lo < hi) {
+        const int64_t lo0 = lo, span = hi - lo;
+        // probed positions, increasing with the group index; all inside [lo0, hi)
+        auto pos = [&](int gg) -> int64_t { return span > 16 ? lo0 + ((int64_t)(gg + 1) * span) / 17 : lo0 + gg; };
+        const int64_t j = pos(g);
+        const bool act = j < hi;
+        bool hit = false;
+        if (act) hit = probe_block(table, nb, has_empty, h[j], q, shift);
+        const uint64_t hits = __ballot(q == 0 && act && hit);
+        const uint64_t miss = __ballot(q == 0 && act && !hit);
+        if (hits) lo = pos((63 - __clzll((long long)hits)) >> 2) + 1;
+        if (miss) hi = pos((__ffsll((long long)miss) - 1) >> 2);
+    }
+    return lo;
+}
+
 // ---------------------------------------------------------------------------
 // grouping by first block hash
 // ---------------------------------------------------------------------------
@@ -411,7 +454,7 @@ __global__ __launch_bounds__(256) void prefix_leaders_kernel(ProbeTables T, int3
                                                              const uint64_t* __restrict__ req_hashes,
                                                              const int32_t* __restrict__ leaders,
                                                              const uint32_t* __restrict__ n_leaders,
-                                                             int32_t* __restrict__ overlap) {
+                                                             int32_t* __restrict__ overlap, int closed) {
     const int lane = threadIdx.x & 63;
     const int64_t total = (int64_t)(*n_leaders) * N;
     const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
@@ -420,8 +463,9 @@ __global__ __launch_bounds__(256) void prefix_leaders_kernel(ProbeTables T, int3
         const int64_t r = leaders[k];
         const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
         const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
-        const int64_t l = extend_run_wave(table, T.nb[i], (T.flags[i] & kFlagHasEmptyKey) != 0, req_hashes + h0, n, 0,
-                                          lane);
+        const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
+        const int64_t l = closed ? search_run_wave(table, T.nb[i], he, req_hashes + h0, n, lane)
+                                 : extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 0, lane);
         if (lane == 0) overlap[r * N + i] = (int32_t)l;
     }
 }
@@ -525,7 +569,7 @@ bool prefix_use_join(int32_t R, int32_t N, int64_t table_slots, int mode) {
 
 hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const int64_t* req_off,
                                const uint64_t* req_hashes, int32_t* overlap, void* workspace, int n_cu,
-                               bool join, hipStream_t s) {
+                               bool join, bool closed, hipStream_t s) {
     const int64_t pairs = (int64_t)R * N;
     if (pairs <= 0) return hipSuccess;
     const int64_t G = group_table_size(R);
@@ -582,7 +626,7 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     int64_t wgrid = (pairs + 3) / 4;
     if (wgrid > (int64_t)n_cu * 16) wgrid = (int64_t)n_cu * 16;
     hipLaunchKernelGGL(prefix_leaders_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
-                       leaders, n_leaders, overlap);
+                       leaders, n_leaders, overlap, closed ? 1 : 0);
     // followers: slices of pairs, one workgroup each
     int64_t slices = (pairs + kResolveThreads - 1) / kResolveThreads;
     if (slices > (int64_t)n_cu * 8) slices = (int64_t)n_cu * 8;

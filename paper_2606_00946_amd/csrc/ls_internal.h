@@ -114,9 +114,11 @@ int64_t prefix_workspace_bytes(int32_t R, int32_t N);
 // Whether followers' continuations go through the semi-join (mode 0 decides
 // from the sizes, 1 always, 2 never).
 bool prefix_use_join(int32_t R, int32_t N, int64_t table_slots, int mode);
+// closed: leaders search the run end instead of walking it (exact only when
+// every cache is prefix-closed for every prompt).
 hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const int64_t* req_off,
                                const uint64_t* req_hashes, int32_t* overlap, void* workspace, int n_cu,
-                               bool join, hipStream_t s);
+                               bool join, bool closed, hipStream_t s);
 
 hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s);
 hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,

@@ -30,6 +30,7 @@ struct ls_ctx {
     float* frag32 = nullptr;
     bool exact_scores = false;
     int prefix_join = 0;     // 0 decide per call, 1 always, 2 never
+    bool prefix_closed = false;
     int n_cu = 1;
     // cache state
     ls::CacheTables tables;
@@ -522,7 +523,7 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
              ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu,
                                      ls::prefix_use_join(R, N, c->tables.total_buckets * ls::kBucketKeys,
                                                          c->prefix_join),
-                                     s));
+                                     c->prefix_closed, s));
     LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     const uint8_t* band = nullptr;
     if (fast) {
@@ -666,6 +667,13 @@ int ls_set_prefix_join(ls_ctx* c, int mode) {
     c->err.clear();
     if (mode < 0 || mode > 2) return fail(c, LS_ERR_INVALID, "prefix join mode must be 0, 1 or 2");
     c->prefix_join = mode;
+    return LS_OK;
+}
+
+int ls_set_prefix_closed(ls_ctx* c, int enable) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    c->prefix_closed = enable != 0;
     return LS_OK;
 }
 

@@ -87,11 +87,12 @@ def library():
         lib.ls_profile_enable.argtypes = [P, ctypes.c_int]
         lib.ls_set_exact_scores.argtypes = [P, ctypes.c_int]
         lib.ls_set_prefix_join.argtypes = [P, ctypes.c_int]
+        lib.ls_set_prefix_closed.argtypes = [P, ctypes.c_int]
         lib.ls_route_batch.argtypes = [P, ctypes.POINTER(ls_policy), i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
-                  lib.ls_set_prefix_join, lib.ls_route_batch):
+                  lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -273,6 +274,9 @@ class Context:
 
     def ls_set_exact_scores(self, enable=True):
         return self._check("ls_set_exact_scores", self.lib.ls_set_exact_scores(self.h, 1 if enable else 0))
+
+    def ls_set_prefix_closed(self, enable=True):
+        return self._check("ls_set_prefix_closed", self.lib.ls_set_prefix_closed(self.h, 1 if enable else 0))
 
     def ls_set_prefix_join(self, mode=0):
         return self._check("ls_set_prefix_join", self.lib.ls_set_prefix_join(self.h, int(mode)))

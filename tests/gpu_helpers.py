@@ -59,7 +59,7 @@ def head_magnitude(w, rows):
 class GpuRun:
     """A context loaded with one workload's model and cache state."""
 
-    def __init__(self, w, dtype=None, params=None, exact=False, prefix_join=0):
+    def __init__(self, w, dtype=None, params=None, exact=False, prefix_join=0, prefix_closed=False):
         import torch
         self.w = w
         cfg = w.cfg
@@ -69,6 +69,8 @@ class GpuRun:
             self.ctx.ls_set_exact_scores(True)
         if prefix_join:
             self.ctx.ls_set_prefix_join(prefix_join)
+        if prefix_closed:
+            self.ctx.ls_set_prefix_closed(True)
         self.ctx.ls_set_model(w.params if params is None else params, w.mu, w.inv_sigma)
         self.inst_hashes = to_dev(w.inst_hashes)
         self.ctx.ls_load_cache_state(w.inst_off, self.inst_hashes)

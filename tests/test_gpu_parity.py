@@ -424,6 +424,19 @@ def test_join_modes_agree_on_a_full_workload(mode):
     np.testing.assert_array_equal(out["overlap"][sel], want)
 
 
+@pytest.mark.parametrize("name", CONFIGS)
+def test_prefix_closed_search(name):
+    """The run-end search for prefix-closed caches (the synthetic caches are,
+    see test_inputs_cpu.py) gives the oracle's overlaps and decisions."""
+    w = workload(name)
+    note(f"prefix-closed search {name}")
+    out = GpuRun(w, prefix_closed=True).score()
+    sel = sampled(w)
+    want = oracle.overlap(w.req_off, w.req_hashes, w.inst_off, w.inst_hashes, sel=sel)
+    np.testing.assert_array_equal(out["overlap"][sel], want)
+    check_scoring(w, out, sel)
+
+
 def test_ties_go_to_lowest_instance():
     """Instances with identical state and cache score identically; the lowest id wins."""
     note("exact ties")
