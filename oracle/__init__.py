@@ -64,7 +64,13 @@ def _open(path):
         lib.lso_heuristic.restype = i32
         lib.lso_route.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, P, P, i32, P, P, P,
                                   ctypes.POINTER(Policy), P, P, P, P, ctypes.c_int]
-        for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update, lib.lso_route):
+        lib.lso_embed.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, P]
+        lib.lso_buffer_push.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, i32, P, P, P, P, P, P, P, i32, P, P,
+                                        P]
+        lib.lso_train_round.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, i32, i32, P, P, i32, P, P, i32, i32,
+                                        f32, P, P]
+        for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update, lib.lso_route, lib.lso_embed,
+                  lib.lso_buffer_push, lib.lso_train_round):
             f.restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
@@ -256,3 +262,65 @@ def route(mode, d, hidden, params, mu, inv_sigma, req_off, req_hashes, prompt_le
                        _ptr(heur), threads)
     assert rc == 0, rc
     return chosen, status, heur
+
+
+def embed(mode, d, hidden, params, mu, inv_sigma, x, y) -> np.ndarray:
+    """Gradient-coreset embeddings (t - y) a_L of raw rows, [n x h_last] double."""
+    lib = _load()
+    h = _c(hidden, np.int32)
+    x = _c(x, np.float32).reshape(-1, d); y = _c(y, np.float32)
+    out = np.zeros((x.shape[0], int(h[-1])), np.float64)
+    rc = lib.lso_embed(_mode(mode), d, h.shape[0], _ptr(h), _ptr(_c(params, np.float32)), _ptr(_c(mu, np.float32)),
+                       _ptr(_c(inv_sigma, np.float32)), x.shape[0], _ptr(x), _ptr(y), _ptr(out))
+    assert rc == 0, rc
+    return out
+
+
+class Buffer:
+    """Host state of the two-pool training buffer (FIFO ring + replay pool)."""
+
+    def __init__(self, d, fifo_cap, rep_cap):
+        self.d, self.fifo_cap, self.rep_cap = d, fifo_cap, rep_cap
+        self.fifo_count = np.zeros(1, np.int32); self.fifo_head = np.zeros(1, np.int32)
+        self.fifo_x = np.zeros((fifo_cap, d), np.float32); self.fifo_y = np.zeros(fifo_cap, np.float32)
+        self.rep_count = np.zeros(1, np.int32)
+        self.rep_x = np.zeros((max(rep_cap, 1), d), np.float32); self.rep_y = np.zeros(max(rep_cap, 1), np.float32)
+
+    def fifo_rows(self):
+        idx = [(int(self.fifo_head[0]) + k) % self.fifo_cap for k in range(int(self.fifo_count[0]))]
+        return self.fifo_x[idx], self.fifo_y[idx]
+
+    def replay_rows(self):
+        n = int(self.rep_count[0])
+        return self.rep_x[:n], self.rep_y[:n]
+
+
+def buffer_push(mode, hidden, params, mu, inv_sigma, buf, x, y) -> int:
+    """Push rows into the buffer (FIFO, then gradient-coreset admission); returns the number admitted."""
+    lib = _load()
+    h = _c(hidden, np.int32)
+    x = _c(x, np.float32).reshape(-1, buf.d); y = _c(y, np.float32)
+    adm = np.zeros(1, np.int32)
+    rc = lib.lso_buffer_push(_mode(mode), buf.d, h.shape[0], _ptr(h), _ptr(_c(params, np.float32)),
+                             _ptr(_c(mu, np.float32)), _ptr(_c(inv_sigma, np.float32)), buf.fifo_cap, buf.rep_cap,
+                             _ptr(buf.fifo_count), _ptr(buf.fifo_head), _ptr(buf.fifo_x), _ptr(buf.fifo_y),
+                             _ptr(buf.rep_count), _ptr(buf.rep_x), _ptr(buf.rep_y), x.shape[0], _ptr(x), _ptr(y),
+                             _ptr(adm))
+    assert rc == 0, rc
+    return int(adm[0])
+
+
+def train_round(mode, hidden, params, mu, inv_sigma, buf, epochs, batch, lr, perm=None):
+    """One retraining round over FIFO and pool; returns (new params, mean loss of the last epoch)."""
+    lib = _load()
+    h = _c(hidden, np.int32)
+    p = _c(params, np.float32).copy()
+    perm_a = None if perm is None else _c(perm, np.int32)
+    loss = np.zeros(1, np.float64)
+    rc = lib.lso_train_round(_mode(mode), buf.d, h.shape[0], _ptr(h), _ptr(p), _ptr(_c(mu, np.float32)),
+                             _ptr(_c(inv_sigma, np.float32)), buf.fifo_cap, int(buf.fifo_count[0]),
+                             int(buf.fifo_head[0]), _ptr(buf.fifo_x), _ptr(buf.fifo_y), int(buf.rep_count[0]),
+                             _ptr(buf.rep_x), _ptr(buf.rep_y), int(epochs), int(batch), float(lr), _ptr(perm_a),
+                             _ptr(loss))
+    assert rc == 0, rc
+    return p, float(loss[0])

@@ -237,9 +237,11 @@ static float* bf16_weights(const lso_net* net, const float* params)
 
 /* One pair in the kernel's precision (fp32 fma chains, optional bf16 operands).
  * In LSO_BF16 mode `net` must already hold bf16-rounded weights (bf16_weights);
- * the inputs and activations of every layer are rounded here. */
+ * the inputs and activations of every layer are rounded here.  `last`
+ * (nullable) receives the input of the output layer (the last hidden layer's
+ * activations). */
 static float forward_lowp(int mode, const lso_net* net, const float* mu, const float* inv_sigma, const double* x,
-                          float* buf_a, float* buf_b)
+                          float* buf_a, float* buf_b, float* last)
 {
     int bf = (mode == LSO_BF16);
     int d = net->in[0];
@@ -260,7 +262,10 @@ static float forward_lowp(int mode, const lso_net* net, const float* mu, const f
             }
             z[j] = acc;
         }
-        if (l + 1 == net->n_layers) return z[0];
+        if (l + 1 == net->n_layers) {
+            if (last) memcpy(last, a, sizeof(float) * (size_t)K);
+            return z[0];
+        }
         for (int j = 0; j < O; ++j) {
             float h = z[j] > 0.0f ? z[j] : 0.0f;
             z[j] = bf ? lso_bf16_round(h) : h;
@@ -292,7 +297,7 @@ int lso_forward(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, co
         for (int64_t r = 0; r < rows; ++r) {
             const double* xr = x + r * d;
             scores[r] = (mode == LSO_F64) ? forward_f64(&net, mu, inv_sigma, xr, da, db)
-                                          : (double)forward_lowp(mode, &net, mu, inv_sigma, xr, fa, fb);
+                                          : (double)forward_lowp(mode, &net, mu, inv_sigma, xr, fa, fb, NULL);
         }
         free(da); free(db); free(fa); free(fb);
     }
@@ -368,7 +373,7 @@ int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
                 double* xi = x + (int64_t)i * d;
                 lso_features(mode, d_inst, inst_feat + (int64_t)i * d_inst, prompt_len[r], (int32_t)n, ov[i], xi);
                 s[i] = (mode == LSO_F64) ? forward_f64(&net, mu, inv_sigma, xi, da, db)
-                                         : (double)forward_lowp(mode, &net, mu, inv_sigma, xi, fa, fb);
+                                         : (double)forward_lowp(mode, &net, mu, inv_sigma, xi, fa, fb, NULL);
             }
             double m;
             int32_t c = lso_argmin(N, s, &m);
@@ -722,5 +727,207 @@ int lso_route(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
         if (heur_out) heur_out[q] = heur;
     }
     free(ov); free(sc); free(cnt); free(inst_ok); free(m); free(C); free(S);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Online-learning data path (Section 4.3.2, Training-data selection): a FIFO */
+/* of the newest samples and a replay pool that admits samples evicted from  */
+/* the FIFO by a gradient-coreset rule, and a retraining round over both.    */
+/*                                                                           */
+/* Gradient coreset: a sample's embedding is its prediction residual times   */
+/* its last-hidden-layer activations, e = (t - y) a_L -- the gradient of the */
+/* squared loss with respect to the output weights, up to the factor 2 --    */
+/* evaluated with the current model in the kernel's precision (the residual  */
+/* in fp32, the products and distances in double, summed over units in       */
+/* ascending order).  Embeddings of the pool are re-evaluated at the start   */
+/* of every push.  A candidate joins a pool with room; a full pool takes it  */
+/* in place of its most redundant member (the one with the smallest nearest- */
+/* neighbour distance, lowest slot on ties) when the candidate's distance to */
+/* the pool is larger than that member's.  Candidates are the samples the    */
+/* FIFO evicts, oldest first.                                                 */
+/* ------------------------------------------------------------------------- */
+
+static double emb_dist(const double* a, const double* b, int32_t H)
+{
+    double s = 0.0;
+    for (int32_t j = 0; j < H; ++j) {
+        double e = a[j] - b[j];
+        s += e * e;
+    }
+    return s;
+}
+
+/* nearest neighbour of slot k among slots [0, n) other than k (lowest slot on ties) */
+static void nn_of(const double* emb, int32_t H, int32_t n, int32_t k, double* dist, int32_t* idx)
+{
+    double best = INFINITY;
+    int32_t bi = -1;
+    for (int32_t j = 0; j < n; ++j) {
+        if (j == k) continue;
+        double v = emb_dist(emb + (int64_t)k * H, emb + (int64_t)j * H, H);
+        if (v < best) { best = v; bi = j; }
+    }
+    *dist = best;
+    *idx = bi;
+}
+
+/* Gradient-coreset embeddings of n raw rows: e[k][j] = (t_k - y_k) a_L[k][j]. */
+int lso_embed(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params, const float* mu,
+              const float* inv_sigma, int32_t n, const float* x, const float* y, double* emb)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    float* q = NULL;
+    if (mode == LSO_BF16) {
+        q = bf16_weights(&net, params);
+        net_init(&net, d, n_hidden, hidden, q);
+    }
+    int32_t H = net.in[net.n_layers - 1];
+    float* fa = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+    float* fb = (float*)malloc(sizeof(float) * (size_t)net.max_width);
+    float* last = (float*)malloc(sizeof(float) * (size_t)H);
+    double* xr = (double*)malloc(sizeof(double) * (size_t)d);
+    for (int32_t k = 0; k < n; ++k) {
+        for (int32_t c = 0; c < d; ++c) xr[c] = (double)x[(int64_t)k * d + c];
+        float t = forward_lowp(mode == LSO_F64 ? LSO_F32 : mode, &net, mu, inv_sigma, xr, fa, fb, last);
+        float res = t - y[k];
+        for (int32_t j = 0; j < H; ++j) emb[(int64_t)k * H + j] = (double)res * (double)last[j];
+    }
+    free(fa); free(fb); free(last); free(xr); free(q);
+    return 0;
+}
+
+int lso_buffer_push(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, const float* params,
+                    const float* mu, const float* inv_sigma, int32_t fifo_cap, int32_t rep_cap,
+                    int32_t* fifo_count, int32_t* fifo_head, float* fifo_x, float* fifo_y,
+                    int32_t* rep_count, float* rep_x, float* rep_y, int32_t B, const float* x, const float* y,
+                    int32_t* n_admitted)
+{
+    lso_net net;
+    if (net_init(&net, d, n_hidden, hidden, params)) return -1;
+    if (fifo_cap < 1 || rep_cap < 0 || B < 0) return -1;
+    float* q = NULL;
+    if (mode == LSO_BF16) {
+        q = bf16_weights(&net, params);
+        net_init(&net, d, n_hidden, hidden, q);
+    }
+    int32_t H = net.in[net.n_layers - 1];
+    /* 1. the FIFO takes the new samples; the ones it evicts are the candidates, oldest first */
+    float* cx = (float*)malloc(sizeof(float) * (size_t)(B > 0 ? B : 1) * d);
+    float* cy = (float*)malloc(sizeof(float) * (size_t)(B > 0 ? B : 1));
+    int32_t nc = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        if (*fifo_count < fifo_cap) {
+            int32_t slot = (*fifo_head + *fifo_count) % fifo_cap;
+            memcpy(fifo_x + (int64_t)slot * d, x + (int64_t)b * d, sizeof(float) * (size_t)d);
+            fifo_y[slot] = y[b];
+            ++*fifo_count;
+        } else {
+            int32_t slot = *fifo_head;
+            memcpy(cx + (int64_t)nc * d, fifo_x + (int64_t)slot * d, sizeof(float) * (size_t)d);
+            cy[nc++] = fifo_y[slot];
+            memcpy(fifo_x + (int64_t)slot * d, x + (int64_t)b * d, sizeof(float) * (size_t)d);
+            fifo_y[slot] = y[b];
+            *fifo_head = (slot + 1) % fifo_cap;
+        }
+    }
+    /* 2. embeddings of the pool and of the candidates with the current model */
+    int32_t n0 = *rep_count;
+    double* emb = (double*)malloc(sizeof(double) * (size_t)(rep_cap > 0 ? rep_cap : 1) * H);
+    double* ce = (double*)malloc(sizeof(double) * (size_t)(nc > 0 ? nc : 1) * H);
+    if (n0 > 0) lso_embed(mode, d, n_hidden, hidden, params, mu, inv_sigma, n0, rep_x, rep_y, emb);
+    if (nc > 0) lso_embed(mode, d, n_hidden, hidden, params, mu, inv_sigma, nc, cx, cy, ce);
+    /* 3. nearest neighbours inside the pool */
+    double* nnd = (double*)malloc(sizeof(double) * (size_t)(rep_cap > 0 ? rep_cap : 1));
+    int32_t* nni = (int32_t*)malloc(sizeof(int32_t) * (size_t)(rep_cap > 0 ? rep_cap : 1));
+    for (int32_t k = 0; k < n0; ++k) nn_of(emb, H, n0, k, &nnd[k], &nni[k]);
+    /* 4. admission, one candidate at a time */
+    int32_t n = n0, admitted = 0;
+    for (int32_t c = 0; c < nc && rep_cap > 0; ++c) {
+        const double* e = ce + (int64_t)c * H;
+        int32_t slot;
+        if (n < rep_cap) {
+            slot = n++;
+        } else {
+            double dc = INFINITY;
+            for (int32_t k = 0; k < n; ++k) {
+                double v = emb_dist(e, emb + (int64_t)k * H, H);
+                if (v < dc) dc = v;
+            }
+            int32_t js = 0;
+            for (int32_t k = 1; k < n; ++k)
+                if (nnd[k] < nnd[js]) js = k;
+            if (!(dc > nnd[js])) continue;
+            slot = js;
+        }
+        memcpy(emb + (int64_t)slot * H, e, sizeof(double) * (size_t)H);
+        memcpy(rep_x + (int64_t)slot * d, cx + (int64_t)c * d, sizeof(float) * (size_t)d);
+        rep_y[slot] = cy[c];
+        ++admitted;
+        for (int32_t k = 0; k < n; ++k) {
+            if (k == slot) continue;
+            if (nni[k] == slot) {
+                nn_of(emb, H, n, k, &nnd[k], &nni[k]);
+            } else {
+                double v = emb_dist(emb + (int64_t)k * H, e, H);
+                if (v < nnd[k] || (v == nnd[k] && slot < nni[k])) { nnd[k] = v; nni[k] = slot; }
+            }
+        }
+        nn_of(emb, H, n, slot, &nnd[slot], &nni[slot]);
+    }
+    *rep_count = n;
+    if (n_admitted) *n_admitted = admitted;
+    free(cx); free(cy); free(emb); free(ce); free(nnd); free(nni); free(q);
+    return 0;
+}
+
+/* One retraining round over the FIFO (oldest first) and the pool (by slot):  */
+/* per epoch the samples are visited in the order perm gives (NULL: natural), */
+/* in minibatches of `batch` (the last one may be shorter), one SGD step of   */
+/* lso_update each.  loss_out (nullable) gets the mean minibatch loss of the  */
+/* last epoch.                                                                 */
+int lso_train_round(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params, const float* mu,
+                    const float* inv_sigma, int32_t fifo_cap, int32_t fifo_count, int32_t fifo_head,
+                    const float* fifo_x, const float* fifo_y, int32_t rep_count, const float* rep_x,
+                    const float* rep_y, int32_t epochs, int32_t batch, float lr, const int32_t* perm,
+                    double* loss_out)
+{
+    int32_t n = fifo_count + rep_count;
+    if (n < 1 || batch < 1 || epochs < 0) return -1;
+    float* X = (float*)malloc(sizeof(float) * (size_t)n * d);
+    float* Y = (float*)malloc(sizeof(float) * (size_t)n);
+    for (int32_t k = 0; k < fifo_count; ++k) {
+        int32_t slot = (fifo_head + k) % fifo_cap;
+        memcpy(X + (int64_t)k * d, fifo_x + (int64_t)slot * d, sizeof(float) * (size_t)d);
+        Y[k] = fifo_y[slot];
+    }
+    for (int32_t k = 0; k < rep_count; ++k) {
+        memcpy(X + (int64_t)(fifo_count + k) * d, rep_x + (int64_t)k * d, sizeof(float) * (size_t)d);
+        Y[fifo_count + k] = rep_y[k];
+    }
+    float* bx = (float*)malloc(sizeof(float) * (size_t)batch * d);
+    float* by = (float*)malloc(sizeof(float) * (size_t)batch);
+    double last = 0.0;
+    for (int32_t ep = 0; ep < epochs; ++ep) {
+        double lsum = 0.0;
+        int32_t nb = 0;
+        for (int32_t s = 0; s < n; s += batch) {
+            int32_t m = n - s < batch ? n - s : batch;
+            for (int32_t u = 0; u < m; ++u) {
+                int32_t k = perm ? perm[(int64_t)ep * n + s + u] : s + u;
+                memcpy(bx + (int64_t)u * d, X + (int64_t)k * d, sizeof(float) * (size_t)d);
+                by[u] = Y[k];
+            }
+            double loss;
+            int rc = lso_update(mode, d, n_hidden, hidden, params, mu, inv_sigma, m, bx, by, lr, NULL, &loss);
+            if (rc) { free(X); free(Y); free(bx); free(by); return rc; }
+            lsum += loss;
+            ++nb;
+        }
+        last = lsum / (double)nb;
+    }
+    if (loss_out) *loss_out = last;
+    free(X); free(Y); free(bx); free(by);
     return 0;
 }

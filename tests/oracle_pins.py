@@ -589,4 +589,131 @@ def pin_route_exact_ties():
         assert c_[r] == tied[_scaled(rnd[r, 2], len(tied))] and st[r] == oracle.ROUTE_TIEBREAK
 
 
+# ---------------------------------------------------------------------------
+# online-learning data path: embeddings, FIFO, gradient-coreset admission, round
+# ---------------------------------------------------------------------------
+def _tiny_model():
+    from paper_2606_00946_amd import synth
+    return synth.generate("tiny")
+
+
+def _numpy_forward_f64(w, x):
+    """(t, last hidden activations) in double, from the packed parameters."""
+    d, (h1, h2) = w.cfg.d, w.cfg.hidden
+    p = w.params.astype(np.float64)
+    o = 0
+    W1 = p[o:o + h1 * d].reshape(h1, d); o += h1 * d
+    b1 = p[o:o + h1]; o += h1
+    W2 = p[o:o + h2 * h1].reshape(h2, h1); o += h2 * h1
+    b2 = p[o:o + h2]; o += h2
+    W3 = p[o:o + h2]; o += h2
+    b3 = p[o]
+    xt = (x.astype(np.float64) - w.mu) * w.inv_sigma
+    a1 = np.maximum(xt @ W1.T + b1, 0)
+    a2 = np.maximum(a1 @ W2.T + b2, 0)
+    return a2 @ W3 + b3, a2
+
+
+def pin_embedding_definition():
+    w = _tiny_model()
+    x, y = w.upd_feats[:50], w.upd_ttft[:50]
+    e = oracle.embed("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, x, y)
+    t, a2 = _numpy_forward_f64(w, x)
+    ref = (t - y.astype(np.float64))[:, None] * a2
+    assert e.shape == ref.shape
+    assert np.linalg.norm(e - ref) <= 1e-4 * np.linalg.norm(ref)
+    # a zero residual gives a zero embedding
+    tk = oracle.forward("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, x).astype(np.float32)
+    assert np.all(oracle.embed("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, x, tk) == 0.0)
+
+
+def _stream(w, n, dup_every=5):
+    """n update rows with every dup_every-th a copy of an earlier one (exact ties)."""
+    x = w.upd_feats[:n].copy(); y = w.upd_ttft[:n].copy()
+    for k in range(dup_every, n, dup_every):
+        x[k] = x[k // 2]; y[k] = y[k // 2]
+    return x, y
+
+
+def _sq(a, b):
+    s = 0.0
+    for u, v in zip(a, b):
+        s += (u - v) * (u - v)
+    return s
+
+
+def _check_buffer_stream(w, x, y, F, P, chunks):
+    """Push x in the given chunk sizes and compare the FIFO and the pool with a
+    brute-force replay that recomputes every nearest-neighbour distance."""
+    cfg = w.cfg
+    buf = oracle.Buffer(cfg.d, F, P)
+    pool, fifo, evicted, s = [], [], 0, 0
+    for k in chunks:
+        chunk = list(range(s, min(s + k, len(x))))
+        cands = []
+        for b in chunk:
+            if len(fifo) == F:
+                cands.append(fifo.pop(0))
+            fifo.append(b)
+        rows = pool + cands
+        if rows:
+            E = oracle.embed("fp32", cfg.d, cfg.hidden, w.params, w.mu, w.inv_sigma, x[rows], y[rows])
+            emb = {r: list(E[q]) for q, r in enumerate(rows)}
+        for c in cands:
+            if len(pool) < P:
+                pool.append(c)
+                continue
+            dc = min(_sq(emb[c], emb[m]) for m in pool)
+            nn = [min(_sq(emb[pool[a]], emb[pool[b]]) for b in range(len(pool)) if b != a) for a in range(len(pool))]
+            js = min(range(len(pool)), key=lambda a: (nn[a], a))
+            if dc > nn[js]:
+                pool[js] = c
+        oracle.buffer_push("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, x[chunk], y[chunk])
+        evicted += len(cands)
+        fx, fy = buf.fifo_rows()
+        np.testing.assert_array_equal(fx, x[fifo]); np.testing.assert_array_equal(fy, y[fifo])
+        rx, ry = buf.replay_rows()
+        assert int(buf.rep_count[0]) == min(P, evicted)
+        np.testing.assert_array_equal(rx, x[pool]); np.testing.assert_array_equal(ry, y[pool])
+        s += k
+
+
+def pin_buffer_fifo_and_gcr(seed=37):
+    """FIFO keeps the newest rows in order; the pool follows the admission rule."""
+    w = _tiny_model()
+    x, y = _stream(w, 90)
+    rng = np.random.default_rng(seed)
+    _check_buffer_stream(w, x, y, 12, 6, [int(v) for v in rng.integers(1, 9, 40)])
+    # an exact tie: the pool holds a duplicated pair (distance 0) and a candidate
+    # duplicates another member (distance 0): it must not be admitted
+    a, b, z = w.upd_feats[0], w.upd_feats[1], w.upd_feats[2]
+    ya, yb, yz = w.upd_ttft[0], w.upd_ttft[1], w.upd_ttft[2]
+    x2 = np.stack([a, a, b, b, z]); y2 = np.array([ya, ya, yb, yb, yz], np.float32)
+    _check_buffer_stream(w, x2, y2, 1, 3, [1] * 5)
+
+
+def pin_train_round_composition():
+    """A round is minibatch SGD over the FIFO (oldest first) then the pool, in
+    the given order, the last minibatch possibly shorter."""
+    w = _tiny_model()
+    cfg = w.cfg
+    buf = oracle.Buffer(cfg.d, 10, 4)
+    x, y = w.upd_feats[:23], w.upd_ttft[:23]
+    oracle.buffer_push("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, x, y)
+    fx, fy = buf.fifo_rows(); rx, ry = buf.replay_rows()
+    X = np.concatenate([fx, rx]); Y = np.concatenate([fy, ry])
+    n = X.shape[0]
+    perm = np.concatenate([np.random.default_rng(e).permutation(n) for e in range(2)]).astype(np.int32)
+    got, _ = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 2, 4, 0.05, perm)
+    p = w.params.copy()
+    for e in range(2):
+        order = perm[e * n:(e + 1) * n]
+        for s0 in range(0, n, 4):
+            idx = order[s0:s0 + 4]
+            p = oracle.update("fp32", cfg.d, cfg.hidden, p, w.mu, w.inv_sigma, X[idx], Y[idx], 0.05)["params"]
+    np.testing.assert_array_equal(got, p)
+    same, _ = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 0, 4, 0.05)
+    np.testing.assert_array_equal(same, w.params)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

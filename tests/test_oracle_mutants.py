@@ -82,6 +82,15 @@ MUTANTS = [
     ("kfilter_ignores_benefit", "saturated && kl_max > pol->tau_ben", "saturated"),
     ("tiebreak_ignores_scope", "if (scope && s[i] <= lim) S[ns++] = i;", "if (s[i] <= lim) S[ns++] = i;"),
     ("tiebreak_strict", "if (scope && s[i] <= lim) S[ns++] = i;", "if (scope && s[i] < lim) S[ns++] = i;"),
+    ("gcr_admits_ties", "if (!(dc > nnd[js])) continue;", "if (!(dc >= nnd[js])) continue;"),
+    ("gcr_replaces_most_isolated", "if (nnd[k] < nnd[js]) js = k;", "if (nnd[k] > nnd[js]) js = k;"),
+    ("gcr_stale_neighbours", "            if (nni[k] == slot) {\n                nn_of(emb, H, n, k, &nnd[k], &nni[k]);",
+     "            if (0) {\n                nn_of(emb, H, n, k, &nnd[k], &nni[k]);"),
+    ("fifo_head_not_advanced", "*fifo_head = (slot + 1) % fifo_cap;", "*fifo_head = slot;"),
+    ("embed_abs_residual", "float res = t - y[k];", "float res = fabsf(t - y[k]);"),
+    ("train_drops_partial_batch", "int32_t m = n - s < batch ? n - s : batch;",
+     "int32_t m = batch;\n            if (n - s < batch) break;"),
+    ("train_skips_replay", "int32_t n = fifo_count + rep_count;", "int32_t n = fifo_count;"),
 ]
 
 _RUNNER = r"""
