@@ -282,12 +282,57 @@ int ls_route_batch(ls_ctx* ctx, const ls_policy* policy, int32_t R, int32_t N,
                    int32_t* chosen, int32_t* status, int32_t* heur, float* feat_out, void* stream);
 
 /*
+ * Online-learning data path (Section 4.3.2, Training-data selection).
+ *
+ * The context keeps a FIFO of the newest fifo_cap logged samples and a replay
+ * pool of up to replay_cap older ones on the device.  Samples the FIFO evicts
+ * (oldest first) are offered to the pool by a gradient-coreset rule: a
+ * sample's embedding is its prediction residual times its last-hidden-layer
+ * activations, (t - y) a_L -- the output-weight gradient of the squared loss,
+ * from the current model in kernel precision, with distances in double.  A
+ * pool with room takes the sample; a full pool takes it in place of its most
+ * redundant member (smallest nearest-neighbour distance, lowest slot on ties)
+ * when the sample's distance to the pool is larger.  Embeddings are
+ * re-evaluated with the current model at every push.  A retraining round runs
+ * minibatch SGD (ls_update steps) over the FIFO and the pool.
+ *
+ *   ls_buffer_init   allocates empty pools (fifo_cap >= 1, replay_cap >= 0);
+ *                    synchronous; discards any earlier contents.
+ *   ls_buffer_push   appends B raw rows feats [B x d] and ttft [B] (device);
+ *                    admitted (device int32, nullable) gets the number of
+ *                    samples the pool took.  Stream-ordered.
+ *   ls_buffer_state  host counters: FIFO size, FIFO ring start, pool size.
+ *   ls_buffer_read   copies the FIFO (oldest first, [fifo_count x d] and
+ *                    [fifo_count]) and the pool (by slot) to device arrays
+ *                    (each nullable).  Stream-ordered.
+ *   ls_train_round   epochs passes over the n = FIFO + pool samples, sample k
+ *                    being the k-th oldest FIFO entry for k < FIFO size and
+ *                    pool slot k - FIFO size after it.  perm (host, nullable)
+ *                    gives each epoch's visiting order as epochs rows of a
+ *                    permutation of [0, n) (NULL: natural order); minibatches
+ *                    of `batch` in that order, the last one possibly shorter,
+ *                    one SGD step of learning rate lr each.  loss_out (device,
+ *                    nullable) gets the mean pre-step minibatch loss of the
+ *                    last epoch.  The model is updated in place, so scoring
+ *                    calls ordered after the round see the new model.
+ * Errors: LS_ERR_STATE before ls_buffer_init, without a model, or on an empty
+ * buffer (train); LS_ERR_INVALID for bad sizes or a perm that is not a
+ * permutation.
+ */
+int ls_buffer_init(ls_ctx* ctx, int32_t fifo_cap, int32_t replay_cap);
+int ls_buffer_push(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, int32_t* admitted, void* stream);
+int ls_buffer_state(ls_ctx* ctx, int32_t* fifo_count, int32_t* fifo_head, int32_t* replay_count);
+int ls_buffer_read(ls_ctx* ctx, float* fifo_x, float* fifo_y, float* replay_x, float* replay_y, void* stream);
+int ls_train_round(ls_ctx* ctx, int32_t epochs, int32_t batch, float lr, const int32_t* perm, float* loss_out,
+                   void* stream);
+
+/*
  * Per-kernel timing (the library's own view of where the routing time goes;
  * Section 5.4 measures the router's overhead end to end).  While enabled, each
  * kernel launch group of the context is bracketed by HIP events on the stream
  * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
  * "score_pairs", "score_pairs_mfma", "band_select", "rescore", "argmin",
- * "update", "route".
+ * "update", "route", "buffer".
  *   ls_profile_enable  enable != 0 starts recording (and clears old records).
  *   ls_profile_read    synchronous; for up to max_kinds kinds writes the kind
  *                      name (static string), the number of launches and the

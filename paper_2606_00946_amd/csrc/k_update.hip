@@ -719,6 +719,56 @@ static hipError_t weight_grad(const float* A, const float* Bt, int M, int N, int
     return hipGetLastError();
 }
 
+// Forward pass of B raw rows in the kernel's precision (the canonical chains),
+// keeping every layer feature-major: xn [d][B], z1/a1 [h1][B], z2/a2 [h2][B], t [B].
+template <bool BF>
+static void forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
+                         const float* feats, float* xn, float* z1, float* a1, float* z2, float* a2, float* t,
+                         hipStream_t s) {
+    const int64_t nB = B;
+    hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, xn, B,
+                       m.d);
+    const uint32_t sb = blocks_for(nB, 256);
+    const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
+    const bool lds_w = m.d <= kDenseMaxK && m.h1 <= kDenseMaxK && m.h2 <= kDenseMaxK;
+    if (lds_w) {
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, xn,
+                           compute + m.c_w1t, compute + m.c_b1, nullptr, z1, a1, B, m.d, m.h1);
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h2 + 31) / 32), dim3(256), 0, s, a1,
+                           compute + m.c_w2t, compute + m.c_b2, nullptr, z2, a2, B, m.h1, m.h2);
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, a2, compute + m.c_w3,
+                           compute + m.c_b3, nullptr, t, nullptr, B, m.h2, 1);
+    } else {
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, xn,
+                           compute + m.c_w1t, compute + m.c_b1, z1, a1, B, m.d, m.h1);
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, a1,
+                           compute + m.c_w2t, compute + m.c_b2, z2, a2, B, m.h1, m.h2);
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, a2, compute + m.c_w3,
+                           compute + m.c_b3, t, nullptr, B, m.h2, 1);
+    }
+}
+
+int64_t forward_rows_floats(const ModelDims& m, int32_t B) {
+    return (int64_t)B * (m.d + 2 * m.h1 + 2 * m.h2 + 1) + 6 * 64;
+}
+
+hipError_t launch_forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
+                               const float* feats, float* ws, float** a2_out, float** t_out, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    auto take = [&](int64_t n) { float* p = ws; ws += (n + 63) & ~int64_t(63); return p; };
+    float* xn = take((int64_t)m.d * B);
+    float* z1 = take((int64_t)m.h1 * B);
+    float* a1 = take((int64_t)m.h1 * B);
+    float* z2 = take((int64_t)m.h2 * B);
+    float* a2 = take((int64_t)m.h2 * B);
+    float* t = take(B);
+    if (m.bf16) forward_rows<true>(m, compute, mu, isig, B, feats, xn, z1, a1, z2, a2, t, s);
+    else forward_rows<false>(m, compute, mu, isig, B, feats, xn, z1, a1, z2, a2, t, s);
+    *a2_out = a2;
+    *t_out = t;
+    return hipGetLastError();
+}
+
 template <bool BF>
 static hipError_t run_update(const ModelDims& m, float* master, float* compute, const float* mu, const float* isig,
                              int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
@@ -726,26 +776,9 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     UpdWs w = plan_ws(m, B, reinterpret_cast<char*>(workspace));
     const int64_t nB = B;
     // forward, saving pre-activations and activations
-    hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, w.xn,
-                       B, m.d);
-    const uint32_t sb = blocks_for(nB, 256);
+    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.z1, w.a1, w.z2, w.a2, w.t, s);
     const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
     const bool lds_w = m.d <= kDenseMaxK && m.h1 <= kDenseMaxK && m.h2 <= kDenseMaxK;
-    if (lds_w) {
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
-                           compute + m.c_w1t, compute + m.c_b1, nullptr, w.z1, w.a1, B, m.d, m.h1);
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
-                           compute + m.c_w2t, compute + m.c_b2, nullptr, w.z2, w.a2, B, m.h1, m.h2);
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, w.a2,
-                           compute + m.c_w3, compute + m.c_b3, nullptr, w.t, nullptr, B, m.h2, 1);
-    } else {
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, w.xn,
-                           compute + m.c_w1t, compute + m.c_b1, w.z1, w.a1, B, m.d, m.h1);
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, w.a1,
-                           compute + m.c_w2t, compute + m.c_b2, w.z2, w.a2, B, m.h1, m.h2);
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, w.a2,
-                           compute + m.c_w3, compute + m.c_b3, w.t, nullptr, B, m.h2, 1);
-    }
     // loss and output gradient
     hipLaunchKernelGGL(loss_grad_kernel<BF>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
     if (loss_out)

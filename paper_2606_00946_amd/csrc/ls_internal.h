@@ -163,6 +163,24 @@ hipError_t launch_rescore(const ModelDims& m, const float* compute, const float*
                           const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
                           const uint32_t* count, float* scores, int n_cu, hipStream_t s);
 
+// Forward pass of B raw rows (canonical chains, kernel precision); a2 [h2][B]
+// and t [B] point into ws, which holds forward_rows_floats(m, B) floats.
+int64_t forward_rows_floats(const ModelDims& m, int32_t B);
+hipError_t launch_forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
+                               const float* feats, float* ws, float** a2_out, float** t_out, hipStream_t s);
+
+// Online-learning data path: row gathers and scatters, and the gradient-coreset
+// admission of nc candidates into a pool of n0 members (cap slots).
+hipError_t launch_gather_rows(const int32_t* code, int32_t n, int d, const float* ax, const float* ay,
+                              const float* bx, const float* by, float* ox, float* oy, hipStream_t s);
+hipError_t launch_scatter_rows(const int32_t* dst, int32_t n, int d, const float* x, const float* y, float* fx,
+                               float* fy, hipStream_t s);
+hipError_t launch_admission(const float* a2, const float* t, const float* y_all, int32_t n0, int32_t nc, int H, int d,
+                            int32_t cap, const float* cx, const float* cy, double* cemb, double* emb, float* rx,
+                            float* ry, double* nnd, int32_t* nni, int32_t* redo, int32_t* admitted, hipStream_t s);
+hipError_t launch_loss_accumulate(const float* loss, double* acc, int reset, hipStream_t s);
+hipError_t launch_loss_finish(const double* acc, int32_t count, float* out, hipStream_t s);
+
 // Online update.  Workspace layout is chosen by update_workspace_floats().
 int64_t update_workspace_bytes(const ModelDims& m, int32_t B);
 hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,

@@ -3,6 +3,7 @@
 // Every entry point validates its arguments on the host before enqueuing
 // anything, keeps the caller's device current only for its own duration, and
 // reports failures through a status code plus a per-context message.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -44,6 +45,15 @@ struct ls_ctx {
     // grow-only workspace
     void* ws = nullptr;
     size_t ws_cap = 0;
+    // online-learning data path (device pools, host-side counters)
+    struct Buffer {
+        int32_t fifo_cap = 0, rep_cap = 0, fifo_count = 0, fifo_head = 0, rep_count = 0;
+        float *fifo_x = nullptr, *fifo_y = nullptr, *rep_x = nullptr, *rep_y = nullptr;
+        double *emb = nullptr, *nnd = nullptr;
+        int32_t* nni = nullptr;
+        void* ws = nullptr;
+        size_t ws_cap = 0;
+    } buf;
     // pinned staging for host -> device copies, reusable once `stage_done` has fired
     void* stage = nullptr;
     size_t stage_cap = 0;
@@ -150,10 +160,12 @@ int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
 }
 
 enum Kind {
-    K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_ROUTE, K_COUNT
+    K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_ROUTE, K_BUFFER,
+    K_COUNT
 };
 const char* const kKindNames[K_COUNT] = {"table_build", "prefix_match", "instance_partial", "score_pairs", "argmin",
-                                         "update", "score_pairs_mfma", "band_select", "rescore", "route"};
+                                         "update", "score_pairs_mfma", "band_select", "rescore", "route",
+                                         "buffer"};
 
 hipEvent_t take_event(ls_ctx* c) {
     if (!c->spare.empty()) {
@@ -308,7 +320,9 @@ void ls_destroy(ls_ctx* c) {
         for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->frag16,
                         (void*)c->frag32, (void*)c->tables.keys,
                         (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
-                        (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws})
+                        (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws, (void*)c->buf.fifo_x,
+                        (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
+                        (void*)c->buf.nnd, (void*)c->buf.nni, c->buf.ws})
             if (p) (void)hipFree(p);
         if (c->stage) (void)hipHostFree(c->stage);
         if (c->stage_done) (void)hipEventDestroy(c->stage_done);
@@ -694,6 +708,242 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     LS_TIMED(c, K_UPDATE, s,
              ls::launch_update(c->dims, c->master, c->compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
                                c->ws, s));
+    if (c->frag16)
+        LS_TIMED(c, K_UPDATE, s,
+                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
+    return LS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// online-learning data path
+// ---------------------------------------------------------------------------
+int ls_buffer_init(ls_ctx* c, int32_t fifo_cap, int32_t replay_cap) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (fifo_cap < 1 || replay_cap < 0) return fail(c, LS_ERR_INVALID, "fifo_cap must be >= 1 and replay_cap >= 0");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    LS_HIP(c, hipDeviceSynchronize());
+    ls_ctx::Buffer& B = c->buf;
+    for (void* p : {(void*)B.fifo_x, (void*)B.fifo_y, (void*)B.rep_x, (void*)B.rep_y, (void*)B.emb, (void*)B.nnd,
+                    (void*)B.nni})
+        if (p) LS_HIP(c, hipFree(p));
+    B.fifo_x = B.fifo_y = B.rep_x = B.rep_y = nullptr;
+    B.emb = B.nnd = nullptr;
+    B.nni = nullptr;
+    B.fifo_cap = B.rep_cap = B.fifo_count = B.fifo_head = B.rep_count = 0;
+    const int d = c->dims.d, H = c->dims.h2;
+    const int32_t rc1 = replay_cap > 0 ? replay_cap : 1;
+    bool ok = hipMalloc((void**)&B.fifo_x, sizeof(float) * (size_t)fifo_cap * d) == hipSuccess &&
+              hipMalloc((void**)&B.fifo_y, sizeof(float) * (size_t)fifo_cap) == hipSuccess &&
+              hipMalloc((void**)&B.rep_x, sizeof(float) * (size_t)rc1 * d) == hipSuccess &&
+              hipMalloc((void**)&B.rep_y, sizeof(float) * (size_t)rc1) == hipSuccess &&
+              hipMalloc((void**)&B.emb, sizeof(double) * (size_t)rc1 * H) == hipSuccess &&
+              hipMalloc((void**)&B.nnd, sizeof(double) * (size_t)rc1) == hipSuccess &&
+              hipMalloc((void**)&B.nni, sizeof(int32_t) * (size_t)rc1) == hipSuccess;
+    if (!ok) {
+        (void)hipGetLastError();
+        return fail(c, LS_ERR_NOMEM, "training buffer allocation failed");
+    }
+    B.fifo_cap = fifo_cap;
+    B.rep_cap = replay_cap;
+    return LS_OK;
+}
+
+int ls_buffer_state(ls_ctx* c, int32_t* fifo_count, int32_t* fifo_head, int32_t* replay_count) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (fifo_count) *fifo_count = c->buf.fifo_count;
+    if (fifo_head) *fifo_head = c->buf.fifo_head;
+    if (replay_count) *replay_count = c->buf.rep_count;
+    return LS_OK;
+}
+
+int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, int32_t* admitted, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    ls_ctx::Buffer& bf = c->buf;
+    if (bf.fifo_cap < 1) return fail(c, LS_ERR_STATE, "the training buffer has not been initialised");
+    if (B < 0) return fail(c, LS_ERR_INVALID, "B must be >= 0");
+    if (B > 0 && (!feats || !ttft)) return fail(c, LS_ERR_INVALID, "feats and ttft must be non-NULL");
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    if (B == 0) return LS_OK;
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const ls::ModelDims& m = c->dims;
+    const int d = m.d, H = m.h2;
+    // the FIFO on the host: which rows leave it (candidates, oldest first) and where the new rows land
+    std::vector<int32_t> slot_src(bf.fifo_cap);       // >= 0: old slot content, < 0: new row -(b + 1)
+    for (int32_t q = 0; q < bf.fifo_cap; ++q) slot_src[q] = q;
+    std::vector<int32_t> cand;                          // gather codes for the candidates
+    std::vector<int32_t> dst(B, -1);
+    int32_t count = bf.fifo_count, head = bf.fifo_head;
+    for (int32_t b = 0; b < B; ++b) {
+        int32_t slot;
+        if (count < bf.fifo_cap) {
+            slot = (head + count) % bf.fifo_cap;
+            ++count;
+        } else {
+            slot = head;
+            const int32_t src = slot_src[slot];
+            if (src < 0) dst[-src - 1] = -1;            // a new row evicted within this push
+            cand.push_back(src);
+            head = (head + 1) % bf.fifo_cap;
+        }
+        slot_src[slot] = -(b + 1);
+        dst[b] = slot;
+    }
+    const int32_t nc = (int32_t)cand.size();
+    const int32_t n0 = bf.rep_count;
+    const int32_t n_all = bf.rep_cap > 0 ? n0 + nc : 0;
+    // workspace
+    const int64_t f_fwd = n_all > 0 ? ls::forward_rows_floats(m, n_all) : 0;
+    size_t need = (size_t)round_up((int64_t)(nc + B) * 4, 256)                       // codes
+                  + (size_t)round_up((int64_t)(nc > 0 ? nc : 1) * (d + 1) * 4, 256)     // candidate rows
+                  + (size_t)round_up((int64_t)(n_all > 0 ? n_all : 1) * (d + 1) * 4, 256)  // forward input
+                  + (size_t)round_up(f_fwd * 4, 256)
+                  + (size_t)round_up((int64_t)(nc > 0 ? nc : 1) * H * 8, 256)          // candidate embeddings
+                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 4, 256) + 256;
+    int rc = grow(c, &bf.ws, &bf.ws_cap, need);
+    if (rc) return rc;
+    WsCarve w{(char*)bf.ws};
+    int32_t* codes = w.take<int32_t>(nc + B);
+    float* cx = w.take<float>((int64_t)(nc > 0 ? nc : 1) * d);
+    float* cy = w.take<float>(nc > 0 ? nc : 1);
+    float* ax = w.take<float>((int64_t)(n_all > 0 ? n_all : 1) * d);
+    float* ay = w.take<float>(n_all > 0 ? n_all : 1);
+    float* fws = w.take<float>(f_fwd > 0 ? f_fwd : 1);
+    double* cemb = w.take<double>((int64_t)(nc > 0 ? nc : 1) * H);
+    int32_t* redo = w.take<int32_t>(bf.rep_cap > 0 ? bf.rep_cap : 1);
+    int32_t* adm = w.take<int32_t>(64);
+    // stage the codes
+    rc = stage_reserve(c, sizeof(int32_t) * (size_t)(nc + B) + 64);
+    if (rc) return rc;
+    if (nc) memcpy(c->stage, cand.data(), sizeof(int32_t) * (size_t)nc);
+    memcpy((int32_t*)c->stage + nc, dst.data(), sizeof(int32_t) * (size_t)B);
+    LS_HIP(c, hipMemcpyAsync(codes, c->stage, sizeof(int32_t) * (size_t)(nc + B), hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    // candidates leave the FIFO before the new rows overwrite it
+    LS_TIMED(c, K_BUFFER, s, ls::launch_gather_rows(codes, nc, d, bf.fifo_x, bf.fifo_y, feats, ttft, cx, cy, s));
+    LS_TIMED(c, K_BUFFER, s, ls::launch_scatter_rows(codes + nc, B, d, feats, ttft, bf.fifo_x, bf.fifo_y, s));
+    if (n_all > 0 && nc > 0) {
+        // forward of the pool (slots 0..n0) followed by the candidates
+        LS_HIP(c, hipMemcpyAsync(ax, bf.rep_x, sizeof(float) * (size_t)n0 * d, hipMemcpyDeviceToDevice, s));
+        LS_HIP(c, hipMemcpyAsync(ay, bf.rep_y, sizeof(float) * (size_t)n0, hipMemcpyDeviceToDevice, s));
+        LS_HIP(c, hipMemcpyAsync(ax + (int64_t)n0 * d, cx, sizeof(float) * (size_t)nc * d, hipMemcpyDeviceToDevice, s));
+        LS_HIP(c, hipMemcpyAsync(ay + n0, cy, sizeof(float) * (size_t)nc, hipMemcpyDeviceToDevice, s));
+        float *a2 = nullptr, *t = nullptr;
+        LS_TIMED(c, K_BUFFER, s, ls::launch_forward_rows(m, c->compute, c->mu, c->isig, n_all, ax, fws, &a2, &t, s));
+        LS_TIMED(c, K_BUFFER, s,
+                 ls::launch_admission(a2, t, ay, n0, nc, H, d, bf.rep_cap, cx, cy, cemb, bf.emb, bf.rep_x, bf.rep_y,
+                                      bf.nnd, bf.nni, redo, admitted ? admitted : adm, s));
+    } else if (admitted) {
+        LS_TIMED(c, K_BUFFER, s, ls::launch_fill_u32(reinterpret_cast<uint32_t*>(admitted), 0u, 1, s));
+    }
+    bf.fifo_count = count;
+    bf.fifo_head = head;
+    bf.rep_count = bf.rep_cap > 0 ? (n0 + nc < bf.rep_cap ? n0 + nc : bf.rep_cap) : 0;
+    return LS_OK;
+}
+
+int ls_buffer_read(ls_ctx* c, float* fifo_x, float* fifo_y, float* replay_x, float* replay_y, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    ls_ctx::Buffer& bf = c->buf;
+    if (bf.fifo_cap < 1) return fail(c, LS_ERR_STATE, "the training buffer has not been initialised");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const int d = c->dims.d;
+    // the FIFO oldest first: at most two contiguous pieces of the ring
+    const int32_t first = bf.fifo_count < bf.fifo_cap - bf.fifo_head ? bf.fifo_count : bf.fifo_cap - bf.fifo_head;
+    if (fifo_x && bf.fifo_count) {
+        LS_HIP(c, hipMemcpyAsync(fifo_x, bf.fifo_x + (int64_t)bf.fifo_head * d, sizeof(float) * (size_t)first * d,
+                                 hipMemcpyDeviceToDevice, s));
+        if (bf.fifo_count > first)
+            LS_HIP(c, hipMemcpyAsync(fifo_x + (int64_t)first * d, bf.fifo_x,
+                                     sizeof(float) * (size_t)(bf.fifo_count - first) * d, hipMemcpyDeviceToDevice, s));
+    }
+    if (fifo_y && bf.fifo_count) {
+        LS_HIP(c, hipMemcpyAsync(fifo_y, bf.fifo_y + bf.fifo_head, sizeof(float) * (size_t)first,
+                                 hipMemcpyDeviceToDevice, s));
+        if (bf.fifo_count > first)
+            LS_HIP(c, hipMemcpyAsync(fifo_y + first, bf.fifo_y, sizeof(float) * (size_t)(bf.fifo_count - first),
+                                     hipMemcpyDeviceToDevice, s));
+    }
+    if (replay_x && bf.rep_count)
+        LS_HIP(c, hipMemcpyAsync(replay_x, bf.rep_x, sizeof(float) * (size_t)bf.rep_count * d, hipMemcpyDeviceToDevice,
+                                 s));
+    if (replay_y && bf.rep_count)
+        LS_HIP(c, hipMemcpyAsync(replay_y, bf.rep_y, sizeof(float) * (size_t)bf.rep_count, hipMemcpyDeviceToDevice, s));
+    return LS_OK;
+}
+
+int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int32_t* perm, float* loss_out,
+                   void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    ls_ctx::Buffer& bf = c->buf;
+    if (bf.fifo_cap < 1) return fail(c, LS_ERR_STATE, "the training buffer has not been initialised");
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    if (epochs < 0 || batch < 1) return fail(c, LS_ERR_INVALID, "epochs must be >= 0 and batch >= 1");
+    if (!std::isfinite(lr)) return fail(c, LS_ERR_INVALID, "lr must be finite");
+    const int32_t n = bf.fifo_count + bf.rep_count;
+    if (n < 1) return fail(c, LS_ERR_STATE, "the training buffer is empty");
+    if (epochs == 0) return LS_OK;
+    // sample k of the round: FIFO oldest first, then the pool by slot; codes for gather_rows
+    std::vector<int32_t> codes((size_t)epochs * n);
+    std::vector<char> seen(n);
+    for (int32_t e = 0; e < epochs; ++e) {
+        std::fill(seen.begin(), seen.end(), 0);
+        for (int32_t k = 0; k < n; ++k) {
+            const int32_t v = perm ? perm[(int64_t)e * n + k] : k;
+            if (v < 0 || v >= n || seen[v]) return fail(c, LS_ERR_INVALID, "perm row %d is not a permutation of %d", e, n);
+            seen[v] = 1;
+            codes[(size_t)e * n + k] =
+                v < bf.fifo_count ? (bf.fifo_head + v) % bf.fifo_cap : -(v - bf.fifo_count) - 1;
+        }
+    }
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const ls::ModelDims& m = c->dims;
+    const int d = m.d;
+    size_t need = (size_t)round_up((int64_t)epochs * n * 4, 256) + (size_t)round_up((int64_t)batch * (d + 1) * 4, 256) +
+                  512 + (size_t)round_up(ls::update_workspace_bytes(m, batch), 256);
+    int rc = grow(c, &bf.ws, &bf.ws_cap, need);
+    if (rc) return rc;
+    WsCarve w{(char*)bf.ws};
+    int32_t* dcodes = w.take<int32_t>((int64_t)epochs * n);
+    float* bx = w.take<float>((int64_t)batch * d);
+    float* by = w.take<float>(batch);
+    float* step_loss = w.take<float>(64);
+    double* acc = w.take<double>(32);
+    void* uws = w.take<char>(ls::update_workspace_bytes(m, batch));
+    rc = stage_reserve(c, sizeof(int32_t) * codes.size() + 64);
+    if (rc) return rc;
+    memcpy(c->stage, codes.data(), sizeof(int32_t) * codes.size());
+    LS_HIP(c, hipMemcpyAsync(dcodes, c->stage, sizeof(int32_t) * codes.size(), hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    int32_t nb = 0;
+    for (int32_t e = 0; e < epochs; ++e) {
+        nb = 0;
+        for (int32_t st = 0; st < n; st += batch) {
+            const int32_t mb = n - st < batch ? n - st : batch;
+            LS_TIMED(c, K_UPDATE, s,
+                     ls::launch_gather_rows(dcodes + (int64_t)e * n + st, mb, d, bf.fifo_x, bf.fifo_y, bf.rep_x,
+                                            bf.rep_y, bx, by, s));
+            LS_TIMED(c, K_UPDATE, s,
+                     ls::launch_update(m, c->master, c->compute, c->mu, c->isig, mb, bx, by, lr, step_loss, nullptr,
+                                       uws, s));
+            if (e + 1 == epochs && loss_out) LS_HIP(c, ls::launch_loss_accumulate(step_loss, acc, nb == 0, s));
+            ++nb;
+        }
+    }
+    if (loss_out) LS_HIP(c, ls::launch_loss_finish(acc, nb, loss_out, s));
     if (c->frag16)
         LS_TIMED(c, K_UPDATE, s,
                  ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));

@@ -88,11 +88,17 @@ def library():
         lib.ls_set_exact_scores.argtypes = [P, ctypes.c_int]
         lib.ls_set_prefix_join.argtypes = [P, ctypes.c_int]
         lib.ls_set_prefix_closed.argtypes = [P, ctypes.c_int]
+        lib.ls_buffer_init.argtypes = [P, i32, i32]
+        lib.ls_buffer_push.argtypes = [P, i32, P, P, P, P]
+        lib.ls_buffer_state.argtypes = [P, P, P, P]
+        lib.ls_buffer_read.argtypes = [P, P, P, P, P, P]
+        lib.ls_train_round.argtypes = [P, i32, i32, f32, P, P, P]
         lib.ls_route_batch.argtypes = [P, ctypes.POINTER(ls_policy), i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
-                  lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed):
+                  lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
+                  lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -259,6 +265,45 @@ class Context:
         ]
         return self._check("ls_route_batch",
                            self.lib.ls_route_batch(self.h, ctypes.byref(policy), R, N, *args, _stream(stream)))
+
+    # -- online-learning data path -----------------------------------------
+    def ls_buffer_init(self, fifo_cap, replay_cap):
+        return self._check("ls_buffer_init", self.lib.ls_buffer_init(self.h, int(fifo_cap), int(replay_cap)))
+
+    def ls_buffer_push(self, feats, ttft, admitted=None, stream=None):
+        import torch
+        B = ttft.numel()
+        args = [_dev(feats, "feats", (torch.float32,), B * self.d), _dev(ttft, "ttft", (torch.float32,), B),
+                _dev(admitted, "admitted", (torch.int32,), 1, allow_none=True)]
+        return self._check("ls_buffer_push", self.lib.ls_buffer_push(self.h, B, *args, _stream(stream)))
+
+    def ls_buffer_state(self):
+        v = [ctypes.c_int32(0) for _ in range(3)]
+        self._check("ls_buffer_state", self.lib.ls_buffer_state(self.h, *[ctypes.byref(x) for x in v]))
+        return tuple(x.value for x in v)          # (fifo_count, fifo_head, replay_count)
+
+    def ls_buffer_read(self, stream=None):
+        """Device copies of the FIFO (oldest first) and the pool (by slot)."""
+        import torch
+        fc, _, rc = self.ls_buffer_state()
+        fx = torch.empty(max(fc, 1) * self.d, dtype=torch.float32, device="cuda")
+        fy = torch.empty(max(fc, 1), dtype=torch.float32, device="cuda")
+        rx = torch.empty(max(rc, 1) * self.d, dtype=torch.float32, device="cuda")
+        ry = torch.empty(max(rc, 1), dtype=torch.float32, device="cuda")
+        self._check("ls_buffer_read", self.lib.ls_buffer_read(self.h, ctypes.c_void_p(fx.data_ptr()),
+                                                              ctypes.c_void_p(fy.data_ptr()),
+                                                              ctypes.c_void_p(rx.data_ptr()),
+                                                              ctypes.c_void_p(ry.data_ptr()), _stream(stream)))
+        return (fx[:fc * self.d].view(fc, self.d), fy[:fc], rx[:rc * self.d].view(rc, self.d), ry[:rc])
+
+    def ls_train_round(self, epochs, batch, lr, perm=None, loss_out=None, stream=None):
+        import torch
+        pa = None if perm is None else np.ascontiguousarray(perm, dtype=np.int32)
+        lo = _dev(loss_out, "loss_out", (torch.float32,), 1, allow_none=True)
+        return self._check("ls_train_round",
+                           self.lib.ls_train_round(self.h, int(epochs), int(batch), float(lr),
+                                                   None if pa is None else pa.ctypes.data_as(ctypes.c_void_p), lo,
+                                                   _stream(stream)))
 
     # -- online update -----------------------------------------------------
     def ls_update(self, feats, ttft, lr, loss_out=None, grad_out=None, stream=None):
