@@ -168,6 +168,32 @@ def time_route(ctx, w, dev_in, reps):
             "tiebreak": int(((st & 0x400) != 0).sum())}
 
 
+def time_online_learning(ctx, w):
+    """The paper's data path at its own sizes (Section 4.3.2): FIFO and replay pool of 5000 each, a push of 1000
+    logged samples into full pools (1000 coreset decisions), then a retraining round over the 10,000 samples."""
+    import torch
+    cfg = w.cfg
+    rng = np.random.default_rng(11)
+    x_all = torch.from_numpy(np.ascontiguousarray(w.upd_feats[:11000])).cuda()
+    y_all = torch.from_numpy(np.ascontiguousarray(w.upd_ttft[:11000])).cuda()
+    ctx.ls_buffer_init(5000, 5000)
+    ctx.ls_buffer_push(x_all[:10000], y_all[:10000])        # fills FIFO and pool
+    torch.cuda.synchronize()
+    adm = torch.zeros(1, dtype=torch.int32, device="cuda")
+    t0 = time.perf_counter()
+    ctx.ls_buffer_push(x_all[10000:11000], y_all[10000:11000], adm)
+    torch.cuda.synchronize()
+    push_ms = (time.perf_counter() - t0) * 1e3
+    perm = np.concatenate([rng.permutation(10000) for _ in range(5)]).astype(np.int32)
+    t0 = time.perf_counter()
+    ctx.ls_train_round(5, 256, w.lr, perm)
+    torch.cuda.synchronize()
+    train_ms = (time.perf_counter() - t0) * 1e3
+    return {"fifo": 5000, "replay": 5000, "push_1000_ms": round(push_ms, 3), "admitted": int(adm.item()),
+            "train_round_ms": round(train_ms, 3), "train_round": "5 epochs x 10000 samples, minibatch 256",
+            "train_samples_per_s": round(5 * 10000 / (train_ms / 1e3), 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,6 +302,7 @@ def main():
         "useful_probes": probes,
     }
     result["route"] = time_route(ctx, w, (req_off, req_h, plen, feat), args.steps)
+    result["online_learning"] = time_online_learning(ctx, w)
     ctx.close()
     if args.copy_probe_mib > 0:
         copy_probe(args.copy_probe_mib)

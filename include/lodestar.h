@@ -296,8 +296,10 @@ int ls_route_batch(ls_ctx* ctx, const ls_policy* policy, int32_t R, int32_t N,
  * re-evaluated with the current model at every push.  A retraining round runs
  * minibatch SGD (ls_update steps) over the FIFO and the pool.
  *
- *   ls_buffer_init   allocates empty pools (fifo_cap >= 1, replay_cap >= 0);
- *                    synchronous; discards any earlier contents.
+ *   ls_buffer_init   allocates empty pools (fifo_cap >= 1, 0 <= replay_cap <=
+ *                    LS_MAX_REPLAY: the pool keeps its pairwise distances,
+ *                    8 replay_cap^2 bytes); synchronous; discards any earlier
+ *                    contents.
  *   ls_buffer_push   appends B raw rows feats [B x d] and ttft [B] (device);
  *                    admitted (device int32, nullable) gets the number of
  *                    samples the pool took.  Stream-ordered.
@@ -319,6 +321,7 @@ int ls_route_batch(ls_ctx* ctx, const ls_policy* policy, int32_t R, int32_t N,
  * buffer (train); LS_ERR_INVALID for bad sizes or a perm that is not a
  * permutation.
  */
+#define LS_MAX_REPLAY 32768
 int ls_buffer_init(ls_ctx* ctx, int32_t fifo_cap, int32_t replay_cap);
 int ls_buffer_push(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, int32_t* admitted, void* stream);
 int ls_buffer_state(ls_ctx* ctx, int32_t* fifo_count, int32_t* fifo_head, int32_t* replay_count);

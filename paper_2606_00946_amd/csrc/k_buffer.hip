@@ -92,14 +92,25 @@ __device__ void block_min_pair(double& v, int32_t& i, double* sv, int32_t* si) {
     i = si[0];
 }
 
-// nearest neighbour of pool slot k among slots [0, n) other than k
-__device__ void nn_of_block(const double* __restrict__ emb, int H, int32_t n, int32_t k, double* sv, int32_t* si,
-                            double* out_d, int32_t* out_i) {
+// The pool keeps its pairwise distances D [cap x cap] (D[k][k] = +inf), so a
+// nearest neighbour is a row minimum.  Every entry is one emb_dist, summed by
+// one thread in ascending unit order.
+__global__ __launch_bounds__(256) void pool_dist_kernel(const double* __restrict__ emb, int H, int32_t n, int32_t cap,
+                                                        double* __restrict__ D) {
+    const int32_t i = blockIdx.y;
+    const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n) return;
+    D[(int64_t)i * cap + j] = (i == j) ? INFINITY : emb_dist(emb + (int64_t)i * H, emb + (int64_t)j * H, H);
+}
+
+// minimum of row k of D over columns [0, n) other than k (lowest column on ties)
+__device__ void row_min_block(const double* __restrict__ D, int32_t cap, int32_t n, int32_t k, double* sv, int32_t* si,
+                              double* out_d, int32_t* out_i) {
     double v = INFINITY;
     int32_t idx = -1;
     for (int32_t j = threadIdx.x; j < n; j += blockDim.x) {
         if (j == k) continue;
-        better_pair(v, idx, emb_dist(emb + (int64_t)k * H, emb + (int64_t)j * H, H), j);
+        better_pair(v, idx, D[(int64_t)k * cap + j], j);
     }
     block_min_pair(v, idx, sv, si);
     if (threadIdx.x == 0) {
@@ -109,73 +120,84 @@ __device__ void nn_of_block(const double* __restrict__ emb, int H, int32_t n, in
     __syncthreads();
 }
 
-// One workgroup per pool member: its nearest neighbour in the pool.
-__global__ __launch_bounds__(256) void pool_nn_kernel(const double* __restrict__ emb, int H, int32_t n,
+__global__ __launch_bounds__(256) void pool_nn_kernel(const double* __restrict__ D, int32_t cap, int32_t n,
                                                       double* __restrict__ nnd, int32_t* __restrict__ nni) {
     __shared__ double sv[4];
     __shared__ int32_t si[4];
-    nn_of_block(emb, H, n, (int32_t)blockIdx.x, sv, si, nnd + blockIdx.x, nni + blockIdx.x);
+    row_min_block(D, cap, n, (int32_t)blockIdx.x, sv, si, nnd + blockIdx.x, nni + blockIdx.x);
 }
 
-__global__ __launch_bounds__(kAdmitThreads) void admit_kernel(const double* __restrict__ cemb,
-                                                              const float* __restrict__ cx,
-                                                              const float* __restrict__ cy, int32_t nc, int d, int H,
-                                                              int32_t n0, int32_t cap, double* __restrict__ emb,
-                                                              float* __restrict__ rx, float* __restrict__ ry,
-                                                              double* __restrict__ nnd, int32_t* __restrict__ nni,
-                                                              int32_t* __restrict__ redo, int32_t* __restrict__ admitted) {
+// distances of one candidate to the n current members
+__global__ __launch_bounds__(256) void cand_row_kernel(const double* __restrict__ e, const double* __restrict__ emb,
+                                                       int H, int32_t n, double* __restrict__ row) {
+    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < n) row[k] = emb_dist(e, emb + (int64_t)k * H, H);
+}
+
+// One decision on a pool of n members (cap slots).  The host knows n: the pool
+// grows by one per candidate until it is full and keeps its size afterwards.
+__global__ __launch_bounds__(kAdmitThreads) void admit_one_kernel(const double* __restrict__ e,
+                                                                  const float* __restrict__ cxr,
+                                                                  const float* __restrict__ cyr, int d, int H,
+                                                                  int32_t n, int32_t cap,
+                                                                  const double* __restrict__ row,
+                                                                  double* __restrict__ emb, float* __restrict__ rx,
+                                                                  float* __restrict__ ry, double* __restrict__ D,
+                                                                  double* __restrict__ nnd, int32_t* __restrict__ nni,
+                                                                  int32_t* __restrict__ redo,
+                                                                  int32_t* __restrict__ admitted) {
     __shared__ double sv[kAdmitThreads / 64];
     __shared__ int32_t si[kAdmitThreads / 64];
     __shared__ int32_t n_redo;
-    int32_t n = n0, count = 0;
-    for (int32_t c = 0; c < nc; ++c) {
-        const double* __restrict__ e = cemb + (int64_t)c * H;
-        int32_t slot;
-        if (n < cap) {
-            slot = n++;
-        } else {
-            double dc = INFINITY;
-            int32_t dci = -1;
-            double mv = INFINITY;
-            int32_t mi = -1;
-            for (int32_t k = threadIdx.x; k < n; k += blockDim.x) {
-                better_pair(dc, dci, emb_dist(e, emb + (int64_t)k * H, H), k);
-                better_pair(mv, mi, nnd[k], k);
-            }
-            block_min_pair(dc, dci, sv, si);
-            block_min_pair(mv, mi, sv, si);
-            if (!(dc > mv)) continue;                    // uniform: every thread holds the reduced values
-            slot = mi;
-        }
-        for (int j = threadIdx.x; j < H; j += blockDim.x) emb[(int64_t)slot * H + j] = e[j];
-        for (int q = threadIdx.x; q < d; q += blockDim.x) rx[(int64_t)slot * d + q] = cx[(int64_t)c * d + q];
-        if (threadIdx.x == 0) {
-            ry[slot] = cy[c];
-            n_redo = 0;
-        }
-        ++count;
-        __syncthreads();
+    int32_t slot, m;
+    if (n < cap) {
+        slot = n;
+        m = n + 1;
+    } else {
+        double dc = INFINITY, mv = INFINITY;
+        int32_t dci = -1, mi = -1;
         for (int32_t k = threadIdx.x; k < n; k += blockDim.x) {
-            if (k == slot) continue;
-            if (nni[k] == slot) {
-                redo[atomicAdd(&n_redo, 1)] = k;
-            } else {
-                const double v = emb_dist(emb + (int64_t)k * H, e, H);
-                if (v < nnd[k] || (v == nnd[k] && slot < nni[k])) {
-                    nnd[k] = v;
-                    nni[k] = slot;
-                }
+            better_pair(dc, dci, row[k], k);
+            better_pair(mv, mi, nnd[k], k);
+        }
+        block_min_pair(dc, dci, sv, si);
+        block_min_pair(mv, mi, sv, si);
+        if (!(dc > mv)) return;                             // uniform across the workgroup
+        slot = mi;
+        m = n;
+    }
+    for (int j = threadIdx.x; j < H; j += blockDim.x) emb[(int64_t)slot * H + j] = e[j];
+    for (int q = threadIdx.x; q < d; q += blockDim.x) rx[(int64_t)slot * d + q] = cxr[q];
+    for (int32_t k = threadIdx.x; k < m; k += blockDim.x) {
+        const double v = (k == slot) ? INFINITY : row[k];
+        D[(int64_t)slot * cap + k] = v;
+        D[(int64_t)k * cap + slot] = v;
+    }
+    if (threadIdx.x == 0) {
+        ry[slot] = *cyr;
+        n_redo = 0;
+        *admitted += 1;
+    }
+    __syncthreads();
+    for (int32_t k = threadIdx.x; k < m; k += blockDim.x) {
+        if (k == slot) continue;
+        if (nni[k] == slot) {
+            redo[atomicAdd(&n_redo, 1)] = k;
+        } else {
+            const double v = row[k];
+            if (v < nnd[k] || (v == nnd[k] && slot < nni[k])) {
+                nnd[k] = v;
+                nni[k] = slot;
             }
         }
-        __syncthreads();
-        const int32_t nr = n_redo;
-        for (int32_t q = 0; q < nr; ++q) {
-            const int32_t k = redo[q];
-            nn_of_block(emb, H, n, k, sv, si, nnd + k, nni + k);
-        }
-        nn_of_block(emb, H, n, slot, sv, si, nnd + slot, nni + slot);
     }
-    if (threadIdx.x == 0 && admitted) *admitted = count;
+    __syncthreads();
+    const int32_t nr = n_redo;
+    for (int32_t q = 0; q < nr; ++q) {
+        const int32_t k = redo[q];
+        row_min_block(D, cap, m, k, sv, si, nnd + k, nni + k);
+    }
+    row_min_block(D, cap, m, slot, sv, si, nnd + slot, nni + slot);
 }
 
 static inline uint32_t grid_of(int64_t n, int block) { return (uint32_t)((n + block - 1) / block); }
@@ -198,14 +220,28 @@ hipError_t launch_scatter_rows(const int32_t* dst, int32_t n, int d, const float
 
 hipError_t launch_admission(const float* a2, const float* t, const float* y_all, int32_t n0, int32_t nc, int H, int d,
                             int32_t cap, const float* cx, const float* cy, double* cemb, double* emb, float* rx,
-                            float* ry, double* nnd, int32_t* nni, int32_t* redo, int32_t* admitted, hipStream_t s) {
+                            float* ry, double* D, double* nnd, int32_t* nni, double* row, int32_t* redo,
+                            int32_t* admitted, hipStream_t s) {
     const int32_t n = n0 + nc;
-    if (n <= 0) return hipSuccess;
+    if (n <= 0 || cap <= 0) return hipSuccess;
     hipLaunchKernelGGL(embed_kernel, dim3(grid_of((int64_t)n * H, 256)), dim3(256), 0, s, a2, t, y_all, n, n0, H, emb,
                        cemb);
-    if (n0 > 0) hipLaunchKernelGGL(pool_nn_kernel, dim3((uint32_t)n0), dim3(256), 0, s, emb, H, n0, nnd, nni);
-    hipLaunchKernelGGL(admit_kernel, dim3(1), dim3(kAdmitThreads), 0, s, cemb, cx, cy, nc, d, H, n0, cap, emb, rx, ry,
-                       nnd, nni, redo, admitted);
+    if (n0 > 0) {
+        hipLaunchKernelGGL(pool_dist_kernel, dim3(grid_of(n0, 256), (uint32_t)n0), dim3(256), 0, s, emb, H, n0, cap, D);
+        hipLaunchKernelGGL(pool_nn_kernel, dim3((uint32_t)n0), dim3(256), 0, s, D, cap, n0, nnd, nni);
+    }
+    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(admitted), 0u, 1, s);
+    if (e != hipSuccess) return e;
+    int32_t size = n0;
+    for (int32_t c = 0; c < nc; ++c) {
+        if (size > 0)
+            hipLaunchKernelGGL(cand_row_kernel, dim3(grid_of(size, 256)), dim3(256), 0, s, cemb + (int64_t)c * H, emb,
+                               H, size, row);
+        hipLaunchKernelGGL(admit_one_kernel, dim3(1), dim3(kAdmitThreads), 0, s, cemb + (int64_t)c * H,
+                           cx + (int64_t)c * d, cy + c, d, H, size, cap, row, emb, rx, ry, D, nnd, nni, redo,
+                           admitted);
+        if (size < cap) ++size;
+    }
     return hipGetLastError();
 }
 

@@ -177,7 +177,8 @@ hipError_t launch_scatter_rows(const int32_t* dst, int32_t n, int d, const float
                                float* fy, hipStream_t s);
 hipError_t launch_admission(const float* a2, const float* t, const float* y_all, int32_t n0, int32_t nc, int H, int d,
                             int32_t cap, const float* cx, const float* cy, double* cemb, double* emb, float* rx,
-                            float* ry, double* nnd, int32_t* nni, int32_t* redo, int32_t* admitted, hipStream_t s);
+                            float* ry, double* D, double* nnd, int32_t* nni, double* row, int32_t* redo,
+                            int32_t* admitted, hipStream_t s);
 hipError_t launch_loss_accumulate(const float* loss, double* acc, int reset, hipStream_t s);
 hipError_t launch_loss_finish(const double* acc, int32_t count, float* out, hipStream_t s);
 

@@ -49,7 +49,7 @@ struct ls_ctx {
     struct Buffer {
         int32_t fifo_cap = 0, rep_cap = 0, fifo_count = 0, fifo_head = 0, rep_count = 0;
         float *fifo_x = nullptr, *fifo_y = nullptr, *rep_x = nullptr, *rep_y = nullptr;
-        double *emb = nullptr, *nnd = nullptr;
+        double *emb = nullptr, *nnd = nullptr, *D = nullptr;   // D: pairwise distances [rep_cap x rep_cap]
         int32_t* nni = nullptr;
         void* ws = nullptr;
         size_t ws_cap = 0;
@@ -322,7 +322,7 @@ void ls_destroy(ls_ctx* c) {
                         (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
                         (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws, (void*)c->buf.fifo_x,
                         (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
-                        (void*)c->buf.nnd, (void*)c->buf.nni, c->buf.ws})
+                        (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws})
             if (p) (void)hipFree(p);
         if (c->stage) (void)hipHostFree(c->stage);
         if (c->stage_done) (void)hipEventDestroy(c->stage_done);
@@ -721,15 +721,17 @@ int ls_buffer_init(ls_ctx* c, int32_t fifo_cap, int32_t replay_cap) {
     if (!c) return LS_ERR_INVALID;
     c->err.clear();
     if (fifo_cap < 1 || replay_cap < 0) return fail(c, LS_ERR_INVALID, "fifo_cap must be >= 1 and replay_cap >= 0");
+    if (replay_cap > LS_MAX_REPLAY)
+        return fail(c, LS_ERR_UNSUPPORTED, "replay_cap above %d (the pool keeps all pairwise distances)", LS_MAX_REPLAY);
     DeviceScope dev(c->device);
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     LS_HIP(c, hipDeviceSynchronize());
     ls_ctx::Buffer& B = c->buf;
     for (void* p : {(void*)B.fifo_x, (void*)B.fifo_y, (void*)B.rep_x, (void*)B.rep_y, (void*)B.emb, (void*)B.nnd,
-                    (void*)B.nni})
+                    (void*)B.nni, (void*)B.D})
         if (p) LS_HIP(c, hipFree(p));
     B.fifo_x = B.fifo_y = B.rep_x = B.rep_y = nullptr;
-    B.emb = B.nnd = nullptr;
+    B.emb = B.nnd = B.D = nullptr;
     B.nni = nullptr;
     B.fifo_cap = B.rep_cap = B.fifo_count = B.fifo_head = B.rep_count = 0;
     const int d = c->dims.d, H = c->dims.h2;
@@ -740,7 +742,8 @@ int ls_buffer_init(ls_ctx* c, int32_t fifo_cap, int32_t replay_cap) {
               hipMalloc((void**)&B.rep_y, sizeof(float) * (size_t)rc1) == hipSuccess &&
               hipMalloc((void**)&B.emb, sizeof(double) * (size_t)rc1 * H) == hipSuccess &&
               hipMalloc((void**)&B.nnd, sizeof(double) * (size_t)rc1) == hipSuccess &&
-              hipMalloc((void**)&B.nni, sizeof(int32_t) * (size_t)rc1) == hipSuccess;
+              hipMalloc((void**)&B.nni, sizeof(int32_t) * (size_t)rc1) == hipSuccess &&
+              hipMalloc((void**)&B.D, sizeof(double) * (size_t)rc1 * rc1) == hipSuccess;
     if (!ok) {
         (void)hipGetLastError();
         return fail(c, LS_ERR_NOMEM, "training buffer allocation failed");
@@ -804,7 +807,8 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
                   + (size_t)round_up((int64_t)(n_all > 0 ? n_all : 1) * (d + 1) * 4, 256)  // forward input
                   + (size_t)round_up(f_fwd * 4, 256)
                   + (size_t)round_up((int64_t)(nc > 0 ? nc : 1) * H * 8, 256)          // candidate embeddings
-                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 4, 256) + 256;
+                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 4, 256) + 256
+                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 8, 256);          // distance row
     int rc = grow(c, &bf.ws, &bf.ws_cap, need);
     if (rc) return rc;
     WsCarve w{(char*)bf.ws};
@@ -817,6 +821,7 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
     double* cemb = w.take<double>((int64_t)(nc > 0 ? nc : 1) * H);
     int32_t* redo = w.take<int32_t>(bf.rep_cap > 0 ? bf.rep_cap : 1);
     int32_t* adm = w.take<int32_t>(64);
+    double* drow = w.take<double>(bf.rep_cap > 0 ? bf.rep_cap : 1);
     // stage the codes
     rc = stage_reserve(c, sizeof(int32_t) * (size_t)(nc + B) + 64);
     if (rc) return rc;
@@ -838,7 +843,7 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
         LS_TIMED(c, K_BUFFER, s, ls::launch_forward_rows(m, c->compute, c->mu, c->isig, n_all, ax, fws, &a2, &t, s));
         LS_TIMED(c, K_BUFFER, s,
                  ls::launch_admission(a2, t, ay, n0, nc, H, d, bf.rep_cap, cx, cy, cemb, bf.emb, bf.rep_x, bf.rep_y,
-                                      bf.nnd, bf.nni, redo, admitted ? admitted : adm, s));
+                                      bf.D, bf.nnd, bf.nni, drow, redo, admitted ? admitted : adm, s));
     } else if (admitted) {
         LS_TIMED(c, K_BUFFER, s, ls::launch_fill_u32(reinterpret_cast<uint32_t*>(admitted), 0u, 1, s));
     }
