@@ -71,7 +71,9 @@ __device__ __forceinline__ void derived_columns(int32_t L, int64_t n, int32_t l,
     x[0] = (float)L;
     x[1] = (float)n;
     x[2] = (float)l;
-    x[3] = (L == 0) ? 0.0f : (float)hit / (float)L;
+    // divide unconditionally by a safe denominator, then select: no branch
+    const float ratio = (float)hit / (float)(L == 0 ? 1 : L);
+    x[3] = (L == 0) ? 0.0f : ratio;
     x[4] = (float)((int64_t)L - hit);
 }
 

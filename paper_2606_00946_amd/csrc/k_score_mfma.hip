@@ -176,17 +176,20 @@ __device__ __forceinline__ bf16x8_t relu_pack(const f32x16_t& acc, int q) {
     return out;
 }
 
-// One wave scores one tile of 32 pairs (one request, 32 consecutive instances)
-// at a time; the eight waves of a workgroup share the W1 and W2 fragments in
-// LDS (32 + 128 KB at h = 256).  Each layer runs in passes of MH row tiles so
-// that few accumulators are live at once.
+// One wave scores two tiles of 32 pairs (32 consecutive instances of one
+// request each; consecutive tiles in request-major order) per pass; the eight
+// waves of a workgroup share the W1 and W2 fragments in LDS (32 + 128 KB at
+// h = 256).  Every weight fragment read from LDS feeds one MFMA per tile, and
+// every bias and head fragment read serves both tiles.  Each layer runs one
+// row tile at a time, so that few accumulators are live beside the second
+// layer's 2 x h1 bf16 inputs.
 template <int MT1, int MT2, int D>
 __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     static_assert(MT1 == MT2, "square hidden layers");
     constexpr int KS2 = 2 * MT1;               // layer-2 k-steps: h1 / 16
-    constexpr int MH = MT1 < 4 ? MT1 : 4;       // row tiles per pass
     constexpr int D_INST = D - 5;
     constexpr int NW1 = 4 * MT1 * 64, NW2 = MT2 * KS2 * 64;
+    constexpr int PT = 2;                      // tiles per pass
     __shared__ bf16x8_t lds_w1[NW1];
     __shared__ bf16x8_t lds_w2[NW2];
     for (int f = threadIdx.x; f < NW1; f += blockDim.x) lds_w1[f] = A.w1frag[f];
@@ -198,22 +201,32 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     const int h = lane >> 5, n = lane & 31;
     const int tiles_per_req = (A.N + 31) >> 5;
     const int64_t n_tiles = (int64_t)A.R * tiles_per_req;
+    const int64_t n_passes = (n_tiles + PT - 1) / PT;
     const float b3 = A.b3[0];
     const bf16x8_t* __restrict__ hf = A.hfrag + lane;
     const bf16x8_t* __restrict__ w1l = lds_w1 + lane;
-    for (int64_t tile = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6); tile < n_tiles;
-         tile += (int64_t)gridDim.x * waves) {
-        const int64_t r = tile / tiles_per_req;
-        const int i = (int)(tile - r * tiles_per_req) * 32 + n;
-        const bool valid = i < A.N;
-        const int ii = valid ? i : 0;
+    for (int64_t pass = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6); pass < n_passes;
+         pass += (int64_t)gridDim.x * waves) {
+        int64_t r[PT];
+        int i[PT];
+        bool valid[PT];
+#pragma unroll
+        for (int p = 0; p < PT; ++p) {                 // a second tile past the end computes on tile 0's data
+            const int64_t t = PT * pass + p;
+            const int64_t tt = t < n_tiles ? t : 0;
+            r[p] = tt / tiles_per_req;
+            i[p] = (int)(tt - r[p] * tiles_per_req) * 32 + n;
+            valid[p] = t < n_tiles && i[p] < A.N;
+        }
 
-        // layer-1 B operands: the pair's normalised bf16 row
-        bf16x8_t xb[4];
-        {
+        // layer-1 B operands: the pairs' normalised bf16 rows
+        bf16x8_t xb[PT][4];
+#pragma unroll
+        for (int p = 0; p < PT; ++p) {
+            const int ii = valid[p] ? i[p] : 0;
             float x[5], xt[5];
-            derived_columns(A.prompt_len[r], A.req_off[r + 1] - A.req_off[r], valid ? A.overlap[r * A.N + i] : 0,
-                            A.block_tokens, x);
+            derived_columns(A.prompt_len[r[p]], A.req_off[r[p] + 1] - A.req_off[r[p]],
+                            valid[p] ? A.overlap[r[p] * A.N + ii] : 0, A.block_tokens, x);
             normalise_tail<true>(x, A.mu, A.isig, D_INST, xt);
             const bf16x8_t* row = reinterpret_cast<const bf16x8_t*>(A.xinst + (int64_t)ii * 64);
 #pragma unroll
@@ -226,90 +239,76 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
                     if (c0 >= 0 && c0 < 5 && h == 0) v[j] = (__bf16)xt[c0 < 5 ? c0 : 0];
                     if (c1 >= 0 && c1 < 5 && h == 1) v[j] = (__bf16)xt[c1 < 5 ? c1 : 0];
                 }
-                xb[s] = valid ? v : bf16x8_t{};
+                xb[p][s] = valid[p] ? v : bf16x8_t{};
             }
         }
 
-        // layer 1 in passes: acc = b1 + W1 x, then bf16(relu(.))
-        bf16x8_t hb[KS2];
+        // layer 1, one row tile at a time: acc = b1 + W1 x, then bf16(relu(.))
+        bf16x8_t hb[PT][KS2];
 #pragma unroll
-        for (int g = 0; g < MT1; g += MH) {
-            f32x16_t acc[MH];
-#pragma unroll
-            for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b1frag + ((g + u) * 2 + h) * 16);
-            bf16x8_t a_cur[MH], a_nxt[MH];
-#pragma unroll
-            for (int u = 0; u < MH; ++u) a_cur[u] = w1l[(g + u) * 64];
+        for (int mt = 0; mt < MT1; ++mt) {
+            const f32x16_t bias = load_bias(A.b1frag + (mt * 2 + h) * 16);
+            f32x16_t acc[PT];
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                if (s + 1 < 4) {
+                const bf16x8_t a = w1l[(s * MT1 + mt) * 64];
 #pragma unroll
-                    for (int u = 0; u < MH; ++u) a_nxt[u] = w1l[((s + 1) * MT1 + g + u) * 64];
-                }
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int u = 0; u < MH; ++u)
-                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[u], xb[s], acc[u], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int u = 0; u < MH; ++u) a_cur[u] = a_nxt[u];
+                for (int p = 0; p < PT; ++p)
+                    acc[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xb[p][s], s == 0 ? bias : acc[p], 0, 0, 0);
             }
 #pragma unroll
-            for (int u = 0; u < MH; ++u) {
-                hb[2 * (g + u)] = relu_pack(acc[u], 0);
-                hb[2 * (g + u) + 1] = relu_pack(acc[u], 1);
+            for (int p = 0; p < PT; ++p) {
+                hb[p][2 * mt] = relu_pack(acc[p], 0);
+                hb[p][2 * mt + 1] = relu_pack(acc[p], 1);
             }
         }
 
-        // layer 2 in passes, each pass fed straight into the head (two
-        // accumulators to halve the dependent chain): row 0 = t, row 1 =
-        // sum_j |w3_j| h2_j
-        f32x16_t hd0 = f32x16_t{}, hd1 = f32x16_t{};
-        hd0[0] = h == 0 ? b3 : 0.0f;
+        // layer 2, one row tile at a time, each fed straight into the head:
+        // row 0 = t, row 1 = sum_j |w3_j| h2_j
+        f32x16_t hd[PT];
 #pragma unroll
-        for (int g = 0; g < MT2; g += MH) {
-            f32x16_t acc[MH];
+        for (int p = 0; p < PT; ++p) {
+            hd[p] = f32x16_t{};
+            hd[p][0] = h == 0 ? b3 : 0.0f;
+        }
 #pragma unroll
-            for (int u = 0; u < MH; ++u) acc[u] = load_bias(A.b2frag + ((g + u) * 2 + h) * 16);
-            // one pass spans MH * KS2 fragments (64 KB at h = 256): a per-pass base
-            // keeps every read within the 16-bit immediate offset of ds_read.  The
-            // empty asm hides the base's value from the optimiser, which would
-            // otherwise hoist one address register per far fragment out of the loop.
-            uint32_t pass_base = (uint32_t)(g * KS2 * 64);
-            asm volatile("" : "+s"(pass_base));
-            const bf16x8_t* __restrict__ w2g = lds_w2 + pass_base + lane;
-            // software pipeline: the next k-step's fragments are read from LDS
-            // while this k-step's MFMAs run (the barriers pin that order)
-            bf16x8_t a_cur[MH], a_nxt[MH];
-#pragma unroll
-            for (int u = 0; u < MH; ++u) a_cur[u] = w2g[u * KS2 * 64];
+        for (int mt = 0; mt < MT2; ++mt) {
+            const f32x16_t bias = load_bias(A.b2frag + (mt * 2 + h) * 16);
+            // a per-row-tile base keeps every read within the 16-bit immediate
+            // offset of ds_read; the empty asm hides its value from the
+            // optimiser, which would otherwise hoist one address register per
+            // far fragment out of the loop
+            uint32_t base = (uint32_t)(mt * KS2 * 64);
+            asm volatile("" : "+s"(base));
+            const bf16x8_t* __restrict__ w2g = lds_w2 + base + lane;
+            f32x16_t acc[PT];
+            // software pipeline: the next k-step's fragment is read while this
+            // k-step's MFMAs run (the barriers pin that order)
+            bf16x8_t a_cur = w2g[0], a_nxt;
 #pragma unroll
             for (int s = 0; s < KS2; ++s) {
-                if (s + 1 < KS2) {
-#pragma unroll
-                    for (int u = 0; u < MH; ++u) a_nxt[u] = w2g[(u * KS2 + s + 1) * 64];
-                }
+                if (s + 1 < KS2) a_nxt = w2g[(s + 1) * 64];
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int u = 0; u < MH; ++u)
-                    acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[u], hb[s], acc[u], 0, 0, 0);
+                for (int p = 0; p < PT; ++p)
+                    acc[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur, hb[p][s], s == 0 ? bias : acc[p], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int u = 0; u < MH; ++u) a_cur[u] = a_nxt[u];
+                a_cur = a_nxt;
             }
+            const bf16x8_t f0 = hf[(2 * mt) * 64], f1 = hf[(2 * mt + 1) * 64];
 #pragma unroll
-            for (int u = 0; u < MH; ++u) {
-                hd0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hf[(2 * (g + u)) * 64], relu_pack(acc[u], 0), hd0, 0, 0,
-                                                              0);
-                hd1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hf[(2 * (g + u) + 1) * 64], relu_pack(acc[u], 1), hd1, 0,
-                                                              0, 0);
+            for (int p = 0; p < PT; ++p) {
+                hd[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0, relu_pack(acc[p], 0), hd[p], 0, 0, 0);
+                hd[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1, relu_pack(acc[p], 1), hd[p], 0, 0, 0);
             }
         }
-        const f32x16_t hd = hd0 + hd1;
-        if (h == 0 && valid) {
-            const int64_t p = r * A.N + i;
-            A.scores[p] = hd[0];
-            A.errb[p] = A.band_rel * (hd[1] + fabsf(b3));
+#pragma unroll
+        for (int p = 0; p < PT; ++p) {
+            if (h == 0 && valid[p]) {
+                const int64_t q = r[p] * A.N + i[p];
+                A.scores[q] = hd[p][0];
+                A.errb[q] = A.band_rel * (hd[p][1] + fabsf(b3));
+            }
         }
     }
 }
@@ -355,7 +354,7 @@ hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, c
     a.block_tokens = m.block_tokens;
     a.band_rel = kBandRel;
     const int64_t tiles = (int64_t)R * ((N + 31) / 32);
-    int64_t grid = (tiles + 7) / 8;
+    int64_t grid = (tiles + 15) / 16;                      // 8 waves of 2 tiles
     if (grid > n_cu) grid = n_cu;
     if (grid < 1) grid = 1;
     if (m.h1 == 256) launch_mfma_d<8>(a, m.d, grid, s);

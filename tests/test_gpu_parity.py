@@ -123,6 +123,22 @@ def test_bf16_fast_decisions_equal_canonical_at_full_size():
     print(f"fast scores bitwise canonical: {same:.3f} of {a['scores'].size} pairs", flush=True)
 
 
+@pytest.mark.parametrize("base,R,N", [("large_batch", 37, 13), ("large_batch", 130, 65), ("large_batch", 2, 256),
+                                      ("homogeneous", 70, 45), ("homogeneous", 9, 300), ("tiny", 40, 33)])
+def test_bf16_matrix_core_ragged(base, R, N):
+    """The matrix-core scorers at each hidden width (256 and 128: W2-stationary,
+    64: LDS-streamed) on ragged shapes -- a partial last instance tile, fewer
+    tiles than CUs, more instances than one request's tiles -- with every
+    request checked: decisions and minima exact, scores within the band."""
+    cfg = synth.dataclasses.replace(synth.CONFIGS[base], dtype="bf16", R=R, N=N)
+    w = synth.generate(cfg)
+    assert uses_fast_path(cfg.d, cfg.hidden, cfg.dtype)
+    note(f"bf16 matrix-core ragged {base} d={cfg.d} h={cfg.hidden} R={R} N={N}")
+    run = GpuRun(w)
+    check_scoring(w, run.score(), np.arange(R, dtype=np.int32))
+    run.ctx.close()
+
+
 def test_bf16_exact_mode_matches_oracle_bitwise():
     """ls_set_exact_scores: every bf16 score on the canonical chain, bit-identical to the oracle."""
     w = workload("large_batch")
