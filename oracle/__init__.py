@@ -69,8 +69,11 @@ def _open(path):
                                         P]
         lib.lso_train_round.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, i32, i32, P, P, i32, P, P, i32, i32,
                                         f32, P, P]
+        lib.lso_stamp.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32]
+        lib.lso_stamp.restype = ctypes.c_uint64
+        lib.lso_commit.argtypes = [i32, P, P, P, P, i32, P, P, P, ctypes.c_uint32, P, P, P]
         for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update, lib.lso_route, lib.lso_embed,
-                  lib.lso_buffer_push, lib.lso_train_round):
+                  lib.lso_buffer_push, lib.lso_train_round, lib.lso_commit):
             f.restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
@@ -324,3 +327,45 @@ def train_round(mode, hidden, params, mu, inv_sigma, buf, epochs, batch, lr, per
                              _ptr(loss))
     assert rc == 0, rc
     return p, float(loss[0])
+
+
+# ---------------------------------------------------------------------------
+# prefix-index maintenance (Section 2 / Section 4.2): exact LRU commit
+# ---------------------------------------------------------------------------
+def stamp(epoch: int, r: int, k: int) -> int:
+    """Recency stamp of block k of request r committed in epoch `epoch`."""
+    return int(_load().lso_stamp(epoch, r, k))
+
+
+def initial_stamps(inst_off) -> np.ndarray:
+    """Stamps of a loaded state: entry j of each instance's list gets j + 1."""
+    inst_off = np.asarray(inst_off, np.int64)
+    counts = np.diff(inst_off)
+    out = np.empty(int(inst_off[-1]), np.uint64)
+    for i, c in enumerate(counts):
+        out[inst_off[i]:inst_off[i + 1]] = np.arange(1, c + 1, dtype=np.uint64)
+    return out
+
+
+def commit(inst_off, inst_hashes, inst_stamps, capacity, req_off, req_hashes, chosen, epoch):
+    """One commit of a routed batch.  Returns (off, hashes, stamps) of the new
+    lists, each instance's newest first."""
+    inst_off = _c(inst_off, np.int64)
+    N = len(inst_off) - 1
+    cap = _c(capacity, np.int64)
+    assert len(cap) == N
+    req_off = _c(req_off, np.int64)
+    R = len(req_off) - 1
+    chosen = _c(chosen, np.int32)
+    ih, ist = _c(inst_hashes, np.uint64), _c(inst_stamps, np.uint64)
+    rh = _c(req_hashes, np.uint64)
+    out_off = np.zeros(N + 1, np.int64)
+    total = max(int(cap.sum()), 1)
+    out_h = np.zeros(total, np.uint64)
+    out_s = np.zeros(total, np.uint64)
+    rc = _load().lso_commit(N, _ptr(inst_off), _ptr(ih), _ptr(ist), _ptr(cap), R, _ptr(req_off), _ptr(rh),
+                            _ptr(chosen), epoch, _ptr(out_off), _ptr(out_h), _ptr(out_s))
+    if rc:
+        raise ValueError("commit arguments outside the stamp layout")
+    n = int(out_off[-1])
+    return out_off, out_h[:n].copy(), out_s[:n].copy()

@@ -931,3 +931,102 @@ int lso_train_round(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden
     free(X); free(Y); free(bx); free(by);
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Prefix-index maintenance (Section 2 Background: after routing a request the */
+/* gateway records the request's prefix blocks on the chosen instance, and    */
+/* each engine evicts its least recently used KV blocks; Section 4.2 Prefix   */
+/* KV cache tracker: the index follows the gateway's own routing history).    */
+/*                                                                             */
+/* Every cached block carries a recency stamp, larger = more recent.  A commit */
+/* of a routed batch (epoch e >= 1) touches, for each request r with a chosen  */
+/* instance, each of its blocks k on that instance with stamp                  */
+/*     e * 2^44 + r * 2^20 + (2^20 - 1 - k),                                   */
+/* so later commits beat earlier ones, later requests of a batch beat earlier  */
+/* ones, and within a request a block nearer the prompt's start is the more    */
+/* recent (an engine frees a sequence's tail first, so what stays cached of a  */
+/* request is a prefix of it).  A block keeps the largest stamp it was given.  */
+/* Then every instance holding more than its capacity drops its smallest      */
+/* stamps until it holds exactly its capacity.  Loaded state: entry j of an   */
+/* instance's list has stamp j + 1 (list order = oldest first).               */
+/* ------------------------------------------------------------------------- */
+#define LSO_STAMP_K_BITS 20
+#define LSO_STAMP_R_BITS 24
+#define LSO_STAMP_E_BITS 20
+
+uint64_t lso_stamp(uint32_t epoch, uint32_t r, uint32_t k)
+{
+    return ((uint64_t)epoch << (LSO_STAMP_K_BITS + LSO_STAMP_R_BITS)) | ((uint64_t)r << LSO_STAMP_K_BITS) |
+           (uint64_t)(((uint32_t)1 << LSO_STAMP_K_BITS) - 1u - k);
+}
+
+typedef struct {
+    uint64_t h, s;
+} lso_entry;
+
+static int cmp_hash_newest_first(const void* a, const void* b)
+{
+    const lso_entry* x = (const lso_entry*)a;
+    const lso_entry* y = (const lso_entry*)b;
+    if (x->h != y->h) return x->h < y->h ? -1 : 1;
+    if (x->s != y->s) return x->s > y->s ? -1 : 1;
+    return 0;
+}
+
+static int cmp_newest_first(const void* a, const void* b)
+{
+    const lso_entry* x = (const lso_entry*)a;
+    const lso_entry* y = (const lso_entry*)b;
+    if (x->s != y->s) return x->s > y->s ? -1 : 1;
+    return 0;
+}
+
+/* in_off/in_hash/in_stamp: the instances' lists (CSR over N).  capacity[i] >= 0.
+   chosen[r] outside [0, N) leaves request r out.  out_* receive the new lists,
+   each newest first; out_hash/out_stamp must hold sum_i capacity[i] entries.
+   Returns 0, or -1 when an argument is out of the stamp layout's range. */
+int lso_commit(int32_t N, const int64_t* in_off, const uint64_t* in_hash, const uint64_t* in_stamp,
+               const int64_t* capacity, int32_t R, const int64_t* req_off, const uint64_t* req_hashes,
+               const int32_t* chosen, uint32_t epoch, int64_t* out_off, uint64_t* out_hash, uint64_t* out_stamp)
+{
+    if (epoch == 0 || epoch >= ((uint32_t)1 << LSO_STAMP_E_BITS)) return -1;
+    if ((int64_t)R > ((int64_t)1 << LSO_STAMP_R_BITS)) return -1;
+    for (int32_t r = 0; r < R; ++r)
+        if (req_off[r + 1] - req_off[r] > ((int64_t)1 << LSO_STAMP_K_BITS)) return -1;
+    out_off[0] = 0;
+    for (int32_t i = 0; i < N; ++i) {
+        int64_t cnt = in_off[i + 1] - in_off[i];
+        for (int32_t r = 0; r < R; ++r)
+            if (chosen[r] == i) cnt += req_off[r + 1] - req_off[r];
+        lso_entry* A = (lso_entry*)malloc(sizeof(lso_entry) * (size_t)(cnt > 0 ? cnt : 1));
+        int64_t m = 0;
+        for (int64_t j = in_off[i]; j < in_off[i + 1]; ++j) {
+            A[m].h = in_hash[j];
+            A[m].s = in_stamp[j];
+            ++m;
+        }
+        for (int32_t r = 0; r < R; ++r) {
+            if (chosen[r] != i) continue;
+            for (int64_t k = 0; k < req_off[r + 1] - req_off[r]; ++k) {
+                A[m].h = req_hashes[req_off[r] + k];
+                A[m].s = lso_stamp(epoch, (uint32_t)r, (uint32_t)k);
+                ++m;
+            }
+        }
+        /* one entry per block, with its largest stamp */
+        qsort(A, (size_t)m, sizeof(lso_entry), cmp_hash_newest_first);
+        int64_t u = 0;
+        for (int64_t t = 0; t < m; ++t)
+            if (u == 0 || A[u - 1].h != A[t].h) A[u++] = A[t];
+        /* least recently used out */
+        qsort(A, (size_t)u, sizeof(lso_entry), cmp_newest_first);
+        int64_t keep = u < capacity[i] ? u : capacity[i];
+        for (int64_t t = 0; t < keep; ++t) {
+            out_hash[out_off[i] + t] = A[t].h;
+            out_stamp[out_off[i] + t] = A[t].s;
+        }
+        out_off[i + 1] = out_off[i] + keep;
+        free(A);
+    }
+    return 0;
+}

@@ -716,4 +716,133 @@ def pin_train_round_composition():
     np.testing.assert_array_equal(same, w.params)
 
 
+# ---------------------------------------------------------------------------
+# prefix-index maintenance (Section 2: the gateway records routed prefixes,
+# engines evict least recently used blocks)
+# ---------------------------------------------------------------------------
+def _lists(off, h, st):
+    return [list(zip(h[off[i]:off[i + 1]].tolist(), st[off[i]:off[i + 1]].tolist())) for i in range(len(off) - 1)]
+
+
+def pin_commit_worked_example():
+    """LRU worked by hand, capacity 3: a new batch evicts the oldest entries; within
+    a request the head is newer than the tail; touching a cached block refreshes it;
+    requests sent nowhere change nothing; capacity 0 keeps nothing."""
+    x, y, z, a, b, c = 101, 102, 103, 201, 202, 301
+    off, h = _csr([[x, y, z], [c]])
+    st = oracle.initial_stamps(off)
+    cap = [3, 0]
+    # epoch 1: request 0 = [a, b] -> instance 0; request 1 = [c] -> nowhere (-1)
+    off, h, st = oracle.commit(off, h, st, cap, *_csr([[a, b], [c]]), [0, -1], 1)
+    assert _lists(off, h, st)[0] == [(a, oracle.stamp(1, 0, 0)), (b, oracle.stamp(1, 0, 1)), (z, 3)]
+    assert _lists(off, h, st)[1] == []                    # capacity 0 empties instance 1
+    # epoch 2: request 0 = [c] -> instance 1 (capacity 0), request 1 = [y, a] -> instance 0:
+    # y comes back, a is refreshed, b (epoch 1) now beats z (loaded), z goes
+    off, h, st = oracle.commit(off, h, st, cap, *_csr([[c], [y, a]]), [1, 0], 2)
+    got = _lists(off, h, st)
+    assert [k for k, _ in got[0]] == [y, a, b]
+    assert got[0][0][1] == oracle.stamp(2, 1, 0) and got[0][1][1] == oracle.stamp(2, 1, 1)
+    assert got[0][2][1] == oracle.stamp(1, 0, 1)
+    assert oracle.stamp(2, 0, 0) > oracle.stamp(1, 5, 0) > oracle.stamp(1, 4, 0) > oracle.stamp(1, 4, 1)
+
+
+def _lru_reference(state, cap, reqs, chosen):
+    """Per-access LRU lists (an OrderedDict per instance, most recent at the end):
+    the batch's accesses in order of recency -- requests in order, each request's
+    blocks from its tail to its head -- then each instance trimmed from its
+    least recent end."""
+    from collections import OrderedDict
+    for r, blocks in enumerate(reqs):
+        i = chosen[r]
+        if not 0 <= i < len(state):
+            continue
+        for blk in reversed(blocks):
+            state[i].pop(blk, None)
+            state[i][blk] = True
+    for i, d in enumerate(state):
+        while len(d) > cap[i]:
+            d.popitem(last=False)
+    return state
+
+
+def pin_commit_matches_lru_lists():
+    """Against a per-access LRU simulation on random small batches: repeated blocks
+    within and across requests, the all-ones hash, requests routed nowhere or out of
+    range, capacities from 0 up, several commits in a row."""
+    from collections import OrderedDict
+    rng = np.random.default_rng(77)
+    for trial in range(6):
+        N = int(rng.integers(1, 5))
+        cap = rng.integers(0, 9, N).tolist()
+        pool = np.array(rng.integers(1, 40, 30).tolist() + [2**64 - 1], dtype=np.uint64)
+        lists0 = [[int(v) for v in dict.fromkeys(rng.choice(pool, int(rng.integers(0, 8))).tolist())]
+                  for _ in range(N)]
+        state = [OrderedDict((k, True) for k in l) for l in lists0]
+        off, h = _csr(lists0)
+        st = oracle.initial_stamps(off)
+        for epoch in range(1, 5):
+            R = int(rng.integers(0, 7))
+            reqs = [[int(v) for v in rng.choice(pool, int(rng.integers(0, 6)))] for _ in range(R)]
+            chosen = rng.integers(-1, N + 1, R).astype(np.int32)
+            state = _lru_reference(state, cap, reqs, chosen)
+            roff, rh = _csr(reqs) if R else (np.zeros(1, np.int64), np.zeros(0, np.uint64))
+            off, h, st = oracle.commit(off, h, st, cap, roff, rh, chosen, epoch)
+            got = _lists(off, h, st)
+            for i in range(N):
+                assert [k for k, _ in got[i]] == list(reversed(state[i])), (trial, epoch, i)
+                stamps = [v for _, v in got[i]]
+                assert stamps == sorted(stamps, reverse=True) and len(set(stamps)) == len(stamps)
+
+
+def _chain(parent_hash, token_block):
+    """A block's hash: a 64-bit mix of its parent's hash and its own tokens."""
+    z = (parent_hash * 0x100000001B3 ^ (token_block + 0x9E3779B97F4A7C15)) & (2**64 - 1)
+    z = ((z ^ (z >> 31)) * 0xD6E8FEB86659FD93) & (2**64 - 1)
+    return z ^ (z >> 29)
+
+
+def pin_commit_keeps_prefixes():
+    """Tail-first eviction keeps every instance's cache closed under prefixes: with
+    chained block hashes (a block's hash covers all earlier blocks), after any
+    sequence of commits every cached block's parent block is cached too."""
+    rng = np.random.default_rng(5)
+    N = 3
+    cap = [12, 20, 7]
+    parent = {}
+    prefixes = []                                        # shared request prefixes
+    for g in range(4):
+        hsh, blocks = 0, []
+        for t in range(int(rng.integers(2, 6))):
+            nh = _chain(hsh, 1000 * g + t)
+            parent[nh] = hsh
+            blocks.append(nh)
+            hsh = nh
+        prefixes.append(blocks)
+    off, h = _csr([[] for _ in range(N)])
+    st = oracle.initial_stamps(off)
+    uid = 0
+    for epoch in range(1, 9):
+        reqs = []
+        for _ in range(int(rng.integers(1, 6))):
+            g = int(rng.integers(0, len(prefixes)))
+            blocks = list(prefixes[g][:int(rng.integers(1, len(prefixes[g]) + 1))])
+            hsh = blocks[-1]
+            for _t in range(int(rng.integers(0, 5))):       # a private suffix
+                uid += 1
+                nh = _chain(hsh, 10**6 + uid)
+                parent[nh] = hsh
+                blocks.append(nh)
+                hsh = nh
+            reqs.append(blocks)
+        chosen = rng.integers(0, N, len(reqs)).astype(np.int32)
+        off, h, st = oracle.commit(off, h, st, cap, *_csr(reqs), chosen, epoch)
+        for i, entries in enumerate(_lists(off, h, st)):
+            cached = {k for k, _ in entries}
+            assert len(cached) <= cap[i]
+            for k in cached:
+                p = parent[k]
+                assert p == 0 or p in cached, (epoch, i)
+        assert int(off[-1]) > 0
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -91,6 +91,16 @@ MUTANTS = [
     ("train_drops_partial_batch", "int32_t m = n - s < batch ? n - s : batch;",
      "int32_t m = batch;\n            if (n - s < batch) break;"),
     ("train_skips_replay", "int32_t n = fifo_count + rep_count;", "int32_t n = fifo_count;"),
+    ("commit_keeps_oldest", "    const lso_entry* y = (const lso_entry*)b;\n    if (x->s != y->s) return x->s > y->s ? -1 : 1;\n    return 0;\n}\n\n/* in_off",
+     "    const lso_entry* y = (const lso_entry*)b;\n    if (x->s != y->s) return x->s < y->s ? -1 : 1;\n    return 0;\n}\n\n/* in_off"),
+    ("commit_block_keeps_first_stamp", "if (x->h != y->h) return x->h < y->h ? -1 : 1;\n    if (x->s != y->s) return x->s > y->s ? -1 : 1;",
+     "if (x->h != y->h) return x->h < y->h ? -1 : 1;\n    if (x->s != y->s) return x->s < y->s ? -1 : 1;"),
+    ("commit_head_first_eviction", "(uint64_t)(((uint32_t)1 << LSO_STAMP_K_BITS) - 1u - k);", "(uint64_t)k;"),
+    ("commit_requests_reversed", "((uint64_t)r << LSO_STAMP_K_BITS)", "((uint64_t)(0xFFFFFFu - r) << LSO_STAMP_K_BITS)"),
+    ("commit_capacity_off_by_one", "int64_t keep = u < capacity[i] ? u : capacity[i];",
+     "int64_t keep = u < capacity[i] ? u : capacity[i] - 1;"),
+    ("commit_no_dedup", "if (u == 0 || A[u - 1].h != A[t].h) A[u++] = A[t];", "A[u++] = A[t];"),
+    ("commit_skips_first_request", "if (chosen[r] != i) continue;", "if (chosen[r] != i || r == 0) continue;"),
 ]
 
 _RUNNER = r"""
