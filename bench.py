@@ -194,6 +194,40 @@ def time_online_learning(ctx, w):
             "train_samples_per_s": round(5 * 10000 / (train_ms / 1e3), 1)}
 
 
+def time_maintenance(w, inst_h, req_off, req_h, chosen, reps):
+    """Prefix-index maintenance (Section 2: the gateway records each routed request's blocks on its instance,
+    engines evict least recently used blocks): the step's routed batch committed into the loaded state with exact
+    LRU eviction to the loaded capacity, then the tables rebuilt.  Each commit runs on a fresh load, untimed."""
+    import torch
+
+    from paper_2606_00946_amd import lodestar
+    cfg = w.cfg
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype, device=0)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    ctx.ls_set_cache_capacity(np.diff(w.inst_off))
+    n_hashes = int(w.req_off[-1])
+    wall, kinds = 0.0, {}
+    for i in range(reps + 1):
+        ctx.ls_load_cache_state(w.inst_off, inst_h)
+        torch.cuda.synchronize()
+        if i > 0:
+            ctx.ls_profile_enable(True)
+        t0 = time.perf_counter()
+        ctx.ls_commit_routes(req_off, req_h, chosen, n_hashes=n_hashes)
+        torch.cuda.synchronize()
+        if i > 0:
+            wall += time.perf_counter() - t0
+            for k, v in ctx.ls_profile_read().items():
+                kinds[k] = kinds.get(k, 0.0) + v[1]
+            ctx.ls_profile_enable(False)
+    off, _, _ = ctx.ls_read_cache_state()
+    ctx.close()
+    ms = wall * 1e3 / reps
+    return {"commit_ms": round(ms, 4), "kernel_ms": {k: round(v / reps, 4) for k, v in kinds.items()},
+            "routed_blocks": n_hashes, "cached_blocks_after": int(off[-1]),
+            "requests_per_s": round(w.cfg.R / (ms / 1e3), 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,6 +337,7 @@ def main():
     }
     result["route"] = time_route(ctx, w, (req_off, req_h, plen, feat), args.steps)
     result["online_learning"] = time_online_learning(ctx, w)
+    result["maintenance"] = time_maintenance(w, inst_h, req_off, req_h, chosen, max(1, min(args.steps, 5)))
     ctx.close()
     if args.copy_probe_mib > 0:
         copy_probe(args.copy_probe_mib)

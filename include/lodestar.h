@@ -116,6 +116,51 @@ int ls_load_cache_state(ls_ctx* ctx, int32_t n_instances, const int64_t* inst_of
                         const uint64_t* hashes, void* stream);
 
 /*
+ * Prefix-index maintenance (Section 2: after routing a request the gateway
+ * records its prefix blocks on the chosen instance, and each engine evicts its
+ * least recently used KV blocks; Section 4.2: the index follows the gateway's
+ * own routing history).  Every cached block carries a recency stamp.
+ *
+ * ls_set_cache_capacity
+ *   capacity  HOST int64 [n_instances], blocks each instance holds (>= 0).
+ *   The next ls_load_cache_state with n_instances instances keeps each
+ *   instance's block list with stamps -- entry j of its loaded hashes gets
+ *   stamp j + 1 (list order = oldest first; a repeated hash keeps its newest
+ *   entry) -- and sizes its table for max(loaded, capacity) blocks.  To change
+ *   capacities, set them and load again.  capacity = NULL turns maintenance
+ *   off (the default).  LS_ERR_INVALID for a negative capacity.
+ *
+ * ls_commit_routes
+ *   DEVICE req_off int64 [R+1], req_hashes uint64 [n_hashes = req_off[R]],
+ *   chosen int32 [R]: request r's blocks go to instance chosen[r]; a value
+ *   outside [0, N) leaves the request out (e.g. -1).  Block k of request r is
+ *   touched with stamp
+ *       epoch * 2^44 + r * 2^20 + (2^20 - 1 - k),
+ *   epoch = commits since the load, from 1: later commits, later requests of
+ *   a batch and blocks nearer the prompt's start are more recent (engines free
+ *   a sequence's tail first, so what stays cached of a request is a prefix of
+ *   it).  A block keeps its largest stamp.  Then every instance above its
+ *   capacity keeps its `capacity` most recent blocks (stamps are unique per
+ *   instance, so the set is exact), and the tables are rebuilt: later calls on
+ *   the stream see the new state.  R <= 2^24 (LS_ERR_INVALID); at most
+ *   2^20 - 2 commits per load (LS_ERR_STATE); n_r <= 2^20 is the caller's
+ *   (later blocks share the last rank).  LS_ERR_STATE unless the state was
+ *   loaded under ls_set_cache_capacity.  Asynchronous; the library-owned
+ *   workspace grows (synchronizing the device) when a batch needs more.
+ *
+ * ls_read_cache_state
+ *   Synchronous.  inst_off HOST int64 [n_instances + 1] out: the lists'
+ *   offsets.  hashes / stamps DEVICE uint64 [max_entries] out (either may be
+ *   NULL): each instance's blocks and stamps, in no particular order.
+ *   LS_ERR_INVALID if an array is given and max_entries < inst_off[N].
+ */
+int ls_set_cache_capacity(ls_ctx* ctx, int32_t n_instances, const int64_t* capacity);
+int ls_commit_routes(ls_ctx* ctx, int32_t R, int64_t n_hashes, const int64_t* req_off,
+                     const uint64_t* req_hashes, const int32_t* chosen, void* stream);
+int ls_read_cache_state(ls_ctx* ctx, int32_t n_instances, int64_t* inst_off, uint64_t* hashes,
+                        uint64_t* stamps, int64_t max_entries, void* stream);
+
+/*
  * Score a batch of R requests against the N loaded instances (Section 4.1
  * greedy routing; Alg. 4 normalise -> batched forward -> argmax of reward,
  * here argmin of predicted TTFT, ties to the lowest instance id).
@@ -335,7 +380,7 @@ int ls_train_round(ls_ctx* ctx, int32_t epochs, int32_t batch, float lr, const i
  * kernel launch group of the context is bracketed by HIP events on the stream
  * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
  * "score_pairs", "score_pairs_mfma", "band_select", "rescore", "argmin",
- * "update", "route", "buffer".
+ * "update", "route", "buffer", "index" (prefix-index maintenance).
  *   ls_profile_enable  enable != 0 starts recording (and clears old records).
  *   ls_profile_read    synchronous; for up to max_kinds kinds writes the kind
  *                      name (static string), the number of launches and the

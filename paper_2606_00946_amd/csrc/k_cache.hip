@@ -21,6 +21,10 @@
 // between a key's home and its slot is full and the slots before it in its
 // bucket are filled, which is all a lookup relies on.  Repeated input keys may
 // each take a slot; the table is sized by the input count, so they still fit.
+// Optionally the build records, for every slot it fills, the input position of
+// the key placed there (`entry_of`), and per instance the position of the
+// all-ones key (`eidx`): with unique keys per instance that is the slot map the
+// index maintenance keeps.
 #include "ls_internal.h"
 
 namespace ls {
@@ -56,11 +60,12 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
     return hipGetLastError();
 }
 
-// Insert `key` into the table of nb buckets, probing from bucket b.  A slot
-// changes at most once (empty -> key), so a stale read can only show a filled
-// slot as empty; the CAS on it then returns the key that holds it.  Each slot
-// is tried at most once per bucket, so the loop ends.
-__device__ void global_insert(uint64_t* table, uint32_t nb, uint32_t b, uint64_t key) {
+// Insert `key` into the table of nb buckets, probing from bucket b; returns the
+// slot (bucket * 8 + position) that holds it, or -1 if the table is full.  A
+// slot changes at most once (empty -> key), so a stale read can only show a
+// filled slot as empty; the CAS on it then returns the key that holds it.
+// Each slot is tried at most once per bucket, so the loop ends.
+__device__ int64_t global_insert(uint64_t* table, uint32_t nb, uint32_t b, uint64_t key) {
     for (uint32_t probe = 0; probe < nb; ++probe) {
         uint64_t* bk = table + (int64_t)b * kBucketKeys;
         const ulonglong2* q = reinterpret_cast<const ulonglong2*>(bk);
@@ -68,30 +73,31 @@ __device__ void global_insert(uint64_t* table, uint32_t nb, uint32_t b, uint64_t
         const uint64_t slot[kBucketKeys] = {v0.x, v0.y, v1.x, v1.y, v2.x, v2.y, v3.x, v3.y};
 #pragma unroll
         for (int s = 0; s < kBucketKeys; ++s) {
-            if (slot[s] == key) return;
+            if (slot[s] == key) return (int64_t)b * kBucketKeys + s;
             if (slot[s] == kEmptyKey) {
                 const unsigned long long old = atomicCAS((unsigned long long*)(bk + s), (unsigned long long)kEmptyKey,
                                                          (unsigned long long)key);
-                if (old == kEmptyKey || old == key) return;
+                if (old == kEmptyKey || old == key) return (int64_t)b * kBucketKeys + s;
             }
         }
         b = (b + 1 == nb) ? 0 : b + 1;                 // bucket full without the key
     }
+    return -1;
 }
 
 // Place `key` in an LDS segment of nbl buckets, probing from local bucket lb:
-// the bucket's fill counter hands out slots in order.  False when the probe
-// runs past the segment's last bucket.
-__device__ __forceinline__ bool segment_place(uint64_t* seg, uint32_t* fill, uint32_t lb, uint32_t nbl,
-                                              uint64_t key) {
+// the bucket's fill counter hands out slots in order.  Returns the local slot,
+// or -1 when the probe runs past the segment's last bucket.
+__device__ __forceinline__ int32_t segment_place(uint64_t* seg, uint32_t* fill, uint32_t lb, uint32_t nbl,
+                                                 uint64_t key) {
     for (; lb < nbl; ++lb) {
         const uint32_t slot = atomicAdd(&fill[lb], 1u);
         if (slot < (uint32_t)kBucketKeys) {
             seg[lb * kBucketKeys + slot] = key;
-            return true;
+            return (int32_t)(lb * kBucketKeys + slot);
         }
     }
-    return false;
+    return -1;
 }
 
 __device__ __forceinline__ int32_t owner_of(const int64_t* __restrict__ off, int32_t n, int64_t t) {
@@ -110,7 +116,7 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     uint64_t* __restrict__ keys, const int64_t* __restrict__ base, const uint32_t* __restrict__ nbuckets,
     uint32_t* __restrict__ flags, const int64_t* __restrict__ inst_off, const int32_t* __restrict__ seg_off,
     int32_t n_inst, const uint64_t* __restrict__ hashes, int64_t* __restrict__ ovf, uint32_t* __restrict__ ovf_count,
-    uint32_t ovf_cap) {
+    uint32_t ovf_cap, uint32_t* __restrict__ entry_of, int64_t* __restrict__ eidx) {
     __shared__ uint64_t seg[kSegBuckets * kBucketKeys];
     __shared__ uint32_t fill[kSegBuckets];
     // Workgroups are dealt to the 8 XCDs round-robin; renumber them so that the
@@ -144,12 +150,19 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             if (t + u * kSegThreads >= t1) continue;
-            if (k[u] == kEmptyKey) { has_empty = 1; continue; }
+            if (k[u] == kEmptyKey) {
+                has_empty = 1;
+                if (eidx) eidx[i] = t + u * kSegThreads;
+                continue;
+            }
             const uint32_t lb = bucket_of(k[u], nb) - b0;
             if (lb >= nbl) continue;                // home bucket in another segment
-            if (!segment_place(seg, fill, lb, nbl, k[u])) {
+            const int32_t ls = segment_place(seg, fill, lb, nbl, k[u]);
+            if (ls < 0) {
                 const uint32_t pos = atomicAdd(ovf_count, 1u);
                 if (pos < ovf_cap) ovf[pos] = t + u * kSegThreads;
+            } else if (entry_of) {
+                entry_of[(base[i] + b0) * kBucketKeys + ls] = (uint32_t)(t + u * kSegThreads);
             }
         }
     }
@@ -167,11 +180,12 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
                                       const uint32_t* __restrict__ nbuckets, const int64_t* __restrict__ inst_off,
                                       int32_t n_inst, const uint64_t* __restrict__ hashes, int64_t total,
                                       const int64_t* __restrict__ ovf, const uint32_t* __restrict__ ovf_count,
-                                      uint32_t ovf_cap) {
+                                      uint32_t ovf_cap, uint32_t* __restrict__ entry_of) {
     const uint32_t n = *ovf_count;
     if (n == 0) return;
     const bool queued = n <= ovf_cap;
-    const int64_t count = queued ? (int64_t)n : total;
+    const int64_t n_keys = inst_off[n_inst] < total ? inst_off[n_inst] : total;   // total bounds the key count
+    const int64_t count = queued ? (int64_t)n : n_keys;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < count; j += stride) {
         const int64_t t = queued ? ovf[j] : j;
@@ -184,7 +198,8 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
             b = (b / kSegBuckets + 1) * kSegBuckets;
             if (b >= nb) b = 0;
         }
-        global_insert(keys + base[i] * kBucketKeys, nb, b, key);
+        const int64_t q = global_insert(keys + base[i] * kBucketKeys, nb, b, key);
+        if (entry_of && q >= 0) entry_of[base[i] * kBucketKeys + q] = (uint32_t)t;
     }
 }
 
@@ -192,17 +207,17 @@ int64_t table_overflow_capacity(int64_t total) { return 4096 + total / 64; }
 
 hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
                               const uint64_t* hashes, int64_t total, int32_t n_inst, void* ovf_ws, int n_cu,
-                              hipStream_t s) {
+                              hipStream_t s, uint32_t* entry_of, int64_t* eidx) {
     uint32_t* count = reinterpret_cast<uint32_t*>(ovf_ws);
     int64_t* list = reinterpret_cast<int64_t*>(static_cast<char*>(ovf_ws) + 256);
     const uint32_t cap = (uint32_t)table_overflow_capacity(total);
     hipError_t e = launch_fill_u32(count, 0u, 1, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(table_segment_kernel, dim3((uint32_t)n_seg), dim3(kSegThreads), 0, s, t.keys, t.base,
-                       t.nbuckets, t.flags, inst_off, seg_off, n_inst, hashes, list, count, cap);
+                       t.nbuckets, t.flags, inst_off, seg_off, n_inst, hashes, list, count, cap, entry_of, eidx);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(table_overflow_kernel, dim3((uint32_t)(4 * n_cu)), dim3(256), 0, s, t.keys, t.base,
-                       t.nbuckets, inst_off, n_inst, hashes, total, list, count, cap);
+                       t.nbuckets, inst_off, n_inst, hashes, total, list, count, cap, entry_of);
     return hipGetLastError();
 }
 

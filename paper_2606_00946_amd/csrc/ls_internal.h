@@ -100,9 +100,59 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
 // bytes) and table_overflow_capacity(total) int64 key indices.
 constexpr uint32_t kSegBuckets = 2048;
 int64_t table_overflow_capacity(int64_t total);
+// Prefix-index maintenance (k_index.hip).  One commit of a routed batch.
+constexpr int64_t kSelChunk = 4096;           // candidates per selection chunk
+struct IndexCommit {
+    int32_t N = 0, R = 0;
+    uint32_t epoch = 0;
+    int n_cu = 1;
+    const int64_t* req_off = nullptr;       // routed batch (device)
+    const uint64_t* req_hashes = nullptr;
+    const int32_t* chosen = nullptr;
+    const int64_t* off = nullptr;           // current lists; stamps touched in place
+    const uint64_t* hash = nullptr;
+    uint64_t* stamp = nullptr;
+    const uint32_t* entry_of = nullptr;     // table slot -> list entry
+    const int64_t* eidx = nullptr;          // [N] entry of the all-ones key, -1 if absent
+    const int64_t* capacity = nullptr;      // [N] blocks
+    int64_t* occ = nullptr;                 // [N] workspace
+    int64_t* fbase = nullptr;               // [N + 1] batch-local set buckets
+    uint64_t* fkey = nullptr;
+    uint64_t* fstamp = nullptr;
+    int64_t fresh_slots_bound = 0;
+    int64_t* fcount = nullptr;              // [N]
+    uint64_t* efresh = nullptr;             // [N]
+    int64_t* cand = nullptr;                // [N]
+    int64_t* off2 = nullptr;                // [N + 1] new lists
+    uint64_t* hash2 = nullptr;
+    uint64_t* stamp2 = nullptr;
+    // selection of each instance's survivors, in chunks of candidates
+    int64_t* nvirt = nullptr;               // [N] candidate positions (listed, set slots, all-ones)
+    int64_t* chunk0 = nullptr;              // [N + 1] first chunk of each instance
+    int64_t chunk_bound = 0;                // upper bound of chunk0[N]
+    int64_t* sel_want = nullptr;            // [N]
+    uint64_t* sel_prefix = nullptr;         // [N]
+    uint64_t* sel_mask = nullptr;           // [N]
+    int64_t* sel_pos = nullptr;             // [N]
+    int64_t* sel_active = nullptr;          // [N]
+    uint32_t* sel_hist = nullptr;           // [N x 256]
+};
+hipError_t launch_position_stamps(const int64_t* off, int32_t N, uint64_t* stamp, int64_t total, int n_cu,
+                                  hipStream_t s);
+hipError_t launch_entry_map(const CacheTables& T, const int64_t* off, int32_t N, const uint64_t* hash,
+                            uint32_t* entry_of, int64_t* eidx, int64_t total_bound, int n_cu, hipStream_t s);
+hipError_t launch_live_entries(const CacheTables& T, const int64_t* off, int32_t N, const uint64_t* hash,
+                               const uint32_t* entry_of, const int64_t* eidx, uint8_t* live, int64_t total_bound,
+                               int n_cu, hipStream_t s);
+hipError_t launch_dedup_lists(const int64_t* off, int32_t N, const uint64_t* hash, const uint64_t* stamp,
+                              const uint8_t* live, int64_t* cand, int64_t* off2, uint64_t* hash2, uint64_t* stamp2,
+                              hipStream_t s);
+hipError_t launch_commit(const CacheTables& T, const IndexCommit& C, hipStream_t s);
+
 hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
                               const uint64_t* hashes, int64_t total, int32_t n_inst, void* ovf_ws, int n_cu,
-                              hipStream_t s);
+                              hipStream_t s, uint32_t* entry_of = nullptr,
+                              int64_t* eidx = nullptr);
 
 // Group table for the prefix-sharing pass: a power of two >= 2R slots.
 inline int64_t group_table_size(int32_t R) {

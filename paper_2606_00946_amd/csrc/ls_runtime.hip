@@ -41,7 +41,26 @@ struct ls_ctx {
     int32_t* seg_off_dev = nullptr;    // [N + 1] first table segment of each instance
     void* tws = nullptr;               // table-build overflow queue
     size_t tws_cap = 0;
+    int64_t tables_nseg = 0;           // table segments of the loaded layout
     bool have_cache = false;
+    // prefix-index maintenance: per-instance lists with recency stamps
+    struct Index {
+        bool on = false;                   // capacities set: loads keep the lists
+        bool live = false;                 // lists of the loaded state present
+        std::vector<int64_t> capacity;     // [n] blocks per instance
+        int32_t n = 0;
+        uint32_t epoch = 0;                // commits since the load
+        int64_t list_entries = 0;          // entries each list buffer holds
+        uint64_t *hash = nullptr, *stamp = nullptr, *hash2 = nullptr, *stamp2 = nullptr;
+        size_t hash_cap = 0, stamp_cap = 0, hash2_cap = 0, stamp2_cap = 0;
+        uint32_t* entry_of = nullptr;      // [table slots] list entry of the key in a slot
+        size_t entry_cap = 0;
+        int64_t* small = nullptr;          // per-instance arrays (layout in index_small)
+        size_t small_cap = 0;
+        int64_t *off = nullptr, *off2 = nullptr;   // [n + 1] each, inside `small`
+        void* ws = nullptr;                // batch-local sets, live flags
+        size_t ws_cap = 0;
+    } idx;
     // grow-only workspace
     void* ws = nullptr;
     size_t ws_cap = 0;
@@ -161,11 +180,11 @@ int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
 
 enum Kind {
     K_TABLE = 0, K_PREFIX, K_PARTIAL, K_SCORE, K_ARGMIN, K_UPDATE, K_SCORE_MFMA, K_BAND, K_RESCORE, K_ROUTE, K_BUFFER,
-    K_COUNT
+    K_INDEX, K_COUNT
 };
 const char* const kKindNames[K_COUNT] = {"table_build", "prefix_match", "instance_partial", "score_pairs", "argmin",
                                          "update", "score_pairs_mfma", "band_select", "rescore", "route",
-                                         "buffer"};
+                                         "buffer", "index"};
 
 hipEvent_t take_event(ls_ctx* c) {
     if (!c->spare.empty()) {
@@ -322,7 +341,9 @@ void ls_destroy(ls_ctx* c) {
                         (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
                         (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws, (void*)c->buf.fifo_x,
                         (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
-                        (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws})
+                        (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws, (void*)c->idx.hash,
+                        (void*)c->idx.stamp, (void*)c->idx.hash2, (void*)c->idx.stamp2, (void*)c->idx.entry_of,
+                        (void*)c->idx.small, c->idx.ws})
             if (p) (void)hipFree(p);
         if (c->stage) (void)hipHostFree(c->stage);
         if (c->stage_done) (void)hipEventDestroy(c->stage_done);
@@ -382,6 +403,89 @@ int ls_get_model(ls_ctx* c, float* params, int64_t n_params, float* mu, float* i
     return LS_OK;
 }
 
+namespace {
+
+// Per-instance arrays of the index, in one allocation of kIndexSmallPerN * N + 4 int64.
+constexpr int64_t kIndexSmallPerN = 16;
+struct IndexSmall {
+    int64_t *off_a, *off_b, *cap, *eidx, *occ, *fbase, *fcount, *cand, *nvirt, *chunk0, *want, *pos, *active;
+    uint64_t *efresh, *prefix, *mask;
+};
+IndexSmall index_small(int64_t* p, int32_t N) {
+    IndexSmall m;
+    m.off_a = p; p += N + 1;
+    m.off_b = p; p += N + 1;
+    m.cap = p; p += N;
+    m.eidx = p; p += N;
+    m.occ = p; p += N;
+    m.fbase = p; p += N + 1;
+    m.fcount = p; p += N;
+    m.cand = p; p += N;
+    m.efresh = reinterpret_cast<uint64_t*>(p); p += N;
+    m.nvirt = p; p += N;
+    m.chunk0 = p; p += N + 1;
+    m.want = p; p += N;
+    m.prefix = reinterpret_cast<uint64_t*>(p); p += N;
+    m.mask = reinterpret_cast<uint64_t*>(p); p += N;
+    m.pos = p; p += N;
+    m.active = p;
+    return m;
+}
+
+// After a load under ls_set_cache_capacity: the loaded hashes become the
+// instances' lists (entry j stamped j + 1; a repeated key keeps its newest
+// entry), and every table slot learns its key's list entry.
+int index_load(ls_ctx* c, int32_t N, int64_t total, int64_t list_entries, const uint64_t* hashes, hipStream_t s) {
+    auto& X = c->idx;
+    const size_t lb = sizeof(uint64_t) * (size_t)(list_entries > 0 ? list_entries : 1);
+    int rc;
+    if ((rc = grow(c, (void**)&X.hash, &X.hash_cap, lb)) || (rc = grow(c, (void**)&X.stamp, &X.stamp_cap, lb)) ||
+        (rc = grow(c, (void**)&X.hash2, &X.hash2_cap, lb)) || (rc = grow(c, (void**)&X.stamp2, &X.stamp2_cap, lb)))
+        return rc;
+    const int64_t slots = c->tables.total_buckets * ls::kBucketKeys;
+    if ((rc = grow(c, (void**)&X.entry_of, &X.entry_cap, sizeof(uint32_t) * (size_t)slots))) return rc;
+    if ((rc = grow(c, (void**)&X.small, &X.small_cap, sizeof(int64_t) * (size_t)(kIndexSmallPerN * N + 4))))
+        return rc;
+    if ((rc = grow(c, &X.ws, &X.ws_cap, (size_t)(total > 0 ? total : 1)))) return rc;
+    const size_t tw = 256 + sizeof(int64_t) * (size_t)ls::table_overflow_capacity(list_entries);
+    if ((rc = grow(c, &c->tws, &c->tws_cap, tw))) return rc;
+    X.list_entries = list_entries;
+    IndexSmall m = index_small(X.small, N);
+    X.off = m.off_a;
+    X.off2 = m.off_b;
+    // capacities through the staging buffer
+    rc = stage_reserve(c, sizeof(int64_t) * (size_t)N);
+    if (rc) return rc;
+    memcpy(c->stage, X.capacity.data(), sizeof(int64_t) * (size_t)N);
+    LS_HIP(c, hipMemcpyAsync(m.cap, c->stage, sizeof(int64_t) * (size_t)N, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipEventRecord(c->stage_done, s));
+    c->stage_pending = true;
+    Timed t(c, K_INDEX, s);
+    LS_HIP(c, hipMemcpyAsync(X.off, c->inst_off_dev, sizeof(int64_t) * (size_t)(N + 1), hipMemcpyDeviceToDevice, s));
+    if (total > 0)
+        LS_HIP(c, hipMemcpyAsync(X.hash, hashes, sizeof(uint64_t) * (size_t)total, hipMemcpyDeviceToDevice, s));
+    LS_HIP(c, ls::launch_position_stamps(X.off, N, X.stamp, total, c->n_cu, s));
+    LS_HIP(c, ls::launch_fill_u32(X.entry_of, 0u, slots, s));
+    LS_HIP(c, ls::launch_entry_map(c->tables, X.off, N, X.hash, X.entry_of, m.eidx, total, c->n_cu, s));
+    uint8_t* live = static_cast<uint8_t*>(X.ws);
+    LS_HIP(c, ls::launch_live_entries(c->tables, X.off, N, X.hash, X.entry_of, m.eidx, live, total, c->n_cu, s));
+    LS_HIP(c, ls::launch_dedup_lists(X.off, N, X.hash, X.stamp, live, m.cand, X.off2, X.hash2, X.stamp2, s));
+    std::swap(X.off, X.off2);
+    std::swap(X.hash, X.hash2);
+    std::swap(X.stamp, X.stamp2);
+    std::swap(X.hash_cap, X.hash2_cap);
+    std::swap(X.stamp_cap, X.stamp2_cap);
+    LS_HIP(c, ls::launch_fill_u32(X.entry_of, 0u, slots, s));
+    LS_HIP(c, ls::launch_entry_map(c->tables, X.off, N, X.hash, X.entry_of, m.eidx, total, c->n_cu, s));
+    t.done();
+    X.n = N;
+    X.epoch = 0;
+    X.live = true;
+    return LS_OK;
+}
+
+}  // namespace
+
 int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off, const uint64_t* hashes,
                         void* stream) {
     if (!c) return LS_ERR_INVALID;
@@ -400,12 +504,16 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     // bucket layout: about four keys per 8-slot bucket (half load), built in
     // segments of kSegBuckets buckets
     const int N = n_instances;
+    const bool keep_lists = c->idx.on && (int32_t)c->idx.capacity.size() == N;
+    c->idx.live = false;
     std::vector<int64_t> base(N);
     std::vector<uint32_t> nb(N);
     std::vector<int32_t> seg_off(N + 1);
-    int64_t nbk = 0, nseg = 0;
+    int64_t nbk = 0, nseg = 0, list_entries = 0;
     for (int i = 0; i < N; ++i) {
         int64_t cnt = inst_off[i + 1] - inst_off[i];
+        if (keep_lists && c->idx.capacity[i] > cnt) cnt = c->idx.capacity[i];   // room for the lists' growth
+        list_entries += cnt;
         int64_t b = (cnt + 3) / 4;
         if (b < 1) b = 1;
         if (b > 0x7fffffff) return fail(c, LS_ERR_UNSUPPORTED, "instance %d caches too many blocks", i);
@@ -462,6 +570,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     c->stage_pending = true;
     c->tables.n = N;
     c->tables.total_buckets = nbk;
+    c->tables_nseg = nseg;
     // build
     {
         Timed t(c, K_TABLE, s);
@@ -471,6 +580,10 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
         LS_HIP(c, e);
     }
     c->have_cache = true;
+    if (keep_lists) {
+        rc = index_load(c, N, total, list_entries, hashes, s);
+        if (rc) return rc;
+    }
     return LS_OK;
 }
 
@@ -998,6 +1111,133 @@ int ls_profile_read(ls_ctx* c, int32_t max_kinds, const char** names, int64_t* l
         ++k;
     }
     if (n_kinds) *n_kinds = k;
+    return LS_OK;
+}
+
+
+int ls_set_cache_capacity(ls_ctx* c, int32_t n_instances, const int64_t* capacity) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!capacity) {
+        c->idx.on = false;
+        c->idx.live = false;
+        c->idx.capacity.clear();
+        return LS_OK;
+    }
+    if (n_instances < 1) return fail(c, LS_ERR_INVALID, "n_instances must be >= 1");
+    for (int32_t i = 0; i < n_instances; ++i)
+        if (capacity[i] < 0) return fail(c, LS_ERR_INVALID, "capacity[%d] is negative", i);
+    c->idx.capacity.assign(capacity, capacity + n_instances);
+    c->idx.on = true;
+    c->idx.live = false;                     // the lists come with the next load
+    return LS_OK;
+}
+
+int ls_commit_routes(ls_ctx* c, int32_t R, int64_t n_hashes, const int64_t* req_off, const uint64_t* req_hashes,
+                     const int32_t* chosen, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    auto& X = c->idx;
+    if (!X.live) return fail(c, LS_ERR_STATE, "no cache state was loaded under ls_set_cache_capacity");
+    if (R < 0 || R > (1 << 24)) return fail(c, LS_ERR_INVALID, "R must be in [0, 2^24]");
+    if (n_hashes < 0) return fail(c, LS_ERR_INVALID, "n_hashes must be >= 0");
+    if (R > 0 && (!req_off || !chosen || (n_hashes > 0 && !req_hashes)))
+        return fail(c, LS_ERR_INVALID, "req_off, req_hashes and chosen must be non-NULL");
+    if (X.epoch + 1 >= (1u << 20)) return fail(c, LS_ERR_STATE, "2^20 - 1 commits since the load: reload the state");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const int32_t N = X.n;
+    // batch-local sets: at most n_hashes / 4 + N + 1 buckets of 8 keys and 8
+    // stamps; then the selection histograms [N x 256]
+    const int64_t fslots = (n_hashes / 4 + N + 1) * ls::kBucketKeys;
+    int rc = grow(c, &X.ws, &X.ws_cap, sizeof(uint64_t) * 2 * (size_t)fslots + sizeof(uint32_t) * 256 * (size_t)N);
+    if (rc) return rc;
+    IndexSmall m = index_small(X.small, N);
+    ls::IndexCommit C;
+    C.N = N;
+    C.R = R;
+    C.epoch = X.epoch + 1;
+    C.n_cu = c->n_cu;
+    C.req_off = req_off;
+    C.req_hashes = req_hashes;
+    C.chosen = chosen;
+    C.off = X.off;
+    C.hash = X.hash;
+    C.stamp = X.stamp;
+    C.entry_of = X.entry_of;
+    C.eidx = m.eidx;
+    C.capacity = m.cap;
+    C.occ = m.occ;
+    C.fbase = m.fbase;
+    C.fkey = static_cast<uint64_t*>(X.ws);
+    C.fstamp = C.fkey + fslots;
+    C.fresh_slots_bound = fslots;
+    C.fcount = m.fcount;
+    C.efresh = m.efresh;
+    C.cand = m.cand;
+    C.off2 = X.off2;
+    C.hash2 = X.hash2;
+    C.stamp2 = X.stamp2;
+    C.nvirt = m.nvirt;
+    C.chunk0 = m.chunk0;
+    // chunks: sum_i ceil(nvirt_i / chunk) <= (listed + set slots + N) / chunk + N
+    C.chunk_bound = (X.list_entries + fslots + N) / ls::kSelChunk + N + 1;
+    C.sel_want = m.want;
+    C.sel_prefix = m.prefix;
+    C.sel_mask = m.mask;
+    C.sel_pos = m.pos;
+    C.sel_active = m.active;
+    C.sel_hist = reinterpret_cast<uint32_t*>(C.fstamp + fslots);
+    {
+        Timed t(c, K_INDEX, s);
+        LS_HIP(c, ls::launch_commit(c->tables, C, s));
+        t.done();
+    }
+    {
+        // the new lists hold each key once per instance, so the build itself
+        // records every slot's list entry and the all-ones key's entry
+        Timed t(c, K_TABLE, s);
+        LS_HIP(c, ls::launch_fill_u64(reinterpret_cast<uint64_t*>(m.eidx), ~0ull, N, s));
+        LS_HIP(c, ls::launch_table_build(c->tables, X.off2, c->seg_off_dev, (int32_t)c->tables_nseg, X.hash2,
+                                         X.list_entries, N, c->tws, c->n_cu, s, X.entry_of, m.eidx));
+        t.done();
+    }
+    std::swap(X.off, X.off2);
+    std::swap(X.hash, X.hash2);
+    std::swap(X.stamp, X.stamp2);
+    std::swap(X.hash_cap, X.hash2_cap);
+    std::swap(X.stamp_cap, X.stamp2_cap);
+    X.epoch += 1;
+    return LS_OK;
+}
+
+int ls_read_cache_state(ls_ctx* c, int32_t n_instances, int64_t* inst_off, uint64_t* hashes, uint64_t* stamps,
+                        int64_t max_entries, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    auto& X = c->idx;
+    if (!X.live) return fail(c, LS_ERR_STATE, "no cache state was loaded under ls_set_cache_capacity");
+    if (n_instances != X.n) return fail(c, LS_ERR_INVALID, "n_instances is %d, the state has %d", n_instances, X.n);
+    if (!inst_off) return fail(c, LS_ERR_INVALID, "inst_off is NULL");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t ob = sizeof(int64_t) * (size_t)(X.n + 1);
+    int rc = stage_reserve(c, ob);
+    if (rc) return rc;
+    LS_HIP(c, hipMemcpyAsync(c->stage, X.off, ob, hipMemcpyDeviceToHost, s));
+    LS_HIP(c, hipStreamSynchronize(s));
+    memcpy(inst_off, c->stage, ob);
+    const int64_t total = inst_off[X.n];
+    if ((hashes || stamps) && max_entries < total)
+        return fail(c, LS_ERR_INVALID, "max_entries is %lld, the lists hold %lld", (long long)max_entries,
+                    (long long)total);
+    if (hashes && total > 0)
+        LS_HIP(c, hipMemcpyAsync(hashes, X.hash, sizeof(uint64_t) * (size_t)total, hipMemcpyDeviceToDevice, s));
+    if (stamps && total > 0)
+        LS_HIP(c, hipMemcpyAsync(stamps, X.stamp, sizeof(uint64_t) * (size_t)total, hipMemcpyDeviceToDevice, s));
+    LS_HIP(c, hipStreamSynchronize(s));
     return LS_OK;
 }
 

@@ -95,10 +95,14 @@ def library():
         lib.ls_train_round.argtypes = [P, i32, i32, f32, P, P, P]
         lib.ls_route_batch.argtypes = [P, ctypes.POINTER(ls_policy), i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
+        lib.ls_set_cache_capacity.argtypes = [P, i32, P]
+        lib.ls_commit_routes.argtypes = [P, i32, i64, P, P, P, P]
+        lib.ls_read_cache_state.argtypes = [P, i32, P, P, P, i64, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
                   lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
-                  lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round):
+                  lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round,
+                  lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -225,6 +229,42 @@ class Context:
         self._check("ls_load_cache_state", rc)
         self.n_instances = N
         return rc
+
+    # -- prefix-index maintenance -----------------------------------------
+    def ls_set_cache_capacity(self, capacity):
+        """capacity: per-instance blocks (host array), or None to turn maintenance off."""
+        if capacity is None:
+            return self._check("ls_set_cache_capacity", self.lib.ls_set_cache_capacity(self.h, 0, None))
+        cap, capp = _host(capacity, np.int64)
+        return self._check("ls_set_cache_capacity", self.lib.ls_set_cache_capacity(self.h, cap.size, capp))
+
+    def ls_commit_routes(self, req_off, req_hashes, chosen, n_hashes=None, stream=None):
+        """Records a routed batch; n_hashes defaults to req_off[-1] (read from the device)."""
+        import torch
+        R = req_off.numel() - 1
+        if n_hashes is None:
+            n_hashes = int(req_off[-1].item()) if R >= 0 else 0
+        op = _dev(req_off, "req_off", (torch.int64,), R + 1)
+        hp = _dev(req_hashes, "req_hashes", (torch.int64, torch.uint64), n_hashes)
+        cp = _dev(chosen, "chosen", (torch.int32,), R)
+        return self._check("ls_commit_routes",
+                           self.lib.ls_commit_routes(self.h, R, int(n_hashes), op, hp, cp, _stream(stream)))
+
+    def ls_read_cache_state(self, stream=None):
+        """(inst_off numpy int64 [N+1], hashes int64 tensor, stamps int64 tensor) of the maintained lists."""
+        import torch
+        N = self.n_instances
+        off = np.zeros(N + 1, np.int64)
+        offp = off.ctypes.data_as(ctypes.c_void_p)
+        self._check("ls_read_cache_state", self.lib.ls_read_cache_state(self.h, N, offp, None, None, 0,
+                                                                         _stream(stream)))
+        total = int(off[-1])
+        h = torch.empty(max(total, 1), dtype=torch.int64, device="cuda")
+        st = torch.empty(max(total, 1), dtype=torch.int64, device="cuda")
+        self._check("ls_read_cache_state",
+                    self.lib.ls_read_cache_state(self.h, N, offp, ctypes.c_void_p(h.data_ptr()),
+                                                 ctypes.c_void_p(st.data_ptr()), h.numel(), _stream(stream)))
+        return off, h[:total], st[:total]
 
     # -- scoring -----------------------------------------------------------
     def ls_score_batch(self, req_off, req_hashes, prompt_len, inst_feat, chosen, min_ttft=None, scores=None,
