@@ -69,11 +69,16 @@ def _open(path):
                                         P]
         lib.lso_train_round.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, i32, i32, P, P, i32, P, P, i32, i32,
                                         f32, P, P]
+        u64 = ctypes.c_uint64
+        lib.lso_update_dropout.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, P, P, f32, dbl, u64, u64, P, P]
+        lib.lso_train_round_dropout.argtypes = [ctypes.c_int, i32, i32, P, P, P, P, i32, i32, i32, P, P, i32, P, P,
+                                                i32, i32, f32, P, dbl, u64, u64, P]
         lib.lso_stamp.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32]
         lib.lso_stamp.restype = ctypes.c_uint64
         lib.lso_commit.argtypes = [i32, P, P, P, P, i32, P, P, P, ctypes.c_uint32, P, P, P]
         for f in (lib.lso_overlap, lib.lso_forward, lib.lso_score, lib.lso_update, lib.lso_route, lib.lso_embed,
-                  lib.lso_buffer_push, lib.lso_train_round, lib.lso_commit):
+                  lib.lso_buffer_push, lib.lso_train_round, lib.lso_commit, lib.lso_update_dropout,
+                  lib.lso_train_round_dropout):
             f.restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
@@ -200,8 +205,9 @@ def score(mode, d, hidden, params, mu, inv_sigma, req_off, req_hashes, prompt_le
     return {"overlap": ov, "scores": sc, "chosen": ch, "min_ttft": mn, "feat": ft}
 
 
-def update(mode, d, hidden, params, mu, inv_sigma, feats, ttft, lr) -> dict:
-    """One SGD step; returns the new params, the gradient and the pre-step loss."""
+def update(mode, d, hidden, params, mu, inv_sigma, feats, ttft, lr, dropout=None) -> dict:
+    """One SGD step; returns the new params, the gradient and the pre-step loss.
+    dropout: None, or (p, seed, step) -- the masks of update call `step`."""
     lib = _load()
     h = _c(hidden, np.int32)
     p = np.array(params, dtype=np.float32, copy=True)
@@ -209,8 +215,14 @@ def update(mode, d, hidden, params, mu, inv_sigma, feats, ttft, lr) -> dict:
     feats = _c(feats, np.float32).reshape(-1, d); ttft = _c(ttft, np.float32)
     grad = np.zeros(p.shape[0], dtype=np.float64)
     loss = np.zeros(1, dtype=np.float64)
-    rc = lib.lso_update(_mode(mode), d, h.shape[0], _ptr(h), _ptr(p), _ptr(mu), _ptr(inv_sigma),
-                        feats.shape[0], _ptr(feats), _ptr(ttft), float(lr), _ptr(grad), _ptr(loss))
+    if dropout is None:
+        rc = lib.lso_update(_mode(mode), d, h.shape[0], _ptr(h), _ptr(p), _ptr(mu), _ptr(inv_sigma),
+                            feats.shape[0], _ptr(feats), _ptr(ttft), float(lr), _ptr(grad), _ptr(loss))
+    else:
+        dp, seed, step = dropout
+        rc = lib.lso_update_dropout(_mode(mode), d, h.shape[0], _ptr(h), _ptr(p), _ptr(mu), _ptr(inv_sigma),
+                                    feats.shape[0], _ptr(feats), _ptr(ttft), float(lr), float(dp),
+                                    ctypes.c_uint64(seed), ctypes.c_uint64(step), _ptr(grad), _ptr(loss))
     assert rc == 0, rc
     return {"params": p, "grad": grad, "loss": float(loss[0])}
 
@@ -313,18 +325,21 @@ def buffer_push(mode, hidden, params, mu, inv_sigma, buf, x, y) -> int:
     return int(adm[0])
 
 
-def train_round(mode, hidden, params, mu, inv_sigma, buf, epochs, batch, lr, perm=None):
-    """One retraining round over FIFO and pool; returns (new params, mean loss of the last epoch)."""
+def train_round(mode, hidden, params, mu, inv_sigma, buf, epochs, batch, lr, perm=None, dropout=None):
+    """One retraining round over FIFO and pool; returns (new params, mean loss of the last epoch).
+    dropout: None, or (p, seed, first step) -- minibatch u of the round is update call first step + u."""
     lib = _load()
     h = _c(hidden, np.int32)
     p = _c(params, np.float32).copy()
     perm_a = None if perm is None else _c(perm, np.int32)
     loss = np.zeros(1, np.float64)
-    rc = lib.lso_train_round(_mode(mode), buf.d, h.shape[0], _ptr(h), _ptr(p), _ptr(_c(mu, np.float32)),
-                             _ptr(_c(inv_sigma, np.float32)), buf.fifo_cap, int(buf.fifo_count[0]),
-                             int(buf.fifo_head[0]), _ptr(buf.fifo_x), _ptr(buf.fifo_y), int(buf.rep_count[0]),
-                             _ptr(buf.rep_x), _ptr(buf.rep_y), int(epochs), int(batch), float(lr), _ptr(perm_a),
-                             _ptr(loss))
+    dp, seed, step0 = dropout if dropout is not None else (0.0, 0, 0)
+    rc = lib.lso_train_round_dropout(_mode(mode), buf.d, h.shape[0], _ptr(h), _ptr(p), _ptr(_c(mu, np.float32)),
+                                     _ptr(_c(inv_sigma, np.float32)), buf.fifo_cap, int(buf.fifo_count[0]),
+                                     int(buf.fifo_head[0]), _ptr(buf.fifo_x), _ptr(buf.fifo_y), int(buf.rep_count[0]),
+                                     _ptr(buf.rep_x), _ptr(buf.rep_y), int(epochs), int(batch), float(lr),
+                                     _ptr(perm_a), float(dp), ctypes.c_uint64(seed), ctypes.c_uint64(step0),
+                                     _ptr(loss))
     assert rc == 0, rc
     return p, float(loss[0])
 

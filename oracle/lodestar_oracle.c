@@ -408,16 +408,43 @@ int lso_score(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, cons
 /* itself summed in the kernel's precision, an fp32 chain in ascending order.  */
 /* grad_out (nullable, double, same packing as params), loss_out (nullable).   */
 /* ------------------------------------------------------------------------- */
-int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
-               const float* mu, const float* inv_sigma, int32_t B, const float* feats, const float* ttft,
-               float lr, double* grad_out, double* loss_out)
+uint64_t lso_splitmix64_mix(uint64_t z);
+
+/* Dropout on the hidden activations while training (Section 4.1 Model         */
+/* architecture: the predictor uses dropout 0.1).  Inverted dropout: a kept     */
+/* unit is scaled by 1/(1-p) (in the kernel's precision, an fp32 multiply by    */
+/* the fp32 value of 1/(1-p), before any bf16 rounding of the next layer's     */
+/* input), a dropped one is 0; the backward pass multiplies the unit's          */
+/* gradient by the same factor.  Unit j of hidden layer l for row b of update   */
+/* call `step` draws the splitmix64 output number c + 1 for seed `seed`, with   */
+/* c = ((step * 4 + l) * 2^24 + b) * 2^10 + j, and is dropped when the draw's   */
+/* top 53 bits are below floor(p * 2^53).                                       */
+static int lso_dropped(uint64_t seed, uint64_t step, int layer, int64_t row, int unit, uint64_t thr53)
+{
+    if (thr53 == 0) return 0;
+    uint64_t c = ((((step * 4u + (uint64_t)layer) << 24) | (uint64_t)row) << 10) | (uint64_t)unit;
+    uint64_t u = lso_splitmix64_mix(seed + (c + 1u) * 0x9e3779b97f4a7c15ull);
+    return (u >> 11) < thr53;
+}
+
+/* One SGD step with dropout rate p in [0, 1) (p = 0: none); rows must be      */
+/* fewer than 2^24, hidden widths at most 2^10, step below 2^36.               */
+int lso_update_dropout(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
+                       const float* mu, const float* inv_sigma, int32_t B, const float* feats, const float* ttft,
+                       float lr, double p, uint64_t seed, uint64_t step, double* grad_out, double* loss_out)
 {
     lso_net net;
     if (net_init(&net, d, n_hidden, hidden, params)) return -1;
     if (B < 1) return -1;
+    if (!(p >= 0.0 && p < 1.0) || B >= (1 << 24)) return -1;
+    for (int l = 0; l < n_hidden; ++l)
+        if (hidden[l] > 1024) return -1;
     int bf = (mode == LSO_BF16);
     int lowp = (mode == LSO_F32 || mode == LSO_BF16);
     int L = net.n_layers;
+    uint64_t thr53 = (uint64_t)ldexp(p, 53);          /* dropped: top 53 bits below this */
+    float scale_f = (float)(1.0 / (1.0 - p));         /* kernel precision */
+    double scale_d = 1.0 / (1.0 - p);                 /* the definition */
     int64_t P = lso_param_count(d, n_hidden, hidden);
     double* grad = (double*)calloc((size_t)P, sizeof(double));
     int W = net.max_width;
@@ -466,6 +493,8 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
                 z[j] = acc;
                 if (l + 1 < L) {
                     double h = acc > 0.0 ? acc : 0.0;
+                    if (lso_dropped(seed, step, l, b, j, thr53)) h = 0.0;
+                    else if (thr53) h = lowp ? (double)((float)h * scale_f) : h * scale_d;
                     an[j] = bf ? (double)lso_bf16_round((float)h) : h;
                 }
             }
@@ -499,6 +528,8 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
                     for (int j = 0; j < O; ++j) s += Wq[net.W_off[l] + (int64_t)j * K + k] * delta[j];
                 }
                 double dk = zp[k] > 0.0 ? s : 0.0;
+                if (lso_dropped(seed, step, l - 1, b, k, thr53)) dk = 0.0;
+                else if (thr53) dk = bf ? (double)((float)dk * scale_f) : dk * (lowp ? (double)scale_f : scale_d);
                 dnext[k] = bf ? (double)lso_bf16_round((float)dk) : dk;
             }
             memcpy(delta, dnext, sizeof(double) * (size_t)K);
@@ -511,6 +542,14 @@ int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, flo
     }
     free(grad); free(act); free(pre); free(delta); free(dnext); free(Wq);
     return 0;
+}
+
+int lso_update(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
+               const float* mu, const float* inv_sigma, int32_t B, const float* feats, const float* ttft,
+               float lr, double* grad_out, double* loss_out)
+{
+    return lso_update_dropout(mode, d, n_hidden, hidden, params, mu, inv_sigma, B, feats, ttft, lr, 0.0, 0, 0,
+                              grad_out, loss_out);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -887,12 +926,13 @@ int lso_buffer_push(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden
 /* in minibatches of `batch` (the last one may be shorter), one SGD step of   */
 /* lso_update each.  loss_out (nullable) gets the mean minibatch loss of the  */
 /* last epoch.                                                                 */
-int lso_train_round(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params, const float* mu,
-                    const float* inv_sigma, int32_t fifo_cap, int32_t fifo_count, int32_t fifo_head,
-                    const float* fifo_x, const float* fifo_y, int32_t rep_count, const float* rep_x,
-                    const float* rep_y, int32_t epochs, int32_t batch, float lr, const int32_t* perm,
-                    double* loss_out)
+int lso_train_round_dropout(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params,
+                            const float* mu, const float* inv_sigma, int32_t fifo_cap, int32_t fifo_count,
+                            int32_t fifo_head, const float* fifo_x, const float* fifo_y, int32_t rep_count,
+                            const float* rep_x, const float* rep_y, int32_t epochs, int32_t batch, float lr,
+                            const int32_t* perm, double p, uint64_t seed, uint64_t step0, double* loss_out)
 {
+    uint64_t step = step0;                       /* each minibatch is one update call */
     int32_t n = fifo_count + rep_count;
     if (n < 1 || batch < 1 || epochs < 0) return -1;
     float* X = (float*)malloc(sizeof(float) * (size_t)n * d);
@@ -920,7 +960,8 @@ int lso_train_round(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden
                 by[u] = Y[k];
             }
             double loss;
-            int rc = lso_update(mode, d, n_hidden, hidden, params, mu, inv_sigma, m, bx, by, lr, NULL, &loss);
+            int rc = lso_update_dropout(mode, d, n_hidden, hidden, params, mu, inv_sigma, m, bx, by, lr, p, seed,
+                                        step++, NULL, &loss);
             if (rc) { free(X); free(Y); free(bx); free(by); return rc; }
             lsum += loss;
             ++nb;
@@ -1029,4 +1070,15 @@ int lso_commit(int32_t N, const int64_t* in_off, const uint64_t* in_hash, const 
         free(A);
     }
     return 0;
+}
+
+int lso_train_round(int mode, int32_t d, int32_t n_hidden, const int32_t* hidden, float* params, const float* mu,
+                    const float* inv_sigma, int32_t fifo_cap, int32_t fifo_count, int32_t fifo_head,
+                    const float* fifo_x, const float* fifo_y, int32_t rep_count, const float* rep_x,
+                    const float* rep_y, int32_t epochs, int32_t batch, float lr, const int32_t* perm,
+                    double* loss_out)
+{
+    return lso_train_round_dropout(mode, d, n_hidden, hidden, params, mu, inv_sigma, fifo_cap, fifo_count, fifo_head,
+                                   fifo_x, fifo_y, rep_count, rep_x, rep_y, epochs, batch, lr, perm, 0.0, 0, 0,
+                                   loss_out);
 }

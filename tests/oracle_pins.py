@@ -845,4 +845,101 @@ def pin_commit_keeps_prefixes():
         assert int(off[-1]) > 0
 
 
+# ---------------------------------------------------------------------------
+# dropout while training (Section 4.1: the predictor uses dropout 0.1)
+# ---------------------------------------------------------------------------
+def _one_unit_net():
+    """d = 6 inputs, one hidden unit, head: z = 0.5 x0 + 0.25, t = 1 + 2 relu(z)."""
+    W1 = np.zeros((1, 6)); W1[0, 0] = 0.5
+    return _pack([(W1, [0.25]), ([[2.0]], [1.0])])
+
+
+def pin_dropout_closed_form():
+    """Inverted dropout on a single hidden unit with x0 = 1 (z = 0.75): a kept unit is
+    scaled by 1/(1-p), so t = 1 + 2 * 0.75 / (1-p); a dropped one gives t = 1.  The
+    observed dropped fraction matches p (binomial bound), and masks differ between
+    the rows of one call."""
+    params = _one_unit_net()
+    mu, isg = np.zeros(6, np.float32), np.ones(6, np.float32)
+    x = np.zeros((1, 6), np.float32); x[0, 0] = 1.0
+    for mode in ("f64", "fp32", "bf16"):
+        vals = []
+        for step in range(400):
+            out = oracle.update(mode, 6, [1], params, mu, isg, x, [0.0], 0.0, dropout=(0.5, 99, step))
+            vals.append(out["loss"])                      # y = 0: loss = t^2
+        vals = np.array(vals)
+        assert set(np.unique(vals)) == {1.0, 16.0}, (mode, np.unique(vals))
+        assert abs((vals == 1.0).mean() - 0.5) < 5 * 0.025, mode
+    # p = 0.1: the fp32 scale is the fp32 value of 1/0.9
+    s = np.float32(1.0 / 0.9)
+    kept_t = np.float32(1.0) + np.float32(2.0) * (np.float32(0.75) * s)
+    vals = np.array([oracle.update("fp32", 6, [1], params, mu, isg, x, [0.0], 0.0, dropout=(0.1, 7, k))["loss"]
+                     for k in range(3000)])
+    assert abs((vals == 1.0).mean() - 0.1) < 5 * np.sqrt(0.09 / 3000)
+    assert np.all((vals == 1.0) | (vals == float(kept_t) ** 2))
+    # p = 0 is no dropout at all
+    plain = oracle.update("fp32", 6, [1], params, mu, isg, x, [0.0], 0.0)
+    assert oracle.update("fp32", 6, [1], params, mu, isg, x, [0.0], 0.0, dropout=(0.0, 5, 3))["loss"] == plain["loss"]
+    # 64 identical rows in one call: some kept, some dropped (the row is part of the draw)
+    X = np.repeat(x, 64, axis=0)
+    losses = [oracle.update("f64", 6, [1], params, mu, isg, X, np.zeros(64), 0.0, dropout=(0.5, 3, k))["loss"]
+              for k in range(4)]
+    assert all(1.0 < l < 16.0 for l in losses), losses
+
+
+def pin_dropout_gradient_fd():
+    """The gradient with dropout is the gradient of the masked network's loss: central
+    finite differences of the double-precision loss with the same masks (same seed
+    and step), over two hidden layers."""
+    rng = np.random.default_rng(12)
+    d, hidden, B = 7, [5, 4], 6
+    n = oracle.param_count(d, hidden)
+    params = (rng.standard_normal(n) * 0.5).astype(np.float32)
+    mu = rng.standard_normal(d).astype(np.float32) * 0.1
+    isg = (1.0 + rng.random(d)).astype(np.float32)
+    X = rng.standard_normal((B, d)).astype(np.float32)
+    Y = rng.standard_normal(B).astype(np.float32)
+    drop = (0.3, 1234, 17)
+    g = oracle.update("f64", d, hidden, params, mu, isg, X, Y, 0.0, dropout=drop)["grad"]
+    assert np.count_nonzero(g) > 0
+    h = 1e-3
+    worst = 0.0
+    for t in rng.choice(n, 24, replace=False):
+        pp, pm = params.astype(np.float64).copy(), params.astype(np.float64).copy()
+        pp[t] += h; pm[t] -= h
+        lp = oracle.update("f64", d, hidden, pp.astype(np.float32), mu, isg, X, Y, 0.0, dropout=drop)["loss"]
+        lm = oracle.update("f64", d, hidden, pm.astype(np.float32), mu, isg, X, Y, 0.0, dropout=drop)["loss"]
+        # the float32 parameters hold pp / pm exactly only up to rounding: use the rounded step
+        step = float(np.float32(pp[t])) - float(np.float32(pm[t]))
+        fd = (lp - lm) / step
+        worst = max(worst, abs(fd - g[t]) / max(1e-3, abs(g[t])))
+    assert worst < 2e-3, worst
+
+
+def pin_train_round_dropout_is_update_sequence():
+    """A retraining round with dropout is the sequence of dropout updates over its
+    minibatches, minibatch u drawing the masks of update call first_step + u."""
+    from paper_2606_00946_amd import synth
+    w = synth.generate("tiny")
+    cfg = w.cfg
+    buf = oracle.Buffer(cfg.d, 10, 4)
+    x, y = w.upd_feats[:20], w.upd_ttft[:20]
+    oracle.buffer_push("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, x, y)
+    fx, fy = buf.fifo_rows(); rx, ry = buf.replay_rows()
+    X = np.concatenate([fx, rx]); Y = np.concatenate([fy, ry])
+    n = X.shape[0]
+    got, _ = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 2, 4, 0.05,
+                                dropout=(0.2, 55, 100))
+    p = w.params.copy()
+    step = 100
+    for e in range(2):
+        for s0 in range(0, n, 4):
+            p = oracle.update("fp32", cfg.d, cfg.hidden, p, w.mu, w.inv_sigma, X[s0:s0 + 4], Y[s0:s0 + 4], 0.05,
+                              dropout=(0.2, 55, step))["params"]
+            step += 1
+    np.testing.assert_array_equal(got, p)
+    plain, _ = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 2, 4, 0.05)
+    assert not np.array_equal(got, plain)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]

@@ -101,6 +101,15 @@ MUTANTS = [
      "int64_t keep = u < capacity[i] ? u : capacity[i] - 1;"),
     ("commit_no_dedup", "if (u == 0 || A[u - 1].h != A[t].h) A[u++] = A[t];", "A[u++] = A[t];"),
     ("commit_skips_first_request", "if (chosen[r] != i) continue;", "if (chosen[r] != i || r == 0) continue;"),
+    ("dropout_keeps_below", "    return (u >> 11) < thr53;", "    return (u >> 11) >= thr53;"),
+    ("dropout_no_scale", "                    else if (thr53) h = lowp ? (double)((float)h * scale_f) : h * scale_d;\n", ""),
+    ("dropout_backward_unmasked", "if (lso_dropped(seed, step, l - 1, b, k, thr53)) dk = 0.0;", "if (0) dk = 0.0;"),
+    ("dropout_backward_wrong_layer", "if (lso_dropped(seed, step, l - 1, b, k, thr53)) dk = 0.0;",
+     "if (lso_dropped(seed, step, l, b, k, thr53)) dk = 0.0;"),
+    ("dropout_row_ignored", "    uint64_t c = ((((step * 4u + (uint64_t)layer) << 24) | (uint64_t)row) << 10) | (uint64_t)unit;",
+     "    uint64_t c = ((((step * 4u + (uint64_t)layer) << 24) | (uint64_t)0 * row) << 10) | (uint64_t)unit;"),
+    ("dropout_round_same_step", "lr, p, seed,\n                                        step++, NULL, &loss);",
+     "lr, p, seed,\n                                        step, NULL, &loss);"),
 ]
 
 _RUNNER = r"""
