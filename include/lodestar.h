@@ -58,7 +58,11 @@ typedef struct ls_ctx ls_ctx;
  *              [ instance state (d - 5 columns) | L, n | l, kappa, u ]:
  *              L = prompt tokens, n = hashed blocks, l = overlap in blocks,
  *              kappa = block_tokens * l / L (0 when L = 0), u = L - block_tokens * l.
- *   n_hidden   hidden layers (this build: 2).
+ *   n_hidden   hidden layers, 1..3 (Section 4.1 uses 3 x 128; the evaluated
+ *              configurations here use 2).  Two-layer models are scored by
+ *              fused kernels (bf16 ones on the matrix cores); other depths by a
+ *              layer-by-layer forward over chunks of pair rows, with the same
+ *              arithmetic order (bias first, inputs ascending).
  *   hidden     widths, each 1..512.
  *   block_tokens tokens per hashed KV block (16 in the evaluated engines).
  *   dtype      LS_FP32 or LS_BF16.
@@ -234,6 +238,22 @@ int ls_set_prefix_closed(ls_ctx* ctx, int enable);
  */
 int ls_update(ls_ctx* ctx, int32_t B, const float* feats, const float* ttft, float lr,
               float* loss_out, float* grad_out, void* stream);
+
+/*
+ * Dropout while training (Section 4.1: the predictor is trained with dropout
+ * 0.1): from the next ls_update / ls_train_round on, inverted dropout on every
+ * hidden layer's activations, rate p in [0, 1) (0 turns it off), scoring
+ * unaffected.  Update calls are counted from 0 at this call (each minibatch of
+ * ls_train_round is one call).  In call s, unit j of hidden layer l for row b
+ * of that call's batch draws the splitmix64 output number c + 1 for `seed`,
+ *     c = ((s * 4 + l) * 2^24 + b) * 2^10 + j,
+ * and is dropped when the draw's top 53 bits are below floor(p * 2^53).  A kept
+ * unit's activation is multiplied by the fp32 value of 1 / (1 - p) (after the
+ * ReLU, before any bf16 rounding of the next layer's input); its gradient gets
+ * the same factor, a dropped unit's is 0.  Requires batches below 2^24 rows
+ * (LS_ERR_INVALID from ls_update) and hidden widths up to 1024.
+ */
+int ls_set_dropout(ls_ctx* ctx, float p, uint64_t seed);
 
 /*
  * Routing policy around the reward model.

@@ -60,10 +60,54 @@ __global__ void refresh_compute_kernel(CopyArgs a, const float* __restrict__ mas
     comp[t] = (weight && a.bf16) ? bf16_rne(v) : v;
 }
 
+// Other depths: every layer as W_l^T [in x out] then b_l, in layer order.
+struct CopyLayers {
+    int L;
+    int in[4], out[4];
+    int64_t m_w[4], m_b[4], c_wt[4], c_bl[4];
+    int64_t n_compute;
+    bool bf16;
+};
+
+__global__ void refresh_layers_kernel(CopyLayers a, const float* __restrict__ master, float* __restrict__ comp) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= a.n_compute) return;
+    int l = 0;
+    while (l < a.L && t >= a.c_wt[l + 1]) ++l;          // the layer whose segment holds t
+    float v;
+    bool weight;
+    if (t < a.c_bl[l]) {                                // W_l^T[k][j] = W_l[j][k]
+        const int64_t e = t - a.c_wt[l];
+        const int64_t k = e / a.out[l], j = e - k * a.out[l];
+        v = master[a.m_w[l] + j * a.in[l] + k];
+        weight = true;
+    } else {
+        v = master[a.m_b[l] + (t - a.c_bl[l])];
+        weight = false;
+    }
+    comp[t] = (weight && a.bf16) ? bf16_rne(v) : v;
+}
+
 hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, float* compute, hipStream_t s) {
+    const int64_t grid = (m.n_compute + 255) / 256;
+    if (m.L != 2) {
+        CopyLayers a{};
+        a.L = m.L;
+        for (int l = 0; l <= m.L; ++l) {
+            a.in[l] = m.in_of(l);
+            a.out[l] = m.out_of(l);
+            a.m_w[l] = m.m_w[l];
+            a.m_b[l] = m.m_b[l];
+            a.c_wt[l] = m.c_wt[l];
+            a.c_bl[l] = m.c_bl[l];
+        }
+        a.n_compute = m.n_compute;
+        a.bf16 = m.bf16;
+        hipLaunchKernelGGL(refresh_layers_kernel, dim3((uint32_t)grid), dim3(256), 0, s, a, master, compute);
+        return hipGetLastError();
+    }
     CopyArgs a{m.d, m.h1, m.h2, m.m_w1, m.m_b1, m.m_w2, m.m_b2, m.m_w3, m.m_b3,
                m.c_w1, m.c_b1, m.c_w2t, m.c_b2, m.c_w3, m.c_b3, m.c_w1t, m.n_compute, m.bf16};
-    int64_t grid = (m.n_compute + 255) / 256;
     hipLaunchKernelGGL(refresh_compute_kernel, dim3((uint32_t)grid), dim3(256), 0, s, a, master, compute);
     return hipGetLastError();
 }

@@ -314,7 +314,7 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
 }
 
 bool mfma_supported(const ModelDims& m) {
-    return m.bf16 && (m.d == 16 || m.d == 32 || m.d == 48 || m.d == 64) &&
+    return m.bf16 && m.L == 2 && (m.d == 16 || m.d == 32 || m.d == 48 || m.d == 64) &&
            (m.h1 == 64 || m.h1 == 128 || m.h1 == 256) && m.h1 == m.h2;
 }
 

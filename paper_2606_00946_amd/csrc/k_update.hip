@@ -11,7 +11,7 @@
 // layer inputs, each layer's output gradient) is a bf16 value; sums are fp32.
 #include <algorithm>
 
-#include "ls_internal.h"
+#include "k_policy.h"
 
 namespace ls {
 
@@ -24,13 +24,27 @@ __device__ __forceinline__ float q_bf16(float x) {
 
 __device__ __forceinline__ float relu_u(float z) { return z > 0.0f ? z : 0.0f; }
 
+// Dropout of unit j of hidden layer `layer` for row b (see DropArgs).
+__device__ __forceinline__ bool drop_unit(const DropArgs& D, int layer, int64_t b, int j) {
+    const uint64_t c = ((((D.step * 4u + (uint64_t)layer) << 24) | (uint64_t)b) << 10) | (uint64_t)j;
+    return (mix64(D.seed + (c + 1u) * 0x9e3779b97f4a7c15ull) >> 11) < D.thr53;
+}
+
+// A hidden activation after dropout (before any bf16 rounding), and likewise a
+// hidden unit's gradient: 0 if dropped, times the scale if kept.
+__device__ __forceinline__ float apply_drop(const DropArgs& D, int layer, int64_t b, int j, float v) {
+    if (D.thr53 == 0) return v;
+    return drop_unit(D, layer, b, j) ? 0.0f : __fmul_rn(v, D.scale);
+}
+
 static inline uint32_t blocks_for(int64_t n, int block) { return (uint32_t)((n + block - 1) / block); }
 
 // ---------------------------------------------------------------------------
 // workspace layout
 // ---------------------------------------------------------------------------
 struct UpdWs {
-    float *xn, *z1, *a1, *z2, *a2, *t, *g, *d2, *d1, *grad, *part, *loss_part;
+    float *xn, *t, *g, *grad, *part, *loss_part;
+    float *z[3], *a[3], *dl[3];      // per hidden layer: pre-activation, activation, dL/dz
     int64_t bytes;
     int S;              // split-K chunks
     int64_t chunk;      // samples per chunk (multiple of 16)
@@ -72,21 +86,32 @@ static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
     w.S = S;
     w.chunk = chunk;
     w.loss_blocks = (int)blocks_for(B, 256);
-    int64_t maxmn = std::max<int64_t>({(int64_t)m.h2 * m.h1, (int64_t)m.h1 * m.d, (int64_t)m.h2});
-    // the matrix-core weight gradients keep one more column (the bias) per partial
-    const int64_t mfma_floats = std::max<int64_t>({(int64_t)wgrad_plan(B, m.h2).S * m.h2 * (m.h1 + 1),
-                                                   (int64_t)wgrad_plan(B, m.h1).S * m.h1 * (m.d + 1),
-                                                   (int64_t)wgrad_plan(B, 1).S * (m.h2 + 1)});
-    const int64_t part_floats = std::max<int64_t>((int64_t)S * maxmn, mfma_floats);
-    int64_t sizes[] = {(int64_t)m.d * B, (int64_t)m.h1 * B, (int64_t)m.h1 * B, (int64_t)m.h2 * B,
-                       (int64_t)m.h2 * B, (int64_t)B, (int64_t)B, (int64_t)m.h2 * B, (int64_t)m.h1 * B,
-                       m.n_params, part_floats, (int64_t)w.loss_blocks};
-    float** slots[] = {&w.xn, &w.z1, &w.a1, &w.z2, &w.a2, &w.t, &w.g, &w.d2, &w.d1, &w.grad, &w.part, &w.loss_part};
-    int64_t off = 0;
-    for (int k = 0; k < 12; ++k) {
-        *slots[k] = base ? reinterpret_cast<float*>(base) + off : nullptr;
-        off += align_floats(sizes[k]);
+    int64_t maxmn = 0, mfma_floats = 0;
+    for (int l = 0; l <= m.L; ++l) {
+        const int64_t O = m.out_of(l), K = m.in_of(l);
+        maxmn = std::max(maxmn, O * K);
+        // the matrix-core weight gradients keep one more column (the bias) per partial
+        mfma_floats = std::max(mfma_floats, (int64_t)wgrad_plan(B, (int)O).S * O * (K + 1));
     }
+    const int64_t part_floats = std::max<int64_t>((int64_t)S * maxmn, mfma_floats);
+    int64_t off = 0;
+    auto take = [&](int64_t n) -> float* {
+        float* p = base ? reinterpret_cast<float*>(base) + off : nullptr;
+        off += align_floats(n);
+        return p;
+    };
+    w.xn = take((int64_t)m.d * B);
+    for (int l = 0; l < 3; ++l) {
+        const int64_t n = l < m.L ? (int64_t)m.h[l] * B : 0;
+        w.z[l] = l < m.L ? take(n) : nullptr;
+        w.a[l] = l < m.L ? take(n) : nullptr;
+        w.dl[l] = l < m.L ? take(n) : nullptr;
+    }
+    w.t = take(B);
+    w.g = take(B);
+    w.grad = take(m.n_params);
+    w.part = take(part_floats);
+    w.loss_part = take(w.loss_blocks);
     w.bytes = off * (int64_t)sizeof(float);
     return w;
 }
@@ -113,7 +138,7 @@ template <bool BF, bool RELU, int U>
 __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const float* __restrict__ wt,
                                           const float* __restrict__ bias, float* __restrict__ z,
                                           float* __restrict__ a, int32_t B, int K, int O, int jb, int64_t b,
-                                          bool valid) {
+                                          bool valid, const DropArgs& D, int layer) {
     float acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = bias[jb + u];
@@ -140,7 +165,7 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
     for (int u = 0; u < U; ++u) {
         z[(int64_t)(jb + u) * B + b] = acc[u];
         if (RELU) {
-            float h = relu_u(acc[u]);
+            const float h = apply_drop(D, layer, b, jb + u, relu_u(acc[u]));
             a[(int64_t)(jb + u) * B + b] = BF ? q_bf16(h) : h;
         }
     }
@@ -152,18 +177,19 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
 template <bool BF, bool RELU>
 __global__ __launch_bounds__(256) void layer_fwd_kernel(const float* __restrict__ in, const float* __restrict__ wt,
                                                         const float* __restrict__ bias, float* __restrict__ z,
-                                                        float* __restrict__ a, int32_t B, int K, int O) {
+                                                        float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
+                                                        int layer) {
     int64_t bt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     bool valid = bt < B;
     int64_t b = valid ? bt : 0;
     int jb = blockIdx.y * 32;
     const int rem = O - jb;
-    if (rem >= 32) { fwd_units<BF, RELU, 32>(in, wt, bias, z, a, B, K, O, jb, b, valid); return; }
-    if (rem & 16) { fwd_units<BF, RELU, 16>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 16; }
-    if (rem & 8) { fwd_units<BF, RELU, 8>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 8; }
-    if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 4; }
-    if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 2; }
-    if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid); jb += 1; }
+    if (rem >= 32) { fwd_units<BF, RELU, 32>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); return; }
+    if (rem & 16) { fwd_units<BF, RELU, 16>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 16; }
+    if (rem & 8) { fwd_units<BF, RELU, 8>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 8; }
+    if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 4; }
+    if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 2; }
+    if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 1; }
 }
 
 // The same chains with the weights of the workgroup's 32 output units staged
@@ -186,7 +212,8 @@ template <bool BF, int MODE, int U>
 __device__ __forceinline__ void dense_units(const float* __restrict__ in, const float* __restrict__ wl,
                                             const float* __restrict__ bias, const float* __restrict__ zmask,
                                             float* __restrict__ z, float* __restrict__ a, int32_t B, int K, int o0,
-                                            int uoff, const int64_t (&b)[kDenseSpl], const bool (&valid)[kDenseSpl]) {
+                                            int uoff, const int64_t (&b)[kDenseSpl], const bool (&valid)[kDenseSpl],
+                                            const DropArgs& D, int layer) {
     constexpr int P = kDenseSpl;
     float acc[P][U];
 #pragma unroll
@@ -230,12 +257,12 @@ __device__ __forceinline__ void dense_units(const float* __restrict__ in, const 
             const int64_t e = (int64_t)(o0 + u) * B + b[j];
             if (MODE == kFwdRelu) {
                 z[e] = acc[j][u];
-                const float h = relu_u(acc[j][u]);
+                const float h = apply_drop(D, layer, b[j], o0 + u, relu_u(acc[j][u]));
                 a[e] = BF ? q_bf16(h) : h;
             } else if (MODE == kFwdHead) {
                 z[e] = acc[j][u];
             } else {
-                const float v = zmask[e] > 0.0f ? acc[j][u] : 0.0f;
+                const float v = apply_drop(D, layer, b[j], o0 + u, zmask[e] > 0.0f ? acc[j][u] : 0.0f);
                 z[e] = BF ? q_bf16(v) : v;
             }
         }
@@ -246,7 +273,8 @@ template <bool BF, int MODE>
 __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict__ in, const float* __restrict__ wt,
                                                          const float* __restrict__ bias,
                                                          const float* __restrict__ zmask, float* __restrict__ z,
-                                                         float* __restrict__ a, int32_t B, int K, int O) {
+                                                         float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
+                                                         int layer) {
     __shared__ __align__(16) float wl[kDenseMaxK * 32];
     const int jb = blockIdx.y * 32;
     const int nu = O - jb < 32 ? O - jb : 32;
@@ -269,15 +297,15 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
         b[j] = valid[j] ? bt : 0;
     }
     if (nu == 32) {
-        dense_units<BF, MODE, 32>(in, wl, bias, zmask, z, a, B, K, jb, 0, b, valid);
+        dense_units<BF, MODE, 32>(in, wl, bias, zmask, z, a, B, K, jb, 0, b, valid, D, layer);
         return;
     }
     int uo = 0;
-    if (nu & 16) { dense_units<BF, MODE, 16>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 16; }
-    if (nu & 8) { dense_units<BF, MODE, 8>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 8; }
-    if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 4; }
-    if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 2; }
-    if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid); uo += 1; }
+    if (nu & 16) { dense_units<BF, MODE, 16>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 16; }
+    if (nu & 8) { dense_units<BF, MODE, 8>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 8; }
+    if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 4; }
+    if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 2; }
+    if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 1; }
 }
 
 // ---------------------------------------------------------------------------
@@ -318,15 +346,16 @@ __global__ void loss_final_kernel(const float* __restrict__ loss_part, int nblk,
     if (threadIdx.x == 0) out[0] = red[0] / (float)B;
 }
 
-// dL/dz of the last hidden layer: g_b * w3[j] where z2 > 0
+// dL/dz of the last hidden layer: g_b * w[j] where z > 0 (then dropout's factor)
 template <bool BF>
-__global__ void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w3,
-                                  const float* __restrict__ z2, float* __restrict__ d2, int32_t B, int h2) {
+__global__ void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
+                                  const float* __restrict__ z, float* __restrict__ dl, int32_t B, int hl, DropArgs D,
+                                  int layer) {
     int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)h2 * B) return;
+    if (t >= (int64_t)hl * B) return;
     int64_t j = t / B, b = t - j * B;
-    float v = z2[t] > 0.0f ? g[b] * w3[j] : 0.0f;
-    d2[t] = BF ? q_bf16(v) : v;
+    const float v = apply_drop(D, layer, b, (int)j, z[t] > 0.0f ? g[b] * w[j] : 0.0f);
+    dl[t] = BF ? q_bf16(v) : v;
 }
 
 // ---------------------------------------------------------------------------
@@ -652,7 +681,7 @@ __global__ __launch_bounds__(256) void rowsum_kernel(const float* __restrict__ X
 template <bool BF>
 __global__ __launch_bounds__(256) void backprop_hidden_kernel(const float* __restrict__ W, const float* __restrict__ D2,
                                                               const float* __restrict__ Z1, float* __restrict__ D1,
-                                                              int M, int K, int32_t B) {
+                                                              int M, int K, int32_t B, DropArgs D, int layer) {
     __shared__ float As[16][64 + 4];
     __shared__ float Bs[16][64 + 4];
     const int tid = threadIdx.x;
@@ -695,7 +724,7 @@ __global__ __launch_bounds__(256) void backprop_hidden_kernel(const float* __res
             int64_t n = n0 + tx * 4 + j;
             if (n >= B) continue;
             int64_t e = (int64_t)m * B + n;
-            float v = Z1[e] > 0.0f ? acc[i][j] : 0.0f;
+            const float v = apply_drop(D, layer, n, m, Z1[e] > 0.0f ? acc[i][j] : 0.0f);
             D1[e] = BF ? q_bf16(v) : v;
         }
     }
@@ -720,104 +749,183 @@ static hipError_t weight_grad(const float* A, const float* Bt, int M, int N, int
 }
 
 // Forward pass of B raw rows in the kernel's precision (the canonical chains),
-// keeping every layer feature-major: xn [d][B], z1/a1 [h1][B], z2/a2 [h2][B], t [B].
+// keeping every layer feature-major: xn [d][B], z[l] / a[l] [h_l][B], t [B].
 template <bool BF>
 static void forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
-                         const float* feats, float* xn, float* z1, float* a1, float* z2, float* a2, float* t,
-                         hipStream_t s) {
+                         const float* feats, float* xn, float* const* z, float* const* a, float* t,
+                         const DropArgs& D, hipStream_t s) {
     const int64_t nB = B;
     hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, xn, B,
                        m.d);
     const uint32_t sb = blocks_for(nB, 256);
     const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
-    const bool lds_w = m.d <= kDenseMaxK && m.h1 <= kDenseMaxK && m.h2 <= kDenseMaxK;
-    if (lds_w) {
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, xn,
-                           compute + m.c_w1t, compute + m.c_b1, nullptr, z1, a1, B, m.d, m.h1);
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (m.h2 + 31) / 32), dim3(256), 0, s, a1,
-                           compute + m.c_w2t, compute + m.c_b2, nullptr, z2, a2, B, m.h1, m.h2);
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, a2, compute + m.c_w3,
-                           compute + m.c_b3, nullptr, t, nullptr, B, m.h2, 1);
-    } else {
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h1 + 31) / 32), dim3(256), 0, s, xn,
-                           compute + m.c_w1t, compute + m.c_b1, z1, a1, B, m.d, m.h1);
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (m.h2 + 31) / 32), dim3(256), 0, s, a1,
-                           compute + m.c_w2t, compute + m.c_b2, z2, a2, B, m.h1, m.h2);
-        hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, a2, compute + m.c_w3,
-                           compute + m.c_b3, t, nullptr, B, m.h2, 1);
+    bool lds_w = m.d <= kDenseMaxK;
+    for (int l = 0; l < m.L; ++l) lds_w = lds_w && m.h[l] <= kDenseMaxK;
+    for (int l = 0; l < m.L; ++l) {
+        const float* in = l == 0 ? xn : a[l - 1];
+        const int K = m.in_of(l), O = m.h[l];
+        if (lds_w)
+            hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + 31) / 32), dim3(256), 0, s, in,
+                               compute + m.c_wt[l], compute + m.c_bl[l], nullptr, z[l], a[l], B, K, O, D, l);
+        else
+            hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (O + 31) / 32), dim3(256), 0, s, in,
+                               compute + m.c_wt[l], compute + m.c_bl[l], z[l], a[l], B, K, O, D, l);
     }
+    const float* last = a[m.L - 1];
+    if (lds_w)
+        hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, last,
+                           compute + m.c_wt[m.L], compute + m.c_bl[m.L], nullptr, t, nullptr, B, m.hl, 1, D, m.L);
+    else
+        hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, last, compute + m.c_wt[m.L],
+                           compute + m.c_bl[m.L], t, nullptr, B, m.hl, 1, D, m.L);
 }
 
 int64_t forward_rows_floats(const ModelDims& m, int32_t B) {
-    return (int64_t)B * (m.d + 2 * m.h1 + 2 * m.h2 + 1) + 6 * 64;
+    int64_t n = (int64_t)B * (m.d + 1) + 64 * (2 * m.L + 2);
+    for (int l = 0; l < m.L; ++l) n += 2 * (int64_t)B * m.h[l];
+    return n;
+}
+
+// Carves xn, z[l], a[l] and t out of ws (forward_rows_floats floats).
+static float* carve_rows(const ModelDims& m, int32_t B, float* ws, float** xn, float** z, float** a) {
+    auto take = [&](int64_t n) { float* p = ws; ws += (n + 63) & ~int64_t(63); return p; };
+    *xn = take((int64_t)m.d * B);
+    for (int l = 0; l < m.L; ++l) {
+        z[l] = take((int64_t)m.h[l] * B);
+        a[l] = take((int64_t)m.h[l] * B);
+    }
+    return take(B);
 }
 
 hipError_t launch_forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
-                               const float* feats, float* ws, float** a2_out, float** t_out, hipStream_t s) {
+                               const float* feats, float* ws, float** alast_out, float** t_out, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    auto take = [&](int64_t n) { float* p = ws; ws += (n + 63) & ~int64_t(63); return p; };
-    float* xn = take((int64_t)m.d * B);
-    float* z1 = take((int64_t)m.h1 * B);
-    float* a1 = take((int64_t)m.h1 * B);
-    float* z2 = take((int64_t)m.h2 * B);
-    float* a2 = take((int64_t)m.h2 * B);
-    float* t = take(B);
-    if (m.bf16) forward_rows<true>(m, compute, mu, isig, B, feats, xn, z1, a1, z2, a2, t, s);
-    else forward_rows<false>(m, compute, mu, isig, B, feats, xn, z1, a1, z2, a2, t, s);
-    *a2_out = a2;
+    float *xn, *z[3] = {}, *a[3] = {};
+    float* t = carve_rows(m, B, ws, &xn, z, a);
+    const DropArgs none{};
+    if (m.bf16) forward_rows<true>(m, compute, mu, isig, B, feats, xn, z, a, t, none, s);
+    else forward_rows<false>(m, compute, mu, isig, B, feats, xn, z, a, t, none, s);
+    *alast_out = a[m.L - 1];
     *t_out = t;
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// scores of every pair for models other than two hidden layers
+// ---------------------------------------------------------------------------
+// The pairs' raw feature rows [instance columns | L, n, l, kappa, u], a chunk
+// at a time, through the same canonical forward (bias first, inputs in
+// ascending order); the two-layer models have fused scorers of their own.
+constexpr int64_t kGenericChunk = 1 << 16;
+
+__global__ void pair_rows_kernel(int64_t p0, int64_t P, int32_t N, int d, int d_inst, int block_tokens,
+                                 const int64_t* __restrict__ req_off, const int32_t* __restrict__ prompt_len,
+                                 const int32_t* __restrict__ overlap, const float* __restrict__ inst_feat,
+                                 float* __restrict__ rows) {
+    const int64_t total = P * d;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+        const int64_t q = t / d;
+        const int c = (int)(t - q * d);
+        const int64_t p = p0 + q;
+        const int64_t r = p / N;
+        const int32_t i = (int32_t)(p - r * N);
+        float v;
+        if (c < d_inst) {
+            v = inst_feat[(int64_t)i * d_inst + c];
+        } else {
+            float x[5];
+            derived_columns(prompt_len[r], req_off[r + 1] - req_off[r], overlap[p], block_tokens, x);
+            v = x[c - d_inst];
+        }
+        rows[t] = v;
+    }
+}
+
+int64_t generic_score_floats(const ModelDims& m, int64_t pairs) {
+    const int32_t P = (int32_t)(pairs < kGenericChunk ? (pairs > 0 ? pairs : 1) : kGenericChunk);
+    return (int64_t)P * m.d + forward_rows_floats(m, P) + 64;
+}
+
+hipError_t launch_score_generic(const ModelDims& m, const float* compute, const float* mu, const float* isig,
+                                int32_t R, int32_t N, const int64_t* req_off, const int32_t* prompt_len,
+                                const int32_t* overlap, const float* inst_feat, float* scores, float* ws, int n_cu,
+                                hipStream_t s) {
+    const int64_t pairs = (int64_t)R * N;
+    const DropArgs none{};
+    for (int64_t p0 = 0; p0 < pairs; p0 += kGenericChunk) {
+        const int32_t P = (int32_t)(pairs - p0 < kGenericChunk ? pairs - p0 : kGenericChunk);
+        float* rows = ws;
+        float* fw = ws + (((int64_t)P * m.d + 63) & ~int64_t(63));
+        int64_t g = ((int64_t)P * m.d + 255) / 256;
+        if (g > (int64_t)n_cu * 16) g = (int64_t)n_cu * 16;
+        hipLaunchKernelGGL(pair_rows_kernel, dim3((uint32_t)g), dim3(256), 0, s, p0, (int64_t)P, N, m.d, m.d_inst,
+                           m.block_tokens, req_off, prompt_len, overlap, inst_feat, rows);
+        float *xn, *z[3] = {}, *a[3] = {};
+        (void)carve_rows(m, P, fw, &xn, z, a);
+        if (m.bf16) forward_rows<true>(m, compute, mu, isig, P, rows, xn, z, a, scores + p0, none, s);
+        else forward_rows<false>(m, compute, mu, isig, P, rows, xn, z, a, scores + p0, none, s);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+// the step
+// ---------------------------------------------------------------------------
 template <bool BF>
 static hipError_t run_update(const ModelDims& m, float* master, float* compute, const float* mu, const float* isig,
                              int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
-                             float* grad_out, void* workspace, hipStream_t s) {
+                             float* grad_out, void* workspace, const DropArgs& D, hipStream_t s) {
     UpdWs w = plan_ws(m, B, reinterpret_cast<char*>(workspace));
     const int64_t nB = B;
-    // forward, saving pre-activations and activations
-    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.z1, w.a1, w.z2, w.a2, w.t, s);
+    const int L = m.L;
+    // forward, saving pre-activations and activations (dropout applied)
+    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.z, w.a, w.t, D, s);
     const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
-    const bool lds_w = m.d <= kDenseMaxK && m.h1 <= kDenseMaxK && m.h2 <= kDenseMaxK;
+    bool lds_w = m.d <= kDenseMaxK;
+    bool mf = BF && m.d <= 256;          // bf16 operands: weight and bias gradients on the matrix cores
+    for (int l = 0; l < L; ++l) {
+        lds_w = lds_w && m.h[l] <= kDenseMaxK;
+        mf = mf && m.h[l] <= 256;
+    }
     // loss and output gradient
     hipLaunchKernelGGL(loss_grad_kernel<BF>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
     if (loss_out)
         hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, s, w.loss_part, w.loss_blocks, B, loss_out);
-    // bf16 operands: weight and bias gradients on the matrix cores
-    const bool mf = BF && m.h1 <= 256 && m.h2 <= 256 && m.d <= 256;
     hipError_t e;
-    // head layer
+    // head
     if (mf) {
-        e = weight_grad_mfma(w.g, w.a2, 1, m.h2, B, w.part, w.grad + m.m_w3, w.grad + m.m_b3, s);
+        e = weight_grad_mfma(w.g, w.a[L - 1], 1, m.hl, B, w.part, w.grad + m.m_w[L], w.grad + m.m_b[L], s);
     } else {
-        e = weight_grad(w.g, w.a2, 1, m.h2, B, w, w.grad + m.m_w3, s);
-        hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b3);
+        e = weight_grad(w.g, w.a[L - 1], 1, m.hl, B, w, w.grad + m.m_w[L], s);
+        hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b[L]);
     }
     if (e != hipSuccess) return e;
-    // second hidden layer
-    hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB * m.h2, 256)), dim3(256), 0, s, w.g,
-                       compute + m.c_w3, w.z2, w.d2, B, m.h2);
-    if (mf) {
-        e = weight_grad_mfma(w.d2, w.a1, m.h2, m.h1, B, w.part, w.grad + m.m_w2, w.grad + m.m_b2, s);
-    } else {
-        e = weight_grad(w.d2, w.a1, m.h2, m.h1, B, w, w.grad + m.m_w2, s);
-        hipLaunchKernelGGL(rowsum_kernel, dim3(m.h2), dim3(256), 0, s, w.d2, B, w.grad + m.m_b2);
+    hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB * m.hl, 256)), dim3(256), 0, s, w.g,
+                       compute + m.c_wt[L], w.z[L - 1], w.dl[L - 1], B, m.hl, D, L - 1);
+    // hidden layers, last to first
+    for (int l = L - 1; l >= 0; --l) {
+        const float* in = l == 0 ? w.xn : w.a[l - 1];
+        const int K = m.in_of(l), O = m.h[l];
+        if (mf) {
+            e = weight_grad_mfma(w.dl[l], in, O, K, B, w.part, w.grad + m.m_w[l], w.grad + m.m_b[l], s);
+        } else {
+            e = weight_grad(w.dl[l], in, O, K, B, w, w.grad + m.m_w[l], s);
+            hipLaunchKernelGGL(rowsum_kernel, dim3(O), dim3(256), 0, s, w.dl[l], B, w.grad + m.m_b[l]);
+        }
+        if (e != hipSuccess) return e;
+        if (l == 0) break;
+        // dL/dz of layer l - 1 = (W_l^T dL/dz_l), masked by z_{l-1} > 0 and dropout
+        const int Kp = m.h[l - 1];
+        if (lds_w)
+            hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + 31) / 32), dim3(256), 0, s, w.dl[l],
+                               compute + m.c_wt[l], nullptr, w.z[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
+        else
+            hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (Kp + 63) / 64), dim3(256), 0, s,
+                               compute + m.c_wt[l], w.dl[l], w.z[l - 1], w.dl[l - 1], Kp, O, B, D, l - 1);
     }
-    if (e != hipSuccess) return e;
-    // first hidden layer
-    if (lds_w)
-        hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (m.h1 + 31) / 32), dim3(256), 0, s, w.d2,
-                           compute + m.c_w2t, nullptr, w.z1, w.d1, nullptr, B, m.h2, m.h1);
-    else
-        hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (m.h1 + 63) / 64), dim3(256), 0, s,
-                           compute + m.c_w2t, w.d2, w.z1, w.d1, m.h1, m.h2, B);
-    if (mf) {
-        e = weight_grad_mfma(w.d1, w.xn, m.h1, m.d, B, w.part, w.grad + m.m_w1, w.grad + m.m_b1, s);
-    } else {
-        e = weight_grad(w.d1, w.xn, m.h1, m.d, B, w, w.grad + m.m_w1, s);
-        hipLaunchKernelGGL(rowsum_kernel, dim3(m.h1), dim3(256), 0, s, w.d1, B, w.grad + m.m_b1);
-    }
-    if (e != hipSuccess) return e;
     // step and refresh the compute copy
     hipLaunchKernelGGL(sgd_kernel, dim3(blocks_for(m.n_params, 256)), dim3(256), 0, s, master, w.grad, lr,
                        m.n_params, grad_out);
@@ -828,10 +936,12 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
 
 hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,
                          const float* inv_sigma, int32_t B, const float* feats, const float* ttft, float lr,
-                         float* loss_out, float* grad_out, void* workspace, hipStream_t s) {
+                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, hipStream_t s) {
     if (m.bf16)
-        return run_update<true>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace, s);
-    return run_update<false>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace, s);
+        return run_update<true>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace,
+                                drop, s);
+    return run_update<false>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace,
+                             drop, s);
 }
 
 }  // namespace ls

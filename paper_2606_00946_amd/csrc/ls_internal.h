@@ -43,12 +43,16 @@ __host__ __device__ inline uint32_t bucket_of(uint64_t key, uint32_t nb) {
 // addresses consecutive output units.
 // ---------------------------------------------------------------------------
 struct ModelDims {
-    int d = 0, d_inst = 0, h1 = 0, h2 = 0;
+    int d = 0, d_inst = 0, h1 = 0, h2 = 0;   // h1, h2: the two hidden widths of a two-layer model
+    int L = 2;                                // hidden layers, 1..3
+    int h[3] = {0, 0, 0};                     // hidden widths
+    int hl = 0;                               // width of the last hidden layer
     bool bf16 = false;
     int block_tokens = 16;
-    // master offsets (floats)
-    int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0, m_b3 = 0, n_params = 0;
-    // compute-copy offsets (floats)
+    // master offsets (floats), the ABI packing: per layer W [out x in] then b [out]
+    int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0, m_b3 = 0, n_params = 0;   // two-layer names
+    int64_t m_w[4] = {0, 0, 0, 0}, m_b[4] = {0, 0, 0, 0};                            // layer l = 0..L (L: head)
+    // compute-copy offsets (floats).  Two-layer layout (the fused scorers):
     int64_t c_w1 = 0;   // [h1 x d]  row-major (W1[k][c])
     int64_t c_b1 = 0;   // [h1]
     int64_t c_w2t = 0;  // [h1 x h2] W2T[k][j] = W2[j][k]
@@ -56,7 +60,22 @@ struct ModelDims {
     int64_t c_w3 = 0;   // [h2]
     int64_t c_b3 = 0;   // [1]
     int64_t c_w1t = 0;  // [d x h1]  W1T[c][k] = W1[k][c]  (update forward)
+    // every depth: layer l's transposed weights W_l^T [in x out] and bias (for
+    // two layers these alias the arrays above)
+    int64_t c_wt[4] = {0, 0, 0, 0}, c_bl[4] = {0, 0, 0, 0};
     int64_t n_compute = 0;
+    int in_of(int l) const { return l == 0 ? d : h[l - 1]; }
+    int out_of(int l) const { return l == L ? 1 : h[l]; }
+};
+
+// Dropout while training (one update call): inverted dropout on the hidden
+// activations, off when thr53 = 0.  Unit j of hidden layer l for row b draws
+// splitmix64 output c + 1 for `seed`, c = ((step * 4 + l) * 2^24 + b) * 2^10 + j,
+// and is dropped when the draw's top 53 bits are below thr53 = floor(p 2^53);
+// a kept unit is multiplied by `scale` = the fp32 value of 1 / (1 - p).
+struct DropArgs {
+    uint64_t seed = 0, step = 0, thr53 = 0;
+    float scale = 1.0f;
 };
 
 ModelDims make_dims(const ls_model_config& cfg);
@@ -213,11 +232,19 @@ hipError_t launch_rescore(const ModelDims& m, const float* compute, const float*
                           const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
                           const uint32_t* count, float* scores, int n_cu, hipStream_t s);
 
-// Forward pass of B raw rows (canonical chains, kernel precision); a2 [h2][B]
-// and t [B] point into ws, which holds forward_rows_floats(m, B) floats.
+// Forward pass of B raw rows (canonical chains, kernel precision); the last
+// hidden layer's activations [hl][B] and t [B] point into ws, which holds
+// forward_rows_floats(m, B) floats.
 int64_t forward_rows_floats(const ModelDims& m, int32_t B);
 hipError_t launch_forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
-                               const float* feats, float* ws, float** a2_out, float** t_out, hipStream_t s);
+                               const float* feats, float* ws, float** alast_out, float** t_out, hipStream_t s);
+// Scores of all R x N pairs for models without two hidden layers, in chunks
+// through the same forward; ws holds generic_score_floats(m, R * N) floats.
+int64_t generic_score_floats(const ModelDims& m, int64_t pairs);
+hipError_t launch_score_generic(const ModelDims& m, const float* compute, const float* mu, const float* isig,
+                                int32_t R, int32_t N, const int64_t* req_off, const int32_t* prompt_len,
+                                const int32_t* overlap, const float* inst_feat, float* scores, float* ws, int n_cu,
+                                hipStream_t s);
 
 // Online-learning data path: row gathers and scatters, and the gradient-coreset
 // admission of nc candidates into a pool of n0 members (cap slots).
@@ -236,6 +263,6 @@ hipError_t launch_loss_finish(const double* acc, int32_t count, float* out, hipS
 int64_t update_workspace_bytes(const ModelDims& m, int32_t B);
 hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,
                          const float* inv_sigma, int32_t B, const float* feats, const float* ttft, float lr,
-                         float* loss_out, float* grad_out, void* workspace, hipStream_t s);
+                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, hipStream_t s);
 
 }  // namespace ls

@@ -30,6 +30,9 @@ struct ls_ctx {
     uint16_t* frag16 = nullptr;
     float* frag32 = nullptr;
     bool exact_scores = false;
+    // dropout while training: rate, seed and the number of update calls since it was set
+    double drop_p = 0.0;
+    uint64_t drop_seed = 0, drop_step = 0;
     int prefix_join = 0;     // 0 decide per call, 1 always, 2 never
     bool prefix_closed = false;
     int n_cu = 1;
@@ -120,6 +123,18 @@ struct DeviceScope {
 };
 
 int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// The dropout of the next update call (and count it).
+ls::DropArgs next_drop(ls_ctx* c) {
+    ls::DropArgs D;
+    if (c->drop_p > 0.0) {
+        D.seed = c->drop_seed;
+        D.step = c->drop_step++;
+        D.thr53 = (uint64_t)ldexp(c->drop_p, 53);
+        D.scale = (float)(1.0 / (1.0 - c->drop_p));
+    }
+    return D;
+}
 
 bool valid_config(const ls_model_config* cfg, std::string* why) {
     if (!cfg) { *why = "config is NULL"; return false; }
@@ -246,27 +261,46 @@ ModelDims make_dims(const ls_model_config& cfg) {
     ModelDims m;
     m.d = cfg.d;
     m.d_inst = cfg.d - LS_DERIVED_COLS;
-    m.h1 = cfg.hidden[0];
-    m.h2 = cfg.n_hidden >= 2 ? cfg.hidden[1] : 0;
+    m.L = cfg.n_hidden;
+    for (int l = 0; l < m.L; ++l) m.h[l] = cfg.hidden[l];
+    m.hl = m.h[m.L - 1];
+    m.h1 = m.h[0];
+    m.h2 = m.L >= 2 ? m.h[1] : 0;
     m.bf16 = cfg.dtype == LS_BF16;
     m.block_tokens = cfg.block_tokens;
+    // masters: the ABI packing, per layer W [out x in] then b [out]
     int64_t o = 0;
-    m.m_w1 = o; o += (int64_t)m.h1 * m.d;
-    m.m_b1 = o; o += m.h1;
-    m.m_w2 = o; o += (int64_t)m.h2 * m.h1;
-    m.m_b2 = o; o += m.h2;
-    m.m_w3 = o; o += m.h2;
-    m.m_b3 = o; o += 1;
+    for (int l = 0; l <= m.L; ++l) {
+        m.m_w[l] = o; o += (int64_t)m.out_of(l) * m.in_of(l);
+        m.m_b[l] = o; o += m.out_of(l);
+    }
     m.n_params = o;
-    o = 0;
-    m.c_w1 = o; o += (int64_t)m.h1 * m.d;
-    m.c_b1 = o; o += m.h1;
-    m.c_w2t = o; o += (int64_t)m.h1 * m.h2;
-    m.c_b2 = o; o += m.h2;
-    m.c_w3 = o; o += m.h2;
-    m.c_b3 = o; o += 1;
-    m.c_w1t = o; o += (int64_t)m.d * m.h1;
-    m.n_compute = o;
+    if (m.L == 2) {
+        m.m_w1 = m.m_w[0]; m.m_b1 = m.m_b[0];
+        m.m_w2 = m.m_w[1]; m.m_b2 = m.m_b[1];
+        m.m_w3 = m.m_w[2]; m.m_b3 = m.m_b[2];
+        // compute copy of the fused two-layer scorers
+        o = 0;
+        m.c_w1 = o; o += (int64_t)m.h1 * m.d;
+        m.c_b1 = o; o += m.h1;
+        m.c_w2t = o; o += (int64_t)m.h1 * m.h2;
+        m.c_b2 = o; o += m.h2;
+        m.c_w3 = o; o += m.h2;
+        m.c_b3 = o; o += 1;
+        m.c_w1t = o; o += (int64_t)m.d * m.h1;
+        m.n_compute = o;
+        m.c_wt[0] = m.c_w1t; m.c_bl[0] = m.c_b1;
+        m.c_wt[1] = m.c_w2t; m.c_bl[1] = m.c_b2;
+        m.c_wt[2] = m.c_w3;  m.c_bl[2] = m.c_b3;
+    } else {
+        // every layer transposed, W_l^T [in x out], then its bias
+        o = 0;
+        for (int l = 0; l <= m.L; ++l) {
+            m.c_wt[l] = o; o += (int64_t)m.in_of(l) * m.out_of(l);
+            m.c_bl[l] = o; o += m.out_of(l);
+        }
+        m.n_compute = o;
+    }
     return m;
 }
 
@@ -297,7 +331,6 @@ int ls_create(const ls_model_config* cfg, int device, ls_ctx** out) {
     *out = nullptr;
     std::string why;
     if (!valid_config(cfg, &why)) return LS_ERR_INVALID;
-    if (cfg->n_hidden != 2) return LS_ERR_UNSUPPORTED;       // this build fuses exactly two hidden layers
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
         (void)hipGetLastError();
@@ -613,6 +646,7 @@ size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool h
     const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
     need += (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256);
+    if (m.L != 2) need += (size_t)round_up(4 * ls::generic_score_floats(m, pairs), 256);
     if (!have_overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!have_scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
@@ -651,8 +685,19 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
                                      ls::prefix_use_join(R, N, c->tables.total_buckets * ls::kBucketKeys,
                                                          c->prefix_join),
                                      c->prefix_closed, s));
-    LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     const uint8_t* band = nullptr;
+    if (m.L != 2) {
+        // other depths: the pairs' rows through the layer-by-layer canonical forward
+        float* gws = w.take<float>(ls::generic_score_floats(m, pairs));
+        LS_TIMED(c, K_SCORE, s,
+                 ls::launch_score_generic(m, c->compute, c->mu, c->isig, R, N, req_off, prompt_len, ov, inst_feat, sc,
+                                          gws, c->n_cu, s));
+        out->ov = ov;
+        out->sc = sc;
+        out->band = nullptr;
+        return LS_OK;
+    }
+    LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     if (fast) {
         uint16_t* xinst = w.take<uint16_t>((int64_t)N * 64);
         float* eb = w.take<float>(pairs);
@@ -818,9 +863,11 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     int64_t need = ls::update_workspace_bytes(c->dims, B);
     int rc = grow(c, &c->ws, &c->ws_cap, (size_t)need);
     if (rc) return rc;
+    if (c->drop_p > 0.0 && B >= (1 << 24)) return fail(c, LS_ERR_INVALID, "B must be below 2^24 with dropout");
+    const ls::DropArgs D = next_drop(c);
     LS_TIMED(c, K_UPDATE, s,
              ls::launch_update(c->dims, c->master, c->compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
-                               c->ws, s));
+                               c->ws, D, s));
     if (c->frag16)
         LS_TIMED(c, K_UPDATE, s,
                  ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
@@ -847,7 +894,7 @@ int ls_buffer_init(ls_ctx* c, int32_t fifo_cap, int32_t replay_cap) {
     B.emb = B.nnd = B.D = nullptr;
     B.nni = nullptr;
     B.fifo_cap = B.rep_cap = B.fifo_count = B.fifo_head = B.rep_count = 0;
-    const int d = c->dims.d, H = c->dims.h2;
+    const int d = c->dims.d, H = c->dims.hl;
     const int32_t rc1 = replay_cap > 0 ? replay_cap : 1;
     bool ok = hipMalloc((void**)&B.fifo_x, sizeof(float) * (size_t)fifo_cap * d) == hipSuccess &&
               hipMalloc((void**)&B.fifo_y, sizeof(float) * (size_t)fifo_cap) == hipSuccess &&
@@ -888,7 +935,7 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
     const ls::ModelDims& m = c->dims;
-    const int d = m.d, H = m.h2;
+    const int d = m.d, H = m.hl;
     // the FIFO on the host: which rows leave it (candidates, oldest first) and where the new rows land
     std::vector<int32_t> slot_src(bf.fifo_cap);       // >= 0: old slot content, < 0: new row -(b + 1)
     for (int32_t q = 0; q < bf.fifo_cap; ++q) slot_src[q] = q;
@@ -1054,9 +1101,10 @@ int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int
             LS_TIMED(c, K_UPDATE, s,
                      ls::launch_gather_rows(dcodes + (int64_t)e * n + st, mb, d, bf.fifo_x, bf.fifo_y, bf.rep_x,
                                             bf.rep_y, bx, by, s));
+            const ls::DropArgs D = next_drop(c);
             LS_TIMED(c, K_UPDATE, s,
                      ls::launch_update(m, c->master, c->compute, c->mu, c->isig, mb, bx, by, lr, step_loss, nullptr,
-                                       uws, s));
+                                       uws, D, s));
             if (e + 1 == epochs && loss_out) LS_HIP(c, ls::launch_loss_accumulate(step_loss, acc, nb == 0, s));
             ++nb;
         }
@@ -1238,6 +1286,18 @@ int ls_read_cache_state(ls_ctx* c, int32_t n_instances, int64_t* inst_off, uint6
     if (stamps && total > 0)
         LS_HIP(c, hipMemcpyAsync(stamps, X.stamp, sizeof(uint64_t) * (size_t)total, hipMemcpyDeviceToDevice, s));
     LS_HIP(c, hipStreamSynchronize(s));
+    return LS_OK;
+}
+
+int ls_set_dropout(ls_ctx* c, float p, uint64_t seed) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!(p >= 0.0f && p < 1.0f)) return fail(c, LS_ERR_INVALID, "dropout rate must be in [0, 1)");
+    for (int l = 0; l < c->dims.L; ++l)
+        if (c->dims.h[l] > 1024) return fail(c, LS_ERR_UNSUPPORTED, "dropout needs hidden widths up to 1024");
+    c->drop_p = (double)p;
+    c->drop_seed = seed;
+    c->drop_step = 0;
     return LS_OK;
 }
 

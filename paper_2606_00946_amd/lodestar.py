@@ -96,13 +96,14 @@ def library():
         lib.ls_route_batch.argtypes = [P, ctypes.POINTER(ls_policy), i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_profile_read.argtypes = [P, i32, P, P, P, P]
         lib.ls_set_cache_capacity.argtypes = [P, i32, P]
+        lib.ls_set_dropout.argtypes = [P, f32, ctypes.c_uint64]
         lib.ls_commit_routes.argtypes = [P, i32, i64, P, P, P, P]
         lib.ls_read_cache_state.argtypes = [P, i32, P, P, P, i64, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
                   lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
                   lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round,
-                  lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state):
+                  lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state, lib.ls_set_dropout):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -229,6 +230,10 @@ class Context:
         self._check("ls_load_cache_state", rc)
         self.n_instances = N
         return rc
+
+    def ls_set_dropout(self, p, seed=0):
+        """Dropout rate p in [0, 1) on the hidden activations of later updates (0: off)."""
+        return self._check("ls_set_dropout", self.lib.ls_set_dropout(self.h, float(p), ctypes.c_uint64(int(seed))))
 
     # -- prefix-index maintenance -----------------------------------------
     def ls_set_cache_capacity(self, capacity):

@@ -47,8 +47,17 @@ def test_create_rejects_bad_configs_on_the_host():
     for cfg in bad:
         assert lib.ls_create(ctypes.byref(cfg), 0, ctypes.byref(h)) == lodestar.LS_ERR_INVALID
         assert h.value is None
-    three = lodestar.make_config(16, [128, 128, 128])
-    assert lib.ls_create(ctypes.byref(three), 0, ctypes.byref(h)) == lodestar.LS_ERR_UNSUPPORTED
+    # depths 1..3 are valid (the paper's model is 3 x 128); here the only failure left is the missing device
+    for hidden in ([128, 128, 128], [64]):
+        cfg = lodestar.make_config(16, hidden)
+        rc = lib.ls_create(ctypes.byref(cfg), 0, ctypes.byref(h))
+        assert rc not in (lodestar.LS_ERR_INVALID, lodestar.LS_ERR_UNSUPPORTED), rc
+        if rc == lodestar.LS_OK:
+            lib.ls_destroy(h)
+        h = ctypes.c_void_p(1)
+    four = lodestar.make_config(16, [8, 8])
+    four.n_hidden = 4
+    assert lib.ls_create(ctypes.byref(four), 0, ctypes.byref(h)) == lodestar.LS_ERR_INVALID
     assert lib.ls_create(None, 0, ctypes.byref(h)) == lodestar.LS_ERR_INVALID
     assert lib.ls_last_error(None) == b"context is NULL"
 

@@ -1,0 +1,162 @@
+"""Models other than two hidden layers -- the paper's 3 x 128 reward model (Section
+4.1) and a single hidden layer -- and dropout while training, through the C ABI
+against the oracle.
+
+Scores on the layer-by-layer path are the canonical chains, so they must be
+bit-identical to the oracle in the kernel's precision; updates (with dropout's
+masks drawn on both sides from the same counter-based generator) within the
+update bars of the two-layer tests."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_helpers import GpuRun, layer_slices, note, rel_ok, to_dev
+from paper_2606_00946_amd import lodestar, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def workload(hidden, dtype, R=160, N=32):
+    cfg = dataclasses.replace(synth.CONFIGS["homogeneous"], hidden=tuple(hidden), dtype=dtype, R=R, N=N,
+                              update_batch=300)
+    return synth.generate(cfg)
+
+
+def mode_of(w):
+    return "bf16" if w.cfg.dtype == "bf16" else "fp32"
+
+
+@pytest.mark.parametrize("hidden,dtype", [((128, 128, 128), "fp32"), ((128, 128, 128), "bf16"), ((64,), "fp32"),
+                                          ((64,), "bf16")])
+def test_depth_scores_are_canonical(hidden, dtype):
+    w = workload(hidden, dtype)
+    note(f"depth scores hidden={hidden} {dtype}")
+    run = GpuRun(w)
+    out = run.score()
+    sel = np.arange(w.cfg.R, dtype=np.int32)
+    ref = oracle.score(mode_of(w), w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                       w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=16)
+    np.testing.assert_array_equal(out["overlap"], ref["overlap"])
+    np.testing.assert_array_equal(out["scores"].view(np.uint32), ref["scores"].astype(np.float32).view(np.uint32))
+    np.testing.assert_array_equal(out["chosen"], ref["chosen"])
+    np.testing.assert_array_equal(out["min_ttft"].view(np.uint32), ref["min_ttft"].astype(np.float32).view(np.uint32))
+    np.testing.assert_array_equal(out["feat"], ref["feat"].astype(np.float32))
+    if dtype == "fp32":
+        ref64 = oracle.score("f64", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                             w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=16)
+        ok, worst = rel_ok(out["scores"], ref64["scores"], 1e-4)
+        assert ok, worst
+    run.ctx.close()
+
+
+def compare_update(w, got, ref, feats):
+    assert abs(got["loss"] - ref["loss"]) <= 1e-5 * abs(ref["loss"]), (got["loss"], ref["loss"])
+    report = []
+    for lname, a, b in layer_slices(w.cfg.d, w.cfg.hidden):
+        g, r = got["grad"][a:b], ref["grad"][a:b]
+        nrm = np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)
+        assert nrm <= 1e-4, f"{lname}: norm-wise relative gradient error {nrm}"
+        ok, worst = rel_ok(g, r, 1e-4)
+        assert ok, f"{lname}: elementwise gradient error {worst}"
+        report.append(f"{lname} {worst:.1e}")
+        dg = got["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
+        dr = ref["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
+        ulp = np.spacing(np.abs(ref["params"][a:b])).astype(np.float64)
+        assert np.all(np.abs(dg - dr) <= 1e-4 * np.abs(dr) + ulp), lname
+    print(f"update B={feats.shape[0]}: " + ", ".join(report), flush=True)
+
+
+@pytest.mark.parametrize("hidden,dtype", [((128, 128, 128), "fp32"), ((128, 128, 128), "bf16"), ((64,), "fp32"),
+                                          ((64,), "bf16")])
+def test_depth_update_parity(hidden, dtype):
+    w = workload(hidden, dtype)
+    feats, ttft = w.upd_feats[:300], w.upd_ttft[:300]
+    note(f"depth update hidden={hidden} {dtype}")
+    run = GpuRun(w)
+    got = run.update(feats, ttft)
+    ref = oracle.update(mode_of(w), w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, feats, ttft, w.lr)
+    compare_update(w, got, ref, feats)
+    run.ctx.close()
+
+
+@pytest.mark.parametrize("hidden,dtype", [((128, 128, 128), "fp32"), ((128, 128, 128), "bf16"), ((128, 128), "fp32"),
+                                          ((256, 256), "bf16")])
+def test_dropout_update_parity(hidden, dtype):
+    """Two consecutive updates with dropout 0.1 (update calls 0 and 1 of the seed):
+    the masks, the loss and every gradient against the oracle's."""
+    w = workload(hidden, dtype)
+    feats, ttft = w.upd_feats[:300], w.upd_ttft[:300]
+    seed = 0xC0FFEE
+    note(f"dropout update hidden={hidden} {dtype}")
+    run = GpuRun(w)
+    run.ctx.ls_set_dropout(0.1, seed)
+    params = w.params
+    for step in range(2):
+        got = run.update(feats, ttft)
+        ref = oracle.update(mode_of(w), w.cfg.d, w.cfg.hidden, params, w.mu, w.inv_sigma, feats, ttft, w.lr,
+                            dropout=(0.1, seed, step))
+        w_step = dataclasses.replace(w, params=params)
+        compare_update(w_step, got, ref, feats)
+        plain = oracle.update(mode_of(w), w.cfg.d, w.cfg.hidden, params, w.mu, w.inv_sigma, feats, ttft, w.lr)
+        assert plain["loss"] != ref["loss"]                       # dropout did act
+        params = ref["params"]
+    run.ctx.close()
+
+
+def test_dropout_train_round_paper_model():
+    """The data path with the paper's 3 x 128 model and dropout 0.1: push, then a
+    retraining round whose minibatches are update calls 0, 1, ... of the seed."""
+    import torch
+    w = workload((128, 128, 128), "fp32")
+    cfg = w.cfg
+    x, y = w.upd_feats[:60], w.upd_ttft[:60]
+    note("dropout retraining round, paper model")
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    ctx.ls_buffer_init(30, 12)
+    ctx.ls_buffer_push(to_dev(x.astype(np.float32)), to_dev(y.astype(np.float32)))
+    buf = oracle.Buffer(cfg.d, 30, 12)
+    oracle.buffer_push("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, x, y)
+    n = 30 + int(buf.rep_count[0])
+    perm = np.concatenate([np.random.default_rng(e).permutation(n) for e in range(2)]).astype(np.int32)
+    ctx.ls_set_dropout(0.1, 77)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    ctx.ls_train_round(2, 8, w.lr, perm, loss)
+    torch.cuda.synchronize()
+    got, _, _ = ctx.ls_get_model()
+    ref, ref_loss = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 2, 8, w.lr, perm,
+                                       dropout=(0.1, 77, 0))
+    for lname, a, b in layer_slices(cfg.d, cfg.hidden):
+        d = got[a:b].astype(np.float64) - w.params[a:b]
+        r = ref[a:b].astype(np.float64) - w.params[a:b]
+        assert np.linalg.norm(d - r) <= 1e-3 * max(np.linalg.norm(r), 1e-30), lname
+    assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-4 * abs(ref_loss)
+    ctx.close()
+
+
+def test_route_paper_model():
+    """The routing policy with the paper's 3 x 128 model (layer-by-layer scores)."""
+    import torch
+    w = workload((128, 128, 128), "fp32", R=96)
+    cfg = w.cfg
+    pol = dict(heuristic=1, count_cols=(0, 1), theta_imbal=4.0, overload_k=0.5, n_samples=100, n_min=10,
+               epsilon=0.2, delta=0.05)
+    rnd = np.random.default_rng(17).integers(0, 1 << 32, (cfg.R, 3), dtype=np.uint64).astype(np.uint32)
+    note("route paper model")
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    ctx.ls_load_cache_state(w.inst_off, to_dev(w.inst_hashes))
+    chosen = torch.full((cfg.R,), -7, dtype=torch.int32, device="cuda")
+    status = torch.full((cfg.R,), -7, dtype=torch.int32, device="cuda")
+    ctx.ls_route_batch(lodestar.make_policy(**pol), to_dev(w.req_off), to_dev(w.req_hashes),
+                       to_dev(w.prompt_len.astype(np.int32)), to_dev(w.inst_feat.astype(np.float32)),
+                       to_dev(rnd.view(np.int32)), chosen, status)
+    torch.cuda.synchronize()
+    want = oracle.route("fp32", cfg.d, cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                        w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, oracle.policy(**pol), rnd,
+                        sel=np.arange(cfg.R, dtype=np.int32))
+    np.testing.assert_array_equal(status.cpu().numpy(), want[1])
+    np.testing.assert_array_equal(chosen.cpu().numpy(), want[0])
+    ctx.close()
