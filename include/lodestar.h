@@ -395,6 +395,41 @@ int ls_train_round(ls_ctx* ctx, int32_t epochs, int32_t batch, float lr, const i
                    void* stream);
 
 /*
+ * Double-buffered retraining (Section 4.3.1, the isolation of training from
+ * inference: a newly trained model replaces the serving one at once, without
+ * stopping routing; Section 4.3.2, retraining runs beside routing).
+ *   ls_set_shadow_training  enable != 0 allocates (first time) a second copy of
+ *                    the model, the shadow, and copies the live model into it
+ *                    on `stream`; from then on ls_update, ls_train_round and
+ *                    the embeddings of ls_buffer_push use the shadow, while
+ *                    ls_score_batch and ls_route_batch keep using the live
+ *                    model.  ls_set_model writes both; ls_get_model reads the
+ *                    live one.  enable == 0 returns updates to the live model
+ *                    (the shadow's contents are then dropped at the next
+ *                    enable).  LS_ERR_STATE without a model.
+ *   ls_swap_model    exchanges live and shadow, ordered on the device: the
+ *                    serving stream waits for the work enqueued so far on the
+ *                    training stream, the training stream waits for the work
+ *                    enqueued so far on the serving stream, then (host side)
+ *                    the two slots trade places and the new live model is
+ *                    copied into the shadow on the training stream, so that
+ *                    training continues from the model now serving.  Scoring
+ *                    calls enqueued on serve_stream after the swap use the new
+ *                    model; those enqueued before it, the old one.  The two
+ *                    streams may be the same.  LS_ERR_STATE without a shadow.
+ * Streams: ls_update, ls_buffer_push and ls_train_round use scratch memory of
+ * their own, apart from the scoring calls', so with the shadow on they may run
+ * on a training stream while ls_score_batch / ls_route_batch run on a serving
+ * stream; the three training calls share their scratch and the buffer, so
+ * they belong on one stream (or are ordered by the caller), as do the scoring
+ * calls and ls_commit_routes among themselves.
+ * Ownership: the shadow is freed by ls_destroy.  A context is still driven from
+ * one host thread: the streams order device work, not host calls.
+ */
+int ls_set_shadow_training(ls_ctx* ctx, int enable, void* stream);
+int ls_swap_model(ls_ctx* ctx, void* serve_stream, void* train_stream);
+
+/*
  * Per-kernel timing (the library's own view of where the routing time goes;
  * Section 5.4 measures the router's overhead end to end).  While enabled, each
  * kernel launch group of the context is bracketed by HIP events on the stream

@@ -30,6 +30,12 @@ struct ls_ctx {
     uint16_t* frag16 = nullptr;
     float* frag32 = nullptr;
     bool exact_scores = false;
+    // shadow model for double-buffered retraining: updates act on it, scoring
+    // on the live model above, until ls_swap_model exchanges the two
+    bool shadow_on = false;
+    float *sh_master = nullptr, *sh_compute = nullptr, *sh_frag32 = nullptr;
+    uint16_t* sh_frag16 = nullptr;
+    hipEvent_t swap_ev[2] = {nullptr, nullptr};
     // dropout while training: rate, seed and the number of update calls since it was set
     double drop_p = 0.0;
     uint64_t drop_seed = 0, drop_step = 0;
@@ -67,6 +73,10 @@ struct ls_ctx {
     // grow-only workspace
     void* ws = nullptr;
     size_t ws_cap = 0;
+    // scratch of ls_update alone, so that an update on a training stream never
+    // shares memory with a scoring call on another stream
+    void* upd_ws = nullptr;
+    size_t upd_ws_cap = 0;
     // online-learning data path (device pools, host-side counters)
     struct Buffer {
         int32_t fifo_cap = 0, rep_cap = 0, fifo_count = 0, fifo_head = 0, rep_count = 0;
@@ -123,6 +133,34 @@ struct DeviceScope {
 };
 
 int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// The model that updates act on: the shadow while double buffering, else the live one.
+struct ModelSlot {
+    float* master;
+    float* compute;
+    uint16_t* frag16;
+    float* frag32;
+};
+ModelSlot train_model(ls_ctx* c) {
+    if (c->shadow_on) return {c->sh_master, c->sh_compute, c->sh_frag16, c->sh_frag32};
+    return {c->master, c->compute, c->frag16, c->frag32};
+}
+
+// Copy one model slot onto another on stream s.
+hipError_t copy_model(ls_ctx* c, const ModelSlot& to, const ModelSlot& from, hipStream_t s) {
+    hipError_t e = hipMemcpyAsync(to.master, from.master, sizeof(float) * (size_t)c->dims.n_params,
+                                  hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(to.compute, from.compute, sizeof(float) * (size_t)c->dims.n_compute,
+                           hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && from.frag16) {
+        const ls::MfmaLayout L = ls::make_mfma_layout(c->dims);
+        e = hipMemcpyAsync(to.frag16, from.frag16, sizeof(uint16_t) * (size_t)L.n16, hipMemcpyDeviceToDevice, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(to.frag32, from.frag32, sizeof(float) * (size_t)L.n32, hipMemcpyDeviceToDevice, s);
+    }
+    return e;
+}
 
 // The dropout of the next update call (and count it).
 ls::DropArgs next_drop(ls_ctx* c) {
@@ -376,10 +414,13 @@ void ls_destroy(ls_ctx* c) {
                         (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
                         (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws, (void*)c->idx.hash,
                         (void*)c->idx.stamp, (void*)c->idx.hash2, (void*)c->idx.stamp2, (void*)c->idx.entry_of,
-                        (void*)c->idx.small, c->idx.ws})
+                        (void*)c->idx.small, c->idx.ws, (void*)c->sh_master, (void*)c->sh_compute, c->upd_ws,
+                        (void*)c->sh_frag16, (void*)c->sh_frag32})
             if (p) (void)hipFree(p);
         if (c->stage) (void)hipHostFree(c->stage);
         if (c->stage_done) (void)hipEventDestroy(c->stage_done);
+        for (hipEvent_t e : c->swap_ev)
+            if (e) (void)hipEventDestroy(e);
         for (auto& r : c->recs) {
             (void)hipEventDestroy(r.start);
             (void)hipEventDestroy(r.stop);
@@ -416,6 +457,9 @@ int ls_set_model(ls_ctx* c, const float* params, int64_t n_params, const float* 
     LS_HIP(c, ls::launch_refresh_compute_copy(c->dims, c->master, c->compute, s));
     if (c->frag16)
         LS_HIP(c, ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
+    if (c->shadow_on)
+        LS_HIP(c, copy_model(c, {c->sh_master, c->sh_compute, c->sh_frag16, c->sh_frag32},
+                             {c->master, c->compute, c->frag16, c->frag32}, s));
     c->have_model = true;
     return LS_OK;
 }
@@ -861,16 +905,17 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
     int64_t need = ls::update_workspace_bytes(c->dims, B);
-    int rc = grow(c, &c->ws, &c->ws_cap, (size_t)need);
+    int rc = grow(c, &c->upd_ws, &c->upd_ws_cap, (size_t)need);
     if (rc) return rc;
     if (c->drop_p > 0.0 && B >= (1 << 24)) return fail(c, LS_ERR_INVALID, "B must be below 2^24 with dropout");
     const ls::DropArgs D = next_drop(c);
+    const ModelSlot M = train_model(c);
     LS_TIMED(c, K_UPDATE, s,
-             ls::launch_update(c->dims, c->master, c->compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
-                               c->ws, D, s));
-    if (c->frag16)
+             ls::launch_update(c->dims, M.master, M.compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
+                               c->upd_ws, D, s));
+    if (M.frag16)
         LS_TIMED(c, K_UPDATE, s,
-                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
+                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), M.master, M.frag16, M.frag32, s));
     return LS_OK;
 }
 
@@ -1000,7 +1045,8 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
         LS_HIP(c, hipMemcpyAsync(ax + (int64_t)n0 * d, cx, sizeof(float) * (size_t)nc * d, hipMemcpyDeviceToDevice, s));
         LS_HIP(c, hipMemcpyAsync(ay + n0, cy, sizeof(float) * (size_t)nc, hipMemcpyDeviceToDevice, s));
         float *a2 = nullptr, *t = nullptr;
-        LS_TIMED(c, K_BUFFER, s, ls::launch_forward_rows(m, c->compute, c->mu, c->isig, n_all, ax, fws, &a2, &t, s));
+        LS_TIMED(c, K_BUFFER, s,
+                 ls::launch_forward_rows(m, train_model(c).compute, c->mu, c->isig, n_all, ax, fws, &a2, &t, s));
         LS_TIMED(c, K_BUFFER, s,
                  ls::launch_admission(a2, t, ay, n0, nc, H, d, bf.rep_cap, cx, cy, cemb, bf.emb, bf.rep_x, bf.rep_y,
                                       bf.D, bf.nnd, bf.nni, drow, redo, admitted ? admitted : adm, s));
@@ -1093,6 +1139,7 @@ int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int
     LS_HIP(c, hipMemcpyAsync(dcodes, c->stage, sizeof(int32_t) * codes.size(), hipMemcpyHostToDevice, s));
     LS_HIP(c, hipEventRecord(c->stage_done, s));
     c->stage_pending = true;
+    const ModelSlot TM = train_model(c);
     int32_t nb = 0;
     for (int32_t e = 0; e < epochs; ++e) {
         nb = 0;
@@ -1103,16 +1150,16 @@ int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int
                                             bf.rep_y, bx, by, s));
             const ls::DropArgs D = next_drop(c);
             LS_TIMED(c, K_UPDATE, s,
-                     ls::launch_update(m, c->master, c->compute, c->mu, c->isig, mb, bx, by, lr, step_loss, nullptr,
+                     ls::launch_update(m, TM.master, TM.compute, c->mu, c->isig, mb, bx, by, lr, step_loss, nullptr,
                                        uws, D, s));
             if (e + 1 == epochs && loss_out) LS_HIP(c, ls::launch_loss_accumulate(step_loss, acc, nb == 0, s));
             ++nb;
         }
     }
     if (loss_out) LS_HIP(c, ls::launch_loss_finish(acc, nb, loss_out, s));
-    if (c->frag16)
+    if (TM.frag16)
         LS_TIMED(c, K_UPDATE, s,
-                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), c->master, c->frag16, c->frag32, s));
+                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), TM.master, TM.frag16, TM.frag32, s));
     return LS_OK;
 }
 
@@ -1298,6 +1345,59 @@ int ls_set_dropout(ls_ctx* c, float p, uint64_t seed) {
     c->drop_p = (double)p;
     c->drop_seed = seed;
     c->drop_step = 0;
+    return LS_OK;
+}
+
+int ls_set_shadow_training(ls_ctx* c, int enable, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!enable) {
+        c->shadow_on = false;
+        return LS_OK;
+    }
+    if (!c->have_model) return fail(c, LS_ERR_STATE, "no model has been set");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    if (!c->sh_master) {
+        bool ok = hipMalloc((void**)&c->sh_master, sizeof(float) * c->dims.n_params) == hipSuccess &&
+                  hipMalloc((void**)&c->sh_compute, sizeof(float) * c->dims.n_compute) == hipSuccess;
+        if (ok && c->frag16) {
+            const ls::MfmaLayout L = ls::make_mfma_layout(c->dims);
+            ok = hipMalloc((void**)&c->sh_frag16, sizeof(uint16_t) * L.n16) == hipSuccess &&
+                 hipMalloc((void**)&c->sh_frag32, sizeof(float) * L.n32) == hipSuccess;
+        }
+        ok = ok && hipEventCreateWithFlags(&c->swap_ev[0], hipEventDisableTiming) == hipSuccess &&
+             hipEventCreateWithFlags(&c->swap_ev[1], hipEventDisableTiming) == hipSuccess;
+        if (!ok) {
+            (void)hipGetLastError();
+            return fail(c, LS_ERR_NOMEM, "shadow model allocation failed");
+        }
+    }
+    LS_HIP(c, copy_model(c, {c->sh_master, c->sh_compute, c->sh_frag16, c->sh_frag32},
+                         {c->master, c->compute, c->frag16, c->frag32}, (hipStream_t)stream));
+    c->shadow_on = true;
+    return LS_OK;
+}
+
+int ls_swap_model(ls_ctx* c, void* serve_stream, void* train_stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!c->shadow_on) return fail(c, LS_ERR_STATE, "no shadow model (ls_set_shadow_training)");
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t serve = (hipStream_t)serve_stream, train = (hipStream_t)train_stream;
+    // serving from here on waits for the training enqueued so far ...
+    LS_HIP(c, hipEventRecord(c->swap_ev[0], train));
+    LS_HIP(c, hipStreamWaitEvent(serve, c->swap_ev[0], 0));
+    // ... and the old live model is overwritten only after the serving enqueued so far
+    LS_HIP(c, hipEventRecord(c->swap_ev[1], serve));
+    LS_HIP(c, hipStreamWaitEvent(train, c->swap_ev[1], 0));
+    std::swap(c->master, c->sh_master);
+    std::swap(c->compute, c->sh_compute);
+    std::swap(c->frag16, c->sh_frag16);
+    std::swap(c->frag32, c->sh_frag32);
+    LS_HIP(c, copy_model(c, {c->sh_master, c->sh_compute, c->sh_frag16, c->sh_frag32},
+                         {c->master, c->compute, c->frag16, c->frag32}, train));
     return LS_OK;
 }
 

@@ -99,11 +99,14 @@ def library():
         lib.ls_set_dropout.argtypes = [P, f32, ctypes.c_uint64]
         lib.ls_commit_routes.argtypes = [P, i32, i64, P, P, P, P]
         lib.ls_read_cache_state.argtypes = [P, i32, P, P, P, i64, P]
+        lib.ls_set_shadow_training.argtypes = [P, ctypes.c_int, P]
+        lib.ls_swap_model.argtypes = [P, P, P]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
                   lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
                   lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round,
-                  lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state, lib.ls_set_dropout):
+                  lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state, lib.ls_set_dropout,
+                  lib.ls_set_shadow_training, lib.ls_swap_model):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -230,6 +233,16 @@ class Context:
         self._check("ls_load_cache_state", rc)
         self.n_instances = N
         return rc
+
+    def ls_set_shadow_training(self, enable=True, stream=None):
+        """Double-buffered retraining: updates act on a shadow copy of the model."""
+        return self._check("ls_set_shadow_training",
+                           self.lib.ls_set_shadow_training(self.h, int(bool(enable)), _stream(stream)))
+
+    def ls_swap_model(self, serve_stream=None, train_stream=None):
+        """Make the shadow model the live one (ordered between the two streams)."""
+        return self._check("ls_swap_model",
+                           self.lib.ls_swap_model(self.h, _stream(serve_stream), _stream(train_stream)))
 
     def ls_set_dropout(self, p, seed=0):
         """Dropout rate p in [0, 1) on the hidden activations of later updates (0: off)."""

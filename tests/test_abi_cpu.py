@@ -69,6 +69,8 @@ def test_entry_points_reject_null_context():
     assert lib.ls_load_cache_state(None, 1, None, None, None) == lodestar.LS_ERR_INVALID
     assert lib.ls_score_batch(None, 1, 1, *([None] * 10)) == lodestar.LS_ERR_INVALID
     assert lib.ls_update(None, 1, None, None, 0.1, None, None, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_set_shadow_training(None, 1, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_swap_model(None, None, None) == lodestar.LS_ERR_INVALID
     lib.ls_destroy(None)
 
 
