@@ -5,8 +5,11 @@
 // mode its weights and every layer input are bf16, sums fp32.  The bulk of the
 // work is the [pairs x h1] x [h1 x h2] hidden layer, a dense contraction, so it
 // runs as v_mfma_f32_32x32x16_bf16 with rows = units and columns = pairs:
-//   layer 1  A = W1 fragments, B = normalised bf16 pair rows, C = b1
-//   layer 2  A = W2 fragments (LDS), B = bf16(relu(layer-1 accumulators))
+//   layer 1  C = the instance's layer-1 partial (b1 and the instance columns,
+//            computed once per instance as the canonical chain), A = the
+//            weights of the 5 derived columns, B = the pair's bf16 derived
+//            columns: one k-step instead of d/16
+//   layer 2  A = W2 fragments (LDS), B = bf16(relu(layer-1 accumulators)), C = b2
 //   head     A = [w3; |w3|; 0...], B = bf16(relu(layer-2 accumulators))
 // An accumulator of a 32x32 tile holds, in lane l and register r, unit
 // 8(r/4) + 4(l/32) + r%4 of pair l%32.  The next layer's B operand needs, in
@@ -57,11 +60,8 @@ __global__ void prepare_mfma_kernel(MfmaLayout L, const float* __restrict__ mast
         const int64_t f = t >> 9;                       // fragment index
         const int m = lane & 31, h = lane >> 5;
         float v = 0.0f;
-        if (f < L.w1_frags) {                            // [s(4)][mt] : W1[32mt+m][16s+8h+j]
-            const int mt1 = h1 / 32;
-            const int s = (int)(f / mt1), mt = (int)(f % mt1);
-            const int c = 16 * s + 8 * h + j;
-            if (c < d) v = W1[(int64_t)(32 * mt + m) * d + c];
+        if (f < L.w1_frags) {                            // [mt] : W1[32mt+m][d_inst+j], half 0, j < 5
+            if (h == 0 && j < 5) v = W1[(int64_t)(32 * f + m) * d + L.d_inst + j];
         } else {                                         // [mt2][s(h1/16)] : W2[32mt2+m][perm(s,h,j)]
             const int64_t g = f - L.w1_frags;
             const int ks = h1 / 16;
@@ -69,23 +69,14 @@ __global__ void prepare_mfma_kernel(MfmaLayout L, const float* __restrict__ mast
             v = W2[(int64_t)(32 * mt2 + m) * h1 + perm_unit(s, h, j)];
         }
         frag16[t] = bf16_bits(v);
-    } else if (t < L.n16) {                              // head fragments [s(h2/16)][lane][j]: rows w3, |w3|
+    } else if (t < L.n16) {                              // head [s(h2/16)][h][row][j]: row 0 w3, row 1 |w3|
         const int64_t e = t - nfrag;
-        const int j = (int)(e & 7), lane = (int)((e >> 3) & 63);
-        const int s = (int)(e >> 9);
-        const int m = lane & 31, h = lane >> 5;
+        const int j = (int)(e & 7), row = (int)((e >> 3) & 1), h = (int)((e >> 4) & 1);
+        const int s = (int)(e >> 5);
         const float w = W3[perm_unit(s, h, j)];
-        frag16[t] = bf16_bits(m == 0 ? w : m == 1 ? fabsf(w) : 0.0f);
-    } else if (t < L.n16 + L.n32) {                      // bias fragments [mt][h][r] for b1 then b2
-        const int64_t e = t - L.n16;
-        const int r = (int)(e & 15), h = (int)((e >> 4) & 1);
-        const int64_t mt = e >> 5;
-        const int unit_in_tile = 8 * (r >> 2) + 4 * h + (r & 3);
-        const int mt1 = h1 / 32;
-        float v;
-        if (mt < mt1) v = master[L.m_b1 + 32 * mt + unit_in_tile];
-        else v = master[L.m_b2 + 32 * (mt - mt1) + unit_in_tile];
-        frag32[e] = v;
+        frag16[t] = bf16_bits(row == 0 ? w : fabsf(w));
+    } else if (t < L.n16 + L.n32) {                      // b2
+        frag32[t - L.n16] = master[L.m_b2 + (t - L.n16)];
     }
 }
 
@@ -97,38 +88,20 @@ hipError_t launch_prepare_mfma(const MfmaLayout& L, const float* master, uint16_
     return hipGetLastError();
 }
 
-// Normalised bf16 instance columns, 64 per instance (zero past d_inst).
-__global__ void instance_rows_kernel(const float* __restrict__ inst_feat, const float* __restrict__ mu,
-                                     const float* __restrict__ isig, int d_inst, int32_t N,
-                                     uint16_t* __restrict__ xinst) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)N * 64) return;
-    const int64_t i = t >> 6;
-    const int c = (int)(t & 63);
-    float v = 0.0f;
-    if (c < d_inst) v = __fmul_rn(__fsub_rn(inst_feat[i * d_inst + c], mu[c]), isig[c]);
-    xinst[t] = bf16_bits(v);
-}
-
-hipError_t launch_instance_rows(const ModelDims& m, const float* mu, const float* inv_sigma, const float* inst_feat,
-                                int32_t N, uint16_t* xinst, hipStream_t s) {
-    const int64_t n = (int64_t)N * 64;
-    hipLaunchKernelGGL(instance_rows_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, inst_feat, mu,
-                       inv_sigma, m.d_inst, N, xinst);
-    return hipGetLastError();
-}
-
 // ---------------------------------------------------------------------------
-// the MFMA scoring kernel: persistent, one 32-pair tile per wave at a time
+// the MFMA scoring kernel: persistent; a workgroup works through units of 32
+// requests x 16 instances (one instance group at a time)
 // ---------------------------------------------------------------------------
+constexpr int kGroupInst = 16;     // instances per group (columns n%16 of a tile)
+constexpr int kUnitReq = 32;       // requests per unit: 8 waves x 2 tiles x 2
+
 struct MfmaArgs {
     const bf16x8_t* __restrict__ w1frag;
     const bf16x8_t* __restrict__ w2frag;
     const bf16x8_t* __restrict__ hfrag;
-    const float* __restrict__ b1frag;
-    const float* __restrict__ b2frag;
+    const float* __restrict__ b2;
     const float* __restrict__ b3;
-    const uint16_t* __restrict__ xinst;
+    const float* __restrict__ part_t;             // [h1][N]: b1 + the instance columns, canonical
     const float* __restrict__ mu;
     const float* __restrict__ isig;
     const int64_t* __restrict__ req_off;
@@ -137,20 +110,11 @@ struct MfmaArgs {
     float* __restrict__ scores;
     float* __restrict__ errb;
     int32_t R, N;
-    int d, d_inst, block_tokens;
+    int d_inst, block_tokens;
     float band_rel;
+    int64_t n_rblocks;                             // ceil(R / 32)
+    int64_t n_units;                               // ceil(N / 16) * n_rblocks
 };
-
-__device__ __forceinline__ f32x16_t load_bias(const float* __restrict__ p) {
-    const float4* q = reinterpret_cast<const float4*>(p);
-    float4 a = q[0], b = q[1], c = q[2], e = q[3];
-    f32x16_t v;
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-    v[8] = c.x; v[9] = c.y; v[10] = c.z; v[11] = c.w;
-    v[12] = e.x; v[13] = e.y; v[14] = e.z; v[15] = e.w;
-    return v;
-}
 
 // bf16(relu(.)) of accumulator registers 8q .. 8q+7 as one B operand.  Rounding
 // first and clamping the bf16 bit patterns at 0 as signed 16-bit integers is the
@@ -176,90 +140,95 @@ __device__ __forceinline__ bf16x8_t relu_pack(const f32x16_t& acc, int q) {
     return out;
 }
 
-// One wave scores two tiles of 32 pairs (32 consecutive instances of one
-// request each; consecutive tiles in request-major order) per pass; the eight
-// waves of a workgroup share the W1 and W2 fragments in LDS (32 + 128 KB at
-// h = 256).  Every weight fragment read from LDS feeds one MFMA per tile, and
-// every bias and head fragment read serves both tiles.  Each layer runs one
-// row tile at a time, so that few accumulators are live beside the second
-// layer's 2 x h1 bf16 inputs.
-template <int MT1, int MT2, int D>
-__global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
-    static_assert(MT1 == MT2, "square hidden layers");
-    constexpr int KS2 = 2 * MT1;               // layer-2 k-steps: h1 / 16
-    constexpr int D_INST = D - 5;
-    constexpr int NW1 = 4 * MT1 * 64, NW2 = MT2 * KS2 * 64;
-    constexpr int PT = 2;                      // tiles per pass
-    __shared__ bf16x8_t lds_w1[NW1];
-    __shared__ bf16x8_t lds_w2[NW2];
-    for (int f = threadIdx.x; f < NW1; f += blockDim.x) lds_w1[f] = A.w1frag[f];
-    for (int f = threadIdx.x; f < NW2; f += blockDim.x) lds_w2[f] = A.w2frag[f];
-    __syncthreads();
-
-    const int lane = threadIdx.x & 63;
-    const int waves = blockDim.x >> 6;
-    const int h = lane >> 5, n = lane & 31;
-    const int tiles_per_req = (A.N + 31) >> 5;
-    const int64_t n_tiles = (int64_t)A.R * tiles_per_req;
-    const int64_t n_passes = (n_tiles + PT - 1) / PT;
-    const float b3 = A.b3[0];
-    const bf16x8_t* __restrict__ hf = A.hfrag + lane;
-    const bf16x8_t* __restrict__ w1l = lds_w1 + lane;
-    for (int64_t pass = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6); pass < n_passes;
-         pass += (int64_t)gridDim.x * waves) {
-        int64_t r[PT];
-        int i[PT];
-        bool valid[PT];
+// 16 consecutive accumulator-shaped floats: registers 4g .. 4g+3 from p[8g .. 8g+3].
+__device__ __forceinline__ f32x16_t load_acc_rows(const float* p) {
+    f32x16_t v;
 #pragma unroll
-        for (int p = 0; p < PT; ++p) {                 // a second tile past the end computes on tile 0's data
-            const int64_t t = PT * pass + p;
-            const int64_t tt = t < n_tiles ? t : 0;
-            r[p] = tt / tiles_per_req;
-            i[p] = (int)(tt - r[p] * tiles_per_req) * 32 + n;
-            valid[p] = t < n_tiles && i[p] < A.N;
-        }
+    for (int g = 0; g < 4; ++g) {
+        const float4 q = *reinterpret_cast<const float4*>(p + 8 * g);
+        v[4 * g] = q.x; v[4 * g + 1] = q.y; v[4 * g + 2] = q.z; v[4 * g + 3] = q.w;
+    }
+    return v;
+}
 
-        // layer-1 B operands: the pairs' normalised bf16 rows
-        bf16x8_t xb[PT][4];
+// Tile = 2 requests x 16 instances (lane column n: request n/16, instance
+// n%16).  A wave scores two tiles per unit, of the same 16 instances, so every
+// LDS read of weights, partials, biases and head rows serves both.  All of
+// them sit in LDS (at h = 256: 8 + 128 KB of fragments, 16.6 KB of partials,
+// 3 KB of biases and head rows); the partials are reloaded when the
+// workgroup's units move on to the next instance group.
+template <int MT>
+__global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
+    constexpr int H = 32 * MT;                 // h1 = h2
+    constexpr int KS2 = 2 * MT;                // layer-2 k-steps: h1 / 16
+    constexpr int QS = H + 4;                  // padded LDS row of one instance's partials
+    constexpr int PT = 2;                      // tiles per wave and unit
+    __shared__ bf16x8_t lds_w1[MT * 64];
+    __shared__ bf16x8_t lds_w2[MT * KS2 * 64];
+    __shared__ bf16x8_t lds_hd[2 * KS2 * 4];   // [s][h][row], then as many zero fragments
+    __shared__ __attribute__((aligned(16))) float lds_b2[H];
+    __shared__ __attribute__((aligned(16))) float lds_q[kGroupInst * QS];
+    const int tid = threadIdx.x;
+    for (int f = tid; f < MT * 64; f += blockDim.x) lds_w1[f] = A.w1frag[f];
+    for (int f = tid; f < MT * KS2 * 64; f += blockDim.x) lds_w2[f] = A.w2frag[f];
+    for (int f = tid; f < 2 * KS2 * 4; f += blockDim.x) lds_hd[f] = f < KS2 * 4 ? A.hfrag[f] : bf16x8_t{};
+    for (int f = tid; f < H; f += blockDim.x) lds_b2[f] = A.b2[f];
+
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5, n = lane & 31;
+    const int ni = n & 15, nr = n >> 4;
+    const float b3 = A.b3[0];
+    // head A operand: rows 0 (w3) and 1 (|w3|) in lanes 0, 1, 32, 33; the other
+    // lanes read the zero fragments at the same offsets
+    const bf16x8_t* hdl = lds_hd + (n < 2 ? h * 2 + n : KS2 * 4);
+    const int64_t u_begin = (int64_t)blockIdx.x * A.n_units / gridDim.x;
+    const int64_t u_end = (int64_t)(blockIdx.x + 1) * A.n_units / gridDim.x;
+    int64_t g_loaded = -1;
+    for (int64_t u = u_begin; u < u_end; ++u) {
+        const int64_t g = u / A.n_rblocks;
+        const int64_t rb = u - g * A.n_rblocks;
+        if (g != g_loaded) {                   // workgroup-uniform
+            __syncthreads();
+            for (int e = tid; e < kGroupInst * H; e += blockDim.x) {
+                const int k = e / kGroupInst, q = e - k * kGroupInst;
+                const int64_t ii = g * kGroupInst + q;
+                lds_q[q * QS + k] = ii < A.N ? A.part_t[(int64_t)k * A.N + ii] : 0.0f;
+            }
+            __syncthreads();
+            g_loaded = g;
+        }
+        const int64_t i = g * kGroupInst + ni;
+        int64_t r[PT];
+        bool valid[PT];
+        bf16x8_t xb[PT];
 #pragma unroll
         for (int p = 0; p < PT; ++p) {
-            const int ii = valid[p] ? i[p] : 0;
+            r[p] = rb * kUnitReq + wave * (2 * PT) + 2 * p + nr;
+            valid[p] = r[p] < A.R && i < A.N;
+            const int64_t rr = valid[p] ? r[p] : 0, ii = valid[p] ? i : 0;
             float x[5], xt[5];
-            derived_columns(A.prompt_len[r[p]], A.req_off[r[p] + 1] - A.req_off[r[p]],
-                            valid[p] ? A.overlap[r[p] * A.N + ii] : 0, A.block_tokens, x);
-            normalise_tail<true>(x, A.mu, A.isig, D_INST, xt);
-            const bf16x8_t* row = reinterpret_cast<const bf16x8_t*>(A.xinst + (int64_t)ii * 64);
+            derived_columns(A.prompt_len[rr], A.req_off[rr + 1] - A.req_off[rr],
+                            valid[p] ? A.overlap[rr * A.N + ii] : 0, A.block_tokens, x);
+            normalise_tail<true>(x, A.mu, A.isig, A.d_inst, xt);
+            bf16x8_t v{};
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                bf16x8_t v = row[2 * s + h];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int c0 = 16 * s + j - D_INST;       // derived column held by half 0
-                    const int c1 = c0 + 8;                    // ... by half 1
-                    if (c0 >= 0 && c0 < 5 && h == 0) v[j] = (__bf16)xt[c0 < 5 ? c0 : 0];
-                    if (c1 >= 0 && c1 < 5 && h == 1) v[j] = (__bf16)xt[c1 < 5 ? c1 : 0];
-                }
-                xb[p][s] = valid[p] ? v : bf16x8_t{};
-            }
+            for (int c = 0; c < 5; ++c) v[c] = (__bf16)xt[c];
+            xb[p] = (valid[p] && h == 0) ? v : bf16x8_t{};
         }
 
-        // layer 1, one row tile at a time: acc = b1 + W1 x, then bf16(relu(.))
+        // layer 1, one row tile at a time: acc = partial + W1_tail x_tail, then bf16(relu(.))
+        const float* qrow = lds_q + ni * QS + 4 * h;
         bf16x8_t hb[PT][KS2];
 #pragma unroll
-        for (int mt = 0; mt < MT1; ++mt) {
-            const f32x16_t bias = load_bias(A.b1frag + (mt * 2 + h) * 16);
-            f32x16_t acc[PT];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const bf16x8_t a = w1l[(s * MT1 + mt) * 64];
-#pragma unroll
-                for (int p = 0; p < PT; ++p)
-                    acc[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xb[p][s], s == 0 ? bias : acc[p], 0, 0, 0);
-            }
+        for (int mt = 0; mt < MT; ++mt) {
+            const f32x16_t c0 = load_acc_rows(qrow + 32 * mt);
+            const bf16x8_t a = lds_w1[mt * 64 + lane];
 #pragma unroll
             for (int p = 0; p < PT; ++p) {
-                hb[p][2 * mt] = relu_pack(acc[p], 0);
-                hb[p][2 * mt + 1] = relu_pack(acc[p], 1);
+                const f32x16_t acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, xb[p], c0, 0, 0, 0);
+                hb[p][2 * mt] = relu_pack(acc, 0);
+                hb[p][2 * mt + 1] = relu_pack(acc, 1);
             }
         }
 
@@ -272,8 +241,9 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             hd[p][0] = h == 0 ? b3 : 0.0f;
         }
 #pragma unroll
-        for (int mt = 0; mt < MT2; ++mt) {
-            const f32x16_t bias = load_bias(A.b2frag + (mt * 2 + h) * 16);
+        for (int mt = 0; mt < MT; ++mt) {
+            const f32x16_t bias = load_acc_rows(lds_b2 + 32 * mt + 4 * h);
+            const bf16x8_t f0 = hdl[(2 * mt) * 4], f1 = hdl[(2 * mt + 1) * 4];
             // a per-row-tile base keeps every read within the 16-bit immediate
             // offset of ds_read; the empty asm hides its value from the
             // optimiser, which would otherwise hoist one address register per
@@ -295,7 +265,6 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
                 __builtin_amdgcn_sched_barrier(0);
                 a_cur = a_nxt;
             }
-            const bf16x8_t f0 = hf[(2 * mt) * 64], f1 = hf[(2 * mt + 1) * 64];
 #pragma unroll
             for (int p = 0; p < PT; ++p) {
                 hd[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0, relu_pack(acc[p], 0), hd[p], 0, 0, 0);
@@ -305,7 +274,7 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
 #pragma unroll
         for (int p = 0; p < PT; ++p) {
             if (h == 0 && valid[p]) {
-                const int64_t q = r[p] * A.N + i[p];
+                const int64_t q = r[p] * A.N + i;
                 A.scores[q] = hd[p][0];
                 A.errb[q] = A.band_rel * (hd[p][1] + fabsf(b3));
             }
@@ -318,28 +287,20 @@ bool mfma_supported(const ModelDims& m) {
            (m.h1 == 64 || m.h1 == 128 || m.h1 == 256) && m.h1 == m.h2;
 }
 
-template <int MT>
-static void launch_mfma_d(const MfmaArgs& a, int d, int64_t grid, hipStream_t s) {
-    if (d == 64) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 64>), dim3((uint32_t)grid), dim3(512), 0, s, a);
-    else if (d == 48) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 48>), dim3((uint32_t)grid), dim3(512), 0, s, a);
-    else if (d == 32) hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 32>), dim3((uint32_t)grid), dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((score_pairs_mfma_kernel<MT, MT, 16>), dim3((uint32_t)grid), dim3(512), 0, s, a);
-}
-
 hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, const float* frag32,
-                                   const float* compute, const uint16_t* xinst, const float* mu,
+                                   const float* compute, const float* part_t, const float* mu,
                                    const float* inv_sigma, int32_t R, int32_t N, const int64_t* req_off,
                                    const int32_t* prompt_len, const int32_t* overlap, float* scores, float* errb,
                                    int n_cu, hipStream_t s) {
+    if (R <= 0 || N <= 0) return hipSuccess;
     const MfmaLayout Lay = make_mfma_layout(m);
     MfmaArgs a;
     a.w1frag = reinterpret_cast<const bf16x8_t*>(frag16);
     a.w2frag = reinterpret_cast<const bf16x8_t*>(frag16 + Lay.w1_frags * 512);
     a.hfrag = reinterpret_cast<const bf16x8_t*>(frag16 + (Lay.w1_frags + Lay.w2_frags) * 512);
-    a.b1frag = frag32;
-    a.b2frag = frag32 + (m.h1 / 32) * 32;
+    a.b2 = frag32;
     a.b3 = compute + m.c_b3;
-    a.xinst = xinst;
+    a.part_t = part_t;
     a.mu = mu;
     a.isig = inv_sigma;
     a.req_off = req_off;
@@ -349,17 +310,19 @@ hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, c
     a.errb = errb;
     a.R = R;
     a.N = N;
-    a.d = m.d;
     a.d_inst = m.d_inst;
     a.block_tokens = m.block_tokens;
     a.band_rel = kBandRel;
-    const int64_t tiles = (int64_t)R * ((N + 31) / 32);
-    int64_t grid = (tiles + 15) / 16;                      // 8 waves of 2 tiles
-    if (grid > n_cu) grid = n_cu;
+    a.n_rblocks = ((int64_t)R + kUnitReq - 1) / kUnitReq;
+    a.n_units = (((int64_t)N + kGroupInst - 1) / kGroupInst) * a.n_rblocks;
+    int64_t grid = a.n_units < n_cu ? a.n_units : n_cu;
     if (grid < 1) grid = 1;
-    if (m.h1 == 256) launch_mfma_d<8>(a, m.d, grid, s);
-    else if (m.h1 == 128) launch_mfma_d<4>(a, m.d, grid, s);
-    else launch_mfma_d<2>(a, m.d, grid, s);
+    if (m.h1 == 256)
+        hipLaunchKernelGGL(score_pairs_mfma_kernel<8>, dim3((uint32_t)grid), dim3(512), 0, s, a);
+    else if (m.h1 == 128)
+        hipLaunchKernelGGL(score_pairs_mfma_kernel<4>, dim3((uint32_t)grid), dim3(512), 0, s, a);
+    else
+        hipLaunchKernelGGL(score_pairs_mfma_kernel<2>, dim3((uint32_t)grid), dim3(512), 0, s, a);
     return hipGetLastError();
 }
 

@@ -84,21 +84,27 @@ ModelDims make_dims(const ls_model_config& cfg);
 // frag16 (bf16 bits): W1 [4][h1/32] fragments, W2 [h2/32][h1/16] fragments and
 // head fragments [h2/16] (rows w3 and |w3|); a fragment is 64 lanes x 8 bf16.
 // frag32: b1 then b2 as [tile][lane half][16].
+// Fragment tables of the matrix-core scorer (bf16 part frag16, fp32 part frag32):
+//   W1 tail  one A fragment per layer-1 row tile, the 5 derived columns only
+//            (the instance columns are resumed from the per-instance partials)
+//   W2       A fragments [row tile][k-step]
+//   head     per k-step and lane half, the 8 inputs of rows w3 and |w3|
+//   b2       the layer-2 biases (fp32)
 struct MfmaLayout {
-    int d = 0, h1 = 0, h2 = 0;
+    int d = 0, d_inst = 0, h1 = 0, h2 = 0;
     int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0;
-    int64_t w1_frags = 0, w2_frags = 0, h_frags = 0, n16 = 0, n32 = 0;
+    int64_t w1_frags = 0, w2_frags = 0, n_head = 0, n16 = 0, n32 = 0;
 };
 
 inline MfmaLayout make_mfma_layout(const ModelDims& m) {
     MfmaLayout L;
-    L.d = m.d; L.h1 = m.h1; L.h2 = m.h2;
+    L.d = m.d; L.d_inst = m.d_inst; L.h1 = m.h1; L.h2 = m.h2;
     L.m_w1 = m.m_w1; L.m_b1 = m.m_b1; L.m_w2 = m.m_w2; L.m_b2 = m.m_b2; L.m_w3 = m.m_w3;
-    L.w1_frags = (int64_t)(m.h1 / 32) * 4;
+    L.w1_frags = m.h1 / 32;
     L.w2_frags = (int64_t)(m.h2 / 32) * (m.h1 / 16);
-    L.h_frags = m.h2 / 16;
-    L.n16 = (L.w1_frags + L.w2_frags + L.h_frags) * 512;
-    L.n32 = (int64_t)(m.h1 / 32 + m.h2 / 32) * 32;
+    L.n_head = (int64_t)(m.h2 / 16) * 32;
+    L.n16 = (L.w1_frags + L.w2_frags) * 512 + L.n_head;
+    L.n32 = m.h2;
     return L;
 }
 
@@ -202,10 +208,8 @@ hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* 
 
 hipError_t launch_prepare_mfma(const MfmaLayout& L, const float* master, uint16_t* frag16, float* frag32,
                                hipStream_t s);
-hipError_t launch_instance_rows(const ModelDims& m, const float* mu, const float* inv_sigma, const float* inst_feat,
-                                int32_t N, uint16_t* xinst, hipStream_t s);
 hipError_t launch_score_pairs_mfma(const ModelDims& m, const uint16_t* frag16, const float* frag32,
-                                   const float* compute, const uint16_t* xinst, const float* mu,
+                                   const float* compute, const float* part_t, const float* mu,
                                    const float* inv_sigma, int32_t R, int32_t N, const int64_t* req_off,
                                    const int32_t* prompt_len, const int32_t* overlap, float* scores, float* errb,
                                    int n_cu, hipStream_t s);

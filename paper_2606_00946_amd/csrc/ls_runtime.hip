@@ -694,7 +694,6 @@ size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool h
     if (!have_overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!have_scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
-        need += (size_t)round_up((int64_t)N * 64 * 2, 256);      // bf16 instance rows
         need += (size_t)round_up(pairs * 4, 256);                // error scales
         need += (size_t)round_up(pairs, 256);                    // candidate flags
         need += (size_t)round_up(pairs * 8, 256);                // candidate list
@@ -743,14 +742,12 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
     }
     LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     if (fast) {
-        uint16_t* xinst = w.take<uint16_t>((int64_t)N * 64);
         float* eb = w.take<float>(pairs);
         uint8_t* flags = w.take<uint8_t>(pairs);
         int64_t* list = w.take<int64_t>(pairs);
         uint32_t* count = w.take<uint32_t>(64);
-        LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_rows(m, c->mu, c->isig, inst_feat, N, xinst, s));
         LS_TIMED(c, K_SCORE_MFMA, s,
-                 ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, xinst, c->mu, c->isig, R, N, req_off,
+                 ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N, req_off,
                                              prompt_len, ov, sc, eb, c->n_cu, s));
         LS_TIMED(c, K_BAND, s, ls::launch_fill_u32(count, 0u, 1, s));
         LS_TIMED(c, K_BAND, s,
