@@ -168,8 +168,15 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     }
     has_empty = __syncthreads_or(has_empty);
     if (s == 0 && tid == 0) flags[i] = has_empty ? kFlagHasEmptyKey : 0u;
+    // streaming stores: the finished segment is not read again by this build,
+    // and keeping it out of L2 leaves room for the keys the instance's other
+    // segments are still scanning
     ulonglong2* dst = reinterpret_cast<ulonglong2*>(keys + (base[i] + b0) * kBucketKeys);
-    for (uint32_t x = tid; x < nbl * (kBucketKeys / 2); x += kSegThreads) dst[x] = seg2[x];
+    for (uint32_t x = tid; x < nbl * (kBucketKeys / 2); x += kSegThreads) {
+        const ulonglong2 v = seg2[x];
+        __builtin_nontemporal_store(v.x, &dst[x].x);
+        __builtin_nontemporal_store(v.y, &dst[x].y);
+    }
 }
 
 // Keys whose probe ran past their segment continue in the next segment.  If

@@ -123,14 +123,20 @@ def test_bf16_fast_decisions_equal_canonical_at_full_size():
     print(f"fast scores bitwise canonical: {same:.3f} of {a['scores'].size} pairs", flush=True)
 
 
-@pytest.mark.parametrize("base,R,N", [("large_batch", 37, 13), ("large_batch", 130, 65), ("large_batch", 2, 256),
-                                      ("homogeneous", 70, 45), ("homogeneous", 9, 300), ("tiny", 40, 33)])
-def test_bf16_matrix_core_ragged(base, R, N):
-    """The matrix-core scorers at each hidden width (256 and 128: W2-stationary,
-    64: LDS-streamed) on ragged shapes -- a partial last instance tile, fewer
-    tiles than CUs, more instances than one request's tiles -- with every
-    request checked: decisions and minima exact, scores within the band."""
+@pytest.mark.parametrize("base,R,N,cap", [("large_batch", 37, 13, None), ("large_batch", 130, 65, None),
+                                          ("large_batch", 2, 256, None), ("large_batch", 224, 640, 2000),
+                                          ("homogeneous", 70, 45, None), ("homogeneous", 9, 300, None),
+                                          ("tiny", 40, 33, None)])
+def test_bf16_matrix_core_ragged(base, R, N, cap):
+    """The matrix-core scorer at each hidden width (256, 128, 64) on ragged
+    shapes -- a partial last group of 16 instances, a partial last block of 32
+    requests, fewer units than CUs, and (224 x 640: 280 units on 256
+    workgroups) workgroups whose units span two instance groups, so that the
+    partials in LDS are reloaded mid-run -- with every request checked:
+    decisions and minima exact, scores within the band."""
     cfg = synth.dataclasses.replace(synth.CONFIGS[base], dtype="bf16", R=R, N=N)
+    if cap is not None:
+        cfg = synth.dataclasses.replace(cfg, capacity=(cap,))
     w = synth.generate(cfg)
     assert uses_fast_path(cfg.d, cfg.hidden, cfg.dtype)
     note(f"bf16 matrix-core ragged {base} d={cfg.d} h={cfg.hidden} R={R} N={N}")
