@@ -256,10 +256,15 @@ hipError_t launch_gather_rows(const int32_t* code, int32_t n, int d, const float
                               const float* bx, const float* by, float* ox, float* oy, hipStream_t s);
 hipError_t launch_scatter_rows(const int32_t* dst, int32_t n, int d, const float* x, const float* y, float* fx,
                                float* fy, hipStream_t s);
+// Candidates are decided in chunks of admission_chunk(nc): dcp holds
+// chunk x cap distances, dcc chunk x chunk, origin cap slots, row and redo cap,
+// rslots chunk + 1.
+int32_t admission_chunk(int32_t nc);
 hipError_t launch_admission(const float* a2, const float* t, const float* y_all, int32_t n0, int32_t nc, int H, int d,
                             int32_t cap, const float* cx, const float* cy, double* cemb, double* emb, float* rx,
                             float* ry, double* D, double* nnd, int32_t* nni, double* row, int32_t* redo,
-                            int32_t* admitted, hipStream_t s);
+                            int32_t* admitted, double* dcp, double* dcc, int32_t* origin, int32_t* rslots,
+                            hipStream_t s);
 hipError_t launch_loss_accumulate(const float* loss, double* acc, int reset, hipStream_t s);
 hipError_t launch_loss_finish(const double* acc, int32_t count, float* out, hipStream_t s);
 

@@ -1004,13 +1004,18 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
     const int32_t n_all = bf.rep_cap > 0 ? n0 + nc : 0;
     // workspace
     const int64_t f_fwd = n_all > 0 ? ls::forward_rows_floats(m, n_all) : 0;
+    const int64_t ch = nc > 0 ? ls::admission_chunk(nc) : 1;
+    const int64_t rcap = bf.rep_cap > 0 ? bf.rep_cap : 1;
     size_t need = (size_t)round_up((int64_t)(nc + B) * 4, 256)                       // codes
                   + (size_t)round_up((int64_t)(nc > 0 ? nc : 1) * (d + 1) * 4, 256)     // candidate rows
                   + (size_t)round_up((int64_t)(n_all > 0 ? n_all : 1) * (d + 1) * 4, 256)  // forward input
                   + (size_t)round_up(f_fwd * 4, 256)
                   + (size_t)round_up((int64_t)(nc > 0 ? nc : 1) * H * 8, 256)          // candidate embeddings
                   + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 4, 256) + 256
-                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 8, 256);          // distance row
+                  + (size_t)round_up((int64_t)(bf.rep_cap > 0 ? bf.rep_cap : 1) * 8, 256)           // distance row
+                  + (size_t)round_up(ch * rcap * 8, 256) + (size_t)round_up(ch * ch * 8, 256)     // chunk distances
+                  + (size_t)round_up(rcap * 4, 256)                                              // slot origins
+                  + (size_t)round_up((ch + 1) * 4, 256);                                         // slots taken
     int rc = grow(c, &bf.ws, &bf.ws_cap, need);
     if (rc) return rc;
     WsCarve w{(char*)bf.ws};
@@ -1024,6 +1029,10 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
     int32_t* redo = w.take<int32_t>(bf.rep_cap > 0 ? bf.rep_cap : 1);
     int32_t* adm = w.take<int32_t>(64);
     double* drow = w.take<double>(bf.rep_cap > 0 ? bf.rep_cap : 1);
+    double* dcp = w.take<double>(ch * rcap);
+    double* dcc = w.take<double>(ch * ch);
+    int32_t* origin = w.take<int32_t>(rcap);
+    int32_t* rslots = w.take<int32_t>(ch + 1);
     // stage the codes
     rc = stage_reserve(c, sizeof(int32_t) * (size_t)(nc + B) + 64);
     if (rc) return rc;
@@ -1046,7 +1055,8 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
                  ls::launch_forward_rows(m, train_model(c).compute, c->mu, c->isig, n_all, ax, fws, &a2, &t, s));
         LS_TIMED(c, K_BUFFER, s,
                  ls::launch_admission(a2, t, ay, n0, nc, H, d, bf.rep_cap, cx, cy, cemb, bf.emb, bf.rep_x, bf.rep_y,
-                                      bf.D, bf.nnd, bf.nni, drow, redo, admitted ? admitted : adm, s));
+                                      bf.D, bf.nnd, bf.nni, drow, redo, admitted ? admitted : adm, dcp, dcc,
+                                      origin, rslots, s));
     } else if (admitted) {
         LS_TIMED(c, K_BUFFER, s, ls::launch_fill_u32(reinterpret_cast<uint32_t*>(admitted), 0u, 1, s));
     }

@@ -71,6 +71,38 @@ def test_buffer_matches_oracle(name, F, P, n):
     ctx.close()
 
 
+@pytest.mark.parametrize("name,F,P,first,second", [("homogeneous", 64, 300, 1200, 700), ("large_batch", 40, 520, 900, 900)])
+def test_buffer_large_pushes(name, F, P, first, second):
+    """Pushes whose FIFO evictions exceed one admission chunk (256 candidates):
+    the pool fills and starts replacing members within one push, and later
+    chunks see slots taken by earlier ones.  Pool and FIFO exactly the oracle's."""
+    import torch
+    w = synth.generate(name)
+    cfg = w.cfg
+    mode = "bf16" if cfg.dtype == "bf16" else "fp32"
+    x, y = _stream(w, first + second)
+    ctx = _ctx(w)
+    ctx.ls_buffer_init(F, P)
+    ob = oracle.Buffer(cfg.d, F, P)
+    for a, b in ((0, first), (first, first + second)):
+        note(f"buffer {name} large push rows {a}..{b}")
+        adm = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ctx.ls_buffer_push(to_dev(x[a:b]), to_dev(y[a:b]), adm)
+        want_adm = oracle.buffer_push(mode, cfg.hidden, w.params, w.mu, w.inv_sigma, ob, x[a:b], y[a:b])
+        torch.cuda.synchronize()
+        assert tuple(ctx.ls_buffer_state()) == (int(ob.fifo_count[0]), int(ob.fifo_head[0]), int(ob.rep_count[0]))
+        fx, fy, rx, ry = (t.cpu().numpy() for t in ctx.ls_buffer_read())
+        wfx, wfy = ob.fifo_rows()
+        wrx, wry = ob.replay_rows()
+        np.testing.assert_array_equal(fx, wfx)
+        np.testing.assert_array_equal(fy, wfy)
+        np.testing.assert_array_equal(rx, wrx)
+        np.testing.assert_array_equal(ry, wry)
+        assert int(adm.item()) == want_adm
+        print(f"{name}: push of {b - a}, admitted {want_adm}, pool {int(ob.rep_count[0])}/{P}", flush=True)
+    ctx.close()
+
+
 def test_buffer_errors():
     import torch
     w = synth.generate("tiny")
