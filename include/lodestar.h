@@ -115,6 +115,8 @@ int ls_get_model(ls_ctx* ctx, float* params, int64_t n_params, float* mu, float*
  *                stream work.
  * The library builds one hash table per instance on the device.  Instance ids
  * are positions 0..N-1, shared with the rows of inst_feat in ls_score_batch.
+ * LS_ERR_UNSUPPORTED for 2^32 or more hashes in all (or, with capacities set,
+ * capacities summing to that).
  */
 int ls_load_cache_state(ls_ctx* ctx, int32_t n_instances, const int64_t* inst_off,
                         const uint64_t* hashes, void* stream);

@@ -11,8 +11,12 @@
 // Build.  Random 64-bit compare-and-swaps on an HBM-resident table move whole
 // cache lines in and out for every key, so the table is built in LDS instead:
 // one workgroup owns a segment of kSegBuckets consecutive buckets of one
-// instance (128 KiB), scans that instance's keys, and places the ones whose
-// home bucket lies in its segment.  A slot is claimed with one LDS add on the
+// instance (128 KiB) and places the keys whose home bucket lies in it.  The
+// keys reach their segment's workgroup through a partition: a counting pass
+// (segment of every key, LDS histograms, one global add per segment touched),
+// a scan of the counts, and a scatter of every key with its input position
+// into its segment's run -- so each key is read three times in all, instead of
+// once by every segment of its instance.  A slot is claimed with one LDS add on the
 // bucket's fill counter (slots fill in order 0..7; a full bucket sends the key
 // on to the next one) and written with one store; the finished segment goes
 // out with coalesced stores.  A key whose probe runs past the segment's last
@@ -111,24 +115,181 @@ __device__ __forceinline__ int32_t owner_of(const int64_t* __restrict__ off, int
 }
 
 constexpr int kSegThreads = 1024;
+constexpr int kPartThreads = 1024;
+constexpr int kPartPerThread = 8;              // consecutive keys per thread
+constexpr int64_t kPartChunk = (int64_t)kPartThreads * kPartPerThread;
+constexpr int kPartBins = 4096;                // LDS counters; wider segment ranges use global adds
+
+constexpr int kPartInst = 1024;                // instances a chunk may span with its table in LDS
+
+// Segment (global index) of every key of the chunk, counted (SCATTER false) or
+// scattered into the segments' runs (SCATTER true).  The workgroup first finds
+// the instances its chunk spans (one parallel pass over the offsets) and copies
+// their offsets, first segments and bucket counts to LDS; a thread then takes 8
+// consecutive keys and walks the instance boundaries from its first key.  In
+// the counting pass the all-ones key also sets its instance's flag (and
+// records its position in eidx).
+template <bool SCATTER>
+__global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __restrict__ hashes,
+                                                            const int64_t* __restrict__ inst_off,
+                                                            const int32_t* __restrict__ seg_off,
+                                                            const uint32_t* __restrict__ nbuckets, int32_t n_inst,
+                                                            int64_t total, uint32_t* __restrict__ seg_count,
+                                                            uint32_t* __restrict__ seg_cursor,
+                                                            uint64_t* __restrict__ part_key,
+                                                            uint32_t* __restrict__ part_idx,
+                                                            uint32_t* __restrict__ flags, int64_t* __restrict__ eidx) {
+    __shared__ uint32_t bin[kPartBins];
+    __shared__ int64_t l_off[kPartInst + 1];
+    __shared__ int32_t l_seg[kPartInst + 1];
+    __shared__ uint32_t l_nb[kPartInst];
+    __shared__ int32_t i_first, i_last;
+    const int64_t n_keys = inst_off[n_inst] < total ? inst_off[n_inst] : total;
+    const int64_t c0 = (int64_t)blockIdx.x * kPartChunk;
+    if (c0 >= n_keys) return;                                     // uniform
+    const int64_t c1 = c0 + kPartChunk < n_keys ? c0 + kPartChunk : n_keys;
+    // the instances holding positions c0 and c1 - 1 (each owned by exactly one non-empty instance)
+    for (int32_t i = threadIdx.x; i < n_inst; i += kPartThreads) {
+        const int64_t a = inst_off[i], b = inst_off[i + 1];
+        if (a <= c0 && c0 < b) i_first = i;
+        if (a <= c1 - 1 && c1 - 1 < b) i_last = i;
+    }
+    for (int x = threadIdx.x; x < kPartBins; x += kPartThreads) bin[x] = 0u;
+    __syncthreads();
+    const int32_t ilo = i_first, ihi = i_last;
+    const bool in_lds = ihi - ilo < kPartInst;
+    if (in_lds) {
+        for (int32_t x = threadIdx.x; x <= ihi - ilo + 1; x += kPartThreads) {
+            l_off[x] = inst_off[ilo + x];
+            l_seg[x] = seg_off[ilo + x];
+            if (x <= ihi - ilo) l_nb[x] = nbuckets[ilo + x];
+        }
+    }
+    __syncthreads();
+    const int32_t seg_lo = seg_off[ilo];
+    const bool local = seg_off[ihi + 1] - seg_lo <= kPartBins;
+    const int64_t t0 = c0 + (int64_t)threadIdx.x * kPartPerThread;
+    uint64_t key[kPartPerThread];
+    int32_t seg[kPartPerThread];
+    uint32_t rank[kPartPerThread];
+#pragma unroll
+    for (int u = 0; u < kPartPerThread; ++u) key[u] = t0 + u < c1 ? hashes[t0 + u] : kEmptyKey;
+    // instance of the first key, relative to ilo when the table is in LDS
+    int32_t i = 0;
+    if (t0 < c1) {
+        if (in_lds) {
+            int32_t lo = 0, hi = ihi - ilo + 1;                   // largest x with l_off[x] <= t0
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (l_off[mid] <= t0) lo = mid; else hi = mid;
+            }
+            i = lo;
+        } else {
+            i = owner_of(inst_off, n_inst, t0);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kPartPerThread; ++u) {
+        const int64_t t = t0 + u;
+        seg[u] = -1;
+        if (t >= c1) continue;
+        int32_t first_seg;
+        uint32_t nb;
+        if (in_lds) {
+            while (l_off[i + 1] <= t) ++i;                       // empty instances are skipped too
+            first_seg = l_seg[i];
+            nb = l_nb[i];
+        } else {
+            while (inst_off[i + 1] <= t) ++i;
+            first_seg = seg_off[i];
+            nb = nbuckets[i];
+        }
+        if (key[u] == kEmptyKey) {
+            if (!SCATTER) {
+                const int32_t gi = in_lds ? ilo + i : i;
+                atomicOr(&flags[gi], kFlagHasEmptyKey);
+                if (eidx) eidx[gi] = t;
+            }
+            continue;
+        }
+        seg[u] = first_seg + (int32_t)(bucket_of(key[u], nb) / kSegBuckets);
+        rank[u] = local ? atomicAdd(&bin[seg[u] - seg_lo], 1u) : 0u;
+        if (!local) {
+            if (SCATTER) {
+                const uint32_t pos = atomicAdd(&seg_cursor[seg[u]], 1u);
+                part_key[pos] = key[u];
+                part_idx[pos] = (uint32_t)t;
+            } else {
+                atomicAdd(&seg_count[seg[u]], 1u);
+            }
+            seg[u] = -1;
+        }
+    }
+    if (!local) return;                                           // uniform
+    __syncthreads();
+    const int32_t nb_local = seg_off[ihi + 1] - seg_lo;
+    for (int x = threadIdx.x; x < nb_local; x += kPartThreads) {
+        const uint32_t cnt = bin[x];
+        if (cnt == 0u) continue;
+        if (SCATTER) bin[x] = atomicAdd(&seg_cursor[seg_lo + x], cnt);   // this chunk's first position in the run
+        else atomicAdd(&seg_count[seg_lo + x], cnt);
+    }
+    if (!SCATTER) return;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kPartPerThread; ++u) {
+        if (seg[u] < 0) continue;
+        const uint32_t pos = bin[seg[u] - seg_lo] + rank[u];
+        part_key[pos] = key[u];
+        part_idx[pos] = (uint32_t)(t0 + u);
+    }
+}
+
+// Exclusive scan of the n_seg counts into run starts (seg_count[n_seg] gets
+// the total); the scatter's cursors start at the run starts.  Also the
+// instance of every segment, for the segment build.
+__global__ __launch_bounds__(1024) void part_scan_kernel(int32_t n_seg, uint32_t* __restrict__ seg_count,
+                                                         uint32_t* __restrict__ seg_cursor,
+                                                         const int32_t* __restrict__ seg_off, int32_t n_inst,
+                                                         int32_t* __restrict__ seg_inst) {
+    for (int32_t i = threadIdx.x; i < n_inst; i += blockDim.x)
+        for (int32_t x = seg_off[i]; x < seg_off[i + 1]; ++x) seg_inst[x] = i;
+    __shared__ uint32_t part[1024];
+    __shared__ uint32_t carry;
+    if (threadIdx.x == 0) carry = 0u;
+    __syncthreads();
+    for (int32_t b0 = 0; b0 < n_seg; b0 += 1024) {
+        const int32_t x = b0 + (int32_t)threadIdx.x;
+        const uint32_t v = x < n_seg ? seg_count[x] : 0u;
+        part[threadIdx.x] = v;
+        __syncthreads();
+        for (int dd = 1; dd < 1024; dd <<= 1) {                   // inclusive Hillis-Steele scan
+            const uint32_t add = threadIdx.x >= (unsigned)dd ? part[threadIdx.x - dd] : 0u;
+            __syncthreads();
+            part[threadIdx.x] += add;
+            __syncthreads();
+        }
+        if (x < n_seg) {
+            const uint32_t start = carry + part[threadIdx.x] - v;
+            seg_count[x] = start;
+            seg_cursor[x] = start;
+        }
+        __syncthreads();
+        if (threadIdx.x == 1023) carry += part[1023];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) seg_count[n_seg] = carry;
+}
 
 __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     uint64_t* __restrict__ keys, const int64_t* __restrict__ base, const uint32_t* __restrict__ nbuckets,
-    uint32_t* __restrict__ flags, const int64_t* __restrict__ inst_off, const int32_t* __restrict__ seg_off,
-    int32_t n_inst, const uint64_t* __restrict__ hashes, int64_t* __restrict__ ovf, uint32_t* __restrict__ ovf_count,
-    uint32_t ovf_cap, uint32_t* __restrict__ entry_of, int64_t* __restrict__ eidx) {
+    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_inst, const uint32_t* __restrict__ run_start,
+    const uint64_t* __restrict__ part_key, const uint32_t* __restrict__ part_idx, int64_t* __restrict__ ovf,
+    uint32_t* __restrict__ ovf_count, uint32_t ovf_cap, uint32_t* __restrict__ entry_of) {
     __shared__ uint64_t seg[kSegBuckets * kBucketKeys];
     __shared__ uint32_t fill[kSegBuckets];
-    // Workgroups are dealt to the 8 XCDs round-robin; renumber them so that the
-    // segments of one instance run on one XCD and share its L2 copy of the keys.
-    const uint32_t G = gridDim.x, G8 = G / 8, w = blockIdx.x;
-    const uint32_t L = (w < G8 * 8) ? (w % 8) * G8 + w / 8 : w;
-    int32_t lo = 0, hi = n_inst;                    // the instance: largest i with seg_off[i] <= L
-    while (hi - lo > 1) {
-        const int32_t mid = (lo + hi) >> 1;
-        if ((uint32_t)seg_off[mid] <= L) lo = mid; else hi = mid;
-    }
-    const int32_t i = lo;
+    const uint32_t L = blockIdx.x;
+    const int32_t i = seg_inst[L];
     const uint32_t s = L - (uint32_t)seg_off[i];
     const uint32_t nb = nbuckets[i];
     const uint32_t b0 = s * kSegBuckets;
@@ -141,36 +302,20 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     for (uint32_t x = tid; x < nbl; x += kSegThreads) fill[x] = 0u;
     __syncthreads();
 
-    const int64_t t0 = inst_off[i], t1 = inst_off[i + 1];
-    int has_empty = 0;
-    for (int64_t t = t0 + tid; t < t1; t += 4 * kSegThreads) {
-        uint64_t k[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) k[u] = (t + u * kSegThreads < t1) ? hashes[t + u * kSegThreads] : kEmptyKey;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            if (t + u * kSegThreads >= t1) continue;
-            if (k[u] == kEmptyKey) {
-                has_empty = 1;
-                if (eidx) eidx[i] = t + u * kSegThreads;
-                continue;
-            }
-            const uint32_t lb = bucket_of(k[u], nb) - b0;
-            if (lb >= nbl) continue;                // home bucket in another segment
-            const int32_t ls = segment_place(seg, fill, lb, nbl, k[u]);
-            if (ls < 0) {
-                const uint32_t pos = atomicAdd(ovf_count, 1u);
-                if (pos < ovf_cap) ovf[pos] = t + u * kSegThreads;
-            } else if (entry_of) {
-                entry_of[(base[i] + b0) * kBucketKeys + ls] = (uint32_t)(t + u * kSegThreads);
-            }
+    const uint32_t r0 = run_start[L], r1 = run_start[L + 1];
+    for (uint32_t q = r0 + tid; q < r1; q += kSegThreads) {
+        const uint64_t key = part_key[q];
+        const uint32_t lb = bucket_of(key, nb) - b0;
+        const int32_t ls = segment_place(seg, fill, lb, nbl, key);
+        if (ls < 0) {
+            const uint32_t pos = atomicAdd(ovf_count, 1u);
+            if (pos < ovf_cap) ovf[pos] = part_idx[q];
+        } else if (entry_of) {
+            entry_of[(base[i] + b0) * kBucketKeys + ls] = part_idx[q];
         }
     }
-    has_empty = __syncthreads_or(has_empty);
-    if (s == 0 && tid == 0) flags[i] = has_empty ? kFlagHasEmptyKey : 0u;
-    // streaming stores: the finished segment is not read again by this build,
-    // and keeping it out of L2 leaves room for the keys the instance's other
-    // segments are still scanning
+    __syncthreads();
+    // streaming stores: the finished segment is not read again by this build
     ulonglong2* dst = reinterpret_cast<ulonglong2*>(keys + (base[i] + b0) * kBucketKeys);
     for (uint32_t x = tid; x < nbl * (kBucketKeys / 2); x += kSegThreads) {
         const ulonglong2 v = seg2[x];
@@ -212,19 +357,75 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
 
 int64_t table_overflow_capacity(int64_t total) { return 4096 + total / 64; }
 
+// Workspace: overflow counter (256 B) and queue, segment counts and cursors,
+// partitioned keys and their input positions.
+struct BuildWs {
+    uint32_t* ovf_count;
+    int64_t* ovf;
+    uint32_t* seg_count;
+    uint32_t* seg_cursor;
+    int32_t* seg_inst;
+    uint64_t* part_key;
+    uint32_t* part_idx;
+};
+
+static BuildWs carve_build_ws(void* ws, int64_t total, int32_t n_seg) {
+    char* p = static_cast<char*>(ws);
+    auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+    BuildWs w;
+    w.ovf_count = reinterpret_cast<uint32_t*>(p);
+    p += 256;
+    w.ovf = reinterpret_cast<int64_t*>(p);
+    p += up(8 * table_overflow_capacity(total));
+    w.seg_count = reinterpret_cast<uint32_t*>(p);
+    p += up(4 * ((int64_t)n_seg + 1));
+    w.seg_cursor = reinterpret_cast<uint32_t*>(p);
+    p += up(4 * ((int64_t)n_seg + 1));
+    w.seg_inst = reinterpret_cast<int32_t*>(p);
+    p += up(4 * ((int64_t)n_seg + 1));
+    w.part_key = reinterpret_cast<uint64_t*>(p);
+    p += up(8 * (total > 0 ? total : 1));
+    w.part_idx = reinterpret_cast<uint32_t*>(p);
+    return w;
+}
+
+int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg) {
+    auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+    const int64_t t = total > 0 ? total : 1;
+    return 256 + up(8 * table_overflow_capacity(total)) + 3 * up(4 * ((int64_t)n_seg + 1)) + up(8 * t) + up(4 * t);
+}
+
 hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
-                              const uint64_t* hashes, int64_t total, int32_t n_inst, void* ovf_ws, int n_cu,
+                              const uint64_t* hashes, int64_t total, int32_t n_inst, void* ws, int n_cu,
                               hipStream_t s, uint32_t* entry_of, int64_t* eidx) {
-    uint32_t* count = reinterpret_cast<uint32_t*>(ovf_ws);
-    int64_t* list = reinterpret_cast<int64_t*>(static_cast<char*>(ovf_ws) + 256);
+    const BuildWs w = carve_build_ws(ws, total, n_seg);
     const uint32_t cap = (uint32_t)table_overflow_capacity(total);
-    hipError_t e = launch_fill_u32(count, 0u, 1, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(table_segment_kernel, dim3((uint32_t)n_seg), dim3(kSegThreads), 0, s, t.keys, t.base,
-                       t.nbuckets, t.flags, inst_off, seg_off, n_inst, hashes, list, count, cap, entry_of, eidx);
+    hipError_t e;
+    if ((e = launch_fill_u32(w.ovf_count, 0u, 1, s)) != hipSuccess) return e;
+    if ((e = launch_fill_u32(w.seg_count, 0u, (int64_t)n_seg + 1, s)) != hipSuccess) return e;
+    if ((e = launch_fill_u32(t.flags, 0u, n_inst, s)) != hipSuccess) return e;
+    const uint32_t chunks = (uint32_t)((total + kPartChunk - 1) / kPartChunk);
+    if (chunks > 0) {
+        hipLaunchKernelGGL(part_kernel<false>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
+                           t.nbuckets, n_inst, total, w.seg_count, w.seg_cursor, w.part_key, w.part_idx, t.flags, eidx);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, n_seg, w.seg_count, w.seg_cursor, seg_off, n_inst,
+                       w.seg_inst);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (chunks > 0) {
+        hipLaunchKernelGGL(part_kernel<true>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
+                           t.nbuckets, n_inst, total, w.seg_count, w.seg_cursor, w.part_key, w.part_idx, t.flags, eidx);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (n_seg > 0) {
+        hipLaunchKernelGGL(table_segment_kernel, dim3((uint32_t)n_seg), dim3(kSegThreads), 0, s, t.keys, t.base,
+                           t.nbuckets, seg_off, w.seg_inst, w.seg_count, w.part_key, w.part_idx, w.ovf, w.ovf_count,
+                           cap, entry_of);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(table_overflow_kernel, dim3((uint32_t)(4 * n_cu)), dim3(256), 0, s, t.keys, t.base,
-                       t.nbuckets, inst_off, n_inst, hashes, total, list, count, cap, entry_of);
+                       t.nbuckets, inst_off, n_inst, hashes, total, w.ovf, w.ovf_count, cap, entry_of);
     return hipGetLastError();
 }
 

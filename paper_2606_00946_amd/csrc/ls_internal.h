@@ -119,12 +119,14 @@ bool mfma_supported(const ModelDims& m);
 // ---------------------------------------------------------------------------
 hipError_t launch_fill_u64(uint64_t* p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t s);
-// Table build: one workgroup per segment of kSegBuckets buckets (seg_off[i] is
-// the first segment of instance i, n_seg the total), then a global pass over
-// the keys that overflowed their segment.  ovf_ws holds a counter (first 256
-// bytes) and table_overflow_capacity(total) int64 key indices.
+// Table build: the keys partitioned by segment of kSegBuckets buckets (seg_off[i]
+// is the first segment of instance i, n_seg the total), one workgroup per
+// segment, then a global pass over the keys that overflowed their segment.  The
+// workspace (table_build_workspace_bytes) holds the partition and an overflow
+// queue of table_overflow_capacity(total) key indices; key indices are 32-bit.
 constexpr uint32_t kSegBuckets = 2048;
 int64_t table_overflow_capacity(int64_t total);
+int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg);
 // Prefix-index maintenance (k_index.hip).  One commit of a routed batch.
 constexpr int64_t kSelChunk = 4096;           // candidates per selection chunk
 struct IndexCommit {

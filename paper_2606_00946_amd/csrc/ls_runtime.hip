@@ -48,7 +48,7 @@ struct ls_ctx {
     int32_t inst_cap = 0;
     int64_t* inst_off_dev = nullptr;
     int32_t* seg_off_dev = nullptr;    // [N + 1] first table segment of each instance
-    void* tws = nullptr;               // table-build overflow queue
+    void* tws = nullptr;               // table-build workspace: key partition, overflow queue
     size_t tws_cap = 0;
     int64_t tables_nseg = 0;           // table segments of the loaded layout
     bool have_cache = false;
@@ -524,7 +524,7 @@ int index_load(ls_ctx* c, int32_t N, int64_t total, int64_t list_entries, const 
     if ((rc = grow(c, (void**)&X.small, &X.small_cap, sizeof(int64_t) * (size_t)(kIndexSmallPerN * N + 4))))
         return rc;
     if ((rc = grow(c, &X.ws, &X.ws_cap, (size_t)(total > 0 ? total : 1)))) return rc;
-    const size_t tw = 256 + sizeof(int64_t) * (size_t)ls::table_overflow_capacity(list_entries);
+    const size_t tw = (size_t)ls::table_build_workspace_bytes(list_entries, (int32_t)c->tables_nseg);
     if ((rc = grow(c, &c->tws, &c->tws_cap, tw))) return rc;
     X.list_entries = list_entries;
     IndexSmall m = index_small(X.small, N);
@@ -574,6 +574,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
         if (inst_off[i + 1] < inst_off[i]) return fail(c, LS_ERR_INVALID, "inst_off decreases at %d", i);
     const int64_t total = inst_off[n_instances];
     if (total > 0 && !hashes) return fail(c, LS_ERR_INVALID, "hashes is NULL");
+    if (total >= ((int64_t)1 << 32)) return fail(c, LS_ERR_UNSUPPORTED, "more than 2^32 - 1 cached blocks");
     DeviceScope dev(c->device);
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
@@ -602,12 +603,14 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
         if (nseg > 0x7fffffff) return fail(c, LS_ERR_UNSUPPORTED, "cache state too large");
     }
     seg_off[N] = (int32_t)nseg;
+    if (list_entries >= ((int64_t)1 << 32))
+        return fail(c, LS_ERR_UNSUPPORTED, "capacities above 2^32 - 1 cached blocks in all");
     // device buffers
     size_t cap = (size_t)c->table_cap_buckets * ls::kBucketKeys * sizeof(uint64_t);
     int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t));
     if (rc) return rc;
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
-    rc = grow(c, &c->tws, &c->tws_cap, 256 + sizeof(int64_t) * (size_t)ls::table_overflow_capacity(total));
+    rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg));
     if (rc) return rc;
     if (N > c->inst_cap) {
         LS_HIP(c, hipDeviceSynchronize());
