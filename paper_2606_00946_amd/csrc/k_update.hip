@@ -208,6 +208,24 @@ enum DenseMode { kFwdRelu = 0, kFwdHead = 1, kBackprop = 2 };
 // kDenseSpl chains.
 constexpr int kDenseSpl = 2;
 
+// The end of one chain of the three products above: sample b, output unit o,
+// element e = o * B + b of the feature-major outputs.
+template <bool BF, int MODE>
+__device__ __forceinline__ void dense_store(float acc, int64_t e, int64_t b, int o, const float* __restrict__ zmask,
+                                            float* __restrict__ z, float* __restrict__ a, const DropArgs& D,
+                                            int layer) {
+    if (MODE == kFwdRelu) {
+        z[e] = acc;
+        const float h = apply_drop(D, layer, b, o, relu_u(acc));
+        a[e] = BF ? q_bf16(h) : h;
+    } else if (MODE == kFwdHead) {
+        z[e] = acc;
+    } else {
+        const float v = apply_drop(D, layer, b, o, zmask[e] > 0.0f ? acc : 0.0f);
+        z[e] = BF ? q_bf16(v) : v;
+    }
+}
+
 template <bool BF, int MODE, int U>
 __device__ __forceinline__ void dense_units(const float* __restrict__ in, const float* __restrict__ wl,
                                             const float* __restrict__ bias, const float* __restrict__ zmask,
@@ -253,19 +271,8 @@ __device__ __forceinline__ void dense_units(const float* __restrict__ in, const 
     for (int j = 0; j < P; ++j) {
         if (!valid[j]) continue;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t e = (int64_t)(o0 + u) * B + b[j];
-            if (MODE == kFwdRelu) {
-                z[e] = acc[j][u];
-                const float h = apply_drop(D, layer, b[j], o0 + u, relu_u(acc[j][u]));
-                a[e] = BF ? q_bf16(h) : h;
-            } else if (MODE == kFwdHead) {
-                z[e] = acc[j][u];
-            } else {
-                const float v = apply_drop(D, layer, b[j], o0 + u, zmask[e] > 0.0f ? acc[j][u] : 0.0f);
-                z[e] = BF ? q_bf16(v) : v;
-            }
-        }
+        for (int u = 0; u < U; ++u)
+            dense_store<BF, MODE>(acc[j][u], (int64_t)(o0 + u) * B + b[j], b[j], o0 + u, zmask, z, a, D, layer);
     }
 }
 
@@ -306,6 +313,44 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
     if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 4; }
     if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 2; }
     if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 1; }
+}
+
+// The same products for small batches, where a workgroup per 32 output units
+// and 512 samples leaves most CUs idle: one thread per (sample, output unit),
+// 64 units by 4 samples per workgroup, the weights read from the compute copy
+// (L2-resident) and the inputs as wave-uniform loads.  Same chains, same order.
+constexpr int kDenseSmallWgs = 256;            // below this many lane-path workgroups
+
+template <bool BF, int MODE>
+__global__ __launch_bounds__(256) void dense_small_kernel(const float* __restrict__ in, const float* __restrict__ wt,
+                                                          const float* __restrict__ bias,
+                                                          const float* __restrict__ zmask, float* __restrict__ z,
+                                                          float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
+                                                          int layer) {
+    const int o = (int)blockIdx.x * 64 + (int)(threadIdx.x & 63);
+    const int64_t b = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6);
+    if (o >= O || b >= B) return;
+    float acc = MODE == kBackprop ? 0.0f : bias[o];
+    int k = 0;
+    for (; k + 8 <= K; k += 8) {
+        float w[8], x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            w[e] = MODE == kBackprop ? wt[(int64_t)o * K + k + e] : wt[(int64_t)(k + e) * O + o];
+            x[e] = in[(int64_t)(k + e) * B + b];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = __builtin_fmaf(w[e], x[e], acc);
+    }
+    for (; k < K; ++k) {
+        const float w = MODE == kBackprop ? wt[(int64_t)o * K + k] : wt[(int64_t)k * O + o];
+        acc = __builtin_fmaf(w, in[(int64_t)k * B + b], acc);
+    }
+    dense_store<BF, MODE>(acc, (int64_t)o * B + b, b, o, zmask, z, a, D, layer);
+}
+
+static bool dense_small(int32_t B, int O) {
+    return (int64_t)((B + 256 * kDenseSpl - 1) / (256 * kDenseSpl)) * ((O + 31) / 32) < kDenseSmallWgs;
 }
 
 // ---------------------------------------------------------------------------
@@ -764,7 +809,10 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
     for (int l = 0; l < m.L; ++l) {
         const float* in = l == 0 ? xn : a[l - 1];
         const int K = m.in_of(l), O = m.h[l];
-        if (lds_w)
+        if (lds_w && dense_small(B, O))
+            hipLaunchKernelGGL((dense_small_kernel<BF, kFwdRelu>), dim3((O + 63) / 64, blocks_for(nB, 4)), dim3(256), 0,
+                               s, in, compute + m.c_wt[l], compute + m.c_bl[l], nullptr, z[l], a[l], B, K, O, D, l);
+        else if (lds_w)
             hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + 31) / 32), dim3(256), 0, s, in,
                                compute + m.c_wt[l], compute + m.c_bl[l], nullptr, z[l], a[l], B, K, O, D, l);
         else
@@ -919,7 +967,11 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         if (l == 0) break;
         // dL/dz of layer l - 1 = (W_l^T dL/dz_l), masked by z_{l-1} > 0 and dropout
         const int Kp = m.h[l - 1];
-        if (lds_w)
+        if (lds_w && dense_small(B, Kp))
+            hipLaunchKernelGGL((dense_small_kernel<BF, kBackprop>), dim3((Kp + 63) / 64, blocks_for(nB, 4)), dim3(256),
+                               0, s, w.dl[l], compute + m.c_wt[l], nullptr, w.z[l - 1], w.dl[l - 1], nullptr, B, O, Kp,
+                               D, l - 1);
+        else if (lds_w)
             hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + 31) / 32), dim3(256), 0, s, w.dl[l],
                                compute + m.c_wt[l], nullptr, w.z[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
         else
