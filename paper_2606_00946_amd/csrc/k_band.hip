@@ -288,7 +288,6 @@ hipError_t launch_rescore(const ModelDims& m, const float* compute, const float*
         return hipGetLastError();
     }
     // enough lanes for about two candidates per request, capped at 8 waves per SIMD
-    // enough lanes for about two candidates per request, capped at 8 waves per SIMD
     int64_t want = ((int64_t)R * 2 + 255) / 256;
     int64_t cap = (int64_t)n_cu * 8;
     int64_t grid = want < cap ? want : cap;

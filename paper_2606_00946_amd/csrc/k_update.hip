@@ -317,8 +317,9 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
 
 // The same products for small batches, where a workgroup per 32 output units
 // and 512 samples leaves most CUs idle: one thread per (sample, output unit),
-// 64 units by 4 samples per workgroup, the weights read from the compute copy
-// (L2-resident) and the inputs as wave-uniform loads.  Same chains, same order.
+// 64 units by 4 samples per workgroup (the head, one unit: 256 samples), the
+// weights read from the compute copy (L2-resident) and the inputs as
+// wave-uniform loads.  Same chains, same order.
 constexpr int kDenseSmallWgs = 256;            // below this many lane-path workgroups
 
 template <bool BF, int MODE>
@@ -327,8 +328,9 @@ __global__ __launch_bounds__(256) void dense_small_kernel(const float* __restric
                                                           const float* __restrict__ zmask, float* __restrict__ z,
                                                           float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
                                                           int layer) {
-    const int o = (int)blockIdx.x * 64 + (int)(threadIdx.x & 63);
-    const int64_t b = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6);
+    const int o = MODE == kFwdHead ? 0 : (int)blockIdx.x * 64 + (int)(threadIdx.x & 63);
+    const int64_t b = MODE == kFwdHead ? (int64_t)blockIdx.y * 256 + threadIdx.x
+                                       : (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6);
     if (o >= O || b >= B) return;
     float acc = MODE == kBackprop ? 0.0f : bias[o];
     int k = 0;
@@ -820,7 +822,10 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
                                compute + m.c_wt[l], compute + m.c_bl[l], z[l], a[l], B, K, O, D, l);
     }
     const float* last = a[m.L - 1];
-    if (lds_w)
+    if (lds_w && dense_small(B, 1))
+        hipLaunchKernelGGL((dense_small_kernel<BF, kFwdHead>), dim3(1, blocks_for(nB, 256)), dim3(256), 0, s, last,
+                           compute + m.c_wt[m.L], compute + m.c_bl[m.L], nullptr, t, nullptr, B, m.hl, 1, D, m.L);
+    else if (lds_w)
         hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdHead>), dim3(sbd, 1), dim3(256), 0, s, last,
                            compute + m.c_wt[m.L], compute + m.c_bl[m.L], nullptr, t, nullptr, B, m.hl, 1, D, m.L);
     else
