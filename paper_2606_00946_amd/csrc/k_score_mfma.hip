@@ -10,7 +10,10 @@
 //            weights of the 5 derived columns, B = the pair's bf16 derived
 //            columns: one k-step instead of d/16
 //   layer 2  A = W2 fragments (LDS), B = bf16(relu(layer-1 accumulators)), C = b2
-//   head     A = [w3; |w3|; 0...], B = bf16(relu(layer-2 accumulators))
+//   head     v_mfma_f32_16x16x32_bf16, A = [w3; |w3|; 0...], B = bf16(relu(layer-2
+//            accumulators)) regrouped by v_permlane16_swap from the 32x32
+//            B layout (16 units of one pair per lane half) into the 16x16x32 one
+//            (8 units per 16-lane row), one row tile (K = 32) per instruction
 // An accumulator of a 32x32 tile holds, in lane l and register r, unit
 // 8(r/4) + 4(l/32) + r%4 of pair l%32.  The next layer's B operand needs, in
 // lane l, eight consecutive k of pair l%32 -- so each layer's inputs are taken
@@ -34,6 +37,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Input unit addressed by k-step s, lane half h, slot j of a B operand built
 // straight from the previous layer's accumulators (s = 2*m_tile + half).
@@ -69,11 +73,13 @@ __global__ void prepare_mfma_kernel(MfmaLayout L, const float* __restrict__ mast
             v = W2[(int64_t)(32 * mt2 + m) * h1 + perm_unit(s, h, j)];
         }
         frag16[t] = bf16_bits(v);
-    } else if (t < L.n16) {                              // head [s(h2/16)][h][row][j]: row 0 w3, row 1 |w3|
+    } else if (t < L.n16) {                              // head [mt][g][row][j]: row 0 w3, row 1 |w3|
+        // the 16x16x32 A operand of row tile mt: k-group g holds the units of
+        // k-step 2mt + (g & 1), lane half g >> 1 of the 32x32 B layout
         const int64_t e = t - nfrag;
-        const int j = (int)(e & 7), row = (int)((e >> 3) & 1), h = (int)((e >> 4) & 1);
-        const int s = (int)(e >> 5);
-        const float w = W3[perm_unit(s, h, j)];
+        const int j = (int)(e & 7), row = (int)((e >> 3) & 1), g = (int)((e >> 4) & 3);
+        const int mt = (int)(e >> 6);
+        const float w = W3[perm_unit(2 * mt + (g & 1), g >> 1, j)];
         frag16[t] = bf16_bits(row == 0 ? w : fabsf(w));
     } else if (t < L.n16 + L.n32) {                      // b2
         frag32[t - L.n16] = master[L.m_b2 + (t - L.n16)];
@@ -165,7 +171,7 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     constexpr int PT = 2;                      // tiles per wave and unit
     __shared__ bf16x8_t lds_w1[MT * 64];
     __shared__ bf16x8_t lds_w2[MT * KS2 * 64];
-    __shared__ bf16x8_t lds_hd[2 * KS2 * 4];   // [s][h][row], then as many zero fragments
+    __shared__ bf16x8_t lds_hd[2 * KS2 * 4];   // [mt][g][row], then as many zero fragments
     __shared__ __attribute__((aligned(16))) float lds_b2[H];
     __shared__ __attribute__((aligned(16))) float lds_q[kGroupInst * QS];
     const int tid = threadIdx.x;
@@ -179,9 +185,11 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     const int h = lane >> 5, n = lane & 31;
     const int ni = n & 15, nr = n >> 4;
     const float b3 = A.b3[0];
-    // head A operand: rows 0 (w3) and 1 (|w3|) in lanes 0, 1, 32, 33; the other
-    // lanes read the zero fragments at the same offsets
-    const bf16x8_t* hdl = lds_hd + (n < 2 ? h * 2 + n : KS2 * 4);
+    // head A operand (16x16x32): lane l holds row l % 16, k-group l / 16; rows 0
+    // (w3) and 1 (|w3|) come from the table, the other lanes read the zero
+    // fragments at the same offsets
+    const int hrow = lane & 15, hgrp = lane >> 4;
+    const bf16x8_t* hdl = lds_hd + (hrow < 2 ? hgrp * 2 + hrow : KS2 * 4);
     const int64_t u_begin = (int64_t)blockIdx.x * A.n_units / gridDim.x;
     const int64_t u_end = (int64_t)(blockIdx.x + 1) * A.n_units / gridDim.x;
     int64_t g_loaded = -1;
@@ -234,16 +242,18 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
 
         // layer 2, one row tile at a time, each fed straight into the head:
         // row 0 = t, row 1 = sum_j |w3_j| h2_j
-        f32x16_t hd[PT];
+        // two 16x16 head tiles per pair tile: pairs 0-15 (its first request) and
+        // 16-31 (its second); row 0 = t, row 1 = sum_j |w3_j| h2_j, in lanes 0-15
+        f32x4_t hd[PT][2];
 #pragma unroll
         for (int p = 0; p < PT; ++p) {
-            hd[p] = f32x16_t{};
-            hd[p][0] = h == 0 ? b3 : 0.0f;
+            hd[p][0] = f32x4_t{lane < 16 ? b3 : 0.0f, 0.0f, 0.0f, 0.0f};
+            hd[p][1] = hd[p][0];
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const f32x16_t bias = load_acc_rows(lds_b2 + 32 * mt + 4 * h);
-            const bf16x8_t f0 = hdl[(2 * mt) * 4], f1 = hdl[(2 * mt + 1) * 4];
+            const bf16x8_t fh = hdl[mt * 8];
             // a per-row-tile base keeps every read within the 16-bit immediate
             // offset of ds_read; the empty asm hides its value from the
             // optimiser, which would otherwise hoist one address register per
@@ -267,16 +277,39 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             }
 #pragma unroll
             for (int p = 0; p < PT; ++p) {
-                hd[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f0, relu_pack(acc[p], 0), hd[p], 0, 0, 0);
-                hd[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f1, relu_pack(acc[p], 1), hd[p], 0, 0, 0);
+                // 16-lane rows of x0: units of k-step 2mt, half 0, of pairs 0-15 and
+                // of 16-31, then half 1 of each; x1 the same for k-step 2mt + 1.  The
+                // swap puts pairs 0-15's four 8-unit groups into b0, 16-31's into b1.
+                const bf16x8_t x0 = relu_pack(acc[p], 0), x1 = relu_pack(acc[p], 1);
+                uint32_t w0[4], w1[4];
+                __builtin_memcpy(w0, &x0, sizeof w0);
+                __builtin_memcpy(w1, &x1, sizeof w1);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const auto sw = __builtin_amdgcn_permlane16_swap(w0[k], w1[k], false, false);
+                    w0[k] = sw[0];
+                    w1[k] = sw[1];
+                }
+                bf16x8_t b0, b1;
+                __builtin_memcpy(&b0, w0, sizeof b0);
+                __builtin_memcpy(&b1, w1, sizeof b1);
+                hd[p][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, b0, hd[p][0], 0, 0, 0);
+                hd[p][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, b1, hd[p][1], 0, 0, 0);
             }
         }
+        // lane c < 16 holds instance c of both requests of each pair tile
+        if (lane < 16 && i < A.N) {
 #pragma unroll
-        for (int p = 0; p < PT; ++p) {
-            if (h == 0 && valid[p]) {
-                const int64_t q = r[p] * A.N + i;
-                A.scores[q] = hd[p][0];
-                A.errb[q] = A.band_rel * (hd[p][1] + fabsf(b3));
+            for (int p = 0; p < PT; ++p) {
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const int64_t rq = r[p] + e;
+                    if (rq < A.R) {
+                        const int64_t q = rq * A.N + i;
+                        A.scores[q] = hd[p][e][0];
+                        A.errb[q] = A.band_rel * (hd[p][e][1] + fabsf(b3));
+                    }
+                }
             }
         }
     }
