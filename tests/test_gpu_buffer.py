@@ -71,11 +71,14 @@ def test_buffer_matches_oracle(name, F, P, n):
     ctx.close()
 
 
-@pytest.mark.parametrize("name,F,P,first,second", [("homogeneous", 64, 300, 1200, 700), ("large_batch", 40, 520, 900, 900)])
+@pytest.mark.parametrize("name,F,P,first,second", [("homogeneous", 64, 300, 1200, 700), ("large_batch", 40, 520, 900, 900),
+                                                   ("large_batch", 16, 6200, 6300, 600)])
 def test_buffer_large_pushes(name, F, P, first, second):
     """Pushes whose FIFO evictions exceed one admission chunk (256 candidates):
     the pool fills and starts replacing members within one push, and later
-    chunks see slots taken by earlier ones.  Pool and FIFO exactly the oracle's."""
+    chunks see slots taken by earlier ones; a pool of 6,200 slots is above what
+    the per-slot state in LDS holds (6,144), so its decisions keep that state in
+    global memory.  Pool and FIFO exactly the oracle's."""
     import torch
     w = synth.generate(name)
     cfg = w.cfg
