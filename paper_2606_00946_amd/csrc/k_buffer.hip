@@ -176,32 +176,6 @@ __global__ __launch_bounds__(256) void pool_nn_kernel(const double* __restrict__
     row_min_block(D, cap, n, (int32_t)blockIdx.x, sv, si, nnd + blockIdx.x, nni + blockIdx.x);
 }
 
-// One step of a wave reduction: combine with the pair that DPP control CTRL
-// moves into this lane (rows outside ROWS, and lanes without a source, keep
-// their own pair, which the minimum absorbs).
-template <int CTRL, int ROWS>
-__device__ __forceinline__ void dpp_min_step(double& v, int32_t& i) {
-    int32_t w[2];
-    __builtin_memcpy(w, &v, sizeof w);
-    const int32_t lo = __builtin_amdgcn_update_dpp(w[0], w[0], CTRL, ROWS, 0xF, false);
-    const int32_t hi = __builtin_amdgcn_update_dpp(w[1], w[1], CTRL, ROWS, 0xF, false);
-    const int32_t oi = __builtin_amdgcn_update_dpp(i, i, CTRL, ROWS, 0xF, false);
-    const int32_t ow[2] = {lo, hi};
-    double ov;
-    __builtin_memcpy(&ov, ow, sizeof ov);
-    better_pair(v, i, ov, oi);
-}
-
-__device__ __forceinline__ double read_lane_f64(double v, int lane) {
-    int32_t w[2];
-    __builtin_memcpy(w, &v, sizeof w);
-    w[0] = __builtin_amdgcn_readlane(w[0], lane);
-    w[1] = __builtin_amdgcn_readlane(w[1], lane);
-    double r;
-    __builtin_memcpy(&r, w, sizeof r);
-    return r;
-}
-
 // Block-wide lexicographic minima of P (value, index) pairs at once, with two
 // barriers for all of them; every thread gets the results.  sv, si: P * 16.
 template <int P>
