@@ -12,11 +12,14 @@
 // cache lines in and out for every key, so the table is built in LDS instead:
 // one workgroup owns a segment of kSegBuckets consecutive buckets of one
 // instance (128 KiB) and places the keys whose home bucket lies in it.  The
-// keys reach their segment's workgroup through a partition: a counting pass
-// (segment of every key, LDS histograms, one global add per segment touched),
-// a scan of the counts, and a scatter of every key with its input position
-// into its segment's run -- so each key is read three times in all, instead of
-// once by every segment of its instance.  A slot is claimed with one LDS add on the
+// keys reach their segment's workgroup through a partition: one pass computes
+// every key's segment and appends the key, with its input position, to that
+// segment's run (LDS histograms per chunk, one global add per segment
+// touched).  A run holds as many keys as the segment has slots (the runs are
+// laid out like the table's slots); keys past that could not all fit in the
+// segment anyway and go straight to the global pass.
+// Each key is thus read twice in all, instead of once by every segment of its
+// instance.  A slot is claimed with one LDS add on the
 // bucket's fill counter (slots fill in order 0..7; a full bucket sends the key
 // on to the next one) and written with one store; the finished segment goes
 // out with coalesced stores.  A key whose probe runs past the segment's last
@@ -122,27 +125,38 @@ constexpr int kPartBins = 4096;                // LDS counters; wider segment ra
 
 constexpr int kPartInst = 1024;                // instances a chunk may span with its table in LDS
 
-// Segment (global index) of every key of the chunk, counted (SCATTER false) or
-// scattered into the segments' runs (SCATTER true).  The workgroup first finds
-// the instances its chunk spans (one parallel pass over the offsets) and copies
-// their offsets, first segments and bucket counts to LDS; a thread then takes 8
-// consecutive keys and walks the instance boundaries from its first key.  In
-// the counting pass the all-ones key also sets its instance's flag (and
-// records its position in eidx).
-template <bool SCATTER>
+// Queue entry for a key that did not fit its segment's run: its position,
+// complemented, so that the global pass probes from its home bucket (an entry
+// that overflowed the segment itself is the position, probed from the next
+// segment).
+__device__ __forceinline__ void queue_overflow(int64_t t, bool from_home, int64_t* ovf, uint32_t* ovf_count,
+                                               uint32_t ovf_cap) {
+    const uint32_t pos = atomicAdd(ovf_count, 1u);
+    if (pos < ovf_cap) ovf[pos] = from_home ? ~t : t;
+}
+
+// Segment (global index) of every key of the chunk, and the key appended to
+// that segment's run.  The workgroup first finds the instances its chunk spans
+// (one parallel pass over the offsets) and copies their offsets, first
+// segments and bucket counts to LDS; a thread then takes 8 consecutive keys and
+// walks the instance boundaries from its first key.  The all-ones key sets its
+// instance's flag instead (and records its position in eidx).
 __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __restrict__ hashes,
                                                             const int64_t* __restrict__ inst_off,
                                                             const int32_t* __restrict__ seg_off,
-                                                            const uint32_t* __restrict__ nbuckets, int32_t n_inst,
-                                                            int64_t total, uint32_t* __restrict__ seg_count,
-                                                            uint32_t* __restrict__ seg_cursor,
+                                                            const uint32_t* __restrict__ nbuckets,
+                                                            const int64_t* __restrict__ base, int32_t n_inst,
+                                                            int64_t total, uint32_t* __restrict__ seg_cursor,
                                                             uint64_t* __restrict__ part_key,
                                                             uint32_t* __restrict__ part_idx,
-                                                            uint32_t* __restrict__ flags, int64_t* __restrict__ eidx) {
+                                                            uint32_t* __restrict__ flags, int64_t* __restrict__ eidx,
+                                                            int64_t* __restrict__ ovf, uint32_t* __restrict__ ovf_count,
+                                                            uint32_t ovf_cap) {
     __shared__ uint32_t bin[kPartBins];
     __shared__ int64_t l_off[kPartInst + 1];
     __shared__ int32_t l_seg[kPartInst + 1];
     __shared__ uint32_t l_nb[kPartInst];
+    __shared__ int64_t l_base[kPartInst];
     __shared__ int32_t i_first, i_last;
     const int64_t n_keys = inst_off[n_inst] < total ? inst_off[n_inst] : total;
     const int64_t c0 = (int64_t)blockIdx.x * kPartChunk;
@@ -162,7 +176,10 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
         for (int32_t x = threadIdx.x; x <= ihi - ilo + 1; x += kPartThreads) {
             l_off[x] = inst_off[ilo + x];
             l_seg[x] = seg_off[ilo + x];
-            if (x <= ihi - ilo) l_nb[x] = nbuckets[ilo + x];
+            if (x <= ihi - ilo) {
+                l_nb[x] = nbuckets[ilo + x];
+                l_base[x] = base[ilo + x];
+            }
         }
     }
     __syncthreads();
@@ -172,6 +189,8 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
     uint64_t key[kPartPerThread];
     int32_t seg[kPartPerThread];
     uint32_t rank[kPartPerThread];
+    int64_t run0[kPartPerThread];      // the segment's run: first slot and length in slots
+    uint32_t runcap[kPartPerThread];
 #pragma unroll
     for (int u = 0; u < kPartPerThread; ++u) key[u] = t0 + u < c1 ? hashes[t0 + u] : kEmptyKey;
     // instance of the first key, relative to ilo when the table is in LDS
@@ -195,32 +214,37 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
         if (t >= c1) continue;
         int32_t first_seg;
         uint32_t nb;
+        int64_t b_inst;
         if (in_lds) {
             while (l_off[i + 1] <= t) ++i;                       // empty instances are skipped too
             first_seg = l_seg[i];
             nb = l_nb[i];
+            b_inst = l_base[i];
         } else {
             while (inst_off[i + 1] <= t) ++i;
             first_seg = seg_off[i];
             nb = nbuckets[i];
+            b_inst = base[i];
         }
         if (key[u] == kEmptyKey) {
-            if (!SCATTER) {
-                const int32_t gi = in_lds ? ilo + i : i;
-                atomicOr(&flags[gi], kFlagHasEmptyKey);
-                if (eidx) eidx[gi] = t;
-            }
+            const int32_t gi = in_lds ? ilo + i : i;
+            atomicOr(&flags[gi], kFlagHasEmptyKey);
+            if (eidx) eidx[gi] = t;
             continue;
         }
-        seg[u] = first_seg + (int32_t)(bucket_of(key[u], nb) / kSegBuckets);
+        const uint32_t sl = bucket_of(key[u], nb) / kSegBuckets;
+        seg[u] = first_seg + (int32_t)sl;
+        run0[u] = (b_inst + (int64_t)sl * kSegBuckets) * kBucketKeys;
+        runcap[u] = min((uint32_t)kSegBuckets, nb - sl * kSegBuckets) * kBucketKeys;
         rank[u] = local ? atomicAdd(&bin[seg[u] - seg_lo], 1u) : 0u;
         if (!local) {
-            if (SCATTER) {
-                const uint32_t pos = atomicAdd(&seg_cursor[seg[u]], 1u);
-                part_key[pos] = key[u];
-                part_idx[pos] = (uint32_t)t;
+            const uint32_t pos = atomicAdd(&seg_cursor[seg[u]], 1u);
+            if (pos < runcap[u]) {
+                const int64_t q = run0[u] + pos;
+                part_key[q] = key[u];
+                part_idx[q] = (uint32_t)t;
             } else {
-                atomicAdd(&seg_count[seg[u]], 1u);
+                queue_overflow(t, true, ovf, ovf_count, ovf_cap);
             }
             seg[u] = -1;
         }
@@ -230,60 +254,33 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
     const int32_t nb_local = seg_off[ihi + 1] - seg_lo;
     for (int x = threadIdx.x; x < nb_local; x += kPartThreads) {
         const uint32_t cnt = bin[x];
-        if (cnt == 0u) continue;
-        if (SCATTER) bin[x] = atomicAdd(&seg_cursor[seg_lo + x], cnt);   // this chunk's first position in the run
-        else atomicAdd(&seg_count[seg_lo + x], cnt);
+        if (cnt != 0u) bin[x] = atomicAdd(&seg_cursor[seg_lo + x], cnt);   // this chunk's first position in the run
     }
-    if (!SCATTER) return;
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < kPartPerThread; ++u) {
         if (seg[u] < 0) continue;
         const uint32_t pos = bin[seg[u] - seg_lo] + rank[u];
-        part_key[pos] = key[u];
-        part_idx[pos] = (uint32_t)(t0 + u);
+        if (pos < runcap[u]) {
+            const int64_t q = run0[u] + pos;
+            part_key[q] = key[u];
+            part_idx[q] = (uint32_t)(t0 + u);
+        } else {
+            queue_overflow(t0 + u, true, ovf, ovf_count, ovf_cap);
+        }
     }
 }
 
-// Exclusive scan of the n_seg counts into run starts (seg_count[n_seg] gets
-// the total); the scatter's cursors start at the run starts.  Also the
-// instance of every segment, for the segment build.
-__global__ __launch_bounds__(1024) void part_scan_kernel(int32_t n_seg, uint32_t* __restrict__ seg_count,
-                                                         uint32_t* __restrict__ seg_cursor,
-                                                         const int32_t* __restrict__ seg_off, int32_t n_inst,
-                                                         int32_t* __restrict__ seg_inst) {
-    for (int32_t i = threadIdx.x; i < n_inst; i += blockDim.x)
-        for (int32_t x = seg_off[i]; x < seg_off[i + 1]; ++x) seg_inst[x] = i;
-    __shared__ uint32_t part[1024];
-    __shared__ uint32_t carry;
-    if (threadIdx.x == 0) carry = 0u;
-    __syncthreads();
-    for (int32_t b0 = 0; b0 < n_seg; b0 += 1024) {
-        const int32_t x = b0 + (int32_t)threadIdx.x;
-        const uint32_t v = x < n_seg ? seg_count[x] : 0u;
-        part[threadIdx.x] = v;
-        __syncthreads();
-        for (int dd = 1; dd < 1024; dd <<= 1) {                   // inclusive Hillis-Steele scan
-            const uint32_t add = threadIdx.x >= (unsigned)dd ? part[threadIdx.x - dd] : 0u;
-            __syncthreads();
-            part[threadIdx.x] += add;
-            __syncthreads();
-        }
-        if (x < n_seg) {
-            const uint32_t start = carry + part[threadIdx.x] - v;
-            seg_count[x] = start;
-            seg_cursor[x] = start;
-        }
-        __syncthreads();
-        if (threadIdx.x == 1023) carry += part[1023];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) seg_count[n_seg] = carry;
+// The instance of every segment, for the segment build.
+__global__ void seg_inst_kernel(const int32_t* __restrict__ seg_off, int32_t n_inst, int32_t* __restrict__ seg_inst) {
+    const int32_t i = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i >= n_inst) return;
+    for (int32_t x = seg_off[i]; x < seg_off[i + 1]; ++x) seg_inst[x] = i;
 }
 
 __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     uint64_t* __restrict__ keys, const int64_t* __restrict__ base, const uint32_t* __restrict__ nbuckets,
-    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_inst, const uint32_t* __restrict__ run_start,
+    const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_inst, const uint32_t* __restrict__ run_len,
     const uint64_t* __restrict__ part_key, const uint32_t* __restrict__ part_idx, int64_t* __restrict__ ovf,
     uint32_t* __restrict__ ovf_count, uint32_t ovf_cap, uint32_t* __restrict__ entry_of) {
     __shared__ uint64_t seg[kSegBuckets * kBucketKeys];
@@ -302,14 +299,14 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     for (uint32_t x = tid; x < nbl; x += kSegThreads) fill[x] = 0u;
     __syncthreads();
 
-    const uint32_t r0 = run_start[L], r1 = run_start[L + 1];
-    for (uint32_t q = r0 + tid; q < r1; q += kSegThreads) {
+    const int64_t r0 = (base[i] + b0) * kBucketKeys;             // the run, laid out like the segment's slots
+    const int64_t r1 = r0 + min(run_len[L], nbl * (uint32_t)kBucketKeys);
+    for (int64_t q = r0 + tid; q < r1; q += kSegThreads) {
         const uint64_t key = part_key[q];
         const uint32_t lb = bucket_of(key, nb) - b0;
         const int32_t ls = segment_place(seg, fill, lb, nbl, key);
         if (ls < 0) {
-            const uint32_t pos = atomicAdd(ovf_count, 1u);
-            if (pos < ovf_cap) ovf[pos] = part_idx[q];
+            queue_overflow(part_idx[q], false, ovf, ovf_count, ovf_cap);
         } else if (entry_of) {
             entry_of[(base[i] + b0) * kBucketKeys + ls] = part_idx[q];
         }
@@ -324,8 +321,9 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     }
 }
 
-// Keys whose probe ran past their segment continue in the next segment.  If
-// more keys overflowed than the queue holds, every key is (re)inserted from
+// Keys whose probe ran past their segment continue in the next segment; keys
+// that did not fit their segment's run are inserted from their home bucket.
+// If more keys overflowed than the queue holds, every key is (re)inserted from
 // its home bucket instead: keys already placed are found on their probe path,
 // so that is correct too, only slower.
 __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t* __restrict__ base,
@@ -340,13 +338,15 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
     const int64_t count = queued ? (int64_t)n : n_keys;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < count; j += stride) {
-        const int64_t t = queued ? ovf[j] : j;
+        const int64_t entry = queued ? ovf[j] : j;
+        const bool from_home = entry < 0;                 // past its segment's run: probe from home
+        const int64_t t = from_home ? ~entry : entry;
         const uint64_t key = hashes[t];
         if (key == kEmptyKey) continue;
         const int32_t i = owner_of(inst_off, n_inst, t);
         const uint32_t nb = nbuckets[i];
         uint32_t b = bucket_of(key, nb);
-        if (queued) {
+        if (queued && !from_home) {
             b = (b / kSegBuckets + 1) * kSegBuckets;
             if (b >= nb) b = 0;
         }
@@ -357,70 +357,65 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
 
 int64_t table_overflow_capacity(int64_t total) { return 4096 + total / 64; }
 
-// Workspace: overflow counter (256 B) and queue, segment counts and cursors,
-// partitioned keys and their input positions.
+// Workspace: overflow counter (256 B) and queue, run lengths, the instance of
+// every segment, and the runs: a key and input position per table slot.
 struct BuildWs {
     uint32_t* ovf_count;
     int64_t* ovf;
-    uint32_t* seg_count;
-    uint32_t* seg_cursor;
+    uint32_t* run_len;
     int32_t* seg_inst;
     uint64_t* part_key;
     uint32_t* part_idx;
 };
 
-static BuildWs carve_build_ws(void* ws, int64_t total, int32_t n_seg) {
+static int64_t up256(int64_t b) { return (b + 255) / 256 * 256; }
+
+static BuildWs carve_build_ws(void* ws, int64_t total, int32_t n_seg, int64_t total_buckets) {
     char* p = static_cast<char*>(ws);
-    auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
+    const int64_t runs = (total_buckets > 0 ? total_buckets : 1) * kBucketKeys;
     BuildWs w;
     w.ovf_count = reinterpret_cast<uint32_t*>(p);
     p += 256;
     w.ovf = reinterpret_cast<int64_t*>(p);
-    p += up(8 * table_overflow_capacity(total));
-    w.seg_count = reinterpret_cast<uint32_t*>(p);
-    p += up(4 * ((int64_t)n_seg + 1));
-    w.seg_cursor = reinterpret_cast<uint32_t*>(p);
-    p += up(4 * ((int64_t)n_seg + 1));
+    p += up256(8 * table_overflow_capacity(total));
+    w.run_len = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * ((int64_t)n_seg + 1));
     w.seg_inst = reinterpret_cast<int32_t*>(p);
-    p += up(4 * ((int64_t)n_seg + 1));
+    p += up256(4 * ((int64_t)n_seg + 1));
     w.part_key = reinterpret_cast<uint64_t*>(p);
-    p += up(8 * (total > 0 ? total : 1));
+    p += up256(8 * runs);
     w.part_idx = reinterpret_cast<uint32_t*>(p);
     return w;
 }
 
-int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg) {
-    auto up = [](int64_t b) { return (b + 255) / 256 * 256; };
-    const int64_t t = total > 0 ? total : 1;
-    return 256 + up(8 * table_overflow_capacity(total)) + 3 * up(4 * ((int64_t)n_seg + 1)) + up(8 * t) + up(4 * t);
+int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg, int64_t total_buckets) {
+    const int64_t runs = (total_buckets > 0 ? total_buckets : 1) * kBucketKeys;
+    return 256 + up256(8 * table_overflow_capacity(total)) + 2 * up256(4 * ((int64_t)n_seg + 1)) + up256(8 * runs) +
+           up256(4 * runs);
 }
 
 hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
                               const uint64_t* hashes, int64_t total, int32_t n_inst, void* ws, int n_cu,
                               hipStream_t s, uint32_t* entry_of, int64_t* eidx) {
-    const BuildWs w = carve_build_ws(ws, total, n_seg);
+    const BuildWs w = carve_build_ws(ws, total, n_seg, t.total_buckets);
     const uint32_t cap = (uint32_t)table_overflow_capacity(total);
     hipError_t e;
     if ((e = launch_fill_u32(w.ovf_count, 0u, 1, s)) != hipSuccess) return e;
-    if ((e = launch_fill_u32(w.seg_count, 0u, (int64_t)n_seg + 1, s)) != hipSuccess) return e;
+    if ((e = launch_fill_u32(w.run_len, 0u, (int64_t)n_seg + 1, s)) != hipSuccess) return e;
     if ((e = launch_fill_u32(t.flags, 0u, n_inst, s)) != hipSuccess) return e;
-    const uint32_t chunks = (uint32_t)((total + kPartChunk - 1) / kPartChunk);
-    if (chunks > 0) {
-        hipLaunchKernelGGL(part_kernel<false>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
-                           t.nbuckets, n_inst, total, w.seg_count, w.seg_cursor, w.part_key, w.part_idx, t.flags, eidx);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(1024), 0, s, n_seg, w.seg_count, w.seg_cursor, seg_off, n_inst,
+    hipLaunchKernelGGL(seg_inst_kernel, dim3((uint32_t)((n_inst + 255) / 256)), dim3(256), 0, s, seg_off, n_inst,
                        w.seg_inst);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    const uint32_t chunks = (uint32_t)((total + kPartChunk - 1) / kPartChunk);
     if (chunks > 0) {
-        hipLaunchKernelGGL(part_kernel<true>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
-                           t.nbuckets, n_inst, total, w.seg_count, w.seg_cursor, w.part_key, w.part_idx, t.flags, eidx);
+        hipLaunchKernelGGL(part_kernel, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off, t.nbuckets,
+                           t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx, w.ovf,
+                           w.ovf_count, cap);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (n_seg > 0) {
         hipLaunchKernelGGL(table_segment_kernel, dim3((uint32_t)n_seg), dim3(kSegThreads), 0, s, t.keys, t.base,
-                           t.nbuckets, seg_off, w.seg_inst, w.seg_count, w.part_key, w.part_idx, w.ovf, w.ovf_count,
+                           t.nbuckets, seg_off, w.seg_inst, w.run_len, w.part_key, w.part_idx, w.ovf, w.ovf_count,
                            cap, entry_of);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }

@@ -126,7 +126,7 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
 // queue of table_overflow_capacity(total) key indices; key indices are 32-bit.
 constexpr uint32_t kSegBuckets = 2048;
 int64_t table_overflow_capacity(int64_t total);
-int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg);
+int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg, int64_t total_buckets);
 // Prefix-index maintenance (k_index.hip).  One commit of a routed batch.
 constexpr int64_t kSelChunk = 4096;           // candidates per selection chunk
 struct IndexCommit {

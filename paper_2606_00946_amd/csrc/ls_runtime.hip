@@ -524,7 +524,8 @@ int index_load(ls_ctx* c, int32_t N, int64_t total, int64_t list_entries, const 
     if ((rc = grow(c, (void**)&X.small, &X.small_cap, sizeof(int64_t) * (size_t)(kIndexSmallPerN * N + 4))))
         return rc;
     if ((rc = grow(c, &X.ws, &X.ws_cap, (size_t)(total > 0 ? total : 1)))) return rc;
-    const size_t tw = (size_t)ls::table_build_workspace_bytes(list_entries, (int32_t)c->tables_nseg);
+    const size_t tw =
+        (size_t)ls::table_build_workspace_bytes(list_entries, (int32_t)c->tables_nseg, c->tables.total_buckets);
     if ((rc = grow(c, &c->tws, &c->tws_cap, tw))) return rc;
     X.list_entries = list_entries;
     IndexSmall m = index_small(X.small, N);
@@ -610,7 +611,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t));
     if (rc) return rc;
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
-    rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg));
+    rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg, nbk));
     if (rc) return rc;
     if (N > c->inst_cap) {
         LS_HIP(c, hipDeviceSynchronize());
