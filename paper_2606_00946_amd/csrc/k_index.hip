@@ -388,10 +388,20 @@ __global__ __launch_bounds__(256) void select_hist_kernel(IndexCommit C, int shi
         const CandView V = cand_view(C, i);
         const int64_t v0 = (ch - C.chunk0[i]) * kSelChunk;
         const int64_t v1 = v0 + kSelChunk < C.nvirt[i] ? v0 + kSelChunk : C.nvirt[i];
-        for (int64_t v = v0 + threadIdx.x; v < v1; v += blockDim.x) {
-            uint64_t h, st;
-            if (V.get(v, h, st) && (st & mask) == prefix) atomicAdd(&lh[(st >> shift) & 255u], 1u);
+        // all of the thread's candidates are loaded before any is used, so the
+        // loads are in flight together
+        constexpr int kPer = (int)(kSelChunk / 256);
+        uint64_t st[kPer];
+        bool ok[kPer];
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int64_t v = v0 + threadIdx.x + (int64_t)u * 256;
+            uint64_t h;
+            ok[u] = v < v1 && V.get(v, h, st[u]);
         }
+#pragma unroll
+        for (int u = 0; u < kPer; ++u)
+            if (ok[u] && (st[u] & mask) == prefix) atomicAdd(&lh[(st[u] >> shift) & 255u], 1u);
         __syncthreads();
         if (lh[threadIdx.x]) atomicAdd(&C.sel_hist[(int64_t)i * 256 + threadIdx.x], lh[threadIdx.x]);
         __syncthreads();
@@ -435,11 +445,19 @@ __global__ __launch_bounds__(256) void select_compact_multi_kernel(IndexCommit C
         const CandView V = cand_view(C, i);
         uint64_t* dh = C.hash2 + C.off2[i];
         uint64_t* ds = C.stamp2 + C.off2[i];
+        // the thread's candidates, read once and all in flight together
+        uint64_t hh[kPer], ss[kPer];
+        bool kept[kPer];
         uint32_t mine = 0;
+#pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            uint64_t h, st;
             const int64_t v = v0 + (int64_t)u * 256;
-            if (v < vend && V.get(v, h, st) && st >= theta) ++mine;
+            kept[u] = v < vend && V.get(v, hh[u], ss[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            kept[u] = kept[u] && ss[u] >= theta;
+            mine += kept[u] ? 1u : 0u;
         }
         // exclusive scan of `mine` over the workgroup (in thread order)
         uint32_t incl = mine;
@@ -457,13 +475,12 @@ __global__ __launch_bounds__(256) void select_compact_multi_kernel(IndexCommit C
         }
         __syncthreads();
         int64_t pos = s_base + before;
+#pragma unroll
         for (int u = 0; u < kPer; ++u) {
-            uint64_t h, st;
-            const int64_t v = v0 + (int64_t)u * 256;
-            if (v < vend && V.get(v, h, st) && st >= theta) {
+            if (kept[u]) {
                 if (pos < keep) {
-                    dh[pos] = h;
-                    ds[pos] = st;
+                    dh[pos] = hh[u];
+                    ds[pos] = ss[u];
                 }
                 ++pos;
             }
