@@ -408,22 +408,59 @@ __global__ __launch_bounds__(256) void select_hist_kernel(IndexCommit C, int shi
     }
 }
 
-// The digit of the want-th largest candidate; the histogram is cleared for
-// the next pass.
-__global__ void select_digit_kernel(IndexCommit C, int shift) {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= C.N || !C.sel_active[i]) return;
+// The digit of the want-th largest candidate: the highest bin d >= 1 whose
+// count, added to the counts of the bins above it, reaches `want` (bin 0 when
+// none does).  One wave per instance: lane l holds bins 255 - 4l .. 252 - 4l,
+// and a scan across the lanes gives each the counts above its bins.  The
+// histogram is cleared for the next pass.
+__global__ __launch_bounds__(256) void select_digit_kernel(IndexCommit C, int shift) {
+    const int32_t i = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (i >= C.N || !C.sel_active[i]) return;           // uniform over the wave
     uint32_t* hh = C.sel_hist + (int64_t)i * 256;
-    int64_t want = C.sel_want[i], cum = 0;
-    int d = 255;
-    for (; d > 0; --d) {
-        if (cum + (int64_t)hh[d] >= want) break;
-        cum += hh[d];
+    uint32_t cnt[4];
+    int64_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        cnt[q] = hh[255 - 4 * lane - q];
+        mine += cnt[q];
     }
-    C.sel_want[i] = want - cum;
-    C.sel_prefix[i] |= (uint64_t)d << shift;
-    C.sel_mask[i] |= 255ull << shift;
-    for (int t = 0; t < 256; ++t) hh[t] = 0;
+    int64_t incl = mine;
+#pragma unroll
+    for (int dd = 1; dd < 64; dd <<= 1) {
+        const int64_t t = __shfl_up(incl, dd);
+        if (lane >= dd) incl += t;
+    }
+    const int64_t want = C.sel_want[i];
+    int64_t cum = incl - mine, cum_at = 0;
+    int found = -1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int bin = 255 - 4 * lane - q;
+        if (found < 0 && bin >= 1 && cum + (int64_t)cnt[q] >= want) {
+            found = bin;
+            cum_at = cum;
+        }
+        cum += cnt[q];
+    }
+    const uint64_t m = __ballot(found >= 0);
+    int digit;
+    int64_t above;
+    if (m) {
+        const int first = __ffsll((long long)m) - 1;
+        digit = __shfl(found, first);
+        above = __shfl(cum_at, first);
+    } else {
+        digit = 0;                                       // every bin but 0: the total less bin 0 (lane 63)
+        above = __shfl(incl, 63) - (int64_t)__shfl((int)cnt[3], 63);
+    }
+    if (lane == 0) {
+        C.sel_want[i] = want - above;
+        C.sel_prefix[i] |= (uint64_t)digit << shift;
+        C.sel_mask[i] |= 255ull << shift;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) hh[255 - 4 * lane - q] = 0;
 }
 
 // Survivors (stamp >= the selected one, or all) into the new lists: a chunk
@@ -620,7 +657,7 @@ hipError_t launch_commit(const CacheTables& T, const IndexCommit& C, hipStream_t
     for (int p = 7; p >= 0; --p) {
         hipLaunchKernelGGL(select_hist_kernel, dim3(grid), dim3(256), 0, s, C, 8 * p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(select_digit_kernel, dim3((uint32_t)((N + 255) / 256)), dim3(256), 0, s, C, 8 * p);
+        hipLaunchKernelGGL(select_digit_kernel, dim3((uint32_t)((N + 3) / 4)), dim3(256), 0, s, C, 8 * p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(select_compact_multi_kernel, dim3(grid), dim3(256), 0, s, C);
