@@ -250,51 +250,77 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             hd[p][0] = f32x4_t{lane < 16 ? b3 : 0.0f, 0.0f, 0.0f, 0.0f};
             hd[p][1] = hd[p][0];
         }
+        // The head of row tile mt runs inside the k-loop of row tile mt + 1
+        // (pair tile 0 over k-steps 1-3, pair tile 1 over 4-6), so its VALU
+        // work issues while the next tile's MFMAs execute.
+        f32x16_t prev[PT];
+        bf16x8_t fh_prev{};
+        uint32_t pw0[PT][4], pw1[PT][4];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const f32x16_t bias = load_acc_rows(lds_b2 + 32 * mt + 4 * h);
-            const bf16x8_t fh = hdl[mt * 8];
-            // a per-row-tile base keeps every read within the 16-bit immediate
-            // offset of ds_read; the empty asm hides its value from the
-            // optimiser, which would otherwise hoist one address register per
-            // far fragment out of the loop
-            uint32_t base = (uint32_t)(mt * KS2 * 64);
-            asm volatile("" : "+s"(base));
-            const bf16x8_t* __restrict__ w2g = lds_w2 + base + lane;
+        for (int mt = 0; mt <= MT; ++mt) {
+            const bool last = mt == MT;
+            f32x16_t bias{};
+            bf16x8_t fh{};
+            const bf16x8_t* __restrict__ w2g = lds_w2;
+            if (!last) {
+                bias = load_acc_rows(lds_b2 + 32 * mt + 4 * h);
+                fh = hdl[mt * 8];
+                // a per-row-tile base keeps every read within the 16-bit immediate
+                // offset of ds_read; the empty asm hides its value from the
+                // optimiser, which would otherwise hoist one address register per
+                // far fragment out of the loop
+                uint32_t base = (uint32_t)(mt * KS2 * 64);
+                asm volatile("" : "+s"(base));
+                w2g = lds_w2 + base + lane;
+            }
             f32x16_t acc[PT];
             // software pipeline: the next k-step's fragment is read while this
             // k-step's MFMAs run (the barriers pin that order)
-            bf16x8_t a_cur = w2g[0], a_nxt;
+            bf16x8_t a_cur{}, a_nxt{};
+            if (!last) a_cur = w2g[0];
 #pragma unroll
-            for (int s = 0; s < KS2; ++s) {
-                if (s + 1 < KS2) a_nxt = w2g[(s + 1) * 64];
+            for (int s = 0; s < (last || KS2 < 7 ? 7 : KS2); ++s) {
+                if (!last && s + 1 < KS2) a_nxt = w2g[(s + 1) * 64];
                 __builtin_amdgcn_sched_barrier(0);
+                if (!last && s < KS2) {
 #pragma unroll
-                for (int p = 0; p < PT; ++p)
-                    acc[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur, hb[p][s], s == 0 ? bias : acc[p], 0, 0, 0);
+                    for (int p = 0; p < PT; ++p)
+                        acc[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur, hb[p][s], s == 0 ? bias : acc[p], 0, 0, 0);
+                }
+                if (mt > 0) {
+                    // 16-lane rows of x0: units of k-step 2(mt-1), half 0, of pairs
+                    // 0-15 and of 16-31, then half 1 of each; x1 the same for the
+                    // next k-step.  The swap puts pairs 0-15's four 8-unit groups
+                    // into b0, 16-31's into b1.
+                    const int p = s < 4 ? 0 : 1, ph = s - 3 * p;
+                    if (s >= 1 && s <= 6) {
+                        if (ph == 1) {
+                            const bf16x8_t x0 = relu_pack(prev[p], 0), x1 = relu_pack(prev[p], 1);
+                            __builtin_memcpy(pw0[p], &x0, sizeof pw0[p]);
+                            __builtin_memcpy(pw1[p], &x1, sizeof pw1[p]);
+                        } else if (ph == 2) {
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) {
+                                const auto sw = __builtin_amdgcn_permlane16_swap(pw0[p][k], pw1[p][k], false, false);
+                                pw0[p][k] = sw[0];
+                                pw1[p][k] = sw[1];
+                            }
+                        } else {
+                            bf16x8_t b0, b1;
+                            __builtin_memcpy(&b0, pw0[p], sizeof b0);
+                            __builtin_memcpy(&b1, pw1[p], sizeof b1);
+                            hd[p][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh_prev, b0, hd[p][0], 0, 0, 0);
+                            hd[p][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh_prev, b1, hd[p][1], 0, 0, 0);
+                        }
+                    }
+                }
                 __builtin_amdgcn_sched_barrier(0);
                 a_cur = a_nxt;
             }
+            if (!last) {
 #pragma unroll
-            for (int p = 0; p < PT; ++p) {
-                // 16-lane rows of x0: units of k-step 2mt, half 0, of pairs 0-15 and
-                // of 16-31, then half 1 of each; x1 the same for k-step 2mt + 1.  The
-                // swap puts pairs 0-15's four 8-unit groups into b0, 16-31's into b1.
-                const bf16x8_t x0 = relu_pack(acc[p], 0), x1 = relu_pack(acc[p], 1);
-                uint32_t w0[4], w1[4];
-                __builtin_memcpy(w0, &x0, sizeof w0);
-                __builtin_memcpy(w1, &x1, sizeof w1);
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const auto sw = __builtin_amdgcn_permlane16_swap(w0[k], w1[k], false, false);
-                    w0[k] = sw[0];
-                    w1[k] = sw[1];
-                }
-                bf16x8_t b0, b1;
-                __builtin_memcpy(&b0, w0, sizeof b0);
-                __builtin_memcpy(&b1, w1, sizeof b1);
-                hd[p][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, b0, hd[p][0], 0, 0, 0);
-                hd[p][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, b1, hd[p][1], 0, 0, 0);
+                for (int p = 0; p < PT; ++p) prev[p] = acc[p];
+                fh_prev = fh;
             }
         }
         // lane c < 16 holds instance c of both requests of each pair tile
