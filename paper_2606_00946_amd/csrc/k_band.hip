@@ -176,20 +176,20 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Each wave scores two pairs at once, so every weight it converts from bf16
-// serves two chains and the two head chains run side by side.
-constexpr int kRescoreWaves = 12;
-constexpr int kRescorePairs = 2;
+// Each wave scores four pairs at once, so every weight it converts from bf16
+// serves four chains and the four head chains run side by side.  Eight waves
+// of four 1 KB rows and W2 fill the 160 KB of LDS exactly; w3 is read from
+// memory (cached) by the head chains.
+constexpr int kRescoreWaves = 8;
+constexpr int kRescorePairs = 4;
 
 template <int H>
 __global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(RescoreArgs A) {
     constexpr int U = H / 64;                  // units per lane
     constexpr int P = kRescorePairs;
     __shared__ uint16_t lds_w2[H * H];
-    __shared__ float lds_w3[H];
     __shared__ __align__(16) float lds_row[kRescoreWaves][P][H];
     for (int e = threadIdx.x; e < H * H; e += 64 * kRescoreWaves) lds_w2[e] = (uint16_t)(__float_as_uint(A.w2t[e]) >> 16);
-    for (int e = threadIdx.x; e < H; e += 64 * kRescoreWaves) lds_w3[e] = A.w3[e];
     __syncthreads();
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     float w1c[U][5], b2v[U];
@@ -258,10 +258,10 @@ __global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(Res
             float t = b3;
             for (int j = 0; j < H; j += 4) {
                 const float4 h4 = *reinterpret_cast<const float4*>(hrow + j);
-                t = __builtin_fmaf(lds_w3[j], h4.x, t);
-                t = __builtin_fmaf(lds_w3[j + 1], h4.y, t);
-                t = __builtin_fmaf(lds_w3[j + 2], h4.z, t);
-                t = __builtin_fmaf(lds_w3[j + 3], h4.w, t);
+                t = __builtin_fmaf(A.w3[j], h4.x, t);
+                t = __builtin_fmaf(A.w3[j + 1], h4.y, t);
+                t = __builtin_fmaf(A.w3[j + 2], h4.z, t);
+                t = __builtin_fmaf(A.w3[j + 3], h4.w, t);
             }
             A.scores[pp[lane]] = t;
         }
