@@ -207,22 +207,39 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
             g_loaded = g;
         }
         const int64_t i = g * kGroupInst + ni;
+        // The B operand of layer 1 holds a pair's five derived columns in lanes
+        // 0-31 (k-group 0).  Lane (n, half) computes the columns of the pair of
+        // its column n in tile p = half, and one permlane32 swap moves tile 1's
+        // down to lanes 0-31.
+        static_assert(PT == 2, "one pair tile per lane half");
         int64_t r[PT];
-        bool valid[PT];
-        bf16x8_t xb[PT];
 #pragma unroll
-        for (int p = 0; p < PT; ++p) {
-            r[p] = rb * kUnitReq + wave * (2 * PT) + 2 * p + nr;
-            valid[p] = r[p] < A.R && i < A.N;
-            const int64_t rr = valid[p] ? r[p] : 0, ii = valid[p] ? i : 0;
+        for (int p = 0; p < PT; ++p) r[p] = rb * kUnitReq + wave * (2 * PT) + 2 * p + nr;
+        bf16x8_t xb[PT];
+        {
+            const int64_t rh = h ? r[1] : r[0];
+            const bool valid = rh < A.R && i < A.N;
+            const int64_t rr = valid ? rh : 0, ii = valid ? i : 0;
             float x[5], xt[5];
-            derived_columns(A.prompt_len[rr], A.req_off[rr + 1] - A.req_off[rr],
-                            valid[p] ? A.overlap[rr * A.N + ii] : 0, A.block_tokens, x);
+            derived_columns(A.prompt_len[rr], A.req_off[rr + 1] - A.req_off[rr], valid ? A.overlap[rr * A.N + ii] : 0,
+                            A.block_tokens, x);
             normalise_tail<true>(x, A.mu, A.isig, A.d_inst, xt);
             bf16x8_t v{};
 #pragma unroll
             for (int c = 0; c < 5; ++c) v[c] = (__bf16)xt[c];
-            xb[p] = (valid[p] && h == 0) ? v : bf16x8_t{};
+            if (!valid) v = bf16x8_t{};
+            uint32_t w[4], u[4];
+            __builtin_memcpy(w, &v, sizeof w);
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {                 // words 0-2 hold the five columns
+                const auto sw = __builtin_amdgcn_permlane32_swap(w[k], w[k], false, false);
+                u[k] = sw[1];                             // lanes 0-31: lane + 32's word
+            }
+            u[3] = 0u;
+            bf16x8_t t1;
+            __builtin_memcpy(&t1, u, sizeof t1);
+            xb[0] = h == 0 ? v : bf16x8_t{};
+            xb[1] = h == 0 ? t1 : bf16x8_t{};
         }
 
         // layer 1, one row tile at a time: acc = partial + W1_tail x_tail, then bf16(relu(.))
