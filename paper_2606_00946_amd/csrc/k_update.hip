@@ -121,14 +121,30 @@ int64_t update_workspace_bytes(const ModelDims& m, int32_t B) { return plan_ws(m
 // ---------------------------------------------------------------------------
 // forward
 // ---------------------------------------------------------------------------
+// Normalised inputs, feature-major: a tile of 64 samples x 64 features is read
+// row by row (coalesced), transposed through LDS and written out one feature
+// row at a time.
 template <bool BF>
-__global__ void normalize_kernel(const float* __restrict__ feats, const float* __restrict__ mu,
-                                 const float* __restrict__ isig, float* __restrict__ xn, int32_t B, int d) {
-    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)B * d) return;
-    int64_t c = t / B, b = t - c * B;
-    float v = __fmul_rn(__fsub_rn(feats[b * d + c], mu[c]), isig[c]);
-    xn[t] = BF ? q_bf16(v) : v;
+__global__ __launch_bounds__(256) void normalize_kernel(const float* __restrict__ feats, const float* __restrict__ mu,
+                                                        const float* __restrict__ isig, float* __restrict__ xn,
+                                                        int32_t B, int d) {
+    __shared__ float tile[64][65];                  // [feature][sample]
+    const int64_t b0 = (int64_t)blockIdx.x * 64;
+    const int c0 = (int)blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t b = b0 + i;
+        const int c = c0 + tx;
+        float v = 0.0f;
+        if (b < B && c < d) v = __fmul_rn(__fsub_rn(feats[b * d + c], mu[c]), isig[c]);
+        tile[tx][i] = BF ? q_bf16(v) : v;
+    }
+    __syncthreads();
+    for (int j = ty; j < 64; j += 4) {
+        const int c = c0 + j;
+        const int64_t b = b0 + tx;
+        if (c < d && b < B) xn[(int64_t)c * B + b] = tile[j][tx];
+    }
 }
 
 // U consecutive output units of one sample: each is the fma chain from its bias
@@ -393,15 +409,17 @@ __global__ void loss_final_kernel(const float* __restrict__ loss_part, int nblk,
     if (threadIdx.x == 0) out[0] = red[0] / (float)B;
 }
 
-// dL/dz of the last hidden layer: g_b * w[j] where z > 0 (then dropout's factor)
+// dL/dz of the last hidden layer: g_b * w[j] where z > 0 (then dropout's factor);
+// blockIdx.y = unit j
 template <bool BF>
-__global__ void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
-                                  const float* __restrict__ z, float* __restrict__ dl, int32_t B, int hl, DropArgs D,
-                                  int layer) {
-    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)hl * B) return;
-    int64_t j = t / B, b = t - j * B;
-    const float v = apply_drop(D, layer, b, (int)j, z[t] > 0.0f ? g[b] * w[j] : 0.0f);
+__global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
+                                                         const float* __restrict__ z, float* __restrict__ dl,
+                                                         int32_t B, DropArgs D, int layer) {
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int j = (int)blockIdx.y;
+    if (b >= B) return;
+    const int64_t t = (int64_t)j * B + b;
+    const float v = apply_drop(D, layer, b, j, z[t] > 0.0f ? g[b] * w[j] : 0.0f);
     dl[t] = BF ? q_bf16(v) : v;
 }
 
@@ -644,6 +662,26 @@ __global__ __launch_bounds__(64) void wgrad_direct_kernel(const float* __restric
     }
 }
 
+// The head's few outputs over many partials: one wave per output; lane l adds
+// partials l, l + 64, ... in ascending order, then a fixed shuffle tree.
+constexpr int64_t kReduceWaveMax = 4096;          // outputs below which a wave takes each
+
+__global__ __launch_bounds__(256) void wgrad_reduce_wave_kernel(const float* __restrict__ part, int S, int M, int N,
+                                                                float* __restrict__ gw, float* __restrict__ gb) {
+    const int64_t ld = N + 1, MN = (int64_t)M * ld;
+    const int64_t e = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (e >= MN) return;                          // uniform over the wave
+    float acc = 0.0f;
+    for (int s = lane; s < S; s += 64) acc += part[(int64_t)s * MN + e];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane != 0) return;
+    const int64_t mm = e / ld, nn = e - mm * ld;
+    if (nn < N) gw[mm * N + nn] = acc;
+    else gb[mm] = acc;
+}
+
 // grad_w[m][n] (n < N) and grad_b[m] from the partials, summed over s ascending
 __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M, int N, float* __restrict__ gw,
                                     float* __restrict__ gb) {
@@ -696,7 +734,10 @@ static hipError_t weight_grad_mfma(const float* A, const float* Bt, int M, int N
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t MN = (int64_t)M * (N + 1);
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks_for(MN, 256)), dim3(256), 0, s, part, p.S, M, N, gw, gb);
+    if (MN < kReduceWaveMax)
+        hipLaunchKernelGGL(wgrad_reduce_wave_kernel, dim3(blocks_for(MN, 4)), dim3(256), 0, s, part, p.S, M, N, gw, gb);
+    else
+        hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks_for(MN, 256)), dim3(256), 0, s, part, p.S, M, N, gw, gb);
     return hipGetLastError();
 }
 
@@ -802,8 +843,8 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
                          const float* feats, float* xn, float* const* z, float* const* a, float* t,
                          const DropArgs& D, hipStream_t s) {
     const int64_t nB = B;
-    hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB * m.d, 256)), dim3(256), 0, s, feats, mu, isig, xn, B,
-                       m.d);
+    hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB, 64), (m.d + 63) / 64), dim3(256), 0, s, feats, mu, isig,
+                       xn, B, m.d);
     const uint32_t sb = blocks_for(nB, 256);
     const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
     bool lds_w = m.d <= kDenseMaxK;
@@ -956,8 +997,8 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b[L]);
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB * m.hl, 256)), dim3(256), 0, s, w.g,
-                       compute + m.c_wt[L], w.z[L - 1], w.dl[L - 1], B, m.hl, D, L - 1);
+    hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB, 256), m.hl), dim3(256), 0, s, w.g,
+                       compute + m.c_wt[L], w.z[L - 1], w.dl[L - 1], B, D, L - 1);
     // hidden layers, last to first
     for (int l = L - 1; l >= 0; --l) {
         const float* in = l == 0 ? w.xn : w.a[l - 1];
