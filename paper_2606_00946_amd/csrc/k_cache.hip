@@ -67,6 +67,36 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream
     return hipGetLastError();
 }
 
+struct FillOps {
+    FillOp op[kMaxFillOps];
+};
+
+// blockIdx.y = the fill
+__global__ void fill_multi_kernel(FillOps F) {
+    const FillOp o = F.op[blockIdx.y];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < o.count; i += stride) {
+        if (o.bytes == 8) static_cast<uint64_t*>(o.p)[i] = o.value;
+        else static_cast<uint32_t*>(o.p)[i] = (uint32_t)o.value;
+    }
+}
+
+hipError_t launch_fill_multi(const FillOp* ops, int n, hipStream_t s) {
+    if (n > kMaxFillOps) return hipErrorInvalidValue;
+    FillOps F{};
+    int m = 0;
+    int64_t most = 0;
+    for (int i = 0; i < n; ++i) {
+        if (ops[i].count <= 0) continue;
+        if (ops[i].bytes != 4 && ops[i].bytes != 8) return hipErrorInvalidValue;
+        F.op[m++] = ops[i];
+        most = ops[i].count > most ? ops[i].count : most;
+    }
+    if (m == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_multi_kernel, dim3(grid_for(most, 256), m), dim3(256), 0, s, F);
+    return hipGetLastError();
+}
+
 // Insert `key` into the table of nb buckets, probing from bucket b; returns the
 // slot (bucket * 8 + position) that holds it, or -1 if the table is full.  A
 // slot changes at most once (empty -> key), so a stale read can only show a
@@ -400,9 +430,8 @@ hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, con
     const BuildWs w = carve_build_ws(ws, total, n_seg, t.total_buckets);
     const uint32_t cap = (uint32_t)table_overflow_capacity(total);
     hipError_t e;
-    if ((e = launch_fill_u32(w.ovf_count, 0u, 1, s)) != hipSuccess) return e;
-    if ((e = launch_fill_u32(w.run_len, 0u, (int64_t)n_seg + 1, s)) != hipSuccess) return e;
-    if ((e = launch_fill_u32(t.flags, 0u, n_inst, s)) != hipSuccess) return e;
+    const FillOp fills[3] = {{w.ovf_count, 0u, 1, 4}, {w.run_len, 0u, (int64_t)n_seg + 1, 4}, {t.flags, 0u, n_inst, 4}};
+    if ((e = launch_fill_multi(fills, 3, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(seg_inst_kernel, dim3((uint32_t)((n_inst + 255) / 256)), dim3(256), 0, s, seg_off, n_inst,
                        w.seg_inst);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -629,9 +629,8 @@ hipError_t launch_dedup_lists(const int64_t* off, int32_t N, const uint64_t* has
 hipError_t launch_commit(const CacheTables& T, const IndexCommit& C, hipStream_t s) {
     const int32_t N = C.N;
     hipError_t e;
-    if ((e = launch_fill_u64(reinterpret_cast<uint64_t*>(C.occ), 0, N, s)) != hipSuccess) return e;
-    if ((e = launch_fill_u64(reinterpret_cast<uint64_t*>(C.fcount), 0, N, s)) != hipSuccess) return e;
-    if ((e = launch_fill_u64(C.efresh, 0, N, s)) != hipSuccess) return e;
+    const FillOp fills[3] = {{C.occ, 0u, N, 8}, {C.fcount, 0u, N, 8}, {C.efresh, 0u, N, 8}};
+    if ((e = launch_fill_multi(fills, 3, s)) != hipSuccess) return e;
     if (C.R > 0) {
         hipLaunchKernelGGL(occupancy_kernel, dim3(grid_of(C.R, 256, C.n_cu)), dim3(256), 0, s, C.R, C.req_off,
                            C.chosen, N, C.occ);

@@ -595,12 +595,11 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     uint64_t* cand = join ? reinterpret_cast<uint64_t*>(take(kContListCap * 8)) : nullptr;
     int64_t* list = reinterpret_cast<int64_t*>(take((int64_t)R * N * 8));
 
-    hipError_t e = launch_fill_u64(gkeys, kEmptyKey, G, s);
-    if (e == hipSuccess) e = launch_fill_u64(reinterpret_cast<uint64_t*>(glead), 0ull, G, s);
-    if (e == hipSuccess) e = launch_fill_u32(n_leaders, 0u, 1, s);
-    if (e == hipSuccess && join) e = launch_fill_u64(qkeys, kEmptyKey, G, s);
-    if (e == hipSuccess && join) e = launch_fill_u32(qseen, 0u, G, s);
-    if (e == hipSuccess && join) e = launch_fill_u32(qfilter, 0u, kContFilterWords, s);
+    const int64_t jn = join ? 1 : 0;
+    const FillOp fills[6] = {{gkeys, kEmptyKey, G, 8},          {glead, 0u, G, 8},
+                             {n_leaders, 0u, 1, 4},              {qkeys, kEmptyKey, jn * G, 8},
+                             {qseen, 0u, jn * G, 4},             {qfilter, 0u, jn * kContFilterWords, 4}};
+    hipError_t e = launch_fill_multi(fills, 6, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_insert_kernel, dim3((uint32_t)(((int64_t)R + kGroupThreads - 1) / kGroupThreads)),
                        dim3(kGroupThreads), 0, s, R, req_off, req_hashes, gkeys, glead, (uint32_t)G, slot_of);

@@ -119,6 +119,15 @@ bool mfma_supported(const ModelDims& m);
 // ---------------------------------------------------------------------------
 hipError_t launch_fill_u64(uint64_t* p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t value, int64_t count, hipStream_t s);
+// Several fills in one launch (4- or 8-byte words; at most kMaxFillOps).
+struct FillOp {
+    void* p;
+    uint64_t value;
+    int64_t count;
+    int bytes;
+};
+constexpr int kMaxFillOps = 8;
+hipError_t launch_fill_multi(const FillOp* ops, int n, hipStream_t s);
 // Table build: the keys partitioned by segment of kSegBuckets buckets (seg_off[i]
 // is the first segment of instance i, n_seg the total), one workgroup per
 // segment, then a global pass over the keys that overflowed their segment.  The

@@ -48,6 +48,7 @@ struct ls_ctx {
     int32_t inst_cap = 0;
     int64_t* inst_off_dev = nullptr;
     int32_t* seg_off_dev = nullptr;    // [N + 1] first table segment of each instance
+    char* inst_meta = nullptr;         // one block: tables.base, tables.nbuckets, inst_off_dev, seg_off_dev
     void* tws = nullptr;               // table-build workspace: key partition, overflow queue
     size_t tws_cap = 0;
     int64_t tables_nseg = 0;           // table segments of the loaded layout
@@ -409,8 +410,7 @@ void ls_destroy(ls_ctx* c) {
         (void)hipDeviceSynchronize();
         for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->frag16,
                         (void*)c->frag32, (void*)c->tables.keys,
-                        (void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags,
-                        (void*)c->inst_off_dev, (void*)c->seg_off_dev, c->tws, c->ws, (void*)c->buf.fifo_x,
+                        (void*)c->inst_meta, (void*)c->tables.flags, c->tws, c->ws, (void*)c->buf.fifo_x,
                         (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
                         (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws, (void*)c->idx.hash,
                         (void*)c->idx.stamp, (void*)c->idx.hash2, (void*)c->idx.stamp2, (void*)c->idx.entry_of,
@@ -613,29 +613,31 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
     rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg, nbk));
     if (rc) return rc;
+    // metadata: bases, bucket counts, offsets and first segments, laid out in
+    // one block (as in the pinned staging buffer) so that one copy moves them
+    const size_t b_base = sizeof(int64_t) * N, b_nb = sizeof(uint32_t) * N, b_off = sizeof(int64_t) * (N + 1);
+    const size_t o_off = (size_t)round_up((int64_t)(b_base + b_nb), 8), o_seg = o_off + b_off;
+    const size_t b_seg = sizeof(int32_t) * (N + 1);
     if (N > c->inst_cap) {
         LS_HIP(c, hipDeviceSynchronize());
-        for (void* p : {(void*)c->tables.base, (void*)c->tables.nbuckets, (void*)c->tables.flags, (void*)c->inst_off_dev,
-                        (void*)c->seg_off_dev})
+        for (void* p : {(void*)c->inst_meta, (void*)c->tables.flags})
             if (p) LS_HIP(c, hipFree(p));
-        c->tables.base = nullptr; c->tables.nbuckets = nullptr; c->tables.flags = nullptr; c->inst_off_dev = nullptr;
-        c->seg_off_dev = nullptr;
+        c->inst_meta = nullptr; c->tables.flags = nullptr;
+        c->tables.base = nullptr; c->tables.nbuckets = nullptr; c->inst_off_dev = nullptr; c->seg_off_dev = nullptr;
         c->inst_cap = 0;
-        bool ok = hipMalloc((void**)&c->tables.base, sizeof(int64_t) * N) == hipSuccess &&
-                  hipMalloc((void**)&c->tables.nbuckets, sizeof(uint32_t) * N) == hipSuccess &&
-                  hipMalloc((void**)&c->tables.flags, sizeof(uint32_t) * N) == hipSuccess &&
-                  hipMalloc((void**)&c->inst_off_dev, sizeof(int64_t) * (N + 1)) == hipSuccess &&
-                  hipMalloc((void**)&c->seg_off_dev, sizeof(int32_t) * (N + 1)) == hipSuccess;
+        bool ok = hipMalloc((void**)&c->inst_meta, o_seg + b_seg) == hipSuccess &&
+                  hipMalloc((void**)&c->tables.flags, sizeof(uint32_t) * N) == hipSuccess;
         if (!ok) {
             (void)hipGetLastError();
             return fail(c, LS_ERR_NOMEM, "instance metadata allocation failed");
         }
         c->inst_cap = N;
     }
-    // metadata through pinned staging
-    const size_t b_base = sizeof(int64_t) * N, b_nb = sizeof(uint32_t) * N, b_off = sizeof(int64_t) * (N + 1);
-    const size_t o_off = (size_t)round_up((int64_t)(b_base + b_nb), 8), o_seg = o_off + b_off;
-    const size_t b_seg = sizeof(int32_t) * (N + 1);
+    // a smaller N than the allocation's packs into the front of the block
+    c->tables.base = reinterpret_cast<int64_t*>(c->inst_meta);
+    c->tables.nbuckets = reinterpret_cast<uint32_t*>(c->inst_meta + b_base);
+    c->inst_off_dev = reinterpret_cast<int64_t*>(c->inst_meta + o_off);
+    c->seg_off_dev = reinterpret_cast<int32_t*>(c->inst_meta + o_seg);
     rc = stage_reserve(c, o_seg + b_seg + 64);
     if (rc) return rc;
     char* st = (char*)c->stage;
@@ -643,10 +645,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     memcpy(st + b_base, nb.data(), b_nb);
     memcpy(st + o_off, inst_off, b_off);
     memcpy(st + o_seg, seg_off.data(), b_seg);
-    LS_HIP(c, hipMemcpyAsync(c->tables.base, st, b_base, hipMemcpyHostToDevice, s));
-    LS_HIP(c, hipMemcpyAsync(c->tables.nbuckets, st + b_base, b_nb, hipMemcpyHostToDevice, s));
-    LS_HIP(c, hipMemcpyAsync(c->inst_off_dev, st + o_off, b_off, hipMemcpyHostToDevice, s));
-    LS_HIP(c, hipMemcpyAsync(c->seg_off_dev, st + o_seg, b_seg, hipMemcpyHostToDevice, s));
+    LS_HIP(c, hipMemcpyAsync(c->inst_meta, st, o_seg + b_seg, hipMemcpyHostToDevice, s));
     LS_HIP(c, hipEventRecord(c->stage_done, s));
     c->stage_pending = true;
     c->tables.n = N;
