@@ -38,10 +38,16 @@ struct BandPolicy {
     const uint64_t* req_hashes;
 };
 
+// Lane l holds pairs i0 + 4l .. i0 + 4l + 3 of each chunk of 256 (VEC, N a
+// multiple of 4: 16-byte reads of t and E, and the four flags written as one
+// word), else pairs i0 + l.  The list is in ascending pair order either way.
+template <bool VEC>
 __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N, const float* __restrict__ t,
                                                            const float* __restrict__ E, BandPolicy BP,
                                                            uint8_t* __restrict__ band, int64_t* __restrict__ list,
                                                            uint32_t* __restrict__ count) {
+    constexpr int V = VEC ? 4 : 1;                  // pairs per lane and chunk
+    constexpr int CH = 64 * V;                      // chunk
     __shared__ uint32_t wcount[kBandWaves];
     __shared__ uint32_t wbase[kBandWaves];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -49,16 +55,31 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
     const bool live = r < R;
     const float* __restrict__ tr = t + (live ? r : 0) * N;
     const float* __restrict__ er = E + (live ? r : 0) * N;
+    auto load = [&](const float* __restrict__ row, int i, float (&v)[V]) {
+        if constexpr (VEC) {
+            const float4 q = *reinterpret_cast<const float4*>(row + i);
+            v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+        } else {
+            v[0] = row[i];
+        }
+    };
     float U = INFINITY, L0 = INFINITY;
     uint32_t cnt = 0;
     int32_t C[LS_MAX_KFILTER];
     int nc = 0;
     if (live) {
-        for (int i = lane; i < N; i += 64) {
-            const float ti = tr[i], ei = er[i];
-            if (finite_f(ti) && finite_f(ei)) {
-                U = fminf(U, ti + ei);
-                L0 = fminf(L0, ti - ei);
+        for (int i0 = 0; i0 < N; i0 += CH) {
+            const int i = i0 + V * lane;
+            if (i < N) {
+                float tv[V], ev[V];
+                load(tr, i, tv);
+                load(er, i, ev);
+#pragma unroll
+                for (int j = 0; j < V; ++j)
+                    if (finite_f(tv[j]) && finite_f(ev[j])) {
+                        U = fminf(U, tv[j] + ev[j]);
+                        L0 = fminf(L0, tv[j] - ev[j]);
+                    }
             }
         }
 #pragma unroll
@@ -75,16 +96,26 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
         U = U + fabsf(U) * 0x1p-20f;                // absorbs the rounding of the sums above
         if (BP.k_filter > 0 && BP.stats->saturated && BP.req_off[r + 1] > BP.req_off[r])
             nc = hrw_topk_wave(BP.req_hashes[BP.req_off[r]], N, BP.k_filter, C, lane);
-        for (int i0 = 0; i0 < N; i0 += 64) {
-            const int i = i0 + lane;
-            bool in = false;
+        for (int i0 = 0; i0 < N; i0 += CH) {
+            const int i = i0 + V * lane;
+            uint32_t bits = 0;
             if (i < N) {
-                in = band_member(tr[i], er[i], U);
-                for (int q = 0; q < nc; ++q) in |= (C[q] == i);
-                band[r * N + i] = in ? 1 : 0;
+                float tv[V], ev[V];
+                load(tr, i, tv);
+                load(er, i, ev);
+#pragma unroll
+                for (int j = 0; j < V; ++j) {
+                    bool in = band_member(tv[j], ev[j], U);
+                    for (int q = 0; q < nc; ++q) in |= (C[q] == i + j);
+                    bits |= (in ? 1u : 0u) << (8 * j);
+                }
+                if constexpr (VEC) *reinterpret_cast<uint32_t*>(band + r * N + i) = bits;
+                else band[r * N + i] = (uint8_t)bits;
             }
-            cnt += (uint32_t)__popcll(__ballot(in));
+            cnt += (uint32_t)__popc(bits);
         }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
     }
     if (lane == 0) wcount[wv] = cnt;
     __syncthreads();
@@ -100,12 +131,25 @@ __global__ __launch_bounds__(1024) void band_select_kernel(int32_t R, int32_t N,
     __syncthreads();
     if (!live) return;
     uint32_t base = wbase[wv];
-    for (int i0 = 0; i0 < N; i0 += 64) {
-        const int i = i0 + lane;
-        const bool in = i < N && band[r * N + i];
-        const uint64_t m = __ballot(in);
-        if (in) list[base + __popcll(m & ((1ull << lane) - 1))] = r * N + i;
-        base += (uint32_t)__popcll(m);
+    for (int i0 = 0; i0 < N; i0 += CH) {
+        const int i = i0 + V * lane;
+        uint32_t bits = 0;
+        if (i < N) {
+            if constexpr (VEC) bits = *reinterpret_cast<const uint32_t*>(band + r * N + i);
+            else bits = band[r * N + i];
+        }
+        const uint32_t mine = (uint32_t)__popc(bits);
+        uint32_t incl = mine;                           // inclusive scan over the lanes
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t up = __shfl_up(incl, d);
+            if (lane >= d) incl += up;
+        }
+        uint32_t pos = base + incl - mine;
+#pragma unroll
+        for (int j = 0; j < V; ++j)
+            if ((bits >> (8 * j)) & 1u) list[pos++] = r * N + i + j;
+        base += __shfl(incl, 63);
     }
 }
 
@@ -120,8 +164,10 @@ hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const
                                      hipStream_t s) {
     if (R <= 0) return hipSuccess;
     BandPolicy BP{delta, k_filter, stats, req_off, req_hashes};
-    hipLaunchKernelGGL(band_select_kernel, dim3((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)),
-                       dim3(64 * kBandWaves), 0, s, R, N, t, E, BP, band, list, count);
+    const dim3 grid((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)), block(64 * kBandWaves);
+    const bool vec = N % 4 == 0 && ((uintptr_t)t | (uintptr_t)E) % 16 == 0 && (uintptr_t)band % 4 == 0;
+    if (vec) hipLaunchKernelGGL(band_select_kernel<true>, grid, block, 0, s, R, N, t, E, BP, band, list, count);
+    else hipLaunchKernelGGL(band_select_kernel<false>, grid, block, 0, s, R, N, t, E, BP, band, list, count);
     return hipGetLastError();
 }
 
