@@ -191,6 +191,9 @@ hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const fl
 // ---------------------------------------------------------------------------
 // K3: per-request argmin, one wave per request
 // ---------------------------------------------------------------------------
+// With a band (VEC: N a multiple of 4, the flags word-aligned) lane l reads the
+// flags of pairs 4l .. 4l + 3 of each chunk of 256 as one word.
+template <bool VEC>
 __global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d, int d_inst, int block_tokens,
                                                      const float* __restrict__ scores,
                                                      const uint8_t* __restrict__ band,
@@ -206,10 +209,22 @@ __global__ __launch_bounds__(256) void argmin_kernel(int32_t R, int32_t N, int d
     const float* __restrict__ s = scores + r * N;
     float bs = 0.0f;
     int bi = INT_MAX;
-    for (int i = lane; i < N; i += 64) {
-        if (band && !band[r * N + i]) continue;          // only candidates that were rescored
-        float v = s[i];
-        if (better(v, i, bs, bi)) { bs = v; bi = i; }
+    if constexpr (VEC) {
+        for (int i = 4 * lane; i < N; i += 256) {
+            const uint32_t bits = *reinterpret_cast<const uint32_t*>(band + r * N + i);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (!((bits >> (8 * j)) & 0xFFu)) continue;      // only candidates that were rescored
+                const float v = s[i + j];
+                if (better(v, i + j, bs, bi)) { bs = v; bi = i + j; }
+            }
+        }
+    } else {
+        for (int i = lane; i < N; i += 64) {
+            if (band && !band[r * N + i]) continue;          // only candidates that were rescored
+            float v = s[i];
+            if (better(v, i, bs, bi)) { bs = v; bi = i; }
+        }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
@@ -236,8 +251,14 @@ hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* 
                          const float* inst_feat, int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s) {
     if (R <= 0) return hipSuccess;
     int64_t grid = ((int64_t)R + 3) / 4;
-    hipLaunchKernelGGL(argmin_kernel, dim3((uint32_t)grid), dim3(256), 0, s, R, N, m.d, m.d_inst, m.block_tokens,
-                       scores, band, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft, feat_out);
+    if (band && N % 4 == 0 && (uintptr_t)band % 4 == 0)
+        hipLaunchKernelGGL(argmin_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, R, N, m.d, m.d_inst,
+                           m.block_tokens, scores, band, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft,
+                           feat_out);
+    else
+        hipLaunchKernelGGL(argmin_kernel<false>, dim3((uint32_t)grid), dim3(256), 0, s, R, N, m.d, m.d_inst,
+                           m.block_tokens, scores, band, req_off, prompt_len, overlap, inst_feat, chosen, min_ttft,
+                           feat_out);
     return hipGetLastError();
 }
 
