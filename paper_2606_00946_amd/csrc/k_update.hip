@@ -521,10 +521,13 @@ __device__ __forceinline__ bf16x8_t load_frag(const float* __restrict__ row, int
 // k-steps (double-buffered) and read from there.
 constexpr int kWgradKs = 2;
 
+// blockIdx.y = a range of NT n-tiles (the bias column with the first range).
 template <int NT, bool VEC>
 __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
                                                          float* __restrict__ part, int M, int N, int32_t B,
                                                          int64_t chunk) {
+    const int n0 = (int)blockIdx.y * NT * 32;
+    const bool with_bias = blockIdx.y == 0;
     constexpr int KS = kWgradKs;
     constexpr int NE = KS * NT * 64;                 // fragment lanes per stage
     constexpr int EPT = (NE + 511) / 512;            // per thread
@@ -546,7 +549,7 @@ __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict
     for (int x = 0; x < EPT; ++x) {
         const int f = tid + 512 * x;
         const int ks = f / (NT * 64), t = (f / 64) % NT, ln = f & 63;
-        const int n = t * 32 + (ln & 31);
+        const int n = n0 + t * 32 + (ln & 31);
         sval[x] = f < NE && n < N;
         srow[x] = Bt + (int64_t)(sval[x] ? n : 0) * B;
         soff[x] = 16 * ks + 8 * (ln >> 5);
@@ -587,7 +590,7 @@ __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict
             for (int t = 0; t < NT; ++t)
                 acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[ks], lds_b[buf][(ks * NT + t) * 64 + lane],
                                                                  acc[t], 0, 0, 0);
-            acc[NT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[ks], ones, acc[NT], 0, 0, 0);
+            if (with_bias) acc[NT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_cur[ks], ones, acc[NT], 0, 0, 0);
         }
         if (more) publish(buf ^ 1);
         __syncthreads();
@@ -601,10 +604,10 @@ __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict
         if (mm >= M) continue;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const int nn = t * 32 + row;
+            const int nn = n0 + t * 32 + row;
             if (nn < N) out[(int64_t)mm * ld + nn] = acc[t][r];
         }
-        if (row == 0) out[(int64_t)mm * ld + N] = acc[NT][r];
+        if (with_bias && row == 0) out[(int64_t)mm * ld + N] = acc[NT][r];
     }
 }
 
@@ -703,32 +706,38 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M
     else gb[mm] = acc;
 }
 
+// NT n-tiles per workgroup, ny workgroups across N (matrix-core path only).
 template <int NT>
 static void launch_wgrad_nt(const float* A, const float* Bt, float* part, int M, int N, int32_t B, int S,
-                            int64_t chunk, hipStream_t s) {
+                            int64_t chunk, int ny, hipStream_t s) {
     const bool vec = B % 4 == 0;
     if (M <= 32) {
         if (vec) hipLaunchKernelGGL((wgrad_direct_kernel<NT, true>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
         else hipLaunchKernelGGL((wgrad_direct_kernel<NT, false>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
     } else {
-        if (vec) hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), dim3(S), dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
-        else hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), dim3(S), dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
+        const dim3 grid((uint32_t)S, (uint32_t)ny);
+        if (vec) hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), grid, dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
+        else hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), grid, dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
     }
 }
 
-// dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.
+// dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.  With
+// fewer sample chunks than CUs the n-tiles are split over two workgroups per
+// chunk (each reads the chunk's A rows, half of its Bt rows).
 static hipError_t weight_grad_mfma(const float* A, const float* Bt, int M, int N, int32_t B, float* part,
-                                   float* gw, float* gb, hipStream_t s) {
+                                   float* gw, float* gb, int n_cu, hipStream_t s) {
     const WgradPlan p = wgrad_plan(B, M);
-    switch ((N + 31) / 32) {
-        case 1: launch_wgrad_nt<1>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 2: launch_wgrad_nt<2>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 3: launch_wgrad_nt<3>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 4: launch_wgrad_nt<4>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 5: launch_wgrad_nt<5>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 6: launch_wgrad_nt<6>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 7: launch_wgrad_nt<7>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
-        case 8: launch_wgrad_nt<8>(A, Bt, part, M, N, B, p.S, p.chunk, s); break;
+    const int tiles = (N + 31) / 32;
+    const int ny = (M > 32 && tiles >= 2 && p.S < n_cu) ? 2 : 1;
+    switch ((tiles + ny - 1) / ny) {
+        case 1: launch_wgrad_nt<1>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 2: launch_wgrad_nt<2>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 3: launch_wgrad_nt<3>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 4: launch_wgrad_nt<4>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 5: launch_wgrad_nt<5>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 6: launch_wgrad_nt<6>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 7: launch_wgrad_nt<7>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
+        case 8: launch_wgrad_nt<8>(A, Bt, part, M, N, B, p.S, p.chunk, ny, s); break;
         default: return hipErrorInvalidValue;
     }
     hipError_t e = hipGetLastError();
@@ -971,7 +980,7 @@ hipError_t launch_score_generic(const ModelDims& m, const float* compute, const 
 template <bool BF>
 static hipError_t run_update(const ModelDims& m, float* master, float* compute, const float* mu, const float* isig,
                              int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
-                             float* grad_out, void* workspace, const DropArgs& D, hipStream_t s) {
+                             float* grad_out, void* workspace, const DropArgs& D, int n_cu, hipStream_t s) {
     UpdWs w = plan_ws(m, B, reinterpret_cast<char*>(workspace));
     const int64_t nB = B;
     const int L = m.L;
@@ -991,7 +1000,7 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     hipError_t e;
     // head
     if (mf) {
-        e = weight_grad_mfma(w.g, w.a[L - 1], 1, m.hl, B, w.part, w.grad + m.m_w[L], w.grad + m.m_b[L], s);
+        e = weight_grad_mfma(w.g, w.a[L - 1], 1, m.hl, B, w.part, w.grad + m.m_w[L], w.grad + m.m_b[L], n_cu, s);
     } else {
         e = weight_grad(w.g, w.a[L - 1], 1, m.hl, B, w, w.grad + m.m_w[L], s);
         hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b[L]);
@@ -1004,7 +1013,7 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         const float* in = l == 0 ? w.xn : w.a[l - 1];
         const int K = m.in_of(l), O = m.h[l];
         if (mf) {
-            e = weight_grad_mfma(w.dl[l], in, O, K, B, w.part, w.grad + m.m_w[l], w.grad + m.m_b[l], s);
+            e = weight_grad_mfma(w.dl[l], in, O, K, B, w.part, w.grad + m.m_w[l], w.grad + m.m_b[l], n_cu, s);
         } else {
             e = weight_grad(w.dl[l], in, O, K, B, w, w.grad + m.m_w[l], s);
             hipLaunchKernelGGL(rowsum_kernel, dim3(O), dim3(256), 0, s, w.dl[l], B, w.grad + m.m_b[l]);
@@ -1034,12 +1043,13 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
 
 hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,
                          const float* inv_sigma, int32_t B, const float* feats, const float* ttft, float lr,
-                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, hipStream_t s) {
+                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, int n_cu,
+                         hipStream_t s) {
     if (m.bf16)
         return run_update<true>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace,
-                                drop, s);
+                                drop, n_cu, s);
     return run_update<false>(m, master, compute, mu, inv_sigma, B, feats, ttft, lr, loss_out, grad_out, workspace,
-                             drop, s);
+                             drop, n_cu, s);
 }
 
 }  // namespace ls

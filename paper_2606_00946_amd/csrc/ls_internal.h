@@ -283,6 +283,7 @@ hipError_t launch_loss_finish(const double* acc, int32_t count, float* out, hipS
 int64_t update_workspace_bytes(const ModelDims& m, int32_t B);
 hipError_t launch_update(const ModelDims& m, float* master, float* compute, const float* mu,
                          const float* inv_sigma, int32_t B, const float* feats, const float* ttft, float lr,
-                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, hipStream_t s);
+                         float* loss_out, float* grad_out, void* workspace, const DropArgs& drop, int n_cu,
+                         hipStream_t s);
 
 }  // namespace ls

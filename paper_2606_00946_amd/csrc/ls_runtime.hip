@@ -912,7 +912,7 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     const ModelSlot M = train_model(c);
     LS_TIMED(c, K_UPDATE, s,
              ls::launch_update(c->dims, M.master, M.compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
-                               c->upd_ws, D, s));
+                               c->upd_ws, D, c->n_cu, s));
     if (M.frag16)
         LS_TIMED(c, K_UPDATE, s,
                  ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), M.master, M.frag16, M.frag32, s));
@@ -1161,7 +1161,7 @@ int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int
             const ls::DropArgs D = next_drop(c);
             LS_TIMED(c, K_UPDATE, s,
                      ls::launch_update(m, TM.master, TM.compute, c->mu, c->isig, mb, bx, by, lr, step_loss, nullptr,
-                                       uws, D, s));
+                                       uws, D, c->n_cu, s));
             if (e + 1 == epochs && loss_out) LS_HIP(c, ls::launch_loss_accumulate(step_loss, acc, nb == 0, s));
             ++nb;
         }
