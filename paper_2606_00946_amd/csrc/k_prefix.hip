@@ -470,6 +470,88 @@ __global__ __launch_bounds__(256) void prefix_leaders_kernel(ProbeTables T, int3
     }
 }
 
+// Leaders, first block: 16 (leader, instance) pairs per wave, four lanes per
+// 64-byte bucket.  A pair whose first block is not cached on the instance (most
+// pairs) or whose prompt has at most one block is answered here; the others go
+// on a list (one atomic per wave) and are extended from block 1 by a wave each.
+__global__ __launch_bounds__(256) void leaders_first_kernel(ProbeTables T, int32_t N,
+                                                            const int64_t* __restrict__ req_off,
+                                                            const uint64_t* __restrict__ req_hashes,
+                                                            const int32_t* __restrict__ leaders,
+                                                            const uint32_t* __restrict__ n_leaders,
+                                                            int32_t* __restrict__ overlap, int64_t* __restrict__ more,
+                                                            uint32_t* __restrict__ n_more) {
+    const int lane = threadIdx.x & 63, g = lane >> 2, q = lane & 3, shift = 4 * g;
+    const int64_t total = (int64_t)(*n_leaders) * N;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t b0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 16; b0 < total;
+         b0 += waves * 16) {
+        const int64_t pair = b0 + g;
+        const bool act = pair < total;
+        int64_t i = 0, r = 0, h0 = 0, n = 0;
+        if (act) {
+            const int64_t k = pair / N;
+            i = pair - k * N;
+            r = leaders[k];
+            h0 = req_off[r];
+            n = req_off[r + 1] - h0;
+        }
+        bool hit = false;
+        if (act && n > 0) {                              // uniform over the group of four lanes
+            const uint64_t key = req_hashes[h0];
+            const uint32_t nb = T.nb[i];
+            if (key == kEmptyKey) {
+                hit = (T.flags[i] & kFlagHasEmptyKey) != 0;
+            } else {
+                const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
+                uint32_t b = bucket_of(key, nb);
+                bool gfound = false, gempty = false;
+                // a full bucket without the key may have overflowed into the next ones
+                for (uint32_t probe = 0; probe < nb && !gfound && !gempty; ++probe) {
+                    const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(table + (int64_t)b * kBucketKeys + q * 2);
+                    gfound = ((__ballot((w.x == key) | (w.y == key)) >> shift) & 0xFull) != 0;
+                    gempty = ((__ballot((w.x == kEmptyKey) | (w.y == kEmptyKey)) >> shift) & 0xFull) != 0;
+                    b = (b + 1 == nb) ? 0 : b + 1;
+                }
+                hit = gfound;
+            }
+        }
+        const bool go_on = act && hit && n > 1;
+        if (act && q == 0 && !go_on) overlap[r * N + i] = hit ? 1 : 0;
+        const uint64_t m = __ballot(go_on && q == 0);
+        if (m) {
+            const int first = __ffsll((long long)m) - 1;
+            uint32_t base = 0;
+            if (lane == first) base = atomicAdd(n_more, (uint32_t)__popcll(m));
+            base = (uint32_t)__shfl((int)base, first);
+            if (go_on && q == 0) more[base + __popcll(m & ((1ull << lane) - 1))] = pair;
+        }
+    }
+}
+
+// The listed leader pairs, one wave each, from block 1 on.
+__global__ __launch_bounds__(256) void leaders_rest_kernel(ProbeTables T, int32_t N,
+                                                           const int64_t* __restrict__ req_off,
+                                                           const uint64_t* __restrict__ req_hashes,
+                                                           const int32_t* __restrict__ leaders,
+                                                           const int64_t* __restrict__ more,
+                                                           const uint32_t* __restrict__ n_more,
+                                                           int32_t* __restrict__ overlap) {
+    const int lane = threadIdx.x & 63;
+    const int64_t total = *n_more;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t x = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); x < total; x += waves) {
+        const int64_t pair = more[x];
+        const int64_t k = pair / N, i = pair - k * N;
+        const int64_t r = leaders[k];
+        const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
+        const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
+        const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
+        const int64_t l = extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane);
+        if (lane == 0) overlap[r * N + i] = (int32_t)l;
+    }
+}
+
 // Lane per pair: followers whose answer follows from the leader's (or from a
 // continuation cached nowhere) are written here; workgroup b covers pairs
 // [b chunk, (b + 1) chunk) and lists the rest in its own slice of the probe
@@ -597,7 +679,7 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
 
     const int64_t jn = join ? 1 : 0;
     const FillOp fills[6] = {{gkeys, kEmptyKey, G, 8},          {glead, 0u, G, 8},
-                             {n_leaders, 0u, 1, 4},              {qkeys, kEmptyKey, jn * G, 8},
+                             {n_leaders, 0u, 2, 4},              {qkeys, kEmptyKey, jn * G, 8},
                              {qseen, 0u, jn * G, 4},             {qfilter, 0u, jn * kContFilterWords, 4}};
     hipError_t e = launch_fill_multi(fills, 6, s);
     if (e != hipSuccess) return e;
@@ -621,11 +703,22 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
                            (uint32_t)G, qseen);
     }
     ProbeTables T{t.keys, t.base, t.nbuckets, t.flags};
-    // leaders: persistent grid of waves over (leader, instance) pairs
+    // leaders: persistent grids of waves over (leader, instance) pairs.  The
+    // probe list of the followers is free until they run and holds the leader
+    // pairs that go past block 0; n_leaders[1] counts them.
     int64_t wgrid = (pairs + 3) / 4;
     if (wgrid > (int64_t)n_cu * 16) wgrid = (int64_t)n_cu * 16;
-    hipLaunchKernelGGL(prefix_leaders_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
-                       leaders, n_leaders, overlap, closed ? 1 : 0);
+    if (closed) {
+        hipLaunchKernelGGL(prefix_leaders_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
+                           leaders, n_leaders, overlap, 1);
+    } else {
+        int64_t fgrid = (pairs + 63) / 64;
+        if (fgrid > (int64_t)n_cu * 16) fgrid = (int64_t)n_cu * 16;
+        hipLaunchKernelGGL(leaders_first_kernel, dim3((uint32_t)fgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
+                           leaders, n_leaders, overlap, list, n_leaders + 1);
+        hipLaunchKernelGGL(leaders_rest_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
+                           leaders, list, n_leaders + 1, overlap);
+    }
     // followers: slices of pairs, one workgroup each
     int64_t slices = (pairs + kResolveThreads - 1) / kResolveThreads;
     if (slices > (int64_t)n_cu * 8) slices = (int64_t)n_cu * 8;
