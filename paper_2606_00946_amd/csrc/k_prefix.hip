@@ -97,20 +97,33 @@ __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ 
                                                    const uint64_t* __restrict__ h, int64_t n, int64_t l, int lane) {
     const int g = lane >> 2, q = lane & 3, shift = g * 4;
     int W = 4;
-    while (l < n) {
-        uint64_t key[4];
-        ulonglong2 v[4];
-        uint32_t bkt[4];
-        bool act[4];
+    // the window's block hashes; the next window's are read while this one's
+    // buckets are in flight (used only if every probe of this window hits)
+    uint64_t key[4];
+    bool act[4];
+    auto load_keys = [&](int64_t l0, int w, uint64_t (&k)[4], bool (&a)[4]) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            act[t] = g + 16 * t < W && l + g + 16 * t < n;
+            a[t] = g + 16 * t < w && l0 + g + 16 * t < n;
+            if (a[t]) k[t] = h[l0 + g + 16 * t];
+        }
+    };
+    load_keys(l, W, key, act);
+    while (l < n) {
+        ulonglong2 v[4];
+        uint32_t bkt[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
             if (act[t]) {
-                key[t] = h[l + g + 16 * t];
                 bkt[t] = bucket_of(key[t], nb);
                 v[t] = *reinterpret_cast<const ulonglong2*>(table + (int64_t)bkt[t] * kBucketKeys + q * 2);
             }
         }
+        const int64_t ln = l + W < n ? l + W : n;
+        const int Wn = W * 2 > 64 ? 64 : W * 2;
+        uint64_t nkey[4];
+        bool nact[4];
+        load_keys(ln, Wn, nkey, nact);
         int64_t stop = -1;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -141,8 +154,13 @@ __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ 
             if (miss) stop = l + 16 * t + ((__ffsll((long long)miss) - 1) >> 2);
         }
         if (stop >= 0) return stop;
-        l = l + W < n ? l + W : n;
-        W = W * 2 > 64 ? 64 : W * 2;
+        l = ln;
+        W = Wn;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            key[t] = nkey[t];
+            act[t] = nact[t];
+        }
     }
     return l;
 }
