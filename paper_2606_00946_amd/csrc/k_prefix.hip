@@ -94,9 +94,9 @@ __device__ __forceinline__ int64_t extend_run(const uint64_t* __restrict__ table
 // window starts at 4 and doubles after every all-hit round (4, 8, ..., 64):
 // long runs advance 64 blocks per dependent round, short ones waste little.
 __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
-                                                   const uint64_t* __restrict__ h, int64_t n, int64_t l, int lane) {
+                                                   const uint64_t* __restrict__ h, int64_t n, int64_t l, int lane,
+                                                   int W = 4) {
     const int g = lane >> 2, q = lane & 3, shift = g * 4;
-    int W = 4;
     // the window's block hashes; the next window's are read while this one's
     // buckets are in flight (used only if every probe of this window hits)
     uint64_t key[4];
@@ -565,7 +565,7 @@ __global__ __launch_bounds__(256) void leaders_rest_kernel(ProbeTables T, int32_
         const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
         const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
         const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
-        const int64_t l = extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane);
+        const int64_t l = extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane, 16);
         if (lane == 0) overlap[r * N + i] = (int32_t)l;
     }
 }
