@@ -308,9 +308,11 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
                                                         int32_t* __restrict__ leaders, uint32_t* __restrict__ n_leaders,
                                                         uint64_t* __restrict__ qkeys, uint32_t G,
                                                         int32_t* __restrict__ cont_of, int join) {
-    const int lane = threadIdx.x & 63;
-    const int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-    if (r >= R) return;
+    // 16 lanes per request (four requests per wave): the chain of dependent
+    // reads before the compare is the cost, so more requests in flight pay
+    const int lane = threadIdx.x & 63, sg = lane >> 4, sl = lane & 15;
+    const int64_t r = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 4 + sg;
+    if (r >= R) return;                               // uniform over the 16 lanes
     const int32_t slot = slot_of[r];
     const int64_t lead = slot < 0 ? r : (int64_t)(0xFFFFFFFFu - (uint32_t)(glead[slot] & 0xFFFFFFFFull));
     const int64_t n = req_off[r + 1] - req_off[r];
@@ -321,17 +323,17 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
         const int64_t nl = req_off[lead + 1] - req_off[lead];
         const int64_t m = n < nl ? n : nl;
         c = m;
-        for (int64_t j0 = 0; j0 < m; j0 += 64) {
-            const int64_t j = j0 + lane;
+        for (int64_t j0 = 0; j0 < m; j0 += 16) {
+            const int64_t j = j0 + sl;
             const bool diff = j < m && a[j] != b[j];
-            const uint64_t mask = __ballot(diff);
+            const uint32_t mask = (uint32_t)(__ballot(diff) >> (16 * sg)) & 0xFFFFu;
             if (mask) {
-                c = j0 + __ffsll((long long)mask) - 1;
+                c = j0 + __ffs((int)mask) - 1;
                 break;
             }
         }
     }
-    if (lane == 0) {
+    if (sl == 0) {
         lead_of[r] = (int32_t)lead;
         lcp_of[r] = (int32_t)c;
         if (lead == r) leaders[atomicAdd(n_leaders, 1u)] = (int32_t)r;
@@ -703,7 +705,7 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_insert_kernel, dim3((uint32_t)(((int64_t)R + kGroupThreads - 1) / kGroupThreads)),
                        dim3(kGroupThreads), 0, s, R, req_off, req_hashes, gkeys, glead, (uint32_t)G, slot_of);
-    hipLaunchKernelGGL(group_lcp_kernel, dim3((uint32_t)(((int64_t)R + 3) / 4)), dim3(256), 0, s, R, req_off,
+    hipLaunchKernelGGL(group_lcp_kernel, dim3((uint32_t)(((int64_t)R + 15) / 16)), dim3(256), 0, s, R, req_off,
                        req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qkeys, (uint32_t)G, cont_of,
                        join ? 1 : 0);
     if (join) {
