@@ -578,10 +578,16 @@ __global__ __launch_bounds__(256) void leaders_rest_kernel(ProbeTables T, int32_
 // list (counted in LDS, so no global counter is shared).
 constexpr int kResolveThreads = 1024;
 
+// VEC (N a multiple of 4, the overlap matrix 16-byte aligned): a thread takes
+// four consecutive instances of one request, reads the leader's four overlaps
+// as one 16-byte word and writes its four back as one when all are resolved;
+// the chunk is then a multiple of 4.
+template <bool VEC>
 __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
     int32_t R, int32_t N, int64_t chunk, const int32_t* __restrict__ lead_of, const int32_t* __restrict__ lcp_of,
     const int32_t* __restrict__ cont_of, const uint32_t* __restrict__ qseen, int32_t* __restrict__ overlap,
     int64_t* __restrict__ list, uint32_t* __restrict__ n_list) {
+    constexpr int V = VEC ? 4 : 1;
     __shared__ uint32_t lcount;
     if (threadIdx.x == 0) lcount = 0u;
     __syncthreads();
@@ -590,32 +596,54 @@ __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
     const int64_t p_begin = (int64_t)blockIdx.x * chunk;
     const int64_t p_end = p_begin + chunk < pairs ? p_begin + chunk : pairs;
     int64_t* __restrict__ mine = list + p_begin;
-    for (int64_t p0 = p_begin; p0 < p_end; p0 += kResolveThreads) {
-        const int64_t pair = p0 + threadIdx.x;
-        bool push = false;
+    for (int64_t p0 = p_begin; p0 < p_end; p0 += V * kResolveThreads) {
+        const int64_t pair = p0 + V * (int64_t)threadIdx.x;
+        uint32_t push = 0;                              // bit j: pair + j goes on the probe list
         if (pair < p_end) {
             const int64_t r = pair / N, i = pair - r * N;
             const int64_t lead = lead_of[r];
             if (lead != r) {
                 const int32_t c = lcp_of[r];
-                const int32_t ll = overlap[lead * N + i];
-                if (ll < c) {
-                    overlap[pair] = ll;
+                const int32_t cont = cont_of[r];
+                // the prompt ends in the shared prefix, or block c is cached nowhere
+                const bool at_c = cont == kContNone || (cont >= 0 && qseen[cont] == 0u);
+                int32_t ll[V], out[V];
+                if constexpr (VEC) {
+                    const int4 q = *reinterpret_cast<const int4*>(overlap + lead * N + i);
+                    ll[0] = q.x; ll[1] = q.y; ll[2] = q.z; ll[3] = q.w;
                 } else {
-                    const int32_t cont = cont_of[r];
-                    if (cont == kContNone) overlap[pair] = c;                    // the prompt ends in the shared prefix
-                    else if (cont >= 0 && qseen[cont] == 0u) overlap[pair] = c;  // block c is cached nowhere
-                    else push = true;
+                    ll[0] = overlap[lead * N + i];
+                }
+#pragma unroll
+                for (int j = 0; j < V; ++j) {
+                    out[j] = ll[j] < c ? ll[j] : c;
+                    if (ll[j] >= c && !at_c) push |= 1u << j;
+                }
+                if (VEC && push == 0) {
+                    *reinterpret_cast<int4*>(overlap + pair) = int4{out[0], out[V > 1 ? 1 : 0], out[V > 2 ? 2 : 0],
+                                                                    out[V > 3 ? 3 : 0]};
+                } else {
+#pragma unroll
+                    for (int j = 0; j < V; ++j)
+                        if (!((push >> j) & 1u)) overlap[pair + j] = out[j];
                 }
             }
         }
-        const uint64_t m = __ballot(push);
-        if (m) {
-            const int first = __ffsll((long long)m) - 1;
+        const uint32_t cnt = (uint32_t)__popc(push);
+        uint32_t incl = cnt;                            // inclusive scan over the wave
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t up = __shfl_up(incl, d);
+            if (lane >= d) incl += up;
+        }
+        const uint32_t total = __shfl(incl, 63);
+        if (total) {
             uint32_t base = 0;
-            if (lane == first) base = atomicAdd(&lcount, (uint32_t)__popcll(m));
-            base = (uint32_t)__shfl((int)base, first);
-            if (push) mine[base + __popcll(m & ((1ull << lane) - 1))] = pair;
+            if (lane == 63) base = atomicAdd(&lcount, total);
+            base = (uint32_t)__shfl((int)base, 63) + incl - cnt;
+#pragma unroll
+            for (int j = 0; j < V; ++j)
+                if ((push >> j) & 1u) mine[base++] = pair + j;
         }
     }
     __syncthreads();
@@ -740,13 +768,19 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
                            leaders, list, n_leaders + 1, overlap);
     }
     // followers: slices of pairs, one workgroup each
+    const bool vec = N % 4 == 0 && (uintptr_t)overlap % 16 == 0;
     int64_t slices = (pairs + kResolveThreads - 1) / kResolveThreads;
     if (slices > (int64_t)n_cu * 8) slices = (int64_t)n_cu * 8;
     if (slices > kMaxSlices) slices = kMaxSlices;
-    const int64_t chunk = (pairs + slices - 1) / slices;
+    int64_t chunk = (pairs + slices - 1) / slices;
+    if (vec) chunk = (chunk + 3) & ~int64_t(3);
     slices = (pairs + chunk - 1) / chunk;
-    hipLaunchKernelGGL(followers_resolve_kernel, dim3((uint32_t)slices), dim3(kResolveThreads), 0, s, R, N, chunk,
-                       lead_of, lcp_of, cont_of, qseen, overlap, list, n_list);
+    if (vec)
+        hipLaunchKernelGGL(followers_resolve_kernel<true>, dim3((uint32_t)slices), dim3(kResolveThreads), 0, s, R, N,
+                           chunk, lead_of, lcp_of, cont_of, qseen, overlap, list, n_list);
+    else
+        hipLaunchKernelGGL(followers_resolve_kernel<false>, dim3((uint32_t)slices), dim3(kResolveThreads), 0, s, R, N,
+                           chunk, lead_of, lcp_of, cont_of, qseen, overlap, list, n_list);
     hipLaunchKernelGGL(followers_probe_kernel, dim3((uint32_t)slices), dim3(256), 0, s, T, N, chunk, req_off,
                        req_hashes, lcp_of, list, n_list, overlap);
     return hipGetLastError();
