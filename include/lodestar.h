@@ -25,7 +25,10 @@
  *   - A context is not thread-safe: use one per host thread, or serialise.
  *   - The library owns its tables, model copies and workspace (hipMalloc);
  *     workspace grows on demand, so a call that needs more than any earlier
- *     call may allocate.
+ *     call may allocate.  Growth is ordered on the call's stream (the
+ *     stream-ordered allocator: the old buffer is freed after the work already
+ *     enqueued on that stream), so it neither waits for the device nor stalls
+ *     other streams.
  */
 #ifndef LODESTAR_H
 #define LODESTAR_H
@@ -152,7 +155,7 @@ int ls_load_cache_state(ls_ctx* ctx, int32_t n_instances, const int64_t* inst_of
  *   2^20 - 2 commits per load (LS_ERR_STATE); n_r <= 2^20 is the caller's
  *   (later blocks share the last rank).  LS_ERR_STATE unless the state was
  *   loaded under ls_set_cache_capacity.  Asynchronous; the library-owned
- *   workspace grows (synchronizing the device) when a batch needs more.
+ *   workspace grows (stream-ordered) when a batch needs more.
  *
  * ls_read_cache_state
  *   Synchronous.  inst_off HOST int64 [n_instances + 1] out: the lists'
@@ -184,6 +187,12 @@ int ls_read_cache_state(ls_ctx* ctx, int32_t n_instances, int64_t* inst_off, uin
  *                              is strictly sequential)
  *   feat_out    fp32  [R x d]  raw feature row of the chosen pair (the training record)
  * R = 0 is a no-op.  N must equal the loaded instance count (LS_ERR_STATE).
+ * Every returned value is the canonical one (the fp32 fma chains, or in bf16
+ * mode bf16 operands with fp32 fma chains, bias first, inputs ascending).  On an
+ * LS_BF16 context a call with scores == NULL scores on the matrix cores and
+ * rescores the candidate band canonically (ls_set_exact_scores); a call that asks
+ * for `scores` runs the canonical chain on every pair, so that the whole matrix
+ * is canonical (much slower at large R x N).
  */
 int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
                    const int64_t* req_off, const uint64_t* req_hashes, const int32_t* prompt_len,
@@ -192,15 +201,40 @@ int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
                    void* stream);
 
 /*
- * Scoring precision of an LS_BF16 context.  By default the bf16 model runs on
- * the matrix cores; every candidate whose fast score lies within an error band
- * of its request's best is then rescored with the canonical fp32 chain, and the
- * decision (`chosen`) and `min_ttft` come from those canonical scores.  Scores
- * outside the band are the fast ones.  enable != 0 scores every pair with the
- * canonical chain instead (exact `scores`, slower).  fp32 contexts always use
- * the canonical chain.  Takes effect for later ls_score_batch calls.
+ * Scoring precision of an LS_BF16 context.  By default a call that does not ask
+ * for the score matrix runs the bf16 model on the matrix cores; every candidate
+ * whose fast score lies within the error band of its request's best (see
+ * ls_fast_scores) is then rescored with the canonical chain, and the decision
+ * (`chosen`) and `min_ttft` come from those canonical scores.  enable != 0 runs
+ * the canonical chain on every pair of every call instead.  fp32 contexts
+ * always use the canonical chain.  Takes effect for later scoring calls.
  */
 int ls_set_exact_scores(ls_ctx* ctx, int enable);
+
+/*
+ * Validation aid for the matrix-core path of an LS_BF16 context (Section 4.1,
+ * the batched forward of Alg. 4): for every pair of the batch, the fast score t
+ * before any rescoring and its error scale err = 2^-7 (sum_j |w3_j| h2_j + |b3|)
+ * -- w3, b3 the output layer, h2 the pair's last hidden activations on the
+ * matrix cores.  band (nullable) gets 1 for the pairs a scoring call would
+ * rescore (t - err <= min over the request of t + err, or a non-finite value),
+ * else 0.  DEVICE arrays: t, err fp32 [R x N], band uint8 [R x N], inputs as in
+ * ls_score_batch.  Decisions are exact whenever |t - t_canonical| <= err for
+ * every pair outside the band.  LS_ERR_UNSUPPORTED if the context's model does
+ * not run on the matrix cores (fp32, or a shape without a matrix-core kernel).
+ */
+int ls_fast_scores(ls_ctx* ctx, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                   const int32_t* prompt_len, const float* inst_feat, float* t, float* err, uint8_t* band,
+                   void* stream);
+
+/*
+ * Launch geometry: persistent and grid-stride kernels are sized for n compute
+ * units (n = 0: all of the device's; a larger n is clamped to them), e.g. to
+ * leave part of the GPU to other work.  Every result is independent of n: the
+ * kernels fix their summation orders and partitions by the data, not by the
+ * grid.  LS_ERR_INVALID for n < 0.  Takes effect for later calls.
+ */
+int ls_set_cu_limit(ls_ctx* ctx, int n);
 
 /*
  * How ls_score_batch finds the overlap of followers -- requests whose first

@@ -41,7 +41,8 @@ struct ls_ctx {
     uint64_t drop_seed = 0, drop_step = 0;
     int prefix_join = 0;     // 0 decide per call, 1 always, 2 never
     bool prefix_closed = false;
-    int n_cu = 1;
+    int n_cu = 1;            // compute units the launches are sized for (ls_set_cu_limit)
+    int n_cu_dev = 1;        // compute units of the device
     // cache state
     ls::CacheTables tables;
     int64_t table_cap_buckets = 0;
@@ -213,17 +214,19 @@ int stage_copy(ls_ctx* c, void* dst, size_t bytes, hipStream_t s) {
     return LS_OK;
 }
 
-// Grow-only device buffer; waits for outstanding device work before freeing.
-int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes) {
+// Grow-only device buffer, ordered on the stream of the call that needs it:
+// the old buffer is released by hipFreeAsync after the work already enqueued on
+// `s` (its last users), and the new one comes from the stream-ordered
+// allocator, so growing never waits for the device or for other streams.
+int grow(ls_ctx* c, void** p, size_t* cap, size_t bytes, hipStream_t s) {
     if (bytes <= *cap) return LS_OK;
     if (*p) {
-        LS_HIP(c, hipDeviceSynchronize());
-        LS_HIP(c, hipFree(*p));
+        LS_HIP(c, hipFreeAsync(*p, s));
         *p = nullptr;
         *cap = 0;
     }
     size_t want = (size_t)round_up((int64_t)bytes, 1 << 20);
-    if (hipMalloc(p, want) != hipSuccess) {
+    if (hipMallocAsync(p, want, s) != hipSuccess) {
         *p = nullptr;
         (void)hipGetLastError();
         return fail(c, LS_ERR_NOMEM, "device allocation of %zu bytes failed", want);
@@ -388,7 +391,8 @@ int ls_create(const ls_model_config* cfg, int device, ls_ctx** out) {
     ok = ok && hipMalloc((void**)&c->mu, sizeof(float) * cfg->d) == hipSuccess;
     ok = ok && hipMalloc((void**)&c->isig, sizeof(float) * cfg->d) == hipSuccess;
     ok = ok && hipEventCreateWithFlags(&c->stage_done, hipEventDisableTiming) == hipSuccess;
-    ok = ok && hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess;
+    ok = ok && hipDeviceGetAttribute(&c->n_cu_dev, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess;
+    c->n_cu = c->n_cu_dev;
     if (ok && ls::mfma_supported(c->dims)) {
         const ls::MfmaLayout L = ls::make_mfma_layout(c->dims);
         ok = hipMalloc((void**)&c->frag16, sizeof(uint16_t) * L.n16) == hipSuccess &&
@@ -516,17 +520,17 @@ int index_load(ls_ctx* c, int32_t N, int64_t total, int64_t list_entries, const 
     auto& X = c->idx;
     const size_t lb = sizeof(uint64_t) * (size_t)(list_entries > 0 ? list_entries : 1);
     int rc;
-    if ((rc = grow(c, (void**)&X.hash, &X.hash_cap, lb)) || (rc = grow(c, (void**)&X.stamp, &X.stamp_cap, lb)) ||
-        (rc = grow(c, (void**)&X.hash2, &X.hash2_cap, lb)) || (rc = grow(c, (void**)&X.stamp2, &X.stamp2_cap, lb)))
+    if ((rc = grow(c, (void**)&X.hash, &X.hash_cap, lb, s)) || (rc = grow(c, (void**)&X.stamp, &X.stamp_cap, lb, s)) ||
+        (rc = grow(c, (void**)&X.hash2, &X.hash2_cap, lb, s)) || (rc = grow(c, (void**)&X.stamp2, &X.stamp2_cap, lb, s)))
         return rc;
     const int64_t slots = c->tables.total_buckets * ls::kBucketKeys;
-    if ((rc = grow(c, (void**)&X.entry_of, &X.entry_cap, sizeof(uint32_t) * (size_t)slots))) return rc;
-    if ((rc = grow(c, (void**)&X.small, &X.small_cap, sizeof(int64_t) * (size_t)(kIndexSmallPerN * N + 4))))
+    if ((rc = grow(c, (void**)&X.entry_of, &X.entry_cap, sizeof(uint32_t) * (size_t)slots, s))) return rc;
+    if ((rc = grow(c, (void**)&X.small, &X.small_cap, sizeof(int64_t) * (size_t)(kIndexSmallPerN * N + 4), s)))
         return rc;
-    if ((rc = grow(c, &X.ws, &X.ws_cap, (size_t)(total > 0 ? total : 1)))) return rc;
+    if ((rc = grow(c, &X.ws, &X.ws_cap, (size_t)(total > 0 ? total : 1), s))) return rc;
     const size_t tw =
         (size_t)ls::table_build_workspace_bytes(list_entries, (int32_t)c->tables_nseg, c->tables.total_buckets);
-    if ((rc = grow(c, &c->tws, &c->tws_cap, tw))) return rc;
+    if ((rc = grow(c, &c->tws, &c->tws_cap, tw, s))) return rc;
     X.list_entries = list_entries;
     IndexSmall m = index_small(X.small, N);
     X.off = m.off_a;
@@ -608,10 +612,10 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
         return fail(c, LS_ERR_UNSUPPORTED, "capacities above 2^32 - 1 cached blocks in all");
     // device buffers
     size_t cap = (size_t)c->table_cap_buckets * ls::kBucketKeys * sizeof(uint64_t);
-    int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t));
+    int rc = grow(c, (void**)&c->tables.keys, &cap, (size_t)nbk * ls::kBucketKeys * sizeof(uint64_t), s);
     if (rc) return rc;
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
-    rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg, nbk));
+    rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg, nbk), s);
     if (rc) return rc;
     // metadata: bases, bucket counts, offsets and first segments, laid out in
     // one block (as in the pinned staging buffer) so that one copy moves them
@@ -687,10 +691,15 @@ int check_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const u
 }
 
 // Workspace of the scoring pipeline.
-size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool have_scores) {
+// Whether a scoring call runs the bf16 model on the matrix cores: only when the
+// caller does not ask for the score matrix, whose every entry must then be the
+// canonical score (the matrix-core path keeps canonical scores for the
+// candidate band alone).
+bool fast_path(const ls_ctx* c, const float* scores) { return c->frag16 && !c->exact_scores && scores == nullptr; }
+
+size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool have_scores, bool fast) {
     const ls::ModelDims& m = c->dims;
     const int64_t pairs = (int64_t)R * N;
-    const bool fast = c->frag16 && !c->exact_scores;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
     need += (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256);
     if (m.L != 2) need += (size_t)round_up(4 * ls::generic_score_floats(m, pairs), 256);
@@ -716,11 +725,10 @@ struct Scored {
 // stats widen the band for the routing policy (delta < 0, k_filter 0: argmin
 // only).
 int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
-                 const int32_t* prompt_len, const float* inst_feat, int32_t* overlap, float* scores, double delta,
-                 int32_t k_filter, const ls::PolicyStats* stats, hipStream_t s, Scored* out) {
+                 const int32_t* prompt_len, const float* inst_feat, int32_t* overlap, float* scores, bool fast,
+                 double delta, int32_t k_filter, const ls::PolicyStats* stats, hipStream_t s, Scored* out) {
     const ls::ModelDims& m = c->dims;
     const int64_t pairs = (int64_t)R * N;
-    const bool fast = c->frag16 && !c->exact_scores;
     float* part_t = w.take<float>((int64_t)m.h1 * N);
     char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R, N));
     int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
@@ -782,16 +790,59 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     DeviceScope dev(c->device);
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
-    rc = grow(c, &c->ws, &c->ws_cap, pipeline_bytes(c, R, N, overlap != nullptr, scores != nullptr));
+    const bool fast = fast_path(c, scores);
+    rc = grow(c, &c->ws, &c->ws_cap, pipeline_bytes(c, R, N, overlap != nullptr, scores != nullptr, fast), s);
     if (rc) return rc;
     WsCarve w{(char*)c->ws};
     Scored out;
-    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, -1.0, 0, nullptr, s,
-                      &out);
+    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, fast, -1.0, 0, nullptr,
+                      s, &out);
     if (rc) return rc;
     LS_TIMED(c, K_ARGMIN, s,
              ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov, inst_feat, chosen, min_ttft,
                                feat_out, s));
+    return LS_OK;
+}
+
+int ls_fast_scores(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                   const int32_t* prompt_len, const float* inst_feat, float* t, float* err, uint8_t* band,
+                   void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (!c->frag16) return fail(c, LS_ERR_UNSUPPORTED, "this model is not scored on the matrix cores");
+    if (R > 0 && (!t || !err)) return fail(c, LS_ERR_INVALID, "t and err must be non-NULL");
+    int rc;
+    // check_batch only tests `chosen` for NULL; t stands in for it
+    if (check_batch(c, R, N, req_off, req_hashes, prompt_len, inst_feat, reinterpret_cast<const int32_t*>(t), &rc))
+        return rc;
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    const ls::ModelDims& m = c->dims;
+    const int64_t pairs = (int64_t)R * N;
+    size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256) + (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256) +
+                  (size_t)round_up(pairs * 4, 256) + (size_t)round_up(pairs * 8, 256) + 256;
+    rc = grow(c, &c->ws, &c->ws_cap, need, s);
+    if (rc) return rc;
+    WsCarve w{(char*)c->ws};
+    float* part_t = w.take<float>((int64_t)m.h1 * N);
+    char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R, N));
+    int32_t* ov = w.take<int32_t>(pairs);
+    int64_t* list = w.take<int64_t>(pairs);
+    uint32_t* count = w.take<uint32_t>(64);
+    LS_TIMED(c, K_PREFIX, s,
+             ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu,
+                                     ls::prefix_use_join(R, N, c->tables.total_buckets * ls::kBucketKeys,
+                                                         c->prefix_join),
+                                     c->prefix_closed, s));
+    LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
+    LS_TIMED(c, K_SCORE_MFMA, s,
+             ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N, req_off,
+                                         prompt_len, ov, t, err, c->n_cu, s));
+    if (band) {
+        LS_TIMED(c, K_BAND, s, ls::launch_fill_u32(count, 0u, 1, s));
+        LS_TIMED(c, K_BAND, s, ls::launch_band_select(R, N, t, err, band, list, count, s));
+    }
     return LS_OK;
 }
 
@@ -826,9 +877,10 @@ int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const 
     DeviceScope dev(c->device);
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
-    size_t need = pipeline_bytes(c, R, N, false, false);
+    const bool fast = fast_path(c, nullptr);
+    size_t need = pipeline_bytes(c, R, N, false, false, fast);
     need += (size_t)round_up((int64_t)N * 8, 256) + 256 + (size_t)round_up((int64_t)2 * m.d * 4, 256);
-    rc = grow(c, &c->ws, &c->ws_cap, need);
+    rc = grow(c, &c->ws, &c->ws_cap, need, s);
     if (rc) return rc;
     WsCarve w{(char*)c->ws};
     double* cnt = w.take<double>(N);
@@ -862,7 +914,7 @@ int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const 
     }
     LS_TIMED(c, K_ROUTE, s, ls::launch_policy_stats(P, inst_feat, N, d_inst, cnt, st, s));
     Scored out;
-    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, nullptr, nullptr, pol->delta,
+    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, nullptr, nullptr, fast, pol->delta,
                       pol->k_filter, st, s, &out);
     if (rc) return rc;
     LS_TIMED(c, K_ROUTE, s,
@@ -875,6 +927,14 @@ int ls_set_exact_scores(ls_ctx* c, int enable) {
     if (!c) return LS_ERR_INVALID;
     c->err.clear();
     c->exact_scores = enable != 0;
+    return LS_OK;
+}
+
+int ls_set_cu_limit(ls_ctx* c, int n) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (n < 0) return fail(c, LS_ERR_INVALID, "the compute-unit limit must be >= 0");
+    c->n_cu = (n == 0 || n > c->n_cu_dev) ? c->n_cu_dev : n;
     return LS_OK;
 }
 
@@ -905,7 +965,7 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
     hipStream_t s = (hipStream_t)stream;
     int64_t need = ls::update_workspace_bytes(c->dims, B);
-    int rc = grow(c, &c->upd_ws, &c->upd_ws_cap, (size_t)need);
+    int rc = grow(c, &c->upd_ws, &c->upd_ws_cap, (size_t)need, s);
     if (rc) return rc;
     if (c->drop_p > 0.0 && B >= (1 << 24)) return fail(c, LS_ERR_INVALID, "B must be below 2^24 with dropout");
     const ls::DropArgs D = next_drop(c);
@@ -1019,7 +1079,7 @@ int ls_buffer_push(ls_ctx* c, int32_t B, const float* feats, const float* ttft, 
                   + (size_t)round_up(ch * rcap * 8, 256) + (size_t)round_up(ch * ch * 8, 256)     // chunk distances
                   + (size_t)round_up(rcap * 4, 256)                                              // slot origins
                   + (size_t)round_up((ch + 1) * 4, 256);                                         // slots taken
-    int rc = grow(c, &bf.ws, &bf.ws_cap, need);
+    int rc = grow(c, &bf.ws, &bf.ws_cap, need, s);
     if (rc) return rc;
     WsCarve w{(char*)bf.ws};
     int32_t* codes = w.take<int32_t>(nc + B);
@@ -1134,7 +1194,7 @@ int ls_train_round(ls_ctx* c, int32_t epochs, int32_t batch, float lr, const int
     const int d = m.d;
     size_t need = (size_t)round_up((int64_t)epochs * n * 4, 256) + (size_t)round_up((int64_t)batch * (d + 1) * 4, 256) +
                   512 + (size_t)round_up(ls::update_workspace_bytes(m, batch), 256);
-    int rc = grow(c, &bf.ws, &bf.ws_cap, need);
+    int rc = grow(c, &bf.ws, &bf.ws_cap, need, s);
     if (rc) return rc;
     WsCarve w{(char*)bf.ws};
     int32_t* dcodes = w.take<int32_t>((int64_t)epochs * n);
@@ -1256,7 +1316,7 @@ int ls_commit_routes(ls_ctx* c, int32_t R, int64_t n_hashes, const int64_t* req_
     // batch-local sets: at most n_hashes / 4 + N + 1 buckets of 8 keys and 8
     // stamps; then the selection histograms [N x 256]
     const int64_t fslots = (n_hashes / 4 + N + 1) * ls::kBucketKeys;
-    int rc = grow(c, &X.ws, &X.ws_cap, sizeof(uint64_t) * 2 * (size_t)fslots + sizeof(uint32_t) * 256 * (size_t)N);
+    int rc = grow(c, &X.ws, &X.ws_cap, sizeof(uint64_t) * 2 * (size_t)fslots + sizeof(uint32_t) * 256 * (size_t)N, s);
     if (rc) return rc;
     IndexSmall m = index_small(X.small, N);
     ls::IndexCommit C;

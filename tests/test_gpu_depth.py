@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_helpers import GpuRun, layer_slices, note, rel_ok, to_dev
+from gpu_helpers import GpuRun, fp32_bound_ok, grad_ok, layer_slices, note, rel_ok, to_dev
 from paper_2606_00946_amd import lodestar, synth
 
 pytestmark = pytest.mark.gpu
@@ -46,8 +46,8 @@ def test_depth_scores_are_canonical(hidden, dtype):
     if dtype == "fp32":
         ref64 = oracle.score("f64", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
                              w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=16)
-        ok, worst = rel_ok(out["scores"], ref64["scores"], 1e-4)
-        assert ok, worst
+        ok, worst = fp32_bound_ok(w, sel, out["overlap"], out["scores"], ref64["scores"])
+        assert ok, f"scores vs double-precision definition: {worst} times the bar"
     run.ctx.close()
 
 
@@ -58,9 +58,9 @@ def compare_update(w, got, ref, feats):
         g, r = got["grad"][a:b], ref["grad"][a:b]
         nrm = np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)
         assert nrm <= 1e-4, f"{lname}: norm-wise relative gradient error {nrm}"
-        ok, worst = rel_ok(g, r, 1e-4)
+        ok, worst, worst3 = grad_ok(g, r)
         assert ok, f"{lname}: elementwise gradient error {worst}"
-        report.append(f"{lname} {worst:.1e}")
+        report.append(f"{lname} {worst:.1e} ({worst3:.1e} at a 1e-3 floor)")
         dg = got["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
         dr = ref["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
         ulp = np.spacing(np.abs(ref["params"][a:b])).astype(np.float64)
@@ -128,10 +128,14 @@ def test_dropout_train_round_paper_model():
     got, _, _ = ctx.ls_get_model()
     ref, ref_loss = oracle.train_round("fp32", cfg.hidden, w.params, w.mu, w.inv_sigma, buf, 2, 8, w.lr, perm,
                                        dropout=(0.1, 77, 0))
+    worst = []
     for lname, a, b in layer_slices(cfg.d, cfg.hidden):
         d = got[a:b].astype(np.float64) - w.params[a:b]
         r = ref[a:b].astype(np.float64) - w.params[a:b]
-        assert np.linalg.norm(d - r) <= 1e-3 * max(np.linalg.norm(r), 1e-30), lname
+        rel = np.linalg.norm(d - r) / max(np.linalg.norm(r), 1e-30)
+        worst.append(f"{lname} {rel:.1e}")
+        assert rel <= 1e-4, f"{lname}: weight change off by {rel:.2e} in norm"
+    print("dropout round, weight change vs oracle (norm-wise): " + ", ".join(worst), flush=True)
     assert abs(float(loss.cpu()[0]) - ref_loss) <= 1e-4 * abs(ref_loss)
     ctx.close()
 

@@ -15,13 +15,13 @@ import pytest
 
 import oracle
 import oracle_pins
-from gpu_helpers import BAND_REL, GpuRun, head_magnitude, layer_slices, note, rel_ok, to_dev, uses_fast_path
+from gpu_helpers import GpuRun, band_check, fp32_bound_ok, grad_ok, layer_slices, note, rel_ok, to_dev, uses_fast_path
 from paper_2606_00946_amd import lodestar, synth
 
 pytestmark = pytest.mark.gpu
 
 CONFIGS = ["tiny", "homogeneous", "heterogeneous", "long_context", "large_batch"]
-FULL_SCORE = {"tiny", "homogeneous"}            # oracle scores every pair; others use sampled requests
+FULL_SCORE = {"tiny", "homogeneous", "heterogeneous", "long_context"}   # the oracle scores every pair
 
 
 @functools.lru_cache(maxsize=2)
@@ -35,7 +35,7 @@ def mode_of(w):
 
 def sampled(w, k=96, seed=0):
     R = w.cfg.R
-    if w.cfg.name in FULL_SCORE and R * w.cfg.N <= 200_000:
+    if w.cfg.name in FULL_SCORE and R * w.cfg.N <= 600_000:
         return np.arange(R, dtype=np.int32)
     rng = np.random.default_rng(seed)
     sel = np.unique(np.concatenate([[0, R - 1], rng.choice(R, k, replace=False)]))
@@ -47,11 +47,15 @@ def oracle_score(w, mode, sel):
                         w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=16)
 
 
-def check_scoring(w, out, sel, exact=False):
-    """Overlaps, decisions, min_ttft and feature rows bit-exact.  Scores: bit-exact
-    on the canonical path; on the bf16 matrix-core path every sampled score must
-    lie within an eighth of the band half-width E of the canonical one (E is the
-    bound the decision relies on, so this validates it with a margin of 8)."""
+def check_scoring(w, out, sel, exact=False, run=None):
+    """`out` is a call that asked for the score matrix, so every score is the
+    canonical one: overlaps, decisions, min_ttft, feature rows and scores
+    bit-exact against the oracle in the kernel's precision on the selected
+    requests (and fp32 scores within 1e-4 of the double-precision definition).
+    With `run` on a context whose bf16 model runs on the matrix cores, the
+    matrix-core call's decisions, minima, overlaps and rows must equal the
+    canonical call's on every request, and every fast score must lie within
+    E/8 of the canonical one (the bound the decision relies on, with a margin)."""
     mode = mode_of(w)
     ref = oracle_score(w, mode, sel)
     np.testing.assert_array_equal(out["overlap"][sel], ref["overlap"])
@@ -60,23 +64,24 @@ def check_scoring(w, out, sel, exact=False):
     np.testing.assert_array_equal(out["feat"][sel], ref["feat"].astype(np.float32))
     got = out["scores"][sel]
     want = ref["scores"].astype(np.float32)
-    if uses_fast_path(w.cfg.d, w.cfg.hidden, w.cfg.dtype, exact):
-        rows = np.stack([np.stack([oracle.features("bf16", w.inst_feat[i], w.prompt_len[r], w.req_off[r + 1] - w.req_off[r],
-                                                   ref["overlap"][q, i]) for i in range(w.cfg.N)])
-                         for q, r in enumerate(sel)])
-        E = BAND_REL * head_magnitude(w, rows.reshape(-1, w.cfg.d)).reshape(got.shape)
-        ratio = np.abs(got.astype(np.float64) - want) / E
-        print(f"fast-path |score - canonical| / E: max {ratio.max():.4f}  p99.9 {np.percentile(ratio, 99.9):.4f}  "
-              f"exact {np.mean(ratio == 0):.3f}", flush=True)
-        assert ratio.max() <= 0.125, f"fast score off by {ratio.max():.3f} E"
-    else:
-        mism = np.argwhere(got.view(np.uint32) != want.view(np.uint32))
-        assert mism.size == 0, f"{len(mism)} scores differ from the oracle, first {mism[:3]}"
+    mism = np.argwhere(got.view(np.uint32) != want.view(np.uint32))
+    assert mism.size == 0, f"{len(mism)} scores differ from the oracle, first {mism[:3]}"
     if mode == "fp32":
         ref64 = oracle_score(w, "f64", sel)
-        ok, worst = rel_ok(got, ref64["scores"], 1e-4)
-        assert ok, f"scores vs double-precision definition: worst relative error {worst}"
+        ok, worst = fp32_bound_ok(w, sel, out["overlap"][sel], got, ref64["scores"])
+        assert ok, f"scores vs double-precision definition: {worst} times the bar"
+    if run is not None and uses_fast_path(w.cfg.d, w.cfg.hidden, w.cfg.dtype, exact):
+        check_fast_path(w, run, out)
     return ref
+
+
+def check_fast_path(w, run, canon, what=None):
+    """The matrix-core path against a canonical call on the same context."""
+    fast = run.score(with_scores=False)
+    for k in ("overlap", "chosen", "feat"):
+        np.testing.assert_array_equal(fast[k], canon[k], err_msg=k)
+    np.testing.assert_array_equal(fast["min_ttft"].view(np.uint32), canon["min_ttft"].view(np.uint32))
+    band_check(run.fast_scores(), canon["scores"], what or f"{w.cfg.name} R={w.cfg.R} N={w.cfg.N}")
 
 
 @pytest.mark.parametrize("name", CONFIGS)
@@ -87,7 +92,7 @@ def test_score_parity(name):
     out = run.score()
     assert np.all(out["chosen"] >= 0) and np.all(out["chosen"] < w.cfg.N)
     sel = sampled(w)
-    check_scoring(w, out, sel)
+    check_scoring(w, out, sel, run=run)
     if w.cfg.R * w.cfg.N <= 600_000:                 # every overlap, not only the sampled requests
         ov = oracle.overlap(w.req_off, w.req_hashes, w.inst_off, w.inst_hashes, threads=16)
         np.testing.assert_array_equal(out["overlap"], ov)
@@ -96,31 +101,68 @@ def test_score_parity(name):
     assert np.all(out["overlap"] >= 0) and np.all(out["overlap"] <= n[:, None])
     row = np.arange(w.cfg.R)
     assert np.array_equal(out["min_ttft"], out["scores"][row, out["chosen"]])
-    if not uses_fast_path(w.cfg.d, w.cfg.hidden, w.cfg.dtype):
-        # on the canonical path the chosen score is the row minimum; on the fast
-        # path pairs outside the band keep fast scores, checked per sample above
-        assert np.all(out["scores"][row, out["chosen"]][:, None] <= out["scores"])
+    assert np.all(out["scores"][row, out["chosen"]][:, None] <= out["scores"])
     run.ctx.close()
 
 
-def test_bf16_fast_decisions_equal_canonical_at_full_size():
-    """Every one of the 65,536 Large-batch decisions and minimum scores from the
-    matrix-core path equals the canonical path's (which the sampled tests show
-    bit-identical to the oracle)."""
+def _trained_large(kind):
+    """The Large-batch model as it stands after online training on the GPU:
+    'initial' (the seeded model), 'sgd25' (25 ls_update steps on the update rows
+    at the workload's learning rate, as the bench applies), or 'round' (a
+    retraining round over a FIFO and replay pool of 5000 each: 5 epochs of
+    minibatch 256 in a seeded order)."""
+    import torch
     w = workload("large_batch")
-    note("bf16 fast vs canonical, full size")
-    fast = GpuRun(w)
-    a = fast.score()
-    fast.ctx.close()
-    exact = GpuRun(w, exact=True)
-    b = exact.score()
-    exact.ctx.close()
-    np.testing.assert_array_equal(a["overlap"], b["overlap"])
-    np.testing.assert_array_equal(a["chosen"], b["chosen"])
-    np.testing.assert_array_equal(a["min_ttft"].view(np.uint32), b["min_ttft"].view(np.uint32))
-    np.testing.assert_array_equal(a["feat"], b["feat"])
-    same = np.mean(a["scores"].view(np.uint32) == b["scores"].view(np.uint32))
-    print(f"fast scores bitwise canonical: {same:.3f} of {a['scores'].size} pairs", flush=True)
+    if kind == "initial":
+        return w.params
+    cfg = w.cfg
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    x, y = to_dev(w.upd_feats), to_dev(w.upd_ttft)
+    if kind == "sgd25":
+        for _ in range(25):
+            ctx.ls_update(x, y, w.lr)
+    else:
+        ctx.ls_buffer_init(5000, 5000)
+        ctx.ls_buffer_push(x[:11000].contiguous(), y[:11000].contiguous())
+        st = ctx.ls_buffer_state()
+        n = int(st[0]) + int(st[2])
+        perm = np.concatenate([np.random.default_rng(e).permutation(n) for e in range(5)]).astype(np.int32)
+        ctx.ls_train_round(5, 256, w.lr, perm)
+    torch.cuda.synchronize()
+    p = ctx.ls_get_model()[0]
+    ctx.close()
+    assert not np.array_equal(p, w.params)
+    return p
+
+
+@pytest.mark.parametrize("kind", ["initial", "sgd25", "round"])
+def test_large_batch_full_size_oracle_parity(kind):
+    """All 65,536 x 256 Large-batch pairs against the oracle (bf16 mode, every
+    request), for the seeded model and for two trained ones: overlaps, decisions,
+    minima and feature rows of the matrix-core path, and every canonical score,
+    bit-exact; every fast score within E/8 of its canonical value."""
+    w = workload("large_batch")
+    note(f"large_batch full-size oracle parity, model {kind}")
+    params = _trained_large(kind)
+    run = GpuRun(w, params=params)
+    canon = run.score()
+    fast = run.score(with_scores=False)
+    bounds = run.fast_scores()
+    run.ctx.close()
+    note(f"large_batch full-size oracle parity, model {kind}: oracle on 16 threads")
+    ref = oracle.score("bf16", w.cfg.d, w.cfg.hidden, params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                       w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, threads=16)
+    for res in (canon, fast):
+        np.testing.assert_array_equal(res["overlap"], ref["overlap"])
+        np.testing.assert_array_equal(res["chosen"], ref["chosen"])
+        np.testing.assert_array_equal(res["min_ttft"].view(np.uint32),
+                                      ref["min_ttft"].astype(np.float32).view(np.uint32))
+        np.testing.assert_array_equal(res["feat"], ref["feat"].astype(np.float32))
+    want = ref["scores"].astype(np.float32)
+    n_bad = int(np.count_nonzero(canon["scores"].view(np.uint32) != want.view(np.uint32)))
+    assert n_bad == 0, f"{n_bad} canonical scores differ from the oracle"
+    band_check(bounds, want, f"large_batch model {kind}")
 
 
 @pytest.mark.parametrize("base,R,N,cap", [("large_batch", 37, 13, None), ("large_batch", 130, 65, None),
@@ -141,7 +183,7 @@ def test_bf16_matrix_core_ragged(base, R, N, cap):
     assert uses_fast_path(cfg.d, cfg.hidden, cfg.dtype)
     note(f"bf16 matrix-core ragged {base} d={cfg.d} h={cfg.hidden} R={R} N={N}")
     run = GpuRun(w)
-    check_scoring(w, run.score(), np.arange(R, dtype=np.int32))
+    check_scoring(w, run.score(), np.arange(R, dtype=np.int32), run=run)
     run.ctx.close()
 
 
@@ -150,8 +192,12 @@ def test_bf16_exact_mode_matches_oracle_bitwise():
     w = workload("large_batch")
     note("bf16 exact mode large_batch")
     run = GpuRun(w, exact=True)
-    out = run.score()
-    check_scoring(w, out, sampled(w, k=24), exact=True)
+    out = run.score(with_scores=False)
+    sel = sampled(w, k=24)
+    ref = oracle_score(w, "bf16", sel)
+    np.testing.assert_array_equal(out["chosen"][sel], ref["chosen"])
+    np.testing.assert_array_equal(out["min_ttft"][sel].view(np.uint32), ref["min_ttft"].astype(np.float32).view(np.uint32))
+    np.testing.assert_array_equal(out["feat"][sel], ref["feat"].astype(np.float32))
     run.ctx.close()
 
 
@@ -176,9 +222,9 @@ def _check_update(w, feats=None, ttft=None):
         g, r = got["grad"][a:b], ref["grad"][a:b]
         nrm = np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)
         assert nrm <= 1e-4, f"{lname}: norm-wise relative gradient error {nrm}"
-        ok, worst = rel_ok(g, r, 1e-4)
+        ok, worst, worst3 = grad_ok(g, r)
         assert ok, f"{lname}: elementwise gradient error {worst}"
-        report.append(f"{lname} {worst:.1e}")
+        report.append(f"{lname} {worst:.1e} ({worst3:.1e} at a 1e-3 floor)")
         # the step: W' - W against the oracle's, allowing one ulp of W' for the final rounding
         dg = got["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
         dr = ref["params"][a:b].astype(np.float64) - w.params[a:b].astype(np.float64)
@@ -294,12 +340,13 @@ def test_adversarial_overlaps_and_features(dtype):
                        inst_hashes=inst_h, inst_feat=rng.uniform(0, 4, (N, d - 5)).astype(np.float32),
                        params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
                        upd_ttft=base.upd_ttft, lr=base.lr)
-    out = GpuRun(w).score()
+    run = GpuRun(w)
+    out = run.score()
     want = np.array([[oracle_pins._brute_overlap(r, c) for c in
                       [list(inst_h[inst_off[i]:inst_off[i + 1]]) for i in range(N)]]
                      for r in [list(req_h[req_off[k]:req_off[k + 1]]) for k in range(R)]])
     np.testing.assert_array_equal(out["overlap"], want)
-    check_scoring(w, out, np.arange(R, dtype=np.int32))
+    check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
 
 
 _PHI = 0x9E3779B97F4A7C15
@@ -370,11 +417,12 @@ def test_table_overflow_paths(case):
                        inst_feat=np.random.default_rng(5).uniform(0, 4, (N, d - 5)).astype(np.float32),
                        params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
                        upd_ttft=base.upd_ttft, lr=base.lr)
-    out = GpuRun(w).score()
+    run = GpuRun(w)
+    out = run.score()
     want = oracle.overlap(req_off, req_h, inst_off, inst_h)
     np.testing.assert_array_equal(out["overlap"], want)
     assert out["overlap"][0, 0] == len(piles[0])
-    check_scoring(w, out, np.arange(R, dtype=np.int32))
+    check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
 
 
 def _follower_workload(rng):
@@ -415,12 +463,17 @@ def _follower_workload(rng):
     return inst_off, inst_h, req_off, req_h, L
 
 
+@pytest.mark.parametrize("pad", [False, True])
 @pytest.mark.parametrize("mode", [0, 1, 2])
-def test_followers_and_continuations(mode):
+def test_followers_and_continuations(mode, pad):
     """Followers resolved from the leader, through the semi-join of their
-    continuation hashes (mode 1), or by probing (mode 2): identical overlaps."""
-    note(f"followers and continuations, join mode {mode}")
+    continuation hashes (mode 1), or by probing (mode 2): identical overlaps.
+    pad adds an eighth (empty) cache, so that N % 4 == 0 and followers are
+    resolved four instances per thread (mixed hit and miss lanes in one word)."""
+    note(f"followers and continuations, join mode {mode}, padded {pad}")
     inst_off, inst_h, req_off, req_h, L = _follower_workload(np.random.default_rng(21))
+    if pad:
+        inst_off = np.append(inst_off, inst_off[-1])
     base = workload("tiny")
     N, R, d = len(inst_off) - 1, len(req_off) - 1, base.cfg.d
     w = synth.Workload(cfg=synth.dataclasses.replace(base.cfg, R=R, N=N), req_off=req_off, req_hashes=req_h,
@@ -428,11 +481,12 @@ def test_followers_and_continuations(mode):
                        inst_feat=np.random.default_rng(6).uniform(0, 4, (N, d - 5)).astype(np.float32),
                        params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
                        upd_ttft=base.upd_ttft, lr=base.lr)
-    out = GpuRun(w, prefix_join=mode).score()
+    run = GpuRun(w, prefix_join=mode)
+    out = run.score()
     want = oracle.overlap(req_off, req_h, inst_off, inst_h)
     np.testing.assert_array_equal(out["overlap"], want)
     assert want[1, 2] == 8 and want[1, 0] == 6 and want[6, 6] == 4
-    check_scoring(w, out, np.arange(R, dtype=np.int32))
+    check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
 
 
 @pytest.mark.parametrize("mode", [1, 2])
@@ -452,11 +506,12 @@ def test_prefix_closed_search(name):
     see test_inputs_cpu.py) gives the oracle's overlaps and decisions."""
     w = workload(name)
     note(f"prefix-closed search {name}")
-    out = GpuRun(w, prefix_closed=True).score()
+    run = GpuRun(w, prefix_closed=True)
+    out = run.score()
     sel = sampled(w)
     want = oracle.overlap(w.req_off, w.req_hashes, w.inst_off, w.inst_hashes, sel=sel)
     np.testing.assert_array_equal(out["overlap"][sel], want)
-    check_scoring(w, out, sel)
+    check_scoring(w, out, sel, run=run)
 
 
 def test_ties_go_to_lowest_instance():
@@ -472,10 +527,11 @@ def test_ties_go_to_lowest_instance():
         feat[i] = feat[i & ~1]
     inst_off = np.zeros(N + 1, np.int64); inst_off[1:] = np.cumsum([len(x) for x in lists])
     w = synth.dataclasses.replace(base, inst_off=inst_off, inst_hashes=np.concatenate(lists), inst_feat=feat)
-    out = GpuRun(w).score()
+    run = GpuRun(w)
+    out = run.score()
     assert np.all(out["chosen"] % 2 == 0)
     np.testing.assert_array_equal(out["scores"][:, 0::2], out["scores"][:, 1::2])
-    check_scoring(w, out, np.arange(cfg.R, dtype=np.int32))
+    check_scoring(w, out, np.arange(cfg.R, dtype=np.int32), run=run)
 
 
 @pytest.mark.parametrize("R,N", [(1, 1), (37, 13), (5, 300), (130, 65)])
@@ -487,7 +543,7 @@ def test_ragged_shapes(R, N):
     got = GpuRun(w).update(w.upd_feats[:77], w.upd_ttft[:77])
     ref = oracle.update("fp32", w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.upd_feats[:77],
                         w.upd_ttft[:77], w.lr)
-    ok, worst = rel_ok(got["grad"], ref["grad"], 1e-4)
+    ok, worst, _ = grad_ok(got["grad"], ref["grad"])
     assert ok, worst
 
 
@@ -508,6 +564,33 @@ def test_deterministic_and_reload():
     # a model read back and installed elsewhere scores identically
     c = GpuRun(w, params=ua["params"])
     assert np.array_equal(c.score()["scores"].view(np.uint32), a.score()["scores"].view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["homogeneous", "large_batch"])
+def test_results_independent_of_launch_geometry(name):
+    """The same batch and update with the launches sized for the whole GPU, for
+    37 compute units and for 8 (ls_set_cu_limit): persistent kernels then walk
+    many more units per workgroup, grid-stride loops many more items per thread.
+    Every output is bitwise the same."""
+    w = workload(name)
+    results = []
+    for cus in (0, 37, 8):
+        note(f"launch geometry {name}: {cus or 'all'} compute units")
+        run = GpuRun(w)
+        run.ctx.ls_set_cu_limit(cus)
+        res = {"canon": run.score()}
+        if uses_fast_path(w.cfg.d, w.cfg.hidden, w.cfg.dtype):
+            res["fast"] = run.score(with_scores=False)
+            res["bounds"] = run.fast_scores()
+        res["update"] = run.update()
+        run.ctx.close()
+        results.append(res)
+    flat = lambda r: [(f"{k}.{j}", np.ascontiguousarray(v).view(np.uint8)) for k, d in r.items() for j, v in d.items()
+                      if isinstance(v, np.ndarray)]
+    base = flat(results[0])
+    for other in results[1:]:
+        for (ka, a), (kb, b) in zip(base, flat(other)):
+            assert ka == kb and np.array_equal(a, b), ka
 
 
 def test_abi_errors_on_device():

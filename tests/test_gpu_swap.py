@@ -25,14 +25,29 @@ def workload(dtype):
 
 
 def score_on(run, stream):
-    """Enqueue one scoring call on `stream`; returns the device outputs."""
+    """Enqueue two scoring calls on `stream`: one that asks for the score matrix
+    (canonical scores of every pair) and one that does not (on a bf16 context,
+    the matrix-core path with canonical rescoring of the band).  Returns the
+    first call's decisions and scores, and the second's decisions and minima."""
     import torch
     R, N = run.w.cfg.R, run.w.cfg.N
     chosen = torch.full((R,), -7, dtype=torch.int32, device="cuda")
     scores = torch.zeros(R * N, dtype=torch.float32, device="cuda")
     run.ctx.ls_score_batch(run.req_off, run.req_hashes, run.prompt_len, run.inst_feat, chosen, scores=scores,
                            stream=stream)
-    return chosen, scores
+    chosen_f = torch.full((R,), -7, dtype=torch.int32, device="cuda")
+    min_f = torch.zeros(R, dtype=torch.float32, device="cuda")
+    run.ctx.ls_score_batch(run.req_off, run.req_hashes, run.prompt_len, run.inst_feat, chosen_f, min_ttft=min_f,
+                           stream=stream)
+    return chosen, scores, chosen_f, min_f
+
+
+def check_fast_call(out, N):
+    """The call without the score matrix decides exactly as the canonical one."""
+    chosen, scores, chosen_f, min_f = (host(t) for t in out)
+    np.testing.assert_array_equal(chosen_f, chosen)
+    best = scores.reshape(-1, N)[np.arange(chosen.size), chosen]
+    np.testing.assert_array_equal(min_f.view(np.uint32), best.view(np.uint32))
 
 
 def host(t):
@@ -58,8 +73,10 @@ def test_shadow_training_and_swap(dtype):
     ctx = run.ctx
     serve = torch.cuda.current_stream()
     train = torch.cuda.Stream()
-    c0, s0 = score_on(run, serve)
+    out0 = score_on(run, serve)
+    c0, s0 = out0[:2]
     before = (host(c0), host(s0))
+    check_fast_call(out0, cfg.N)
     xa, ya = w.upd_feats[:160], w.upd_ttft[:160]
     xb, yb = w.upd_feats[160:260], w.upd_ttft[160:260]
     dev = [to_dev(np.asarray(a, np.float32)) for a in (xa, ya, xb, yb)]
@@ -75,8 +92,10 @@ def test_shadow_training_and_swap(dtype):
     n = int(ob.fifo_count[0]) + int(ob.rep_count[0])
     perm1 = np.concatenate([np.random.default_rng(e).permutation(n) for e in range(2)]).astype(np.int32)
     ctx.ls_train_round(2, 16, w.lr, perm1, loss, stream=train)
-    c1, s1 = score_on(run, serve)                 # may overlap the training
+    out1 = score_on(run, serve)                   # may overlap the training
+    c1, s1 = out1[:2]
     torch.cuda.synchronize()
+    check_fast_call(out1, cfg.N)
     np.testing.assert_array_equal(host(c1), before[0])
     np.testing.assert_array_equal(host(s1).view(np.uint32), before[1].view(np.uint32))
     np.testing.assert_array_equal(ctx.ls_get_model()[0], w.params.astype(np.float32))
@@ -84,8 +103,10 @@ def test_shadow_training_and_swap(dtype):
     note(f"swap {dtype}: push on the shadow, swap without a host wait")
     ctx.ls_buffer_push(dev[2], dev[3], stream=train)
     ctx.ls_swap_model(serve_stream=serve, train_stream=train)
-    c2, s2 = score_on(run, serve)
+    out2 = score_on(run, serve)
+    c2, s2 = out2[:2]
     torch.cuda.synchronize()
+    check_fast_call(out2, cfg.N)
     p1 = ctx.ls_get_model()[0]
     want1, _ = oracle.train_round(mode, cfg.hidden, w.params, w.mu, w.inv_sigma, ob, 2, 16, w.lr, perm1)
     assert_close_to(p1, want1, w.params, cfg.d, cfg.hidden, 1e-4, "first round")
