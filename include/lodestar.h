@@ -201,6 +201,28 @@ int ls_score_batch(ls_ctx* ctx, int32_t R, int32_t N,
                    void* stream);
 
 /*
+ * ls_score_batch for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, hosts that forbid allocation during
+ * serving.  Same arguments, results and errors as ls_score_batch, but the call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine): its
+ * scratch is one array of LS_NOALLOC_SCRATCH_BYTES per GPU, reserved while the
+ * library is loaded and shared by every context on that GPU.  A batch whose
+ * scratch would exceed it (about 29 bytes per pair plus 33 MiB at most;
+ * passing `overlap` and `scores` saves 8 bytes per pair) gets LS_ERR_INVALID
+ * before anything is enqueued.  Each call clears what it needs, but the array
+ * keeps the last call's contents: calls that overlap on one GPU (different
+ * streams, contexts or host threads) race on it, so the caller serialises them.
+ * The context's cache state, model and caller buffers must already exist.
+ * Per-kernel profiling records are not taken by this call.
+ */
+#define LS_NOALLOC_SCRATCH_BYTES (96u << 20)
+int ls_score_batch_noalloc(ls_ctx* ctx, int32_t R, int32_t N,
+                           const int64_t* req_off, const uint64_t* req_hashes, const int32_t* prompt_len,
+                           const float* inst_feat,
+                           int32_t* chosen, float* min_ttft, float* scores, int32_t* overlap, float* feat_out,
+                           void* stream);
+
+/*
  * Scoring precision of an LS_BF16 context.  By default a call that does not ask
  * for the score matrix runs the bf16 model on the matrix cores; every candidate
  * whose fast score lies within the error band of its request's best (see

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -100,7 +101,38 @@ struct ls_ctx {
     std::vector<hipEvent_t> spare;
 };
 
+// Scratch of the allocation-free scoring entry point: one array per GPU,
+// reserved while the library is loaded.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in for the symbol); it uses
+// the device address that hipGetSymbolAddress returns for the current device.
+constexpr size_t kNoAllocScratchBytes = LS_NOALLOC_SCRATCH_BYTES;
+static_assert(kNoAllocScratchBytes % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+hipError_t g_scratch_err[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on `device`, looked up once per device with that
+// device current (the caller's DeviceScope); nullptr if the lookup failed.
+void* scratch_on(int device) {
+    if (device < 0 || device >= kMaxScratchDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device] && g_scratch_err[device] == hipSuccess) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            g_scratch_err[device] = e != hipSuccess ? e : hipErrorInvalidSymbol;
+            (void)hipGetLastError();
+        } else {
+            g_scratch_ptr[device] = ptr;
+        }
+    }
+    return g_scratch_ptr[device];
+}
 
 int fail(ls_ctx* c, int code, const char* fmt, ...) {
     if (c) {
@@ -393,6 +425,9 @@ int ls_create(const ls_model_config* cfg, int device, ls_ctx** out) {
     ok = ok && hipEventCreateWithFlags(&c->stage_done, hipEventDisableTiming) == hipSuccess;
     ok = ok && hipDeviceGetAttribute(&c->n_cu_dev, hipDeviceAttributeMultiprocessorCount, device) == hipSuccess;
     c->n_cu = c->n_cu_dev;
+    // set-up of the allocation-free entry point: this device's address of its
+    // scratch array (a failed lookup only disables that entry point)
+    if (ok) (void)scratch_on(device);
     if (ok && ls::mfma_supported(c->dims)) {
         const ls::MfmaLayout L = ls::make_mfma_layout(c->dims);
         ok = hipMalloc((void**)&c->frag16, sizeof(uint16_t) * L.n16) == hipSuccess &&
@@ -802,6 +837,41 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
              ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov, inst_feat, chosen, min_ttft,
                                feat_out, s));
     return LS_OK;
+}
+
+int ls_score_batch_noalloc(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,
+                           const int32_t* prompt_len, const float* inst_feat, int32_t* chosen, float* min_ttft,
+                           float* scores, int32_t* overlap, float* feat_out, void* stream) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    int rc;
+    if (check_batch(c, R, N, req_off, req_hashes, prompt_len, inst_feat, chosen, &rc)) return rc;
+    const bool fast = fast_path(c, scores);
+    const size_t need = pipeline_bytes(c, R, N, overlap != nullptr, scores != nullptr, fast);
+    if (need > kNoAllocScratchBytes)
+        return fail(c, LS_ERR_INVALID,
+                    "this batch needs %zu bytes of scratch; the allocation-free entry point has %zu (fewer pairs, "
+                    "or pass overlap and scores buffers, or use ls_score_batch)",
+                    need, kNoAllocScratchBytes);
+    DeviceScope dev(c->device);
+    if (!dev.ok) return fail(c, LS_ERR_DEVICE, "cannot select device %d", c->device);
+    void* base = scratch_on(c->device);
+    if (!base) return fail(c, LS_ERR_DEVICE, "the scratch array of device %d has no device address", c->device);
+    hipStream_t s = (hipStream_t)stream;
+    // no profiling events here: creating one may allocate
+    const bool prof = c->profiling;
+    c->profiling = false;
+    WsCarve w{(char*)base};
+    Scored out;
+    rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, fast, -1.0, 0, nullptr,
+                      s, &out);
+    if (rc == LS_OK) {
+        const hipError_t e = ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov,
+                                               inst_feat, chosen, min_ttft, feat_out, s);
+        if (e != hipSuccess) rc = fail(c, LS_ERR_DEVICE, "%s", hipGetErrorString(e));
+    }
+    c->profiling = prof;
+    return rc;
 }
 
 int ls_fast_scores(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const uint64_t* req_hashes,

@@ -102,13 +102,15 @@ def library():
         lib.ls_set_shadow_training.argtypes = [P, ctypes.c_int, P]
         lib.ls_swap_model.argtypes = [P, P, P]
         lib.ls_fast_scores.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P]
+        lib.ls_score_batch_noalloc.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_set_cu_limit.argtypes = [P, ctypes.c_int]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
                   lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
                   lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round,
                   lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state, lib.ls_set_dropout,
-                  lib.ls_set_shadow_training, lib.ls_swap_model, lib.ls_fast_scores, lib.ls_set_cu_limit):
+                  lib.ls_set_shadow_training, lib.ls_swap_model, lib.ls_fast_scores, lib.ls_set_cu_limit,
+                  lib.ls_score_batch_noalloc):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -305,6 +307,26 @@ class Context:
             _dev(feat_out, "feat_out", (torch.float32,), R * self.d, allow_none=True),
         ]
         return self._check("ls_score_batch", self.lib.ls_score_batch(self.h, R, N, *args, _stream(stream)))
+
+    def ls_score_batch_noalloc(self, req_off, req_hashes, prompt_len, inst_feat, chosen, min_ttft=None, scores=None,
+                               overlap=None, feat_out=None, stream=None):
+        import torch
+        R = req_off.numel() - 1
+        N = inst_feat.shape[0] if inst_feat.dim() == 2 else (self.n_instances or 0)
+        d_inst = self.d - DERIVED_COLS
+        args = [
+            _dev(req_off, "req_off", (torch.int64,), R + 1),
+            _dev(req_hashes, "req_hashes", (torch.int64, torch.uint64)),
+            _dev(prompt_len, "prompt_len", (torch.int32,), R),
+            _dev(inst_feat, "inst_feat", (torch.float32,), N * d_inst),
+            _dev(chosen, "chosen", (torch.int32,), R),
+            _dev(min_ttft, "min_ttft", (torch.float32,), R, allow_none=True),
+            _dev(scores, "scores", (torch.float32,), R * N, allow_none=True),
+            _dev(overlap, "overlap", (torch.int32,), R * N, allow_none=True),
+            _dev(feat_out, "feat_out", (torch.float32,), R * self.d, allow_none=True),
+        ]
+        return self._check("ls_score_batch_noalloc",
+                           self.lib.ls_score_batch_noalloc(self.h, R, N, *args, _stream(stream)))
 
     def ls_route_batch(self, policy, req_off, req_hashes, prompt_len, inst_feat, rnd, chosen, status=None, heur=None,
                        feat_out=None, stream=None):
