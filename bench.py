@@ -6,17 +6,20 @@ every input already resident in HBM:
   1. ls_load_cache_state  -- rebuild every instance's prefix-cache hash table
   2. ls_score_batch       -- prefix overlap, features, reward model, argmin
   3. ls_update            -- one online SGD step of the reward model
-The printed value is (request, instance) pairs scored per second of step time;
-updates per second and per-kernel timings ride along.  Per-kernel durations
+The printed value is (request, instance) pairs scored per second of step time.
+Beside it: pairs per second of the scoring call alone (R N / t_score), the
+update's own steps and samples per second, per-kernel timings and rooflines, and
+one entry per other workload (scoring and update only, as the cache state of a
+serving router changes far less often than its batches).  Per-kernel durations
 come from HIP events recorded by the library on the stream of each call.
 
     python bench.py [--steps K] [--warmup W] [--config large_batch] [--no-cpu-baseline]
-                    [--copy-probe-mib M]
+                    [--no-other-configs] [--copy-probe-mib M]
 
 --copy-probe-mib runs M MiB device-to-device copies after the timed region; a
 hardware-counter pass over the same command reads FETCH_SIZE / WRITE_SIZE of
-that plain copy beside the scorer's kernels, which calibrates the counters.
-"roofline.traffic" is filled from a committed counter record
+that plain copy beside the kernels, which calibrates the counters.
+"traffic" is filled from a committed counter record
 (profiles/traffic_<kind>_<workload>.md) only while the sources of that kernel
 still hash to the digest the record was taken at; otherwise it is null.
 """
@@ -117,32 +120,39 @@ def update_flops(cfg, B):
     return B * (fwd + wgrad + igrad)
 
 
-def cpu_baseline(w, target_s=12.0):
-    """The oracle, untuned, on a bounded sample of requests (all instances each)."""
+def cpu_baseline(w, target_s=12.0, single_requests=256):
+    """The oracle, untuned, on a bounded sample of requests (all instances each):
+    on every host core, then on one thread over the first `single_requests`
+    requests."""
     import oracle
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
     cfg = w.cfg
     mode = "bf16" if cfg.dtype == "bf16" else "fp32"
     rng = np.random.default_rng(7)
 
-    def run(S):
-        sel = np.sort(rng.choice(cfg.R, min(S, cfg.R), replace=False)).astype(np.int32)
+    def run(sel, nthreads):
         t = time.perf_counter()
         oracle.score(mode, cfg.d, cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes, w.prompt_len,
-                     w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=threads)
+                     w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=nthreads)
         return len(sel), time.perf_counter() - t
 
+    pick = lambda S: np.sort(rng.choice(cfg.R, min(S, cfg.R), replace=False)).astype(np.int32)
     # two points separate the per-call cost (building the instance sets) from the per-request cost
-    s0, t0 = run(16)
-    s1, t1 = run(64)
+    s0, t0 = run(pick(16), threads)
+    s1, t1 = run(pick(64), threads)
     per_req = max((t1 - t0) / max(s1 - s0, 1), 1e-6)
     fixed = max(t0 - s0 * per_req, 0.0)
     S = int(min(cfg.R, max(64, (target_s - fixed) / per_req)))
-    s1, t1 = run(S)
+    s1, t1 = run(pick(S), threads)
+    sg = min(single_requests, cfg.R)
+    s2, t2 = run(np.arange(sg, dtype=np.int32), 1)
     return {
         "value": s1 * cfg.N / t1, "unit": "pairs/s", "cores": threads, "kind": "oracle",
         "sample": (f"{s1} of {cfg.R} requests x all {cfg.N} instances, {mode} oracle "
                    f"(set build + overlap + features + MLP + argmin), {t1:.1f} s wall"),
+        "single_thread": {"value": s2 * cfg.N / t2, "unit": "pairs/s", "cores": 1,
+                          "sample": f"first {s2} requests x all {cfg.N} instances, {mode} oracle, {t2:.1f} s wall "
+                                    "(per-call set build included)"},
     }
 
 
@@ -236,6 +246,142 @@ def time_maintenance(w, inst_h, req_off, req_h, chosen, reps):
             "requests_per_s": round(w.cfg.R / (ms / 1e3), 1)}
 
 
+def k1_algorithmic_bytes(w, ov):
+    """Bytes the prefix-overlap step must move for this batch with shared
+    prefixes answered once (Section 2: reuse is strictly sequential, so a request
+    that shares its first c blocks with a longer request of the batch has that
+    request's overlap wherever it is below c):
+      every request hash read once (8 B), the overlap matrix written once (4 B
+      per pair), and one 64-B bucket per useful probe -- for each group of
+      requests with the same first block, the longest one (lowest id on ties)
+      probes min(l + 1, n) blocks per instance; every other request, with
+      common prefix c with it, probes min(l - c + 1, n - c) blocks on the
+      instances where the longer one's run reaches c, none elsewhere.
+    Speculative probes past a miss and table lines read twice are overhead."""
+    req_off, h = w.req_off, w.req_hashes
+    R, N = ov.shape
+    n = np.diff(req_off)
+    has = n > 0
+    first = np.where(has, h[np.minimum(req_off[:-1], max(h.size - 1, 0))], 0)
+    order = np.lexsort((np.arange(R), -n, first))            # by first hash, longest first, lowest id
+    probes = 0
+    i = 0
+    while i < R:
+        j = i
+        r0 = order[i]
+        while j < R and first[order[j]] == first[r0] and has[order[j]] == has[r0]:
+            j += 1
+        if has[r0]:
+            lead = r0
+            hl = h[req_off[lead]:req_off[lead + 1]]
+            ll = ov[lead]
+            probes += int(np.minimum(ll + 1, n[lead]).sum())
+            for k in range(i + 1, j):
+                f = order[k]
+                hf = h[req_off[f]:req_off[f + 1]]
+                m = min(hf.size, hl.size)
+                diff = np.flatnonzero(hf[:m] != hl[:m])
+                c = int(diff[0]) if diff.size else m
+                if c >= n[f]:
+                    continue
+                reach = ll >= c
+                probes += int(np.minimum(ov[f][reach] - c + 1, n[f] - c).sum())
+        i = j
+    return 64 * probes + 8 * int(n.sum()) + 4 * R * N, probes
+
+
+def roofline_entry(kind, bound, work, peak, unit, calls, total_ms, cfg_name, extra=None):
+    """achieved = algorithmic work per call / the kind's average device time per
+    call (all of its launch groups within one call of the entry point)."""
+    avg_s = total_ms / max(calls, 1) / 1e3
+    achieved = work / avg_s if avg_s > 0 else 0.0
+    rec = traffic_record(kind, cfg_name)
+    out = {"bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1), "unit": unit,
+           "frac": round(achieved / peak, 4), "avg_ms": round(avg_s * 1e3, 4),
+           "traffic": None if rec is None else round(rec["bytes_per_launch"] / 1e9, 4),
+           "traffic_unit": "GB per launch",
+           "digest": sources_digest(kind) if kind in KIND_KERNELS else None}
+    if extra:
+        out.update(extra)
+    return out
+
+
+def scoring_rooflines(cfg, prof, steps, exec_tflop, model_tflop, k1_gb):
+    """Rooflines of the scoring kernels from one profile of `steps` scoring calls:
+    K1 on HBM, the scorer on the matrix cores (bf16) or the vector ALUs (fp32
+    canonical chains)."""
+    out = {}
+    if "prefix_match" in prof:
+        out["prefix_match"] = roofline_entry("prefix_match", "hbm", k1_gb, PEAK_HBM_GBS, "GB/s", steps,
+                                             prof["prefix_match"][1], cfg.name)
+    for kind, bound, peak in (("score_pairs_mfma", "mfma", PEAK_BF16_TFLOPS),
+                              ("score_pairs", "alu", PEAK_VALU_FP32_TFLOPS)):
+        if kind in prof:
+            ms = prof[kind][1]
+            out[kind] = roofline_entry(kind, bound, exec_tflop, peak, "TFLOP/s", steps, ms, cfg.name,
+                                       {"model_flop_rate": round(model_tflop / (ms / steps / 1e3), 3)})
+    return out
+
+
+SCORE_KINDS = ("prefix_match", "instance_partial", "score_pairs", "score_pairs_mfma", "band_select", "rescore",
+               "argmin")
+
+
+def run_other_config(name, steps, warmup):
+    """Scoring and update of another workload: pairs/s of the scoring call, the
+    update's steps/s, per-kernel times and the rooflines of K1 and the scorer."""
+    import torch
+
+    from paper_2606_00946_amd import lodestar, synth
+    w = synth.generate(name)
+    cfg = w.cfg
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a.view(np.int64) if a.dtype == np.uint64 else a)).cuda()
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype, device=0)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    inst_h = dev(w.inst_hashes)
+    ctx.ls_load_cache_state(w.inst_off, inst_h)
+    ins = (dev(w.req_off), dev(w.req_hashes), dev(w.prompt_len), dev(w.inst_feat))
+    x, y = dev(w.upd_feats), dev(w.upd_ttft)
+    R, N, B = cfg.R, cfg.N, cfg.update_batch
+    chosen = torch.empty(R, dtype=torch.int32, device="cuda")
+    min_ttft = torch.empty(R, dtype=torch.float32, device="cuda")
+    overlap = torch.empty(R * N, dtype=torch.int32, device="cuda")
+
+    def step():
+        ctx.ls_score_batch(*ins, chosen, min_ttft, None, overlap, None)
+        ctx.ls_update(x, y, w.lr)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.ls_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    prof = ctx.ls_profile_read()
+    ctx.ls_profile_enable(False)
+    ctx.close()
+    ms = {k: v[1] / steps for k, v in prof.items()}
+    t_score = sum(ms.get(k, 0.0) for k in SCORE_KINDS)
+    t_upd = ms.get("update", 0.0)
+    ov = overlap.cpu().numpy().reshape(R, N).astype(np.int64)
+    k1_bytes, probes = k1_algorithmic_bytes(w, ov)
+    rl = scoring_rooflines(cfg, prof, steps, executed_flops_per_pair(cfg) * R * N / 1e12,
+                           model_flops_per_pair(cfg) * R * N / 1e12, k1_bytes / 1e9)
+    if "update" in prof:
+        rl["update"] = roofline_entry("update", "mfma" if cfg.dtype == "bf16" else "alu", update_flops(cfg, B) / 1e12,
+                                      PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_VALU_FP32_TFLOPS,
+                                      "TFLOP/s", steps, prof["update"][1], cfg.name)
+    return {"requests": R, "instances": N, "predictor": f"{cfg.d}-" + "-".join(map(str, cfg.hidden)) + f"-1 {cfg.dtype}",
+            "update_batch": B, "score_pairs_per_s": round(R * N / (t_score / 1e3), 1),
+            "score_ms": round(t_score, 4), "updates_per_s": round(1e3 / t_upd, 2) if t_upd else None,
+            "update_samples_per_s": round(B * 1e3 / t_upd, 1) if t_upd else None,
+            "wall_ms_per_step": round(wall_ms, 4), "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
+            "useful_probes": probes, "rooflines": rl}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -243,6 +389,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="large_batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -299,29 +446,43 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     pairs_per_s = R * N / (ms_step / 1e3)
     phases = {k: round(v[1] / args.steps, 4) for k, v in prof.items()}
+    t_score = sum(v[1] for k, v in prof.items() if k in SCORE_KINDS) / args.steps
+    t_upd = prof["update"][1] / args.steps if "update" in prof else None
 
     # algorithmic work of each kernel kind per launch
     n = np.diff(w.req_off)
     ov = overlap.cpu().numpy().reshape(R, N).astype(np.int64)
-    probes = int(np.minimum(ov + 1, n[:, None]).sum())
-    k1_bytes = 64 * probes + 8 * int(n.sum()) + 4 * R * N
-    model_tflop = model_flops_per_pair(cfg) * R * N / 1e12
+    k1_bytes, probes = k1_algorithmic_bytes(w, ov)
     exec_tflop = executed_flops_per_pair(cfg) * R * N / 1e12
-    roof = {
-        "prefix_match": ("hbm", k1_bytes / 1e9, PEAK_HBM_GBS, "GB/s"),
-        "score_pairs": ("alu", exec_tflop, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
-        "score_pairs_mfma": ("mfma", exec_tflop, PEAK_BF16_TFLOPS, "TFLOP/s"),
-        "update": ("alu", update_flops(cfg, B) / 1e12, PEAK_VALU_FP32_TFLOPS, "TFLOP/s"),
-        "table_build": ("hbm", (8 + 64) * int(w.inst_hashes.size) / 1e9, PEAK_HBM_GBS, "GB/s"),
-    }
-    dom = max((k for k in prof if k in roof), key=lambda k: prof[k][1])
-    bound, work, peak, unit = roof[dom]
-    avg_s = prof[dom][1] / prof[dom][0] / 1e3
-    achieved = work / avg_s
-    # the unfactorised model's flops over the same time, for comparison
-    model_rate = round(model_tflop / avg_s, 3) if dom in ("score_pairs", "score_pairs_mfma") else None
-    rec = traffic_record(dom, cfg.name)
-    traffic = None if rec is None else round(rec["bytes_per_launch"] / 1e9, 4)
+    model_tflop = model_flops_per_pair(cfg) * R * N / 1e12
+    steps = args.steps
+    rooflines = scoring_rooflines(cfg, prof, steps, exec_tflop, model_tflop, k1_bytes / 1e9)
+    if "update" in prof:
+        rooflines["update"] = roofline_entry("update", "mfma" if cfg.dtype == "bf16" else "alu",
+                                             update_flops(cfg, B) / 1e12,
+                                             PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_VALU_FP32_TFLOPS,
+                                             "TFLOP/s", steps, prof["update"][1], cfg.name)
+    if "table_build" in prof:
+        # each cached key read once (8 B) and its table written once (two 8-byte slots per key at half load)
+        rooflines["table_build"] = roofline_entry("table_build", "hbm", (8 + 16) * int(w.inst_hashes.size) / 1e9,
+                                                  PEAK_HBM_GBS, "GB/s", steps, prof["table_build"][1], cfg.name)
+    dom = max((k for k in rooflines), key=lambda k: prof[k][1])
+    roof = dict(rooflines[dom])
+    roof = {"kernel": dom, **roof}
+
+    # candidates the band sends to canonical rescoring, per request (after the timed region)
+    band = None
+    tt = torch.empty(R * N, dtype=torch.float32, device="cuda")
+    ee = torch.empty(R * N, dtype=torch.float32, device="cuda")
+    bb = torch.empty(R * N, dtype=torch.uint8, device="cuda")
+    try:
+        ctx.ls_fast_scores(req_off, req_h, plen, feat, tt, ee, bb)
+        torch.cuda.synchronize()
+        band = round(float(bb.sum(dtype=torch.int64).item()) / R, 4)
+    except lodestar.LodestarError:
+        pass                                      # no matrix-core path for this model
+    del tt, ee, bb
+
     result = {
         "metric": METRIC,
         "value": round(pairs_per_s, 1),
@@ -338,19 +499,31 @@ def main():
         "config": {"workload": cfg.name, "requests": R, "instances": N, "update_batch": B,
                    "cached_blocks": int(w.inst_hashes.size), "prompt_blocks": int(n.sum()),
                    "predictor": f"{cfg.d}-{cfg.hidden[0]}-{cfg.hidden[1]}-1 {cfg.dtype}"},
-        "updates_per_s": round(1e3 / ms_step, 3),
-        "update_samples_per_s": round(B * 1e3 / ms_step, 1),
+        "score_pairs_per_s": round(R * N / (t_score / 1e3), 1),
+        "score_ms": round(t_score, 4),
+        "updates_per_s": round(1e3 / t_upd, 3) if t_upd else None,
+        "update_samples_per_s": round(B * 1e3 / t_upd, 1) if t_upd else None,
         "kernel_ms_per_step": phases,
-        "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1),
-                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
-                     "traffic_unit": "GB per launch", "digest": sources_digest(dom) if dom in KIND_KERNELS else None,
-                     "model_flop_rate": model_rate},
+        "roofline": roof,
+        "rooflines": rooflines,
         "useful_probes": probes,
+        "band_candidates_per_request": band,
     }
     result["route"] = time_route(ctx, w, (req_off, req_h, plen, feat), args.steps)
     result["online_learning"] = time_online_learning(ctx, w)
     result["maintenance"] = time_maintenance(w, inst_h, req_off, req_h, chosen, max(1, min(args.steps, 5)))
     ctx.close()
+    del inst_h, req_off, req_h, plen, feat, upd_x, upd_y, overlap
+    torch.cuda.empty_cache()
+    if not args.no_other_configs:
+        others = {}
+        for name in ("tiny", "homogeneous", "heterogeneous", "long_context"):
+            if name == cfg.name:
+                continue
+            others[name] = run_other_config(name, args.steps, max(1, args.warmup))
+            log(f"{name}: {others[name]['score_pairs_per_s']:.4g} pairs/s, {others[name]['score_ms']} ms scoring")
+            torch.cuda.empty_cache()
+        result["other_configs"] = others
     if args.copy_probe_mib > 0:
         copy_probe(args.copy_probe_mib)
     if not args.no_cpu_baseline:
