@@ -171,6 +171,173 @@ hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const
     return hipGetLastError();
 }
 
+// Two-stage selection for scoring calls.  Stage 1 lists each request's fast
+// argmin (smallest finite t, lowest id on ties) for canonical rescoring; its
+// canonical score c1 is then an upper bound of the request's canonical minimum.
+// Stage 2 keeps every pair whose canonical score can still be <= c1 (or, with a
+// tie-break margin delta, within the near-best set's largest bound
+// c1 + delta |c1|): t - E <= that bound, a non-finite t or E, or one of the
+// K-filter's instances.  With |t - c| <= E for every pair this holds the
+// canonical argmin, every exact tie with it and every near-best member, and it
+// is about half as wide as the band around min (t + E), which has to allow for
+// the best pair's own error as well.
+__global__ __launch_bounds__(64 * kBandWaves) void band_lead_kernel(int32_t R, int32_t N, const float* __restrict__ t,
+                                                                    int64_t* __restrict__ lead) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * kBandWaves + (threadIdx.x >> 6);
+    if (r >= R) return;
+    const float* __restrict__ tr = t + r * N;
+    float best = INFINITY;
+    int bi = N;                                   // N: no finite score seen
+    for (int i = lane; i < N; i += 64) {
+        const float v = tr[i];
+        if (finite_f(v) && (v < best || (v == best && i < bi))) {
+            best = v;
+            bi = i;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const float ov = __shfl_xor(best, off);
+        const int oi = __shfl_xor(bi, off);
+        if (ov < best || (ov == best && oi < bi)) {
+            best = ov;
+            bi = oi;
+        }
+    }
+    if (lane == 0) lead[r] = r * N + (bi < N ? bi : 0);
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(1024) void band_rest_kernel(int32_t R, int32_t N, const float* __restrict__ t,
+                                                         const float* __restrict__ E, const float* __restrict__ canon,
+                                                         const int64_t* __restrict__ lead, BandPolicy BP,
+                                                         uint8_t* __restrict__ band, int64_t* __restrict__ list,
+                                                         uint32_t* __restrict__ count) {
+    constexpr int V = VEC ? 4 : 1;
+    constexpr int CH = 64 * V;
+    __shared__ uint32_t wcount[kBandWaves];
+    __shared__ uint32_t wbase[kBandWaves];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t r = (int64_t)blockIdx.x * kBandWaves + wv;
+    const bool live = r < R;
+    const float* __restrict__ tr = t + (live ? r : 0) * N;
+    const float* __restrict__ er = E + (live ? r : 0) * N;
+    auto load = [&](const float* __restrict__ row, int i, float (&v)[V]) {
+        if constexpr (VEC) {
+            const float4 q = *reinterpret_cast<const float4*>(row + i);
+            v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+        } else {
+            v[0] = row[i];
+        }
+    };
+    int i1 = -1;
+    bool all = false;
+    float thr = 0.0f;
+    int32_t C[LS_MAX_KFILTER];
+    int nc = 0;
+    uint32_t cnt = 0;
+    if (live) {
+        const int64_t l1 = lead[r];
+        i1 = (int)(l1 - r * N);
+        const float c1 = canon[l1];
+        if (!finite_f(c1)) {
+            // +inf or NaN: any finite canonical score beats it; -inf: only -inf ties
+            all = c1 != -INFINITY;
+            thr = c1;
+        } else if (BP.delta >= 0.0) {
+            // c + delta |c| grows with c, so the near-best bound of the true minimum is at most this
+            const double b = (double)c1 + BP.delta * fabs((double)c1);
+            float f = (float)b;
+            if ((double)f < b) f = nextafterf(f, INFINITY);
+            thr = f;
+        } else {
+            thr = c1;     // fl(t - E) <= c1 whenever t - E <= c1: rounding is monotone and c1 is a float
+        }
+        if (BP.k_filter > 0 && BP.stats->saturated && BP.req_off[r + 1] > BP.req_off[r])
+            nc = hrw_topk_wave(BP.req_hashes[BP.req_off[r]], N, BP.k_filter, C, lane);
+        for (int i0 = 0; i0 < N; i0 += CH) {
+            const int i = i0 + V * lane;
+            uint32_t bits = 0, listed = 0;
+            if (i < N) {
+                float tv[V], ev[V];
+                load(tr, i, tv);
+                load(er, i, ev);
+#pragma unroll
+                for (int j = 0; j < V; ++j) {
+                    bool in = all || !(finite_f(tv[j]) && finite_f(ev[j])) || (tv[j] - ev[j] <= thr);
+                    for (int q = 0; q < nc; ++q) in |= (C[q] == i + j);
+                    const bool lead_pair = i + j == i1;
+                    bits |= ((in || lead_pair) ? 1u : 0u) << (8 * j);
+                    listed |= ((in && !lead_pair) ? 1u : 0u) << (8 * j);
+                }
+                if constexpr (VEC) *reinterpret_cast<uint32_t*>(band + r * N + i) = bits;
+                else band[r * N + i] = (uint8_t)bits;
+            }
+            cnt += (uint32_t)__popc(listed);
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
+    }
+    if (lane == 0) wcount[wv] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t total = 0;
+        for (int k = 0; k < kBandWaves; ++k) total += wcount[k];
+        uint32_t base = total ? atomicAdd(count, total) : 0u;
+        for (int k = 0; k < kBandWaves; ++k) {
+            wbase[k] = base;
+            base += wcount[k];
+        }
+    }
+    __syncthreads();
+    if (!live) return;
+    uint32_t base = wbase[wv];
+    for (int i0 = 0; i0 < N; i0 += CH) {
+        const int i = i0 + V * lane;
+        uint32_t bits = 0;
+        if (i < N) {
+            if constexpr (VEC) bits = *reinterpret_cast<const uint32_t*>(band + r * N + i);
+            else bits = band[r * N + i];
+            if (i1 >= i && i1 < i + V) bits &= ~(1u << (8 * (i1 - i)));     // the lead pair is rescored already
+        }
+        const uint32_t mine = (uint32_t)__popc(bits);
+        uint32_t incl = mine;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t up = __shfl_up(incl, d);
+            if (lane >= d) incl += up;
+        }
+        uint32_t pos = base + incl - mine;
+#pragma unroll
+        for (int j = 0; j < V; ++j)
+            if ((bits >> (8 * j)) & 1u) list[pos++] = r * N + i + j;
+        base += __shfl(incl, 63);
+    }
+}
+
+hipError_t launch_band_lead(int32_t R, int32_t N, const float* t, int64_t* lead, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    const dim3 grid((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)), block(64 * kBandWaves);
+    hipLaunchKernelGGL(band_lead_kernel, grid, block, 0, s, R, N, t, lead);
+    return hipGetLastError();
+}
+
+hipError_t launch_band_rest(int32_t R, int32_t N, const float* t, const float* E, const float* canon,
+                            const int64_t* lead, double delta, int32_t k_filter, const PolicyStats* stats,
+                            const int64_t* req_off, const uint64_t* req_hashes, uint8_t* band, int64_t* list,
+                            uint32_t* count, hipStream_t s) {
+    if (R <= 0) return hipSuccess;
+    BandPolicy BP{delta, k_filter, stats, req_off, req_hashes};
+    const dim3 grid((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)), block(64 * kBandWaves);
+    const bool vec = N % 4 == 0 && ((uintptr_t)t | (uintptr_t)E) % 16 == 0 && (uintptr_t)band % 4 == 0;
+    if (vec)
+        hipLaunchKernelGGL(band_rest_kernel<true>, grid, block, 0, s, R, N, t, E, canon, lead, BP, band, list, count);
+    else
+        hipLaunchKernelGGL(band_rest_kernel<false>, grid, block, 0, s, R, N, t, E, canon, lead, BP, band, list, count);
+    return hipGetLastError();
+}
+
 // Canonical score of every listed pair, written over its fast score.
 template <bool BF>
 __global__ __launch_bounds__(256) void rescore_kernel(PairModel M, const float* __restrict__ mu,
@@ -223,9 +390,12 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // Each wave scores four pairs at once, so every weight it converts from bf16
-// serves four chains and the four head chains run side by side.  Eight waves
-// of four 1 KB rows and W2 fill the 160 KB of LDS exactly; w3 is read from
-// memory (cached) by the head chains.
+// feeds four chains and the four head chains run side by side.  W2 (as bf16
+// bits, 128 KB at H = 256) and eight waves' rows (four pairs x H fp32) fill the
+// 160 KB of LDS: two waves per SIMD, so that one wave's layer-1 loads and head
+// chains overlap the other's layer-2 FMAs; each block of four inputs' operands
+// is read one block ahead of its FMAs.  (Eight pairs per wave at one wave per
+// SIMD leaves those serial phases exposed and is slower.)
 constexpr int kRescoreWaves = 8;
 constexpr int kRescorePairs = 4;
 
@@ -233,9 +403,29 @@ template <int H>
 __global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(RescoreArgs A) {
     constexpr int U = H / 64;                  // units per lane
     constexpr int P = kRescorePairs;
-    __shared__ uint16_t lds_w2[H * H];
-    __shared__ __align__(16) float lds_row[kRescoreWaves][P][H];
-    for (int e = threadIdx.x; e < H * H; e += 64 * kRescoreWaves) lds_w2[e] = (uint16_t)(__float_as_uint(A.w2t[e]) >> 16);
+    constexpr int RS = H;
+    static_assert(U == 1 || U == 2 || U == 4, "H in {64, 128, 256}");
+    __shared__ __align__(16) uint16_t lds_w2[H * H];
+    __shared__ __align__(16) float lds_row[kRescoreWaves][P][RS];
+    {
+        // W2 into LDS as bf16 bits: 16-byte loads, eight in flight per thread
+        // before any is used (one memory round trip per eight, not per element)
+        constexpr int NV = H * H / 4, T = 64 * kRescoreWaves, B8 = 8;
+        const float4* __restrict__ src = reinterpret_cast<const float4*>(A.w2t);
+        uint2* dst = reinterpret_cast<uint2*>(lds_w2);
+        for (int base = threadIdx.x; base < NV; base += T * B8) {
+            float4 v[B8];
+#pragma unroll
+            for (int j = 0; j < B8; ++j)
+                if (base + j * T < NV) v[j] = src[base + j * T];
+#pragma unroll
+            for (int j = 0; j < B8; ++j)
+                if (base + j * T < NV)
+                    dst[base + j * T] =
+                        make_uint2((__float_as_uint(v[j].x) >> 16) | (__float_as_uint(v[j].y) & 0xffff0000u),
+                                   (__float_as_uint(v[j].z) >> 16) | (__float_as_uint(v[j].w) & 0xffff0000u));
+        }
+    }
     __syncthreads();
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     float w1c[U][5], b2v[U];
@@ -247,6 +437,7 @@ __global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(Res
     }
     const float b3 = A.b3[0];
     const int64_t cnt = *A.count;
+    float (*rows)[RS] = lds_row[wave];
     for (int64_t q = ((int64_t)blockIdx.x * kRescoreWaves + wave) * P; q < cnt;
          q += (int64_t)gridDim.x * kRescoreWaves * P) {
         int64_t pp[P];
@@ -265,42 +456,76 @@ __global__ __launch_bounds__(64 * kRescoreWaves, 1) void rescore_wave_kernel(Res
                 float z = A.part_t[(int64_t)k * A.N + i];
 #pragma unroll
                 for (int c = 0; c < 5; ++c) z = __builtin_fmaf(w1c[v][c], xt[c], z);
-                lds_row[wave][e][k] = bf16_rne_num(relu(z));
+                rows[e][k] = bf16_rne_num(relu(z));
             }
         }
         wave_sync();
-        // layer 2: units U lane .. U lane + U - 1
+        // layer 2: units U lane .. U lane + U - 1, inputs ascending
         float acc[P][U];
 #pragma unroll
         for (int e = 0; e < P; ++e)
 #pragma unroll
             for (int u = 0; u < U; ++u) acc[e][u] = b2v[u];
-        for (int k = 0; k < H; k += 4) {
-            float av[P][4];
+        auto load_block = [&](int k, float4 (&av)[P], uint32_t (&wb)[4][(U + 1) / 2]) {
 #pragma unroll
-            for (int e = 0; e < P; ++e) {
-                const float4 a4 = *reinterpret_cast<const float4*>(&lds_row[wave][e][k]);
-                av[e][0] = a4.x; av[e][1] = a4.y; av[e][2] = a4.z; av[e][3] = a4.w;
-            }
+            for (int e = 0; e < P; ++e) av[e] = *reinterpret_cast<const float4*>(&rows[e][k]);
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
                 const uint16_t* wr = lds_w2 + (k + kk) * H + U * lane;
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const float wv = __uint_as_float((uint32_t)wr[u] << 16);
-#pragma unroll
-                    for (int e = 0; e < P; ++e) acc[e][u] = __builtin_fmaf(wv, av[e][kk], acc[e][u]);
+                if constexpr (U == 4) {
+                    const uint2 w2 = *reinterpret_cast<const uint2*>(wr);
+                    wb[kk][0] = w2.x;
+                    wb[kk][1] = w2.y;
+                } else if constexpr (U == 2) {
+                    wb[kk][0] = *reinterpret_cast<const uint32_t*>(wr);
+                } else {
+                    wb[kk][0] = wr[0];
                 }
             }
+        };
+        auto fma_block = [&](const float4 (&a4)[P], const uint32_t (&wbk)[4][(U + 1) / 2]) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                float wv[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t bits = wbk[kk][u >> 1];
+                    wv[u] = __uint_as_float((u & 1) ? (bits & 0xffff0000u) : (bits << 16));
+                }
+#pragma unroll
+                for (int e = 0; e < P; ++e) {
+                    const float a = kk == 0 ? a4[e].x : kk == 1 ? a4[e].y : kk == 2 ? a4[e].z : a4[e].w;
+#pragma unroll
+                    for (int u = 0; u < U; ++u) acc[e][u] = __builtin_fmaf(wv[u], a, acc[e][u]);
+                }
+            }
+        };
+        // two operand buffers in turn: block k + 4's reads are issued before block k's FMAs
+        float4 av[P], an[P];
+        uint32_t wb[4][(U + 1) / 2], wn[4][(U + 1) / 2];
+        load_block(0, av, wb);
+        for (int k = 0; k < H; k += 8) {
+            load_block(k + 4, an, wn);
+            fma_block(av, wb);
+            if (k + 8 < H) load_block(k + 8, av, wb);
+            fma_block(an, wn);
         }
         wave_sync();
 #pragma unroll
-        for (int e = 0; e < P; ++e)
+        for (int e = 0; e < P; ++e) {
+            if constexpr (U == 4) {
+                *reinterpret_cast<float4*>(&rows[e][4 * lane]) =
+                    make_float4(bf16_rne_num(relu(acc[e][0])), bf16_rne_num(relu(acc[e][1])),
+                                bf16_rne_num(relu(acc[e][2])), bf16_rne_num(relu(acc[e][3])));
+            } else {
 #pragma unroll
-            for (int u = 0; u < U; ++u) lds_row[wave][e][U * lane + u] = bf16_rne_num(relu(acc[e][u]));
+                for (int u = 0; u < U; ++u) rows[e][U * lane + u] = bf16_rne_num(relu(acc[e][u]));
+            }
+        }
         wave_sync();
+        // head: lane e < P runs pair e's chain over the units in ascending order
         if (lane < P && q + lane < cnt) {
-            const float* hrow = lds_row[wave][lane];
+            const float* hrow = rows[lane];
             float t = b3;
             for (int j = 0; j < H; j += 4) {
                 const float4 h4 = *reinterpret_cast<const float4*>(hrow + j);

@@ -235,6 +235,14 @@ hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const
                                      int32_t k_filter, const PolicyStats* stats, const int64_t* req_off,
                                      const uint64_t* req_hashes, uint8_t* band, int64_t* list, uint32_t* count,
                                      hipStream_t s);
+// Two-stage candidate selection of a scoring call: the fast argmin of each
+// request first (lead[r], to be rescored), then, from its canonical score in
+// `canon`, every pair that can still be the canonical argmin or near-best.
+hipError_t launch_band_lead(int32_t R, int32_t N, const float* t, int64_t* lead, hipStream_t s);
+hipError_t launch_band_rest(int32_t R, int32_t N, const float* t, const float* E, const float* canon,
+                            const int64_t* lead, double delta, int32_t k_filter, const PolicyStats* stats,
+                            const int64_t* req_off, const uint64_t* req_hashes, uint8_t* band, int64_t* list,
+                            uint32_t* count, hipStream_t s);
 hipError_t launch_policy_stats(const PolicyArgs& P, const float* inst_feat, int32_t N, int d_inst, double* cnt,
                                PolicyStats* st, hipStream_t s);
 hipError_t launch_route(const PolicyArgs& P, const PolicyStats* st, const double* cnt, const ModelDims& m, int32_t R,

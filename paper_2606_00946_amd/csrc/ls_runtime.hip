@@ -743,8 +743,9 @@ size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool h
     if (fast) {
         need += (size_t)round_up(pairs * 4, 256);                // error scales
         need += (size_t)round_up(pairs, 256);                    // candidate flags
+        need += (size_t)round_up((int64_t)R * 8, 256);           // each request's fast argmin
         need += (size_t)round_up(pairs * 8, 256);                // candidate list
-        need += 256;                                             // candidate count
+        need += 256;                                             // candidate counts
     }
     return need;
 }
@@ -790,18 +791,25 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
     if (fast) {
         float* eb = w.take<float>(pairs);
         uint8_t* flags = w.take<uint8_t>(pairs);
+        int64_t* lead = w.take<int64_t>(R);
         int64_t* list = w.take<int64_t>(pairs);
-        uint32_t* count = w.take<uint32_t>(64);
+        uint32_t* count = w.take<uint32_t>(64);       // [0]: stage-1 candidates (R), [32]: stage 2
         LS_TIMED(c, K_SCORE_MFMA, s,
                  ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N, req_off,
                                              prompt_len, ov, sc, eb, c->n_cu, s));
-        LS_TIMED(c, K_BAND, s, ls::launch_fill_u32(count, 0u, 1, s));
-        LS_TIMED(c, K_BAND, s,
-                 ls::launch_band_select_policy(R, N, sc, eb, delta, k_filter, stats, req_off, req_hashes, flags, list,
-                                               count, s));
+        // stage 1: every request's fast argmin, rescored; stage 2: what can still beat it
+        const ls::FillOp fills[2] = {{count, (uint64_t)(uint32_t)R, 1, 4}, {count + 32, 0u, 1, 4}};
+        LS_TIMED(c, K_BAND, s, ls::launch_fill_multi(fills, 2, s));
+        LS_TIMED(c, K_BAND, s, ls::launch_band_lead(R, N, sc, lead, s));
         LS_TIMED(c, K_RESCORE, s,
-                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list, count,
+                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, lead, count,
                                     sc, c->n_cu, s));
+        LS_TIMED(c, K_BAND, s,
+                 ls::launch_band_rest(R, N, sc, eb, sc, lead, delta, k_filter, stats, req_off, req_hashes, flags, list,
+                                      count + 32, s));
+        LS_TIMED(c, K_RESCORE, s,
+                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list,
+                                    count + 32, sc, c->n_cu, s));
         band = flags;
     } else {
         LS_TIMED(c, K_SCORE, s,
