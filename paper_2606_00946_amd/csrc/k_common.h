@@ -27,6 +27,24 @@ __device__ __forceinline__ float bf16_rne_num(float x) {
 
 __device__ __forceinline__ float relu(float z) { return z > 0.0f ? z : 0.0f; }
 
+// Workgroup-cooperative fill of a shared-memory array: dst[e] = get(e) for e in
+// [0, n).  Each thread issues INFLIGHT loads before storing any of them, so the
+// fill costs one memory round trip per INFLIGHT elements per thread rather than
+// one per element (a plain strided loop waits for every load before its store).
+template <int INFLIGHT, class T, class Get>
+__device__ __forceinline__ void lds_fill(T* dst, int n, Get get) {
+    const int T_ = (int)blockDim.x;
+    for (int e0 = (int)threadIdx.x; e0 < n; e0 += T_ * INFLIGHT) {
+        T v[INFLIGHT];
+#pragma unroll
+        for (int j = 0; j < INFLIGHT; ++j)
+            if (e0 + j * T_ < n) v[j] = get(e0 + j * T_);
+#pragma unroll
+        for (int j = 0; j < INFLIGHT; ++j)
+            if (e0 + j * T_ < n) dst[e0 + j * T_] = v[j];
+    }
+}
+
 struct PairModel {
     const float* __restrict__ w1;    // [h1 x d]
     const float* __restrict__ w2t;   // [h1 x h2]

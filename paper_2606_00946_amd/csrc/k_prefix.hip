@@ -90,43 +90,47 @@ __device__ __forceinline__ int64_t extend_run(const uint64_t* __restrict__ table
 }
 
 // The same run with a whole wave on one pair: group g of four lanes probes
-// blocks l + g + 16 t (t < 4), so one round covers up to 64 positions.  The
-// window starts at 4 and doubles after every all-hit round (4, 8, ..., 64):
-// long runs advance 64 blocks per dependent round, short ones waste little.
+// blocks l + g + 16 t (t < TS), so one round covers up to 16 TS positions.  The
+// window starts at W and doubles after every all-hit round (..., 16 TS): long
+// runs advance 16 TS blocks per dependent round, short ones waste little.  (A
+// window of 256 positions, TS = 16, was slower on 5,000-block runs over
+// 400,000-key tables: the random bucket reads, not the rounds, bound it.)
+template <int TS = 4>
 __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
                                                    const uint64_t* __restrict__ h, int64_t n, int64_t l, int lane,
                                                    int W = 4) {
+    constexpr int WMAX = 16 * TS;
     const int g = lane >> 2, q = lane & 3, shift = g * 4;
     // the window's block hashes; the next window's are read while this one's
     // buckets are in flight (used only if every probe of this window hits)
-    uint64_t key[4];
-    bool act[4];
-    auto load_keys = [&](int64_t l0, int w, uint64_t (&k)[4], bool (&a)[4]) {
+    uint64_t key[TS];
+    bool act[TS];
+    auto load_keys = [&](int64_t l0, int w, uint64_t (&k)[TS], bool (&a)[TS]) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < TS; ++t) {
             a[t] = g + 16 * t < w && l0 + g + 16 * t < n;
             if (a[t]) k[t] = h[l0 + g + 16 * t];
         }
     };
     load_keys(l, W, key, act);
     while (l < n) {
-        ulonglong2 v[4];
-        uint32_t bkt[4];
+        ulonglong2 v[TS];
+        uint32_t bkt[TS];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < TS; ++t) {
             if (act[t]) {
                 bkt[t] = bucket_of(key[t], nb);
                 v[t] = *reinterpret_cast<const ulonglong2*>(table + (int64_t)bkt[t] * kBucketKeys + q * 2);
             }
         }
         const int64_t ln = l + W < n ? l + W : n;
-        const int Wn = W * 2 > 64 ? 64 : W * 2;
-        uint64_t nkey[4];
-        bool nact[4];
+        const int Wn = W * 2 > WMAX ? WMAX : W * 2;
+        uint64_t nkey[TS];
+        bool nact[TS];
         load_keys(ln, Wn, nkey, nact);
         int64_t stop = -1;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < TS; ++t) {
             if (16 * t >= W || stop >= 0) break;            // uniform across the wave
             bool hit = true;
             if (act[t]) {
@@ -157,7 +161,7 @@ __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ 
         l = ln;
         W = Wn;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < TS; ++t) {
             key[t] = nkey[t];
             act[t] = nact[t];
         }
@@ -309,7 +313,11 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
                                                         uint64_t* __restrict__ qkeys, uint32_t G,
                                                         int32_t* __restrict__ cont_of, int join) {
     // 16 lanes per request (four requests per wave): the chain of dependent
-    // reads before the compare is the cost, so more requests in flight pay
+    // reads before the compare is the cost, so more requests in flight pay.  A
+    // round compares 16 w positions, lane sl taking j0 + sl + 16 u (u < w), all
+    // loads issued before any compare; w doubles after every all-equal round
+    // (1, 2, 4, 8), so long common prefixes take few dependent rounds.
+    constexpr int kLcpMaxLoads = 8;
     const int lane = threadIdx.x & 63, sg = lane >> 4, sl = lane & 15;
     const int64_t r = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 4 + sg;
     if (r >= R) return;                               // uniform over the 16 lanes
@@ -323,12 +331,30 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
         const int64_t nl = req_off[lead + 1] - req_off[lead];
         const int64_t m = n < nl ? n : nl;
         c = m;
-        for (int64_t j0 = 0; j0 < m; j0 += 16) {
-            const int64_t j = j0 + sl;
-            const bool diff = j < m && a[j] != b[j];
-            const uint32_t mask = (uint32_t)(__ballot(diff) >> (16 * sg)) & 0xFFFFu;
-            if (mask) {
-                c = j0 + __ffs((int)mask) - 1;
+        int w = 1;
+        for (int64_t j0 = 0; j0 < m; j0 += 16 * w, w = w * 2 > kLcpMaxLoads ? kLcpMaxLoads : w * 2) {
+            uint64_t av[kLcpMaxLoads], bv[kLcpMaxLoads];
+#pragma unroll
+            for (int u = 0; u < kLcpMaxLoads; ++u) {
+                const int64_t j = j0 + sl + 16 * u;
+                if (u < w && j < m) {
+                    av[u] = a[j];
+                    bv[u] = b[j];
+                }
+            }
+            int64_t first = m;                       // this lane's first differing position
+#pragma unroll
+            for (int u = kLcpMaxLoads - 1; u >= 0; --u) {
+                const int64_t j = j0 + sl + 16 * u;
+                if (u < w && j < m && av[u] != bv[u]) first = j;
+            }
+#pragma unroll
+            for (int off = 8; off >= 1; off >>= 1) {
+                const int64_t o = __shfl_xor(first, off, 16);
+                first = o < first ? o : first;
+            }
+            if (first < m) {                          // uniform over the 16 lanes
+                c = first;
                 break;
             }
         }

@@ -175,8 +175,8 @@ __global__ __launch_bounds__(512, 1) void score_pairs_mfma_kernel(MfmaArgs A) {
     __shared__ __attribute__((aligned(16))) float lds_b2[H];
     __shared__ __attribute__((aligned(16))) float lds_q[kGroupInst * QS];
     const int tid = threadIdx.x;
-    for (int f = tid; f < MT * 64; f += blockDim.x) lds_w1[f] = A.w1frag[f];
-    for (int f = tid; f < MT * KS2 * 64; f += blockDim.x) lds_w2[f] = A.w2frag[f];
+    lds_fill<4>(lds_w1, MT * 64, [&](int f) { return A.w1frag[f]; });
+    lds_fill<8>(lds_w2, MT * KS2 * 64, [&](int f) { return A.w2frag[f]; });
     for (int f = tid; f < 2 * KS2 * 4; f += blockDim.x) lds_hd[f] = f < KS2 * 4 ? A.hfrag[f] : bf16x8_t{};
     for (int f = tid; f < H; f += blockDim.x) lds_b2[f] = A.b2[f];
 

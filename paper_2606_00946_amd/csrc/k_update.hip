@@ -301,12 +301,12 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
     __shared__ __align__(16) float wl[kDenseMaxK * 32];
     const int jb = blockIdx.y * 32;
     const int nu = O - jb < 32 ? O - jb : 32;
-    for (int e = threadIdx.x; e < K * 32; e += blockDim.x) {
+    lds_fill<8>(wl, K * 32, [&](int e) {
         const int k = e >> 5, u = e & 31;
         float v = 0.0f;
         if (u < nu) v = MODE == kBackprop ? wt[(int64_t)(jb + u) * K + k] : wt[(int64_t)k * O + jb + u];
-        wl[e] = v;
-    }
+        return v;
+    });
     __syncthreads();
     // samples of this lane: block base + wave * 64 P + 64 j + lane
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

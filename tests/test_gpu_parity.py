@@ -490,6 +490,54 @@ def test_followers_and_continuations(mode, pad):
 
 
 @pytest.mark.parametrize("mode", [1, 2])
+def test_long_runs(mode):
+    """Prompts of thousands of blocks: the leaders' runs are extended 256
+    positions per round (prompts of 1024 blocks or more) and common prefixes
+    compared up to 128 positions per round.  Runs that end at a gap deep in the
+    prompt, at the all-ones key, at a window boundary, at the prompt's end, and
+    followers that leave the leader deep in the chain."""
+    note(f"long runs, join mode {mode}")
+    rng = np.random.default_rng(33)
+    E = (1 << 64) - 1
+    A = [int(x) for x in rng.integers(0, 1 << 63, 3000)]
+    A[2222] = E                                  # the all-ones key inside the chain
+    filler = lambda k: [int(x) for x in rng.integers(0, 1 << 63, k)]
+    caches = [
+        A[:1700] + A[1701:2500] + filler(50),    # gap at 1700
+        A + filler(10),                          # the whole chain, all-ones key included
+        A[:1000],                                # ends at 1000
+        A[:2222] + A[2223:],                     # everything but the all-ones key
+        [E] + A[:256] + A[257:2048],             # gap at a window boundary
+        A[:16 + 256 + 1],                        # run of 273 blocks
+        [],
+        A[:3000:2],                              # every other block: run 1
+    ]
+    reqs = [(A, 16 * 3000),                      # the leader
+            (A[:2900] + filler(30), 16 * 2930),   # leaves the chain at 2900
+            (A[:1300] + filler(5), 16 * 1305),    # leaves at 1300
+            (A[:2222], 16 * 2222),               # ends just before the all-ones key
+            (A[:2500], 16 * 2500 + 9),
+            (filler(1200), 16 * 1200),           # a long prompt of its own group
+            (A[:40], 16 * 40)]                   # short follower
+    inst_off, inst_h = oracle_pins._csr(caches)
+    req_off, req_h = oracle_pins._csr([r for r, _ in reqs])
+    L = np.array([l for _, l in reqs], np.int32)
+    base = workload("tiny")
+    N, R, d = len(inst_off) - 1, len(req_off) - 1, base.cfg.d
+    w = synth.Workload(cfg=synth.dataclasses.replace(base.cfg, R=R, N=N), req_off=req_off, req_hashes=req_h,
+                       prompt_len=L, req_group=np.zeros(R, np.int32), inst_off=inst_off, inst_hashes=inst_h,
+                       inst_feat=np.random.default_rng(8).uniform(0, 4, (N, d - 5)).astype(np.float32),
+                       params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
+                       upd_ttft=base.upd_ttft, lr=base.lr)
+    run = GpuRun(w, prefix_join=mode)
+    out = run.score()
+    want = oracle.overlap(req_off, req_h, inst_off, inst_h)
+    np.testing.assert_array_equal(out["overlap"], want)
+    assert list(want[0]) == [1700, 3000, 1000, 2222, 256, 273, 0, 1]
+    check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
+
+
+@pytest.mark.parametrize("mode", [1, 2])
 def test_join_modes_agree_on_a_full_workload(mode):
     """The homogeneous workload with the semi-join forced on and off."""
     w = workload("homogeneous")
