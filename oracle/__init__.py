@@ -22,9 +22,16 @@ _LIB = os.path.join(_HERE, "liblsoracle.so")
 _CFLAGS = ["-O2", "-mfma", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared", "-fPIC", "-std=c11"]
 
 
-def compile_c(src: str, out: str) -> str:
+# The same source with AddressSanitizer and UndefinedBehaviorSanitizer (any
+# finding aborts); a process loads it with both runtimes preloaded.
+SANITIZE_FLAGS = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                  "-fno-omit-frame-pointer"]
+
+
+def compile_c(src: str, out: str, extra=()) -> str:
     tmp = f"{out}.{os.getpid()}.tmp"
-    subprocess.check_call(["gcc", *_CFLAGS, "-o", tmp, src, "-lm"])
+    flags = [f for f in _CFLAGS if not (extra and f.startswith("-O"))]
+    subprocess.check_call(["gcc", *flags, *extra, "-o", tmp, src, "-lm"])
     os.replace(tmp, out)
     return out
 
