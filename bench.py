@@ -50,14 +50,20 @@ PEAK_VALU_FP32_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 # sources they are compiled from.
 KIND_KERNELS = {
     "score_pairs_mfma": (["ls::score_pairs_mfma_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
-    "table_build": (["ls::table_segment_kernel", "ls::table_overflow_kernel"], ["k_cache.hip", "ls_internal.h"]),
+    "table_build": (["ls::seg_inst_kernel", "ls::part_kernel", "ls::table_segment_kernel", "ls::table_overflow_kernel"],
+                    ["k_cache.hip", "ls_internal.h"]),
     "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_filter_kernel",
-                      "ls::cont_scan_kernel", "ls::cont_probe_kernel", "ls::prefix_leaders_kernel",
-                      "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
-    "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "ls_internal.h"]),
-    "update": (["ls::dense_lane_kernel", "ls::wgrad_mfma_kernel", "ls::wgrad_direct_kernel", "ls::wgrad_reduce_kernel",
-                "ls::delta_head_kernel", "ls::normalize_kernel", "ls::loss_grad_kernel", "ls::loss_final_kernel",
-                "ls::sgd_kernel", "ls::refresh_compute_kernel"], ["k_update.hip", "k_score.hip", "ls_internal.h"]),
+                      "ls::cont_scan_kernel", "ls::cont_probe_kernel", "ls::leaders_first_kernel",
+                      "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel", "ls::followers_resolve_kernel",
+                      "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
+    "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
+    "update": (["ls::normalize_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel", "ls::layer_fwd_kernel",
+                "ls::loss_grad_kernel", "ls::loss_final_kernel", "ls::wgrad_direct_kernel",
+                "ls::wgrad_reduce_wave_kernel", "ls::wgrad_reduce_kernel", "ls::wgrad_mfma_kernel",
+                "ls::delta_head_kernel", "ls::backprop_hidden_kernel", "ls::gemm_nt_splitk_kernel",
+                "ls::splitk_reduce_kernel", "ls::rowsum_kernel", "ls::sgd_kernel", "ls::refresh_compute_kernel",
+                "ls::prepare_mfma_kernel"],
+               ["k_update.hip", "k_score.hip", "k_score_mfma.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
 }
 
 
@@ -192,8 +198,9 @@ def time_online_learning(ctx, w):
     import torch
     cfg = w.cfg
     rng = np.random.default_rng(11)
-    x_all = torch.from_numpy(np.ascontiguousarray(w.upd_feats[:11000])).cuda()
-    y_all = torch.from_numpy(np.ascontiguousarray(w.upd_ttft[:11000])).cuda()
+    # 11,000 logged rows (the workload's update rows, repeated if it has fewer)
+    x_all = torch.from_numpy(np.ascontiguousarray(np.resize(w.upd_feats, (11000, cfg.d)))).cuda()
+    y_all = torch.from_numpy(np.ascontiguousarray(np.resize(w.upd_ttft, 11000))).cuda()
     ctx.ls_buffer_init(5000, 5000)
     ctx.ls_buffer_push(x_all[:10000], y_all[:10000])        # fills FIFO and pool
     torch.cuda.synchronize()

@@ -77,9 +77,11 @@ static int64_t align_floats(int64_t n) { return (n + 63) & ~int64_t(63); }
 
 static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
     UpdWs w{};
-    int S = B / 1024;
-    if (S < 1) S = 1;
-    if (S > 128) S = 128;
+    // vector-ALU weight gradients: chunks of 64 samples (up to 256 chunks), so
+    // that even a one-row gradient spreads over many workgroups; the partition
+    // depends on B alone, so the summation order is fixed
+    int64_t S0 = ((int64_t)B + 63) / 64;
+    int S = (int)(S0 < 1 ? 1 : (S0 > 256 ? 256 : S0));
     int64_t chunk = ((int64_t)B + S - 1) / S;
     chunk = (chunk + 15) & ~int64_t(15);
     S = (int)(((int64_t)B + chunk - 1) / chunk);
