@@ -126,6 +126,13 @@ def update_flops(cfg, B):
     return B * (fwd + wgrad + igrad)
 
 
+def chain_flops(cfg, B):
+    """Flops of the update's canonical fma chains: the forward layers and head,
+    and the gradient into the first hidden layer."""
+    d, (h1, h2) = cfg.d, cfg.hidden
+    return B * (2 * (d * h1 + h1 * h2 + h2) + 2 * h1 * h2)
+
+
 def cpu_baseline(w, target_s=12.0, single_requests=256):
     """The oracle, untuned, on a bounded sample of requests (all instances each):
     on every host core, then on one thread over the first `single_requests`
@@ -465,10 +472,15 @@ def main():
     steps = args.steps
     rooflines = scoring_rooflines(cfg, prof, steps, exec_tflop, model_tflop, k1_bytes / 1e9)
     if "update" in prof:
+        t_u = prof["update"][1] / steps / 1e3
+        # the canonical chains (forward layers, head and hidden backprop) run on the vector ALUs
+        chain_tflop = chain_flops(cfg, B) / 1e12
         rooflines["update"] = roofline_entry("update", "mfma" if cfg.dtype == "bf16" else "alu",
                                              update_flops(cfg, B) / 1e12,
                                              PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_VALU_FP32_TFLOPS,
-                                             "TFLOP/s", steps, prof["update"][1], cfg.name)
+                                             "TFLOP/s", steps, prof["update"][1], cfg.name,
+                                             {"valu_chain_tflop_per_s": round(chain_tflop / t_u, 3),
+                                              "valu_chain_frac": round(chain_tflop / t_u / PEAK_VALU_FP32_TFLOPS, 4)})
     if "table_build" in prof:
         # each cached key read once (8 B) and its table written once (two 8-byte slots per key at half load)
         rooflines["table_build"] = roofline_entry("table_build", "hbm", (8 + 16) * int(w.inst_hashes.size) / 1e9,
