@@ -32,6 +32,11 @@
 // the key placed there (`entry_of`), and per instance the position of the
 // all-ones key (`eidx`): with unique keys per instance that is the slot map the
 // index maintenance keeps.
+// Every build also leaves a 32-bit fingerprint of each cached key, segment by
+// segment, for the prefix pass: the segment workgroup writes its run's
+// fingerprints with coalesced stores as it reads the run (4 bytes per key, a
+// quarter of what the table's slots take), and the global pass lists those of
+// the keys it inserts.
 #include "ls_internal.h"
 
 namespace ls {
@@ -312,7 +317,8 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     uint64_t* __restrict__ keys, const int64_t* __restrict__ base, const uint32_t* __restrict__ nbuckets,
     const int32_t* __restrict__ seg_off, const int32_t* __restrict__ seg_inst, const uint32_t* __restrict__ run_len,
     const uint64_t* __restrict__ part_key, const uint32_t* __restrict__ part_idx, int64_t* __restrict__ ovf,
-    uint32_t* __restrict__ ovf_count, uint32_t ovf_cap, uint32_t* __restrict__ entry_of) {
+    uint32_t* __restrict__ ovf_count, uint32_t ovf_cap, uint32_t* __restrict__ entry_of, uint32_t* __restrict__ fp,
+    uint32_t* __restrict__ fp_len, uint32_t* __restrict__ fp_inst) {
     __shared__ uint64_t seg[kSegBuckets * kBucketKeys];
     __shared__ uint32_t fill[kSegBuckets];
     const uint32_t L = blockIdx.x;
@@ -330,9 +336,16 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     __syncthreads();
 
     const int64_t r0 = (base[i] + b0) * kBucketKeys;             // the run, laid out like the segment's slots
-    const int64_t r1 = r0 + min(run_len[L], nbl * (uint32_t)kBucketKeys);
+    const uint32_t len = min(run_len[L], nbl * (uint32_t)kBucketKeys);
+    const int64_t r1 = r0 + len;
+    uint32_t* __restrict__ fp_run = fp + (int64_t)L * kSegSlots;
+    if (tid == 0) {
+        fp_len[L] = len;
+        fp_inst[L] = (uint32_t)i;
+    }
     for (int64_t q = r0 + tid; q < r1; q += kSegThreads) {
         const uint64_t key = part_key[q];
+        fp_run[q - r0] = key_fp(key);        // every key of the run is cached, placed here or by the global pass
         const uint32_t lb = bucket_of(key, nb) - b0;
         const int32_t ls = segment_place(seg, fill, lb, nbl, key);
         if (ls < 0) {
@@ -355,15 +368,21 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
 // that did not fit their segment's run are inserted from their home bucket.
 // If more keys overflowed than the queue holds, every key is (re)inserted from
 // its home bucket instead: keys already placed are found on their probe path,
-// so that is correct too, only slower.
+// so that is correct too, only slower.  The fingerprints of the queued keys go
+// to fp_extra (entry j of the queue at j) and their count to fp_meta[0]; a full
+// queue records a count above both capacities, as the keys past a run's end
+// are then listed nowhere.
 __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t* __restrict__ base,
                                       const uint32_t* __restrict__ nbuckets, const int64_t* __restrict__ inst_off,
                                       int32_t n_inst, const uint64_t* __restrict__ hashes, int64_t total,
                                       const int64_t* __restrict__ ovf, const uint32_t* __restrict__ ovf_count,
-                                      uint32_t ovf_cap, uint32_t* __restrict__ entry_of) {
+                                      uint32_t ovf_cap, uint32_t* __restrict__ entry_of, uint32_t* __restrict__ fp_extra,
+                                      uint32_t* __restrict__ fp_extra_inst, uint32_t fp_extra_cap,
+                                      uint32_t* __restrict__ fp_meta) {
     const uint32_t n = *ovf_count;
-    if (n == 0) return;
     const bool queued = n <= ovf_cap;
+    if (blockIdx.x == 0 && threadIdx.x == 0) fp_meta[0] = queued && n <= fp_extra_cap ? n : 0xFFFFFFFFu;
+    if (n == 0) return;
     const int64_t n_keys = inst_off[n_inst] < total ? inst_off[n_inst] : total;   // total bounds the key count
     const int64_t count = queued ? (int64_t)n : n_keys;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -372,8 +391,12 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
         const bool from_home = entry < 0;                 // past its segment's run: probe from home
         const int64_t t = from_home ? ~entry : entry;
         const uint64_t key = hashes[t];
-        if (key == kEmptyKey) continue;
         const int32_t i = owner_of(inst_off, n_inst, t);
+        if (queued && j < (int64_t)fp_extra_cap) {
+            fp_extra[j] = key == kEmptyKey ? kFpEmpty : key_fp(key);
+            fp_extra_inst[j] = (uint32_t)i;
+        }
+        if (key == kEmptyKey) continue;
         const uint32_t nb = nbuckets[i];
         uint32_t b = bucket_of(key, nb);
         if (queued && !from_home) {
@@ -387,6 +410,31 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
 
 int64_t table_overflow_capacity(int64_t total) { return 4096 + total / 64; }
 
+static int64_t up256(int64_t b) { return (b + 255) / 256 * 256; }
+
+int64_t table_fp_bytes(int32_t n_seg, int64_t extra_cap) {
+    const int64_t segs = n_seg > 0 ? n_seg : 1, extra = extra_cap > 0 ? extra_cap : 1;
+    return up256(4 * segs * kSegSlots) + 2 * up256(4 * segs) + 2 * up256(4 * extra) + 256;
+}
+
+void carve_table_fp(CacheTables& t, void* buf, int32_t n_seg, int64_t extra_cap) {
+    char* p = static_cast<char*>(buf);
+    const int64_t segs = n_seg > 0 ? n_seg : 1, extra = extra_cap > 0 ? extra_cap : 1;
+    t.fp = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * segs * kSegSlots);
+    t.fp_len = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * segs);
+    t.fp_inst = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * segs);
+    t.fp_extra = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * extra);
+    t.fp_extra_inst = reinterpret_cast<uint32_t*>(p);
+    p += up256(4 * extra);
+    t.fp_meta = reinterpret_cast<uint32_t*>(p);
+    t.fp_extra_cap = extra_cap;
+    t.n_seg = n_seg;
+}
+
 // Workspace: overflow counter (256 B) and queue, run lengths, the instance of
 // every segment, and the runs: a key and input position per table slot.
 struct BuildWs {
@@ -397,8 +445,6 @@ struct BuildWs {
     uint64_t* part_key;
     uint32_t* part_idx;
 };
-
-static int64_t up256(int64_t b) { return (b + 255) / 256 * 256; }
 
 static BuildWs carve_build_ws(void* ws, int64_t total, int32_t n_seg, int64_t total_buckets) {
     char* p = static_cast<char*>(ws);
@@ -427,6 +473,8 @@ int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg, int64_t total_
 hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, const int32_t* seg_off, int32_t n_seg,
                               const uint64_t* hashes, int64_t total, int32_t n_inst, void* ws, int n_cu,
                               hipStream_t s, uint32_t* entry_of, int64_t* eidx) {
+    if (!t.fp || !t.fp_len || !t.fp_inst || !t.fp_extra || !t.fp_extra_inst || !t.fp_meta || t.n_seg < n_seg)
+        return hipErrorInvalidValue;
     const BuildWs w = carve_build_ws(ws, total, n_seg, t.total_buckets);
     const uint32_t cap = (uint32_t)table_overflow_capacity(total);
     hipError_t e;
@@ -445,11 +493,12 @@ hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, con
     if (n_seg > 0) {
         hipLaunchKernelGGL(table_segment_kernel, dim3((uint32_t)n_seg), dim3(kSegThreads), 0, s, t.keys, t.base,
                            t.nbuckets, seg_off, w.seg_inst, w.run_len, w.part_key, w.part_idx, w.ovf, w.ovf_count,
-                           cap, entry_of);
+                           cap, entry_of, t.fp, t.fp_len, t.fp_inst);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(table_overflow_kernel, dim3((uint32_t)(4 * n_cu)), dim3(256), 0, s, t.keys, t.base,
-                       t.nbuckets, inst_off, n_inst, hashes, total, w.ovf, w.ovf_count, cap, entry_of);
+                       t.nbuckets, inst_off, n_inst, hashes, total, w.ovf, w.ovf_count, cap, entry_of, t.fp_extra,
+                       t.fp_extra_inst, (uint32_t)(t.fp_extra_cap < 0xFFFFFFFFll ? t.fp_extra_cap : 0xFFFFFFFEll), t.fp_meta);
     return hipGetLastError();
 }
 

@@ -18,10 +18,13 @@
 // Continuations.  Where l[lead,i] >= c, the follower's run goes on from block
 // c, whose hash is usually the follower's own (its question after a shared
 // template) and cached nowhere.  For a large batch the library first collects
-// those continuation hashes in a small table and marks, in one sequential pass
-// over every cached key, the ones some instance holds (a semi-join).  A
-// follower whose continuation is cached nowhere has l[r,i] = c wherever
-// l[lead,i] >= c, with no probe; only the others are probed.
+// the 32-bit fingerprints of those continuation hashes in a small table and
+// marks, in one sequential pass over the fingerprints of every cached key
+// (which each table build leaves behind, 4 bytes per key), the ones some
+// instance's key shares (a semi-join).  A follower whose continuation's
+// fingerprint is unmarked has its block c cached nowhere, so l[r,i] = c
+// wherever l[lead,i] >= c, with no probe; the others are probed.  Two keys that
+// share a fingerprint only cost probes, never a wrong overlap.
 //
 // Probing.  Four lanes share one 64-byte bucket (16 bytes each), so a wave
 // probes 16 pairs at once and every probe is one coalesced 64-byte read.  A
@@ -29,6 +32,8 @@
 // of consecutive positions that doubles after every all-hit window (1, 2, 4,
 // ... kMaxWindow): short runs waste few probes, long runs keep kMaxWindow reads
 // in flight.  The first miss ends the pair.
+#include <type_traits>
+
 #include "ls_internal.h"
 
 namespace ls {
@@ -284,34 +289,65 @@ __global__ __launch_bounds__(kGroupThreads) void group_insert_kernel(int32_t R, 
     if (r < R) slot_of[r] = lidx >= 0 ? lslot[lidx] : -1;
 }
 
-// Continuation table: open addressing over G slots of uint64 keys.
-__device__ __forceinline__ int32_t cont_insert(uint64_t* __restrict__ qkeys, uint32_t G, uint64_t key) {
-    uint32_t b = bucket_of(key, G);
+// Continuation table: open addressing over G slots (a power of two, at most
+// half full) of fingerprints, kFpEmpty marking an empty slot.  The thread that
+// claims a slot also sets the fingerprint's three bits in the scan's filter, a
+// Bloom filter blocked by 32-bit word: word f >> 17, bits f & 31, (f >> 5) & 31
+// and (f >> 10) & 31, so a test is one word read and a few bit operations
+// (about 0.6 % of other fingerprints pass at 65,536 continuations).
+constexpr int kContFilterLog = 20;
+constexpr int kContFilterWords = (1 << kContFilterLog) / 32;     // 128 KiB
+static_assert(kContFilterWords == 1 << 15, "the filter word is the fingerprint's top 15 bits");
+
+__device__ __forceinline__ uint32_t fp_slot(uint32_t f, uint32_t G) {
+    return (uint32_t)(((uint64_t)(f * 0x85EBCA77u) * G) >> 32);
+}
+
+__device__ __forceinline__ uint32_t fp_word_bits(uint32_t f) {
+    return (1u << (f & 31)) | (1u << ((f >> 5) & 31)) | (1u << ((f >> 10) & 31));
+}
+
+__device__ __forceinline__ int32_t cont_insert(uint32_t* __restrict__ qfp, uint32_t G, uint32_t f,
+                                               uint32_t* __restrict__ filter) {
+    uint32_t b = fp_slot(f, G);
     for (uint32_t probe = 0; probe < G; ++probe) {
-        const uint64_t cur = qkeys[b];
-        if (cur == key) return (int32_t)b;
-        if (cur == kEmptyKey) {
-            const unsigned long long old = atomicCAS((unsigned long long*)(qkeys + b), (unsigned long long)kEmptyKey,
-                                                     (unsigned long long)key);
-            if (old == kEmptyKey || old == key) return (int32_t)b;
+        const uint32_t cur = qfp[b];
+        if (cur == f) return (int32_t)b;
+        if (cur == kFpEmpty) {
+            const uint32_t old = atomicCAS(qfp + b, kFpEmpty, f);
+            if (old == kFpEmpty) {
+                atomicOr(&filter[f >> 17], fp_word_bits(f));
+                return (int32_t)b;
+            }
+            if (old == f) return (int32_t)b;
         }
         b = (b + 1 == G) ? 0 : b + 1;
     }
     return kContProbe;
 }
 
+// What the semi-join found for a continuation slot: qseen counts the matches,
+// and the first kSeenInst of them record their instance in qinst (a 16-byte
+// word per slot).  0: the continuation's block is cached nowhere; 1 ..
+// kSeenInst: at most on the recorded instances; more: on any instance.  A
+// nonzero qall (the build's key listing incomplete, or a candidate list
+// overflowed) makes every continuation count as cached on any instance.
+constexpr uint32_t kSeenInst = 4;
+constexpr uint32_t kSeenAny = kSeenInst + 1;
+
 // One wave per request: leader id and common-prefix length with the leader;
 // leaders append themselves to the leader list.  With the semi-join on, a
-// follower registers the hash of its block c (cont_of: slot, kContNone when c
-// reaches its end, kContProbe when it must be probed).
+// follower registers the fingerprint of its block c (cont_of: slot, kContNone
+// when c reaches its end, kContProbe when it must be probed).
 __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t* __restrict__ req_off,
                                                         const uint64_t* __restrict__ req_hashes,
                                                         const unsigned long long* __restrict__ glead,
                                                         const int32_t* __restrict__ slot_of,
                                                         int32_t* __restrict__ lead_of, int32_t* __restrict__ lcp_of,
                                                         int32_t* __restrict__ leaders, uint32_t* __restrict__ n_leaders,
-                                                        uint64_t* __restrict__ qkeys, uint32_t G,
-                                                        int32_t* __restrict__ cont_of, int join) {
+                                                        uint32_t* __restrict__ qfp, uint32_t G,
+                                                        uint32_t* __restrict__ qfilter, int32_t* __restrict__ cont_of,
+                                                        int join) {
     // 16 lanes per request (four requests per wave): the chain of dependent
     // reads before the compare is the cost, so more requests in flight pay.  A
     // round compares 16 w positions, lane sl taking j0 + sl + 16 u (u < w), all
@@ -366,122 +402,218 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
         int32_t cont = kContNone;
         if (lead != r && c < n) {
             const uint64_t key = req_hashes[req_off[r] + c];
-            cont = (join && key != kEmptyKey) ? cont_insert(qkeys, G, key) : kContProbe;
+            cont = (join && key != kEmptyKey) ? cont_insert(qfp, G, key_fp(key), qfilter) : kContProbe;
         }
         cont_of[r] = cont;
     }
 }
 
-// The semi-join pass: every cached key looks itself up among the continuation
-// hashes and marks the ones it finds.  A two-bit Bloom filter of the
-// continuation hashes (kContFilterBits) sits in LDS, so the scan streams the
-// tables and tests two LDS bits per key; keys that pass go on a list, and a
-// second kernel looks them up in the continuation table.  If the list
-// overflows, every continuation is marked seen (its followers are probed, so
-// the overlaps stay exact).
-constexpr int kContFilterLog = 20;
-constexpr int kContFilterWords = (1 << kContFilterLog) / 32;     // 128 KiB
+// The semi-join pass: every cached key's fingerprint looks itself up among the
+// continuations'.  The continuations' Bloom filter sits in LDS, so the pass
+// streams the fingerprint runs of the table build and tests one LDS word per
+// key.  The positions of the fingerprints that pass go on a list of the wave's
+// own in LDS, which the wave looks up in the continuation table whenever it
+// holds kWaveFlush or more and at the end (a wave whose list overflows makes
+// every continuation count as cached everywhere).  A match records its instance with the
+// continuation: the follower is then probed on the recorded instances only.
+// Waves take whole segments and run unsynchronised after the filter copy, so
+// the tests and lookups of some overlap the loads of others.  If the build
+// could not list every key that went through its overflow pass, every
+// continuation counts as cached everywhere (its followers are probed, so the
+// overlaps stay exact).
 constexpr int kContThreads = 1024;
-constexpr int64_t kContListCap = 1 << 22;
+constexpr int kContWaves = kContThreads / 64;
+constexpr int kContLoads = 8;                      // 16-byte loads per lane per chunk
+constexpr uint32_t kContChunk = 64 * 4 * kContLoads;   // fingerprints per chunk of a wave (2048)
+constexpr uint32_t kWaveCand = 512;                // LDS candidate list of each wave: positions (2 KiB)
+constexpr uint32_t kWaveFlush = 256;               // a wave looks its list up once it holds this many
+constexpr uint32_t kExtraTag = 0x80000000u;        // list entry of the overflow pass's list
 
-__device__ __forceinline__ void cont_bits(uint64_t key, uint32_t& b0, uint32_t& b1) {
-    const uint64_t x = key * 0xD6E8FEB86659FD93ull;
-    b0 = (uint32_t)(x >> (64 - kContFilterLog));
-    b1 = (uint32_t)(x >> 8) & ((1u << kContFilterLog) - 1);
+__device__ __forceinline__ void cont_mark(const uint32_t* __restrict__ qfp, uint32_t G, uint32_t f, uint32_t inst,
+                                          uint32_t* __restrict__ qseen, uint32_t* __restrict__ qinst) {
+    uint32_t b = fp_slot(f, G);
+    for (uint32_t probe = 0; probe < G; ++probe) {
+        const uint32_t cur = qfp[b];
+        if (cur == kFpEmpty) return;
+        if (cur == f) {
+            if (qseen[b] > kSeenInst) return;             // already unlimited
+            const uint32_t k = atomicAdd(qseen + b, 1u);
+            if (k < kSeenInst) qinst[(int64_t)b * kSeenInst + k] = inst;
+            return;
+        }
+        b = (b + 1 == G) ? 0 : b + 1;
+    }
 }
 
-__global__ void cont_filter_kernel(const uint64_t* __restrict__ qkeys, uint32_t G, uint32_t* __restrict__ filter) {
-    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= G) return;
-    const uint64_t key = qkeys[b];
-    if (key == kEmptyKey) return;
-    uint32_t b0, b1;
-    cont_bits(key, b0, b1);
-    atomicOr(&filter[b0 >> 5], 1u << (b0 & 31));
-    atomicOr(&filter[b1 >> 5], 1u << (b1 & 31));
-}
-
-// Workgroup b appends the keys that pass the filter to its own slice of the
-// candidate list (cap entries, counted in LDS); no global counter is shared.
-__global__ __launch_bounds__(kContThreads) void cont_scan_kernel(const uint64_t* __restrict__ keys, int64_t n_slots,
-                                                                 const uint32_t* __restrict__ filter,
-                                                                 uint64_t* __restrict__ cand, uint32_t cap,
-                                                                 uint32_t* __restrict__ n_cand) {
+__global__ __launch_bounds__(kContThreads) void cont_scan_kernel(
+    const uint32_t* __restrict__ fp, const uint32_t* __restrict__ fp_len, const uint32_t* __restrict__ fp_inst,
+    int32_t n_seg, const uint32_t* __restrict__ fp_extra, const uint32_t* __restrict__ fp_extra_inst,
+    const uint32_t* __restrict__ fp_meta, uint32_t fp_extra_cap, const uint32_t* __restrict__ filter,
+    const uint32_t* __restrict__ qfp, uint32_t G, uint32_t* __restrict__ qseen, uint32_t* __restrict__ qinst,
+    uint32_t* __restrict__ qall) {
     __shared__ uint32_t lf[kContFilterWords];
-    __shared__ uint32_t lcount;
+    __shared__ uint32_t cand[kContWaves][kWaveCand];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t n_extra = fp_meta[0];
+    if (n_extra > fp_extra_cap) {                         // uniform: some cached keys are listed nowhere
+        if (blockIdx.x == 0 && tid == 0) qall[0] = 1u;
+        return;
+    }
+    uint32_t* __restrict__ mine = cand[wv];
+    uint32_t wcount = 0;                                  // entries of this wave's list (uniform)
+    // looks the wave's listed candidates up in the continuation table; an
+    // entry is the fingerprint's position in the runs, or kExtraTag | j for
+    // entry j of the overflow pass's list
+    auto flush = [&]() {
+        for (uint32_t e = (uint32_t)lane; e < wcount; e += 64) {
+            const uint32_t p = mine[e];
+            uint32_t f, inst;
+            if (p & kExtraTag) {
+                f = fp_extra[p & ~kExtraTag];
+                inst = fp_extra_inst[p & ~kExtraTag];
+            } else {
+                f = fp[p];
+                inst = fp_inst[p / (uint32_t)kSegSlots];
+            }
+            cont_mark(qfp, G, f, inst, qseen, qinst);
+        }
+        wcount = 0;
+    };
+    // appends the entries pos + k of the lanes whose bit is set in the ballot
+    // m[k] (K of them) to the wave's list: entry k of a lane goes after the
+    // wave's entries of slots below k and the lanes below it (lane-mask
+    // counts).  A list that overflows drops the rest and sets qall, which
+    // makes every continuation count as cached on every instance.  Every lane
+    // of the wave calls it, and only when some lane hit.
+    auto append = [&](const uint64_t* m, uint32_t pos, int K) {
+        uint32_t at0 = wcount;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if ((m[k] >> lane) & 1ull) {
+                const uint32_t at = at0 + __builtin_amdgcn_mbcnt_hi((uint32_t)(m[k] >> 32),
+                                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m[k], 0u));
+                if (at < kWaveCand) mine[at] = pos + (uint32_t)k;
+            }
+            at0 += (uint32_t)__popcll(m[k]);
+        }
+        if (at0 > kWaveCand) {                            // uniform
+            if (lane == 0) qall[0] = 1u;
+            at0 = kWaveCand;
+        }
+        wcount = at0;
+    };
+    // tests four fingerprints of a lane, at positions e0 .. e0 + 3 of segment
+    // L's run of len (FULL: the wave's whole group lies inside the run); the
+    // LDS reads go out together and each test is a ballot
+    auto test4 = [&](auto full_tag, const uint4& x, uint32_t e0, uint32_t len, uint32_t run0) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const uint32_t f[4] = {x.x, x.y, x.z, x.w};
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = lf[f[k] >> 17];
+        uint64_t m[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t bits = fp_word_bits(f[k]);
+            if constexpr (FULL) m[k] = __ballot((w[k] & bits) == bits);
+            else m[k] = __ballot(((w[k] & bits) == bits) & (e0 + (uint32_t)k < len));
+        }
+        if ((m[0] | m[1] | m[2] | m[3]) != 0) append(m, run0 + e0, 4);   // uniform over the wave
+    };
+    // The wave's chunks: segments w, w + W, ... of the grid's W waves, each in
+    // chunks of kContChunk fingerprints.  Two chunk buffers (A, B) alternate:
+    // a chunk's loads go out before the chunk ahead of it is tested, and the
+    // first two go out before the filter copy.  The cursor is uniform over the
+    // wave, and no barrier ties the waves together after the copy.
+    struct Chunk {
+        uint32_t c0, len;
+        int64_t L;
+        bool on;
+    };
+    const int64_t W = (int64_t)gridDim.x * kContWaves;
+    int64_t cur_L = (int64_t)blockIdx.x * kContWaves + wv;
+    uint32_t cur_c0 = 0, cur_len = cur_L < n_seg ? fp_len[cur_L] : 0u;
+    auto take = [&](Chunk& d) {
+        d.on = cur_L < n_seg;
+        if (!d.on) {
+            d.L = 0;
+            d.c0 = 0;
+            d.len = 0;
+            return;
+        }
+        d.L = cur_L;
+        d.c0 = cur_c0;
+        d.len = cur_len;
+        cur_c0 += kContChunk;
+        if (cur_c0 >= cur_len) {
+            cur_L += W;
+            cur_c0 = 0;
+            cur_len = cur_L < n_seg ? fp_len[cur_L] : 0u;
+        }
+    };
+    // Every lane issues all kContLoads loads of a chunk, so that each refill is
+    // the same straight run of loads and a test waits only for its own buffer.
+    // They stay inside the segment's slots: c0 is a multiple of kContChunk
+    // below len <= kSegSlots, so e < kSegSlots; past len (or, with no chunk,
+    // in segment 0) they read data the test ignores.
+    static_assert(kSegSlots % kContChunk == 0, "chunks tile a segment's slots");
+    auto load = [&](const Chunk& d, uint4 (&x)[kContLoads]) {
+        const uint4* __restrict__ run = reinterpret_cast<const uint4*>(fp + d.L * kSegSlots);
+#pragma unroll
+        for (int u = 0; u < kContLoads; ++u) x[u] = run[d.c0 / 4 + (uint32_t)(lane + 64 * u)];
+    };
+    // a group of four past the run's end for the whole wave is skipped, one
+    // inside it for the whole wave is tested without the bound; the wave looks
+    // its list up when it holds kWaveFlush entries or more
+    auto test_chunk = [&](const Chunk& d, const uint4 (&x)[kContLoads]) {
+        const uint32_t run0 = (uint32_t)(d.L * kSegSlots);
+        if (d.c0 + kContChunk <= d.len) {                // uniform: the whole chunk lies inside the run
+#pragma unroll
+            for (int u = 0; u < kContLoads; ++u)
+                test4(std::true_type{}, x[u], d.c0 + 4u * (uint32_t)(lane + 64 * u), d.len, run0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kContLoads; ++u) {
+                const uint32_t first = d.c0 + 256u * (uint32_t)u;
+                if (first < d.len) test4(std::false_type{}, x[u], d.c0 + 4u * (uint32_t)(lane + 64 * u), d.len, run0);
+            }
+        }
+        if (wcount >= kWaveFlush) flush();
+    };
+    Chunk da, db;
+    uint4 xa[kContLoads], xb[kContLoads];
+    take(da);
+    load(da, xa);
+    take(db);
+    load(db, xb);
     {
         const uint4* __restrict__ f4 = reinterpret_cast<const uint4*>(filter);
         uint4* l4 = reinterpret_cast<uint4*>(lf);
-        for (int e = threadIdx.x; e < kContFilterWords / 4; e += kContThreads) l4[e] = f4[e];
-        if (threadIdx.x == 0) lcount = 0u;
+        for (int e = tid; e < kContFilterWords / 4; e += kContThreads) l4[e] = f4[e];
     }
     __syncthreads();
-    const int lane = threadIdx.x & 63;
-    uint64_t* __restrict__ mine = cand + (int64_t)blockIdx.x * cap;
-    const ulonglong2* __restrict__ k2 = reinterpret_cast<const ulonglong2*>(keys);
-    const int64_t n2 = n_slots / 2;
-    const int64_t stride = (int64_t)gridDim.x * kContThreads;
-    // every lane runs the same number of iterations (the ballots below need the whole wave)
-    for (int64_t e0 = (int64_t)blockIdx.x * kContThreads + threadIdx.x; e0 - threadIdx.x < n2; e0 += 4 * stride) {
-        ulonglong2 v[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int64_t e = e0 + u * stride;
-            v[u] = e < n2 ? k2[e] : ulonglong2{kEmptyKey, kEmptyKey};
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint64_t kk[2] = {v[u].x, v[u].y};
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const uint64_t key = kk[j];
-                bool pass = false;
-                if (key != kEmptyKey) {
-                    uint32_t b0, b1;
-                    cont_bits(key, b0, b1);
-                    pass = ((lf[b0 >> 5] >> (b0 & 31)) & 1u) && ((lf[b1 >> 5] >> (b1 & 31)) & 1u);
-                }
-                const uint64_t m = __ballot(pass);
-                if (m) {
-                    const int first = __ffsll((long long)m) - 1;
-                    uint32_t base = 0;
-                    if (lane == first) base = atomicAdd(&lcount, (uint32_t)__popcll(m));
-                    base = (uint32_t)__shfl((int)base, first);
-                    const uint32_t pos = base + (uint32_t)__popcll(m & ((1ull << lane) - 1));
-                    if (pass && pos < cap) mine[pos] = key;
-                }
-            }
-        }
+    while (da.on || db.on) {                              // uniform over the wave
+        test_chunk(da, xa);                               // nothing to test without a chunk (len 0)
+        take(da);
+        load(da, xa);
+        test_chunk(db, xb);
+        take(db);
+        load(db, xb);
     }
-    __syncthreads();
-    if (threadIdx.x == 0) n_cand[blockIdx.x] = lcount;
-}
-
-// Block b looks up slice b.  A slice that overflowed marks every continuation
-// seen (its keys are lost, so their followers must be probed).
-__global__ __launch_bounds__(256) void cont_probe_kernel(const uint64_t* __restrict__ cand, uint32_t cap,
-                                                         const uint32_t* __restrict__ n_cand,
-                                                         const uint64_t* __restrict__ qkeys, uint32_t G,
-                                                         uint32_t* __restrict__ qseen) {
-    const uint32_t cnt = n_cand[blockIdx.x];
-    if (cnt > cap) {
-        for (uint32_t b = threadIdx.x; b < G; b += blockDim.x) qseen[b] = 1u;
-        return;
-    }
-    const uint64_t* __restrict__ mine = cand + (int64_t)blockIdx.x * cap;
-    for (uint32_t e = threadIdx.x; e < cnt; e += blockDim.x) {
-        const uint64_t key = mine[e];
-        uint32_t b = bucket_of(key, G);
-        for (uint32_t probe = 0; probe < G; ++probe) {
-            const uint64_t cur = qkeys[b];
-            if (cur == kEmptyKey) break;
-            if (cur == key) {
-                qseen[b] = 1u;
-                break;
-            }
-            b = (b + 1 == G) ? 0 : b + 1;
+    // the keys of the overflow pass, 64 per wave of the grid
+    for (int64_t j0 = ((int64_t)blockIdx.x * kContWaves + wv) * 64; j0 < n_extra; j0 += W * 64) {
+        const int64_t j = j0 + lane;
+        bool hit = false;
+        if (j < n_extra) {
+            const uint32_t f = fp_extra[j];
+            const uint32_t bits = fp_word_bits(f);
+            hit = f != kFpEmpty && (lf[f >> 17] & bits) == bits;
         }
+        const uint64_t m[1] = {__ballot(hit)};
+        if (m[0] != 0) append(m, kExtraTag | (uint32_t)j, 1);
+        if (wcount >= kWaveFlush) flush();
     }
+    flush();
 }
 
 // ---------------------------------------------------------------------------
@@ -519,20 +651,28 @@ __global__ __launch_bounds__(256) void prefix_leaders_kernel(ProbeTables T, int3
 // Leaders, first block: 16 (leader, instance) pairs per wave, four lanes per
 // 64-byte bucket.  A pair whose first block is not cached on the instance (most
 // pairs) or whose prompt has at most one block is answered here; the others go
-// on a list (one atomic per wave) and are extended from block 1 by a wave each.
-__global__ __launch_bounds__(256) void leaders_first_kernel(ProbeTables T, int32_t N,
-                                                            const int64_t* __restrict__ req_off,
-                                                            const uint64_t* __restrict__ req_hashes,
-                                                            const int32_t* __restrict__ leaders,
-                                                            const uint32_t* __restrict__ n_leaders,
-                                                            int32_t* __restrict__ overlap, int64_t* __restrict__ more,
-                                                            uint32_t* __restrict__ n_more) {
+// on a list and are extended from block 1 by a wave each.  The workgroup's
+// waves step through the pairs together, kLeadThreads / 4 per round, and a
+// round's list entries are counted in LDS and claimed with one global add:
+// adds to one global counter from every wave serialise.
+constexpr int kLeadThreads = 1024;
+constexpr int64_t kLeadPairs = kLeadThreads / 4;
+
+__global__ __launch_bounds__(kLeadThreads) void leaders_first_kernel(ProbeTables T, int32_t N,
+                                                                     const int64_t* __restrict__ req_off,
+                                                                     const uint64_t* __restrict__ req_hashes,
+                                                                     const int32_t* __restrict__ leaders,
+                                                                     const uint32_t* __restrict__ n_leaders,
+                                                                     int32_t* __restrict__ overlap,
+                                                                     int64_t* __restrict__ more,
+                                                                     uint32_t* __restrict__ n_more) {
+    __shared__ uint32_t lcount, lbase;
     const int lane = threadIdx.x & 63, g = lane >> 2, q = lane & 3, shift = 4 * g;
     const int64_t total = (int64_t)(*n_leaders) * N;
-    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
-    for (int64_t b0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 16; b0 < total;
-         b0 += waves * 16) {
-        const int64_t pair = b0 + g;
+    for (int64_t r0 = (int64_t)blockIdx.x * kLeadPairs; r0 < total; r0 += (int64_t)gridDim.x * kLeadPairs) {
+        if (threadIdx.x == 0) lcount = 0u;
+        __syncthreads();
+        const int64_t pair = r0 + (threadIdx.x >> 2);
         const bool act = pair < total;
         int64_t i = 0, r = 0, h0 = 0, n = 0;
         if (act) {
@@ -565,13 +705,16 @@ __global__ __launch_bounds__(256) void leaders_first_kernel(ProbeTables T, int32
         const bool go_on = act && hit && n > 1;
         if (act && q == 0 && !go_on) overlap[r * N + i] = hit ? 1 : 0;
         const uint64_t m = __ballot(go_on && q == 0);
-        if (m) {
-            const int first = __ffsll((long long)m) - 1;
-            uint32_t base = 0;
-            if (lane == first) base = atomicAdd(n_more, (uint32_t)__popcll(m));
-            base = (uint32_t)__shfl((int)base, first);
-            if (go_on && q == 0) more[base + __popcll(m & ((1ull << lane) - 1))] = pair;
+        uint32_t wbase = 0;
+        if (m != 0 && lane == __ffsll((long long)m) - 1) wbase = atomicAdd(&lcount, (uint32_t)__popcll(m));
+        __syncthreads();
+        if (threadIdx.x == 0) lbase = lcount ? atomicAdd(n_more, lcount) : 0u;
+        __syncthreads();
+        if (m != 0) {
+            wbase = lbase + (uint32_t)__shfl((int)wbase, __ffsll((long long)m) - 1);
+            if (go_on && q == 0) more[wbase + __popcll(m & ((1ull << lane) - 1))] = pair;
         }
+        __syncthreads();                                  // lcount and lbase are reused next round
     }
 }
 
@@ -611,13 +754,15 @@ constexpr int kResolveThreads = 1024;
 template <bool VEC>
 __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
     int32_t R, int32_t N, int64_t chunk, const int32_t* __restrict__ lead_of, const int32_t* __restrict__ lcp_of,
-    const int32_t* __restrict__ cont_of, const uint32_t* __restrict__ qseen, int32_t* __restrict__ overlap,
-    int64_t* __restrict__ list, uint32_t* __restrict__ n_list) {
+    const int32_t* __restrict__ cont_of, const uint32_t* __restrict__ qseen, const uint4* __restrict__ qinst,
+    const uint32_t* __restrict__ qall, int32_t* __restrict__ overlap, int64_t* __restrict__ list,
+    uint32_t* __restrict__ n_list) {
     constexpr int V = VEC ? 4 : 1;
     __shared__ uint32_t lcount;
     if (threadIdx.x == 0) lcount = 0u;
     __syncthreads();
     const int lane = threadIdx.x & 63;
+    const bool any_inst = qall[0] != 0u;                 // every continuation may be cached anywhere
     const int64_t pairs = (int64_t)R * N;
     const int64_t p_begin = (int64_t)blockIdx.x * chunk;
     const int64_t p_end = p_begin + chunk < pairs ? p_begin + chunk : pairs;
@@ -631,8 +776,17 @@ __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
             if (lead != r) {
                 const int32_t c = lcp_of[r];
                 const int32_t cont = cont_of[r];
+                const uint32_t seen = cont < 0 || any_inst ? kSeenAny : qseen[cont];
                 // the prompt ends in the shared prefix, or block c is cached nowhere
-                const bool at_c = cont == kContNone || (cont >= 0 && qseen[cont] == 0u);
+                const bool at_c = cont == kContNone || seen == 0u;
+                // the instances that may hold block c, when the semi-join recorded them all
+                uint4 holders = {~0u, ~0u, ~0u, ~0u};
+                if (!at_c && seen <= kSeenInst) holders = qinst[cont];
+                auto may_hold = [&](uint32_t inst) -> bool {
+                    if (seen > kSeenInst) return true;
+                    return (holders.x == inst) | (seen > 1u && holders.y == inst) | (seen > 2u && holders.z == inst) |
+                           (seen > 3u && holders.w == inst);
+                };
                 int32_t ll[V], out[V];
                 if constexpr (VEC) {
                     const int4 q = *reinterpret_cast<const int4*>(overlap + lead * N + i);
@@ -643,7 +797,8 @@ __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
 #pragma unroll
                 for (int j = 0; j < V; ++j) {
                     out[j] = ll[j] < c ? ll[j] : c;
-                    if (ll[j] >= c && !at_c) push |= 1u << j;
+                    // block c may be cached on this instance: probe it
+                    if (ll[j] >= c && !at_c && may_hold((uint32_t)(i + j))) push |= 1u << j;
                 }
                 if (VEC && push == 0) {
                     *reinterpret_cast<int4*>(overlap + pair) = int4{out[0], out[V > 1 ? 1 : 0], out[V > 2 ? 2 : 0],
@@ -710,9 +865,9 @@ int64_t prefix_workspace_bytes(int32_t R, int32_t N) {
     return 2 * ws_round(G * 8)                  // group table, leader words
            + 5 * ws_round((int64_t)R * 4)       // slot_of, lead_of, lcp_of, leaders, cont_of
            + 256                                // leader counter
-           + ws_round(G * 8) + ws_round(G * 4)  // continuation keys, seen flags
+           + 2 * ws_round(G * 4)                // continuation fingerprints, seen flags
+           + ws_round(G * 16)                   // instances recorded per continuation
            + ws_round((int64_t)kContFilterWords * 4)
-           + ws_round(kMaxSlices * 4) + ws_round(kContListCap * 8)   // semi-join candidates
            + ws_round(kMaxSlices * 4) + ws_round((int64_t)R * N * 8);  // probe list
 }
 
@@ -743,38 +898,38 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     int32_t* leaders = reinterpret_cast<int32_t*>(take((int64_t)R * 4));
     int32_t* cont_of = reinterpret_cast<int32_t*>(take((int64_t)R * 4));
     uint32_t* n_leaders = reinterpret_cast<uint32_t*>(take(256));
-    uint64_t* qkeys = reinterpret_cast<uint64_t*>(take(G * 8));
+    uint32_t* qfp = reinterpret_cast<uint32_t*>(take(G * 4));
     uint32_t* qseen = reinterpret_cast<uint32_t*>(take(G * 4));
+    uint32_t* qinst = reinterpret_cast<uint32_t*>(take(G * 16));
     uint32_t* n_list = reinterpret_cast<uint32_t*>(take(kMaxSlices * 4));
     uint32_t* qfilter = reinterpret_cast<uint32_t*>(take((int64_t)kContFilterWords * 4));
-    uint32_t* n_cand = reinterpret_cast<uint32_t*>(take(kMaxSlices * 4));
-    uint64_t* cand = join ? reinterpret_cast<uint64_t*>(take(kContListCap * 8)) : nullptr;
     int64_t* list = reinterpret_cast<int64_t*>(take((int64_t)R * N * 8));
 
+    if (join && (!t.fp || !t.fp_len || !t.fp_inst || !t.fp_extra || !t.fp_extra_inst || !t.fp_meta))
+        return hipErrorInvalidValue;
+    // the semi-join's lists hold 31-bit positions: tables of 2^31 slots or more go without it
+    if ((int64_t)t.n_seg * kSegSlots > (int64_t)kExtraTag || t.fp_extra_cap >= (int64_t)kExtraTag) join = false;
     const int64_t jn = join ? 1 : 0;
+    uint32_t* qall = n_leaders + 2;                // leader counters, then the semi-join's flag
     const FillOp fills[6] = {{gkeys, kEmptyKey, G, 8},          {glead, 0u, G, 8},
-                             {n_leaders, 0u, 2, 4},              {qkeys, kEmptyKey, jn * G, 8},
+                             {n_leaders, 0u, 3, 4},              {qfp, kFpEmpty, jn * G, 4},
                              {qseen, 0u, jn * G, 4},             {qfilter, 0u, jn * kContFilterWords, 4}};
     hipError_t e = launch_fill_multi(fills, 6, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_insert_kernel, dim3((uint32_t)(((int64_t)R + kGroupThreads - 1) / kGroupThreads)),
                        dim3(kGroupThreads), 0, s, R, req_off, req_hashes, gkeys, glead, (uint32_t)G, slot_of);
     hipLaunchKernelGGL(group_lcp_kernel, dim3((uint32_t)(((int64_t)R + 15) / 16)), dim3(256), 0, s, R, req_off,
-                       req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qkeys, (uint32_t)G, cont_of,
-                       join ? 1 : 0);
+                       req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qfp, (uint32_t)G, qfilter,
+                       cont_of, join ? 1 : 0);
     if (join) {
-        const int64_t n_slots = t.total_buckets * kBucketKeys;
-        int64_t grid = (n_slots / 2 + kContThreads - 1) / kContThreads;
+        // a wave per segment, up to a workgroup per compute unit
+        int64_t grid = ((int64_t)t.n_seg + kContWaves - 1) / kContWaves;
         if (grid > n_cu) grid = n_cu;
-        if (grid > kMaxSlices) grid = kMaxSlices;
         if (grid < 1) grid = 1;
-        hipLaunchKernelGGL(cont_filter_kernel, dim3((uint32_t)((G + 255) / 256)), dim3(256), 0, s, qkeys, (uint32_t)G,
-                           qfilter);
-        const uint32_t cap = (uint32_t)(kContListCap / grid);
-        hipLaunchKernelGGL(cont_scan_kernel, dim3((uint32_t)grid), dim3(kContThreads), 0, s, t.keys, n_slots, qfilter,
-                           cand, cap, n_cand);
-        hipLaunchKernelGGL(cont_probe_kernel, dim3((uint32_t)grid), dim3(256), 0, s, cand, cap, n_cand, qkeys,
-                           (uint32_t)G, qseen);
+        const uint32_t xcap = (uint32_t)(t.fp_extra_cap < 0xFFFFFFFFll ? t.fp_extra_cap : 0xFFFFFFFEll);
+        hipLaunchKernelGGL(cont_scan_kernel, dim3((uint32_t)grid), dim3(kContThreads), 0, s, t.fp, t.fp_len,
+                           t.fp_inst, t.n_seg, t.fp_extra, t.fp_extra_inst, t.fp_meta, xcap, qfilter, qfp,
+                           (uint32_t)G, qseen, qinst, qall);
     }
     ProbeTables T{t.keys, t.base, t.nbuckets, t.flags};
     // leaders: persistent grids of waves over (leader, instance) pairs.  The
@@ -786,10 +941,11 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
         hipLaunchKernelGGL(prefix_leaders_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
                            leaders, n_leaders, overlap, 1);
     } else {
-        int64_t fgrid = (pairs + 63) / 64;
-        if (fgrid > (int64_t)n_cu * 16) fgrid = (int64_t)n_cu * 16;
-        hipLaunchKernelGGL(leaders_first_kernel, dim3((uint32_t)fgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
-                           leaders, n_leaders, overlap, list, n_leaders + 1);
+        // pairs <= R N bound the leader pairs; every round of a workgroup takes kLeadPairs
+        int64_t fgrid = (pairs + kLeadPairs - 1) / kLeadPairs;
+        if (fgrid > (int64_t)n_cu * 4) fgrid = (int64_t)n_cu * 4;
+        hipLaunchKernelGGL(leaders_first_kernel, dim3((uint32_t)fgrid), dim3(kLeadThreads), 0, s, T, N, req_off,
+                           req_hashes, leaders, n_leaders, overlap, list, n_leaders + 1);
         hipLaunchKernelGGL(leaders_rest_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
                            leaders, list, n_leaders + 1, overlap);
     }
@@ -803,10 +959,12 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     slices = (pairs + chunk - 1) / chunk;
     if (vec)
         hipLaunchKernelGGL(followers_resolve_kernel<true>, dim3((uint32_t)slices), dim3(kResolveThreads), 0, s, R, N,
-                           chunk, lead_of, lcp_of, cont_of, qseen, overlap, list, n_list);
+                           chunk, lead_of, lcp_of, cont_of, qseen, reinterpret_cast<const uint4*>(qinst), qall, overlap, list,
+                           n_list);
     else
         hipLaunchKernelGGL(followers_resolve_kernel<false>, dim3((uint32_t)slices), dim3(kResolveThreads), 0, s, R, N,
-                           chunk, lead_of, lcp_of, cont_of, qseen, overlap, list, n_list);
+                           chunk, lead_of, lcp_of, cont_of, qseen, reinterpret_cast<const uint4*>(qinst), qall, overlap, list,
+                           n_list);
     hipLaunchKernelGGL(followers_probe_kernel, dim3((uint32_t)slices), dim3(256), 0, s, T, N, chunk, req_off,
                        req_hashes, lcp_of, list, n_list, overlap);
     return hipGetLastError();

@@ -27,7 +27,30 @@ struct CacheTables {
     uint32_t* flags = nullptr;       // [N]
     int32_t n = 0;
     int64_t total_buckets = 0;
+    // Fingerprints (key_fp) of every cached key, written by each build for the
+    // prefix pass's semi-join: segment L's keys at fp[L * kSegBuckets *
+    // kBucketKeys], fp_len[L] of them, all of instance fp_inst[L]; the keys the
+    // overflow pass inserted in fp_extra, with their instances in
+    // fp_extra_inst, their count in fp_meta[0] (a count above fp_extra_cap
+    // means they are not all listed).
+    uint32_t* fp = nullptr;
+    uint32_t* fp_len = nullptr;      // [n_seg]
+    uint32_t* fp_inst = nullptr;     // [n_seg]
+    uint32_t* fp_extra = nullptr;    // [fp_extra_cap]
+    uint32_t* fp_extra_inst = nullptr;
+    uint32_t* fp_meta = nullptr;     // [1]
+    int64_t fp_extra_cap = 0;
+    int32_t n_seg = 0;
 };
+
+// A 32-bit fingerprint of a block hash: the high word of a multiplicative hash
+// (independent of bucket_of's), never the all-ones word, which marks an empty
+// slot of the tables that hold fingerprints.  Distinct keys may share one.
+constexpr uint32_t kFpEmpty = 0xFFFFFFFFu;
+__host__ __device__ inline uint32_t key_fp(uint64_t key) {
+    const uint32_t f = (uint32_t)((key * 0xD6E8FEB86659FD93ull) >> 32);
+    return f == kFpEmpty ? kFpEmpty - 1u : f;
+}
 
 // Bucket of `key` in a table of nb buckets: Fibonacci hashing of the whole key,
 // high 32 bits mapped onto [0, nb) by a multiply-shift.
@@ -134,7 +157,12 @@ hipError_t launch_fill_multi(const FillOp* ops, int n, hipStream_t s);
 // workspace (table_build_workspace_bytes) holds the partition and an overflow
 // queue of table_overflow_capacity(total) key indices; key indices are 32-bit.
 constexpr uint32_t kSegBuckets = 2048;
+constexpr int64_t kSegSlots = (int64_t)kSegBuckets * kBucketKeys;
 int64_t table_overflow_capacity(int64_t total);
+// Bytes of the fingerprint buffer for n_seg segments and an overflow list of
+// extra_cap keys, and its carving into t's fp fields.
+int64_t table_fp_bytes(int32_t n_seg, int64_t extra_cap);
+void carve_table_fp(CacheTables& t, void* buf, int32_t n_seg, int64_t extra_cap);
 int64_t table_build_workspace_bytes(int64_t total, int32_t n_seg, int64_t total_buckets);
 // Prefix-index maintenance (k_index.hip).  One commit of a routed batch.
 constexpr int64_t kSelChunk = 4096;           // candidates per selection chunk

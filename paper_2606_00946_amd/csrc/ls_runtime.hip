@@ -53,6 +53,8 @@ struct ls_ctx {
     char* inst_meta = nullptr;         // one block: tables.base, tables.nbuckets, inst_off_dev, seg_off_dev
     void* tws = nullptr;               // table-build workspace: key partition, overflow queue
     size_t tws_cap = 0;
+    void* fpb = nullptr;               // fingerprints of the cached keys (tables.fp and the rest)
+    size_t fpb_cap = 0;
     int64_t tables_nseg = 0;           // table segments of the loaded layout
     bool have_cache = false;
     // prefix-index maintenance: per-instance lists with recency stamps
@@ -448,7 +450,7 @@ void ls_destroy(ls_ctx* c) {
         DeviceScope dev(c->device);
         (void)hipDeviceSynchronize();
         for (void* p : {(void*)c->master, (void*)c->compute, (void*)c->mu, (void*)c->isig, (void*)c->frag16,
-                        (void*)c->frag32, (void*)c->tables.keys,
+                        (void*)c->frag32, (void*)c->tables.keys, c->fpb,
                         (void*)c->inst_meta, (void*)c->tables.flags, c->tws, c->ws, (void*)c->buf.fifo_x,
                         (void*)c->buf.fifo_y, (void*)c->buf.rep_x, (void*)c->buf.rep_y, (void*)c->buf.emb,
                         (void*)c->buf.nnd, (void*)c->buf.nni, (void*)c->buf.D, c->buf.ws, (void*)c->idx.hash,
@@ -624,6 +626,7 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     const int N = n_instances;
     const bool keep_lists = c->idx.on && (int32_t)c->idx.capacity.size() == N;
     c->idx.live = false;
+    c->have_cache = false;                 // until this load's build is queued
     std::vector<int64_t> base(N);
     std::vector<uint32_t> nb(N);
     std::vector<int32_t> seg_off(N + 1);
@@ -652,6 +655,12 @@ int ls_load_cache_state(ls_ctx* c, int32_t n_instances, const int64_t* inst_off,
     c->table_cap_buckets = (int64_t)(cap / (ls::kBucketKeys * sizeof(uint64_t)));
     rc = grow(c, &c->tws, &c->tws_cap, (size_t)ls::table_build_workspace_bytes(total, (int32_t)nseg, nbk), s);
     if (rc) return rc;
+    // fingerprints: the overflow list sized for the largest build of this
+    // layout (the index maintenance rebuilds from lists of list_entries keys)
+    const int64_t fp_extra = ls::table_overflow_capacity(list_entries > total ? list_entries : total);
+    rc = grow(c, &c->fpb, &c->fpb_cap, (size_t)ls::table_fp_bytes((int32_t)nseg, fp_extra), s);
+    if (rc) return rc;
+    ls::carve_table_fp(c->tables, c->fpb, (int32_t)nseg, fp_extra);
     // metadata: bases, bucket counts, offsets and first segments, laid out in
     // one block (as in the pinned staging buffer) so that one copy moves them
     const size_t b_base = sizeof(int64_t) * N, b_nb = sizeof(uint32_t) * N, b_off = sizeof(int64_t) * (N + 1);

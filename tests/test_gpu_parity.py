@@ -425,6 +425,99 @@ def test_table_overflow_paths(case):
     check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
 
 
+_FP_MUL = 0xD6E8FEB86659FD93
+_FP_MUL_INV = pow(_FP_MUL, -1, 1 << 64)
+
+
+def _fp_twin(key):
+    """A different key with the same 32-bit fingerprint as `key` under the
+    library's fingerprint rule (high word of key * _FP_MUL mod 2^64): the low
+    bit of the product flipped and mapped back."""
+    return (((key * _FP_MUL) % (1 << 64) ^ 1) * _FP_MUL_INV) % (1 << 64)
+
+
+def _semi_join_workload(case):
+    """Instance 0 holds a shared chain A and a pile of keys homed in its first
+    table segment, placed last in its input; requests lead with A + 3 blocks and
+    follow with A + a continuation.  run_overflow: the pile overfills the
+    segment's run, so its later keys reach the table only through the overflow
+    pass, and the continuations are taken among them.  requeue_all: a pile so
+    large that the overflow queue itself overflows.  collisions: continuations
+    whose fingerprint some other cached key shares, cached or not.
+    widely_cached: every cached continuation also on eight more instances, more
+    (continuation, instance) matches than the pair table of a batch this size
+    holds.  Instance 3 holds A and every third cached continuation."""
+    rng = np.random.default_rng({"run_overflow": 41, "requeue_all": 42, "collisions": 43, "widely_cached": 44}[case])
+    filler = lambda k: [int(x) for x in rng.integers(0, 1 << 63, k)]
+    A = filler(5)
+    cnt = 30000
+    nb = (cnt + 3) // 4
+    P = {"run_overflow": 15000, "requeue_all": 25000, "collisions": 0, "widely_cached": 15000}[case]
+    pile = set()
+    while len(pile) < P:
+        b = int(rng.integers(0, 2048))
+        pile.update(_keys_homed_at(rng, b, nb, 1))
+    pile = [k for k in pile if k not in set(A)]
+    rng.shuffle(pile)
+    conts, cached_conts = [], set()
+    if case == "collisions":
+        X = filler(60)                        # not cached; their twins are
+        Y = filler(60)                        # cached; their twins are continuations too
+        twins_x = [_fp_twin(k) for k in X]
+        big = A + twins_x + Y + filler(cnt - 5 - 120)
+        conts = X + Y + [_fp_twin(k) for k in Y]
+        cached_conts = set(Y)
+    else:
+        big = A + filler(cnt - 5 - len(pile)) + pile
+        conts = pile[-300:] + filler(40)      # late pile keys, and keys cached nowhere
+        cached_conts = set(pile[-300:])
+    held = [k for k in conts if k in cached_conts]
+    caches = [big, A[:3] + filler(200), [], A + held[::3] + filler(100)]
+    if case == "widely_cached":
+        caches += [A + held + filler(50) for _ in range(8)]
+    reqs = [(A + filler(3), 16 * 8)]          # the leader (longest of group A)
+    for k in conts:
+        reqs.append((A + [k], 16 * 6 + 5))
+    for k in conts[:50]:
+        reqs.append((A + [k] + A[:1], 16 * 7))
+    inst_off, inst_h = oracle_pins._csr(caches)
+    req_off, req_h = oracle_pins._csr([r for r, _ in reqs])
+    L = np.array([l for _, l in reqs], np.int32)
+    return inst_off, inst_h, req_off, req_h, L, cached_conts, conts
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+@pytest.mark.parametrize("case", ["run_overflow", "requeue_all", "collisions", "widely_cached"])
+def test_semi_join_fingerprints(case, mode):
+    """The semi-join over the fingerprints a table build leaves: continuations
+    cached only through the build's overflow pass, a build whose overflow queue
+    overflowed (its keys then are not all listed, so every continuation counts
+    as cached), fingerprints shared by distinct keys, and continuations cached
+    on many instances (more matches than the pair table holds).  With the join
+    on (mode 1) and off (mode 2), every overlap equals the oracle's."""
+    note(f"semi-join fingerprints {case}, join mode {mode}")
+    inst_off, inst_h, req_off, req_h, L, cached_conts, conts = _semi_join_workload(case)
+    base = workload("tiny")
+    N, R, d = len(inst_off) - 1, len(req_off) - 1, base.cfg.d
+    w = synth.Workload(cfg=synth.dataclasses.replace(base.cfg, R=R, N=N), req_off=req_off, req_hashes=req_h,
+                       prompt_len=L, req_group=np.zeros(R, np.int32), inst_off=inst_off, inst_hashes=inst_h,
+                       inst_feat=np.random.default_rng(9).uniform(0, 4, (N, d - 5)).astype(np.float32),
+                       params=base.params, mu=base.mu, inv_sigma=base.inv_sigma, upd_feats=base.upd_feats,
+                       upd_ttft=base.upd_ttft, lr=base.lr)
+    run = GpuRun(w, prefix_join=mode)
+    out = run.score()
+    want = oracle.overlap(req_off, req_h, inst_off, inst_h)
+    np.testing.assert_array_equal(out["overlap"], want)
+    # the continuations that are cached extend the run on instance 0, the others stop it at A
+    got0 = want[1:1 + len(conts), 0]
+    assert np.array_equal(got0 >= 6, np.array([k in cached_conts for k in conts]))
+    assert int(np.count_nonzero(got0 >= 6)) == len(cached_conts) > 0
+    got3 = want[1:1 + len(conts), 3]
+    assert 0 < int(np.count_nonzero(got3 >= 6)) < len(cached_conts)
+    check_scoring(w, out, np.arange(R, dtype=np.int32), run=run)
+    run.ctx.close()
+
+
 def _follower_workload(rng):
     """A shared chain A with followers that leave it at different blocks and
     continue with hashes cached on some instances, on none, or equal to the
