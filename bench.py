@@ -52,10 +52,9 @@ KIND_KERNELS = {
     "score_pairs_mfma": (["ls::score_pairs_mfma_kernel"], ["k_score_mfma.hip", "k_common.h", "ls_internal.h"]),
     "table_build": (["ls::seg_inst_kernel", "ls::part_kernel", "ls::table_segment_kernel", "ls::table_overflow_kernel"],
                     ["k_cache.hip", "ls_internal.h"]),
-    "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_filter_kernel",
-                      "ls::cont_scan_kernel", "ls::cont_probe_kernel", "ls::leaders_first_kernel",
-                      "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel", "ls::followers_resolve_kernel",
-                      "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
+    "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_scan_kernel",
+                      "ls::leaders_first_kernel", "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel",
+                      "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
     "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
     "update": (["ls::normalize_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel", "ls::layer_fwd_kernel",
                 "ls::loss_grad_kernel", "ls::loss_final_kernel", "ls::wgrad_direct_kernel",
