@@ -181,31 +181,64 @@ hipError_t launch_band_select_policy(int32_t R, int32_t N, const float* t, const
 // canonical argmin, every exact tie with it and every near-best member, and it
 // is about half as wide as the band around min (t + E), which has to allow for
 // the best pair's own error as well.
+// A wave takes kLeadRows consecutive requests, and every lane's loads for all
+// of them go out before any comparison.  VEC (N a multiple of 4, t 16-byte
+// aligned): lane l reads pairs i0 + 4l .. i0 + 4l + 3 of each chunk of 256 as
+// one 16-byte load.
+constexpr int kLeadRows = 4;
+
+template <bool VEC>
 __global__ __launch_bounds__(64 * kBandWaves) void band_lead_kernel(int32_t R, int32_t N, const float* __restrict__ t,
                                                                     int64_t* __restrict__ lead) {
+    constexpr int V = VEC ? 4 : 1, CH = 64 * V;
     const int lane = threadIdx.x & 63;
-    const int64_t r = (int64_t)blockIdx.x * kBandWaves + (threadIdx.x >> 6);
-    if (r >= R) return;
-    const float* __restrict__ tr = t + r * N;
-    float best = INFINITY;
-    int bi = N;                                   // N: no finite score seen
-    for (int i = lane; i < N; i += 64) {
-        const float v = tr[i];
-        if (finite_f(v) && (v < best || (v == best && i < bi))) {
-            best = v;
-            bi = i;
+    const int64_t r0 = ((int64_t)blockIdx.x * kBandWaves + (threadIdx.x >> 6)) * kLeadRows;
+    if (r0 >= R) return;                          // uniform over the wave
+    float best[kLeadRows];
+    int bi[kLeadRows];                            // N: no finite score seen
+#pragma unroll
+    for (int k = 0; k < kLeadRows; ++k) {
+        best[k] = INFINITY;
+        bi[k] = N;
+    }
+    for (int i0 = 0; i0 < N; i0 += CH) {
+        const int i = i0 + V * lane;
+        float v[kLeadRows][V];
+#pragma unroll
+        for (int k = 0; k < kLeadRows; ++k) {
+            const bool ok = r0 + k < R && i < N;
+            const float* __restrict__ tr = t + (r0 + k) * N;
+            if constexpr (VEC) {
+                const float4 q = ok ? *reinterpret_cast<const float4*>(tr + i) : float4{INFINITY, INFINITY, INFINITY, INFINITY};
+                v[k][0] = q.x; v[k][1] = q.y; v[k][2] = q.z; v[k][3] = q.w;
+            } else {
+                v[k][0] = ok ? tr[i] : INFINITY;
+            }
         }
+#pragma unroll
+        for (int k = 0; k < kLeadRows; ++k)
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                const float x = v[k][j];
+                if (i + j < N && finite_f(x) && (x < best[k] || (x == best[k] && i + j < bi[k]))) {
+                    best[k] = x;
+                    bi[k] = i + j;
+                }
+            }
     }
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const float ov = __shfl_xor(best, off);
-        const int oi = __shfl_xor(bi, off);
-        if (ov < best || (ov == best && oi < bi)) {
-            best = ov;
-            bi = oi;
+    for (int k = 0; k < kLeadRows; ++k) {
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const float ov = __shfl_xor(best[k], off);
+            const int oi = __shfl_xor(bi[k], off);
+            if (ov < best[k] || (ov == best[k] && oi < bi[k])) {
+                best[k] = ov;
+                bi[k] = oi;
+            }
         }
+        if (lane == 0 && r0 + k < R) lead[r0 + k] = (r0 + k) * N + (bi[k] < N ? bi[k] : 0);
     }
-    if (lane == 0) lead[r] = r * N + (bi < N ? bi : 0);
 }
 
 template <bool VEC>
@@ -318,8 +351,10 @@ __global__ __launch_bounds__(1024) void band_rest_kernel(int32_t R, int32_t N, c
 
 hipError_t launch_band_lead(int32_t R, int32_t N, const float* t, int64_t* lead, hipStream_t s) {
     if (R <= 0) return hipSuccess;
-    const dim3 grid((uint32_t)(((int64_t)R + kBandWaves - 1) / kBandWaves)), block(64 * kBandWaves);
-    hipLaunchKernelGGL(band_lead_kernel, grid, block, 0, s, R, N, t, lead);
+    const int64_t per = (int64_t)kBandWaves * kLeadRows;
+    const dim3 grid((uint32_t)(((int64_t)R + per - 1) / per)), block(64 * kBandWaves);
+    if (N % 4 == 0 && (uintptr_t)t % 16 == 0) hipLaunchKernelGGL(band_lead_kernel<true>, grid, block, 0, s, R, N, t, lead);
+    else hipLaunchKernelGGL(band_lead_kernel<false>, grid, block, 0, s, R, N, t, lead);
     return hipGetLastError();
 }
 

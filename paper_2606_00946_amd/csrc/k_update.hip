@@ -44,7 +44,8 @@ static inline uint32_t blocks_for(int64_t n, int block) { return (uint32_t)((n +
 // ---------------------------------------------------------------------------
 struct UpdWs {
     float *xn, *t, *g, *grad, *part, *loss_part;
-    float *z[3], *a[3], *dl[3];      // per hidden layer: pre-activation, activation, dL/dz
+    uint64_t* zb[3];                 // per hidden layer: ReLU mask (z > 0), one bit per sample
+    float *a[3], *dl[3];             // per hidden layer: activation, dL/dz
     int64_t bytes;
     int S;              // split-K chunks
     int64_t chunk;      // samples per chunk (multiple of 16)
@@ -105,7 +106,7 @@ static UpdWs plan_ws(const ModelDims& m, int32_t B, char* base) {
     w.xn = take((int64_t)m.d * B);
     for (int l = 0; l < 3; ++l) {
         const int64_t n = l < m.L ? (int64_t)m.h[l] * B : 0;
-        w.z[l] = l < m.L ? take(n) : nullptr;
+        w.zb[l] = l < m.L ? reinterpret_cast<uint64_t*>(take(2 * (int64_t)m.h[l] * ((B + 63) / 64))) : nullptr;
         w.a[l] = l < m.L ? take(n) : nullptr;
         w.dl[l] = l < m.L ? take(n) : nullptr;
     }
@@ -149,14 +150,24 @@ __global__ __launch_bounds__(256) void normalize_kernel(const float* __restrict_
     }
 }
 
+// ReLU masks of the hidden layers: the backward pass only needs z > 0 of each
+// pre-activation, so the forward keeps one bit per (unit, sample), bit b & 63
+// of word o * ceil(B / 64) + (b >> 6), instead of z itself (2 MB instead of
+// 67 MB per 256-unit layer at B = 65,536).  A wave of 64 consecutive samples
+// writes a whole word with one ballot.
+__host__ __device__ __forceinline__ int64_t mask_words(int32_t B) { return ((int64_t)B + 63) >> 6; }
+__device__ __forceinline__ bool mask_bit(const uint64_t* __restrict__ zb, int32_t B, int o, int64_t b) {
+    return (zb[(int64_t)o * mask_words(B) + (b >> 6)] >> (b & 63)) & 1ull;
+}
+
 // U consecutive output units of one sample: each is the fma chain from its bias
 // over the inputs in ascending order.  Inputs are fetched eight at a time ahead
 // of their multiply-adds; the order of every chain is unchanged.
 template <bool BF, bool RELU, int U>
 __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const float* __restrict__ wt,
                                           const float* __restrict__ bias, float* __restrict__ z,
-                                          float* __restrict__ a, int32_t B, int K, int O, int jb, int64_t b,
-                                          bool valid, const DropArgs& D, int layer) {
+                                          uint64_t* __restrict__ zb, float* __restrict__ a, int32_t B, int K, int O,
+                                          int jb, int64_t b, int64_t wsamp, bool valid, const DropArgs& D, int layer) {
     float acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = bias[jb + u];
@@ -178,13 +189,21 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
 #pragma unroll
         for (int u = 0; u < U; ++u) acc[u] = __builtin_fmaf(w[u], x, acc[u]);
     }
+    if (RELU && zb != nullptr) {                     // uniform; the wave's samples start at wsamp
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint64_t mk = __ballot(valid && acc[u] > 0.0f);
+            if ((threadIdx.x & 63) == 0 && wsamp < B) zb[(int64_t)(jb + u) * mask_words(B) + (wsamp >> 6)] = mk;
+        }
+    }
     if (!valid) return;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        z[(int64_t)(jb + u) * B + b] = acc[u];
         if (RELU) {
             const float h = apply_drop(D, layer, b, jb + u, relu_u(acc[u]));
             a[(int64_t)(jb + u) * B + b] = BF ? q_bf16(h) : h;
+        } else {
+            z[(int64_t)(jb + u) * B + b] = acc[u];
         }
     }
 }
@@ -195,19 +214,20 @@ __device__ __forceinline__ void fwd_units(const float* __restrict__ in, const fl
 template <bool BF, bool RELU>
 __global__ __launch_bounds__(256) void layer_fwd_kernel(const float* __restrict__ in, const float* __restrict__ wt,
                                                         const float* __restrict__ bias, float* __restrict__ z,
-                                                        float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
-                                                        int layer) {
+                                                        uint64_t* __restrict__ zb, float* __restrict__ a, int32_t B,
+                                                        int K, int O, DropArgs D, int layer) {
     int64_t bt = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t wsamp = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~63u);
     bool valid = bt < B;
     int64_t b = valid ? bt : 0;
     int jb = blockIdx.y * 32;
     const int rem = O - jb;
-    if (rem >= 32) { fwd_units<BF, RELU, 32>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); return; }
-    if (rem & 16) { fwd_units<BF, RELU, 16>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 16; }
-    if (rem & 8) { fwd_units<BF, RELU, 8>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 8; }
-    if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 4; }
-    if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 2; }
-    if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, a, B, K, O, jb, b, valid, D, layer); jb += 1; }
+    if (rem >= 32) { fwd_units<BF, RELU, 32>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); return; }
+    if (rem & 16) { fwd_units<BF, RELU, 16>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); jb += 16; }
+    if (rem & 8) { fwd_units<BF, RELU, 8>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); jb += 8; }
+    if (rem & 4) { fwd_units<BF, RELU, 4>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); jb += 4; }
+    if (rem & 2) { fwd_units<BF, RELU, 2>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); jb += 2; }
+    if (rem & 1) { fwd_units<BF, RELU, 1>(in, wt, bias, z, zb, a, B, K, O, jb, b, wsamp, valid, D, layer); jb += 1; }
 }
 
 // The same chains with the weights of the workgroup's 32 output units staged
@@ -223,33 +243,39 @@ constexpr int kDenseMaxK = 256;
 enum DenseMode { kFwdRelu = 0, kFwdHead = 1, kBackprop = 2 };
 
 // Each lane carries kDenseSpl samples (64 apart), so one LDS weight read feeds
-// kDenseSpl chains.
-constexpr int kDenseSpl = 2;
+// kDenseSpl chains, and a workgroup covers kDenseUnits output units.  The
+// weights reach the lanes as LDS broadcasts: a 16-byte read returns 1 KiB to
+// the wave, about 8 cycles of the compute unit's LDS, and feeds 4 kDenseSpl
+// fma instructions of 4 cycles on one SIMD, so four samples per lane keep the
+// LDS at half the rate the four SIMDs' fmas need (two samples saturate it).
+constexpr int kDenseSpl = 4;
+constexpr int kDenseUnits = 16;
 
 // The end of one chain of the three products above: sample b, output unit o,
 // element e = o * B + b of the feature-major outputs.
+// `on` is the ReLU mask bit of (o, b) in kBackprop.
 template <bool BF, int MODE>
-__device__ __forceinline__ void dense_store(float acc, int64_t e, int64_t b, int o, const float* __restrict__ zmask,
-                                            float* __restrict__ z, float* __restrict__ a, const DropArgs& D,
-                                            int layer) {
+__device__ __forceinline__ void dense_store(float acc, int64_t e, int64_t b, int o, bool on, float* __restrict__ z,
+                                            float* __restrict__ a, const DropArgs& D, int layer) {
     if (MODE == kFwdRelu) {
-        z[e] = acc;
         const float h = apply_drop(D, layer, b, o, relu_u(acc));
         a[e] = BF ? q_bf16(h) : h;
     } else if (MODE == kFwdHead) {
         z[e] = acc;
     } else {
-        const float v = apply_drop(D, layer, b, o, zmask[e] > 0.0f ? acc : 0.0f);
+        const float v = apply_drop(D, layer, b, o, on ? acc : 0.0f);
         z[e] = BF ? q_bf16(v) : v;
     }
 }
 
+// zb: the layer's ReLU mask, written in kFwdRelu (when not null) and read in
+// kBackprop; wsamp: the wave's first sample (slot j holds wsamp + 64 j + lane).
 template <bool BF, int MODE, int U>
 __device__ __forceinline__ void dense_units(const float* __restrict__ in, const float* __restrict__ wl,
-                                            const float* __restrict__ bias, const float* __restrict__ zmask,
+                                            const float* __restrict__ bias, uint64_t* __restrict__ zb,
                                             float* __restrict__ z, float* __restrict__ a, int32_t B, int K, int o0,
                                             int uoff, const int64_t (&b)[kDenseSpl], const bool (&valid)[kDenseSpl],
-                                            const DropArgs& D, int layer) {
+                                            int64_t wsamp, const DropArgs& D, int layer) {
     constexpr int P = kDenseSpl;
     float acc[P][U];
 #pragma unroll
@@ -267,7 +293,7 @@ __device__ __forceinline__ void dense_units(const float* __restrict__ in, const 
             for (int j = 0; j < P; ++j) x[e][j] = in[(int64_t)(k + e) * B + b[j]];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float* __restrict__ w = wl + (k + e) * 32 + uoff;
+            const float* __restrict__ w = wl + (k + e) * kDenseUnits + uoff;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const float wv = w[u];
@@ -277,7 +303,7 @@ __device__ __forceinline__ void dense_units(const float* __restrict__ in, const 
         }
     }
     for (; k < K; ++k) {
-        const float* __restrict__ w = wl + k * 32 + uoff;
+        const float* __restrict__ w = wl + k * kDenseUnits + uoff;
 #pragma unroll
         for (int j = 0; j < P; ++j) {
             const float x = in[(int64_t)k * B + b[j]];
@@ -287,24 +313,38 @@ __device__ __forceinline__ void dense_units(const float* __restrict__ in, const 
     }
 #pragma unroll
     for (int j = 0; j < P; ++j) {
+        const int64_t ws = wsamp + 64 * j;
+        if (MODE == kFwdRelu && zb != nullptr) {         // uniform
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint64_t mk = __ballot(valid[j] && acc[j][u] > 0.0f);
+                if ((threadIdx.x & 63) == 0 && ws < B) zb[(int64_t)(o0 + u) * mask_words(B) + (ws >> 6)] = mk;
+            }
+        }
         if (!valid[j]) continue;
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            dense_store<BF, MODE>(acc[j][u], (int64_t)(o0 + u) * B + b[j], b[j], o0 + u, zmask, z, a, D, layer);
+        for (int u = 0; u < U; ++u) {
+            bool on = true;
+            if (MODE == kBackprop) on = mask_bit(zb, B, o0 + u, b[j]);
+            dense_store<BF, MODE>(acc[j][u], (int64_t)(o0 + u) * B + b[j], b[j], o0 + u, on, z, a, D, layer);
+        }
     }
 }
 
+// Four waves per SIMD (at most 128 VGPRs): at the Large update's 1,024
+// workgroups every one is resident at once.
 template <bool BF, int MODE>
-__global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict__ in, const float* __restrict__ wt,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void dense_lane_kernel(
+    const float* __restrict__ in, const float* __restrict__ wt,
                                                          const float* __restrict__ bias,
-                                                         const float* __restrict__ zmask, float* __restrict__ z,
+                                                         uint64_t* __restrict__ zb, float* __restrict__ z,
                                                          float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
                                                          int layer) {
-    __shared__ __align__(16) float wl[kDenseMaxK * 32];
-    const int jb = blockIdx.y * 32;
-    const int nu = O - jb < 32 ? O - jb : 32;
-    lds_fill<8>(wl, K * 32, [&](int e) {
-        const int k = e >> 5, u = e & 31;
+    __shared__ __align__(16) float wl[kDenseMaxK * kDenseUnits];
+    const int jb = blockIdx.y * kDenseUnits;
+    const int nu = O - jb < kDenseUnits ? O - jb : kDenseUnits;
+    lds_fill<8>(wl, K * kDenseUnits, [&](int e) {
+        const int k = e / kDenseUnits, u = e % kDenseUnits;
         float v = 0.0f;
         if (u < nu) v = MODE == kBackprop ? wt[(int64_t)(jb + u) * K + k] : wt[(int64_t)k * O + jb + u];
         return v;
@@ -312,7 +352,8 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
     __syncthreads();
     // samples of this lane: block base + wave * 64 P + 64 j + lane
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t base = (int64_t)blockIdx.x * blockDim.x * kDenseSpl + (int64_t)wave * 64 * kDenseSpl + lane;
+    const int64_t wsamp = (int64_t)blockIdx.x * blockDim.x * kDenseSpl + (int64_t)wave * 64 * kDenseSpl;
+    const int64_t base = wsamp + lane;
     int64_t b[kDenseSpl];
     bool valid[kDenseSpl];
 #pragma unroll
@@ -321,16 +362,17 @@ __global__ __launch_bounds__(256) void dense_lane_kernel(const float* __restrict
         valid[j] = bt < B;
         b[j] = valid[j] ? bt : 0;
     }
-    if (nu == 32) {
-        dense_units<BF, MODE, 32>(in, wl, bias, zmask, z, a, B, K, jb, 0, b, valid, D, layer);
+    if (nu == kDenseUnits) {
+        dense_units<BF, MODE, kDenseUnits>(in, wl, bias, zb, z, a, B, K, jb, 0, b, valid, wsamp, D, layer);
         return;
     }
+    static_assert(kDenseUnits <= 32 && (kDenseUnits & (kDenseUnits - 1)) == 0, "a power of two up to 32");
     int uo = 0;
-    if (nu & 16) { dense_units<BF, MODE, 16>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 16; }
-    if (nu & 8) { dense_units<BF, MODE, 8>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 8; }
-    if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 4; }
-    if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 2; }
-    if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zmask, z, a, B, K, jb + uo, uo, b, valid, D, layer); uo += 1; }
+    if (kDenseUnits > 16 && (nu & 16)) { dense_units<BF, MODE, 16>(in, wl, bias, zb, z, a, B, K, jb + uo, uo, b, valid, wsamp, D, layer); uo += 16; }
+    if (nu & 8) { dense_units<BF, MODE, 8>(in, wl, bias, zb, z, a, B, K, jb + uo, uo, b, valid, wsamp, D, layer); uo += 8; }
+    if (nu & 4) { dense_units<BF, MODE, 4>(in, wl, bias, zb, z, a, B, K, jb + uo, uo, b, valid, wsamp, D, layer); uo += 4; }
+    if (nu & 2) { dense_units<BF, MODE, 2>(in, wl, bias, zb, z, a, B, K, jb + uo, uo, b, valid, wsamp, D, layer); uo += 2; }
+    if (nu & 1) { dense_units<BF, MODE, 1>(in, wl, bias, zb, z, a, B, K, jb + uo, uo, b, valid, wsamp, D, layer); uo += 1; }
 }
 
 // The same products for small batches, where a workgroup per 32 output units
@@ -343,7 +385,7 @@ constexpr int kDenseSmallWgs = 256;            // below this many lane-path work
 template <bool BF, int MODE>
 __global__ __launch_bounds__(256) void dense_small_kernel(const float* __restrict__ in, const float* __restrict__ wt,
                                                           const float* __restrict__ bias,
-                                                          const float* __restrict__ zmask, float* __restrict__ z,
+                                                          uint64_t* __restrict__ zb, float* __restrict__ z,
                                                           float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
                                                           int layer) {
     const int o = MODE == kFwdHead ? 0 : (int)blockIdx.x * 64 + (int)(threadIdx.x & 63);
@@ -366,11 +408,16 @@ __global__ __launch_bounds__(256) void dense_small_kernel(const float* __restric
         const float w = MODE == kBackprop ? wt[(int64_t)o * K + k] : wt[(int64_t)k * O + o];
         acc = __builtin_fmaf(w, in[(int64_t)k * B + b], acc);
     }
-    dense_store<BF, MODE>(acc, (int64_t)o * B + b, b, o, zmask, z, a, D, layer);
+    // the mask bits of a word come from different threads here: zb starts zeroed
+    if (MODE == kFwdRelu && zb != nullptr && acc > 0.0f)
+        atomicOr(reinterpret_cast<unsigned long long*>(zb + (int64_t)o * mask_words(B) + (b >> 6)), 1ull << (b & 63));
+    const bool on = MODE == kBackprop ? mask_bit(zb, B, o, b) : true;
+    dense_store<BF, MODE>(acc, (int64_t)o * B + b, b, o, on, z, a, D, layer);
 }
 
 static bool dense_small(int32_t B, int O) {
-    return (int64_t)((B + 256 * kDenseSpl - 1) / (256 * kDenseSpl)) * ((O + 31) / 32) < kDenseSmallWgs;
+    return (int64_t)((B + 256 * kDenseSpl - 1) / (256 * kDenseSpl)) * ((O + kDenseUnits - 1) / kDenseUnits) <
+           kDenseSmallWgs;
 }
 
 // ---------------------------------------------------------------------------
@@ -415,13 +462,13 @@ __global__ void loss_final_kernel(const float* __restrict__ loss_part, int nblk,
 // blockIdx.y = unit j
 template <bool BF>
 __global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
-                                                         const float* __restrict__ z, float* __restrict__ dl,
+                                                         const uint64_t* __restrict__ zb, float* __restrict__ dl,
                                                          int32_t B, DropArgs D, int layer) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int j = (int)blockIdx.y;
     if (b >= B) return;
     const int64_t t = (int64_t)j * B + b;
-    const float v = apply_drop(D, layer, b, j, z[t] > 0.0f ? g[b] * w[j] : 0.0f);
+    const float v = apply_drop(D, layer, b, j, mask_bit(zb, B, j, b) ? g[b] * w[j] : 0.0f);
     dl[t] = BF ? q_bf16(v) : v;
 }
 
@@ -779,7 +826,7 @@ __global__ __launch_bounds__(256) void rowsum_kernel(const float* __restrict__ X
 // D1[m][n] = (Z1[m][n] > 0) ? q(sum_j W[m][j] * D2[j][n]) : 0   (W [M x K], D2 [K x B])
 template <bool BF>
 __global__ __launch_bounds__(256) void backprop_hidden_kernel(const float* __restrict__ W, const float* __restrict__ D2,
-                                                              const float* __restrict__ Z1, float* __restrict__ D1,
+                                                              const uint64_t* __restrict__ Z1, float* __restrict__ D1,
                                                               int M, int K, int32_t B, DropArgs D, int layer) {
     __shared__ float As[16][64 + 4];
     __shared__ float Bs[16][64 + 4];
@@ -823,7 +870,7 @@ __global__ __launch_bounds__(256) void backprop_hidden_kernel(const float* __res
             int64_t n = n0 + tx * 4 + j;
             if (n >= B) continue;
             int64_t e = (int64_t)m * B + n;
-            const float v = apply_drop(D, layer, n, m, Z1[e] > 0.0f ? acc[i][j] : 0.0f);
+            const float v = apply_drop(D, layer, n, m, mask_bit(Z1, B, m, n) ? acc[i][j] : 0.0f);
             D1[e] = BF ? q_bf16(v) : v;
         }
     }
@@ -848,10 +895,11 @@ static hipError_t weight_grad(const float* A, const float* Bt, int M, int N, int
 }
 
 // Forward pass of B raw rows in the kernel's precision (the canonical chains),
-// keeping every layer feature-major: xn [d][B], z[l] / a[l] [h_l][B], t [B].
+// keeping every layer feature-major: xn [d][B], a[l] [h_l][B], t [B], and,
+// where zb[l] is not null, layer l's ReLU mask.
 template <bool BF>
 static void forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
-                         const float* feats, float* xn, float* const* z, float* const* a, float* t,
+                         const float* feats, float* xn, uint64_t* const* zb, float* const* a, float* t,
                          const DropArgs& D, hipStream_t s) {
     const int64_t nB = B;
     hipLaunchKernelGGL(normalize_kernel<BF>, dim3(blocks_for(nB, 64), (m.d + 63) / 64), dim3(256), 0, s, feats, mu, isig,
@@ -863,15 +911,18 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
     for (int l = 0; l < m.L; ++l) {
         const float* in = l == 0 ? xn : a[l - 1];
         const int K = m.in_of(l), O = m.h[l];
-        if (lds_w && dense_small(B, O))
+        if (lds_w && dense_small(B, O)) {
+            if (zb[l]) (void)launch_fill_u64(zb[l], 0ull, (int64_t)O * mask_words(B), s);   // bits set by atomics
             hipLaunchKernelGGL((dense_small_kernel<BF, kFwdRelu>), dim3((O + 63) / 64, blocks_for(nB, 4)), dim3(256), 0,
-                               s, in, compute + m.c_wt[l], compute + m.c_bl[l], nullptr, z[l], a[l], B, K, O, D, l);
-        else if (lds_w)
-            hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + 31) / 32), dim3(256), 0, s, in,
-                               compute + m.c_wt[l], compute + m.c_bl[l], nullptr, z[l], a[l], B, K, O, D, l);
-        else
+                               s, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
+        } else if (lds_w) {
+            hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + kDenseUnits - 1) / kDenseUnits),
+                               dim3(256), 0, s, in,
+                               compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
+        } else {
             hipLaunchKernelGGL((layer_fwd_kernel<BF, true>), dim3(sb, (O + 31) / 32), dim3(256), 0, s, in,
-                               compute + m.c_wt[l], compute + m.c_bl[l], z[l], a[l], B, K, O, D, l);
+                               compute + m.c_wt[l], compute + m.c_bl[l], nullptr, zb[l], a[l], B, K, O, D, l);
+        }
     }
     const float* last = a[m.L - 1];
     if (lds_w && dense_small(B, 1))
@@ -882,34 +933,32 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
                            compute + m.c_wt[m.L], compute + m.c_bl[m.L], nullptr, t, nullptr, B, m.hl, 1, D, m.L);
     else
         hipLaunchKernelGGL((layer_fwd_kernel<BF, false>), dim3(sb, 1), dim3(256), 0, s, last, compute + m.c_wt[m.L],
-                           compute + m.c_bl[m.L], t, nullptr, B, m.hl, 1, D, m.L);
+                           compute + m.c_bl[m.L], t, nullptr, nullptr, B, m.hl, 1, D, m.L);
 }
 
 int64_t forward_rows_floats(const ModelDims& m, int32_t B) {
-    int64_t n = (int64_t)B * (m.d + 1) + 64 * (2 * m.L + 2);
-    for (int l = 0; l < m.L; ++l) n += 2 * (int64_t)B * m.h[l];
+    int64_t n = (int64_t)B * (m.d + 1) + 64 * (m.L + 2);
+    for (int l = 0; l < m.L; ++l) n += (int64_t)B * m.h[l];
     return n;
 }
 
-// Carves xn, z[l], a[l] and t out of ws (forward_rows_floats floats).
-static float* carve_rows(const ModelDims& m, int32_t B, float* ws, float** xn, float** z, float** a) {
+// Carves xn, a[l] and t out of ws (forward_rows_floats floats); scoring keeps no masks.
+static float* carve_rows(const ModelDims& m, int32_t B, float* ws, float** xn, float** a) {
     auto take = [&](int64_t n) { float* p = ws; ws += (n + 63) & ~int64_t(63); return p; };
     *xn = take((int64_t)m.d * B);
-    for (int l = 0; l < m.L; ++l) {
-        z[l] = take((int64_t)m.h[l] * B);
-        a[l] = take((int64_t)m.h[l] * B);
-    }
+    for (int l = 0; l < m.L; ++l) a[l] = take((int64_t)m.h[l] * B);
     return take(B);
 }
 
 hipError_t launch_forward_rows(const ModelDims& m, const float* compute, const float* mu, const float* isig, int32_t B,
                                const float* feats, float* ws, float** alast_out, float** t_out, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    float *xn, *z[3] = {}, *a[3] = {};
-    float* t = carve_rows(m, B, ws, &xn, z, a);
+    float *xn, *a[3] = {};
+    uint64_t* zb[3] = {};
+    float* t = carve_rows(m, B, ws, &xn, a);
     const DropArgs none{};
-    if (m.bf16) forward_rows<true>(m, compute, mu, isig, B, feats, xn, z, a, t, none, s);
-    else forward_rows<false>(m, compute, mu, isig, B, feats, xn, z, a, t, none, s);
+    if (m.bf16) forward_rows<true>(m, compute, mu, isig, B, feats, xn, zb, a, t, none, s);
+    else forward_rows<false>(m, compute, mu, isig, B, feats, xn, zb, a, t, none, s);
     *alast_out = a[m.L - 1];
     *t_out = t;
     return hipGetLastError();
@@ -966,10 +1015,11 @@ hipError_t launch_score_generic(const ModelDims& m, const float* compute, const 
         if (g > (int64_t)n_cu * 16) g = (int64_t)n_cu * 16;
         hipLaunchKernelGGL(pair_rows_kernel, dim3((uint32_t)g), dim3(256), 0, s, p0, (int64_t)P, N, m.d, m.d_inst,
                            m.block_tokens, req_off, prompt_len, overlap, inst_feat, rows);
-        float *xn, *z[3] = {}, *a[3] = {};
-        (void)carve_rows(m, P, fw, &xn, z, a);
-        if (m.bf16) forward_rows<true>(m, compute, mu, isig, P, rows, xn, z, a, scores + p0, none, s);
-        else forward_rows<false>(m, compute, mu, isig, P, rows, xn, z, a, scores + p0, none, s);
+        float *xn, *a[3] = {};
+        uint64_t* zb[3] = {};
+        (void)carve_rows(m, P, fw, &xn, a);
+        if (m.bf16) forward_rows<true>(m, compute, mu, isig, P, rows, xn, zb, a, scores + p0, none, s);
+        else forward_rows<false>(m, compute, mu, isig, P, rows, xn, zb, a, scores + p0, none, s);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -987,7 +1037,7 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     const int64_t nB = B;
     const int L = m.L;
     // forward, saving pre-activations and activations (dropout applied)
-    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.z, w.a, w.t, D, s);
+    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.zb, w.a, w.t, D, s);
     const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
     bool lds_w = m.d <= kDenseMaxK;
     bool mf = BF && m.d <= 256;          // bf16 operands: weight and bias gradients on the matrix cores
@@ -1009,7 +1059,7 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     }
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB, 256), m.hl), dim3(256), 0, s, w.g,
-                       compute + m.c_wt[L], w.z[L - 1], w.dl[L - 1], B, D, L - 1);
+                       compute + m.c_wt[L], w.zb[L - 1], w.dl[L - 1], B, D, L - 1);
     // hidden layers, last to first
     for (int l = L - 1; l >= 0; --l) {
         const float* in = l == 0 ? w.xn : w.a[l - 1];
@@ -1026,14 +1076,15 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         const int Kp = m.h[l - 1];
         if (lds_w && dense_small(B, Kp))
             hipLaunchKernelGGL((dense_small_kernel<BF, kBackprop>), dim3((Kp + 63) / 64, blocks_for(nB, 4)), dim3(256),
-                               0, s, w.dl[l], compute + m.c_wt[l], nullptr, w.z[l - 1], w.dl[l - 1], nullptr, B, O, Kp,
+                               0, s, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp,
                                D, l - 1);
         else if (lds_w)
-            hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + 31) / 32), dim3(256), 0, s, w.dl[l],
-                               compute + m.c_wt[l], nullptr, w.z[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
+            hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + kDenseUnits - 1) / kDenseUnits),
+                               dim3(256), 0, s, w.dl[l],
+                               compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
         else
             hipLaunchKernelGGL(backprop_hidden_kernel<BF>, dim3(blocks_for(nB, 64), (Kp + 63) / 64), dim3(256), 0, s,
-                               compute + m.c_wt[l], w.dl[l], w.z[l - 1], w.dl[l - 1], Kp, O, B, D, l - 1);
+                               compute + m.c_wt[l], w.dl[l], w.zb[l - 1], w.dl[l - 1], Kp, O, B, D, l - 1);
     }
     // step and refresh the compute copy
     hipLaunchKernelGGL(sgd_kernel, dim3(blocks_for(m.n_params, 256)), dim3(256), 0, s, master, w.grad, lr,
