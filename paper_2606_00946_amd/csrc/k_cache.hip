@@ -170,12 +170,18 @@ __device__ __forceinline__ void queue_overflow(int64_t t, bool from_home, int64_
     if (pos < ovf_cap) ovf[pos] = from_home ? ~t : t;
 }
 
+// A build without a slot map keeps no input positions beside the runs: a key
+// that overflows its segment is queued by its position q in the runs instead,
+// as kRunPosTag + q, and probed from the next segment like a position entry.
+constexpr int64_t kRunPosTag = (int64_t)1 << 62;
+
 // Segment (global index) of every key of the chunk, and the key appended to
 // that segment's run.  The workgroup first finds the instances its chunk spans
 // (one parallel pass over the offsets) and copies their offsets, first
 // segments and bucket counts to LDS; a thread then takes 8 consecutive keys and
 // walks the instance boundaries from its first key.  The all-ones key sets its
 // instance's flag instead (and records its position in eidx).
+template <bool IDX>
 __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __restrict__ hashes,
                                                             const int64_t* __restrict__ inst_off,
                                                             const int32_t* __restrict__ seg_off,
@@ -277,7 +283,7 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
             if (pos < runcap[u]) {
                 const int64_t q = run0[u] + pos;
                 part_key[q] = key[u];
-                part_idx[q] = (uint32_t)t;
+                if (IDX) part_idx[q] = (uint32_t)t;
             } else {
                 queue_overflow(t, true, ovf, ovf_count, ovf_cap);
             }
@@ -299,7 +305,7 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
         if (pos < runcap[u]) {
             const int64_t q = run0[u] + pos;
             part_key[q] = key[u];
-            part_idx[q] = (uint32_t)(t0 + u);
+            if (IDX) part_idx[q] = (uint32_t)(t0 + u);
         } else {
             queue_overflow(t0 + u, true, ovf, ovf_count, ovf_cap);
         }
@@ -349,7 +355,12 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
         const uint32_t lb = bucket_of(key, nb) - b0;
         const int32_t ls = segment_place(seg, fill, lb, nbl, key);
         if (ls < 0) {
-            queue_overflow(part_idx[q], false, ovf, ovf_count, ovf_cap);
+            if (entry_of) {
+                queue_overflow(part_idx[q], false, ovf, ovf_count, ovf_cap);
+            } else {
+                const uint32_t pos = atomicAdd(ovf_count, 1u);
+                if (pos < ovf_cap) ovf[pos] = kRunPosTag + q;
+            }
         } else if (entry_of) {
             entry_of[(base[i] + b0) * kBucketKeys + ls] = part_idx[q];
         }
@@ -375,6 +386,7 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
 __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t* __restrict__ base,
                                       const uint32_t* __restrict__ nbuckets, const int64_t* __restrict__ inst_off,
                                       int32_t n_inst, const uint64_t* __restrict__ hashes, int64_t total,
+                                      const uint64_t* __restrict__ part_key,
                                       const int64_t* __restrict__ ovf, const uint32_t* __restrict__ ovf_count,
                                       uint32_t ovf_cap, uint32_t* __restrict__ entry_of, uint32_t* __restrict__ fp_extra,
                                       uint32_t* __restrict__ fp_extra_inst, uint32_t fp_extra_cap,
@@ -388,10 +400,22 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < count; j += stride) {
         const int64_t entry = queued ? ovf[j] : j;
-        const bool from_home = entry < 0;                 // past its segment's run: probe from home
-        const int64_t t = from_home ? ~entry : entry;
-        const uint64_t key = hashes[t];
-        const int32_t i = owner_of(inst_off, n_inst, t);
+        uint64_t key;
+        int32_t i;
+        int64_t t = -1;                                   // input position, when the entry has one
+        bool next_segment;
+        if (queued && entry >= kRunPosTag) {              // overflowed its segment, queued by run position
+            const int64_t q = entry - kRunPosTag;
+            key = part_key[q];
+            i = owner_of(base, n_inst, q / kBucketKeys);  // base[i]: instance i's first bucket, increasing
+            next_segment = true;
+        } else {
+            const bool from_home = entry < 0;             // past its segment's run: probe from home
+            t = from_home ? ~entry : entry;
+            key = hashes[t];
+            i = owner_of(inst_off, n_inst, t);
+            next_segment = queued && !from_home;
+        }
         if (queued && j < (int64_t)fp_extra_cap) {
             fp_extra[j] = key == kEmptyKey ? kFpEmpty : key_fp(key);
             fp_extra_inst[j] = (uint32_t)i;
@@ -399,12 +423,12 @@ __global__ void table_overflow_kernel(uint64_t* __restrict__ keys, const int64_t
         if (key == kEmptyKey) continue;
         const uint32_t nb = nbuckets[i];
         uint32_t b = bucket_of(key, nb);
-        if (queued && !from_home) {
+        if (next_segment) {
             b = (b / kSegBuckets + 1) * kSegBuckets;
             if (b >= nb) b = 0;
         }
         const int64_t q = global_insert(keys + base[i] * kBucketKeys, nb, b, key);
-        if (entry_of && q >= 0) entry_of[base[i] * kBucketKeys + q] = (uint32_t)t;
+        if (entry_of && q >= 0 && t >= 0) entry_of[base[i] * kBucketKeys + q] = (uint32_t)t;
     }
 }
 
@@ -485,9 +509,15 @@ hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, con
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t chunks = (uint32_t)((total + kPartChunk - 1) / kPartChunk);
     if (chunks > 0) {
-        hipLaunchKernelGGL(part_kernel, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off, t.nbuckets,
-                           t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx, w.ovf,
-                           w.ovf_count, cap);
+        // input positions beside the runs only for a slot map
+        if (entry_of)
+            hipLaunchKernelGGL(part_kernel<true>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
+                               t.nbuckets, t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx,
+                               w.ovf, w.ovf_count, cap);
+        else
+            hipLaunchKernelGGL(part_kernel<false>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
+                               t.nbuckets, t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx,
+                               w.ovf, w.ovf_count, cap);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (n_seg > 0) {
@@ -497,7 +527,8 @@ hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, con
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(table_overflow_kernel, dim3((uint32_t)(4 * n_cu)), dim3(256), 0, s, t.keys, t.base,
-                       t.nbuckets, inst_off, n_inst, hashes, total, w.ovf, w.ovf_count, cap, entry_of, t.fp_extra,
+                       t.nbuckets, inst_off, n_inst, hashes, total, w.part_key, w.ovf, w.ovf_count, cap, entry_of,
+                       t.fp_extra,
                        t.fp_extra_inst, (uint32_t)(t.fp_extra_cap < 0xFFFFFFFFll ? t.fp_extra_cap : 0xFFFFFFFEll), t.fp_meta);
     return hipGetLastError();
 }
