@@ -234,6 +234,19 @@ int ls_score_batch_noalloc(ls_ctx* ctx, int32_t R, int32_t N,
 int ls_set_exact_scores(ls_ctx* ctx, int enable);
 
 /*
+ * Which kernels run the canonical fp32 chains of ls_update (the forward layers
+ * and the hidden layers' backpropagated gradients, Section 4.3.2) and of the
+ * layer-by-layer scorer of models other than two hidden layers (Section 4.1).
+ * mode 0 (the default): on the matrix cores wherever a call's batch fills the
+ * device.  There v_mfma_f32_32x32x1_2b_f32 takes one input k per instruction
+ * and rounds each multiply-add once, as fmaf does, so every chain keeps its
+ * order and its bits.  mode 1: on the vector ALUs only.  The two give
+ * bit-identical results; the switch exists to compare them.  LS_ERR_INVALID
+ * for another mode.  Takes effect for later calls.
+ */
+int ls_set_chain_kernels(ls_ctx* ctx, int mode);
+
+/*
  * Validation aid for the matrix-core path of an LS_BF16 context (Section 4.1,
  * the batched forward of Alg. 4): for every pair of the batch, the fast score t
  * before any rescoring and its error scale err = 2^-7 (sum_j |w3_j| h2_j + |b3|)

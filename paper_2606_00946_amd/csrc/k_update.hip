@@ -10,6 +10,7 @@
 // bitwise reproducible.  In bf16 mode every multiplication operand (weights,
 // layer inputs, each layer's output gradient) is a bf16 value; sums are fp32.
 #include <algorithm>
+#include <type_traits>
 
 #include "k_policy.h"
 
@@ -418,6 +419,314 @@ __global__ __launch_bounds__(256) void dense_small_kernel(const float* __restric
 static bool dense_small(int32_t B, int O) {
     return (int64_t)((B + 256 * kDenseSpl - 1) / (256 * kDenseSpl)) * ((O + kDenseUnits - 1) / kDenseUnits) <
            kDenseSmallWgs;
+}
+
+// The same chains on the matrix cores.  v_mfma_f32_32x32x1_2b_f32 gives each
+// of its outputs one multiply-add rounded once, as fmaf does (denormals kept),
+// so an accumulator that starts at the bias and takes the inputs k = 0, 1, ...
+// one instruction each holds the chain's value bit for bit.  A wave owns 64
+// samples (block 0: the first 32, block 1: the next 32) and kMfTiles tiles of
+// 32 output units; per input k its B operand is row k of the feature-major
+// input, one coalesced 256-byte load, and each tile's A operand is the unit
+// slice's weight column k.  The accumulator's rows are units: register i of
+// lane l holds unit 8 (i % 16 / 4) + 4 (l / 32) + i % 4 of its tile, sample
+// 32 (i / 16) + l % 32 of the wave.
+//
+// The slice sits in LDS unit-major, wl[u][k] with a row stride of mf_ldk(K)
+// floats (K rounded up to 4, plus 4 when that is a multiple of 8), so that one
+// 16-byte read gives a lane its unit's weights for four consecutive k and the
+// 32 lanes of a tile read without bank conflicts.  A group of kMfPre inputs
+// takes all of its A operands in one batch of reads issued before its first
+// multiply-add, and its B operands one group ahead.
+constexpr int kMfTiles = 4;
+constexpr int kMfUnits = 32 * kMfTiles;       // output units per workgroup
+constexpr int kMfWaves = 8;                   // 64 samples each
+constexpr int kMfPre = 8;                     // inputs per group
+constexpr int kMfMaxLdk = kDenseMaxK + 4;
+
+__host__ __device__ constexpr int mf_ldk(int K) {
+    return ((K + 3) & ~3) + ((((K + 3) >> 2) & 1) ? 0 : 4);
+}
+
+typedef float f32x32_t __attribute__((ext_vector_type(32)));
+
+// DROP: dropout on (the stores then draw each unit's mask).  A wave whose 64
+// samples and 128 units all exist (every wave but the edges) takes the
+// epilogue without per-element tests: row bases are scalar, lane offsets 32-bit,
+// and the ReLU mask words of its 128 units are gathered into two registers per
+// lane and written with two stores.
+template <bool BF, int MODE, bool DROP>
+__global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* __restrict__ in,
+                                                                   const float* __restrict__ wt,
+                                                                   const float* __restrict__ bias,
+                                                                   uint64_t* __restrict__ zb, float* __restrict__ z,
+                                                                   float* __restrict__ a, int32_t B, int K, int O,
+                                                                   DropArgs D, int layer) {
+    static_assert(MODE == kFwdRelu || MODE == kBackprop, "hidden layers only");
+    __shared__ __align__(16) float wl[kMfUnits * kMfMaxLdk];
+    __shared__ __align__(16) float bl[kMfUnits];
+    const int jb = blockIdx.y * kMfUnits;
+    const int nu = O - jb < kMfUnits ? O - jb : kMfUnits;
+    const int ldk = mf_ldk(K);
+    const int tid = (int)threadIdx.x, T_ = (int)blockDim.x;
+    // the slice, zero past O and past K
+    if ((MODE == kBackprop ? (K & 3) == 0 : (O & 3) == 0) && (reinterpret_cast<uintptr_t>(wt) & 15) == 0) {
+        // 16-byte loads, all of a thread's in flight at once.  Gradients (wt is
+        // [units][K]): a load is four k of one unit, written as one 16-byte LDS
+        // store.  Forward (wt is [K][O]): a load is four units of one k; a wave's
+        // 64 loads cover 16 units x 16 k (64-byte runs of wt), so that its four
+        // 4-byte LDS stores each hit 64 distinct banks (row stride = 4 mod 64).
+        constexpr int kFillMax = (kMfUnits * kMfMaxLdk / 4 + 64 * kMfWaves - 1) / (64 * kMfWaves) + 1;
+        const int q4 = ldk >> 2;
+        const int n4 = MODE == kBackprop ? kMfUnits * q4 : (kMfUnits / 16) * ((ldk + 15) >> 4) * 64;
+        float4 v[kFillMax];
+        bool ok[kFillMax];            // zeroed at the LDS write: no register write behind a pending load
+        auto where = [&](int e, int& u, int& k) {
+            if (MODE == kBackprop) {
+                u = e / q4;
+                k = 4 * (e - u * q4);
+            } else {
+                const int tile = e >> 6, l = e & 63;
+                k = 16 * (tile / (kMfUnits / 16)) + (l >> 2);
+                u = 16 * (tile % (kMfUnits / 16)) + 4 * (l & 3);
+            }
+        };
+#pragma unroll
+        for (int j = 0; j < kFillMax; ++j) {
+            const int e = tid + j * T_ < n4 ? tid + j * T_ : n4 - 1;
+            int u, k;
+            where(e, u, k);
+            // clamped into the slice: a whole float4 of units (forward) or of k (gradients)
+            const int uc = u < nu ? u : (MODE == kBackprop ? nu - 1 : nu - 4);
+            const int kc = k < K ? k : (MODE == kBackprop ? K - 4 : K - 1);
+            v[j] = MODE == kBackprop ? *reinterpret_cast<const float4*>(wt + (int64_t)(jb + uc) * K + kc)
+                                     : *reinterpret_cast<const float4*>(wt + (int64_t)kc * O + jb + uc);
+            ok[j] = u < nu && k < K;
+        }
+#pragma unroll
+        for (int j = 0; j < kFillMax; ++j) {
+            const int e = tid + j * T_;
+            if (e >= n4) break;
+            int u, k;
+            where(e, u, k);
+            if (k >= ldk) continue;
+            const float4 q = ok[j] ? v[j] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (MODE == kBackprop) {
+                *reinterpret_cast<float4*>(wl + u * ldk + k) = q;
+            } else {
+                wl[(u + 0) * ldk + k] = q.x;
+                wl[(u + 1) * ldk + k] = q.y;
+                wl[(u + 2) * ldk + k] = q.z;
+                wl[(u + 3) * ldk + k] = q.w;
+            }
+        }
+    } else {
+        const int n = kMfUnits * ldk;
+        for (int e0 = tid; e0 < n; e0 += 16 * T_) {
+            float v[16];
+            bool ok[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int e = e0 + j * T_ < n ? e0 + j * T_ : n - 1;
+                int k, u;
+                if (MODE == kBackprop) {
+                    u = e / ldk;
+                    k = e - u * ldk;
+                } else {
+                    k = e / kMfUnits;
+                    u = e - k * kMfUnits;
+                }
+                const int uc = u < nu ? u : nu - 1, kc = k < K ? k : K - 1;
+                v[j] = MODE == kBackprop ? wt[(int64_t)(jb + uc) * K + kc] : wt[(int64_t)kc * O + jb + uc];
+                ok[j] = u < nu && k < K;
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int e = e0 + j * T_;
+                if (e < n) {
+                    int k, u;
+                    if (MODE == kBackprop) {
+                        u = e / ldk;
+                        k = e - u * ldk;
+                    } else {
+                        k = e / kMfUnits;
+                        u = e - k * kMfUnits;
+                    }
+                    wl[u * ldk + k] = ok[j] ? v[j] : 0.0f;
+                }
+            }
+        }
+    }
+    if (tid < kMfUnits) bl[tid] = (MODE == kBackprop || tid >= nu) ? 0.0f : bias[jb + tid];
+    __syncthreads();
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t b0 = (int64_t)blockIdx.x * (64 * kMfWaves) + 64 * wave;
+    if (b0 >= B) return;
+    const int64_t bl_ = b0 + lane;
+    const float* __restrict__ src = in + (bl_ < B ? bl_ : (int64_t)B - 1);   // lanes past B read a valid row
+    const int hi = lane >> 5, col = lane & 31;
+    // accumulators start at the bias (zero for the gradients and for units past O)
+    f32x32_t acc[kMfTiles];
+#pragma unroll
+    for (int t = 0; t < kMfTiles; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float4 q = *reinterpret_cast<const float4*>(bl + 32 * t + 8 * r + 4 * hi);
+            acc[t][4 * r + 0] = acc[t][16 + 4 * r + 0] = q.x;
+            acc[t][4 * r + 1] = acc[t][16 + 4 * r + 1] = q.y;
+            acc[t][4 * r + 2] = acc[t][16 + 4 * r + 2] = q.z;
+            acc[t][4 * r + 3] = acc[t][16 + 4 * r + 3] = q.w;
+        }
+    // tile t's unit for this lane: row (32 t + col) of the slice
+    const float* __restrict__ wrow = wl + col * ldk;
+    // inputs k0 .. k0 + kMfPre - 1 (rows past K clamped to K - 1: always in bounds)
+    auto load = [&](float (&x)[kMfPre], int k0) {
+#pragma unroll
+        for (int e = 0; e < kMfPre; ++e) {
+            const int k = k0 + e < K ? k0 + e : K - 1;
+            x[e] = src[(int64_t)k * B];
+        }
+    };
+    // one group of inputs; FULL: all kMfPre of them are below K (no per-step test,
+    // so the reads of the A operands stay ahead of the multiply-adds)
+    auto step = [&](const float (&x)[kMfPre], int k0, auto full) {
+        float4 w[kMfPre / 4][kMfTiles];
+#pragma unroll
+        for (int g = 0; g < kMfPre / 4; ++g)
+#pragma unroll
+            for (int t = 0; t < kMfTiles; ++t) {
+                const int kk = k0 + 4 * g < ldk - 3 ? k0 + 4 * g : ldk - 4;
+                w[g][t] = *reinterpret_cast<const float4*>(wrow + 32 * t * ldk + kk);
+            }
+#pragma unroll
+        for (int e = 0; e < kMfPre; ++e) {
+            if (!decltype(full)::value && k0 + e >= K) break;
+#pragma unroll
+            for (int t = 0; t < kMfTiles; ++t) {
+                const float4 q = w[e >> 2][t];
+                const float wv = (e & 3) == 0 ? q.x : (e & 3) == 1 ? q.y : (e & 3) == 2 ? q.z : q.w;
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x1f32(wv, x[e], acc[t], 0, 0, 0);
+            }
+        }
+    };
+    using Full = std::integral_constant<bool, true>;
+    using Tail = std::integral_constant<bool, false>;
+    float xa[kMfPre], xb[kMfPre];
+    load(xa, 0);
+    int k0 = 0;
+    for (; k0 + 2 * kMfPre <= K; k0 += 2 * kMfPre) {
+        load(xb, k0 + kMfPre);
+        step(xa, k0, Full{});
+        load(xa, k0 + 2 * kMfPre);
+        step(xb, k0 + kMfPre, Full{});
+    }
+    if (k0 < K) {
+        load(xb, k0 + kMfPre);
+        step(xa, k0, Tail{});
+        if (k0 + kMfPre < K) step(xb, k0 + kMfPre, Tail{});
+    }
+    // epilogue: masks, ReLU or masked gradient, dropout, bf16 rounding.  Register
+    // i of tile t holds unit u = 32 t + 8 (i % 16 / 4) + 4 hi + i % 4 of the slice
+    // for sample b0 + 32 (i / 16) + col.
+    const int mw = (int)mask_words(B);
+    float* __restrict__ outp = MODE == kFwdRelu ? a : z;
+    if (b0 + 64 <= B && nu == kMfUnits) {
+        // mask words of this wave's sample word for units lane and 64 + lane
+        uint32_t wlo[2] = {0u, 0u}, whi[2] = {0u, 0u};
+        if (MODE == kBackprop) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint64_t w = zb[(int64_t)(jb + 64 * h + lane) * mw + (b0 >> 6)];
+                wlo[h] = (uint32_t)w;
+                whi[h] = (uint32_t)(w >> 32);
+            }
+        }
+        const uint32_t loff = (uint32_t)(4 * hi) * (uint32_t)B + (uint32_t)col;   // lane offset from a row base
+#pragma unroll
+        for (int t = 0; t < kMfTiles; ++t)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int u0 = 32 * t + 8 * (i >> 2) + (i & 3);          // lanes 0-31: u0, lanes 32-63: u0 + 4
+                float* __restrict__ row = outp + (int64_t)(jb + u0) * B + b0;
+                float c0 = acc[t][i], c1 = acc[t][i + 16];
+                if (MODE == kFwdRelu) {
+                    if (zb != nullptr) {     // uniform
+                        const uint64_t m0 = __ballot(c0 > 0.0f), m1 = __ballot(c1 > 0.0f);
+                        const int h = u0 >> 6, ln = u0 & 63;
+                        if (lane == ln) {
+                            wlo[h] = (uint32_t)m0;
+                            whi[h] = (uint32_t)m1;
+                        }
+                        if (lane == ln + 4) {
+                            wlo[h] = (uint32_t)(m0 >> 32);
+                            whi[h] = (uint32_t)(m1 >> 32);
+                        }
+                    }
+                    c0 = relu_u(c0);
+                    c1 = relu_u(c1);
+                } else {
+                    // this lane's unit's word: lane u0 (+ 4) of the gathered words
+                    const int h = u0 >> 6, ln = (u0 & 63) + 4 * hi;
+                    const uint32_t lo = __builtin_amdgcn_ds_bpermute(ln << 2, (int)wlo[h]);
+                    const uint32_t hw = __builtin_amdgcn_ds_bpermute(ln << 2, (int)whi[h]);
+                    if (!((lo >> col) & 1u)) c0 = 0.0f;
+                    if (!((hw >> col) & 1u)) c1 = 0.0f;
+                }
+                if (DROP) {
+                    const int o = jb + u0 + 4 * hi;
+                    c0 = apply_drop(D, layer, b0 + col, o, c0);
+                    c1 = apply_drop(D, layer, b0 + 32 + col, o, c1);
+                }
+                row[loff] = BF ? q_bf16(c0) : c0;
+                row[loff + 32] = BF ? q_bf16(c1) : c1;
+            }
+        if (MODE == kFwdRelu && zb != nullptr) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                zb[(int64_t)(jb + 64 * h + lane) * mw + (b0 >> 6)] = ((uint64_t)whi[h] << 32) | wlo[h];
+        }
+        return;
+    }
+    // edge waves: per-element tests
+    const int64_t s0 = b0 + col, s1 = b0 + 32 + col;
+    const bool v0 = s0 < B, v1 = s1 < B;
+#pragma unroll
+    for (int t = 0; t < kMfTiles; ++t) {
+        const f32x32_t& c = acc[t];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int o = jb + 32 * t + 8 * (i >> 2) + 4 * hi + (i & 3);
+            const float c0 = c[i], c1 = c[i + 16];
+            bool on0 = true, on1 = true;
+            if (MODE == kFwdRelu) {
+                if (zb != nullptr) {     // uniform
+                    const uint64_t m0 = __ballot(v0 && c0 > 0.0f), m1 = __ballot(v1 && c1 > 0.0f);
+                    // lanes 0-31 hold unit o of both blocks, lanes 32-63 unit o + 4
+                    const uint64_t word = hi ? ((m0 >> 32) | (m1 & 0xFFFFFFFF00000000ull))
+                                             : ((m0 & 0xFFFFFFFFull) | (m1 << 32));
+                    if (col == 0 && o < O) zb[(int64_t)o * mw + (b0 >> 6)] = word;
+                }
+            } else if (o < O) {
+                const uint64_t word = zb[(int64_t)o * mw + (b0 >> 6)];
+                on0 = (word >> col) & 1ull;
+                on1 = (word >> (32 + col)) & 1ull;
+            }
+            if (o < O) {
+                if (v0) dense_store<BF, MODE>(c0, (int64_t)o * B + s0, s0, o, on0, z, a, D, layer);
+                if (v1) dense_store<BF, MODE>(c1, (int64_t)o * B + s1, s1, o, on1, z, a, D, layer);
+            }
+        }
+    }
+}
+
+// The matrix-core chains pay off once the batch fills the chip: a workgroup
+// per 512 samples and 128 output units.
+constexpr int kMfMinWgs = 128;
+
+static bool dense_mfma(const ModelDims& m, int32_t B, int O) {
+    return m.mfma_chains && B <= (1 << 28) &&
+           (int64_t)((B + 64 * kMfWaves - 1) / (64 * kMfWaves)) * ((O + kMfUnits - 1) / kMfUnits) >= kMfMinWgs;
 }
 
 // ---------------------------------------------------------------------------
@@ -915,6 +1224,14 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
             if (zb[l]) (void)launch_fill_u64(zb[l], 0ull, (int64_t)O * mask_words(B), s);   // bits set by atomics
             hipLaunchKernelGGL((dense_small_kernel<BF, kFwdRelu>), dim3((O + 63) / 64, blocks_for(nB, 4)), dim3(256), 0,
                                s, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
+        } else if (lds_w && dense_mfma(m, B, O)) {
+            const dim3 grid(blocks_for(nB, 64 * kMfWaves), (O + kMfUnits - 1) / kMfUnits);
+            if (D.thr53)
+                hipLaunchKernelGGL((dense_mfma_kernel<BF, kFwdRelu, true>), grid, dim3(64 * kMfWaves), 0, s, in,
+                                   compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
+            else
+                hipLaunchKernelGGL((dense_mfma_kernel<BF, kFwdRelu, false>), grid, dim3(64 * kMfWaves), 0, s, in,
+                                   compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
         } else if (lds_w) {
             hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + kDenseUnits - 1) / kDenseUnits),
                                dim3(256), 0, s, in,
@@ -1078,6 +1395,15 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
             hipLaunchKernelGGL((dense_small_kernel<BF, kBackprop>), dim3((Kp + 63) / 64, blocks_for(nB, 4)), dim3(256),
                                0, s, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp,
                                D, l - 1);
+        else if (lds_w && dense_mfma(m, B, Kp)) {
+            const dim3 grid(blocks_for(nB, 64 * kMfWaves), (Kp + kMfUnits - 1) / kMfUnits);
+            if (D.thr53)
+                hipLaunchKernelGGL((dense_mfma_kernel<BF, kBackprop, true>), grid, dim3(64 * kMfWaves), 0, s, w.dl[l],
+                                   compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
+            else
+                hipLaunchKernelGGL((dense_mfma_kernel<BF, kBackprop, false>), grid, dim3(64 * kMfWaves), 0, s, w.dl[l],
+                                   compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
+        }
         else if (lds_w)
             hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + kDenseUnits - 1) / kDenseUnits),
                                dim3(256), 0, s, w.dl[l],

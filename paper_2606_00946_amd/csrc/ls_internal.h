@@ -71,6 +71,7 @@ struct ModelDims {
     int h[3] = {0, 0, 0};                     // hidden widths
     int hl = 0;                               // width of the last hidden layer
     bool bf16 = false;
+    bool mfma_chains = true;                  // canonical chains on the matrix cores where the batch fills the device
     int block_tokens = 16;
     // master offsets (floats), the ABI packing: per layer W [out x in] then b [out]
     int64_t m_w1 = 0, m_b1 = 0, m_w2 = 0, m_b2 = 0, m_w3 = 0, m_b3 = 0, n_params = 0;   // two-layer names

@@ -1017,6 +1017,14 @@ int ls_set_exact_scores(ls_ctx* c, int enable) {
     return LS_OK;
 }
 
+int ls_set_chain_kernels(ls_ctx* c, int mode) {
+    if (!c) return LS_ERR_INVALID;
+    c->err.clear();
+    if (mode != 0 && mode != 1) return fail(c, LS_ERR_INVALID, "chain kernel mode must be 0 or 1");
+    c->dims.mfma_chains = mode == 0;
+    return LS_OK;
+}
+
 int ls_set_cu_limit(ls_ctx* c, int n) {
     if (!c) return LS_ERR_INVALID;
     c->err.clear();

@@ -104,12 +104,14 @@ def library():
         lib.ls_fast_scores.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P]
         lib.ls_score_batch_noalloc.argtypes = [P, i32, i32, P, P, P, P, P, P, P, P, P, P]
         lib.ls_set_cu_limit.argtypes = [P, ctypes.c_int]
+        lib.ls_set_chain_kernels.argtypes = [P, ctypes.c_int]
         for f in (lib.ls_create, lib.ls_set_model, lib.ls_get_model, lib.ls_load_cache_state, lib.ls_score_batch,
                   lib.ls_update, lib.ls_profile_enable, lib.ls_profile_read, lib.ls_set_exact_scores,
                   lib.ls_set_prefix_join, lib.ls_route_batch, lib.ls_set_prefix_closed, lib.ls_buffer_init,
                   lib.ls_buffer_push, lib.ls_buffer_state, lib.ls_buffer_read, lib.ls_train_round,
                   lib.ls_set_cache_capacity, lib.ls_commit_routes, lib.ls_read_cache_state, lib.ls_set_dropout,
                   lib.ls_set_shadow_training, lib.ls_swap_model, lib.ls_fast_scores, lib.ls_set_cu_limit,
+                  lib.ls_set_chain_kernels,
                   lib.ls_score_batch_noalloc):
             f.restype = ctypes.c_int
         _lib = lib
@@ -398,6 +400,9 @@ class Context:
         lo = _dev(loss_out, "loss_out", (torch.float32,), 1, allow_none=True)
         go = _dev(grad_out, "grad_out", (torch.float32,), self.n_params, allow_none=True)
         return self._check("ls_update", self.lib.ls_update(self.h, B, *args, float(lr), lo, go, _stream(stream)))
+
+    def ls_set_chain_kernels(self, mode):
+        return self._check("ls_set_chain_kernels", self.lib.ls_set_chain_kernels(self.h, int(mode)))
 
     def ls_set_exact_scores(self, enable=True):
         return self._check("ls_set_exact_scores", self.lib.ls_set_exact_scores(self.h, 1 if enable else 0))

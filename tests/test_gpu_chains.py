@@ -1,0 +1,118 @@
+"""The canonical fp32 chains on the matrix cores against the same chains on the
+vector ALUs, bit for bit, through the C ABI.
+
+The chains are the update's forward layers and hidden-layer gradients (Section
+4.3.2) and the layer-by-layer scorer of models other than two hidden layers
+(Section 4.1). ls_set_chain_kernels(0) runs them as v_mfma_f32_32x32x1_2b_f32
+steps, one input k per instruction, wherever a call's batch fills the device.
+ls_set_chain_kernels(1) keeps them on the vector ALUs. The instruction rounds
+each multiply-add once, as fmaf does, and both kernels take the inputs in the
+chain's order, so the loss, every gradient and every updated weight must be
+equal bit for bit. Batches are chosen so that the matrix-core kernel runs:
+full and ragged 512-sample workgroups, output widths of 64, 128 and 256 units,
+bf16 and fp32 models, and dropout. The scores of the layer-by-layer path are
+also compared with the oracle's chains, bit for bit."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_helpers import GpuRun, note
+from paper_2606_00946_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _workload(base, B=None, hidden=None, dtype=None, R=64, N=16):
+    """The base config's model and update rows at batch B, with a small scoring
+    batch and cache (only the update's rows and the model matter here)."""
+    cfg = synth.CONFIGS[base]
+    kw = {"R": R, "N": N, "capacity": tuple(2000 for _ in cfg.capacity), "warmup_requests": 0}
+    if B is not None:
+        kw["update_batch"] = B
+    if hidden is not None:
+        kw["hidden"] = tuple(hidden)
+    if dtype is not None:
+        kw["dtype"] = dtype
+    return synth.generate(dataclasses.replace(cfg, **kw))
+
+
+def _two_updates(w, mode, dropout=None):
+    """Two consecutive updates on the chain kernels of `mode`."""
+    run = GpuRun(w)
+    run.ctx.ls_set_chain_kernels(mode)
+    if dropout is not None:
+        run.ctx.ls_set_dropout(*dropout)
+    out = [run.update(), run.update()]
+    run.ctx.close()
+    return out
+
+
+def _assert_same(a, b, what):
+    for step, (x, y) in enumerate(zip(a, b)):
+        assert np.float32(x["loss"]).view(np.uint32) == np.float32(y["loss"]).view(np.uint32), (what, step, "loss")
+        gx, gy = x["grad"].view(np.uint32), y["grad"].view(np.uint32)
+        bad = np.flatnonzero(gx != gy)
+        assert bad.size == 0, f"{what} step {step}: {bad.size} gradient elements differ, first at {bad[:5]}"
+        px, py = x["params"].view(np.uint32), y["params"].view(np.uint32)
+        assert np.array_equal(px, py), f"{what} step {step}: updated weights differ"
+
+
+# (base config, batch, hidden widths, dtype, dropout)
+UPDATE_CASES = [
+    ("large_batch", None, None, None, None),                       # 65,536 x 64-256-256 bf16
+    ("large_batch", 33001, None, None, None),                      # ragged last workgroup and wave
+    ("large_batch", 40000, None, None, (0.1, 0xC0FFEE)),           # dropout in the epilogue
+    ("heterogeneous", 40001, None, None, None),                    # fp32 48-256-256
+    ("homogeneous", 66000, None, None, None),                      # fp32 32-128-128
+    ("homogeneous", 66000, (128, 128, 128), "fp32", None),         # the paper's 3 x 128 model
+    ("homogeneous", 66000, (128, 128, 128), "bf16", (0.1, 7)),
+    ("homogeneous", 70000, (64,), "bf16", None),                   # half-filled unit tiles
+    ("tiny", None, None, None, None),                              # the five configs at their own batch
+    ("homogeneous", None, None, None, None),
+    ("heterogeneous", None, None, None, None),
+    ("long_context", None, None, None, None),
+]
+
+
+@pytest.mark.parametrize("base,B,hidden,dtype,dropout", UPDATE_CASES)
+def test_update_chain_kernels_bitwise(base, B, hidden, dtype, dropout):
+    w = _workload(base, B, hidden, dtype)
+    note(f"update chains {base} B={w.cfg.update_batch} hidden={w.cfg.hidden} {w.cfg.dtype} dropout={dropout}")
+    mf = _two_updates(w, 0, dropout)
+    vec = _two_updates(w, 1, dropout)
+    _assert_same(mf, vec, f"{base} B={w.cfg.update_batch}")
+    # the matrix-core run against the oracle's update on the first step
+    mode = "bf16" if w.cfg.dtype == "bf16" else "fp32"
+    drop = None if dropout is None else (dropout[0], dropout[1], 0)
+    ref = oracle.update(mode, w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.upd_feats, w.upd_ttft, w.lr,
+                        dropout=drop)
+    assert abs(mf[0]["loss"] - ref["loss"]) <= 1e-5 * abs(ref["loss"])
+    g, r = mf[0]["grad"].astype(np.float64), ref["grad"].astype(np.float64)
+    assert np.linalg.norm(g - r) <= 1e-4 * np.linalg.norm(r)
+
+
+@pytest.mark.parametrize("hidden,dtype", [((128, 128, 128), "fp32"), ((128, 128, 128), "bf16"), ((64,), "bf16")])
+def test_layer_by_layer_scores_on_matrix_cores(hidden, dtype):
+    """2,100 x 33 pairs: a 65,536-pair chunk on the matrix cores and a ragged
+    3,764-pair chunk on the vector ALUs, every score against the oracle's chain."""
+    w = _workload("homogeneous", hidden=hidden, dtype=dtype, R=2100, N=33)
+    note(f"layer-by-layer scores on the matrix cores hidden={hidden} {dtype}")
+    outs = []
+    for mode in (0, 1):
+        run = GpuRun(w)
+        run.ctx.ls_set_chain_kernels(mode)
+        outs.append(run.score())
+        run.ctx.close()
+    for k in ("scores", "chosen", "min_ttft"):
+        assert np.array_equal(np.asarray(outs[0][k]).view(np.uint32), np.asarray(outs[1][k]).view(np.uint32)), k
+    sel = np.arange(w.cfg.R, dtype=np.int32)
+    mode = "bf16" if dtype == "bf16" else "fp32"
+    ref = oracle.score(mode, w.cfg.d, w.cfg.hidden, w.params, w.mu, w.inv_sigma, w.req_off, w.req_hashes,
+                       w.prompt_len, w.inst_feat, w.inst_off, w.inst_hashes, sel=sel, threads=16)
+    out = outs[0]
+    np.testing.assert_array_equal(out["overlap"], ref["overlap"])
+    np.testing.assert_array_equal(out["scores"].view(np.uint32), ref["scores"].astype(np.float32).view(np.uint32))
+    np.testing.assert_array_equal(out["chosen"], ref["chosen"])
+    np.testing.assert_array_equal(out["min_ttft"].view(np.uint32), ref["min_ttft"].astype(np.float32).view(np.uint32))
