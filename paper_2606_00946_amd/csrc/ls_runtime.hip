@@ -320,6 +320,7 @@ struct Timed {
 
 struct WsCarve {
     char* base;
+    size_t cap = SIZE_MAX;   // bytes behind base
     size_t off = 0;
     template <class T>
     T* take(int64_t count) {
@@ -327,6 +328,7 @@ struct WsCarve {
         off += (size_t)round_up(count * (int64_t)sizeof(T), 256);
         return p;
     }
+    bool ok() const { return off <= cap; }
 };
 
 }  // namespace
@@ -741,12 +743,17 @@ int check_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, const u
 // candidate band alone).
 bool fast_path(const ls_ctx* c, const float* scores) { return c->frag16 && !c->exact_scores && scores == nullptr; }
 
+// Whether a scoring call takes the layer-by-layer forward (and its scratch):
+// models other than two hidden layers.  The sizing below and run_pipeline both
+// ask this.
+bool layer_by_layer(const ls::ModelDims& m) { return m.L != 2; }
+
 size_t pipeline_bytes(ls_ctx* c, int32_t R, int32_t N, bool have_overlap, bool have_scores, bool fast) {
     const ls::ModelDims& m = c->dims;
     const int64_t pairs = (int64_t)R * N;
     size_t need = (size_t)round_up((int64_t)m.h1 * N * 4, 256);
     need += (size_t)round_up(ls::prefix_workspace_bytes(R, N), 256);
-    if (m.L != 2) need += (size_t)round_up(4 * ls::generic_score_floats(m, pairs), 256);
+    if (layer_by_layer(m)) need += (size_t)round_up(4 * ls::generic_score_floats(m, pairs), 256);
     if (!have_overlap) need += (size_t)round_up(pairs * 4, 256);
     if (!have_scores) need += (size_t)round_up(pairs * 4, 256);
     if (fast) {
@@ -778,6 +785,8 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
     char* prefix_ws = w.take<char>(ls::prefix_workspace_bytes(R, N));
     int32_t* ov = overlap ? overlap : w.take<int32_t>(pairs);
     float* sc = scores ? scores : w.take<float>(pairs);
+    const char* undersized = "scoring scratch smaller than the call's carving (internal sizing error)";
+    if (!w.ok()) return fail(c, LS_ERR_NOMEM, "%s", undersized);
 
     LS_TIMED(c, K_PREFIX, s,
              ls::launch_prefix_match(c->tables, R, N, req_off, req_hashes, ov, prefix_ws, c->n_cu,
@@ -785,9 +794,10 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
                                                          c->prefix_join),
                                      c->prefix_closed, s));
     const uint8_t* band = nullptr;
-    if (m.L != 2) {
+    if (layer_by_layer(m)) {
         // other depths: the pairs' rows through the layer-by-layer canonical forward
         float* gws = w.take<float>(ls::generic_score_floats(m, pairs));
+        if (!w.ok()) return fail(c, LS_ERR_NOMEM, "%s", undersized);
         LS_TIMED(c, K_SCORE, s,
                  ls::launch_score_generic(m, c->compute, c->mu, c->isig, R, N, req_off, prompt_len, ov, inst_feat, sc,
                                           gws, c->n_cu, s));
@@ -803,6 +813,7 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
         int64_t* lead = w.take<int64_t>(R);
         int64_t* list = w.take<int64_t>(pairs);
         uint32_t* count = w.take<uint32_t>(64);       // [0]: stage-1 candidates (R), [32]: stage 2
+        if (!w.ok()) return fail(c, LS_ERR_NOMEM, "%s", undersized);
         LS_TIMED(c, K_SCORE_MFMA, s,
                  ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N, req_off,
                                              prompt_len, ov, sc, eb, c->n_cu, s));
@@ -845,7 +856,7 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     const bool fast = fast_path(c, scores);
     rc = grow(c, &c->ws, &c->ws_cap, pipeline_bytes(c, R, N, overlap != nullptr, scores != nullptr, fast), s);
     if (rc) return rc;
-    WsCarve w{(char*)c->ws};
+    WsCarve w{(char*)c->ws, c->ws_cap};
     Scored out;
     rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, fast, -1.0, 0, nullptr,
                       s, &out);
@@ -878,7 +889,7 @@ int ls_score_batch_noalloc(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_o
     // no profiling events here: creating one may allocate
     const bool prof = c->profiling;
     c->profiling = false;
-    WsCarve w{(char*)base};
+    WsCarve w{(char*)base, kNoAllocScratchBytes};
     Scored out;
     rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, fast, -1.0, 0, nullptr,
                       s, &out);
@@ -969,7 +980,7 @@ int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const 
     need += (size_t)round_up((int64_t)N * 8, 256) + 256 + (size_t)round_up((int64_t)2 * m.d * 4, 256);
     rc = grow(c, &c->ws, &c->ws_cap, need, s);
     if (rc) return rc;
-    WsCarve w{(char*)c->ws};
+    WsCarve w{(char*)c->ws, c->ws_cap};
     double* cnt = w.take<double>(N);
     ls::PolicyStats* st = w.take<ls::PolicyStats>(1);
     float* bounds = w.take<float>(2 * (int64_t)m.d);
