@@ -2,8 +2,9 @@
 vector ALUs, bit for bit, through the C ABI.
 
 The chains are the update's forward layers and hidden-layer gradients (Section
-4.3.2) and the layer-by-layer scorer of models other than two hidden layers
-(Section 4.1). ls_set_chain_kernels(0) runs them as v_mfma_f32_32x32x1_2b_f32
+4.3.2), the layer-by-layer scorer of models other than two hidden layers, and
+the canonical scores of two-layer models (Section 4.1: the fp32 workloads, and
+the bf16 model's exact mode). ls_set_chain_kernels(0) runs them as v_mfma_f32_32x32x1_2b_f32
 steps, one input k per instruction, wherever a call's batch fills the device.
 ls_set_chain_kernels(1) keeps them on the vector ALUs. The instruction rounds
 each multiply-add once, as fmaf does, and both kernels take the inputs in the
@@ -116,3 +117,29 @@ def test_layer_by_layer_scores_on_matrix_cores(hidden, dtype):
     np.testing.assert_array_equal(out["scores"].view(np.uint32), ref["scores"].astype(np.float32).view(np.uint32))
     np.testing.assert_array_equal(out["chosen"], ref["chosen"])
     np.testing.assert_array_equal(out["min_ttft"].view(np.uint32), ref["min_ttft"].astype(np.float32).view(np.uint32))
+
+
+# (config, R, exact mode): the fp32 workloads score canonically; the bf16 model
+# scores canonically in exact mode
+TWO_LAYER_CASES = [("tiny", None, False), ("tiny", 65, False), ("homogeneous", None, False),
+                   ("heterogeneous", None, False), ("long_context", None, False), ("large_batch", 2049, True)]
+
+
+@pytest.mark.parametrize("name,R,exact", TWO_LAYER_CASES)
+def test_two_layer_scores_on_matrix_cores(name, R, exact):
+    """The fused two-layer canonical scorer (layer 1 resumed from the instance
+    partials, every pass of layer 2 on v_mfma_f32_32x32x1_2b_f32, the head on the
+    vector ALUs) against the vector-ALU scorer: every score, decision and
+    min_ttft bit for bit; Tiny at 65 requests leaves a ragged last group of 32
+    pairs."""
+    w = synth.generate(name, R=R)
+    note(f"two-layer canonical scores on the matrix cores {name} R={w.cfg.R} exact={exact}")
+    outs = []
+    for mode in (0, 1):
+        run = GpuRun(w, exact=exact)
+        run.ctx.ls_set_chain_kernels(mode)
+        outs.append(run.score())
+        run.ctx.close()
+    for k in ("scores", "chosen", "min_ttft", "overlap"):
+        a, b = np.asarray(outs[0][k]), np.asarray(outs[1][k])
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
