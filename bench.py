@@ -44,6 +44,8 @@ PEAK_BF16_TFLOPS = 2500.0
 # fp32 FMA on the vector ALUs without packed-fp32 instructions (disabled in this
 # build): 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
 PEAK_VALU_FP32_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+# fp32 on the matrix cores (dense), where the canonical chains run as K=1 steps
+PEAK_FP32_MFMA_TFLOPS = 157.3
 
 
 # Kernels behind each timed kind (names as rocprofv3 prints them) and the
@@ -56,7 +58,10 @@ KIND_KERNELS = {
                       "ls::leaders_first_kernel", "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel",
                       "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
     "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
-    "update": (["ls::normalize_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel", "ls::layer_fwd_kernel",
+    "score_pairs": (["ls::score_chain_mfma_kernel", "ls::score_pairs_kernel"],
+                    ["k_score_chain.hip", "k_score.hip", "k_common.h", "ls_internal.h"]),
+    "update": (["ls::normalize_kernel", "ls::dense_mfma_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel",
+                "ls::layer_fwd_kernel",
                 "ls::loss_grad_kernel", "ls::loss_final_kernel", "ls::wgrad_direct_kernel",
                 "ls::wgrad_reduce_wave_kernel", "ls::wgrad_reduce_kernel", "ls::wgrad_mfma_kernel",
                 "ls::delta_head_kernel", "ls::backprop_hidden_kernel", "ls::gemm_nt_splitk_kernel",
@@ -321,14 +326,15 @@ def roofline_entry(kind, bound, work, peak, unit, calls, total_ms, cfg_name, ext
 
 def scoring_rooflines(cfg, prof, steps, exec_tflop, model_tflop, k1_gb):
     """Rooflines of the scoring kernels from one profile of `steps` scoring calls:
-    K1 on HBM, the scorer on the matrix cores (bf16) or the vector ALUs (fp32
-    canonical chains)."""
+    K1 on HBM, the bf16 scorer on the matrix cores at the bf16 peak, and the
+    canonical fp32 chains (K=1 fp32 matrix-core steps) at the fp32 matrix-core
+    peak."""
     out = {}
     if "prefix_match" in prof:
         out["prefix_match"] = roofline_entry("prefix_match", "hbm", k1_gb, PEAK_HBM_GBS, "GB/s", steps,
                                              prof["prefix_match"][1], cfg.name)
     for kind, bound, peak in (("score_pairs_mfma", "mfma", PEAK_BF16_TFLOPS),
-                              ("score_pairs", "alu", PEAK_VALU_FP32_TFLOPS)):
+                              ("score_pairs", "mfma", PEAK_FP32_MFMA_TFLOPS)):
         if kind in prof:
             ms = prof[kind][1]
             out[kind] = roofline_entry(kind, bound, exec_tflop, peak, "TFLOP/s", steps, ms, cfg.name,
@@ -472,14 +478,20 @@ def main():
     rooflines = scoring_rooflines(cfg, prof, steps, exec_tflop, model_tflop, k1_bytes / 1e9)
     if "update" in prof:
         t_u = prof["update"][1] / steps / 1e3
-        # the canonical chains (forward layers, head and hidden backprop) run on the vector ALUs
+        # the canonical chains (forward layers and hidden backprop) run as K=1 fp32
+        # matrix-core steps, the weight gradients as bf16 matrix-core products: the
+        # floor prices each part at its own peak
         chain_tflop = chain_flops(cfg, B) / 1e12
+        grad_tflop = update_flops(cfg, B) / 1e12 - chain_tflop
+        floor_ms = (chain_tflop / PEAK_FP32_MFMA_TFLOPS + grad_tflop / PEAK_BF16_TFLOPS) * 1e3
         rooflines["update"] = roofline_entry("update", "mfma" if cfg.dtype == "bf16" else "alu",
                                              update_flops(cfg, B) / 1e12,
                                              PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_VALU_FP32_TFLOPS,
                                              "TFLOP/s", steps, prof["update"][1], cfg.name,
-                                             {"valu_chain_tflop_per_s": round(chain_tflop / t_u, 3),
-                                              "valu_chain_frac": round(chain_tflop / t_u / PEAK_VALU_FP32_TFLOPS, 4)})
+                                             {"chain_tflop_per_s": round(chain_tflop / t_u, 3),
+                                              "chain_frac_fp32_mfma": round(chain_tflop / t_u / PEAK_FP32_MFMA_TFLOPS, 4),
+                                              "floor_ms_at_peaks": round(floor_ms, 4),
+                                              "floor_frac": round(floor_ms / (t_u * 1e3), 4)})
     if "table_build" in prof:
         # each cached key read once (8 B) and its table written once (two 8-byte slots per key at half load)
         rooflines["table_build"] = roofline_entry("table_build", "hbm", (8 + 16) * int(w.inst_hashes.size) / 1e9,

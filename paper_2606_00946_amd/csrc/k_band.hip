@@ -579,6 +579,10 @@ hipError_t launch_rescore(const ModelDims& m, const float* compute, const float*
                           const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
                           const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
                           const uint32_t* count, float* scores, int n_cu, hipStream_t s) {
+    // the same chains as K=1 fp32 matrix-core steps (bit-identical), 32 candidates per wave
+    if (m.mfma_chains && chain_mfma_supported(m))
+        return launch_score_chain_mfma(m, compute, mu, inv_sigma, part_t, R, N, req_off, prompt_len, overlap, list,
+                                       count, n_cu, scores, s);
     PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
                 m.d, m.d_inst, m.h1, m.h2};
     if (m.bf16 && m.h1 == m.h2 && (m.h1 == 64 || m.h1 == 128 || m.h1 == 256)) {

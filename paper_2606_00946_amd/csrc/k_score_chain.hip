@@ -45,21 +45,38 @@ __device__ __forceinline__ float act(float z) {
     return BF ? bf16_rne_num(a) : a;
 }
 
-template <bool BF, int H1, int H2>
-__global__ __launch_bounds__(64) void score_chain_mfma_kernel(PairModel M, const float* __restrict__ mu,
+}  // namespace
+
+// LIST: score the pairs list[0 .. *count) (pair indices r * N + i), with
+// persistent waves that take 32 list entries at a time; otherwise every pair,
+// one group of 32 per workgroup.  Up to h1 = 128 the tile leaves LDS for two
+// waves per SIMD, so the registers are held to that; at 256, one.
+template <bool BF, int H1, int H2, bool LIST>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(H1 <= 128 ? 2 : 1))) void score_chain_mfma_kernel(PairModel M, const float* __restrict__ mu,
                                                               const float* __restrict__ isig,
                                                               const float* __restrict__ part_t, int32_t R, int32_t N,
                                                               const int64_t* __restrict__ req_off,
                                                               const int32_t* __restrict__ prompt_len,
                                                               const int32_t* __restrict__ overlap, int block_tokens,
+                                                              const int64_t* __restrict__ list,
+                                                              const uint32_t* __restrict__ count,
                                                               float* __restrict__ scores) {
     static_assert(H1 % 64 == 0 && H2 % 64 == 0 && H1 <= 256 && H2 <= 256, "64-unit passes");
     constexpr int P1 = H1 / 64, P2 = H2 / 64, LDH = chain_ldh(H1);
     extern __shared__ __align__(16) float hl[];          // [kChainPairs][LDH]
     const int lane = threadIdx.x, col = lane & 31, hi = lane >> 5;
-    const int64_t total = (int64_t)R * N;
-    const int64_t p0 = (int64_t)blockIdx.x * kChainPairs;
-    const int64_t q = p0 + col < total ? p0 + col : total - 1;   // lanes past the end score a valid pair
+    const int64_t cnt = LIST ? (int64_t)*count : (int64_t)R * N;
+    for (int64_t e0 = (int64_t)blockIdx.x * kChainPairs; e0 < cnt; e0 += (int64_t)gridDim.x * kChainPairs) {
+    // the model's bases, opaque to the optimiser: their loads stay inside the
+    // loop instead of holding b2, w3, W1 columns, W2T rows and partial addresses
+    // in registers across tasks
+    // (an opaque zero offset: the pointers keep their global address space)
+    int32_t z0 = 0;
+    asm volatile("" : "+s"(z0));
+    const float *w1b = M.w1 + z0, *w2b = M.w2t + z0, *b2b = M.b2 + z0, *w3b = M.w3 + z0, *ptb = part_t + z0;
+    const int32_t Nb = N + z0;
+    const int64_t e = e0 + col < cnt ? e0 + col : cnt - 1;       // lanes past the end score a valid pair
+    const int64_t q = LIST ? list[e] : e;
     const int64_t r = q / N;
     const int32_t inst = (int32_t)(q - r * N);
     float x[5], xt[5];
@@ -74,9 +91,9 @@ __global__ __launch_bounds__(64) void score_chain_mfma_kernel(PairModel M, const
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
             const int u = 64 * p + 32 * (i >> 4) + 8 * ((i & 15) >> 2) + 4 * hi + (i & 3);
-            acc[i] = part_t[(int64_t)u * N + inst];
+            acc[i] = ptb[(uint32_t)(u * Nb + inst)];           // h1 N < 2^31
         }
-        const float* __restrict__ w1 = M.w1 + (int64_t)(64 * p + lane) * M.d + M.d_inst;
+        const float* __restrict__ w1 = w1b + (int64_t)(64 * p + lane) * M.d + M.d_inst;
         float a[5];
 #pragma unroll
         for (int c = 0; c < 5; ++c) a[c] = w1[c];
@@ -96,8 +113,8 @@ __global__ __launch_bounds__(64) void score_chain_mfma_kernel(PairModel M, const
 #pragma unroll
     for (int p = 0; p < P2; ++p)
 #pragma unroll
-        for (int i = 0; i < 32; ++i) acc[p][i] = M.b2[64 * p + 32 * (i >> 4) + 8 * ((i & 15) >> 2) + 4 * hi + (i & 3)];
-    const float* __restrict__ w2 = M.w2t + lane;            // W2T[k][64 p + lane] = w2[k * H2 + 64 p]
+        for (int i = 0; i < 32; ++i) acc[p][i] = b2b[64 * p + 32 * (i >> 4) + 8 * ((i & 15) >> 2) + 4 * hi + (i & 3)];
+    const float* __restrict__ w2 = w2b + lane;              // W2T[k][64 p + lane] = w2[k * H2 + 64 p]
     constexpr int G = 8;                                    // inputs per group
     auto load = [&](float (&w)[G][P2], int k0) {
 #pragma unroll
@@ -144,37 +161,50 @@ __global__ __launch_bounds__(64) void score_chain_mfma_kernel(PairModel M, const
                 up[e] = __shfl_xor(h, 32);
             }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) t = __builtin_fmaf(M.w3[u + e], lo[e], t);
+            for (int e = 0; e < 4; ++e) t = __builtin_fmaf(w3b[u + e], lo[e], t);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) t = __builtin_fmaf(M.w3[u + 4 + e], up[e], t);
+            for (int e = 0; e < 4; ++e) t = __builtin_fmaf(w3b[u + 4 + e], up[e], t);
         }
-    if (hi == 0 && p0 + col < total) scores[p0 + col] = t;
+    if (hi == 0 && e0 + col < cnt) scores[q] = t;
+    }
 }
+
+namespace {
 
 template <bool BF, int H1, int H2>
 hipError_t launch_chain(const PairModel& M, const float* mu, const float* isig, const float* part_t, int32_t R,
                         int32_t N, const int64_t* req_off, const int32_t* prompt_len, const int32_t* overlap,
-                        int block_tokens, float* scores, hipStream_t s) {
-    const int64_t total = (int64_t)R * N;
-    const int64_t grid = (total + kChainPairs - 1) / kChainPairs;
+                        int block_tokens, const int64_t* list, const uint32_t* count, int n_cu, float* scores,
+                        hipStream_t s) {
     const size_t lds = sizeof(float) * kChainPairs * chain_ldh(H1);
-    hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2>), dim3((uint32_t)grid), dim3(64), lds, s, M, mu, isig,
-                       part_t, R, N, req_off, prompt_len, overlap, block_tokens, scores);
+    if (list) {
+        // persistent: as many single-wave workgroups as the LDS lets every CU hold
+        const int per_cu = (int)((160u << 10) / lds) < 8 ? (int)((160u << 10) / lds) : 8;
+        hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2, true>), dim3((uint32_t)(n_cu * per_cu)), dim3(64),
+                           lds, s, M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count,
+                           scores);
+    } else {
+        const int64_t grid = ((int64_t)R * N + kChainPairs - 1) / kChainPairs;
+        hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2, false>), dim3((uint32_t)grid), dim3(64), lds, s, M,
+                           mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count, scores);
+    }
     return hipGetLastError();
 }
 
 template <bool BF>
 hipError_t dispatch_chain(const ModelDims& m, const PairModel& M, const float* mu, const float* isig,
                           const float* part_t, int32_t R, int32_t N, const int64_t* req_off, const int32_t* prompt_len,
-                          const int32_t* overlap, float* scores, hipStream_t s) {
+                          const int32_t* overlap, const int64_t* list, const uint32_t* count, int n_cu, float* scores,
+                          hipStream_t s) {
     const int bt = m.block_tokens;
-    if (m.h1 == 64 && m.h2 == 64)
-        return launch_chain<BF, 64, 64>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, scores, s);
-    if (m.h1 == 128 && m.h2 == 128)
-        return launch_chain<BF, 128, 128>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, scores, s);
-    if (m.h1 == 256 && m.h2 == 256)
-        return launch_chain<BF, 256, 256>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, scores, s);
-    return hipErrorInvalidValue;
+    if (m.h1 == 64)
+        return launch_chain<BF, 64, 64>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, list, count, n_cu,
+                                        scores, s);
+    if (m.h1 == 128)
+        return launch_chain<BF, 128, 128>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, list, count,
+                                          n_cu, scores, s);
+    return launch_chain<BF, 256, 256>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, bt, list, count, n_cu,
+                                      scores, s);
 }
 
 }  // namespace
@@ -185,14 +215,17 @@ bool chain_mfma_supported(const ModelDims& m) {
 
 hipError_t launch_score_chain_mfma(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
                                    const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
-                                   const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s) {
+                                   const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
+                                   const uint32_t* count, int n_cu, float* scores, hipStream_t s) {
     if ((int64_t)R * N <= 0) return hipSuccess;
-    if (!chain_mfma_supported(m)) return hipErrorInvalidValue;
+    if (!chain_mfma_supported(m) || (list == nullptr) != (count == nullptr)) return hipErrorInvalidValue;
     PairModel M{compute + m.c_w1, compute + m.c_w2t, compute + m.c_b2, compute + m.c_w3, compute + m.c_b3,
                 m.d, m.d_inst, m.h1, m.h2};
     if (m.bf16)
-        return dispatch_chain<true>(m, M, mu, inv_sigma, part_t, R, N, req_off, prompt_len, overlap, scores, s);
-    return dispatch_chain<false>(m, M, mu, inv_sigma, part_t, R, N, req_off, prompt_len, overlap, scores, s);
+        return dispatch_chain<true>(m, M, mu, inv_sigma, part_t, R, N, req_off, prompt_len, overlap, list, count, n_cu,
+                                    scores, s);
+    return dispatch_chain<false>(m, M, mu, inv_sigma, part_t, R, N, req_off, prompt_len, overlap, list, count, n_cu,
+                                 scores, s);
 }
 
 }  // namespace ls

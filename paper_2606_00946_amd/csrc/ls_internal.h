@@ -243,11 +243,14 @@ hipError_t launch_score_pairs(const ModelDims& m, const float* compute, const fl
                               const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
                               const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s);
 // The same canonical scores on the matrix cores (two hidden layers of equal
-// width 64, 128 or 256): bit-identical to launch_score_pairs.
+// width 64, 128 or 256): bit-identical to launch_score_pairs.  With list and
+// count (device; both or neither) only the pairs list[0 .. *count) are scored,
+// as launch_rescore does.
 bool chain_mfma_supported(const ModelDims& m);
 hipError_t launch_score_chain_mfma(const ModelDims& m, const float* compute, const float* mu, const float* inv_sigma,
                                    const float* part_t, int32_t R, int32_t N, const int64_t* req_off,
-                                   const int32_t* prompt_len, const int32_t* overlap, float* scores, hipStream_t s);
+                                   const int32_t* prompt_len, const int32_t* overlap, const int64_t* list,
+                                   const uint32_t* count, int n_cu, float* scores, hipStream_t s);
 hipError_t launch_argmin(const ModelDims& m, int32_t R, int32_t N, const float* scores, const uint8_t* band,
                          const int64_t* req_off, const int32_t* prompt_len, const int32_t* overlap,
                          const float* inst_feat, int32_t* chosen, float* min_ttft, float* feat_out, hipStream_t s);

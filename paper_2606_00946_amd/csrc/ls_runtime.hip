@@ -833,8 +833,8 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
         band = flags;
     } else if (m.mfma_chains && ls::chain_mfma_supported(m)) {
         LS_TIMED(c, K_SCORE, s,
-                 ls::launch_score_chain_mfma(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc,
-                                             s));
+                 ls::launch_score_chain_mfma(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov,
+                                             nullptr, nullptr, c->n_cu, sc, s));
     } else {
         LS_TIMED(c, K_SCORE, s,
                  ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));

@@ -143,3 +143,22 @@ def test_two_layer_scores_on_matrix_cores(name, R, exact):
     for k in ("scores", "chosen", "min_ttft", "overlap"):
         a, b = np.asarray(outs[0][k]), np.asarray(outs[1][k])
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+
+
+@pytest.mark.parametrize("R", [4096, 777])
+def test_rescoring_on_matrix_cores(R):
+    """The bf16 fast path's canonical rescoring of its candidate band (stage 1:
+    every request's fast argmin; stage 2: what can still beat it) as K=1 fp32
+    matrix-core chains over the candidate list against the vector-ALU rescoring:
+    decisions, min_ttft, overlaps and chosen feature rows bit for bit."""
+    w = synth.generate("large_batch", R=R)
+    note(f"fast-path rescoring on the matrix cores large_batch R={R}")
+    outs = []
+    for mode in (0, 1):
+        run = GpuRun(w)
+        run.ctx.ls_set_chain_kernels(mode)
+        outs.append(run.score(with_scores=False))
+        run.ctx.close()
+    for k in ("chosen", "min_ttft", "overlap", "feat"):
+        a, b = np.asarray(outs[0][k]), np.asarray(outs[1][k])
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
