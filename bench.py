@@ -57,7 +57,8 @@ KIND_KERNELS = {
     "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_scan_kernel",
                       "ls::leaders_first_kernel", "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel",
                       "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
-    "rescore": (["ls::rescore_wave_kernel"], ["k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
+    "rescore": (["ls::rescore_chain_mfma_kernel", "ls::rescore_wave_kernel"],
+                ["k_score_chain.hip", "k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
     "score_pairs": (["ls::score_chain_mfma_kernel", "ls::score_pairs_kernel"],
                     ["k_score_chain.hip", "k_score.hip", "k_common.h", "ls_internal.h"]),
     "update": (["ls::normalize_kernel", "ls::dense_mfma_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel",

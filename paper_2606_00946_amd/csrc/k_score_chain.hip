@@ -50,17 +50,15 @@ __device__ __forceinline__ float act(float z) {
 // LIST: score the pairs list[0 .. *count) (pair indices r * N + i), with
 // persistent waves that take 32 list entries at a time; otherwise every pair,
 // one group of 32 per workgroup.  Up to h1 = 128 the tile leaves LDS for two
-// waves per SIMD, so the registers are held to that; at 256, one.
+// waves per SIMD, so the kernels hold their registers to that; at 256, one.
 template <bool BF, int H1, int H2, bool LIST>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(H1 <= 128 ? 2 : 1))) void score_chain_mfma_kernel(PairModel M, const float* __restrict__ mu,
-                                                              const float* __restrict__ isig,
-                                                              const float* __restrict__ part_t, int32_t R, int32_t N,
-                                                              const int64_t* __restrict__ req_off,
-                                                              const int32_t* __restrict__ prompt_len,
-                                                              const int32_t* __restrict__ overlap, int block_tokens,
-                                                              const int64_t* __restrict__ list,
-                                                              const uint32_t* __restrict__ count,
-                                                              float* __restrict__ scores) {
+__device__ __forceinline__ void chain_body(const PairModel& M, const float* __restrict__ mu,
+                                           const float* __restrict__ isig, const float* __restrict__ part_t,
+                                           int32_t R, int32_t N, const int64_t* __restrict__ req_off,
+                                           const int32_t* __restrict__ prompt_len,
+                                           const int32_t* __restrict__ overlap, int block_tokens,
+                                           const int64_t* __restrict__ list, const uint32_t* __restrict__ count,
+                                           float* __restrict__ scores) {
     static_assert(H1 % 64 == 0 && H2 % 64 == 0 && H1 <= 256 && H2 <= 256, "64-unit passes");
     constexpr int P1 = H1 / 64, P2 = H2 / 64, LDH = chain_ldh(H1);
     extern __shared__ __align__(16) float hl[];          // [kChainPairs][LDH]
@@ -169,6 +167,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(H1 <= 128 ? 
     }
 }
 
+// Every pair, one group of 32 per workgroup.
+template <bool BF, int H1, int H2>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(H1 <= 128 ? 2 : 1))) void score_chain_mfma_kernel(
+    PairModel M, const float* __restrict__ mu, const float* __restrict__ isig, const float* __restrict__ part_t,
+    int32_t R, int32_t N, const int64_t* __restrict__ req_off, const int32_t* __restrict__ prompt_len,
+    const int32_t* __restrict__ overlap, int block_tokens, float* __restrict__ scores) {
+    chain_body<BF, H1, H2, false>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, nullptr,
+                                  nullptr, scores);
+}
+
+// The candidate band's rescoring: the pairs list[0 .. *count), persistent waves.
+template <bool BF, int H1, int H2>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(H1 <= 128 ? 2 : 1))) void rescore_chain_mfma_kernel(
+    PairModel M, const float* __restrict__ mu, const float* __restrict__ isig, const float* __restrict__ part_t,
+    int32_t R, int32_t N, const int64_t* __restrict__ req_off, const int32_t* __restrict__ prompt_len,
+    const int32_t* __restrict__ overlap, int block_tokens, const int64_t* __restrict__ list,
+    const uint32_t* __restrict__ count, float* __restrict__ scores) {
+    chain_body<BF, H1, H2, true>(M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count,
+                                 scores);
+}
+
 namespace {
 
 template <bool BF, int H1, int H2>
@@ -180,13 +199,13 @@ hipError_t launch_chain(const PairModel& M, const float* mu, const float* isig, 
     if (list) {
         // persistent: as many single-wave workgroups as the LDS lets every CU hold
         const int per_cu = (int)((160u << 10) / lds) < 8 ? (int)((160u << 10) / lds) : 8;
-        hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2, true>), dim3((uint32_t)(n_cu * per_cu)), dim3(64),
-                           lds, s, M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count,
+        hipLaunchKernelGGL((rescore_chain_mfma_kernel<BF, H1, H2>), dim3((uint32_t)(n_cu * per_cu)), dim3(64), lds,
+                           s, M, mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count,
                            scores);
     } else {
         const int64_t grid = ((int64_t)R * N + kChainPairs - 1) / kChainPairs;
-        hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2, false>), dim3((uint32_t)grid), dim3(64), lds, s, M,
-                           mu, isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, list, count, scores);
+        hipLaunchKernelGGL((score_chain_mfma_kernel<BF, H1, H2>), dim3((uint32_t)grid), dim3(64), lds, s, M, mu,
+                           isig, part_t, R, N, req_off, prompt_len, overlap, block_tokens, scores);
     }
     return hipGetLastError();
 }

@@ -768,17 +768,33 @@ __global__ void loss_final_kernel(const float* __restrict__ loss_part, int nblk,
 }
 
 // dL/dz of the last hidden layer: g_b * w[j] where z > 0 (then dropout's factor);
-// blockIdx.y = unit j
+// blockIdx.y = unit j.  VEC (B a multiple of 4): four consecutive samples per
+// thread, one 16-byte load of g and one 16-byte store.
 template <bool BF>
+__device__ __forceinline__ float head_delta(const float* __restrict__ g, float wj, const uint64_t word, int64_t b,
+                                            int j, const DropArgs& D, int layer) {
+    const float v = apply_drop(D, layer, b, j, ((word >> (b & 63)) & 1ull) ? g[b] * wj : 0.0f);
+    return BF ? q_bf16(v) : v;
+}
+
+template <bool BF, bool VEC>
 __global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
                                                          const uint64_t* __restrict__ zb, float* __restrict__ dl,
                                                          int32_t B, DropArgs D, int layer) {
-    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    constexpr int S = VEC ? 4 : 1;
+    const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * S;
     const int j = (int)blockIdx.y;
     if (b >= B) return;
+    const float wj = w[j];
+    const uint64_t word = zb[(int64_t)j * mask_words(B) + (b >> 6)];     // the S samples share it
     const int64_t t = (int64_t)j * B + b;
-    const float v = apply_drop(D, layer, b, j, mask_bit(zb, B, j, b) ? g[b] * w[j] : 0.0f);
-    dl[t] = BF ? q_bf16(v) : v;
+    if constexpr (VEC) {
+        *reinterpret_cast<float4*>(dl + t) =
+            make_float4(head_delta<BF>(g, wj, word, b, j, D, layer), head_delta<BF>(g, wj, word, b + 1, j, D, layer),
+                        head_delta<BF>(g, wj, word, b + 2, j, D, layer), head_delta<BF>(g, wj, word, b + 3, j, D, layer));
+    } else {
+        dl[t] = head_delta<BF>(g, wj, word, b, j, D, layer);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1375,8 +1391,12 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         hipLaunchKernelGGL(rowsum_kernel, dim3(1), dim3(256), 0, s, w.g, B, w.grad + m.m_b[L]);
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(delta_head_kernel<BF>, dim3(blocks_for(nB, 256), m.hl), dim3(256), 0, s, w.g,
-                       compute + m.c_wt[L], w.zb[L - 1], w.dl[L - 1], B, D, L - 1);
+    if (B % 4 == 0)
+        hipLaunchKernelGGL((delta_head_kernel<BF, true>), dim3(blocks_for(nB, 1024), m.hl), dim3(256), 0, s, w.g,
+                           compute + m.c_wt[L], w.zb[L - 1], w.dl[L - 1], B, D, L - 1);
+    else
+        hipLaunchKernelGGL((delta_head_kernel<BF, false>), dim3(blocks_for(nB, 256), m.hl), dim3(256), 0, s, w.g,
+                           compute + m.c_wt[L], w.zb[L - 1], w.dl[L - 1], B, D, L - 1);
     // hidden layers, last to first
     for (int l = L - 1; l >= 0; --l) {
         const float* in = l == 0 ? w.xn : w.a[l - 1];
