@@ -438,8 +438,6 @@ static bool dense_small(int32_t B, int O) {
 // 32 lanes of a tile read without bank conflicts.  A group of kMfPre inputs
 // takes all of its A operands in one batch of reads issued before its first
 // multiply-add, and its B operands one group ahead.
-constexpr int kMfTiles = 4;
-constexpr int kMfUnits = 32 * kMfTiles;       // output units per workgroup
 constexpr int kMfWaves = 8;                   // 64 samples each
 constexpr int kMfPre = 8;                     // inputs per group
 constexpr int kMfMaxLdk = kDenseMaxK + 4;
@@ -455,7 +453,7 @@ typedef float f32x32_t __attribute__((ext_vector_type(32)));
 // epilogue without per-element tests: row bases are scalar, lane offsets 32-bit,
 // and the ReLU mask words of its 128 units are gathered into two registers per
 // lane and written with two stores.
-template <bool BF, int MODE, bool DROP>
+template <bool BF, int MODE, bool DROP, int TILES>
 __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* __restrict__ in,
                                                                    const float* __restrict__ wt,
                                                                    const float* __restrict__ bias,
@@ -463,6 +461,10 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
                                                                    float* __restrict__ a, int32_t B, int K, int O,
                                                                    DropArgs D, int layer) {
     static_assert(MODE == kFwdRelu || MODE == kBackprop, "hidden layers only");
+    static_assert(TILES == 1 || TILES == 2 || TILES == 4, "tiles per wave");
+    constexpr int kMfUnits = 32 * TILES;          // output units per workgroup
+    constexpr int kMfTiles = TILES;
+    constexpr int NW = (kMfUnits + 63) / 64;      // mask-word registers per lane
     __shared__ __align__(16) float wl[kMfUnits * kMfMaxLdk];
     __shared__ __align__(16) float bl[kMfUnits];
     const int jb = blockIdx.y * kMfUnits;
@@ -633,11 +635,14 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
     float* __restrict__ outp = MODE == kFwdRelu ? a : z;
     if (b0 + 64 <= B && nu == kMfUnits) {
         // mask words of this wave's sample word for units lane and 64 + lane
-        uint32_t wlo[2] = {0u, 0u}, whi[2] = {0u, 0u};
+        uint32_t wlo[NW], whi[NW];
+#pragma unroll
+        for (int h = 0; h < NW; ++h) wlo[h] = whi[h] = 0u;
         if (MODE == kBackprop) {
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const uint64_t w = zb[(int64_t)(jb + 64 * h + lane) * mw + (b0 >> 6)];
+            for (int h = 0; h < NW; ++h) {
+                const int u = 64 * h + lane < kMfUnits ? 64 * h + lane : kMfUnits - 1;
+                const uint64_t w = zb[(int64_t)(jb + u) * mw + (b0 >> 6)];
                 wlo[h] = (uint32_t)w;
                 whi[h] = (uint32_t)(w >> 32);
             }
@@ -683,8 +688,9 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
             }
         if (MODE == kFwdRelu && zb != nullptr) {
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
-                zb[(int64_t)(jb + 64 * h + lane) * mw + (b0 >> 6)] = ((uint64_t)whi[h] << 32) | wlo[h];
+            for (int h = 0; h < NW; ++h)
+                if (64 * h + lane < kMfUnits)
+                    zb[(int64_t)(jb + 64 * h + lane) * mw + (b0 >> 6)] = ((uint64_t)whi[h] << 32) | wlo[h];
         }
         return;
     }
@@ -720,13 +726,41 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
     }
 }
 
-// The matrix-core chains pay off once the batch fills the chip: a workgroup
-// per 512 samples and 128 output units.
+// Tiles per wave for the matrix-core chains (0: keep the vector-lane kernels).
+// Four (a workgroup per 512 samples and 128 output units) once that fills the
+// chip; one (32 units per workgroup, four times the workgroups) for smaller
+// batches, down to 16 workgroups; below that the thread-per-element kernels.
 constexpr int kMfMinWgs = 128;
+constexpr int kMfMinWgs1 = 16;
 
-static bool dense_mfma(const ModelDims& m, int32_t B, int O) {
-    return m.mfma_chains && B <= (1 << 28) &&
-           (int64_t)((B + 64 * kMfWaves - 1) / (64 * kMfWaves)) * ((O + kMfUnits - 1) / kMfUnits) >= kMfMinWgs;
+static int dense_mfma(const ModelDims& m, int32_t B, int O) {
+    if (!m.mfma_chains || B > (1 << 28)) return 0;
+    const int64_t sb = (B + 64 * kMfWaves - 1) / (64 * kMfWaves);
+    if (sb * ((O + 127) / 128) >= kMfMinWgs) return 4;
+    if (sb * ((O + 31) / 32) >= kMfMinWgs1) return 1;
+    return 0;
+}
+
+template <bool BF, int MODE>
+static void launch_dense_mfma(int tiles, const float* in, const float* wt, const float* bias, uint64_t* zb, float* z,
+                              float* a, int32_t B, int K, int O, const DropArgs& D, int layer, hipStream_t s) {
+    const dim3 block(64 * kMfWaves);
+    const dim3 grid(blocks_for(B, 64 * kMfWaves), (O + 32 * tiles - 1) / (32 * tiles));
+    if (tiles == 4) {
+        if (D.thr53)
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 4>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
+                               O, D, layer);
+        else
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 4>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
+                               O, D, layer);
+    } else {
+        if (D.thr53)
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 1>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
+                               O, D, layer);
+        else
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 1>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
+                               O, D, layer);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1236,18 +1270,14 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
     for (int l = 0; l < m.L; ++l) {
         const float* in = l == 0 ? xn : a[l - 1];
         const int K = m.in_of(l), O = m.h[l];
-        if (lds_w && dense_small(B, O)) {
+        const int tiles = lds_w ? dense_mfma(m, B, O) : 0;
+        if (tiles) {
+            launch_dense_mfma<BF, kFwdRelu>(tiles, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l],
+                                            B, K, O, D, l, s);
+        } else if (lds_w && dense_small(B, O)) {
             if (zb[l]) (void)launch_fill_u64(zb[l], 0ull, (int64_t)O * mask_words(B), s);   // bits set by atomics
             hipLaunchKernelGGL((dense_small_kernel<BF, kFwdRelu>), dim3((O + 63) / 64, blocks_for(nB, 4)), dim3(256), 0,
                                s, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
-        } else if (lds_w && dense_mfma(m, B, O)) {
-            const dim3 grid(blocks_for(nB, 64 * kMfWaves), (O + kMfUnits - 1) / kMfUnits);
-            if (D.thr53)
-                hipLaunchKernelGGL((dense_mfma_kernel<BF, kFwdRelu, true>), grid, dim3(64 * kMfWaves), 0, s, in,
-                                   compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
-            else
-                hipLaunchKernelGGL((dense_mfma_kernel<BF, kFwdRelu, false>), grid, dim3(64 * kMfWaves), 0, s, in,
-                                   compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l], B, K, O, D, l);
         } else if (lds_w) {
             hipLaunchKernelGGL((dense_lane_kernel<BF, kFwdRelu>), dim3(sbd, (O + kDenseUnits - 1) / kDenseUnits),
                                dim3(256), 0, s, in,
@@ -1411,19 +1441,14 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         if (l == 0) break;
         // dL/dz of layer l - 1 = (W_l^T dL/dz_l), masked by z_{l-1} > 0 and dropout
         const int Kp = m.h[l - 1];
-        if (lds_w && dense_small(B, Kp))
+        const int tiles = lds_w ? dense_mfma(m, B, Kp) : 0;
+        if (tiles)
+            launch_dense_mfma<BF, kBackprop>(tiles, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1],
+                                             nullptr, B, O, Kp, D, l - 1, s);
+        else if (lds_w && dense_small(B, Kp))
             hipLaunchKernelGGL((dense_small_kernel<BF, kBackprop>), dim3((Kp + 63) / 64, blocks_for(nB, 4)), dim3(256),
                                0, s, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp,
                                D, l - 1);
-        else if (lds_w && dense_mfma(m, B, Kp)) {
-            const dim3 grid(blocks_for(nB, 64 * kMfWaves), (Kp + kMfUnits - 1) / kMfUnits);
-            if (D.thr53)
-                hipLaunchKernelGGL((dense_mfma_kernel<BF, kBackprop, true>), grid, dim3(64 * kMfWaves), 0, s, w.dl[l],
-                                   compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
-            else
-                hipLaunchKernelGGL((dense_mfma_kernel<BF, kBackprop, false>), grid, dim3(64 * kMfWaves), 0, s, w.dl[l],
-                                   compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1], nullptr, B, O, Kp, D, l - 1);
-        }
         else if (lds_w)
             hipLaunchKernelGGL((dense_lane_kernel<BF, kBackprop>), dim3(sbd, (Kp + kDenseUnits - 1) / kDenseUnits),
                                dim3(256), 0, s, w.dl[l],
