@@ -40,6 +40,20 @@ __device__ __forceinline__ float apply_drop(const DropArgs& D, int layer, int64_
 
 static inline uint32_t blocks_for(int64_t n, int block) { return (uint32_t)((n + block - 1) / block); }
 
+// Storage of the update's saved activations and layer gradients: fp32, or, for
+// bf16 models whose layers all run on the matrix cores, the bf16 bit patterns
+// (every stored value is already a bf16 number there, so nothing is lost and
+// each pass moves half the bytes).
+typedef uint16_t bf16s_t;
+__device__ __forceinline__ float ld_act(const float* __restrict__ p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_act(const bf16s_t* __restrict__ p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+__device__ __forceinline__ void st_act(float* __restrict__ p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void st_act(bf16s_t* __restrict__ p, int64_t i, float v) {
+    p[i] = v != v ? (bf16s_t)0x7FC0u : (bf16s_t)(__float_as_uint(v) >> 16);
+}
+
 // ---------------------------------------------------------------------------
 // workspace layout
 // ---------------------------------------------------------------------------
@@ -128,9 +142,9 @@ int64_t update_workspace_bytes(const ModelDims& m, int32_t B) { return plan_ws(m
 // Normalised inputs, feature-major: a tile of 64 samples x 64 features is read
 // row by row (coalesced), transposed through LDS and written out one feature
 // row at a time.
-template <bool BF>
+template <bool BF, typename TA = float>
 __global__ __launch_bounds__(256) void normalize_kernel(const float* __restrict__ feats, const float* __restrict__ mu,
-                                                        const float* __restrict__ isig, float* __restrict__ xn,
+                                                        const float* __restrict__ isig, TA* __restrict__ xn,
                                                         int32_t B, int d) {
     __shared__ float tile[64][65];                  // [feature][sample]
     const int64_t b0 = (int64_t)blockIdx.x * 64;
@@ -147,7 +161,7 @@ __global__ __launch_bounds__(256) void normalize_kernel(const float* __restrict_
     for (int j = ty; j < 64; j += 4) {
         const int c = c0 + j;
         const int64_t b = b0 + tx;
-        if (c < d && b < B) xn[(int64_t)c * B + b] = tile[j][tx];
+        if (c < d && b < B) st_act(xn, (int64_t)c * B + b, tile[j][tx]);
     }
 }
 
@@ -269,6 +283,16 @@ __device__ __forceinline__ void dense_store(float acc, int64_t e, int64_t b, int
     }
 }
 
+// The value dense_store stores, for kernels that store it themselves.
+template <bool BF, int MODE>
+__device__ __forceinline__ float dense_value(float acc, int64_t b, int o, bool on, const DropArgs& D, int layer) {
+    float v;
+    if (MODE == kFwdRelu) v = apply_drop(D, layer, b, o, relu_u(acc));
+    else if (MODE == kFwdHead) return acc;
+    else v = apply_drop(D, layer, b, o, on ? acc : 0.0f);
+    return BF ? q_bf16(v) : v;
+}
+
 // zb: the layer's ReLU mask, written in kFwdRelu (when not null) and read in
 // kBackprop; wsamp: the wave's first sample (slot j holds wsamp + 64 j + lane).
 template <bool BF, int MODE, int U>
@@ -383,8 +407,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void d
 // wave-uniform loads.  Same chains, same order.
 constexpr int kDenseSmallWgs = 256;            // below this many lane-path workgroups
 
-template <bool BF, int MODE>
-__global__ __launch_bounds__(256) void dense_small_kernel(const float* __restrict__ in, const float* __restrict__ wt,
+template <bool BF, int MODE, typename TIN = float>
+__global__ __launch_bounds__(256) void dense_small_kernel(const TIN* __restrict__ in, const float* __restrict__ wt,
                                                           const float* __restrict__ bias,
                                                           uint64_t* __restrict__ zb, float* __restrict__ z,
                                                           float* __restrict__ a, int32_t B, int K, int O, DropArgs D,
@@ -400,14 +424,14 @@ __global__ __launch_bounds__(256) void dense_small_kernel(const float* __restric
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             w[e] = MODE == kBackprop ? wt[(int64_t)o * K + k + e] : wt[(int64_t)(k + e) * O + o];
-            x[e] = in[(int64_t)(k + e) * B + b];
+            x[e] = ld_act(in, (int64_t)(k + e) * B + b);
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc = __builtin_fmaf(w[e], x[e], acc);
     }
     for (; k < K; ++k) {
         const float w = MODE == kBackprop ? wt[(int64_t)o * K + k] : wt[(int64_t)k * O + o];
-        acc = __builtin_fmaf(w, in[(int64_t)k * B + b], acc);
+        acc = __builtin_fmaf(w, ld_act(in, (int64_t)k * B + b), acc);
     }
     // the mask bits of a word come from different threads here: zb starts zeroed
     if (MODE == kFwdRelu && zb != nullptr && acc > 0.0f)
@@ -453,12 +477,12 @@ typedef float f32x32_t __attribute__((ext_vector_type(32)));
 // epilogue without per-element tests: row bases are scalar, lane offsets 32-bit,
 // and the ReLU mask words of its 128 units are gathered into two registers per
 // lane and written with two stores.
-template <bool BF, int MODE, bool DROP, int TILES>
-__global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* __restrict__ in,
+template <bool BF, int MODE, bool DROP, int TILES, typename TA = float>
+__global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const TA* __restrict__ in,
                                                                    const float* __restrict__ wt,
                                                                    const float* __restrict__ bias,
-                                                                   uint64_t* __restrict__ zb, float* __restrict__ z,
-                                                                   float* __restrict__ a, int32_t B, int K, int O,
+                                                                   uint64_t* __restrict__ zb, TA* __restrict__ z,
+                                                                   TA* __restrict__ a, int32_t B, int K, int O,
                                                                    DropArgs D, int layer) {
     static_assert(MODE == kFwdRelu || MODE == kBackprop, "hidden layers only");
     static_assert(TILES == 1 || TILES == 2 || TILES == 4, "tiles per wave");
@@ -566,7 +590,7 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
     const int64_t b0 = (int64_t)blockIdx.x * (64 * kMfWaves) + 64 * wave;
     if (b0 >= B) return;
     const int64_t bl_ = b0 + lane;
-    const float* __restrict__ src = in + (bl_ < B ? bl_ : (int64_t)B - 1);   // lanes past B read a valid row
+    const TA* __restrict__ src = in + (bl_ < B ? bl_ : (int64_t)B - 1);      // lanes past B read a valid row
     const int hi = lane >> 5, col = lane & 31;
     // accumulators start at the bias (zero for the gradients and for units past O)
     f32x32_t acc[kMfTiles];
@@ -587,7 +611,7 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
 #pragma unroll
         for (int e = 0; e < kMfPre; ++e) {
             const int k = k0 + e < K ? k0 + e : K - 1;
-            x[e] = src[(int64_t)k * B];
+            x[e] = ld_act(src, (int64_t)k * B);
         }
     };
     // one group of inputs; FULL: all kMfPre of them are below K (no per-step test,
@@ -632,7 +656,7 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
     // i of tile t holds unit u = 32 t + 8 (i % 16 / 4) + 4 hi + i % 4 of the slice
     // for sample b0 + 32 (i / 16) + col.
     const int mw = (int)mask_words(B);
-    float* __restrict__ outp = MODE == kFwdRelu ? a : z;
+    TA* __restrict__ outp = MODE == kFwdRelu ? a : z;
     if (b0 + 64 <= B && nu == kMfUnits) {
         // mask words of this wave's sample word for units lane and 64 + lane
         uint32_t wlo[NW], whi[NW];
@@ -653,7 +677,7 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int u0 = 32 * t + 8 * (i >> 2) + (i & 3);          // lanes 0-31: u0, lanes 32-63: u0 + 4
-                float* __restrict__ row = outp + (int64_t)(jb + u0) * B + b0;
+                TA* __restrict__ row = outp + (int64_t)(jb + u0) * B + b0;
                 float c0 = acc[t][i], c1 = acc[t][i + 16];
                 if (MODE == kFwdRelu) {
                     if (zb != nullptr) {     // uniform
@@ -683,8 +707,8 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
                     c0 = apply_drop(D, layer, b0 + col, o, c0);
                     c1 = apply_drop(D, layer, b0 + 32 + col, o, c1);
                 }
-                row[loff] = BF ? q_bf16(c0) : c0;
-                row[loff + 32] = BF ? q_bf16(c1) : c1;
+                st_act(row, loff, BF ? q_bf16(c0) : c0);
+                st_act(row, loff + 32, BF ? q_bf16(c1) : c1);
             }
         if (MODE == kFwdRelu && zb != nullptr) {
 #pragma unroll
@@ -719,8 +743,8 @@ __global__ __launch_bounds__(64 * kMfWaves) void dense_mfma_kernel(const float* 
                 on1 = (word >> (32 + col)) & 1ull;
             }
             if (o < O) {
-                if (v0) dense_store<BF, MODE>(c0, (int64_t)o * B + s0, s0, o, on0, z, a, D, layer);
-                if (v1) dense_store<BF, MODE>(c1, (int64_t)o * B + s1, s1, o, on1, z, a, D, layer);
+                if (v0) st_act(outp, (int64_t)o * B + s0, dense_value<BF, MODE>(c0, s0, o, on0, D, layer));
+                if (v1) st_act(outp, (int64_t)o * B + s1, dense_value<BF, MODE>(c1, s1, o, on1, D, layer));
             }
         }
     }
@@ -741,25 +765,25 @@ static int dense_mfma(const ModelDims& m, int32_t B, int O) {
     return 0;
 }
 
-template <bool BF, int MODE>
-static void launch_dense_mfma(int tiles, const float* in, const float* wt, const float* bias, uint64_t* zb, float* z,
-                              float* a, int32_t B, int K, int O, const DropArgs& D, int layer, hipStream_t s) {
+template <bool BF, int MODE, typename TA = float>
+static void launch_dense_mfma(int tiles, const TA* in, const float* wt, const float* bias, uint64_t* zb, TA* z, TA* a,
+                              int32_t B, int K, int O, const DropArgs& D, int layer, hipStream_t s) {
     const dim3 block(64 * kMfWaves);
     const dim3 grid(blocks_for(B, 64 * kMfWaves), (O + 32 * tiles - 1) / (32 * tiles));
     if (tiles == 4) {
         if (D.thr53)
-            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 4>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
-                               O, D, layer);
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 4, TA>), grid, block, 0, s, in, wt, bias, zb, z, a, B,
+                               K, O, D, layer);
         else
-            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 4>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
-                               O, D, layer);
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 4, TA>), grid, block, 0, s, in, wt, bias, zb, z, a, B,
+                               K, O, D, layer);
     } else {
         if (D.thr53)
-            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 1>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
-                               O, D, layer);
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, true, 1, TA>), grid, block, 0, s, in, wt, bias, zb, z, a, B,
+                               K, O, D, layer);
         else
-            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 1>), grid, block, 0, s, in, wt, bias, zb, z, a, B, K,
-                               O, D, layer);
+            hipLaunchKernelGGL((dense_mfma_kernel<BF, MODE, false, 1, TA>), grid, block, 0, s, in, wt, bias, zb, z, a, B,
+                               K, O, D, layer);
     }
 }
 
@@ -811,9 +835,9 @@ __device__ __forceinline__ float head_delta(const float* __restrict__ g, float w
     return BF ? q_bf16(v) : v;
 }
 
-template <bool BF, bool VEC>
+template <bool BF, bool VEC, typename TA = float>
 __global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict__ g, const float* __restrict__ w,
-                                                         const uint64_t* __restrict__ zb, float* __restrict__ dl,
+                                                         const uint64_t* __restrict__ zb, TA* __restrict__ dl,
                                                          int32_t B, DropArgs D, int layer) {
     constexpr int S = VEC ? 4 : 1;
     const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * S;
@@ -822,12 +846,20 @@ __global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict
     const float wj = w[j];
     const uint64_t word = zb[(int64_t)j * mask_words(B) + (b >> 6)];     // the S samples share it
     const int64_t t = (int64_t)j * B + b;
-    if constexpr (VEC) {
+    if constexpr (VEC && std::is_same<TA, float>::value) {
         *reinterpret_cast<float4*>(dl + t) =
             make_float4(head_delta<BF>(g, wj, word, b, j, D, layer), head_delta<BF>(g, wj, word, b + 1, j, D, layer),
                         head_delta<BF>(g, wj, word, b + 2, j, D, layer), head_delta<BF>(g, wj, word, b + 3, j, D, layer));
+    } else if constexpr (VEC) {
+        bf16s_t h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) st_act(h, e, head_delta<BF>(g, wj, word, b + e, j, D, layer));
+        uint2 pk;
+        pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        *reinterpret_cast<uint2*>(dl + t) = pk;
     } else {
-        dl[t] = head_delta<BF>(g, wj, word, b, j, D, layer);
+        st_act(dl, t, head_delta<BF>(g, wj, word, b, j, D, layer));
     }
 }
 
@@ -910,6 +942,22 @@ __device__ __forceinline__ bf16x8_t pack_bf16x8(const float (&v)[8]) {
     return out;
 }
 
+// Eight consecutive bf16 values from bf16 storage (VEC: one 16-byte load).
+template <bool VEC>
+__device__ __forceinline__ bf16x8_t load_frag(const bf16s_t* __restrict__ row, int64_t k, int64_t ke, bool valid) {
+    bf16x8_t out;
+    if (VEC && valid && k + 8 <= ke) {
+        const uint4 p = *reinterpret_cast<const uint4*>(row + k);
+        __builtin_memcpy(&out, &p, sizeof out);
+    } else {
+        uint16_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (valid && k + j < ke) ? row[k + j] : (uint16_t)0;
+        __builtin_memcpy(&out, v, sizeof out);
+    }
+    return out;
+}
+
 template <bool VEC>
 __device__ __forceinline__ bf16x8_t load_frag(const float* __restrict__ row, int64_t k, int64_t ke, bool valid) {
     float v[8];
@@ -930,8 +978,8 @@ __device__ __forceinline__ bf16x8_t load_frag(const float* __restrict__ row, int
 constexpr int kWgradKs = 2;
 
 // blockIdx.y = a range of NT n-tiles (the bias column with the first range).
-template <int NT, bool VEC>
-__global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
+template <int NT, bool VEC, typename TA = float, typename TB = float>
+__global__ __launch_bounds__(512) void wgrad_mfma_kernel(const TA* __restrict__ A, const TB* __restrict__ Bt,
                                                          float* __restrict__ part, int M, int N, int32_t B,
                                                          int64_t chunk) {
     const int n0 = (int)blockIdx.y * NT * 32;
@@ -948,9 +996,9 @@ __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict
     const int64_t ke = min(kb + chunk, (int64_t)B);
     const int m = mt * 32 + row;
     const bool mvalid = m < M;
-    const float* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
+    const TA* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
     // the fragment lanes this thread stages: (k-step, n-tile, lane) = f
-    const float* __restrict__ srow[EPT];
+    const TB* __restrict__ srow[EPT];
     bool sval[EPT];
     int soff[EPT];
 #pragma unroll
@@ -1021,8 +1069,8 @@ __global__ __launch_bounds__(512) void wgrad_mfma_kernel(const float* __restrict
 
 // A single m-tile (the head layer): one wave, no sharing, fragments straight
 // from memory.
-template <int NT, bool VEC>
-__global__ __launch_bounds__(64) void wgrad_direct_kernel(const float* __restrict__ A, const float* __restrict__ Bt,
+template <int NT, bool VEC, typename TA = float, typename TB = float>
+__global__ __launch_bounds__(64) void wgrad_direct_kernel(const TA* __restrict__ A, const TB* __restrict__ Bt,
                                                          float* __restrict__ part, int M, int N, int32_t B,
                                                          int64_t chunk) {
     const int lane = threadIdx.x & 63, mt = 0;
@@ -1032,8 +1080,8 @@ __global__ __launch_bounds__(64) void wgrad_direct_kernel(const float* __restric
     const int64_t ke = min(kb + chunk, (int64_t)B);
     const int m = mt * 32 + row;
     const bool mvalid = m < M;
-    const float* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
-    const float* __restrict__ brow[NT];
+    const TA* __restrict__ arow = A + (int64_t)(mvalid ? m : 0) * B;
+    const TB* __restrict__ brow[NT];
     bool nvalid[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -1115,24 +1163,34 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int S, int M
 }
 
 // NT n-tiles per workgroup, ny workgroups across N (matrix-core path only).
-template <int NT>
-static void launch_wgrad_nt(const float* A, const float* Bt, float* part, int M, int N, int32_t B, int S,
+template <int NT, typename TA, typename TB>
+static void launch_wgrad_nt(const TA* A, const TB* Bt, float* part, int M, int N, int32_t B, int S,
                             int64_t chunk, int ny, hipStream_t s) {
-    const bool vec = B % 4 == 0;
+    // 16-byte rows: 4 fp32 or 8 bf16 values
+    const bool vec = B % (std::is_same<TA, float>::value && std::is_same<TB, float>::value ? 4 : 8) == 0;
     if (M <= 32) {
-        if (vec) hipLaunchKernelGGL((wgrad_direct_kernel<NT, true>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
-        else hipLaunchKernelGGL((wgrad_direct_kernel<NT, false>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B, chunk);
+        if (vec)
+            hipLaunchKernelGGL((wgrad_direct_kernel<NT, true, TA, TB>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B,
+                               chunk);
+        else
+            hipLaunchKernelGGL((wgrad_direct_kernel<NT, false, TA, TB>), dim3(S), dim3(64), 0, s, A, Bt, part, M, N, B,
+                               chunk);
     } else {
         const dim3 grid((uint32_t)S, (uint32_t)ny);
-        if (vec) hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true>), grid, dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
-        else hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false>), grid, dim3(512), 0, s, A, Bt, part, M, N, B, chunk);
+        if (vec)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<NT, true, TA, TB>), grid, dim3(512), 0, s, A, Bt, part, M, N, B,
+                               chunk);
+        else
+            hipLaunchKernelGGL((wgrad_mfma_kernel<NT, false, TA, TB>), grid, dim3(512), 0, s, A, Bt, part, M, N, B,
+                               chunk);
     }
 }
 
 // dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.  With
 // fewer sample chunks than CUs the n-tiles are split over two workgroups per
 // chunk (each reads the chunk's A rows, half of its Bt rows).
-static hipError_t weight_grad_mfma(const float* A, const float* Bt, int M, int N, int32_t B, float* part,
+template <typename TA, typename TB>
+static hipError_t weight_grad_mfma(const TA* A, const TB* Bt, int M, int N, int32_t B, float* part,
                                    float* gw, float* gb, int n_cu, hipStream_t s) {
     const WgradPlan p = wgrad_plan(B, M);
     const int tiles = (N + 31) / 32;
@@ -1272,7 +1330,7 @@ static void forward_rows(const ModelDims& m, const float* compute, const float* 
         const int K = m.in_of(l), O = m.h[l];
         const int tiles = lds_w ? dense_mfma(m, B, O) : 0;
         if (tiles) {
-            launch_dense_mfma<BF, kFwdRelu>(tiles, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l],
+            launch_dense_mfma<BF, kFwdRelu, float>(tiles, in, compute + m.c_wt[l], compute + m.c_bl[l], zb[l], nullptr, a[l],
                                             B, K, O, D, l, s);
         } else if (lds_w && dense_small(B, O)) {
             if (zb[l]) (void)launch_fill_u64(zb[l], 0ull, (int64_t)O * mask_words(B), s);   // bits set by atomics
@@ -1392,6 +1450,52 @@ hipError_t launch_score_generic(const ModelDims& m, const float* compute, const 
 // ---------------------------------------------------------------------------
 // the step
 // ---------------------------------------------------------------------------
+// bf16 models whose hidden layers all run on the matrix-core chains (and B a
+// multiple of 8, for 16-byte fragment loads): the same step, with the saved
+// normalised inputs, activations and layer gradients stored as bf16 bits.
+static hipError_t run_update_b16(const ModelDims& m, float* master, float* compute, const float* mu, const float* isig,
+                                 int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
+                                 float* grad_out, const UpdWs& w, const DropArgs& D, int n_cu, hipStream_t s) {
+    const int64_t nB = B;
+    const int L = m.L;
+    bf16s_t* xn = reinterpret_cast<bf16s_t*>(w.xn);
+    bf16s_t *a[3] = {}, *dl[3] = {};
+    for (int l = 0; l < L; ++l) {
+        a[l] = reinterpret_cast<bf16s_t*>(w.a[l]);
+        dl[l] = reinterpret_cast<bf16s_t*>(w.dl[l]);
+    }
+    hipLaunchKernelGGL((normalize_kernel<true, bf16s_t>), dim3(blocks_for(nB, 64), (m.d + 63) / 64), dim3(256), 0, s,
+                       feats, mu, isig, xn, B, m.d);
+    for (int l = 0; l < L; ++l)
+        launch_dense_mfma<true, kFwdRelu, bf16s_t>(dense_mfma(m, B, m.h[l]), l == 0 ? xn : a[l - 1],
+                                                   compute + m.c_wt[l], compute + m.c_bl[l], w.zb[l], nullptr, a[l], B,
+                                                   m.in_of(l), m.h[l], D, l, s);
+    hipLaunchKernelGGL((dense_small_kernel<true, kFwdHead, bf16s_t>), dim3(1, blocks_for(nB, 256)), dim3(256), 0, s,
+                       a[L - 1], compute + m.c_wt[L], compute + m.c_bl[L], nullptr, w.t, nullptr, B, m.hl, 1, D, L);
+    hipLaunchKernelGGL(loss_grad_kernel<true>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
+    if (loss_out)
+        hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, s, w.loss_part, w.loss_blocks, B, loss_out);
+    hipError_t e = weight_grad_mfma(w.g, (const bf16s_t*)a[L - 1], 1, m.hl, B, w.part, w.grad + m.m_w[L],
+                                    w.grad + m.m_b[L], n_cu, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((delta_head_kernel<true, true, bf16s_t>), dim3(blocks_for(nB, 1024), m.hl), dim3(256), 0, s,
+                       w.g, compute + m.c_wt[L], w.zb[L - 1], dl[L - 1], B, D, L - 1);
+    for (int l = L - 1; l >= 0; --l) {
+        e = weight_grad_mfma((const bf16s_t*)dl[l], (const bf16s_t*)(l == 0 ? xn : a[l - 1]), m.h[l], m.in_of(l), B,
+                             w.part, w.grad + m.m_w[l], w.grad + m.m_b[l], n_cu, s);
+        if (e != hipSuccess) return e;
+        if (l == 0) break;
+        launch_dense_mfma<true, kBackprop, bf16s_t>(dense_mfma(m, B, m.h[l - 1]), dl[l], compute + m.c_wt[l], nullptr,
+                                                    w.zb[l - 1], dl[l - 1], nullptr, B, m.h[l], m.h[l - 1], D, l - 1,
+                                                    s);
+    }
+    hipLaunchKernelGGL(sgd_kernel, dim3(blocks_for(m.n_params, 256)), dim3(256), 0, s, master, w.grad, lr,
+                       m.n_params, grad_out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_refresh_compute_copy(m, master, compute, s);
+}
+
 template <bool BF>
 static hipError_t run_update(const ModelDims& m, float* master, float* compute, const float* mu, const float* isig,
                              int32_t B, const float* feats, const float* ttft, float lr, float* loss_out,
@@ -1399,15 +1503,18 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
     UpdWs w = plan_ws(m, B, reinterpret_cast<char*>(workspace));
     const int64_t nB = B;
     const int L = m.L;
-    // forward, saving pre-activations and activations (dropout applied)
-    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.zb, w.a, w.t, D, s);
-    const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
     bool lds_w = m.d <= kDenseMaxK;
     bool mf = BF && m.d <= 256;          // bf16 operands: weight and bias gradients on the matrix cores
     for (int l = 0; l < L; ++l) {
         lds_w = lds_w && m.h[l] <= kDenseMaxK;
         mf = mf && m.h[l] <= 256;
     }
+    bool b16 = BF && mf && lds_w && B % 8 == 0 && dense_small(B, 1);
+    for (int l = 0; l < L; ++l) b16 = b16 && dense_mfma(m, B, m.h[l]) > 0;
+    if (b16) return run_update_b16(m, master, compute, mu, isig, B, feats, ttft, lr, loss_out, grad_out, w, D, n_cu, s);
+    // forward, saving pre-activations and activations (dropout applied)
+    forward_rows<BF>(m, compute, mu, isig, B, feats, w.xn, w.zb, w.a, w.t, D, s);
+    const uint32_t sbd = blocks_for(nB, 256 * kDenseSpl);
     // loss and output gradient
     hipLaunchKernelGGL(loss_grad_kernel<BF>, dim3(w.loss_blocks), dim3(256), 0, s, w.t, ttft, w.g, w.loss_part, B);
     if (loss_out)
@@ -1443,7 +1550,7 @@ static hipError_t run_update(const ModelDims& m, float* master, float* compute, 
         const int Kp = m.h[l - 1];
         const int tiles = lds_w ? dense_mfma(m, B, Kp) : 0;
         if (tiles)
-            launch_dense_mfma<BF, kBackprop>(tiles, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1],
+            launch_dense_mfma<BF, kBackprop, float>(tiles, w.dl[l], compute + m.c_wt[l], nullptr, w.zb[l - 1], w.dl[l - 1],
                                              nullptr, B, O, Kp, D, l - 1, s);
         else if (lds_w && dense_small(B, Kp))
             hipLaunchKernelGGL((dense_small_kernel<BF, kBackprop>), dim3((Kp + 63) / 64, blocks_for(nB, 4)), dim3(256),
