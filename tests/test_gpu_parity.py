@@ -768,6 +768,9 @@ def test_abi_errors_on_device():
     assert lib.ls_load_cache_state(ctx.h, 2, bad_off.ctypes.data_as(P), ptr(req_h), None) == lodestar.LS_ERR_INVALID
     assert lib.ls_update(ctx.h, 0, ptr(feat), ptr(feat), 0.1, None, None, None) == lodestar.LS_ERR_INVALID
     assert lib.ls_update(ctx.h, 4, ptr(feat), ptr(feat), float("nan"), None, None, None) == lodestar.LS_ERR_INVALID
+    assert lib.ls_set_chain_kernels(ctx.h, 2) == lodestar.LS_ERR_INVALID
+    assert lib.ls_set_chain_kernels(ctx.h, -1) == lodestar.LS_ERR_INVALID
+    assert lib.ls_set_chain_kernels(None, 0) == lodestar.LS_ERR_INVALID
     # the context still works after rejected calls
     ctx.ls_score_batch(req_off, req_h, plen, feat, chosen)
     torch.cuda.synchronize()
