@@ -178,10 +178,16 @@ constexpr int64_t kRunPosTag = (int64_t)1 << 62;
 // Segment (global index) of every key of the chunk, and the key appended to
 // that segment's run.  The workgroup first finds the instances its chunk spans
 // (one parallel pass over the offsets) and copies their offsets, first
-// segments and bucket counts to LDS; a thread then takes 8 consecutive keys and
-// walks the instance boundaries from its first key.  The all-ones key sets its
-// instance's flag instead (and records its position in eidx).
-template <bool IDX>
+// segments and bucket counts to LDS; a thread then takes PER consecutive keys
+// and walks the instance boundaries from its first key.  The all-ones key sets
+// its instance's flag instead (and records its position in eidx).
+//
+// STAGE (builds without a slot map): the chunk's keys are first gathered in
+// LDS ordered by segment (the counts' prefix sums plus each key's rank), then
+// written out with consecutive threads on consecutive slots of each run, so
+// the run writes are coalesced instead of one scattered 8-byte store per key.
+// Every key lands in the slot the direct write would give it.
+template <bool IDX, int PER, bool STAGE>
 __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __restrict__ hashes,
                                                             const int64_t* __restrict__ inst_off,
                                                             const int32_t* __restrict__ seg_off,
@@ -193,23 +199,30 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
                                                             uint32_t* __restrict__ flags, int64_t* __restrict__ eidx,
                                                             int64_t* __restrict__ ovf, uint32_t* __restrict__ ovf_count,
                                                             uint32_t ovf_cap) {
-    __shared__ uint32_t bin[kPartBins];
+    static_assert(!(STAGE && IDX), "staging keeps no input positions");
+    constexpr int64_t CH = (int64_t)kPartThreads * PER;
+    constexpr int BINS = STAGE ? kPartThreads : kPartBins;        // staging: one bin per thread for the scan
+    __shared__ uint32_t bin[BINS];
     __shared__ int64_t l_off[kPartInst + 1];
     __shared__ int32_t l_seg[kPartInst + 1];
     __shared__ uint32_t l_nb[kPartInst];
     __shared__ int64_t l_base[kPartInst];
     __shared__ int32_t i_first, i_last;
+    __shared__ uint64_t stage_k[STAGE ? CH : 1];                  // keys ordered by segment
+    __shared__ uint16_t stage_s[STAGE ? CH : 1];                  // their local segment
+    __shared__ uint32_t lofs[STAGE ? BINS : 1];                   // first staged slot of each local segment
+    __shared__ uint32_t wsum[kPartThreads / 64];
     const int64_t n_keys = inst_off[n_inst] < total ? inst_off[n_inst] : total;
-    const int64_t c0 = (int64_t)blockIdx.x * kPartChunk;
+    const int64_t c0 = (int64_t)blockIdx.x * CH;
     if (c0 >= n_keys) return;                                     // uniform
-    const int64_t c1 = c0 + kPartChunk < n_keys ? c0 + kPartChunk : n_keys;
+    const int64_t c1 = c0 + CH < n_keys ? c0 + CH : n_keys;
     // the instances holding positions c0 and c1 - 1 (each owned by exactly one non-empty instance)
     for (int32_t i = threadIdx.x; i < n_inst; i += kPartThreads) {
         const int64_t a = inst_off[i], b = inst_off[i + 1];
         if (a <= c0 && c0 < b) i_first = i;
         if (a <= c1 - 1 && c1 - 1 < b) i_last = i;
     }
-    for (int x = threadIdx.x; x < kPartBins; x += kPartThreads) bin[x] = 0u;
+    for (int x = threadIdx.x; x < BINS; x += kPartThreads) bin[x] = 0u;
     __syncthreads();
     const int32_t ilo = i_first, ihi = i_last;
     const bool in_lds = ihi - ilo < kPartInst;
@@ -225,15 +238,15 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
     }
     __syncthreads();
     const int32_t seg_lo = seg_off[ilo];
-    const bool local = seg_off[ihi + 1] - seg_lo <= kPartBins;
-    const int64_t t0 = c0 + (int64_t)threadIdx.x * kPartPerThread;
-    uint64_t key[kPartPerThread];
-    int32_t seg[kPartPerThread];
-    uint32_t rank[kPartPerThread];
-    int64_t run0[kPartPerThread];      // the segment's run: first slot and length in slots
-    uint32_t runcap[kPartPerThread];
+    const bool local = seg_off[ihi + 1] - seg_lo <= BINS;
+    const int64_t t0 = c0 + (int64_t)threadIdx.x * PER;
+    uint64_t key[PER];
+    int32_t seg[PER];
+    uint32_t rank[PER];
+    int64_t run0[PER];                 // the segment's run: first slot and length in slots
+    uint32_t runcap[PER];
 #pragma unroll
-    for (int u = 0; u < kPartPerThread; ++u) key[u] = t0 + u < c1 ? hashes[t0 + u] : kEmptyKey;
+    for (int u = 0; u < PER; ++u) key[u] = t0 + u < c1 ? hashes[t0 + u] : kEmptyKey;
     // instance of the first key, relative to ilo when the table is in LDS
     int32_t i = 0;
     if (t0 < c1) {
@@ -249,7 +262,7 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
         }
     }
 #pragma unroll
-    for (int u = 0; u < kPartPerThread; ++u) {
+    for (int u = 0; u < PER; ++u) {
         const int64_t t = t0 + u;
         seg[u] = -1;
         if (t >= c1) continue;
@@ -293,13 +306,69 @@ __global__ __launch_bounds__(kPartThreads) void part_kernel(const uint64_t* __re
     if (!local) return;                                           // uniform
     __syncthreads();
     const int32_t nb_local = seg_off[ihi + 1] - seg_lo;
+    // staging reads the instances' segments from LDS: only when they are there
+    if (STAGE && in_lds) {                                        // uniform
+        // exclusive prefix sum of the counts, one bin per thread (wave scans,
+        // then the waves' totals)
+        const int x = (int)threadIdx.x, lane = x & 63, wv = x >> 6;
+        const uint32_t cnt = x < nb_local ? bin[x] : 0u;
+        uint32_t v = cnt;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(v, off);
+            if (lane >= off) v += y;
+        }
+        if (lane == 63) wsum[wv] = v;
+        __syncthreads();
+        if (wv == 0) {
+            uint32_t w = lane < kPartThreads / 64 ? wsum[lane] : 0u;
+#pragma unroll
+            for (int off = 1; off < kPartThreads / 64; off <<= 1) {
+                const uint32_t y = __shfl_up(w, off);
+                if (lane >= off) w += y;
+            }
+            if (lane < kPartThreads / 64) wsum[lane] = w;
+        }
+        __syncthreads();
+        const uint32_t staged = wsum[kPartThreads / 64 - 1];
+        if (x < nb_local) {
+            lofs[x] = (wv ? wsum[wv - 1] : 0u) + v - cnt;
+            if (cnt != 0u) bin[x] = atomicAdd(&seg_cursor[seg_lo + x], cnt);   // this chunk's first position in the run
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            if (seg[u] < 0) continue;
+            const int ls = seg[u] - seg_lo;
+            const uint32_t at = lofs[ls] + rank[u];
+            stage_s[at] = (uint16_t)ls;
+            stage_k[at] = key[u];
+            if (bin[ls] + rank[u] >= runcap[u]) queue_overflow(t0 + u, true, ovf, ovf_count, ovf_cap);
+        }
+        __syncthreads();
+        for (uint32_t at = threadIdx.x; at < staged; at += kPartThreads) {
+            const int ls = stage_s[at];
+            const uint32_t pos = bin[ls] + (at - lofs[ls]);
+            // the instance holding local segment ls: the last one whose segments start at or before it
+            const int32_t g = seg_lo + ls;
+            int32_t lo = 0, hi = ihi - ilo + 1;
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (l_seg[mid] <= g) lo = mid; else hi = mid;
+            }
+            const uint32_t sl = (uint32_t)(g - l_seg[lo]);
+            const uint32_t cap = min((uint32_t)kSegBuckets, l_nb[lo] - sl * kSegBuckets) * kBucketKeys;
+            if (pos < cap) part_key[(l_base[lo] + (int64_t)sl * kSegBuckets) * kBucketKeys + pos] = stage_k[at];
+        }
+        return;
+    }
     for (int x = threadIdx.x; x < nb_local; x += kPartThreads) {
         const uint32_t cnt = bin[x];
         if (cnt != 0u) bin[x] = atomicAdd(&seg_cursor[seg_lo + x], cnt);   // this chunk's first position in the run
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < kPartPerThread; ++u) {
+    for (int u = 0; u < PER; ++u) {
         if (seg[u] < 0) continue;
         const uint32_t pos = bin[seg[u] - seg_lo] + rank[u];
         if (pos < runcap[u]) {
@@ -507,17 +576,20 @@ hipError_t launch_table_build(const CacheTables& t, const int64_t* inst_off, con
     hipLaunchKernelGGL(seg_inst_kernel, dim3((uint32_t)((n_inst + 255) / 256)), dim3(256), 0, s, seg_off, n_inst,
                        w.seg_inst);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const uint32_t chunks = (uint32_t)((total + kPartChunk - 1) / kPartChunk);
-    if (chunks > 0) {
-        // input positions beside the runs only for a slot map
-        if (entry_of)
-            hipLaunchKernelGGL(part_kernel<true>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
-                               t.nbuckets, t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx,
-                               w.ovf, w.ovf_count, cap);
-        else
-            hipLaunchKernelGGL(part_kernel<false>, dim3(chunks), dim3(kPartThreads), 0, s, hashes, inst_off, seg_off,
-                               t.nbuckets, t.base, n_inst, total, w.run_len, w.part_key, w.part_idx, t.flags, eidx,
-                               w.ovf, w.ovf_count, cap);
+    if (total > 0) {
+        // input positions beside the runs only for a slot map; otherwise the
+        // runs are written through LDS staging, half-size chunks
+        if (entry_of) {
+            constexpr int64_t ch = kPartChunk;
+            hipLaunchKernelGGL((part_kernel<true, kPartPerThread, false>), dim3((uint32_t)((total + ch - 1) / ch)),
+                               dim3(kPartThreads), 0, s, hashes, inst_off, seg_off, t.nbuckets, t.base, n_inst, total,
+                               w.run_len, w.part_key, w.part_idx, t.flags, eidx, w.ovf, w.ovf_count, cap);
+        } else {
+            constexpr int64_t ch = (int64_t)kPartThreads * (kPartPerThread / 2);
+            hipLaunchKernelGGL((part_kernel<false, kPartPerThread / 2, true>), dim3((uint32_t)((total + ch - 1) / ch)),
+                               dim3(kPartThreads), 0, s, hashes, inst_off, seg_off, t.nbuckets, t.base, n_inst, total,
+                               w.run_len, w.part_key, w.part_idx, t.flags, eidx, w.ovf, w.ovf_count, cap);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (n_seg > 0) {
