@@ -504,7 +504,8 @@ int ls_swap_model(ls_ctx* ctx, void* serve_stream, void* train_stream);
  * Per-kernel timing (the library's own view of where the routing time goes;
  * Section 5.4 measures the router's overhead end to end).  While enabled, each
  * kernel launch group of the context is bracketed by HIP events on the stream
- * of its call.  Kinds: "table_build", "prefix_match", "instance_partial",
+ * of its call (events without a system-scope fence: they order nothing and
+ * cost no cache writeback).  Kinds: "table_build", "prefix_match", "instance_partial",
  * "score_pairs", "score_pairs_mfma", "band_select", "rescore", "argmin",
  * "update", "route", "buffer", "index" (prefix-index maintenance).
  *   ls_profile_enable  enable != 0 starts recording (and clears old records).

@@ -403,6 +403,19 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     const uint32_t b0 = s * kSegBuckets;
     const uint32_t nbl = min((uint32_t)kSegBuckets, nb - b0);
     const int tid = threadIdx.x;
+    constexpr int SPT = (int)(kSegSlots / kSegThreads);           // run slots per thread
+    static_assert(kSegSlots % kSegThreads == 0, "a run fills whole rounds of the workgroup");
+
+    // the run, laid out like the segment's slots: every key of the thread is
+    // loaded at once, before the segment is cleared
+    const int64_t r0 = (base[i] + b0) * kBucketKeys;
+    const uint32_t len = min(run_len[L], nbl * (uint32_t)kBucketKeys);
+    uint64_t rk[SPT];
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+        const uint32_t o = (uint32_t)tid + (uint32_t)u * kSegThreads;
+        rk[u] = o < len ? part_key[r0 + o] : kEmptyKey;
+    }
 
     ulonglong2* seg2 = reinterpret_cast<ulonglong2*>(seg);
     const ulonglong2 empty2 = {kEmptyKey, kEmptyKey};
@@ -410,17 +423,18 @@ __global__ __launch_bounds__(kSegThreads) void table_segment_kernel(
     for (uint32_t x = tid; x < nbl; x += kSegThreads) fill[x] = 0u;
     __syncthreads();
 
-    const int64_t r0 = (base[i] + b0) * kBucketKeys;             // the run, laid out like the segment's slots
-    const uint32_t len = min(run_len[L], nbl * (uint32_t)kBucketKeys);
-    const int64_t r1 = r0 + len;
     uint32_t* __restrict__ fp_run = fp + (int64_t)L * kSegSlots;
     if (tid == 0) {
         fp_len[L] = len;
         fp_inst[L] = (uint32_t)i;
     }
-    for (int64_t q = r0 + tid; q < r1; q += kSegThreads) {
-        const uint64_t key = part_key[q];
-        fp_run[q - r0] = key_fp(key);        // every key of the run is cached, placed here or by the global pass
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+        const uint32_t o = (uint32_t)tid + (uint32_t)u * kSegThreads;
+        if (o >= len) continue;
+        const int64_t q = r0 + o;
+        const uint64_t key = rk[u];
+        fp_run[o] = key_fp(key);             // every key of the run is cached, placed here or by the global pass
         const uint32_t lb = bucket_of(key, nb) - b0;
         const int32_t ls = segment_place(seg, fill, lb, nbl, key);
         if (ls < 0) {

@@ -283,8 +283,10 @@ hipEvent_t take_event(ls_ctx* c) {
         c->spare.pop_back();
         return e;
     }
+    // timing only: without the system-scope fence a record costs no L2
+    // writeback, so the events do not stretch the work they bracket
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
