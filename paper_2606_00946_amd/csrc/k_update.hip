@@ -165,6 +165,45 @@ __global__ __launch_bounds__(256) void normalize_kernel(const float* __restrict_
     }
 }
 
+// bf16 storage with B a multiple of 8: the same tiles, written as 16-byte runs
+// of eight consecutive samples of a feature row.  Same values as
+// normalize_kernel.
+__global__ __launch_bounds__(256) void normalize_b16_kernel(const float* __restrict__ feats,
+                                                            const float* __restrict__ mu,
+                                                            const float* __restrict__ isig, bf16s_t* __restrict__ xn,
+                                                            int32_t B, int d) {
+    __shared__ float tile[64][65];                  // [feature][sample]
+    const int64_t b0 = (int64_t)blockIdx.x * 64;
+    const int c0 = (int)blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int c = c0 + tx;
+    const float m_c = c < d ? mu[c] : 0.0f, s_c = c < d ? isig[c] : 0.0f;
+#pragma unroll
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t b = b0 + i;
+        float v = 0.0f;
+        if (b < B && c < d) v = __fmul_rn(__fsub_rn(feats[b * d + c], m_c), s_c);
+        tile[tx][i] = q_bf16(v);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = threadIdx.x; p < 64 * 8; p += 256) {
+        const int j = p >> 3, s8 = (p & 7) * 8;
+        const int cj = c0 + j;
+        const int64_t b = b0 + s8;
+        if (cj >= d || b >= B) continue;            // b + 8 <= B: B and b are multiples of 8
+        bf16s_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) st_act(h, e, tile[j][s8 + e]);
+        uint4 pk;
+        pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        pk.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+        pk.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+        *reinterpret_cast<uint4*>(xn + (int64_t)cj * B + b) = pk;
+    }
+}
+
 // ReLU masks of the hidden layers: the backward pass only needs z > 0 of each
 // pre-activation, so the forward keeps one bit per (unit, sample), bit b & 63
 // of word o * ceil(B / 64) + (b >> 6), instead of z itself (2 MB instead of
@@ -863,6 +902,49 @@ __global__ __launch_bounds__(256) void delta_head_kernel(const float* __restrict
     }
 }
 
+// bf16 storage with B a multiple of 8: eight consecutive samples per thread
+// (g read once, two 16-byte loads) over kDeltaUnits units (one 16-byte store
+// each); blockIdx.y = a group of units.  Same values as delta_head_kernel.
+constexpr int kDeltaUnits = 8;
+
+__global__ __launch_bounds__(256) void delta_head_b16_kernel(const float* __restrict__ g, const float* __restrict__ w,
+                                                             const uint64_t* __restrict__ zb, bf16s_t* __restrict__ dl,
+                                                             int32_t B, int H, DropArgs D, int layer) {
+    const int64_t b = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+    if (b >= B) return;                             // b + 8 <= B: B and b are multiples of 8
+    const float4 ga = *reinterpret_cast<const float4*>(g + b), gb = *reinterpret_cast<const float4*>(g + b + 4);
+    const float gv[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+    const int64_t mw = mask_words(B);
+    const int j0 = (int)blockIdx.y * kDeltaUnits;
+    // every unit's weight and mask word (the eight samples share it) first
+    float wv[kDeltaUnits];
+    uint64_t wd[kDeltaUnits];
+#pragma unroll
+    for (int u = 0; u < kDeltaUnits; ++u) {
+        const int j = j0 + u;
+        wv[u] = j < H ? w[j] : 0.0f;
+        wd[u] = j < H ? zb[(int64_t)j * mw + (b >> 6)] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kDeltaUnits; ++u) {
+        const int j = j0 + u;
+        if (j >= H) continue;
+        bf16s_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int64_t be = b + e;
+            const float v = apply_drop(D, layer, be, j, ((wd[u] >> (be & 63)) & 1ull) ? gv[e] * wv[u] : 0.0f);
+            st_act(h, e, q_bf16(v));
+        }
+        uint4 pk;
+        pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        pk.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+        pk.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+        *reinterpret_cast<uint4*>(dl + (int64_t)j * B + b) = pk;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // C_part[s][m][n] = sum_{b in chunk s} A[m][b] * Bt[n][b]   (A [M x B], Bt [N x B])
 // 64 x 64 tile per block, 4 x 4 per thread, slabs of 16 samples through LDS.
@@ -1464,8 +1546,8 @@ static hipError_t run_update_b16(const ModelDims& m, float* master, float* compu
         a[l] = reinterpret_cast<bf16s_t*>(w.a[l]);
         dl[l] = reinterpret_cast<bf16s_t*>(w.dl[l]);
     }
-    hipLaunchKernelGGL((normalize_kernel<true, bf16s_t>), dim3(blocks_for(nB, 64), (m.d + 63) / 64), dim3(256), 0, s,
-                       feats, mu, isig, xn, B, m.d);
+    hipLaunchKernelGGL(normalize_b16_kernel, dim3(blocks_for(nB, 64), (m.d + 63) / 64), dim3(256), 0, s, feats, mu,
+                       isig, xn, B, m.d);
     for (int l = 0; l < L; ++l)
         launch_dense_mfma<true, kFwdRelu, bf16s_t>(dense_mfma(m, B, m.h[l]), l == 0 ? xn : a[l - 1],
                                                    compute + m.c_wt[l], compute + m.c_bl[l], w.zb[l], nullptr, a[l], B,
@@ -1478,8 +1560,8 @@ static hipError_t run_update_b16(const ModelDims& m, float* master, float* compu
     hipError_t e = weight_grad_mfma(w.g, (const bf16s_t*)a[L - 1], 1, m.hl, B, w.part, w.grad + m.m_w[L],
                                     w.grad + m.m_b[L], n_cu, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((delta_head_kernel<true, true, bf16s_t>), dim3(blocks_for(nB, 1024), m.hl), dim3(256), 0, s,
-                       w.g, compute + m.c_wt[L], w.zb[L - 1], dl[L - 1], B, D, L - 1);
+    hipLaunchKernelGGL(delta_head_b16_kernel, dim3(blocks_for(nB, 2048), (m.hl + kDeltaUnits - 1) / kDeltaUnits),
+                       dim3(256), 0, s, w.g, compute + m.c_wt[L], w.zb[L - 1], dl[L - 1], B, m.hl, D, L - 1);
     for (int l = L - 1; l >= 0; --l) {
         e = weight_grad_mfma((const bf16s_t*)dl[l], (const bf16s_t*)(l == 0 ? xn : a[l - 1]), m.h[l], m.in_of(l), B,
                              w.part, w.grad + m.m_w[l], w.grad + m.m_b[l], n_cu, s);

@@ -78,11 +78,13 @@ def head_magnitude(w, rows):
 class GpuRun:
     """A context loaded with one workload's model and cache state."""
 
-    def __init__(self, w, dtype=None, params=None, exact=False, prefix_join=0, prefix_closed=False):
+    def __init__(self, w, dtype=None, params=None, exact=False, prefix_join=0, prefix_closed=False, profile=False):
         import torch
         self.w = w
         cfg = w.cfg
         self.ctx = lodestar.Context(cfg.d, cfg.hidden, dtype or cfg.dtype)
+        if profile:
+            self.ctx.ls_profile_enable(True)
         self.exact = exact
         if exact:
             self.ctx.ls_set_exact_scores(True)
