@@ -98,9 +98,13 @@ struct ls_ctx {
     bool stage_pending = false;
     // optional per-kernel timing
     bool profiling = false;
-    struct Rec { int kind; hipEvent_t start, stop; };
+    // shared_start: the start is the stop of the record before it (its
+    // owner), so it is released and destroyed with that record only
+    struct Rec { int kind; hipEvent_t start, stop; bool shared_start; };
     std::vector<Rec> recs;
     std::vector<hipEvent_t> spare;
+    hipEvent_t last_stop = nullptr;          // stop of the group timed last, while the next may follow it
+    hipStream_t last_stop_stream = nullptr;
 };
 
 // Scratch of the allocation-free scoring entry point: one array per GPU,
@@ -290,22 +294,35 @@ hipEvent_t take_event(ls_ctx* c) {
     return e;
 }
 
-// Brackets one launch group with events when profiling is on.
+// Brackets one launch group with events when profiling is on.  A group that
+// follows another on the same stream with nothing enqueued between them
+// (`follows`) starts at the other's stop event instead of a new one: one
+// event per boundary, each event record costing the stream a short idle gap.
 struct Timed {
     ls_ctx* c;
     int kind;
     hipStream_t s;
     hipEvent_t start = nullptr;
-    Timed(ls_ctx* c_, int kind_, hipStream_t s_) : c(c_), kind(kind_), s(s_) {
-        if (c->profiling && (start = take_event(c)) != nullptr) (void)hipEventRecord(start, s);
+    bool shared = false;
+    Timed(ls_ctx* c_, int kind_, hipStream_t s_, bool follows = false) : c(c_), kind(kind_), s(s_) {
+        if (!c->profiling) return;
+        if (follows && c->last_stop && c->last_stop_stream == s) {
+            start = c->last_stop;
+            shared = true;
+        } else if ((start = take_event(c)) != nullptr) {
+            (void)hipEventRecord(start, s);
+        }
+        c->last_stop = nullptr;
     }
     void done() {
         if (!start) return;
         hipEvent_t stop = take_event(c);
         if (stop && hipEventRecord(stop, s) == hipSuccess) {
-            c->recs.push_back({kind, start, stop});
+            c->recs.push_back({kind, start, stop, shared});
+            c->last_stop = stop;
+            c->last_stop_stream = s;
         } else {
-            c->spare.push_back(start);
+            if (!shared) c->spare.push_back(start);
             if (stop) c->spare.push_back(stop);
         }
         start = nullptr;
@@ -315,6 +332,15 @@ struct Timed {
 #define LS_TIMED(ctx, kind, s, expr)        \
     do {                                     \
         Timed t_((ctx), (kind), (s));        \
+        hipError_t e2_ = (expr);             \
+        t_.done();                           \
+        LS_HIP((ctx), e2_);                  \
+    } while (0)
+
+// A group enqueued right after the timed group before it, on the same stream.
+#define LS_TIMED_NEXT(ctx, kind, s, expr)    \
+    do {                                     \
+        Timed t_((ctx), (kind), (s), true);  \
         hipError_t e2_ = (expr);             \
         t_.done();                           \
         LS_HIP((ctx), e2_);                  \
@@ -467,7 +493,7 @@ void ls_destroy(ls_ctx* c) {
         for (hipEvent_t e : c->swap_ev)
             if (e) (void)hipEventDestroy(e);
         for (auto& r : c->recs) {
-            (void)hipEventDestroy(r.start);
+            if (!r.shared_start) (void)hipEventDestroy(r.start);
             (void)hipEventDestroy(r.stop);
         }
         for (hipEvent_t e : c->spare) (void)hipEventDestroy(e);
@@ -808,7 +834,7 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
         out->band = nullptr;
         return LS_OK;
     }
-    LS_TIMED(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
+    LS_TIMED_NEXT(c, K_PARTIAL, s, ls::launch_instance_partial(m, c->compute, c->mu, c->isig, inst_feat, N, part_t, s));
     if (fast) {
         float* eb = w.take<float>(pairs);
         uint8_t* flags = w.take<uint8_t>(pairs);
@@ -816,30 +842,34 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
         int64_t* list = w.take<int64_t>(pairs);
         uint32_t* count = w.take<uint32_t>(64);       // [0]: stage-1 candidates (R), [32]: stage 2
         if (!w.ok()) return fail(c, LS_ERR_NOMEM, "%s", undersized);
-        LS_TIMED(c, K_SCORE_MFMA, s,
-                 ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N, req_off,
-                                             prompt_len, ov, sc, eb, c->n_cu, s));
+        LS_TIMED_NEXT(c, K_SCORE_MFMA, s,
+                      ls::launch_score_pairs_mfma(m, c->frag16, c->frag32, c->compute, part_t, c->mu, c->isig, R, N,
+                                                  req_off, prompt_len, ov, sc, eb, c->n_cu, s));
         // stage 1: every request's fast argmin, rescored; stage 2: what can still beat it
         const ls::FillOp fills[2] = {{count, (uint64_t)(uint32_t)R, 1, 4}, {count + 32, 0u, 1, 4}};
-        LS_TIMED(c, K_BAND, s, ls::launch_fill_multi(fills, 2, s));
-        LS_TIMED(c, K_BAND, s, ls::launch_band_lead(R, N, sc, lead, s));
-        LS_TIMED(c, K_RESCORE, s,
-                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, lead, count,
-                                    sc, c->n_cu, s));
-        LS_TIMED(c, K_BAND, s,
-                 ls::launch_band_rest(R, N, sc, eb, sc, lead, delta, k_filter, stats, req_off, req_hashes, flags, list,
-                                      count + 32, s));
-        LS_TIMED(c, K_RESCORE, s,
+        auto lead_pass = [&]() {
+            hipError_t e = ls::launch_fill_multi(fills, 2, s);
+            return e != hipSuccess ? e : ls::launch_band_lead(R, N, sc, lead, s);
+        };
+        LS_TIMED_NEXT(c, K_BAND, s, lead_pass());
+        LS_TIMED_NEXT(c, K_RESCORE, s,
+                      ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, lead,
+                                         count, sc, c->n_cu, s));
+        LS_TIMED_NEXT(c, K_BAND, s,
+                      ls::launch_band_rest(R, N, sc, eb, sc, lead, delta, k_filter, stats, req_off, req_hashes, flags,
+                                           list, count + 32, s));
+        LS_TIMED_NEXT(c, K_RESCORE, s,
                  ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list,
                                     count + 32, sc, c->n_cu, s));
         band = flags;
     } else if (m.mfma_chains && ls::chain_mfma_supported(m)) {
-        LS_TIMED(c, K_SCORE, s,
-                 ls::launch_score_chain_mfma(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov,
-                                             nullptr, nullptr, c->n_cu, sc, s));
+        LS_TIMED_NEXT(c, K_SCORE, s,
+                      ls::launch_score_chain_mfma(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov,
+                                                  nullptr, nullptr, c->n_cu, sc, s));
     } else {
-        LS_TIMED(c, K_SCORE, s,
-                 ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc, s));
+        LS_TIMED_NEXT(c, K_SCORE, s,
+                      ls::launch_score_pairs(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, sc,
+                                             s));
     }
     out->ov = ov;
     out->sc = sc;
@@ -867,9 +897,9 @@ int ls_score_batch(ls_ctx* c, int32_t R, int32_t N, const int64_t* req_off, cons
     rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, overlap, scores, fast, -1.0, 0, nullptr,
                       s, &out);
     if (rc) return rc;
-    LS_TIMED(c, K_ARGMIN, s,
-             ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov, inst_feat, chosen, min_ttft,
-                               feat_out, s));
+    LS_TIMED_NEXT(c, K_ARGMIN, s,
+                  ls::launch_argmin(c->dims, R, N, out.sc, out.band, req_off, prompt_len, out.ov, inst_feat, chosen,
+                                    min_ttft, feat_out, s));
     return LS_OK;
 }
 
@@ -1021,7 +1051,7 @@ int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const 
     rc = run_pipeline(c, w, R, N, req_off, req_hashes, prompt_len, inst_feat, nullptr, nullptr, fast, pol->delta,
                       pol->k_filter, st, s, &out);
     if (rc) return rc;
-    LS_TIMED(c, K_ROUTE, s,
+    LS_TIMED_NEXT(c, K_ROUTE, s,
              ls::launch_route(P, st, cnt, m, R, N, req_off, req_hashes, prompt_len, out.ov, out.sc, out.band, inst_feat,
                               rnd, chosen, status, heur, feat_out, s));
     return LS_OK;
@@ -1082,12 +1112,15 @@ int ls_update(ls_ctx* c, int32_t B, const float* feats, const float* ttft, float
     if (c->drop_p > 0.0 && B >= (1 << 24)) return fail(c, LS_ERR_INVALID, "B must be below 2^24 with dropout");
     const ls::DropArgs D = next_drop(c);
     const ModelSlot M = train_model(c);
-    LS_TIMED(c, K_UPDATE, s,
-             ls::launch_update(c->dims, M.master, M.compute, c->mu, c->isig, B, feats, ttft, lr, loss_out, grad_out,
-                               c->upd_ws, D, c->n_cu, s));
-    if (M.frag16)
-        LS_TIMED(c, K_UPDATE, s,
-                 ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), M.master, M.frag16, M.frag32, s));
+    // the step and the refresh of the matrix-core fragments, timed as one group
+    auto step = [&]() {
+        hipError_t e = ls::launch_update(c->dims, M.master, M.compute, c->mu, c->isig, B, feats, ttft, lr, loss_out,
+                                         grad_out, c->upd_ws, D, c->n_cu, s);
+        if (e == hipSuccess && M.frag16)
+            e = ls::launch_prepare_mfma(ls::make_mfma_layout(c->dims), M.master, M.frag16, M.frag32, s);
+        return e;
+    };
+    LS_TIMED(c, K_UPDATE, s, step());
     return LS_OK;
 }
 
@@ -1352,11 +1385,12 @@ int ls_profile_enable(ls_ctx* c, int enable) {
     if (!c->recs.empty()) {
         LS_HIP(c, hipDeviceSynchronize());
         for (auto& r : c->recs) {
-            c->spare.push_back(r.start);
+            if (!r.shared_start) c->spare.push_back(r.start);
             c->spare.push_back(r.stop);
         }
         c->recs.clear();
     }
+    c->last_stop = nullptr;
     c->profiling = enable != 0;
     return LS_OK;
 }
