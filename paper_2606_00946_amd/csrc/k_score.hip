@@ -113,32 +113,76 @@ hipError_t launch_refresh_compute_copy(const ModelDims& m, const float* master, 
 }
 
 // ---------------------------------------------------------------------------
-// layer-1 instance partials: part_t[k][i] = chain over the instance columns
+// layer-1 instance partials: part_t[k][i] = chain from b1[k] over the
+// instance columns in ascending order.  A workgroup takes kPartInsts
+// instances: their normalised columns go to LDS once per chunk of kPartCols
+// columns, and each thread runs one unit's chains for all of them (independent
+// chains; the unit's weights read eight columns ahead).
 // ---------------------------------------------------------------------------
+constexpr int kPartInsts = 8;
+constexpr int kPartCols = 256;
+
 template <bool BF>
-__global__ void instance_partial_kernel(const float* __restrict__ w1, const float* __restrict__ b1,
-                                        const float* __restrict__ mu, const float* __restrict__ isig,
-                                        const float* __restrict__ inst_feat, int d, int d_inst, int h1, int32_t N,
-                                        float* __restrict__ part_t) {
-    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)h1 * N) return;
-    int64_t k = t / N, i = t - k * N;
-    float acc = b1[k];
-    const float* __restrict__ row = inst_feat + i * d_inst;
-    const float* __restrict__ w = w1 + k * d;
-    for (int c = 0; c < d_inst; ++c) {
-        float x = __fmul_rn(__fsub_rn(row[c], mu[c]), isig[c]);
-        if (BF) x = bf16_rne(x);
-        acc = __builtin_fmaf(w[c], x, acc);
+__global__ __launch_bounds__(256) void instance_partial_kernel(const float* __restrict__ w1,
+                                                               const float* __restrict__ b1,
+                                                               const float* __restrict__ mu,
+                                                               const float* __restrict__ isig,
+                                                               const float* __restrict__ inst_feat, int d, int d_inst,
+                                                               int h1, int32_t N, float* __restrict__ part_t) {
+    __shared__ float xs[kPartInsts][kPartCols];
+    const int32_t i0 = (int32_t)blockIdx.x * kPartInsts;
+    const int tid = threadIdx.x;
+    for (int kb = 0; kb < h1; kb += 256) {                        // uniform
+        const int k = kb + tid;
+        const bool kval = k < h1;
+        const float* __restrict__ w = w1 + (int64_t)(kval ? k : 0) * d;
+        float acc[kPartInsts];
+        const float bk = kval ? b1[k] : 0.0f;
+#pragma unroll
+        for (int ii = 0; ii < kPartInsts; ++ii) acc[ii] = bk;
+        for (int c0 = 0; c0 < d_inst; c0 += kPartCols) {          // uniform
+            const int nc = min(kPartCols, d_inst - c0);
+            __syncthreads();                                      // the last chunk's reads are done
+            for (int e = tid; e < kPartInsts * kPartCols; e += 256) {
+                const int ii = e / kPartCols, c = e - ii * kPartCols;
+                const int32_t i = i0 + ii;
+                float x = 0.0f;
+                if (i < N && c < nc) {
+                    x = __fmul_rn(__fsub_rn(inst_feat[(int64_t)i * d_inst + c0 + c], mu[c0 + c]), isig[c0 + c]);
+                    if (BF) x = bf16_rne(x);
+                }
+                xs[ii][c] = x;
+            }
+            __syncthreads();
+            int c = 0;
+            for (; c + 8 <= nc; c += 8) {
+                float wc[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) wc[j] = w[c0 + c + j];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+#pragma unroll
+                    for (int ii = 0; ii < kPartInsts; ++ii) acc[ii] = __builtin_fmaf(wc[j], xs[ii][c + j], acc[ii]);
+            }
+            for (; c < nc; ++c) {
+                const float wc = w[c0 + c];
+#pragma unroll
+                for (int ii = 0; ii < kPartInsts; ++ii) acc[ii] = __builtin_fmaf(wc, xs[ii][c], acc[ii]);
+            }
+        }
+        if (kval) {
+#pragma unroll
+            for (int ii = 0; ii < kPartInsts; ++ii)
+                if (i0 + ii < N) part_t[(int64_t)k * N + i0 + ii] = acc[ii];
+        }
     }
-    part_t[t] = acc;
 }
 
 hipError_t launch_instance_partial(const ModelDims& m, const float* compute, const float* mu,
                                    const float* inv_sigma, const float* inst_feat, int32_t N, float* part_t,
                                    hipStream_t s) {
-    int64_t n = (int64_t)m.h1 * N;
-    int64_t grid = (n + 255) / 256;
+    const int64_t grid = ((int64_t)N + kPartInsts - 1) / kPartInsts;
+    if (grid == 0) return hipSuccess;
     if (m.bf16)
         hipLaunchKernelGGL(instance_partial_kernel<true>, dim3((uint32_t)grid), dim3(256), 0, s, compute + m.c_w1,
                            compute + m.c_b1, mu, inv_sigma, inst_feat, m.d, m.d_inst, m.h1, N, part_t);
