@@ -859,8 +859,8 @@ int run_pipeline(ls_ctx* c, WsCarve& w, int32_t R, int32_t N, const int64_t* req
                       ls::launch_band_rest(R, N, sc, eb, sc, lead, delta, k_filter, stats, req_off, req_hashes, flags,
                                            list, count + 32, s));
         LS_TIMED_NEXT(c, K_RESCORE, s,
-                 ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list,
-                                    count + 32, sc, c->n_cu, s));
+                      ls::launch_rescore(m, c->compute, c->mu, c->isig, part_t, R, N, req_off, prompt_len, ov, list,
+                                         count + 32, sc, c->n_cu, s));
         band = flags;
     } else if (m.mfma_chains && ls::chain_mfma_supported(m)) {
         LS_TIMED_NEXT(c, K_SCORE, s,
@@ -1052,8 +1052,8 @@ int ls_route_batch(ls_ctx* c, const ls_policy* pol, int32_t R, int32_t N, const 
                       pol->k_filter, st, s, &out);
     if (rc) return rc;
     LS_TIMED_NEXT(c, K_ROUTE, s,
-             ls::launch_route(P, st, cnt, m, R, N, req_off, req_hashes, prompt_len, out.ov, out.sc, out.band, inst_feat,
-                              rnd, chosen, status, heur, feat_out, s));
+                  ls::launch_route(P, st, cnt, m, R, N, req_off, req_hashes, prompt_len, out.ov, out.sc, out.band,
+                                   inst_feat, rnd, chosen, status, heur, feat_out, s));
     return LS_OK;
 }
 
