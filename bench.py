@@ -55,7 +55,7 @@ KIND_KERNELS = {
     "table_build": (["ls::seg_inst_kernel", "ls::part_kernel", "ls::table_segment_kernel", "ls::table_overflow_kernel"],
                     ["k_cache.hip", "ls_internal.h"]),
     "prefix_match": (["ls::group_insert_kernel", "ls::group_lcp_kernel", "ls::cont_scan_kernel",
-                      "ls::leaders_first_kernel", "ls::leaders_rest_kernel", "ls::prefix_leaders_kernel",
+                      "ls::leaders_first_kernel", "ls::leaders_rest_kernel",
                       "ls::followers_resolve_kernel", "ls::followers_probe_kernel"], ["k_prefix.hip", "ls_internal.h"]),
     "rescore": (["ls::rescore_chain_mfma_kernel", "ls::rescore_wave_kernel"],
                 ["k_score_chain.hip", "k_band.hip", "k_common.h", "k_policy.h", "ls_internal.h"]),
@@ -347,6 +347,38 @@ SCORE_KINDS = ("prefix_match", "instance_partial", "score_pairs", "score_pairs_m
                "argmin")
 
 
+def time_prefix_closed(w, inst_h, ins, overlap_ref, steps):
+    """The scoring call with the caches declared prefix-closed (ls_set_prefix_closed: K1 finds each run's end
+    by search, exact when every cached block's predecessor in the prompt is cached as well -- Section 2: prefix
+    reuse is strictly sequential and engines evict least recently used blocks, tail first; the synthetic caches
+    are built so): K1's and the call's device time, and whether every overlap equals the general path's."""
+    import torch
+
+    from paper_2606_00946_amd import lodestar
+    cfg = w.cfg
+    R, N = cfg.R, cfg.N
+    ctx = lodestar.Context(cfg.d, cfg.hidden, cfg.dtype, device=0)
+    ctx.ls_set_model(w.params, w.mu, w.inv_sigma)
+    ctx.ls_set_prefix_closed(True)
+    ctx.ls_load_cache_state(w.inst_off, inst_h)
+    chosen = torch.empty(R, dtype=torch.int32, device="cuda")
+    overlap = torch.empty(R * N, dtype=torch.int32, device="cuda")
+    ctx.ls_score_batch(*ins, chosen, None, None, overlap, None)
+    torch.cuda.synchronize()
+    ctx.ls_profile_enable(True)
+    for _ in range(steps):
+        ctx.ls_score_batch(*ins, chosen, None, None, overlap, None)
+    torch.cuda.synchronize()
+    prof = ctx.ls_profile_read()
+    ctx.ls_profile_enable(False)
+    ctx.close()
+    ms = {k: v[1] / steps for k, v in prof.items()}
+    t_score = sum(ms.get(k, 0.0) for k in SCORE_KINDS)
+    return {"prefix_match_ms": round(ms.get("prefix_match", 0.0), 4), "score_ms": round(t_score, 4),
+            "score_pairs_per_s": round(R * N / (t_score / 1e3), 1),
+            "overlaps_equal_general": bool(torch.equal(overlap, overlap_ref))}
+
+
 def run_other_config(name, steps, warmup):
     """Scoring and update of another workload: pairs/s of the scoring call, the
     update's steps/s, per-kernel times and the rooflines of K1 and the scorer."""
@@ -383,6 +415,7 @@ def run_other_config(name, steps, warmup):
     prof = ctx.ls_profile_read()
     ctx.ls_profile_enable(False)
     ctx.close()
+    closed = time_prefix_closed(w, inst_h, ins, overlap, steps)
     ms = {k: v[1] / steps for k, v in prof.items()}
     t_score = sum(ms.get(k, 0.0) for k in SCORE_KINDS)
     t_upd = ms.get("update", 0.0)
@@ -399,7 +432,7 @@ def run_other_config(name, steps, warmup):
             "score_ms": round(t_score, 4), "updates_per_s": round(1e3 / t_upd, 2) if t_upd else None,
             "update_samples_per_s": round(B * 1e3 / t_upd, 1) if t_upd else None,
             "wall_ms_per_step": round(wall_ms, 4), "kernel_ms": {k: round(v, 4) for k, v in ms.items()},
-            "useful_probes": probes, "rooflines": rl}
+            "useful_probes": probes, "rooflines": rl, "prefix_closed": closed}
 
 
 def main():
@@ -544,6 +577,7 @@ def main():
     result["online_learning"] = time_online_learning(ctx, w)
     result["maintenance"] = time_maintenance(w, inst_h, req_off, req_h, chosen, max(1, min(args.steps, 5)))
     ctx.close()
+    result["prefix_closed"] = time_prefix_closed(w, inst_h, (req_off, req_h, plen, feat), overlap, args.steps)
     del inst_h, req_off, req_h, plen, feat, upd_x, upd_y, overlap
     torch.cuda.empty_cache()
     if not args.no_other_configs:

@@ -181,7 +181,9 @@ __device__ __forceinline__ int64_t extend_run_wave(const uint64_t* __restrict__ 
 // searches instead of walking: each round probes 16 positions spread over the
 // open interval [lo, hi) (group g takes lo + (g + 1)(hi - lo) / 17, or lo + g
 // when the interval is short), which shrinks it about 17-fold; about four
-// rounds settle an 8k-block prompt.  Exact only under that invariant.
+// rounds settle an 8k-block prompt.  Exact only under that invariant.  It runs
+// on the leader pairs whose first block the first-block pass found cached, from
+// block 1 on.
 __device__ __forceinline__ bool probe_block(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
                                            uint64_t key, int q, int shift) {
     if (key == kEmptyKey) return has_empty;
@@ -197,10 +199,12 @@ __device__ __forceinline__ bool probe_block(const uint64_t* __restrict__ table, 
     return false;
 }
 
+// `start`: blocks [0, start) are known to be cached.
 __device__ __forceinline__ int64_t search_run_wave(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
-                                                   const uint64_t* __restrict__ h, int64_t n, int lane) {
+                                                   const uint64_t* __restrict__ h, int64_t n, int64_t start,
+                                                   int lane) {
     const int g = lane >> 2, q = lane & 3, shift = g * 4;
-    int64_t lo = 0, hi = n;                      // blocks [0, lo) cached; block hi is the first miss (or n)
+    int64_t lo = start, hi = n;                  // blocks [0, lo) cached; block hi is the first miss (or n)
     while (lo < hi) {
         const int64_t lo0 = lo, span = hi - lo;
         // probed positions, increasing with the group index; all inside [lo0, hi)
@@ -626,28 +630,6 @@ struct ProbeTables {
     const uint32_t* __restrict__ flags;
 };
 
-// One wave per (leader, instance) pair, persistent over the pairs.
-__global__ __launch_bounds__(256) void prefix_leaders_kernel(ProbeTables T, int32_t N,
-                                                             const int64_t* __restrict__ req_off,
-                                                             const uint64_t* __restrict__ req_hashes,
-                                                             const int32_t* __restrict__ leaders,
-                                                             const uint32_t* __restrict__ n_leaders,
-                                                             int32_t* __restrict__ overlap, int closed) {
-    const int lane = threadIdx.x & 63;
-    const int64_t total = (int64_t)(*n_leaders) * N;
-    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
-    for (int64_t pair = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); pair < total; pair += waves) {
-        const int64_t k = pair / N, i = pair - k * N;
-        const int64_t r = leaders[k];
-        const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
-        const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
-        const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
-        const int64_t l = closed ? search_run_wave(table, T.nb[i], he, req_hashes + h0, n, lane)
-                                 : extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 0, lane);
-        if (lane == 0) overlap[r * N + i] = (int32_t)l;
-    }
-}
-
 // Leaders, first block: 16 (leader, instance) pairs per wave, four lanes per
 // 64-byte bucket.  A pair whose first block is not cached on the instance (most
 // pairs) or whose prompt has at most one block is answered here; the others go
@@ -718,14 +700,15 @@ __global__ __launch_bounds__(kLeadThreads) void leaders_first_kernel(ProbeTables
     }
 }
 
-// The listed leader pairs, one wave each, from block 1 on.
+// The listed leader pairs, one wave each, from block 1 on: walked, or with
+// prefix-closed caches (`closed`) searched for the run's end.
 __global__ __launch_bounds__(256) void leaders_rest_kernel(ProbeTables T, int32_t N,
                                                            const int64_t* __restrict__ req_off,
                                                            const uint64_t* __restrict__ req_hashes,
                                                            const int32_t* __restrict__ leaders,
                                                            const int64_t* __restrict__ more,
                                                            const uint32_t* __restrict__ n_more,
-                                                           int32_t* __restrict__ overlap) {
+                                                           int32_t* __restrict__ overlap, int closed) {
     const int lane = threadIdx.x & 63;
     const int64_t total = *n_more;
     const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
@@ -736,7 +719,8 @@ __global__ __launch_bounds__(256) void leaders_rest_kernel(ProbeTables T, int32_
         const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
         const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
         const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
-        const int64_t l = extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane, 16);
+        const int64_t l = closed ? search_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane)
+                                 : extend_run_wave(table, T.nb[i], he, req_hashes + h0, n, 1, lane, 16);
         if (lane == 0) overlap[r * N + i] = (int32_t)l;
     }
 }
@@ -937,17 +921,14 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     // pairs that go past block 0; n_leaders[1] counts them.
     int64_t wgrid = (pairs + 3) / 4;
     if (wgrid > (int64_t)n_cu * 16) wgrid = (int64_t)n_cu * 16;
-    if (closed) {
-        hipLaunchKernelGGL(prefix_leaders_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
-                           leaders, n_leaders, overlap, 1);
-    } else {
+    {
         // pairs <= R N bound the leader pairs; every round of a workgroup takes kLeadPairs
         int64_t fgrid = (pairs + kLeadPairs - 1) / kLeadPairs;
         if (fgrid > (int64_t)n_cu * 4) fgrid = (int64_t)n_cu * 4;
         hipLaunchKernelGGL(leaders_first_kernel, dim3((uint32_t)fgrid), dim3(kLeadThreads), 0, s, T, N, req_off,
                            req_hashes, leaders, n_leaders, overlap, list, n_leaders + 1);
         hipLaunchKernelGGL(leaders_rest_kernel, dim3((uint32_t)wgrid), dim3(256), 0, s, T, N, req_off, req_hashes,
-                           leaders, list, n_leaders + 1, overlap);
+                           leaders, list, n_leaders + 1, overlap, closed ? 1 : 0);
     }
     // followers: slices of pairs, one workgroup each
     const bool vec = N % 4 == 0 && (uintptr_t)overlap % 16 == 0;

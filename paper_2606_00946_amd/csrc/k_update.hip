@@ -179,7 +179,8 @@ __global__ __launch_bounds__(256) void normalize_b16_kernel(const float* __restr
     const int c = c0 + tx;
     const float m_c = c < d ? mu[c] : 0.0f, s_c = c < d ? isig[c] : 0.0f;
 #pragma unroll
-    for (int i = ty; i < 64; i += 4) {
+    for (int q = 0; q < 16; ++q) {
+        const int i = ty + 4 * q;
         const int64_t b = b0 + i;
         float v = 0.0f;
         if (b < B && c < d) v = __fmul_rn(__fsub_rn(feats[b * d + c], m_c), s_c);
@@ -187,7 +188,8 @@ __global__ __launch_bounds__(256) void normalize_b16_kernel(const float* __restr
     }
     __syncthreads();
 #pragma unroll
-    for (int p = threadIdx.x; p < 64 * 8; p += 256) {
+    for (int q = 0; q < 2; ++q) {
+        const int p = (int)threadIdx.x + 256 * q;
         const int j = p >> 3, s8 = (p & 7) * 8;
         const int cj = c0 + j;
         const int64_t b = b0 + s8;
