@@ -199,6 +199,32 @@ __device__ __forceinline__ bool probe_block(const uint64_t* __restrict__ table, 
     return false;
 }
 
+// Prefix-closed caches only: the first miss at or after l, given blocks
+// [0, l) cached, by galloping (probing l, l + 2, l + 6, l + 14, ... while they
+// hit, each hit proving every block before it) and then bisecting between the
+// last hit and the miss.  A run of L blocks takes about 2 log2(L) probes
+// instead of about L / 8 rounds of the walk.  All four lanes of a group call it
+// together (group-wide ballots).
+__device__ __forceinline__ int64_t gallop_run(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
+                                              const uint64_t* __restrict__ h, int64_t n, int64_t l, int q,
+                                              int shift) {
+    int64_t lo = l, hi = n;                      // blocks [0, lo) cached; block hi missing (or hi = n)
+    for (int64_t step = 1; lo < hi; step *= 2) {
+        const int64_t j = lo + step - 1 < hi ? lo + step - 1 : hi - 1;
+        if (!probe_block(table, nb, has_empty, h[j], q, shift)) {
+            hi = j;
+            break;
+        }
+        lo = j + 1;
+    }
+    while (lo < hi) {
+        const int64_t j = lo + (hi - lo) / 2;
+        if (probe_block(table, nb, has_empty, h[j], q, shift)) lo = j + 1;
+        else hi = j;
+    }
+    return lo;
+}
+
 // `start`: blocks [0, start) are known to be cached.
 __device__ __forceinline__ int64_t search_run_wave(const uint64_t* __restrict__ table, uint32_t nb, bool has_empty,
                                                    const uint64_t* __restrict__ h, int64_t n, int64_t start,
@@ -815,14 +841,16 @@ __global__ __launch_bounds__(kResolveThreads) void followers_resolve_kernel(
     if (threadIdx.x == 0) n_list[blockIdx.x] = lcount;
 }
 
-// Block b probes the pairs of slice b, 16 per wave (four lanes per bucket).
+// Block b probes the pairs of slice b, 16 per wave (four lanes per bucket),
+// walking from the common prefix, or with prefix-closed caches (`closed`)
+// galloping from it.
 __global__ __launch_bounds__(256) void followers_probe_kernel(ProbeTables T, int32_t N, int64_t chunk,
                                                               const int64_t* __restrict__ req_off,
                                                               const uint64_t* __restrict__ req_hashes,
                                                               const int32_t* __restrict__ lcp_of,
                                                               const int64_t* __restrict__ list,
                                                               const uint32_t* __restrict__ n_list,
-                                                              int32_t* __restrict__ overlap) {
+                                                              int32_t* __restrict__ overlap, int closed) {
     const int lane = threadIdx.x & 63;
     const int group = lane >> 2, q = lane & 3, shift = group * 4;
     const int64_t total = n_list[blockIdx.x];
@@ -834,8 +862,9 @@ __global__ __launch_bounds__(256) void followers_probe_kernel(ProbeTables T, int
         const int64_t r = pair / N, i = pair - r * N;
         const int64_t h0 = req_off[r], n = req_off[r + 1] - h0;
         const uint64_t* table = T.keys + T.base[i] * kBucketKeys;
-        const int64_t l = extend_run(table, T.nb[i], (T.flags[i] & kFlagHasEmptyKey) != 0, req_hashes + h0, n,
-                                     lcp_of[r], q, shift);
+        const bool he = (T.flags[i] & kFlagHasEmptyKey) != 0;
+        const int64_t l = closed ? gallop_run(table, T.nb[i], he, req_hashes + h0, n, lcp_of[r], q, shift)
+                                 : extend_run(table, T.nb[i], he, req_hashes + h0, n, lcp_of[r], q, shift);
         if (q == 0) overlap[pair] = (int32_t)l;
     }
 }
@@ -947,7 +976,7 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
                            chunk, lead_of, lcp_of, cont_of, qseen, reinterpret_cast<const uint4*>(qinst), qall, overlap, list,
                            n_list);
     hipLaunchKernelGGL(followers_probe_kernel, dim3((uint32_t)slices), dim3(256), 0, s, T, N, chunk, req_off,
-                       req_hashes, lcp_of, list, n_list, overlap);
+                       req_hashes, lcp_of, list, n_list, overlap, closed ? 1 : 0);
     return hipGetLastError();
 }
 
