@@ -369,6 +369,7 @@ constexpr uint32_t kSeenAny = kSeenInst + 1;
 // leaders append themselves to the leader list.  With the semi-join on, a
 // follower registers the fingerprint of its block c (cont_of: slot, kContNone
 // when c reaches its end, kContProbe when it must be probed).
+template <int LPR>
 __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t* __restrict__ req_off,
                                                         const uint64_t* __restrict__ req_hashes,
                                                         const unsigned long long* __restrict__ glead,
@@ -378,15 +379,17 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
                                                         uint32_t* __restrict__ qfp, uint32_t G,
                                                         uint32_t* __restrict__ qfilter, int32_t* __restrict__ cont_of,
                                                         int join) {
-    // 16 lanes per request (four requests per wave): the chain of dependent
-    // reads before the compare is the cost, so more requests in flight pay.  A
-    // round compares 16 w positions, lane sl taking j0 + sl + 16 u (u < w), all
-    // loads issued before any compare; w doubles after every all-equal round
-    // (1, 2, 4, 8), so long common prefixes take few dependent rounds.
+    // LPR lanes per request (16: four requests per wave, for large batches,
+    // where more requests in flight pay; 64: a wave per request, for small
+    // batches of long prompts, where the rounds of one request are the cost).
+    // A round compares LPR w positions, lane sl taking j0 + sl + LPR u (u < w),
+    // all loads issued before any compare; w doubles after every all-equal
+    // round (1, 2, 4, 8), so long common prefixes take few dependent rounds.
+    static_assert(LPR == 16 || LPR == 64, "a request's lanes share one wave");
     constexpr int kLcpMaxLoads = 8;
-    const int lane = threadIdx.x & 63, sg = lane >> 4, sl = lane & 15;
-    const int64_t r = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * 4 + sg;
-    if (r >= R) return;                               // uniform over the 16 lanes
+    const int lane = threadIdx.x & 63, sg = lane / LPR, sl = lane % LPR;
+    const int64_t r = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * (64 / LPR) + sg;
+    if (r >= R) return;                               // uniform over the request's lanes
     const int32_t slot = slot_of[r];
     const int64_t lead = slot < 0 ? r : (int64_t)(0xFFFFFFFFu - (uint32_t)(glead[slot] & 0xFFFFFFFFull));
     const int64_t n = req_off[r + 1] - req_off[r];
@@ -398,11 +401,11 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
         const int64_t m = n < nl ? n : nl;
         c = m;
         int w = 1;
-        for (int64_t j0 = 0; j0 < m; j0 += 16 * w, w = w * 2 > kLcpMaxLoads ? kLcpMaxLoads : w * 2) {
+        for (int64_t j0 = 0; j0 < m; j0 += LPR * w, w = w * 2 > kLcpMaxLoads ? kLcpMaxLoads : w * 2) {
             uint64_t av[kLcpMaxLoads], bv[kLcpMaxLoads];
 #pragma unroll
             for (int u = 0; u < kLcpMaxLoads; ++u) {
-                const int64_t j = j0 + sl + 16 * u;
+                const int64_t j = j0 + sl + LPR * u;
                 if (u < w && j < m) {
                     av[u] = a[j];
                     bv[u] = b[j];
@@ -411,15 +414,15 @@ __global__ __launch_bounds__(256) void group_lcp_kernel(int32_t R, const int64_t
             int64_t first = m;                       // this lane's first differing position
 #pragma unroll
             for (int u = kLcpMaxLoads - 1; u >= 0; --u) {
-                const int64_t j = j0 + sl + 16 * u;
+                const int64_t j = j0 + sl + LPR * u;
                 if (u < w && j < m && av[u] != bv[u]) first = j;
             }
 #pragma unroll
-            for (int off = 8; off >= 1; off >>= 1) {
-                const int64_t o = __shfl_xor(first, off, 16);
+            for (int off = LPR / 2; off >= 1; off >>= 1) {
+                const int64_t o = __shfl_xor(first, off, LPR);
                 first = o < first ? o : first;
             }
-            if (first < m) {                          // uniform over the 16 lanes
+            if (first < m) {                          // uniform over the request's lanes
                 c = first;
                 break;
             }
@@ -931,9 +934,15 @@ hipError_t launch_prefix_match(const CacheTables& t, int32_t R, int32_t N, const
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(group_insert_kernel, dim3((uint32_t)(((int64_t)R + kGroupThreads - 1) / kGroupThreads)),
                        dim3(kGroupThreads), 0, s, R, req_off, req_hashes, gkeys, glead, (uint32_t)G, slot_of);
-    hipLaunchKernelGGL(group_lcp_kernel, dim3((uint32_t)(((int64_t)R + 15) / 16)), dim3(256), 0, s, R, req_off,
-                       req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qfp, (uint32_t)G, qfilter,
-                       cont_of, join ? 1 : 0);
+    // a wave per request when the batch leaves most of the device idle at four per wave
+    if ((int64_t)R * 16 < (int64_t)n_cu * 256)
+        hipLaunchKernelGGL(group_lcp_kernel<64>, dim3((uint32_t)(((int64_t)R + 3) / 4)), dim3(256), 0, s, R, req_off,
+                           req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qfp, (uint32_t)G, qfilter,
+                           cont_of, join ? 1 : 0);
+    else
+        hipLaunchKernelGGL(group_lcp_kernel<16>, dim3((uint32_t)(((int64_t)R + 15) / 16)), dim3(256), 0, s, R,
+                           req_off, req_hashes, glead, slot_of, lead_of, lcp_of, leaders, n_leaders, qfp, (uint32_t)G,
+                           qfilter, cont_of, join ? 1 : 0);
     if (join) {
         // a wave per segment, up to a workgroup per compute unit
         int64_t grid = ((int64_t)t.n_seg + kContWaves - 1) / kContWaves;
