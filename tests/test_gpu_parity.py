@@ -655,6 +655,25 @@ def test_prefix_closed_search(name):
     check_scoring(w, out, sel, run=run)
 
 
+@pytest.mark.parametrize("name", ["large_batch", "long_context", "heterogeneous", "tiny"])
+def test_prefix_closed_equals_general_at_full_size(name):
+    """Every overlap, decision and minimum of the full batch with the caches
+    declared prefix-closed (leaders' run-end search from block 1, followers
+    galloping from their common prefix) equals the general walk's: the
+    synthetic caches are prefix-closed, so both are exact.  Long-context and
+    Tiny also take the wave-per-request common-prefix pass."""
+    w = workload(name)
+    note(f"prefix-closed against the general walk at full size {name}")
+    outs = []
+    for closed in (False, True):
+        run = GpuRun(w, prefix_closed=closed)
+        outs.append(run.score(with_scores=False))
+        run.ctx.close()
+    for k in ("overlap", "chosen", "min_ttft"):
+        a, b = np.asarray(outs[0][k]), np.asarray(outs[1][k])
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), k
+
+
 def test_ties_go_to_lowest_instance():
     """Instances with identical state and cache score identically; the lowest id wins."""
     note("exact ties")
