@@ -63,7 +63,7 @@ KIND_KERNELS = {
                     ["k_score_chain.hip", "k_score.hip", "k_common.h", "ls_internal.h"]),
     "update": (["ls::normalize_kernel", "ls::normalize_b16_kernel", "ls::dense_mfma_kernel", "ls::dense_lane_kernel", "ls::dense_small_kernel",
                 "ls::layer_fwd_kernel",
-                "ls::loss_grad_kernel", "ls::loss_final_kernel", "ls::wgrad_direct_kernel",
+                "ls::loss_grad_kernel", "ls::loss_final_kernel", "ls::wgrad_direct_kernel", "ls::wgrad_row_kernel",
                 "ls::wgrad_reduce_wave_kernel", "ls::wgrad_reduce_kernel", "ls::wgrad_mfma_kernel",
                 "ls::delta_head_kernel", "ls::delta_head_b16_kernel", "ls::backprop_hidden_kernel", "ls::gemm_nt_splitk_kernel",
                 "ls::splitk_reduce_kernel", "ls::rowsum_kernel", "ls::sgd_kernel", "ls::refresh_compute_kernel",

@@ -1270,12 +1270,87 @@ static void launch_wgrad_nt(const TA* A, const TB* Bt, float* part, int M, int N
     }
 }
 
+// The gradient of a one-output layer (the head): dW[n] = sum over b of
+// g[b] Bt[n][b] and db = sum of g[b], a workgroup per n (the last one the
+// bias).  Thread t adds samples 8 t .. 8 t + 7, then 8 t + 8192 .., in
+// ascending order, then a fixed tree over the workgroup: the order depends on B
+// alone and is the same for bf16 storage and fp32 rows.  The products of bf16
+// numbers are exact in fp32, so only the sums round.  VEC (B a multiple of 8,
+// rows 16-byte aligned): each thread's eight samples as 16-byte loads.
+constexpr int kRowThreads = 1024;
+
+template <bool VEC, typename TB>
+__global__ __launch_bounds__(kRowThreads) void wgrad_row_kernel(const float* __restrict__ g,
+                                                                const TB* __restrict__ Bt, int N, int32_t B,
+                                                                float* __restrict__ gw, float* __restrict__ gb) {
+    __shared__ float red[kRowThreads];
+    const int n = (int)blockIdx.x;
+    const bool bias = n == N;
+    const TB* __restrict__ row = Bt + (int64_t)(bias ? 0 : n) * B;
+    const int tid = (int)threadIdx.x;
+    float acc = 0.0f;
+    for (int64_t b0 = (int64_t)tid * 8; b0 < B; b0 += (int64_t)kRowThreads * 8) {
+        float gv[8], xv[8];
+        if (VEC) {
+            const float4 p = *reinterpret_cast<const float4*>(g + b0);
+            const float4 q = *reinterpret_cast<const float4*>(g + b0 + 4);
+            gv[0] = p.x; gv[1] = p.y; gv[2] = p.z; gv[3] = p.w; gv[4] = q.x; gv[5] = q.y; gv[6] = q.z; gv[7] = q.w;
+            if (bias) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xv[e] = 1.0f;
+            } else if constexpr (std::is_same<TB, bf16s_t>::value) {
+                const uint4 r = *reinterpret_cast<const uint4*>(row + b0);
+                const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xv[e] = __uint_as_float(((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu) << 16);
+            } else {
+                const float4 r0 = *reinterpret_cast<const float4*>(row + b0);
+                const float4 r1 = *reinterpret_cast<const float4*>(row + b0 + 4);
+                xv[0] = r0.x; xv[1] = r0.y; xv[2] = r0.z; xv[3] = r0.w;
+                xv[4] = r1.x; xv[5] = r1.y; xv[6] = r1.z; xv[7] = r1.w;
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const bool in = b0 + e < B;
+                gv[e] = in ? g[b0 + e] : 0.0f;
+                xv[e] = in && !bias ? ld_act(row, b0 + e) : 1.0f;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc += gv[e] * xv[e];
+    }
+    red[tid] = acc;
+    __syncthreads();
+#pragma unroll
+    for (int w = kRowThreads / 2; w > 0; w >>= 1) {
+        if (tid < w) red[tid] += red[tid + w];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        if (bias) gb[0] = red[0];
+        else gw[n] = red[0];
+    }
+}
+
 // dW = A Bt^T and db = A 1 for A [M x B], Bt [N x B]; M, N <= 256.  With
 // fewer sample chunks than CUs the n-tiles are split over two workgroups per
 // chunk (each reads the chunk's A rows, half of its Bt rows).
 template <typename TA, typename TB>
 static hipError_t weight_grad_mfma(const TA* A, const TB* Bt, int M, int N, int32_t B, float* part,
                                    float* gw, float* gb, int n_cu, hipStream_t s) {
+    if constexpr (std::is_same<TA, float>::value) {
+        if (M == 1) {                                 // the head: a dot product per weight
+            const bool vec = B % 8 == 0 && (reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(Bt)) % 16 == 0;
+            if (vec)
+                hipLaunchKernelGGL((wgrad_row_kernel<true, TB>), dim3((uint32_t)N + 1), dim3(kRowThreads), 0, s, A, Bt,
+                                   N, B, gw, gb);
+            else
+                hipLaunchKernelGGL((wgrad_row_kernel<false, TB>), dim3((uint32_t)N + 1), dim3(kRowThreads), 0, s, A,
+                                   Bt, N, B, gw, gb);
+            return hipGetLastError();
+        }
+    }
     const WgradPlan p = wgrad_plan(B, M);
     const int tiles = (N + 31) / 32;
     const int ny = (M > 32 && tiles >= 2 && p.S < n_cu) ? 2 : 1;
